@@ -1,0 +1,199 @@
+/*
+ * CPU oracle for sorted segment reduction and its fused gather-weight form.
+ *
+ * TEST INFRASTRUCTURE ONLY. This file is the reference the GPU library is
+ * checked against. Only the test suite, the smoke check and the bench's CPU
+ * baseline load it; the GPU library never includes, links or calls it, and it
+ * includes nothing from the GPU library.
+ *
+ * What it computes is the plain definition of segment reduction (GeoT paper,
+ * Section II-B, "Segment Reduction"): Idx is a non-decreasing 1-D array of
+ * length M, X is an M x N matrix (N = F features), and output row s of the
+ * |V| x N result Y reduces the rows i of X with Idx[i] == s. The aggregate
+ * step of message passing (Eq. 2) is the sum case; the reduction may also be
+ * mean or max (Fig. "scatter" caption; Section VI, diverse reduction types).
+ * The fused form (Section IV and Listing "GeoT solution for fusion"; the
+ * weighted variant used as SpMM in Section V-D) reduces the messages
+ * w[e] * x[col[e], :] by the sorted destination row of each edge.
+ *
+ * Readings where the paper is silent (all stated, none derived from a GPU):
+ *  - empty segments produce 0.0f for sum, mean and max;
+ *  - sum and mean accumulate in fp64 and round once to fp32 at the end;
+ *    mean divides the fp64 sum by the row (edge) count in fp64;
+ *  - max starts from the first member and keeps a strictly larger value, in
+ *    fp32; a max never rounds, so it is exact;
+ *  - a weighted term is one fp32 multiply w[e] * x (round to nearest even);
+ *    without weights the term is x itself;
+ *  - the output is overwritten in full (not accumulated into).
+ *
+ * Build: gcc -O2 -fno-fast-math -ffp-contract=off -shared -fPIC.
+ * Error codes: 0 ok, 1 invalid argument, 2 index not sorted, 3 index (or
+ * column) out of range.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_OK = 0, OR_INVALID = 1, OR_NOT_SORTED = 2, OR_OUT_OF_RANGE = 3 };
+enum { OR_SUM = 0, OR_MEAN = 1, OR_MAX = 2 };
+
+/* Check the preconditions of the definition: Idx non-decreasing, 0 <= Idx < S. */
+int oracle_check_index(const int64_t *idx, int64_t nnz, int64_t S)
+{
+    if (nnz < 0 || S < 0) return OR_INVALID;
+    for (int64_t i = 0; i < nnz; ++i) {
+        if (idx[i] < 0 || idx[i] >= S) return OR_OUT_OF_RANGE;
+        if (i > 0 && idx[i] < idx[i - 1]) return OR_NOT_SORTED;
+    }
+    return OR_OK;
+}
+
+/* start[s] = first row i with idx[i] >= s, for s = 0..S (start[S] = nnz).
+ * Rows of segment s are start[s] .. start[s+1]-1. Computed by one linear walk. */
+static void segment_starts(const int64_t *idx, int64_t nnz, int64_t S, int64_t *start)
+{
+    int64_t i = 0;
+    for (int64_t s = 0; s <= S; ++s) {
+        while (i < nnz && idx[i] < s) ++i;
+        start[s] = i;
+    }
+}
+
+/* The term a segment reduces for (row or edge) e and feature f. */
+static float term(const float *rows, int64_t F, const int64_t *col, const float *w,
+                  int64_t e, int64_t f)
+{
+    if (col == NULL) return rows[e * F + f];
+    float x = rows[col[e] * F + f];
+    if (w == NULL) return x;
+    float t = w[e] * x; /* one fp32 multiply */
+    return t;
+}
+
+/* Shared body of both operations: for each segment s and feature f reduce the
+ * terms of rows start[s]..start[s+1]-1 with op. */
+static void reduce_segments(const float *rows, int64_t F, const int64_t *col, const float *w,
+                            const int64_t *start, int64_t S, int op, float *out)
+{
+    for (int64_t s = 0; s < S; ++s) {
+        int64_t b = start[s], e = start[s + 1];
+        int64_t count = e - b;
+        for (int64_t f = 0; f < F; ++f) {
+            float result;
+            if (count == 0) {
+                result = 0.0f; /* empty segment */
+            } else if (op == OR_MAX) {
+                float m = term(rows, F, col, w, b, f);
+                for (int64_t i = b + 1; i < e; ++i) {
+                    float t = term(rows, F, col, w, i, f);
+                    if (t > m) m = t;
+                }
+                result = m;
+            } else {
+                double acc = 0.0;
+                for (int64_t i = b; i < e; ++i) acc += (double)term(rows, F, col, w, i, f);
+                if (op == OR_MEAN) acc = acc / (double)count;
+                result = (float)acc;
+            }
+            out[s * F + f] = result;
+        }
+    }
+}
+
+/* out[s, :] = op over { src[i, :] : idx[i] == s }, s in [0, S). */
+int oracle_segment_reduce(const float *src, const int64_t *idx, int64_t nnz, int64_t S,
+                          int64_t F, int op, float *out)
+{
+    if (nnz < 0 || S < 0 || F < 0 || op < OR_SUM || op > OR_MAX) return OR_INVALID;
+    if (S == 0 || F == 0) return OR_OK;
+    int rc = oracle_check_index(idx, nnz, S);
+    if (rc != OR_OK) return rc;
+    int64_t *start = (int64_t *)malloc((size_t)(S + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(idx, nnz, S, start);
+    reduce_segments(src, F, NULL, NULL, start, S, op, out);
+    free(start);
+    return OR_OK;
+}
+
+/* out[r, :] = op over { w[e] * X[col[e], :] : row[e] == r }, r in [0, R);
+ * w == NULL means every weight is 1 (the term is X[col[e], :] itself). */
+int oracle_gather_scatter(const float *X, int64_t n_x, const int64_t *col, const float *w,
+                          const int64_t *row, int64_t nnz, int64_t R, int64_t F, int op,
+                          float *out)
+{
+    if (nnz < 0 || R < 0 || F < 0 || n_x < 0 || op < OR_SUM || op > OR_MAX) return OR_INVALID;
+    if (R == 0 || F == 0) return OR_OK;
+    int rc = oracle_check_index(row, nnz, R);
+    if (rc != OR_OK) return rc;
+    for (int64_t e = 0; e < nnz; ++e)
+        if (col[e] < 0 || col[e] >= n_x) return OR_OUT_OF_RANGE;
+    int64_t *start = (int64_t *)malloc((size_t)(R + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(row, nnz, R, start);
+    reduce_segments(X, F, col, w, start, R, op, out);
+    free(start);
+    return OR_OK;
+}
+
+/* Per output element, the sum of |term| that the element reduces, in fp64
+ * (for mean, each term is divided by the count). Used to state the
+ * floating-point tolerance of sum and mean; col == NULL selects plain rows. */
+int oracle_abs_term_sum(const float *rows, int64_t n_x, const int64_t *col, const float *w,
+                        const int64_t *idx, int64_t nnz, int64_t S, int64_t F, int op,
+                        double *out)
+{
+    if (nnz < 0 || S < 0 || F < 0) return OR_INVALID;
+    if (S == 0 || F == 0) return OR_OK;
+    int rc = oracle_check_index(idx, nnz, S);
+    if (rc != OR_OK) return rc;
+    if (col)
+        for (int64_t e = 0; e < nnz; ++e)
+            if (col[e] < 0 || col[e] >= n_x) return OR_OUT_OF_RANGE;
+    int64_t *start = (int64_t *)malloc((size_t)(S + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(idx, nnz, S, start);
+    for (int64_t s = 0; s < S; ++s) {
+        int64_t b = start[s], e = start[s + 1];
+        for (int64_t f = 0; f < F; ++f) {
+            double acc = 0.0;
+            for (int64_t i = b; i < e; ++i) acc += fabs((double)term(rows, F, col, w, i, f));
+            if (op == OR_MEAN && e > b) acc /= (double)(e - b);
+            out[s * F + f] = acc;
+        }
+    }
+    free(start);
+    return OR_OK;
+}
+
+/* Segment-length statistics of a sorted index over S segments:
+ * mean = nnz / S, var = (1/S) * sum_s (len_s - mean)^2 (population variance),
+ * the longest segment, the number of empty segments and sum_s len_s^2. */
+int oracle_index_stats(const int64_t *idx, int64_t nnz, int64_t S, double *mean, double *var,
+                       int64_t *max_len, int64_t *num_empty, int64_t *sum_len_sq)
+{
+    if (nnz < 0 || S <= 0) return OR_INVALID;
+    int rc = oracle_check_index(idx, nnz, S);
+    if (rc != OR_OK) return rc;
+    int64_t *start = (int64_t *)malloc((size_t)(S + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(idx, nnz, S, start);
+    double m = (double)nnz / (double)S, v = 0.0;
+    int64_t mx = 0, ne = 0, sq = 0;
+    for (int64_t s = 0; s < S; ++s) {
+        int64_t len = start[s + 1] - start[s];
+        double d = (double)len - m;
+        v += d * d;
+        if (len > mx) mx = len;
+        if (len == 0) ++ne;
+        sq += len * len;
+    }
+    *mean = m;
+    *var = v / (double)S;
+    *max_len = mx;
+    *num_empty = ne;
+    *sum_len_sq = sq;
+    free(start);
+    return OR_OK;
+}

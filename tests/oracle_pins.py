@@ -1,0 +1,323 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each ``pin_*`` function takes an oracle implementation (``oracle.OracleLib``)
+and raises ``AssertionError`` when the implementation disagrees with:
+
+* hand-worked examples (``tests/golden/hand_examples.json``);
+* brute force over every non-decreasing index of tiny problems, written as the
+  literal per-segment filter of the definition (Section II-B) with exact
+  integer / rational arithmetic;
+* invariants of the definition (conservation of totals, mean times count equals
+  sum, empty segments, max is a member and dominates, length-1 segments, S = 1);
+* library routines: numpy's unbuffered ``add.at`` / ``maximum.at``, torch's
+  ``scatter_reduce`` and a dense fp64 matrix product for the fused form;
+* the fusion identity of Listing "GeoT solution for fusion" with the messages
+  formed by numpy's own fp32 multiply.
+
+The pins are shared by ``test_oracle_pins.py`` (real oracle must pass every
+pin) and ``test_oracle_mutants.py`` (planted mistakes must each fail one).
+"""
+from __future__ import annotations
+
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+from workloads import random_gather_problem, random_problem
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hand_examples.json")
+OPS = ("sum", "mean", "max")
+
+
+def within_tol(got, ref, abs_terms, rel=1e-5, absol=1e-6):
+    """The fp32 sum/mean bound: |got - ref| <= rel * sum|terms| + absol, per element."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return np.all(np.abs(got - ref) <= rel * np.asarray(abs_terms) + absol)
+
+
+def _f32(x):
+    return np.float32(x)
+
+
+def _golden_value(entry, op):
+    if op == "mean":
+        return np.array([[np.float32(n / d) for (n, d) in row] for row in entry], dtype=np.float32)
+    return np.array(entry, dtype=np.float32)
+
+
+# ----------------------------------------------------------------------------
+def pin_golden(impl):
+    g = json.load(open(GOLDEN))
+    sr = g["segment_reduce"]
+    src = np.array(sr["src"], dtype=np.float32)
+    idx = np.array(sr["index"], dtype=np.int64)
+    for op in OPS:
+        got = impl.segment_reduce(src, idx, sr["num_segments"], op)
+        assert np.array_equal(got, _golden_value(sr[op], op)), f"golden segment_reduce {op}"
+    gs = g["gather_scatter"]
+    X = np.array(gs["X"], dtype=np.float32)
+    col = np.array(gs["col"], dtype=np.int64)
+    row = np.array(gs["row"], dtype=np.int64)
+    w = np.array(gs["weight"], dtype=np.float32)
+    for key, weight in (("weighted", w), ("unweighted", None)):
+        for op in OPS:
+            got = impl.gather_scatter(X, col, weight, row, gs["num_rows"], op)
+            assert np.array_equal(got, _golden_value(gs[key][op], op)), f"golden gather {key} {op}"
+
+
+# ----------------------------------------------------------------------------
+def _brute_segment(values_int, idx, S, F, op):
+    """Literal definition: for each segment, filter the rows whose index equals it."""
+    out = np.zeros((S, F), dtype=np.float32)
+    for s in range(S):
+        members = [i for i in range(len(idx)) if idx[i] == s]
+        for f in range(F):
+            terms = [values_int[i][f] for i in members]
+            if not terms:
+                out[s, f] = 0.0
+            elif op == "sum":
+                out[s, f] = _f32(sum(terms))
+            elif op == "mean":
+                out[s, f] = _f32(float(Fraction(sum(terms), len(terms))))
+            else:
+                out[s, f] = _f32(max(terms))
+    return out
+
+
+def pin_bruteforce_segment(impl, max_nnz=5, max_S=4, Fs=(1, 3)):
+    rng = np.random.default_rng(11)
+    for S in range(1, max_S + 1):
+        for nnz in range(0, max_nnz + 1):
+            for idx_t in itertools.combinations_with_replacement(range(S), nnz):
+                idx = np.array(idx_t, dtype=np.int64)
+                for F in Fs:
+                    vals = rng.integers(-8, 9, size=(nnz, F))
+                    src = vals.astype(np.float32).reshape(nnz, F)
+                    for op in OPS:
+                        want = _brute_segment(vals.tolist(), idx_t, S, F, op)
+                        got = impl.segment_reduce(src, idx, S, op)
+                        assert np.array_equal(got, want), f"brute segment {op} idx={idx_t} F={F}"
+
+
+def pin_bruteforce_gather(impl, max_nnz=4, max_R=3, n_x=3, F=2):
+    rng = np.random.default_rng(12)
+    for R in range(1, max_R + 1):
+        for nnz in range(0, max_nnz + 1):
+            for row_t in itertools.combinations_with_replacement(range(R), nnz):
+                row = np.array(row_t, dtype=np.int64)
+                col = rng.integers(0, n_x, nnz).astype(np.int64)
+                Xi = rng.integers(-8, 9, size=(n_x, F))
+                X = Xi.astype(np.float32)
+                wq = rng.integers(-4, 5, nnz)  # weights in quarter steps: products exact
+                w = (wq / 4.0).astype(np.float32)
+                for weighted in (True, False):
+                    msgs = []
+                    for e in range(nnz):
+                        scale = Fraction(int(wq[e]), 4) if weighted else Fraction(1)
+                        msgs.append([scale * int(Xi[col[e], f]) for f in range(F)])
+                    for op in OPS:
+                        want = np.zeros((R, F), dtype=np.float32)
+                        for r in range(R):
+                            members = [e for e in range(nnz) if row_t[e] == r]
+                            for f in range(F):
+                                terms = [msgs[e][f] for e in members]
+                                if not terms:
+                                    continue
+                                if op == "sum":
+                                    want[r, f] = _f32(float(sum(terms)))
+                                elif op == "mean":
+                                    want[r, f] = _f32(float(sum(terms) / len(terms)))
+                                else:
+                                    want[r, f] = _f32(float(max(terms)))
+                        got = impl.gather_scatter(X, col, w if weighted else None, row, R, op)
+                        assert np.array_equal(got, want), \
+                            f"brute gather {op} weighted={weighted} row={row_t} col={col.tolist()}"
+
+
+# ----------------------------------------------------------------------------
+_INV_CASES = (
+    # seed, nnz, S, F, dist, values, empty_frac
+    (21, 3000, 200, 3, "uniform", "uniform", 0.1),
+    (22, 5000, 300, 1, "zipf", "normal", 0.05),
+    (23, 4000, 150, 8, "lognormal", "uniform", 0.0),
+    (24, 2000, 50, 5, "one_heavy", "normal", 0.2),
+    (25, 1000, 100, 4, "uniform", "negative", 0.1),
+)
+
+
+def pin_invariants(impl):
+    for seed, nnz, S, F, dist, values, ef in _INV_CASES:
+        p = random_problem(seed, nnz, S, F, dist, values, ef)
+        src, idx, L = p["src"], p["index"], p["lengths"]
+        out = {op: impl.segment_reduce(src, idx, S, op) for op in OPS}
+        abs_sum = np.zeros((S, F))
+        np.add.at(abs_sum, idx, np.abs(src.astype(np.float64)))
+        # conservation of per-feature totals (sum)
+        tot = src.astype(np.float64).sum(axis=0)
+        got_tot = out["sum"].astype(np.float64).sum(axis=0)
+        assert np.all(np.abs(got_tot - tot) <= 1e-5 * abs_sum.sum(axis=0) + 1e-6 * S), \
+            f"conservation case {seed}"
+        # empty segments hold 0 for every op
+        empty = L == 0
+        for op in OPS:
+            assert np.all(out[op][empty] == 0.0), f"empty fill {op} case {seed}"
+        # mean * count == sum within the bound
+        ne = ~empty
+        assert within_tol(out["mean"][ne] * L[ne, None], out["sum"][ne], abs_sum[ne]), \
+            f"mean*count case {seed}"
+        # max: a member of its segment and >= every member
+        starts = np.concatenate([[0], np.cumsum(L)])
+        for s in np.flatnonzero(ne):
+            seg = src[starts[s]:starts[s + 1]]
+            assert np.all(out["max"][s] >= seg), f"max dominance seg {s} case {seed}"
+            assert np.all((seg == out["max"][s]).any(axis=0)), f"max membership seg {s} case {seed}"
+        # length-1 segments return their row unchanged for every op
+        for s in np.flatnonzero(L == 1):
+            for op in OPS:
+                assert np.array_equal(out[op][s], src[starts[s]]), f"length-1 {op} case {seed}"
+
+
+def pin_single_segment(impl):
+    """S = 1 is a column reduction: numpy's fp64 sum / max / mean over axis 0."""
+    p = random_problem(31, 4000, 1, 6, "uniform", "normal")
+    src, idx = p["src"], p["index"]
+    s64 = src.astype(np.float64)
+    absum = np.abs(s64).sum(axis=0)
+    for op, ref in (("sum", s64.sum(axis=0)), ("mean", s64.mean(axis=0))):
+        got = impl.segment_reduce(src, idx, 1, op)[0].astype(np.float64)
+        scale = absum if op == "sum" else absum / len(src)
+        # one fp32 rounding of the result plus fp64 reordering noise
+        assert np.all(np.abs(got - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12 * scale), f"S=1 {op}"
+    assert np.array_equal(impl.segment_reduce(src, idx, 1, "max")[0], src.max(axis=0)), "S=1 max"
+
+
+def pin_column_independence(impl):
+    p = random_problem(32, 3000, 120, 3, "zipf", "normal", 0.1)
+    src, idx, S = p["src"], p["index"], p["num_segments"]
+    for op in OPS:
+        whole = impl.segment_reduce(src, idx, S, op)
+        for f in range(3):
+            part = impl.segment_reduce(np.ascontiguousarray(src[:, f:f + 1]), idx, S, op)
+            assert np.array_equal(whole[:, f:f + 1], part), f"column independence {op} f={f}"
+
+
+def pin_library_scatter(impl):
+    import torch
+
+    for seed, dist, F in ((41, "lognormal", 4), (42, "zipf", 7), (43, "uniform", 1)):
+        p = random_problem(seed, 6000, 400, F, dist, "normal", 0.05)
+        src, idx, S, L = p["src"], p["index"], p["num_segments"], p["lengths"]
+        s64 = src.astype(np.float64)
+        acc = np.zeros((S, F))
+        np.add.at(acc, idx, s64)  # unbuffered, in row order, fp64
+        assert np.array_equal(impl.segment_reduce(src, idx, S, "sum"), acc.astype(np.float32)), \
+            f"add.at sum {seed}"
+        cnt = np.maximum(L, 1)[:, None]
+        assert np.array_equal(impl.segment_reduce(src, idx, S, "mean"),
+                              (acc / cnt).astype(np.float32)), f"add.at mean {seed}"
+        mx = np.full((S, F), -np.inf, dtype=np.float32)
+        np.maximum.at(mx, idx, src)
+        mx[L == 0] = 0.0
+        assert np.array_equal(impl.segment_reduce(src, idx, S, "max"), mx), f"maximum.at {seed}"
+        # torch scatter_reduce on the CPU as a third opinion
+        ts = torch.from_numpy(src)
+        ti = torch.from_numpy(idx)[:, None].expand(-1, F)
+        abs_sum = np.zeros((S, F))
+        np.add.at(abs_sum, idx, np.abs(s64))
+        for op, tname in (("sum", "sum"), ("mean", "mean"), ("max", "amax")):
+            t = torch.zeros(S, F, dtype=torch.float32).scatter_reduce(0, ti, ts, tname,
+                                                                     include_self=False).numpy()
+            got = impl.segment_reduce(src, idx, S, op)
+            if op == "max":
+                assert np.array_equal(got, t), f"torch amax {seed}"
+            else:
+                tol = abs_sum / cnt if op == "mean" else abs_sum
+                assert within_tol(got, t, tol), f"torch {op} {seed}"
+
+
+def pin_dense_matmul(impl):
+    for seed, weighted in ((51, True), (52, False)):
+        p = random_gather_problem(seed, 3000, 150, 90, 5, "zipf", "normal", weighted, 0.1)
+        X, col, w, row, R = p["X"], p["col"], p["weight"], p["index"], p["num_segments"]
+        A = np.zeros((R, X.shape[0]))
+        np.add.at(A, (row, col), 1.0 if w is None else w.astype(np.float64))
+        dense = A @ X.astype(np.float64)
+        absA = np.zeros_like(A)
+        np.add.at(absA, (row, col), 1.0 if w is None else np.abs(w.astype(np.float64)))
+        bound = absA @ np.abs(X.astype(np.float64))
+        got = impl.gather_scatter(X, col, w, row, R, "sum")
+        assert within_tol(got, dense, bound), f"dense A@X weighted={weighted}"
+
+
+def pin_fusion_equivalence(impl):
+    p = random_gather_problem(61, 4000, 300, 200, 6, "lognormal", "normal", True, 0.05)
+    X, col, w, row, R = p["X"], p["col"], p["weight"], p["index"], p["num_segments"]
+    msgs = (w[:, None] * X[col]).astype(np.float32)  # numpy fp32 multiply, one rounding
+    for op in OPS:
+        assert np.array_equal(impl.gather_scatter(X, col, w, row, R, op),
+                              impl.segment_reduce(msgs, row, R, op)), f"fusion identity {op}"
+        assert np.array_equal(impl.gather_scatter(X, col, None, row, R, op),
+                              impl.segment_reduce(np.ascontiguousarray(X[col]), row, R, op)), \
+            f"fusion identity unweighted {op}"
+
+
+def pin_errors(impl):
+    from oracle import OracleError
+
+    src = np.ones((4, 2), dtype=np.float32)
+    for idx, code in (([0, 2, 1, 3], 2), ([0, 1, 1, 5], 3), ([-1, 0, 0, 1], 3)):
+        try:
+            impl.segment_reduce(src, np.array(idx, dtype=np.int64), 4, "sum")
+        except OracleError as e:
+            assert e.code == code, f"error code for {idx}"
+        else:
+            raise AssertionError(f"no error for {idx}")
+    try:
+        impl.gather_scatter(src, np.array([0, 9]), None, np.array([0, 1]), 2, "sum")
+    except OracleError as e:
+        assert e.code == 3
+    else:
+        raise AssertionError("no error for column out of range")
+
+
+def pin_abs_term_sum(impl):
+    p = random_gather_problem(71, 2000, 100, 50, 3, "zipf", "normal", True, 0.1)
+    X, col, w, row, R, L = p["X"], p["col"], p["weight"], p["index"], p["num_segments"], p["lengths"]
+    msgs = np.abs((w[:, None] * X[col]).astype(np.float32).astype(np.float64))
+    want = np.zeros((R, 3))
+    np.add.at(want, row, msgs)
+    got = impl.abs_term_sum(X, row, R, "sum", col, w)
+    assert np.allclose(got, want, rtol=1e-12, atol=0), "abs term sum"
+    got_mean = impl.abs_term_sum(X, row, R, "mean", col, w)
+    assert np.allclose(got_mean, want / np.maximum(L, 1)[:, None], rtol=1e-12, atol=0), "abs mean"
+
+
+def pin_index_stats(impl):
+    for seed, dist, ef in ((81, "zipf", 0.1), (82, "fixed", 0.0), (83, "lognormal", 0.3)):
+        p = random_problem(seed, 5000, 700, 1, dist, "uniform", ef)
+        L = np.bincount(p["index"], minlength=700)
+        st = impl.index_stats(p["index"], 700)
+        assert st["max_len"] == L.max() and st["num_empty"] == int((L == 0).sum())
+        assert st["sum_len_sq"] == int((L.astype(np.int64) ** 2).sum())
+        assert abs(st["mean_len"] - L.mean()) <= 1e-12 * L.mean()
+        assert abs(st["var_len"] - L.var()) <= 1e-9 * max(L.var(), 1.0)
+
+
+ALL_PINS = (
+    pin_golden,
+    pin_bruteforce_segment,
+    pin_bruteforce_gather,
+    pin_invariants,
+    pin_single_segment,
+    pin_column_independence,
+    pin_library_scatter,
+    pin_dense_matmul,
+    pin_fusion_equivalence,
+    pin_errors,
+    pin_abs_term_sum,
+    pin_index_stats,
+)
