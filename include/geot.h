@@ -1,0 +1,196 @@
+/*
+ * geot.h - C-ABI of libgeot_hip, sorted segment reduction for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Operations (GeoT paper, arXiv 2404.03019):
+ *  - segment reduction (Section II-B): Idx is a non-decreasing index of length
+ *    M (one entry per row), X is M x F, and output row s of the S x F result
+ *    reduces the rows i with Idx[i] == s. Aggregation in message passing
+ *    (Eq. 2) is the sum case; mean and max are the other reduction types the
+ *    paper names (Fig. "scatter" caption, Section VI);
+ *  - the fused gather-weight-scatter form (Section IV, Listing "GeoT solution
+ *    for fusion", and the weighted form used as SpMM in Section V-D): the
+ *    rows reduced are the messages weight[e] * X[col[e], :] of edges e, grouped
+ *    by the sorted destination row of each edge;
+ *  - a kernel selector (Section III-C): a decision tree over cheap input
+ *    features picks the kernel family and its tiling parameters.
+ *
+ * Conventions shared by every call:
+ *  - Array arguments are DEVICE pointers owned by the caller: fp32 values and
+ *    int64 indices, contiguous and row-major. The library never frees them
+ *    and keeps no reference after the call returns.
+ *  - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *    Calls are asynchronous: they return after the kernels are enqueued, and
+ *    device faults surface at the caller's next synchronisation. Calls that
+ *    return host data say "synchronizes".
+ *  - `out` is overwritten in full, including empty segments (it is never
+ *    accumulated into). Empty segments hold GEOT_EMPTY_FILL for every op.
+ *  - Temporary device memory (partial results of segments that cross block
+ *    boundaries) comes from a stream-ordered pool owned by the library and is
+ *    released on the same stream.
+ *  - Preconditions: the index is non-decreasing and 0 <= index < num_segments;
+ *    for the gather form 0 <= col < num_x_rows. They are not checked by the
+ *    reduction calls (geot_check_index checks them). Violations give
+ *    unspecified values but never an out-of-bounds access: stores to rows
+ *    outside [0, num_segments) and loads of rows outside [0, num_x_rows) are
+ *    skipped.
+ *  - Errors are returned as geot_status_t; nothing is thrown across the ABI.
+ *    Argument checks run on the host before any device work and touch no
+ *    device memory; geot_last_error_detail() explains the last failure of the
+ *    calling thread.
+ *  - Accumulation is fp32. Sum and mean differ from an fp64 reference by at
+ *    most 1e-5 * sum|terms| + 1e-6 per element; max is exact.
+ */
+#ifndef GEOT_H
+#define GEOT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GEOT_VERSION 1
+
+/* Value written to every element of an empty segment, for every op. */
+#define GEOT_EMPTY_FILL 0.0f
+
+typedef enum {
+    GEOT_OP_SUM = 0,  /* sum of the rows of a segment */
+    GEOT_OP_MEAN = 1, /* sum divided by the number of rows (edges), not by sum of weights */
+    GEOT_OP_MAX = 2   /* elementwise maximum of the rows (the rounded products for the gather form) */
+} geot_op_t;
+
+typedef enum {
+    GEOT_SUCCESS = 0,
+    GEOT_ERROR_INVALID_VALUE = 1, /* bad argument (null pointer, negative size, unknown op, overlap) */
+    GEOT_ERROR_NOT_SORTED = 2,    /* geot_check_index: index decreases somewhere */
+    GEOT_ERROR_OUT_OF_RANGE = 3,  /* geot_check_index: index or column outside its range */
+    GEOT_ERROR_HIP = 4,           /* a HIP runtime call failed (detail has the HIP error) */
+    GEOT_ERROR_UNSUPPORTED = 5    /* a forced kernel choice that cannot run this shape */
+} geot_status_t;
+
+/* Kernel families (Section III-B: how the M-loop over rows is split).
+ *  EP: element-parallel. Every row group (`lanes` lanes sharing one row) takes
+ *      a fixed run of `rows` consecutive rows regardless of where segments
+ *      begin, reduces it serially in registers (the paper's sequential
+ *      reduction inside a group), and the groups of a block are combined by
+ *      a segmented scan across lanes (the paper's parallel reduction). Parts
+ *      of segments that cross block boundaries are combined by the same
+ *      kernel run over the per-block partials. Load-balanced for any length
+ *      distribution.
+ *  SP: segment-parallel. One row group (or `groups` row groups of one wave)
+ *      per segment, with segment bounds found first by one pass over the
+ *      index. No cross-group combining; suited to short, even segments.     */
+typedef enum { GEOT_FAMILY_AUTO = 0, GEOT_FAMILY_EP = 1, GEOT_FAMILY_SP = 2 } geot_family_t;
+
+/* A kernel choice (the tunable parameters of Table I, re-cut for 64-wide
+ * waves). Zero in any field means "derive it from the shape". */
+typedef struct {
+    int32_t family; /* geot_family_t */
+    int32_t vec;    /* floats per lane load: 1, 2 or 4 (clamped down to what F and alignment allow) */
+    int32_t lanes;  /* lanes sharing one row: 1, 2, 4, 8, 16, 32 or 64 */
+    int32_t rows;   /* EP: consecutive rows per row group (1..4096) */
+    int32_t groups; /* SP: row groups of one wave that cooperate on one segment (1..64/lanes) */
+    int32_t flags;  /* reserved, must be 0 */
+} geot_kernel_choice_t;
+
+/* Segment-length statistics of a sorted index (all lengths over
+ * [0, num_segments), empties included). */
+typedef struct {
+    int64_t nnz;
+    int64_t num_segments;
+    int64_t max_len;    /* longest segment */
+    int64_t num_empty;  /* segments with no row */
+    int64_t sum_len_sq; /* sum over segments of length^2 */
+    double mean_len;    /* nnz / num_segments */
+    double var_len;     /* population variance of the lengths */
+} geot_index_stats_t;
+
+/* Segment reduction (Section II-B; Listing "GeoT solution for fusion", upper
+ * part: segment_reduce(idx, msg, reduce)).
+ *   src           [nnz x F] fp32, row-major
+ *   sorted_index  [nnz] int64, non-decreasing, values in [0, num_segments)
+ *   out           [num_segments x F] fp32, overwritten; must not overlap inputs
+ * nnz == 0 fills `out` with GEOT_EMPTY_FILL; num_segments == 0 or F == 0 is a
+ * no-op. Returns GEOT_ERROR_INVALID_VALUE for null pointers with nonzero
+ * sizes, negative sizes, an unknown op or overlapping `out`.              */
+geot_status_t geot_segment_reduce(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                  int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                  void *stream);
+
+/* Fused gather-weight-scatter (Section IV index_segment_reduce and its
+ * weighted form used as SpMM in Section V-D):
+ *   out[r, :] = op over edges e with sorted_row[e] == r of weight[e] * X[col[e], :]
+ *   X           [num_x_rows x F] fp32
+ *   col         [nnz] int64 source row of each edge, in [0, num_x_rows)
+ *   weight      [nnz] fp32, or NULL for weight 1 (then the term is X[col[e], :])
+ *   sorted_row  [nnz] int64 destination row, non-decreasing, in [0, num_rows)
+ *   out         [num_rows x F] fp32, overwritten
+ * Each weighted term is one fp32 multiply; mean divides by the edge count.
+ * Same error behaviour as geot_segment_reduce.                              */
+geot_status_t geot_gather_scatter(const float *X, int64_t num_x_rows, const int64_t *col,
+                                  const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                  int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                  void *stream);
+
+/* As the two calls above, with the kernel choice forced (tuning, tests).
+ * `choice` NULL means "use the selector". Fields are validated on the host:
+ * an impossible combination returns GEOT_ERROR_UNSUPPORTED.                */
+geot_status_t geot_segment_reduce_with(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                       int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                       void *stream, const geot_kernel_choice_t *choice);
+geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const int64_t *col,
+                                       const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                       int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                       void *stream, const geot_kernel_choice_t *choice);
+
+/* The selector (Section III-C: a decision tree over O(1) input features,
+ * compiled to if/else). Pure host function: no device access.
+ *   gather  nonzero for geot_gather_scatter, zero for geot_segment_reduce
+ *   stats   optional (NULL allowed); when given, the length variance and the
+ *           longest segment join the features
+ * Writes a fully specified choice to *out.                                  */
+geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, int32_t gather,
+                          const geot_index_stats_t *stats, geot_kernel_choice_t *out);
+
+/* Segment-length statistics of a sorted index (one pass over the index on
+ * the device). Synchronizes `stream`; writes the host struct *host_out.
+ * Precondition as for the reductions; results for an unsorted index are
+ * unspecified.                                                              */
+geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
+                               geot_index_stats_t *host_out, void *stream);
+
+/* Checks the preconditions on the device: index non-decreasing and in
+ * [0, num_segments); when col is non-NULL also 0 <= col < num_x_rows.
+ * Synchronizes `stream`. Returns GEOT_SUCCESS, GEOT_ERROR_NOT_SORTED or
+ * GEOT_ERROR_OUT_OF_RANGE (out of range wins when both hold).              */
+geot_status_t geot_check_index(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
+                               const int64_t *col, int64_t num_x_rows, void *stream);
+
+/* The kernel choice the calling thread's last successful reduction used. */
+geot_status_t geot_last_choice(geot_kernel_choice_t *out);
+
+/* Per-launch timing of the main reduction kernel, for measurement tools.
+ * geot_profile_begin(n) arms up to n records (HIP events on the stream of
+ * each call, around its main kernel only); geot_profile_end synchronizes the
+ * recorded events, writes up to `capacity` durations in milliseconds and the
+ * number recorded, and disarms. Not thread-safe; default off.              */
+geot_status_t geot_profile_begin(int32_t max_records);
+geot_status_t geot_profile_end(float *durations_ms, int32_t capacity, int32_t *count);
+
+/* Static description of a status code. */
+const char *geot_status_string(geot_status_t status);
+
+/* Detail of the calling thread's last failure ("" when none). */
+const char *geot_last_error_detail(void);
+
+/* GEOT_VERSION of the built library. */
+int32_t geot_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GEOT_H */

@@ -1,0 +1,24 @@
+"""libgeot_hip: sorted segment reduction and fused gather-weight-scatter on MI355X (gfx950).
+
+The computation lives in hand-written HIP kernels behind the C-ABI of
+include/geot.h; this package only builds that library and marshals torch
+tensors into it (see ``geot.py``).
+"""
+from .geot import (  # noqa: F401
+    FAMILIES,
+    OPS,
+    GeotError,
+    KernelChoice,
+    IndexStats,
+    LIB_PATH,
+    lib,
+    segment_reduce,
+    gather_scatter,
+    index_stats,
+    check_index,
+    select,
+    last_choice,
+    profile_begin,
+    profile_end,
+    version,
+)

@@ -1,0 +1,627 @@
+// Host side of libgeot_hip: argument checks, kernel selection, temporary
+// memory, launch sequencing and the extern "C" entry points of geot.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/geot.h"
+#include "internal.h"
+#include "selector_generated.h"
+
+namespace geot {
+namespace {
+
+thread_local std::string t_detail;
+thread_local geot_kernel_choice_t t_last_choice = {0, 0, 0, 0, 0, 0};
+
+geot_status_t fail(geot_status_t st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    t_detail = buf;
+    return st;
+}
+
+geot_status_t hip_fail(hipError_t e, const char *what) {
+    return fail(GEOT_ERROR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+#define GEOT_HIP(expr, what)                        \
+    do {                                            \
+        hipError_t e_ = (expr);                     \
+        if (e_ != hipSuccess) return hip_fail(e_, what); \
+    } while (0)
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int pow2ceil(int64_t x) {
+    int p = 1;
+    while (p < x && p < (1 << 30)) p <<= 1;
+    return p;
+}
+
+bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// ---------------------------------------------------------------------------
+// temporary device memory: one stream-ordered pool per device
+// ---------------------------------------------------------------------------
+std::mutex g_pool_mu;
+std::map<int, hipMemPool_t> g_pools;
+
+geot_status_t scratch_alloc(void **p, size_t bytes, hipStream_t st) {
+    *p = nullptr;
+    if (bytes == 0) return GEOT_SUCCESS;
+    int dev = 0;
+    GEOT_HIP(hipGetDevice(&dev), "hipGetDevice");
+    hipMemPool_t pool = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_pool_mu);
+        auto it = g_pools.find(dev);
+        if (it == g_pools.end()) {
+            hipMemPoolProps props;
+            memset(&props, 0, sizeof(props));
+            props.allocType = hipMemAllocationTypePinned;
+            props.location.type = hipMemLocationTypeDevice;
+            props.location.id = dev;
+            GEOT_HIP(hipMemPoolCreate(&pool, &props), "hipMemPoolCreate");
+            uint64_t keep = UINT64_MAX;  // keep freed blocks for reuse
+            GEOT_HIP(hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep),
+                     "hipMemPoolSetAttribute");
+            g_pools[dev] = pool;
+        } else {
+            pool = it->second;
+        }
+    }
+    GEOT_HIP(hipMallocFromPoolAsync(p, bytes, pool, st), "hipMallocFromPoolAsync");
+    return GEOT_SUCCESS;
+}
+
+geot_status_t scratch_free(void *p, hipStream_t st) {
+    if (p) GEOT_HIP(hipFreeAsync(p, st), "hipFreeAsync");
+    return GEOT_SUCCESS;
+}
+
+struct ScratchGuard {
+    void *p = nullptr;
+    hipStream_t st = nullptr;
+    ~ScratchGuard() {
+        if (p) (void)hipFreeAsync(p, st);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// measurement hooks (geot_profile_begin / _end)
+// ---------------------------------------------------------------------------
+struct Profile {
+    bool armed = false;
+    int cap = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+} g_prof;
+
+bool prof_take(hipEvent_t *a, hipEvent_t *b) {
+    if (!g_prof.armed || (int)g_prof.ev.size() >= g_prof.cap) return false;
+    hipEvent_t e0, e1;
+    if (hipEventCreate(&e0) != hipSuccess) return false;
+    if (hipEventCreate(&e1) != hipSuccess) {
+        (void)hipEventDestroy(e0);
+        return false;
+    }
+    g_prof.ev.emplace_back(e0, e1);
+    *a = e0;
+    *b = e1;
+    return true;
+}
+
+// ---------------------------------------------------------------------------
+// problem description and choice resolution
+// ---------------------------------------------------------------------------
+struct Problem {
+    bool gather;
+    const float *src;      // rows or X
+    int64_t num_x_rows;
+    const int64_t *col;
+    const float *w;
+    const int64_t *idx;
+    int64_t nnz, S, F;
+    geot_op_t op;
+    float *out;
+};
+
+struct Resolved {
+    int family, V, NT, L, K, groups, ntiles;
+};
+
+int max_nt(int V) { return V == 4 ? 1 : (V == 2 ? 2 : 4); }
+
+bool valid_shape(int V, int NT, int L) {
+    if (!(V == 1 || V == 2 || V == 4)) return false;
+    if (!is_pow2(L) || L > 64) return false;
+    if (NT == 1) return true;
+    return L == 64 && NT <= max_nt(V) && is_pow2(NT);
+}
+
+void auto_lanes(int64_t F, int V, int *L, int *NT) {
+    const int64_t vecs = ceil_div(F, V);
+    if (vecs <= 64) {
+        *L = pow2ceil(vecs);
+        *NT = 1;
+    } else {
+        *L = 64;
+        *NT = std::min<int>(max_nt(V), pow2ceil(ceil_div(vecs, 64)));
+    }
+}
+
+int auto_rows(int64_t nnz, int L, int V, int NT, int ntiles) {
+    const int64_t G = kBlock / L;
+    const int64_t row_bytes = (int64_t)L * V * NT * 4;
+    const int64_t target_rows = std::max<int64_t>(512, (256 * 1024) / row_bytes);
+    int64_t K = ceil_div(target_rows, G);
+    // keep at least ~1024 blocks in flight when the input allows it
+    const int64_t k_fill = ceil_div(nnz, G * std::max<int64_t>(1, 1024 / ntiles));
+    K = std::min(K, std::max<int64_t>(k_fill, 1));
+    return (int)std::max<int64_t>(1, std::min<int64_t>(K, 512));
+}
+
+int widest_vec(const Problem &p) {
+    auto aligned = [&](int V) {
+        const uintptr_t m = (uintptr_t)(4 * V - 1);
+        if (p.F % V != 0) return false;
+        if (((uintptr_t)p.src & m) != 0 || ((uintptr_t)p.out & m) != 0) return false;
+        return true;
+    };
+    if (aligned(4)) return 4;
+    if (aligned(2)) return 2;
+    return 1;
+}
+
+geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r) {
+    if (c.flags != 0) return fail(GEOT_ERROR_UNSUPPORTED, "choice.flags must be 0");
+    r->family = c.family == GEOT_FAMILY_AUTO ? GEOT_FAMILY_EP : c.family;
+    if (r->family != GEOT_FAMILY_EP && r->family != GEOT_FAMILY_SP)
+        return fail(GEOT_ERROR_UNSUPPORTED, "unknown kernel family %d", c.family);
+    const int vmax = widest_vec(p);
+    int V = c.vec == 0 ? vmax : c.vec;
+    if (!(V == 1 || V == 2 || V == 4)) return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2 or 4");
+    while (V > vmax) V >>= 1;  // clamp to what F and the pointers allow
+    int L, NT;
+    auto_lanes(p.F, V, &L, &NT);
+    if (c.lanes != 0) {
+        if (!is_pow2(c.lanes) || c.lanes > 64)
+            return fail(GEOT_ERROR_UNSUPPORTED, "lanes must be a power of two <= 64");
+        L = c.lanes;
+        if (L != 64) NT = 1;
+    }
+    if (!valid_shape(V, NT, L)) NT = 1;
+    r->V = V;
+    r->NT = NT;
+    r->L = L;
+    const int64_t TW = (int64_t)L * V * NT;
+    const int64_t ntiles = ceil_div(p.F, TW);
+    if (ntiles > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "F too large for lanes*vec");
+    r->ntiles = (int)ntiles;
+    if (c.rows < 0 || c.rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
+    r->K = c.rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles) : c.rows;
+    const int GW = 64 / L;
+    if (c.groups < 0 || (c.groups != 0 && (!is_pow2(c.groups) || c.groups > GW)))
+        return fail(GEOT_ERROR_UNSUPPORTED, "groups must be a power of two <= 64/lanes");
+    if (c.groups != 0) {
+        r->groups = c.groups;
+    } else {
+        const double mean = p.S > 0 ? (double)p.nnz / (double)p.S : 0.0;
+        int gsz = 1;
+        while (gsz < GW && mean >= 16.0 * gsz) gsz <<= 1;
+        r->groups = gsz;
+    }
+    return GEOT_SUCCESS;
+}
+
+geot_kernel_choice_t to_choice(const Resolved &r) {
+    geot_kernel_choice_t c;
+    c.family = r.family;
+    c.vec = r.V;
+    c.lanes = r.L;
+    c.rows = r.K;
+    c.groups = r.groups;
+    c.flags = 0;
+    return c;
+}
+
+void select_raw(int64_t nnz, int64_t S, int64_t F, geot_op_t op, int gather,
+                const geot_index_stats_t *stats, geot_kernel_choice_t *c) {
+    double cv = 0.0, max_rel = 0.0;
+    const double mean = S > 0 ? (double)nnz / (double)S : 0.0;
+    if (stats && mean > 0) {
+        cv = stats->var_len > 0 ? std::sqrt(stats->var_len) / mean : 0.0;
+        max_rel = (double)stats->max_len / mean;
+    }
+    int32_t o[5];
+    tree_select((double)nnz, (double)S, (double)F, (int)op, gather, stats != nullptr, cv, max_rel, o);
+    c->family = o[0];
+    c->vec = o[1];
+    c->lanes = o[2];
+    c->rows = o[3];
+    c->groups = o[4];
+    c->flags = 0;
+}
+
+// ---------------------------------------------------------------------------
+// argument checks (host only, before any device work)
+// ---------------------------------------------------------------------------
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + nb && b0 < a0 + na;
+}
+
+geot_status_t check_args(const Problem &p) {
+    if (p.op != GEOT_OP_SUM && p.op != GEOT_OP_MEAN && p.op != GEOT_OP_MAX)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)p.op);
+    if (p.nnz < 0 || p.S < 0 || p.F < 0 || (p.gather && p.num_x_rows < 0))
+        return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (p.S == 0 || p.F == 0) return GEOT_SUCCESS;
+    const int64_t kMax = (int64_t)1 << 62;
+    if (p.F > ((int64_t)1 << 31) || p.S > kMax / p.F || p.nnz > kMax / p.F ||
+        (p.gather && p.num_x_rows > kMax / p.F))
+        return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
+    if (!p.out) return fail(GEOT_ERROR_INVALID_VALUE, "out is NULL");
+    const size_t out_bytes = (size_t)(p.S * p.F) * 4;
+    if (p.nnz > 0) {
+        if (!p.idx) return fail(GEOT_ERROR_INVALID_VALUE, "index is NULL");
+        if (!p.src) return fail(GEOT_ERROR_INVALID_VALUE, p.gather ? "X is NULL" : "src is NULL");
+        if (p.gather) {
+            if (!p.col) return fail(GEOT_ERROR_INVALID_VALUE, "col is NULL");
+            if (p.num_x_rows == 0) return fail(GEOT_ERROR_INVALID_VALUE, "X has no rows but nnz > 0");
+        }
+        const size_t src_rows = (size_t)(p.gather ? p.num_x_rows : p.nnz);
+        if (overlaps(p.out, out_bytes, p.src, src_rows * (size_t)p.F * 4) ||
+            overlaps(p.out, out_bytes, p.idx, (size_t)p.nnz * 8) ||
+            overlaps(p.out, out_bytes, p.col, p.gather ? (size_t)p.nnz * 8 : 0) ||
+            overlaps(p.out, out_bytes, p.w, p.gather ? (size_t)p.nnz * 4 : 0))
+            return fail(GEOT_ERROR_INVALID_VALUE, "out overlaps an input");
+    }
+    return GEOT_SUCCESS;
+}
+
+// ---------------------------------------------------------------------------
+// launch sequences
+// ---------------------------------------------------------------------------
+struct Level {
+    int64_t n, K, nchunks;
+};
+
+int64_t piece_rows_k(int64_t n, int64_t G) {
+    if (n <= G * 512) return ceil_div(n, G);  // one block finishes it
+    return std::max<int64_t>(4, std::min<int64_t>(512, ceil_div(n, G * 256)));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
+    const int64_t G = kBlock / r.L;
+    const int64_t TW = (int64_t)r.L * r.V * r.NT;
+    const int64_t ld_p = ceil_div(p.F, 4) * 4;
+    std::vector<Level> lv;
+    lv.push_back({p.nnz, r.K, ceil_div(p.nnz, G * r.K)});
+    while (lv.back().nchunks > 1) {
+        const int64_t n = 2 * lv.back().nchunks;
+        const int64_t K = piece_rows_k(n, G);
+        lv.push_back({n, K, ceil_div(n, G * K)});
+        if (lv.size() > 64) return fail(GEOT_ERROR_HIP, "internal: level count");
+    }
+    (void)TW;
+    // partial buffers of levels 1..: values, segment ids, counts
+    std::vector<size_t> off_v(lv.size(), 0), off_s(lv.size(), 0), off_c(lv.size(), 0);
+    size_t bytes = 0;
+    for (size_t l = 1; l < lv.size(); ++l) {
+        off_v[l] = bytes;
+        bytes = align256(bytes + (size_t)lv[l].n * (size_t)ld_p * 4);
+        off_s[l] = bytes;
+        bytes = align256(bytes + (size_t)lv[l].n * 8);
+        off_c[l] = bytes;
+        bytes = align256(bytes + (size_t)lv[l].n * 8);
+    }
+    ScratchGuard sg;
+    sg.st = st;
+    geot_status_t s = scratch_alloc(&sg.p, bytes, st);
+    if (s != GEOT_SUCCESS) return s;
+    char *base = (char *)sg.p;
+    const int red = p.op == GEOT_OP_MAX ? RED_MAX : RED_SUM;
+    for (size_t l = 0; l < lv.size(); ++l) {
+        EpArgs a;
+        memset(&a, 0, sizeof(a));
+        if (l == 0) {
+            a.src = p.src;
+            a.ld_src = p.F;
+            a.idx = p.idx;
+            a.col = p.col;
+            a.w = p.w;
+            a.num_x_rows = p.num_x_rows;
+            a.fill_gaps = 1;
+        } else {
+            a.src = (const float *)(base + off_v[l]);
+            a.ld_src = ld_p;
+            a.idx = (const int64_t *)(base + off_s[l]);
+            a.cnt = (const int64_t *)(base + off_c[l]);
+            a.fill_gaps = 0;
+        }
+        a.n = lv[l].n;
+        a.S = p.S;
+        a.F = p.F;
+        a.out = p.out;
+        a.ld_out = p.F;
+        if (l + 1 < lv.size()) {
+            a.pv = (float *)(base + off_v[l + 1]);
+            a.pseg = (int64_t *)(base + off_s[l + 1]);
+            a.pcnt = (int64_t *)(base + off_c[l + 1]);
+            a.ld_p = ld_p;
+        }
+        a.K = (int32_t)lv[l].K;
+        a.ntiles = r.ntiles;
+        a.mean = p.op == GEOT_OP_MEAN ? 1 : 0;
+        const int mode = l == 0 ? (p.gather ? SRC_GATHER : SRC_ROWS) : SRC_PIECES;
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        const bool prof = l == 0 && prof_take(&e0, &e1);
+        if (prof) GEOT_HIP(hipEventRecord(e0, st), "hipEventRecord");
+        GEOT_HIP(launch_ep(a, red, mode, r.V, r.NT, r.L, lv[l].nchunks, st), "launch element-parallel kernel");
+        if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+    }
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    return scratch_free(p_free, st);
+}
+
+geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
+    ScratchGuard sg;
+    sg.st = st;
+    geot_status_t s = scratch_alloc(&sg.p, (size_t)(p.S + 1) * 8, st);
+    if (s != GEOT_SUCCESS) return s;
+    int64_t *off = (int64_t *)sg.p;
+    GEOT_HIP(launch_offsets(p.idx, p.nnz, p.S, off, st), "launch offsets kernel");
+    SpArgs a;
+    memset(&a, 0, sizeof(a));
+    a.src = p.src;
+    a.ld_src = p.F;
+    a.off = off;
+    a.col = p.col;
+    a.w = p.w;
+    a.num_x_rows = p.num_x_rows;
+    a.S = p.S;
+    a.F = p.F;
+    a.out = p.out;
+    a.ld_out = p.F;
+    a.groups = r.groups;
+    a.ntiles = r.ntiles;
+    a.mean = p.op == GEOT_OP_MEAN ? 1 : 0;
+    const int red = p.op == GEOT_OP_MAX ? RED_MAX : RED_SUM;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    const bool prof = prof_take(&e0, &e1);
+    if (prof) GEOT_HIP(hipEventRecord(e0, st), "hipEventRecord");
+    GEOT_HIP(launch_sp(a, red, p.gather ? SRC_GATHER : SRC_ROWS, r.V, r.NT, r.L, st),
+             "launch segment-parallel kernel");
+    if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    return scratch_free(p_free, st);
+}
+
+geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_t *forced) {
+    t_detail.clear();
+    geot_status_t s = check_args(p);
+    if (s != GEOT_SUCCESS) return s;
+    if (p.S == 0 || p.F == 0) return GEOT_SUCCESS;
+    if (p.nnz == 0) {
+        GEOT_HIP(launch_fill(p.out, p.S, p.F, p.F, GEOT_EMPTY_FILL, st), "launch fill kernel");
+        t_last_choice = geot_kernel_choice_t{0, 0, 0, 0, 0, 0};
+        return GEOT_SUCCESS;
+    }
+    geot_kernel_choice_t c;
+    if (forced) {
+        c = *forced;
+    } else {
+        select_raw(p.nnz, p.S, p.F, p.op, p.gather ? 1 : 0, nullptr, &c);
+    }
+    Resolved r;
+    s = resolve(p, c, &r);
+    if (s != GEOT_SUCCESS) return s;
+    s = r.family == GEOT_FAMILY_SP ? run_sp(p, r, st) : run_ep(p, r, st);
+    if (s == GEOT_SUCCESS) t_last_choice = to_choice(r);
+    return s;
+}
+
+}  // namespace
+}  // namespace geot
+
+using namespace geot;
+
+extern "C" {
+
+geot_status_t geot_segment_reduce_with(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                       int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                       void *stream, const geot_kernel_choice_t *choice) {
+    Problem p{false, src, 0, nullptr, nullptr, sorted_index, nnz, num_segments, F, op, out};
+    return reduce(p, (hipStream_t)stream, choice);
+}
+
+geot_status_t geot_segment_reduce(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                  int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                  void *stream) {
+    return geot_segment_reduce_with(src, sorted_index, nnz, num_segments, F, op, out, stream, nullptr);
+}
+
+geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const int64_t *col,
+                                       const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                       int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                       void *stream, const geot_kernel_choice_t *choice) {
+    Problem p{true, X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, op, out};
+    return reduce(p, (hipStream_t)stream, choice);
+}
+
+geot_status_t geot_gather_scatter(const float *X, int64_t num_x_rows, const int64_t *col,
+                                  const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                  int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                  void *stream) {
+    return geot_gather_scatter_with(X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, op,
+                                    out, stream, nullptr);
+}
+
+geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, int32_t gather,
+                          const geot_index_stats_t *stats, geot_kernel_choice_t *out) {
+    t_detail.clear();
+    if (!out) return fail(GEOT_ERROR_INVALID_VALUE, "out is NULL");
+    if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
+    if (nnz < 0 || num_segments < 0 || F < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    geot_kernel_choice_t c;
+    select_raw(nnz, num_segments, F, op, gather ? 1 : 0, stats, &c);
+    if (F == 0) {
+        *out = c;
+        return GEOT_SUCCESS;
+    }
+    // resolve against 256-byte aligned pointers (what device allocators return)
+    Problem p{gather != 0, (const float *)(uintptr_t)256, 0, nullptr, nullptr, nullptr,
+              nnz, num_segments, F, op, (float *)(uintptr_t)256};
+    Resolved r;
+    geot_status_t s = resolve(p, c, &r);
+    if (s != GEOT_SUCCESS) return s;
+    *out = to_choice(r);
+    return GEOT_SUCCESS;
+}
+
+geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
+                               geot_index_stats_t *host_out, void *stream) {
+    t_detail.clear();
+    if (!host_out) return fail(GEOT_ERROR_INVALID_VALUE, "host_out is NULL");
+    if (nnz < 0 || num_segments <= 0) return fail(GEOT_ERROR_INVALID_VALUE, "need nnz >= 0 and num_segments > 0");
+    if (nnz > 0 && !sorted_index) return fail(GEOT_ERROR_INVALID_VALUE, "index is NULL");
+    geot_index_stats_t o;
+    memset(&o, 0, sizeof(o));
+    o.nnz = nnz;
+    o.num_segments = num_segments;
+    o.mean_len = (double)nnz / (double)num_segments;
+    if (nnz == 0) {
+        o.num_empty = num_segments;
+        *host_out = o;
+        return GEOT_SUCCESS;
+    }
+    hipStream_t st = (hipStream_t)stream;
+    ScratchGuard sg;
+    sg.st = st;
+    const size_t off_bytes = align256((size_t)(num_segments + 1) * 8);
+    geot_status_t s = scratch_alloc(&sg.p, off_bytes + 64, st);
+    if (s != GEOT_SUCCESS) return s;
+    int64_t *off = (int64_t *)sg.p;
+    unsigned long long *acc = (unsigned long long *)((char *)sg.p + off_bytes);
+    GEOT_HIP(launch_offsets(sorted_index, nnz, num_segments, off, st), "launch offsets kernel");
+    GEOT_HIP(launch_zero_u64(acc, 3, st), "launch zero kernel");
+    GEOT_HIP(launch_len_stats(off, num_segments, acc, st), "launch length statistics kernel");
+    unsigned long long h[3] = {0, 0, 0};
+    GEOT_HIP(hipMemcpyAsync(h, acc, sizeof(h), hipMemcpyDeviceToHost, st), "hipMemcpyAsync");
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    s = scratch_free(p_free, st);
+    if (s != GEOT_SUCCESS) return s;
+    GEOT_HIP(hipStreamSynchronize(st), "hipStreamSynchronize");
+    o.sum_len_sq = (int64_t)h[0];
+    o.max_len = (int64_t)h[1];
+    o.num_empty = (int64_t)h[2];
+    const double ex2 = (double)o.sum_len_sq / (double)num_segments;
+    o.var_len = std::max(0.0, ex2 - o.mean_len * o.mean_len);
+    *host_out = o;
+    return GEOT_SUCCESS;
+}
+
+geot_status_t geot_check_index(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
+                               const int64_t *col, int64_t num_x_rows, void *stream) {
+    t_detail.clear();
+    if (nnz < 0 || num_segments < 0 || num_x_rows < 0)
+        return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (nnz == 0) return GEOT_SUCCESS;
+    if (!sorted_index) return fail(GEOT_ERROR_INVALID_VALUE, "index is NULL");
+    hipStream_t st = (hipStream_t)stream;
+    ScratchGuard sg;
+    sg.st = st;
+    geot_status_t s = scratch_alloc(&sg.p, 64, st);
+    if (s != GEOT_SUCCESS) return s;
+    unsigned int *flags = (unsigned int *)sg.p;
+    GEOT_HIP(launch_zero_u64((unsigned long long *)sg.p, 1, st), "launch zero kernel");
+    GEOT_HIP(launch_check(sorted_index, nnz, num_segments, col, num_x_rows, flags, st),
+             "launch check kernel");
+    unsigned int h = 0;
+    GEOT_HIP(hipMemcpyAsync(&h, flags, sizeof(h), hipMemcpyDeviceToHost, st), "hipMemcpyAsync");
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    s = scratch_free(p_free, st);
+    if (s != GEOT_SUCCESS) return s;
+    GEOT_HIP(hipStreamSynchronize(st), "hipStreamSynchronize");
+    if (h & 1u) return fail(GEOT_ERROR_OUT_OF_RANGE, "index or column out of range");
+    if (h & 2u) return fail(GEOT_ERROR_NOT_SORTED, "index is not non-decreasing");
+    return GEOT_SUCCESS;
+}
+
+geot_status_t geot_last_choice(geot_kernel_choice_t *out) {
+    if (!out) return fail(GEOT_ERROR_INVALID_VALUE, "out is NULL");
+    *out = t_last_choice;
+    return GEOT_SUCCESS;
+}
+
+geot_status_t geot_profile_begin(int32_t max_records) {
+    if (max_records < 0 || max_records > (1 << 20)) return fail(GEOT_ERROR_INVALID_VALUE, "bad max_records");
+    for (auto &e : g_prof.ev) {
+        (void)hipEventDestroy(e.first);
+        (void)hipEventDestroy(e.second);
+    }
+    g_prof.ev.clear();
+    g_prof.ev.reserve((size_t)max_records);
+    g_prof.cap = max_records;
+    g_prof.armed = max_records > 0;
+    return GEOT_SUCCESS;
+}
+
+geot_status_t geot_profile_end(float *durations_ms, int32_t capacity, int32_t *count) {
+    geot_status_t st = GEOT_SUCCESS;
+    int32_t n = 0;
+    for (auto &e : g_prof.ev) {
+        float ms = 0.0f;
+        hipError_t r = hipEventSynchronize(e.second);
+        if (r == hipSuccess) r = hipEventElapsedTime(&ms, e.first, e.second);
+        if (r != hipSuccess && st == GEOT_SUCCESS) st = hip_fail(r, "profile events");
+        if (durations_ms && n < capacity) durations_ms[n] = ms;
+        ++n;
+        (void)hipEventDestroy(e.first);
+        (void)hipEventDestroy(e.second);
+    }
+    g_prof.ev.clear();
+    g_prof.armed = false;
+    g_prof.cap = 0;
+    if (count) *count = n;
+    return st;
+}
+
+const char *geot_status_string(geot_status_t status) {
+    switch (status) {
+        case GEOT_SUCCESS: return "success";
+        case GEOT_ERROR_INVALID_VALUE: return "invalid value";
+        case GEOT_ERROR_NOT_SORTED: return "index not sorted";
+        case GEOT_ERROR_OUT_OF_RANGE: return "index out of range";
+        case GEOT_ERROR_HIP: return "HIP runtime error";
+        case GEOT_ERROR_UNSUPPORTED: return "unsupported kernel choice";
+    }
+    return "unknown status";
+}
+
+const char *geot_last_error_detail(void) { return t_detail.c_str(); }
+
+int32_t geot_version(void) { return GEOT_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,142 @@
+// Small helper kernels: output fill, segment starts from a sorted index,
+// segment-length statistics and the precondition check.
+#include "common.h"
+
+namespace geot {
+
+namespace {
+
+__global__ __launch_bounds__(256) void fill_kernel(float *out, int64_t rows, int64_t F, int64_t ld,
+                                                   float value) {
+    const int64_t total = rows * F;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / F;
+        out[r * ld + (i - r * F)] = value;
+    }
+}
+
+// off[s] = first row i with idx[i] >= s. Row i writes the starts of every
+// segment in (idx[i-1], idx[i]] (so empty segments get the next start), and
+// the last row also writes (idx[n-1], S] = n.
+__global__ __launch_bounds__(256) void offsets_kernel(const int64_t *idx, int64_t n, int64_t S,
+                                                      int64_t *off) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t s = idx[i];
+        const int64_t sp = i > 0 ? idx[i - 1] : -1;
+        const int64_t hi = min(s, S);
+        for (int64_t t = max(sp + 1, (int64_t)0); t <= hi; ++t) off[t] = i;
+        if (i == n - 1)
+            for (int64_t t = max(s + 1, (int64_t)0); t <= S; ++t) off[t] = n;
+    }
+}
+
+__global__ __launch_bounds__(256) void len_stats_kernel(const int64_t *off, int64_t S,
+                                                        unsigned long long *acc) {
+    unsigned long long sq = 0, mx = 0, ne = 0;
+    for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < S;
+         s += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t len = off[s + 1] - off[s];
+        const unsigned long long l = len > 0 ? (unsigned long long)len : 0ull;
+        sq += l * l;
+        mx = l > mx ? l : mx;
+        ne += len == 0 ? 1ull : 0ull;
+    }
+    __shared__ unsigned long long s_sq[256], s_mx[256], s_ne[256];
+    s_sq[threadIdx.x] = sq;
+    s_mx[threadIdx.x] = mx;
+    s_ne[threadIdx.x] = ne;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) {
+            s_sq[threadIdx.x] += s_sq[threadIdx.x + h];
+            s_mx[threadIdx.x] = max(s_mx[threadIdx.x], s_mx[threadIdx.x + h]);
+            s_ne[threadIdx.x] += s_ne[threadIdx.x + h];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        atomicAdd(&acc[0], s_sq[0]);
+        atomicMax(&acc[1], s_mx[0]);
+        atomicAdd(&acc[2], s_ne[0]);
+    }
+}
+
+__global__ __launch_bounds__(256) void check_kernel(const int64_t *idx, int64_t n, int64_t S,
+                                                    const int64_t *col, int64_t nx,
+                                                    unsigned int *flags) {
+    unsigned int bad = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t s = idx[i];
+        if (s < 0 || s >= S) bad |= 1u;
+        if (i > 0 && s < idx[i - 1]) bad |= 2u;
+        if (col != nullptr) {
+            const int64_t c = col[i];
+            if (c < 0 || c >= nx) bad |= 1u;
+        }
+    }
+    __shared__ unsigned int s_bad[256];
+    s_bad[threadIdx.x] = bad;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) s_bad[threadIdx.x] |= s_bad[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0 && s_bad[0] != 0) atomicOr(flags, s_bad[0]);
+}
+
+__global__ void zero_u64_kernel(unsigned long long *p, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0ull;
+}
+
+unsigned grid_for(int64_t work, int64_t per_block, int64_t cap) {
+    int64_t b = (work + per_block - 1) / per_block;
+    if (b < 1) b = 1;
+    if (b > cap) b = cap;
+    return (unsigned)b;
+}
+
+}  // namespace
+
+hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float value,
+                       hipStream_t stream) {
+    if (rows <= 0 || F <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_kernel, dim3(grid_for(rows * F, 256 * 8, 65536)), dim3(256), 0, stream,
+                       out, rows, F, ld, value);
+    return hipGetLastError();
+}
+
+hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off,
+                          hipStream_t stream) {
+    if (n <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(offsets_kernel, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
+                       idx, n, S, off);
+    return hipGetLastError();
+}
+
+hipError_t launch_len_stats(const int64_t *off, int64_t S, unsigned long long *acc,
+                            hipStream_t stream) {
+    hipLaunchKernelGGL(len_stats_kernel, dim3(grid_for(S, 256 * 16, 4096)), dim3(256), 0, stream,
+                       off, S, acc);
+    return hipGetLastError();
+}
+
+hipError_t launch_check(const int64_t *idx, int64_t n, int64_t S, const int64_t *col, int64_t nx,
+                        unsigned int *flags, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(check_kernel, dim3(grid_for(n, 256 * 16, 8192)), dim3(256), 0, stream, idx,
+                       n, S, col, nx, flags);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero_u64(unsigned long long *p, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(grid_for(n, 256, 1024)), dim3(256), 0, stream, p, n);
+    return hipGetLastError();
+}
+
+}  // namespace geot

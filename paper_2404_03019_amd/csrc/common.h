@@ -1,0 +1,72 @@
+// Device helpers shared by the reduction kernels: vector loads/stores of 1, 2
+// or 4 floats, the reduction operator and lane shuffles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "internal.h"
+
+namespace geot {
+
+template <int RED>
+__device__ __forceinline__ float red_neutral() {
+    return RED == RED_SUM ? 0.0f : -INFINITY;
+}
+
+template <int RED>
+__device__ __forceinline__ float red_apply(float a, float b) {
+    if constexpr (RED == RED_SUM) {
+        return a + b;
+    } else {
+        return fmaxf(a, b);
+    }
+}
+
+template <int V>
+__device__ __forceinline__ void load_vec(const float *p, float *x) {
+    if constexpr (V == 4) {
+        const float4 t = *reinterpret_cast<const float4 *>(p);
+        x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    } else if constexpr (V == 2) {
+        const float2 t = *reinterpret_cast<const float2 *>(p);
+        x[0] = t.x; x[1] = t.y;
+    } else {
+        x[0] = *p;
+    }
+}
+
+template <int V>
+__device__ __forceinline__ void store_vec(float *p, const float *x) {
+    if constexpr (V == 4) {
+        *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
+    } else if constexpr (V == 2) {
+        *reinterpret_cast<float2 *>(p) = make_float2(x[0], x[1]);
+    } else {
+        *p = x[0];
+    }
+}
+
+// Value of `v` held by lane (lane - delta) of the wave; lanes below `delta`
+// get their own value back (callers mask them). ds_bpermute underneath.
+__device__ __forceinline__ float shfl_up_f(float v, int delta) {
+    return __shfl_up(v, (unsigned)delta, 64);
+}
+
+__device__ __forceinline__ int shfl_up_i(int v, int delta) {
+    return __shfl_up(v, (unsigned)delta, 64);
+}
+
+__device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int delta) {
+    const int lo = __shfl_up((int)(uint32_t)(uint64_t)v, (unsigned)delta, 64);
+    const int hi = __shfl_up((int)(uint32_t)((uint64_t)v >> 32), (unsigned)delta, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+}
+
+__device__ __forceinline__ float shfl_down_f(float v, int delta) {
+    return __shfl_down(v, (unsigned)delta, 64);
+}
+
+}  // namespace geot

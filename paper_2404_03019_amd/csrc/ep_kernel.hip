@@ -1,0 +1,382 @@
+// Element-parallel segment reduction for gfx950.
+//
+// The rows are cut into chunks of equal size, one chunk per block and column
+// tile, regardless of where segments begin, so the work per block is the same
+// for any length distribution (the heavy tails of power-law graphs included).
+// Inside a block, each row group (L lanes sharing one row; lane j holds
+// columns j*V .. j*V+V-1 of the tile, NT times) takes K consecutive rows and
+// reduces them serially in registers, storing every segment that starts and
+// ends inside its run with one plain store (the paper's sequential reduction,
+// Section III-B, with the N-loop held in registers). The first and last
+// segment of each run are then combined across the row groups of the block
+// by a segmented scan (the paper's parallel reduction, Algorithm 1, recast):
+// a Hillis-Steele scan over row groups inside each wave with lane shuffles,
+// and across the four waves through LDS. A segment that crosses the block's
+// first or last row leaves one partial per block side ("lo" and "hi"); these
+// partials are themselves a sorted list of rows with counts, and the same
+// kernel reduces them at the next level until one block remains. No atomics,
+// no output memset, and the result does not depend on timing.
+#include "common.h"
+
+namespace geot {
+
+namespace {
+
+template <int RED, int MODE, int V, int NT, int L>
+__global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
+    constexpr int NV = V * NT;        // floats per lane
+    constexpr int GW = 64 / L;        // row groups per wave
+    constexpr int NW = kBlock / 64;   // waves per block
+    constexpr int G = kBlock / L;     // row groups per block
+    constexpr int TW = NT * L * V;    // columns per tile
+    constexpr int U = NV >= 4 ? 4 : 8;  // rows loaded ahead per row group
+
+    __shared__ float s_v[NW][TW];
+    __shared__ int64_t s_n[NW];
+    __shared__ int s_f[NW];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int gw = lane / L;          // row group within the wave
+    const int gl = lane - gw * L;     // lane within the row group
+    const int g = wave * GW + gw;     // row group within the block
+
+    const int64_t chunk = blockIdx.x / a.ntiles;
+    const int tile = (int)(blockIdx.x - chunk * a.ntiles);
+    const int64_t bsize = (int64_t)G * a.K;
+    const int64_t bstart = chunk * bsize;
+    const int64_t bend = min(bstart + bsize, a.n);
+    const int64_t r0 = min(bstart + (int64_t)g * a.K, bend);
+    const int64_t r1 = min(r0 + (int64_t)a.K, bend);
+    const bool has_rows = r0 < r1;
+
+    int64_t cb[NT];
+    bool cv[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        cb[j] = (int64_t)tile * TW + (int64_t)(j * L + gl) * V;
+        cv[j] = cb[j] < a.F;
+    }
+    const float neutral = red_neutral<RED>();
+
+    // ---- helpers -------------------------------------------------------
+    auto store_seg = [&](int64_t seg, const float *v, int64_t n) {
+        if (MODE == SRC_PIECES && n == 0) return;     // only empty partials: stored elsewhere
+        if ((uint64_t)seg >= (uint64_t)a.S) return;   // out-of-range id: skip the store
+        float *o = a.out + seg * a.ld_out;
+        const float fn = (float)n;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            if (!cv[j]) continue;
+            float t[V];
+#pragma unroll
+            for (int k = 0; k < V; ++k) t[k] = a.mean ? v[j * V + k] / fn : v[j * V + k];
+            store_vec<V>(o + cb[j], t);
+        }
+    };
+    auto fill_empty = [&](int64_t s_lo, int64_t s_hi) {  // segments [s_lo, s_hi) have no rows
+        s_lo = max(s_lo, (int64_t)0);
+        s_hi = min(s_hi, a.S);
+        float z[V];
+#pragma unroll
+        for (int k = 0; k < V; ++k) z[k] = 0.0f;
+        for (int64_t s = s_lo; s < s_hi; ++s) {
+            float *o = a.out + s * a.ld_out;
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                if (cv[j]) store_vec<V>(o + cb[j], z);
+        }
+    };
+    auto write_partial = [&](int slot, int64_t seg, const float *v, int64_t n) {
+        if (a.pv == nullptr) return;
+        const int64_t row = 2 * chunk + slot;
+        if (n > 0) {
+            float *p = a.pv + row * a.ld_p;
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                if (cv[j]) store_vec<V>(p + cb[j], v + j * V);
+        }
+        if (tile == 0 && gl == 0) {
+            a.pseg[row] = seg;
+            a.pcnt[row] = n;
+        }
+    };
+    auto load_term = [&](int64_t r, float *x, int64_t &c) {
+        if constexpr (MODE == SRC_ROWS) {
+            c = 1;
+            const float *p = a.src + r * a.ld_src;
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                if (cv[j]) load_vec<V>(p + cb[j], x + j * V);
+                else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
+            }
+        } else if constexpr (MODE == SRC_PIECES) {
+            c = a.cnt[r];
+            const float *p = a.src + r * a.ld_src;
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                if (cv[j] && c > 0) load_vec<V>(p + cb[j], x + j * V);
+                else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
+            }
+        } else {
+            c = 1;
+            const int64_t src_row = a.col[r];
+            const float wt = a.w ? a.w[r] : 1.0f;
+            const bool ok = (uint64_t)src_row < (uint64_t)a.num_x_rows;
+            const float *p = a.src + src_row * a.ld_src;
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                if (cv[j] && ok) {
+                    load_vec<V>(p + cb[j], x + j * V);
+#pragma unroll
+                    for (int k = 0; k < V; ++k) x[j * V + k] = wt * x[j * V + k];
+                } else {
+                    for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
+                }
+            }
+        }
+    };
+
+    // ---- serial reduction of this row group's run [r0, r1) --------------
+    int64_t first_seg = -1, cur = -1, accn = 0, headn = 0;
+    float acc[NV], head[NV];
+    bool head_done = false;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) { acc[k] = neutral; head[k] = neutral; }
+
+    auto step = [&](int64_t s, const float *x, int64_t c) {
+        if (s != cur) {
+            if (!head_done) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) head[k] = acc[k];
+                headn = accn;
+                head_done = true;
+            } else {
+                store_seg(cur, acc, accn);  // started and ended inside this run
+            }
+            if (a.fill_gaps) fill_empty(cur + 1, s);
+            cur = s;
+#pragma unroll
+            for (int k = 0; k < NV; ++k) acc[k] = x[k];
+            accn = c;
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) acc[k] = red_apply<RED>(acc[k], x[k]);
+            accn += c;
+        }
+    };
+
+    int64_t prev = -1, next = -1;
+    if (has_rows) {
+        first_seg = a.idx[r0];
+        cur = first_seg;
+        prev = r0 > 0 ? a.idx[r0 - 1] : -1;
+        next = r1 < a.n ? a.idx[r1] : -1;
+        if (a.fill_gaps) fill_empty(prev + 1, first_seg);
+
+        int64_t r = r0;
+        for (; r + U <= r1; r += U) {
+            int64_t s[U], c[U];
+            float x[U][NV];
+#pragma unroll
+            for (int u = 0; u < U; ++u) s[u] = a.idx[r + u];
+#pragma unroll
+            for (int u = 0; u < U; ++u) load_term(r + u, x[u], c[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) step(s[u], x[u], c[u]);
+        }
+        for (; r < r1; ++r) {
+            float x[NV];
+            int64_t c;
+            const int64_t s = a.idx[r];
+            load_term(r, x, c);
+            step(s, x, c);
+        }
+        if (a.fill_gaps && r1 == a.n) fill_empty(cur + 1, a.S);  // trailing empty segments
+    }
+    const bool single_run = !head_done;  // the run holds one segment only: head == tail
+    if (single_run) {
+#pragma unroll
+        for (int k = 0; k < NV; ++k) head[k] = acc[k];
+        headn = accn;
+    }
+    const int64_t last_seg = cur;
+    const bool starts = has_rows && prev != first_seg;     // first segment begins at r0
+    const bool ends_tail = has_rows && next != last_seg;   // last segment ends at r1 - 1
+
+    // ---- segmented scan of the run tails across row groups --------------
+    // Element of group g: (flag = a segment begins inside the run, tail partial, tail count).
+    // (f1, v1, n1) (+) (f2, v2, n2) = (f1 | f2, f2 ? v2 : v1 (+) v2, f2 ? n2 : n1 + n2).
+    bool f = has_rows && (starts || !single_run);
+    float v[NV];
+    int64_t n = has_rows ? accn : 0;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] = acc[k];
+#pragma unroll
+    for (int d = 1; d < GW; d <<= 1) {
+        const int fo = shfl_up_i((int)f, d * L);
+        const int64_t no = shfl_up_i64(n, d * L);
+        float vo[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], d * L);
+        if (gw >= d) {
+            if (!f) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) v[k] = red_apply<RED>(vo[k], v[k]);
+                n += no;
+            }
+            f = f || fo;
+        }
+    }
+    if (gw == GW - 1) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int k = 0; k < V; ++k) s_v[wave][(j * L + gl) * V + k] = v[j * V + k];
+        if (gl == 0) {
+            s_n[wave] = n;
+            s_f[wave] = (int)f;
+        }
+    }
+    __syncthreads();
+
+    // exclusive prefix of this group: waves before this one, then groups before it in the wave
+    bool ef = false;
+    float ev[NV];
+    int64_t en = 0;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) ev[k] = neutral;
+    for (int w2 = 0; w2 < wave; ++w2) {
+        const bool f2 = s_f[w2] != 0;
+        const int64_t n2 = s_n[w2];
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                const float x2 = s_v[w2][(j * L + gl) * V + k];
+                ev[j * V + k] = f2 ? x2 : red_apply<RED>(ev[j * V + k], x2);
+            }
+        en = f2 ? n2 : en + n2;
+        ef = ef || f2;
+    }
+    {
+        const int fo = shfl_up_i((int)f, L);
+        const int64_t no = shfl_up_i64(n, L);
+        float vo[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], L);
+        if (gw > 0) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) ev[k] = fo ? vo[k] : red_apply<RED>(ev[k], vo[k]);
+            en = fo ? no : en + no;
+            ef = ef || (fo != 0);
+        }
+    }
+
+    // ---- finish the head and tail segments of the run -------------------
+    if (has_rows) {
+        const bool last_group = (r1 == bend);
+        bool hi_written = false;
+        // value of the run's first segment including what precedes it in the block
+        float hv[NV];
+        int64_t hn;
+        bool h_in_block;
+        if (starts) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) hv[k] = head[k];
+            hn = headn;
+            h_in_block = true;
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) hv[k] = red_apply<RED>(ev[k], head[k]);
+            hn = en + headn;
+            h_in_block = ef;
+        }
+        if (!single_run) {
+            // the first segment ends inside the run
+            if (h_in_block) store_seg(first_seg, hv, hn);
+            else write_partial(0, first_seg, hv, hn);
+            // the last segment began inside the run
+            if (ends_tail) {
+                store_seg(last_seg, acc, accn);
+            } else if (last_group) {
+                write_partial(1, last_seg, acc, accn);
+                hi_written = true;
+            }
+        } else if (ends_tail) {
+            if (h_in_block) store_seg(first_seg, hv, hn);
+            else write_partial(0, first_seg, hv, hn);
+        } else if (last_group) {
+            write_partial(h_in_block ? 1 : 0, first_seg, hv, hn);
+            hi_written = h_in_block;
+        }
+        // empty partials keep the list of partials sorted and complete
+        if (g == 0 && starts && a.pv != nullptr && tile == 0 && gl == 0) {
+            a.pseg[2 * chunk] = first_seg;
+            a.pcnt[2 * chunk] = 0;
+        }
+        if (last_group && !hi_written && a.pv != nullptr && tile == 0 && gl == 0) {
+            a.pseg[2 * chunk + 1] = last_seg;
+            a.pcnt[2 * chunk + 1] = 0;
+        }
+    }
+}
+
+template <int RED, int MODE, int V, int NT, int L>
+hipError_t launch_one(const EpArgs &a, int64_t nchunks, hipStream_t stream) {
+    const int64_t blocks = nchunks * a.ntiles;
+    if (blocks <= 0) return hipSuccess;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((ep_kernel<RED, MODE, V, NT, L>), dim3((unsigned)blocks), dim3(kBlock), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+template <int RED, int MODE, int V, int NT>
+hipError_t by_lanes(const EpArgs &a, int L, int64_t nchunks, hipStream_t st) {
+    if constexpr (NT > 1) {
+        if (L != 64) return hipErrorInvalidValue;
+        return launch_one<RED, MODE, V, NT, 64>(a, nchunks, st);
+    } else {
+        switch (L) {
+            case 1: return launch_one<RED, MODE, V, 1, 1>(a, nchunks, st);
+            case 2: return launch_one<RED, MODE, V, 1, 2>(a, nchunks, st);
+            case 4: return launch_one<RED, MODE, V, 1, 4>(a, nchunks, st);
+            case 8: return launch_one<RED, MODE, V, 1, 8>(a, nchunks, st);
+            case 16: return launch_one<RED, MODE, V, 1, 16>(a, nchunks, st);
+            case 32: return launch_one<RED, MODE, V, 1, 32>(a, nchunks, st);
+            case 64: return launch_one<RED, MODE, V, 1, 64>(a, nchunks, st);
+            default: return hipErrorInvalidValue;
+        }
+    }
+}
+
+template <int RED, int MODE>
+hipError_t by_shape(const EpArgs &a, int V, int NT, int L, int64_t nchunks, hipStream_t st) {
+    if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1>(a, L, nchunks, st);
+    if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1>(a, L, nchunks, st);
+    if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2>(a, L, nchunks, st);
+    if (V == 1 && NT == 1) return by_lanes<RED, MODE, 1, 1>(a, L, nchunks, st);
+    if (V == 1 && NT == 2) return by_lanes<RED, MODE, 1, 2>(a, L, nchunks, st);
+    if (V == 1 && NT == 4) return by_lanes<RED, MODE, 1, 4>(a, L, nchunks, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_ep(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
+                     hipStream_t stream) {
+    if (red == RED_SUM) {
+        if (mode == SRC_ROWS) return by_shape<RED_SUM, SRC_ROWS>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_GATHER) return by_shape<RED_SUM, SRC_GATHER>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_PIECES) return by_shape<RED_SUM, SRC_PIECES>(a, V, NT, L, nchunks, stream);
+    } else if (red == RED_MAX) {
+        if (mode == SRC_ROWS) return by_shape<RED_MAX, SRC_ROWS>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_GATHER) return by_shape<RED_MAX, SRC_GATHER>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_PIECES) return by_shape<RED_MAX, SRC_PIECES>(a, V, NT, L, nchunks, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace geot

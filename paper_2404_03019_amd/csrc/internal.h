@@ -1,0 +1,84 @@
+// Internal declarations shared by the kernel files and the host dispatch of
+// libgeot_hip. Not part of the public ABI (include/geot.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace geot {
+
+constexpr int kBlock = 256;  // threads per block for every reduction kernel (4 waves of 64)
+
+enum SrcMode : int {
+    SRC_ROWS = 0,    // term = src[row, :]
+    SRC_GATHER = 1,  // term = w[row] * X[col[row], :] (w == nullptr: X[col[row], :])
+    SRC_PIECES = 2,  // term = partial[row, :] carrying a row count (cnt[row] == 0: no term)
+};
+
+enum RedOp : int { RED_SUM = 0, RED_MAX = 1 };  // mean = sum, divided by the count on store
+
+// Arguments of one element-parallel pass (level 0 over the input rows, or a
+// later level over the partials of segments that crossed block boundaries).
+struct EpArgs {
+    const float *src;       // rows (SRC_ROWS / SRC_PIECES) or X (SRC_GATHER)
+    int64_t ld_src;         // row stride of src in floats
+    const int64_t *idx;     // sorted segment id of each row
+    const int64_t *cnt;     // SRC_PIECES: rows represented by each partial
+    const int64_t *col;     // SRC_GATHER: source row of each edge
+    const float *w;         // SRC_GATHER: edge weight or nullptr
+    int64_t num_x_rows;     // SRC_GATHER: rows of X
+    int64_t n;              // rows (edges, partials) of this pass
+    int64_t S;              // output rows
+    int64_t F;              // columns
+    float *out;             // [S x ld_out]
+    int64_t ld_out;
+    float *pv;              // partials of this pass: [2 * chunks x ld_p], nullptr when one chunk
+    int64_t *pseg;          // segment id of each partial
+    int64_t *pcnt;          // row count of each partial
+    int64_t ld_p;
+    int32_t K;              // rows per row group
+    int32_t ntiles;         // column tiles (blocks per chunk)
+    int32_t mean;           // divide by the count when a segment is stored
+    int32_t fill_gaps;      // write empty segments (level 0 only)
+};
+
+hipError_t launch_ep(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
+                     hipStream_t stream);
+
+// Segment-parallel pass: segment s covers rows off[s] .. off[s+1]-1.
+struct SpArgs {
+    const float *src;
+    int64_t ld_src;
+    const int64_t *off;     // [S + 1] segment starts
+    const int64_t *col;
+    const float *w;
+    int64_t num_x_rows;
+    int64_t S;
+    int64_t F;
+    float *out;
+    int64_t ld_out;
+    int32_t groups;         // row groups cooperating on one segment (power of two, <= 64 / L)
+    int32_t ntiles;
+    int32_t mean;
+};
+
+hipError_t launch_sp(const SpArgs &a, int red, int mode, int V, int NT, int L, hipStream_t stream);
+
+// off[s] = first row with idx >= s for s in [0, S]; one pass over the index.
+hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, hipStream_t stream);
+
+// out[0 .. rows*ld) = value for the first F columns of each row.
+hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float value, hipStream_t stream);
+
+// Index statistics from segment starts: acc[0] += sum len^2, acc[1] = max len,
+// acc[2] += empty count. acc must be zeroed first (launch_zero_i64).
+hipError_t launch_len_stats(const int64_t *off, int64_t S, unsigned long long *acc, hipStream_t stream);
+
+// Precondition check: flags |= 1 (out of range), 2 (not sorted).
+hipError_t launch_check(const int64_t *idx, int64_t n, int64_t S, const int64_t *col, int64_t nx,
+                        unsigned int *flags, hipStream_t stream);
+
+hipError_t launch_zero_u64(unsigned long long *p, int64_t n, hipStream_t stream);
+
+}  // namespace geot

@@ -1,0 +1,233 @@
+"""Python binding of libgeot_hip (argument marshalling only).
+
+Every call here forwards torch tensors' device pointers and the current HIP
+stream to the extern "C" functions declared in include/geot.h; all arithmetic
+runs in the library's HIP kernels. There is no fallback: if the library is
+not built, or a tensor is not on the GPU, the call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgeot_hip.so")
+
+OPS = {"sum": 0, "mean": 1, "max": 2}
+FAMILIES = {"auto": 0, "ep": 1, "sp": 2}
+STATUS = {0: "success", 1: "invalid value", 2: "index not sorted", 3: "index out of range",
+          4: "HIP runtime error", 5: "unsupported kernel choice"}
+
+
+class GeotError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class KernelChoice(ctypes.Structure):
+    _fields_ = [("family", ctypes.c_int32), ("vec", ctypes.c_int32), ("lanes", ctypes.c_int32),
+                ("rows", ctypes.c_int32), ("groups", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+    def as_dict(self) -> dict:
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+class IndexStats(ctypes.Structure):
+    _fields_ = [("nnz", ctypes.c_int64), ("num_segments", ctypes.c_int64),
+                ("max_len", ctypes.c_int64), ("num_empty", ctypes.c_int64),
+                ("sum_len_sq", ctypes.c_int64), ("mean_len", ctypes.c_double),
+                ("var_len", ctypes.c_double)]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise GeotError(4, f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    pc = ctypes.POINTER(KernelChoice)
+    L.geot_segment_reduce.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p]
+    L.geot_segment_reduce_with.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, pc]
+    L.geot_gather_scatter.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p]
+    L.geot_gather_scatter_with.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, pc]
+    L.geot_select.argtypes = [i64, i64, i64, ctypes.c_int, i32, ctypes.POINTER(IndexStats), pc]
+    L.geot_index_stats.argtypes = [p, i64, i64, ctypes.POINTER(IndexStats), p]
+    L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
+    L.geot_last_choice.argtypes = [pc]
+    L.geot_profile_begin.argtypes = [i32]
+    L.geot_profile_end.argtypes = [ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
+    L.geot_status_string.argtypes = [ctypes.c_int]
+    L.geot_status_string.restype = ctypes.c_char_p
+    L.geot_last_error_detail.argtypes = []
+    L.geot_last_error_detail.restype = ctypes.c_char_p
+    L.geot_version.restype = i32
+    for name in ("geot_segment_reduce", "geot_segment_reduce_with", "geot_gather_scatter",
+                 "geot_gather_scatter_with", "geot_select", "geot_index_stats", "geot_check_index",
+                 "geot_last_choice", "geot_profile_begin", "geot_profile_end"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _raise(status: int):
+    if status != 0:
+        detail = lib().geot_last_error_detail().decode()
+        raise GeotError(status, detail)
+
+
+def _choice(choice) -> KernelChoice | None:
+    if choice is None:
+        return None
+    if isinstance(choice, KernelChoice):
+        return choice
+    c = dict(choice)
+    fam = c.get("family", 0)
+    if isinstance(fam, str):
+        fam = FAMILIES[fam]
+    return KernelChoice(int(fam), int(c.get("vec", 0)), int(c.get("lanes", 0)),
+                        int(c.get("rows", 0)), int(c.get("groups", 0)), int(c.get("flags", 0)))
+
+
+def _dev(t: torch.Tensor, name: str, dtype, ndim):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str = "sum",
+                   out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+    """out[s] = reduce over rows i of src with index[i] == s (geot_segment_reduce)."""
+    _dev(src, "src", torch.float32, 2)
+    _dev(index, "index", torch.int64, 1)
+    if index.numel() != src.shape[0]:
+        raise ValueError("index must have one entry per row of src")
+    if index.device != src.device:
+        raise ValueError("src and index must be on the same device")
+    S, F = int(num_segments), src.shape[1]
+    if out is None:
+        out = torch.empty((S, F), dtype=torch.float32, device=src.device)
+    else:
+        _dev(out, "out", torch.float32, 2)
+        if tuple(out.shape) != (S, F):
+            raise ValueError("out must be [num_segments, F]")
+    c = _choice(choice)
+    with torch.cuda.device(src.device):
+        st = lib().geot_segment_reduce_with(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
+                                            OPS[reduce], out.data_ptr(), _stream(src.device),
+                                            ctypes.byref(c) if c is not None else None)
+    _raise(st)
+    return out
+
+
+def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
+                   row: torch.Tensor, num_rows: int, reduce: str = "sum",
+                   out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+    """out[r] = reduce over edges e with row[e] == r of weight[e] * x[col[e]] (geot_gather_scatter)."""
+    _dev(x, "x", torch.float32, 2)
+    _dev(col, "col", torch.int64, 1)
+    _dev(row, "row", torch.int64, 1)
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+        if weight.numel() != row.numel():
+            raise ValueError("weight must have one entry per edge")
+    if col.numel() != row.numel():
+        raise ValueError("col and row must have one entry per edge")
+    R, F = int(num_rows), x.shape[1]
+    if out is None:
+        out = torch.empty((R, F), dtype=torch.float32, device=x.device)
+    else:
+        _dev(out, "out", torch.float32, 2)
+        if tuple(out.shape) != (R, F):
+            raise ValueError("out must be [num_rows, F]")
+    c = _choice(choice)
+    wp = weight.data_ptr() if weight is not None else None
+    with torch.cuda.device(x.device):
+        st = lib().geot_gather_scatter_with(x.data_ptr(), x.shape[0], col.data_ptr(), wp,
+                                            row.data_ptr(), row.numel(), R, F, OPS[reduce],
+                                            out.data_ptr(), _stream(x.device),
+                                            ctypes.byref(c) if c is not None else None)
+    _raise(st)
+    return out
+
+
+def index_stats(index: torch.Tensor, num_segments: int) -> dict:
+    """Segment-length statistics of a sorted index (geot_index_stats; synchronizes)."""
+    _dev(index, "index", torch.int64, 1)
+    o = IndexStats()
+    with torch.cuda.device(index.device):
+        st = lib().geot_index_stats(index.data_ptr(), index.numel(), int(num_segments),
+                                    ctypes.byref(o), _stream(index.device))
+    _raise(st)
+    return o.as_dict()
+
+
+def check_index(index: torch.Tensor, num_segments: int, col: torch.Tensor | None = None,
+                num_x_rows: int = 0) -> int:
+    """Precondition check (geot_check_index; synchronizes). Returns the status code."""
+    _dev(index, "index", torch.int64, 1)
+    cp = None
+    if col is not None:
+        _dev(col, "col", torch.int64, 1)
+        cp = col.data_ptr()
+    with torch.cuda.device(index.device):
+        return int(lib().geot_check_index(index.data_ptr(), index.numel(), int(num_segments), cp,
+                                          int(num_x_rows), _stream(index.device)))
+
+
+def select(nnz: int, num_segments: int, F: int, reduce: str = "sum", gather: bool = False,
+           stats: dict | None = None) -> dict:
+    """The selector's kernel choice for a shape (geot_select; host only)."""
+    c = KernelChoice()
+    sp = None
+    if stats is not None:
+        s = IndexStats(**{k: stats[k] for k, _ in IndexStats._fields_})
+        sp = ctypes.byref(s)
+    _raise(lib().geot_select(int(nnz), int(num_segments), int(F), OPS[reduce], int(bool(gather)),
+                             sp, ctypes.byref(c)))
+    return c.as_dict()
+
+
+def last_choice() -> dict:
+    c = KernelChoice()
+    _raise(lib().geot_last_choice(ctypes.byref(c)))
+    return c.as_dict()
+
+
+def profile_begin(max_records: int):
+    _raise(lib().geot_profile_begin(int(max_records)))
+
+
+def profile_end(capacity: int = 4096) -> list:
+    buf = (ctypes.c_float * capacity)()
+    n = ctypes.c_int32()
+    _raise(lib().geot_profile_end(buf, capacity, ctypes.byref(n)))
+    return [float(buf[i]) for i in range(min(n.value, capacity))]
+
+
+def version() -> int:
+    return int(lib().geot_version())

@@ -1,0 +1,130 @@
+"""The C-ABI library: loads, exports every declared symbol, and its host-side logic
+(argument checks, forced-choice validation, selector) runs without a GPU.
+
+Every call here returns before any device work: invalid arguments and
+impossible kernel choices are rejected on the host, and geot_select touches
+no device memory. Fake (never dereferenced) pointer values stand in for
+device buffers.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2404_03019_amd as geot
+from paper_2404_03019_amd.geot import KernelChoice, lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "geot.h")
+
+SUCCESS, INVALID, NOT_SORTED, OUT_OF_RANGE, HIP, UNSUPPORTED = range(6)
+FAKE = 0x10000000  # 256-byte aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(geot_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("geot_segment_reduce", "geot_gather_scatter", "geot_select", "geot_index_stats",
+              "geot_check_index", "geot_segment_reduce_with", "geot_gather_scatter_with"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = lib()
+    missing = [n for n in declared_functions() if not hasattr(L, n)]
+    assert not missing, missing
+
+
+def test_version_and_status_strings():
+    L = lib()
+    assert geot.version() == 1
+    assert L.geot_status_string(0) == b"success"
+    assert L.geot_status_string(2) == b"index not sorted"
+    assert L.geot_status_string(99) == b"unknown status"
+
+
+def _sr(src, idx, nnz, S, F, op, out, choice=None):
+    L = lib()
+    return L.geot_segment_reduce_with(src, idx, nnz, S, F, op, out, None,
+                                      ctypes.byref(choice) if choice is not None else None)
+
+
+def _gs(X, nx, col, w, row, nnz, R, F, op, out, choice=None):
+    L = lib()
+    return L.geot_gather_scatter_with(X, nx, col, w, row, nnz, R, F, op, out, None,
+                                      ctypes.byref(choice) if choice is not None else None)
+
+
+def _detail():
+    return lib().geot_last_error_detail().decode()
+
+
+def test_invalid_arguments_are_rejected_on_the_host():
+    out = FAKE + (1 << 30)
+    assert _sr(FAKE, FAKE + (1 << 28), 10, 4, 3, 7, out) == INVALID and "op" in _detail()
+    assert _sr(FAKE, FAKE + (1 << 28), -1, 4, 3, 0, out) == INVALID
+    assert _sr(FAKE, FAKE + (1 << 28), 10, -4, 3, 0, out) == INVALID
+    assert _sr(FAKE, FAKE + (1 << 28), 10, 4, -3, 0, out) == INVALID
+    assert _sr(None, FAKE, 10, 4, 3, 0, out) == INVALID and "src" in _detail()
+    assert _sr(FAKE, None, 10, 4, 3, 0, out) == INVALID and "index" in _detail()
+    assert _sr(FAKE, FAKE + (1 << 28), 10, 4, 3, 0, None) == INVALID and "out" in _detail()
+    # out overlapping src, or the index
+    assert _sr(FAKE, FAKE + (1 << 28), 100, 4, 8, 0, FAKE + 64) == INVALID and "overlap" in _detail()
+    assert _sr(FAKE, FAKE + (1 << 28), 100, 4, 8, 0, FAKE + (1 << 28) + 8) == INVALID
+    # size overflow
+    assert _sr(FAKE, FAKE, 1 << 61, 4, 8, 0, out) == INVALID
+
+
+def test_noops_return_success_without_device_work():
+    assert _sr(None, None, 0, 0, 5, 0, None) == SUCCESS
+    assert _sr(None, None, 10, 5, 0, 0, None) == SUCCESS
+    assert _gs(None, 0, None, None, None, 10, 0, 4, 0, None) == SUCCESS
+
+
+def test_gather_arguments_are_checked():
+    out = FAKE + (1 << 30)
+    assert _gs(FAKE, 10, None, None, FAKE + (1 << 26), 5, 3, 4, 0, out) == INVALID and "col" in _detail()
+    assert _gs(None, 10, FAKE, None, FAKE + (1 << 26), 5, 3, 4, 0, out) == INVALID and "X" in _detail()
+    assert _gs(FAKE, 0, FAKE + (1 << 27), None, FAKE + (1 << 26), 5, 3, 4, 0, out) == INVALID
+    assert _gs(FAKE, -1, FAKE, None, FAKE, 5, 3, 4, 0, out) == INVALID
+
+
+@pytest.mark.parametrize("choice", [
+    dict(family=7), dict(vec=3), dict(lanes=3), dict(lanes=128), dict(rows=-1), dict(rows=5000),
+    dict(family=2, lanes=16, groups=8), dict(family=2, groups=3), dict(flags=1),
+])
+def test_impossible_forced_choices_are_unsupported(choice):
+    c = geot.geot._choice(choice)
+    out = FAKE + (1 << 30)
+    assert _sr(FAKE, FAKE + (1 << 28), 1000, 10, 32, 0, out, c) == UNSUPPORTED
+
+
+def test_selector_is_a_host_function():
+    c = geot.select(114_615_892, 232_965, 32, "sum")
+    assert c["family"] == 1 and c["vec"] == 4 and c["lanes"] == 8 and c["rows"] >= 1
+    c = geot.select(61_859_140, 2_449_029, 128, "sum", gather=True)
+    assert c["vec"] == 4 and c["lanes"] == 32
+    for F in (1, 2, 3, 4, 5, 8, 15, 16, 17, 33, 64, 100, 128, 255, 256, 257, 1000):
+        c = geot.select(2_000_000, 100_000, F, "max")
+        assert c["family"] in (1, 2) and c["vec"] in (1, 2, 4) and F % c["vec"] == 0
+        assert c["lanes"] in (1, 2, 4, 8, 16, 32, 64)
+        if F <= 256:  # one column tile covers the row
+            nt = 1 if c["lanes"] < 64 else max(1, -(-F // (64 * c["vec"])))
+            assert c["lanes"] * c["vec"] * nt >= F
+    assert lib().geot_select(10, 10, 4, 9, 0, None, ctypes.byref(KernelChoice())) == INVALID
+    assert lib().geot_select(-1, 10, 4, 0, 0, None, ctypes.byref(KernelChoice())) == INVALID
+
+
+def test_selector_uses_stats_when_given():
+    even = dict(nnz=16 * 1000, num_segments=1000, max_len=16, num_empty=0, sum_len_sq=256 * 1000,
+                mean_len=16.0, var_len=0.0)
+    skew = dict(nnz=16 * 1000, num_segments=1000, max_len=9000, num_empty=900,
+                sum_len_sq=9000 ** 2, mean_len=16.0, var_len=8.0e4)
+    assert geot.select(16000, 1000, 64, "mean", stats=skew)["family"] == 1
+    assert geot.select(16000, 1000, 64, "mean", stats=even)["family"] in (1, 2)

@@ -1,0 +1,249 @@
+"""GPU parity: libgeot_hip (through its C-ABI) against the CPU oracle, element by element.
+
+Covers every kernel family and tiling choice on exhaustive tiny inputs, random
+inputs with several length distributions and feature widths (odd F, F that is
+not a multiple of the vector width, F above one column tile), multi-level
+partial combining (forced small row runs), the fused gather form, exact
+arithmetic (bit-exact sums), determinism, edge cases, index statistics and the
+precondition check.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2404_03019_amd as geot
+from gpu_util import compare, oracle_gather, oracle_segment, say
+from workloads import random_gather_problem, random_problem
+
+pytestmark = pytest.mark.gpu
+OPS = ("sum", "mean", "max")
+DEV = "cuda:0"
+
+
+def up(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def run_sr(src, idx, S, op, choice=None):
+    out = geot.segment_reduce(up(src), up(idx), S, op, choice=choice)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def run_gs(X, col, w, row, R, op, choice=None):
+    out = geot.gather_scatter(up(X), up(col), up(w), up(row), R, op, choice=choice)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+TINY_CHOICES = [
+    None,
+    dict(family="ep", rows=1),
+    dict(family="ep", lanes=64, rows=1),           # 4 rows per block: partials cross blocks
+    dict(family="ep", lanes=64, vec=1, rows=2),
+    dict(family="ep", lanes=1, rows=3),
+    dict(family="sp", groups=1),
+    dict(family="sp", lanes=4, groups=16),
+]
+
+
+@pytest.mark.parametrize("F", [1, 3, 4, 8])
+def test_tiny_exhaustive_bit_exact(F):
+    """Every non-decreasing index with nnz <= 5 over S <= 4 segments, integer values:
+    every partial sum is exact, so sum and max must be bit-exact for every kernel choice."""
+    rng = np.random.default_rng(100 + F)
+    for S in range(1, 5):
+        for nnz in range(1, 6):
+            for idx_t in itertools.combinations_with_replacement(range(S), nnz):
+                idx = np.array(idx_t, dtype=np.int64)
+                src = rng.integers(-8, 9, size=(nnz, F)).astype(np.float32)
+                refs = {op: oracle_segment(src, idx, S, op) for op in OPS}
+                for ci, ch in enumerate(TINY_CHOICES):
+                    for op in OPS:
+                        got = run_sr(src, idx, S, op, ch)
+                        ref, terms = refs[op]
+                        if op == "mean":
+                            compare(got, ref, op, terms, f"tiny F={F} idx={idx_t} choice={ch}")
+                        else:
+                            assert np.array_equal(got, ref), \
+                                f"tiny {op} F={F} idx={idx_t} choice={ch}: {got} vs {ref}"
+
+
+RANDOM_CASES = [
+    # seed, nnz, S, F, dist, values, empty_frac
+    (1, 30000, 2000, 32, "zipf", "uniform", 0.05),
+    (2, 25000, 400, 1, "lognormal", "normal", 0.1),
+    (3, 20000, 3000, 3, "uniform", "normal", 0.2),
+    (4, 40000, 50, 64, "one_heavy", "normal", 0.3),
+    (5, 15000, 1500, 15, "poisson", "uniform", 0.0),
+    (6, 12000, 700, 17, "zipf", "normal", 0.1),
+    (7, 10000, 600, 128, "lognormal", "uniform", 0.05),
+    (8, 6000, 300, 255, "uniform", "normal", 0.1),
+    (9, 5000, 200, 256, "zipf", "normal", 0.0),
+    (10, 4000, 300, 300, "uniform", "normal", 0.1),
+    (11, 20000, 20000, 8, "uniform", "normal", 0.6),
+    (12, 30000, 1, 16, "fixed", "normal", 0.0),
+    (13, 9000, 9000, 2, "fixed", "negative", 0.0),
+]
+
+RANDOM_CHOICES = [
+    None,
+    dict(family="ep", rows=1),
+    dict(family="ep", lanes=64, rows=1),
+    dict(family="ep", lanes=2, vec=1, rows=7),
+    dict(family="ep", rows=33),
+    dict(family="sp"),
+    dict(family="sp", lanes=16, groups=2),
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=lambda c: f"seed{c[0]}-F{c[3]}-{c[4]}")
+def test_random_parity_all_choices(case):
+    seed, nnz, S, F, dist, values, ef = case
+    p = random_problem(seed, nnz, S, F, dist, values, ef)
+    src, idx = p["src"], p["index"]
+    for op in OPS:
+        ref, terms = oracle_segment(src, idx, S, op)
+        for ch in RANDOM_CHOICES:
+            say(f"segment_reduce seed={seed} F={F} op={op} choice={ch}")
+            got = run_sr(src, idx, S, op, ch)
+            compare(got, ref, op, terms, f"seed={seed} F={F} op={op} choice={ch}")
+
+
+GATHER_CASES = [
+    # seed, nnz, R, n_x, F, dist, values, weighted, empty_frac
+    (21, 30000, 2000, 1500, 32, "zipf", "normal", True, 0.05),
+    (22, 20000, 500, 3000, 1, "lognormal", "normal", True, 0.1),
+    (23, 15000, 1000, 800, 3, "uniform", "uniform", False, 0.1),
+    (24, 10000, 300, 5000, 128, "one_heavy", "normal", True, 0.2),
+    (25, 8000, 900, 900, 17, "poisson", "normal", False, 0.0),
+    (26, 6000, 400, 700, 256, "zipf", "normal", True, 0.0),
+]
+
+
+@pytest.mark.parametrize("case", GATHER_CASES, ids=lambda c: f"seed{c[0]}-F{c[4]}-w{int(c[7])}")
+def test_gather_parity_all_choices(case):
+    seed, nnz, R, nx, F, dist, values, weighted, ef = case
+    p = random_gather_problem(seed, nnz, R, nx, F, dist, values, weighted, ef)
+    X, col, w, row = p["X"], p["col"], p["weight"], p["index"]
+    for op in OPS:
+        ref, terms = oracle_gather(X, col, w, row, R, op)
+        for ch in RANDOM_CHOICES:
+            say(f"gather_scatter seed={seed} F={F} op={op} choice={ch}")
+            got = run_gs(X, col, w, row, R, op, ch)
+            compare(got, ref, op, terms, f"gather seed={seed} F={F} op={op} choice={ch}")
+
+
+def test_fusion_identity_on_gpu():
+    """gather_scatter(X, col, w, row) equals segment_reduce(w * X[col], row) (Section IV):
+    bit-exact for max, within the bound for sum and mean."""
+    p = random_gather_problem(31, 50000, 3000, 4000, 24, "lognormal", "normal", True, 0.05)
+    X, col, w, row, R = p["X"], p["col"], p["weight"], p["index"], p["num_segments"]
+    msgs = (w[:, None] * X[col]).astype(np.float32)
+    for op in OPS:
+        a = run_gs(X, col, w, row, R, op)
+        b = run_sr(msgs, row, R, op)
+        _, terms = oracle_segment(msgs, row, R, op)
+        compare(a, b, op, None if op == "max" else 2 * terms, f"fusion identity {op}")
+
+
+def test_exact_arithmetic_at_scale_is_bit_exact():
+    """Values in {-1, 0, 1}: every partial sum is an integer below 2^24, so sums are
+    exact in any order and the GPU must match the oracle bit for bit, long segments included."""
+    p = random_problem(41, 3_000_000, 5000, 16, "one_heavy", "ternary", 0.1)
+    src, idx, S = p["src"], p["index"], p["num_segments"]
+    ref = oracle.segment_reduce(src, idx, S, "sum")
+    for ch in (None, dict(family="ep", rows=1), dict(family="ep", lanes=64, rows=4), dict(family="sp")):
+        say(f"exact arithmetic choice={ch}")
+        got = run_sr(src, idx, S, "sum", ch)
+        assert np.array_equal(got, ref), f"exact sum choice={ch}"
+
+
+def test_results_are_deterministic():
+    """No atomics on the reduction path: repeated calls give identical bits for every op."""
+    p = random_problem(42, 400000, 3000, 32, "lognormal", "normal", 0.05)
+    s, i = up(p["src"]), up(p["index"])
+    for op in OPS:
+        outs = [geot.segment_reduce(s, i, 3000, op).cpu().numpy() for _ in range(3)]
+        assert all(np.array_equal(outs[0], o) for o in outs[1:]), op
+
+
+def test_empty_and_degenerate_inputs():
+    F = 5
+    # nnz == 0: every segment is empty
+    out = geot.segment_reduce(torch.empty((0, F), device=DEV), torch.empty(0, dtype=torch.int64, device=DEV),
+                              7, "max")
+    assert torch.all(out == 0)
+    # S == 0: no-op returning an empty tensor
+    out = geot.segment_reduce(torch.ones((3, F), device=DEV), torch.zeros(3, dtype=torch.int64, device=DEV),
+                              0, "sum")
+    assert out.shape == (0, F)
+    # nnz == 1 with leading and trailing empties; a non-empty all-negative max is not clipped at 0
+    src = np.full((1, F), -3.5, dtype=np.float32)
+    for op in OPS:
+        got = run_sr(src, np.array([2], dtype=np.int64), 5, op)
+        want = np.zeros((5, F), dtype=np.float32)
+        want[2] = -3.5
+        assert np.array_equal(got, want), op
+    # every row in the last segment of many
+    src = np.arange(4000 * 3, dtype=np.float32).reshape(4000, 3) / 7
+    idx = np.full(4000, 999, dtype=np.int64)
+    for op in OPS:
+        ref, terms = oracle_segment(src, idx, 1000, op)
+        compare(run_sr(src, idx, 1000, op), ref, op, terms, f"all-in-last {op}")
+
+
+def test_misaligned_views_use_narrower_vectors():
+    """Views with a storage offset break 16-byte alignment; results must not change."""
+    p = random_problem(43, 20000, 500, 8, "zipf", "normal", 0.1)
+    big = torch.zeros(20000 * 8 + 1, device=DEV)
+    big[1:] = up(p["src"]).reshape(-1)
+    view = big[1:].view(20000, 8)
+    idx = up(p["index"])
+    for op in OPS:
+        got = geot.segment_reduce(view, idx, 500, op).cpu().numpy()
+        assert geot.last_choice()["vec"] == 1
+        ref, terms = oracle_segment(p["src"], p["index"], 500, op)
+        compare(got, ref, op, terms, f"misaligned {op}")
+
+
+def test_out_is_overwritten_not_accumulated():
+    p = random_problem(44, 5000, 300, 4, "uniform", "normal", 0.2)
+    out = torch.full((300, 4), 123.0, device=DEV)
+    geot.segment_reduce(up(p["src"]), up(p["index"]), 300, "sum", out=out)
+    ref, terms = oracle_segment(p["src"], p["index"], 300, "sum")
+    compare(out.cpu().numpy(), ref, "sum", terms, "overwrite")
+
+
+def test_index_stats_match_oracle():
+    for seed, dist, ef in ((51, "zipf", 0.1), (52, "fixed", 0.0), (53, "one_heavy", 0.5)):
+        p = random_problem(seed, 200000, 7000, 1, dist, "uniform", ef)
+        got = geot.index_stats(up(p["index"]), 7000)
+        want = oracle.index_stats(p["index"], 7000)
+        for k in ("max_len", "num_empty", "sum_len_sq"):
+            assert got[k] == want[k], k
+        assert got["nnz"] == 200000 and got["num_segments"] == 7000
+        assert abs(got["mean_len"] - want["mean_len"]) <= 1e-12 * want["mean_len"]
+        assert abs(got["var_len"] - want["var_len"]) <= 1e-9 * max(1.0, want["var_len"])
+
+
+def test_check_index_reports_violations():
+    idx = up(np.array([0, 0, 1, 3, 3], dtype=np.int64))
+    assert geot.check_index(idx, 4) == 0
+    assert geot.check_index(idx, 3) == 3
+    assert geot.check_index(up(np.array([0, 2, 1, 3], dtype=np.int64)), 4) == 2
+    assert geot.check_index(idx, 4, col=up(np.array([0, 1, 2, 3, 9], dtype=np.int64)), num_x_rows=5) == 3
+    assert geot.check_index(idx, 4, col=up(np.array([0, 1, 2, 3, 4], dtype=np.int64)), num_x_rows=5) == 0
+
+
+def test_profile_hooks_record_main_kernel_time():
+    p = random_problem(54, 200000, 5000, 32, "lognormal", "normal", 0.0)
+    s, i = up(p["src"]), up(p["index"])
+    geot.profile_begin(8)
+    for _ in range(3):
+        geot.segment_reduce(s, i, 5000, "sum")
+    ms = geot.profile_end()
+    assert len(ms) == 3 and all(0.0 < t < 1000.0 for t in ms)
