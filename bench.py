@@ -1,0 +1,259 @@
+"""Throughput of the segment-reduction hot path on one MI355X.
+
+One step = one geot_segment_reduce (sum) over the power-law graph workload
+(src [114,615,892 x 32] fp32, 232,965 segments with lognormal(5.5, 1.2)
+lengths) plus one geot_gather_scatter (sum) over the SpMM workload (X
+[2,449,029 x 128] fp32, 61,859,140 edges with Zipf(2.0) row lengths, uniform
+columns, U(0,1) weights). Inputs are synthetic (seeded generators in
+``workloads``) and resident in HBM before timing starts.
+
+The metric is effective HBM bandwidth: algorithmic bytes per step divided by
+the time per step, where algorithmic bytes are
+  segment_reduce: nnz*F*4 (src) + nnz*8 (index) + S*F*4 (out)
+  gather_scatter: nnz*(8 col + 4 weight + 8 row) + nnz*F*4 (gathered X rows) + R*F*4 (out)
+
+Prints ONE JSON line. ``roofline`` describes the dominant kernel (the main
+kernel of the call that takes longest), timed per launch with HIP events on
+the stream it runs on; ``traffic`` comes from committed rocprofv3 counter
+readings (profiles/traffic.json) and is null when the kernel source changed
+since. ``cpu_baseline`` times the CPU oracle on a bounded sample of the same
+inputs on the host (one thread).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "segment_reduce / gather_scatter effective HBM GB/s and % of MI355X HBM peak"
+KERNEL_SOURCES = ("paper_2404_03019_amd/csrc/ep_kernel.hip", "paper_2404_03019_amd/csrc/common.h",
+                  "paper_2404_03019_amd/csrc/internal.h")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def seg_bytes(nnz, S, F):
+    return nnz * F * 4 + nnz * 8 + S * F * 4
+
+
+def gather_bytes(nnz, R, F):
+    return nnz * (8 + 4 + 8) + nnz * F * 4 + R * F * 4
+
+
+def load_traffic(kernel_key: str):
+    """Counter-derived HBM bytes per launch for kernel_key, if taken on the current source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    e = d.get(kernel_key)
+    if not e or e.get("source_hash") != kernel_source_hash():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(c3, c4, frac3: float, frac4: float):
+    """The oracle (serial C, fp64 accumulation) on the first segments of each workload."""
+    import numpy as np
+
+    import oracle
+
+    L3 = c3["lengths"]
+    s3 = max(1, int(L3.size * frac3))
+    n3 = int(L3[:s3].sum())
+    L4 = c4["lengths"]
+    s4 = max(1, int(L4.size * frac4))
+    n4 = int(L4[:s4].sum())
+    src = np.ascontiguousarray(c3["src"][:n3])
+    idx3 = np.ascontiguousarray(c3["index"][:n3])
+    col = np.ascontiguousarray(c4["col"][:n4])
+    w = np.ascontiguousarray(c4["weight"][:n4])
+    row = np.ascontiguousarray(c4["index"][:n4])
+    oracle.default()
+    t0 = time.perf_counter()
+    oracle.segment_reduce(src, idx3, s3, "sum")
+    t1 = time.perf_counter()
+    oracle.gather_scatter(c4["X"], col, w, row, s4, "sum")
+    t2 = time.perf_counter()
+    b = seg_bytes(n3, s3, 32) + gather_bytes(n4, s4, 128)
+    return {
+        "value": round(b / (t2 - t0) / 1e9, 3),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"first {s3} of 232,965 segments of the power-law graph ({n3} rows, "
+                   f"{t1 - t0:.1f} s) + first {s4} of 2,449,029 rows of the SpMM workload "
+                   f"({n4} edges, {t2 - t1:.1f} s), same algorithmic-byte formulas"),
+    }
+
+
+def copy_probe(n: int):
+    """A plain copy of known size: 2 GiB read and 2 GiB written per launch."""
+    import torch
+
+    a = torch.ones(1 << 29, device="cuda:0")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / n
+    print(json.dumps({"copy_bytes_read": 1 << 31, "copy_bytes_written": 1 << 31,
+                      "ms_per_copy": round(dt * 1e3, 4),
+                      "GB/s": round(2 * (1 << 31) / dt / 1e9, 1)}), flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-frac", type=float, default=0.04,
+                    help="fraction of segments / rows of each workload the oracle reduces")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="N",
+                    help="only run N plain device copies of 2 GiB (calibrates HBM byte counters)")
+    args = ap.parse_args()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the path does not shard across GPUs); "
+              f"got --gpus {args.gpus}", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        sys.exit("steps must be >= 1 and warmup >= 0")
+
+    import numpy as np
+    import torch
+
+    import paper_2404_03019_amd as geot
+    from workloads import make_config
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    geot.lib()  # fail loudly if the library is missing
+
+    log("generating power-law graph workload")
+    c3 = make_config("c3_powerlaw_graph")
+    log("generating SpMM workload")
+    c4 = make_config("c4_spmm")
+    S3, F3, n3 = c3["num_segments"], 32, c3["index"].size
+    R4, F4, n4 = c4["num_segments"], 128, c4["index"].size
+    log("uploading")
+    src = torch.from_numpy(c3["src"]).to(dev)
+    idx = torch.from_numpy(c3["index"]).to(dev)
+    X = torch.from_numpy(c4["X"]).to(dev)
+    col = torch.from_numpy(c4["col"]).to(dev)
+    w = torch.from_numpy(c4["weight"]).to(dev)
+    row = torch.from_numpy(c4["index"]).to(dev)
+    out3 = torch.empty((S3, F3), device=dev)
+    out4 = torch.empty((R4, F4), device=dev)
+    torch.cuda.synchronize()
+
+    b3 = seg_bytes(n3, S3, F3)
+    b4 = gather_bytes(n4, R4, F4)
+
+    def step():
+        geot.segment_reduce(src, idx, S3, "sum", out=out3)
+        geot.gather_scatter(X, col, w, row, R4, "sum", out=out4)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    choice3 = geot.select(n3, S3, F3, "sum")
+    choice4 = geot.select(n4, R4, F4, "sum", gather=True)
+
+    # timed region: exactly `steps` steps, main-kernel durations recorded by HIP events
+    geot.profile_begin(2 * args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    durs = geot.profile_end(2 * args.steps)
+    elapsed_ms = (t1 - t0) * 1e3
+    ms_per_step = elapsed_ms / args.steps
+    value = (b3 + b4) / (ms_per_step * 1e-3) / 1e9
+
+    k3 = durs[0::2]
+    k4 = durs[1::2]
+    avg3 = float(np.mean(k3))
+    avg4 = float(np.mean(k4))
+    if avg4 >= avg3:
+        dom_key, dom_bytes, dom_ms, dom_name = "ep_kernel/gather/c4_spmm", b4, avg4, "gather_scatter main kernel"
+    else:
+        dom_key, dom_bytes, dom_ms, dom_name = "ep_kernel/rows/c3_powerlaw_graph", b3, avg3, "segment_reduce main kernel"
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = load_traffic(dom_key)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded generators; the paper's datasets are not used)",
+        "config": {
+            "workload": ("power-law graph segment_reduce sum [114,615,892 x 32], 232,965 segments "
+                         "+ SpMM gather_scatter sum X [2,449,029 x 128], 61,859,140 edges"),
+            "bytes_per_step": b3 + b4,
+            "parts": [
+                {"op": "segment_reduce sum", "bytes": b3, "main_kernel_ms": round(avg3, 4),
+                 "GB/s": round(b3 / (avg3 * 1e-3) / 1e9, 1), "choice": choice3},
+                {"op": "gather_scatter sum", "bytes": b4, "main_kernel_ms": round(avg4, 4),
+                 "GB/s": round(b4 / (avg4 * 1e-3) / 1e9, 1), "choice": choice4},
+            ],
+            "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 1),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dom_name,
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": dom_bytes,
+            "avg_launch_ms": round(dom_ms, 4),
+        },
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        del src, idx, X, col, w, row
+        torch.cuda.empty_cache()
+        log("timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(c3, c4, args.cpu_frac, args.cpu_frac)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -4,9 +4,13 @@ The five named workloads stand in for the graph, mesh and point-cloud inputs of
 the paper's evaluation (Table II graphs and GNN aggregation, Sections II-A/B and
 V); the real datasets are not used. Every recipe is deterministic:
 
-* ``numpy.random.default_rng(seed)`` (PCG64), drawn in the order written below;
-* arrays longer than ``CHUNK`` rows are drawn in consecutive ``CHUNK``-row
-  pieces (the chunking is part of the recipe, because it fixes the draw order);
+* segment lengths come from ``numpy.random.default_rng(seed)`` (PCG64), drawn
+  in the order written below;
+* large value arrays (src, X, col, weight) are drawn in ``CHUNK``-row pieces,
+  piece ``k`` of array stream ``a`` from its own generator
+  ``numpy.random.default_rng([seed, a, k])``; the pieces are independent, so
+  they are filled by a thread pool and the result does not depend on the
+  number of threads;
 * fp32 values are drawn directly in fp32;
 * segment lengths that must add up to a fixed total are rescaled with the
   largest-remainder rule ``lr_rescale``;
@@ -15,6 +19,9 @@ V); the real datasets are not used. Every recipe is deterministic:
 Nothing here computes a reduction: these are inputs only.
 """
 from __future__ import annotations
+
+import concurrent.futures as cf
+import os
 
 import numpy as np
 
@@ -80,35 +87,45 @@ def lengths_from_index(index, num_segments: int) -> np.ndarray:
     return np.bincount(np.asarray(index, dtype=np.int64), minlength=num_segments).astype(np.int64)
 
 
-def _chunked_2d(rng, rows: int, cols: int, draw) -> np.ndarray:
-    out = np.empty((rows, cols), dtype=np.float32)
-    for r0 in range(0, rows, CHUNK):
-        r1 = min(rows, r0 + CHUNK)
-        out[r0:r1] = draw(rng, (r1 - r0, cols))
+_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def _fill_chunks(out: np.ndarray, seed: int, stream: int, draw) -> np.ndarray:
+    """Fill out[k*CHUNK:(k+1)*CHUNK] with draw(default_rng([seed, stream, k]), view) for every k."""
+    n = out.shape[0]
+    starts = list(range(0, n, CHUNK))
+
+    def one(k):
+        r0 = starts[k]
+        draw(np.random.default_rng([seed, stream, k]), out[r0:min(n, r0 + CHUNK)])
+
+    if len(starts) <= 1:
+        for k in range(len(starts)):
+            one(k)
+    else:
+        with cf.ThreadPoolExecutor(max_workers=_THREADS) as ex:
+            list(ex.map(one, range(len(starts))))
     return out
 
 
-def values_uniform(rng, rows: int, cols: int) -> np.ndarray:
-    """U(-1, 1) fp32 as 2*u - 1 with u = rng.random(dtype=float32) (exact in fp32)."""
-    def draw(g, shape):
-        u = g.random(shape, dtype=np.float32)
-        u *= np.float32(2.0)
-        u -= np.float32(1.0)
-        return u
-    return _chunked_2d(rng, rows, cols, draw)
+def _draw_uniform(g, view):
+    g.random(out=view, dtype=np.float32)
+    view *= np.float32(2.0)
+    view -= np.float32(1.0)
 
 
-def values_normal(rng, rows: int, cols: int) -> np.ndarray:
-    """N(0, 1) fp32 drawn with rng.standard_normal(dtype=float32)."""
-    return _chunked_2d(rng, rows, cols, lambda g, shape: g.standard_normal(shape, dtype=np.float32))
+def _draw_normal(g, view):
+    g.standard_normal(out=view, dtype=np.float32)
 
 
-def _chunked_1d(rng, n: int, draw, dtype) -> np.ndarray:
-    out = np.empty(n, dtype=dtype)
-    for i0 in range(0, n, CHUNK):
-        i1 = min(n, i0 + CHUNK)
-        out[i0:i1] = draw(rng, i1 - i0)
-    return out
+def values_uniform(seed: int, stream: int, rows: int, cols: int) -> np.ndarray:
+    """U(-1, 1) fp32 as 2*u - 1 with u = random(dtype=float32) (exact in fp32)."""
+    return _fill_chunks(np.empty((rows, cols), dtype=np.float32), seed, stream, _draw_uniform)
+
+
+def values_normal(seed: int, stream: int, rows: int, cols: int) -> np.ndarray:
+    """N(0, 1) fp32 drawn with standard_normal(dtype=float32)."""
+    return _fill_chunks(np.empty((rows, cols), dtype=np.float32), seed, stream, _draw_normal)
 
 
 # ----------------------------------------------------------------------------
@@ -154,16 +171,17 @@ def make_config(name: str, F: int | None = None) -> dict:
     Returns a dict with ``kind`` ("segment_reduce" or "gather_scatter"), the
     arrays, ``num_segments`` (output rows), ``F`` and ``ops``.
     """
-    rng, lengths = config_lengths(name)
+    _, lengths = config_lengths(name)
     S = int(lengths.size)
     nnz = int(lengths.sum())
     index = index_from_lengths(lengths)
+    seed = CONFIGS[name][0]
     if name in ("c1_zipf_small", "c1_literal"):
-        src = values_uniform(rng, nnz, 32)
+        src = values_uniform(seed, 1, nnz, 32)
         return dict(kind="segment_reduce", src=src, index=index, num_segments=S, F=32,
                     lengths=lengths, ops=("sum",))
     if name == "c2_poisson_fsweep":
-        full = values_normal(rng, nnz, 256)
+        full = values_normal(seed, 1, nnz, 256)
         F = 256 if F is None else int(F)
         if not 1 <= F <= 256:
             raise ValueError("F must be in 1..256 for the F sweep")
@@ -171,18 +189,20 @@ def make_config(name: str, F: int | None = None) -> dict:
         return dict(kind="segment_reduce", src=src, index=index, num_segments=S, F=F,
                     lengths=lengths, ops=("sum", "mean", "max"))
     if name == "c3_powerlaw_graph":
-        src = values_uniform(rng, nnz, 32)
+        src = values_uniform(seed, 1, nnz, 32)
         return dict(kind="segment_reduce", src=src, index=index, num_segments=S, F=32,
                     lengths=lengths, ops=("sum",))
     if name == "c4_spmm":
         n_nodes = S
-        col = _chunked_1d(rng, nnz, lambda g, n: g.integers(0, n_nodes, n, dtype=np.int64), np.int64)
-        w = _chunked_1d(rng, nnz, lambda g, n: g.random(n, dtype=np.float32), np.float32)
-        X = values_normal(rng, n_nodes, 128)
+        col = _fill_chunks(np.empty(nnz, dtype=np.int64), seed, 2,
+                           lambda g, v: v.__setitem__(slice(None), g.integers(0, n_nodes, v.size, dtype=np.int64)))
+        w = _fill_chunks(np.empty(nnz, dtype=np.float32), seed, 3,
+                         lambda g, v: g.random(out=v, dtype=np.float32))
+        X = values_normal(seed, 1, n_nodes, 128)
         return dict(kind="gather_scatter", X=X, col=col, weight=w, index=index, num_segments=S,
                     F=128, lengths=lengths, ops=("sum",))
     if name == "c5_pointcloud_knn":
-        src = values_normal(rng, nnz, 64)
+        src = values_normal(seed, 1, nnz, 64)
         return dict(kind="segment_reduce", src=src, index=index, num_segments=S, F=64,
                     lengths=lengths, ops=("mean", "max"))
     raise KeyError(name)
@@ -220,9 +240,12 @@ def _random_lengths(rng, S: int, nnz: int, dist: str, empty_frac: float) -> np.n
 
 def _random_values(rng, rows: int, cols: int, values: str) -> np.ndarray:
     if values == "uniform":
-        return values_uniform(rng, rows, cols)
+        u = rng.random((rows, cols), dtype=np.float32)
+        u *= np.float32(2.0)
+        u -= np.float32(1.0)
+        return u
     if values == "normal":
-        return values_normal(rng, rows, cols)
+        return rng.standard_normal((rows, cols), dtype=np.float32)
     if values == "int":      # integers in [-8, 8]: every partial sum is exact in fp32
         return rng.integers(-8, 9, size=(rows, cols)).astype(np.float32)
     if values == "ternary":  # {-1, 0, 1}
