@@ -270,6 +270,7 @@ geot_status_t check_args(const Problem &p) {
     if (p.nnz < 0 || p.S < 0 || p.F < 0 || (p.gather && p.num_x_rows < 0))
         return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
     if (p.S == 0 || p.F == 0) return GEOT_SUCCESS;
+    if (p.S > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments must be < 2^31");
     const int64_t kMax = (int64_t)1 << 62;
     if (p.F > ((int64_t)1 << 31) || p.S > kMax / p.F || p.nnz > kMax / p.F ||
         (p.gather && p.num_x_rows > kMax / p.F))

@@ -65,6 +65,9 @@ __device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int delta) {
     return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
 }
 
+__device__ __forceinline__ int32_t shfl_up_cnt(int32_t v, int delta) { return shfl_up_i(v, delta); }
+__device__ __forceinline__ int64_t shfl_up_cnt(int64_t v, int delta) { return shfl_up_i64(v, delta); }
+
 __device__ __forceinline__ float shfl_down_f(float v, int delta) {
     return __shfl_down(v, (unsigned)delta, 64);
 }

@@ -16,6 +16,8 @@
 // partials are themselves a sorted list of rows with counts, and the same
 // kernel reduces them at the next level until one block remains. No atomics,
 // no output memset, and the result does not depend on timing.
+#include <type_traits>
+
 #include "common.h"
 
 namespace geot {
@@ -29,10 +31,14 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     constexpr int NW = kBlock / 64;   // waves per block
     constexpr int G = kBlock / L;     // row groups per block
     constexpr int TW = NT * L * V;    // columns per tile
-    constexpr int U = NV >= 4 ? 4 : 8;  // rows loaded ahead per row group
+    constexpr int U = NV >= 4 ? 4 : 8;   // rows loaded ahead per row group
+    constexpr int UG = NV >= 4 ? 4 : 8;  // edges per batch of the gather pipeline
+    // Segment ids fit 32 bits (the host rejects num_segments >= 2^31). Row counts
+    // of one block fit 32 bits; partial levels add counts of many blocks: 64 bits.
+    using Cnt = typename std::conditional<MODE == SRC_PIECES, int64_t, int32_t>::type;
 
     __shared__ float s_v[NW][TW];
-    __shared__ int64_t s_n[NW];
+    __shared__ Cnt s_n[NW];
     __shared__ int s_f[NW];
 
     const int tid = threadIdx.x;
@@ -61,10 +67,10 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     const float neutral = red_neutral<RED>();
 
     // ---- helpers -------------------------------------------------------
-    auto store_seg = [&](int64_t seg, const float *v, int64_t n) {
+    auto store_seg = [&](int32_t seg, const float *v, Cnt n) {
         if (MODE == SRC_PIECES && n == 0) return;     // only empty partials: stored elsewhere
-        if ((uint64_t)seg >= (uint64_t)a.S) return;   // out-of-range id: skip the store
-        float *o = a.out + seg * a.ld_out;
+        if (seg < 0 || (int64_t)seg >= a.S) return;   // out-of-range id: skip the store
+        float *o = a.out + (int64_t)seg * a.ld_out;
         const float fn = (float)n;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
@@ -88,7 +94,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 if (cv[j]) store_vec<V>(o + cb[j], z);
         }
     };
-    auto write_partial = [&](int slot, int64_t seg, const float *v, int64_t n) {
+    auto write_partial = [&](int slot, int32_t seg, const float *v, Cnt n) {
         if (a.pv == nullptr) return;
         const int64_t row = 2 * chunk + slot;
         if (n > 0) {
@@ -98,11 +104,11 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 if (cv[j]) store_vec<V>(p + cb[j], v + j * V);
         }
         if (tile == 0 && gl == 0) {
-            a.pseg[row] = seg;
-            a.pcnt[row] = n;
+            a.pseg[row] = (int64_t)seg;
+            a.pcnt[row] = (int64_t)n;
         }
     };
-    auto load_term = [&](int64_t r, float *x, int64_t &c) {
+    auto load_term = [&](int64_t r, float *x, Cnt &c) {
         if constexpr (MODE == SRC_ROWS) {
             c = 1;
             const float *p = a.src + r * a.ld_src;
@@ -112,40 +118,25 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
             }
         } else if constexpr (MODE == SRC_PIECES) {
-            c = a.cnt[r];
+            c = (Cnt)a.cnt[r];
             const float *p = a.src + r * a.ld_src;
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
                 if (cv[j] && c > 0) load_vec<V>(p + cb[j], x + j * V);
                 else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
             }
-        } else {
-            c = 1;
-            const int64_t src_row = a.col[r];
-            const float wt = a.w ? a.w[r] : 1.0f;
-            const bool ok = (uint64_t)src_row < (uint64_t)a.num_x_rows;
-            const float *p = a.src + src_row * a.ld_src;
-#pragma unroll
-            for (int j = 0; j < NT; ++j) {
-                if (cv[j] && ok) {
-                    load_vec<V>(p + cb[j], x + j * V);
-#pragma unroll
-                    for (int k = 0; k < V; ++k) x[j * V + k] = wt * x[j * V + k];
-                } else {
-                    for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
-                }
-            }
         }
     };
 
     // ---- serial reduction of this row group's run [r0, r1) --------------
-    int64_t first_seg = -1, cur = -1, accn = 0, headn = 0;
+    int32_t first_seg = -1, cur = -1;
+    Cnt accn = 0, headn = 0;
     float acc[NV], head[NV];
     bool head_done = false;
 #pragma unroll
     for (int k = 0; k < NV; ++k) { acc[k] = neutral; head[k] = neutral; }
 
-    auto step = [&](int64_t s, const float *x, int64_t c) {
+    auto step = [&](int32_t s, const float *x, Cnt c) {
         if (s != cur) {
             if (!head_done) {
 #pragma unroll
@@ -155,7 +146,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             } else {
                 store_seg(cur, acc, accn);  // started and ended inside this run
             }
-            if (a.fill_gaps) fill_empty(cur + 1, s);
+            if (a.fill_gaps) fill_empty((int64_t)cur + 1, (int64_t)s);
             cur = s;
 #pragma unroll
             for (int k = 0; k < NV; ++k) acc[k] = x[k];
@@ -167,33 +158,100 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         }
     };
 
-    int64_t prev = -1, next = -1;
+    int32_t prev = -1, next = -1;
     if (has_rows) {
-        first_seg = a.idx[r0];
+        first_seg = (int32_t)a.idx[r0];
         cur = first_seg;
-        prev = r0 > 0 ? a.idx[r0 - 1] : -1;
-        next = r1 < a.n ? a.idx[r1] : -1;
-        if (a.fill_gaps) fill_empty(prev + 1, first_seg);
+        prev = r0 > 0 ? (int32_t)a.idx[r0 - 1] : -1;
+        next = r1 < a.n ? (int32_t)a.idx[r1] : -1;
+        if (a.fill_gaps) fill_empty((int64_t)prev + 1, (int64_t)first_seg);
 
-        int64_t r = r0;
-        for (; r + U <= r1; r += U) {
-            int64_t s[U], c[U];
-            float x[U][NV];
+        if constexpr (MODE == SRC_GATHER) {
+            // Edge metadata (segment id, source row, weight) of the next UG edges is
+            // loaded while the X rows of the current UG edges are in flight, so the
+            // dependent gathers never wait behind their own column loads. Rows past
+            // r1 are clamped to r1 - 1 (valid addresses) and not reduced.
+            // With at least UG lanes per row group, lane u of the group loads the
+            // metadata of edge r + u (one coalesced load per array) and every lane
+            // reads it back with a lane shuffle; otherwise each lane loads all UG.
+            constexpr bool kShared = L >= UG;
+            constexpr int UM = kShared ? 1 : UG;
+            const int gbase = gw * L;
+            int32_t ns[UM];
+            int64_t nc[UM];
+            float nw[UM];
+            auto load_meta = [&](int64_t rb) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) s[u] = a.idx[r + u];
+                for (int m = 0; m < UM; ++m) {
+                    const int64_t rr = min(rb + (kShared ? (int64_t)min(gl, UG - 1) : (int64_t)m), r1 - 1);
+                    ns[m] = (int32_t)a.idx[rr];
+                    nc[m] = a.col[rr];
+                    nw[m] = a.w ? a.w[rr] : 1.0f;
+                }
+            };
+            load_meta(r0);
+            for (int64_t r = r0; r < r1; r += UG) {
+                int32_t s[UG];
+                float wt[UG];
+                float x[UG][NV];
 #pragma unroll
-            for (int u = 0; u < U; ++u) load_term(r + u, x[u], c[u]);
+                for (int u = 0; u < UG; ++u) {
+                    int64_t c;
+                    if constexpr (kShared) {
+                        s[u] = __shfl(ns[0], gbase + u, 64);
+                        wt[u] = __shfl(nw[0], gbase + u, 64);
+                        const int lo = __shfl((int)(uint32_t)(uint64_t)nc[0], gbase + u, 64);
+                        const int hi = __shfl((int)(uint32_t)((uint64_t)nc[0] >> 32), gbase + u, 64);
+                        c = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+                    } else {
+                        s[u] = ns[u];
+                        wt[u] = nw[u];
+                        c = nc[u];
+                    }
+                    const bool ok = (uint64_t)c < (uint64_t)a.num_x_rows;
+                    const float *p = a.src + c * a.ld_src;
 #pragma unroll
-            for (int u = 0; u < U; ++u) step(s[u], x[u], c[u]);
+                    for (int j = 0; j < NT; ++j) {
+                        if (cv[j] && ok) {
+                            load_vec<V>(p + cb[j], x[u] + j * V);
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
+                        }
+                    }
+                }
+                if (r + UG < r1) load_meta(r + UG);
+#pragma unroll
+                for (int u = 0; u < UG; ++u) {
+                    if (r + u < r1) {
+#pragma unroll
+                        for (int k = 0; k < NV; ++k) x[u][k] = wt[u] * x[u][k];
+                        step(s[u], x[u], 1);
+                    }
+                }
+            }
+        } else {
+            int64_t r = r0;
+            for (; r + U <= r1; r += U) {
+                int32_t s[U];
+                Cnt c[U];
+                float x[U][NV];
+#pragma unroll
+                for (int u = 0; u < U; ++u) s[u] = (int32_t)a.idx[r + u];
+#pragma unroll
+                for (int u = 0; u < U; ++u) load_term(r + u, x[u], c[u]);
+#pragma unroll
+                for (int u = 0; u < U; ++u) step(s[u], x[u], c[u]);
+            }
+            for (; r < r1; ++r) {
+                float x[NV];
+                Cnt c;
+                const int32_t s = (int32_t)a.idx[r];
+                load_term(r, x, c);
+                step(s, x, c);
+            }
         }
-        for (; r < r1; ++r) {
-            float x[NV];
-            int64_t c;
-            const int64_t s = a.idx[r];
-            load_term(r, x, c);
-            step(s, x, c);
-        }
-        if (a.fill_gaps && r1 == a.n) fill_empty(cur + 1, a.S);  // trailing empty segments
+        if (a.fill_gaps && r1 == a.n) fill_empty((int64_t)cur + 1, a.S);  // trailing empty segments
     }
     const bool single_run = !head_done;  // the run holds one segment only: head == tail
     if (single_run) {
@@ -201,7 +259,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         for (int k = 0; k < NV; ++k) head[k] = acc[k];
         headn = accn;
     }
-    const int64_t last_seg = cur;
+    const int32_t last_seg = cur;
     const bool starts = has_rows && prev != first_seg;     // first segment begins at r0
     const bool ends_tail = has_rows && next != last_seg;   // last segment ends at r1 - 1
 
@@ -210,13 +268,13 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     // (f1, v1, n1) (+) (f2, v2, n2) = (f1 | f2, f2 ? v2 : v1 (+) v2, f2 ? n2 : n1 + n2).
     bool f = has_rows && (starts || !single_run);
     float v[NV];
-    int64_t n = has_rows ? accn : 0;
+    Cnt n = has_rows ? accn : 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) v[k] = acc[k];
 #pragma unroll
     for (int d = 1; d < GW; d <<= 1) {
         const int fo = shfl_up_i((int)f, d * L);
-        const int64_t no = shfl_up_i64(n, d * L);
+        const Cnt no = shfl_up_cnt(n, d * L);
         float vo[NV];
 #pragma unroll
         for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], d * L);
@@ -244,12 +302,12 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     // exclusive prefix of this group: waves before this one, then groups before it in the wave
     bool ef = false;
     float ev[NV];
-    int64_t en = 0;
+    Cnt en = 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) ev[k] = neutral;
     for (int w2 = 0; w2 < wave; ++w2) {
         const bool f2 = s_f[w2] != 0;
-        const int64_t n2 = s_n[w2];
+        const Cnt n2 = s_n[w2];
 #pragma unroll
         for (int j = 0; j < NT; ++j)
 #pragma unroll
@@ -262,7 +320,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     }
     {
         const int fo = shfl_up_i((int)f, L);
-        const int64_t no = shfl_up_i64(n, L);
+        const Cnt no = shfl_up_cnt(n, L);
         float vo[NV];
 #pragma unroll
         for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], L);
@@ -280,7 +338,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         bool hi_written = false;
         // value of the run's first segment including what precedes it in the block
         float hv[NV];
-        int64_t hn;
+        Cnt hn;
         bool h_in_block;
         if (starts) {
 #pragma unroll
@@ -313,11 +371,11 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         }
         // empty partials keep the list of partials sorted and complete
         if (g == 0 && starts && a.pv != nullptr && tile == 0 && gl == 0) {
-            a.pseg[2 * chunk] = first_seg;
+            a.pseg[2 * chunk] = (int64_t)first_seg;
             a.pcnt[2 * chunk] = 0;
         }
         if (last_group && !hi_written && a.pv != nullptr && tile == 0 && gl == 0) {
-            a.pseg[2 * chunk + 1] = last_seg;
+            a.pseg[2 * chunk + 1] = (int64_t)last_seg;
             a.pcnt[2 * chunk + 1] = 0;
         }
     }
