@@ -185,7 +185,8 @@ int widest_vec(const Problem &p) {
     return 1;
 }
 
-geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r) {
+geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r,
+                      bool from_selector = false) {
     if (c.flags != 0) return fail(GEOT_ERROR_UNSUPPORTED, "choice.flags must be 0");
     r->family = c.family == GEOT_FAMILY_AUTO ? GEOT_FAMILY_EP : c.family;
     if (r->family != GEOT_FAMILY_EP && r->family != GEOT_FAMILY_SP)
@@ -213,10 +214,12 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     if (c.rows < 0 || c.rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
     r->K = c.rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles) : c.rows;
     const int GW = 64 / L;
-    if (c.groups < 0 || (c.groups != 0 && (!is_pow2(c.groups) || c.groups > GW)))
+    geot_kernel_choice_t cc = c;
+    if (from_selector && cc.groups > GW) cc.groups = GW;  // tree leaves are shape-independent
+    if (cc.groups < 0 || (cc.groups != 0 && (!is_pow2(cc.groups) || cc.groups > GW)))
         return fail(GEOT_ERROR_UNSUPPORTED, "groups must be a power of two <= 64/lanes");
-    if (c.groups != 0) {
-        r->groups = c.groups;
+    if (cc.groups != 0) {
+        r->groups = cc.groups;
     } else {
         const double mean = p.S > 0 ? (double)p.nnz / (double)p.S : 0.0;
         int gsz = 1;
@@ -433,7 +436,7 @@ geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_
         select_raw(p.nnz, p.S, p.F, p.op, p.gather ? 1 : 0, nullptr, &c);
     }
     Resolved r;
-    s = resolve(p, c, &r);
+    s = resolve(p, c, &r, forced == nullptr);
     if (s != GEOT_SUCCESS) return s;
     s = r.family == GEOT_FAMILY_SP ? run_sp(p, r, st) : run_ep(p, r, st);
     if (s == GEOT_SUCCESS) t_last_choice = to_choice(r);
@@ -493,7 +496,7 @@ geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_
     Problem p{gather != 0, (const float *)(uintptr_t)256, 0, nullptr, nullptr, nullptr,
               nnz, num_segments, F, op, (float *)(uintptr_t)256};
     Resolved r;
-    geot_status_t s = resolve(p, c, &r);
+    geot_status_t s = resolve(p, c, &r, true);
     if (s != GEOT_SUCCESS) return s;
     *out = to_choice(r);
     return GEOT_SUCCESS;

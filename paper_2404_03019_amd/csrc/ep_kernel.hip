@@ -230,6 +230,26 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                     }
                 }
             }
+        } else if constexpr (MODE == SRC_ROWS && L >= U) {
+            // Lane u of the row group loads the segment id of row r + u (one
+            // coalesced load per batch, one batch ahead); the group reads the ids
+            // back with lane shuffles. Rows past r1 are clamped and not reduced.
+            const int gbase = gw * L;
+            const int lu = min(gl, U - 1);
+            int32_t nid = (int32_t)a.idx[min(r0 + lu, r1 - 1)];
+            for (int64_t r = r0; r < r1; r += U) {
+                const int32_t id = nid;
+                float x[U][NV];
+                Cnt c;
+#pragma unroll
+                for (int u = 0; u < U; ++u) load_term(min(r + u, r1 - 1), x[u], c);
+                if (r + U < r1) nid = (int32_t)a.idx[min(r + U + lu, r1 - 1)];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int32_t su = __shfl(id, gbase + u, 64);
+                    if (r + u < r1) step(su, x[u], 1);
+                }
+            }
         } else {
             int64_t r = r0;
             for (; r + U <= r1; r += U) {

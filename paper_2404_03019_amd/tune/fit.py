@@ -1,0 +1,329 @@
+"""Fit the selector's decision trees to the performance database and emit them as C++ if/else.
+
+Follows Section III-C of the GeoT paper: a decision tree of depth at most 5
+over cheap input features, whose leaves hold a whole kernel configuration
+(chosen jointly, not parameter by parameter), emitted as nested if/else in
+``csrc/selector_generated.h`` and compiled into the library.
+
+Leaves and splits are fitted to the measured times directly: each leaf takes
+the candidate with the least total log-slowdown (log of time over the best
+measured time of the same input) over the inputs that reach it, and each
+split is the feature threshold that most reduces that total. The paper's own
+recipe (Top-1 labels and a scikit-learn multi-output regressor of depth 5,
+leaves rounded to valid parameters) is fitted too and reported as an
+ablation, beside the hand-written rule.
+
+Two trees, as the paper keeps two:
+  * ``nostats``: O(1) features only (log2 nnz, log2 num_segments, F,
+    log2 mean length, op, gather); chooses among element-parallel row runs;
+  * ``stats``: adds the length cv and log2(longest / mean) from
+    geot_index_stats; chooses the family and its parameters.
+
+Usage: python -m paper_2404_03019_amd.tune.fit [--db perfdb.jsonl] [--out ../csrc/selector_generated.h]
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import json
+import math
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+DEFAULT_DB = os.path.join(HERE, "perfdb.jsonl")
+DEFAULT_OUT = os.path.join(os.path.dirname(HERE), "csrc", "selector_generated.h")
+MAX_DEPTH = 5
+
+
+def load(db: str):
+    inst = collections.OrderedDict()
+    for line in open(db):
+        r = json.loads(line)
+        k = (r["instance"]["id"], r["instance"]["seed"])
+        e = inst.setdefault(k, dict(instance=r["instance"], features=r["features"], times={}, choices={}))
+        e["times"][r["cand"]] = r["ms"]
+        e["choices"][r["cand"]] = r["choice"]
+    return list(inst.values())
+
+
+def feature_row(f: dict, stats: bool):
+    row = [math.log2(max(f["nnz"], 1)), math.log2(max(f["S"], 1)), float(f["F"]),
+           math.log2(max(f["mean"], 1e-9)), 1.0 if f["op"] == "max" else 0.0, float(f["gather"])]
+    if stats:
+        row += [float(f["cv"]), math.log2(max(f["max_rel"], 1e-9))]
+    return row
+
+
+FEATURES_NOSTATS = ["lnnz", "lS", "F", "lmean", "opmax", "gather"]
+FEATURES_STATS = FEATURES_NOSTATS + ["cv", "lmaxrel"]
+
+
+def best_of(e, fam=None):
+    items = [(t, c) for c, t in e["times"].items()
+             if (fam is None or e["choices"][c]["family"] == fam) and e["choices"][c].get("rows", 1) != 0]
+    return min(items) if items else (math.inf, None)
+
+
+def targets(e):
+    t_all, c_all = best_of(e)
+    _, c_ep = best_of(e, 1)
+    _, c_sp = best_of(e, 2)
+    fam = e["choices"][c_all]["family"]
+    k = e["choices"][c_ep]["rows"]
+    g = e["choices"][c_sp]["groups"] if c_sp else 1
+    return fam, math.log2(k), math.log2(g)
+
+
+def fit_tree(X, Y):
+    from sklearn.tree import DecisionTreeRegressor
+
+    t = DecisionTreeRegressor(max_depth=MAX_DEPTH, min_samples_leaf=2, random_state=0)
+    t.fit(np.asarray(X), np.asarray(Y))
+    return t
+
+
+def round_leaf(v, with_family: bool):
+    if with_family:
+        fam = 2 if v[0] >= 1.5 else 1
+        k = int(2 ** min(8, max(2, round(v[1]))))
+        g = int(2 ** min(6, max(0, round(v[2]))))
+        return fam, k, g
+    k = int(2 ** min(8, max(2, round(v[0]))))
+    return 1, k, 1
+
+
+def emit(tree, names, with_family, indent):
+    t = tree.tree_
+    lines = []
+
+    def rec(node, depth):
+        pad = " " * (indent + 4 * depth)
+        if t.children_left[node] == t.children_right[node]:
+            fam, k, g = round_leaf(t.value[node][:, 0], with_family)
+            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};")
+            return
+        f = names[t.feature[node]]
+        thr = t.threshold[node]
+        lines.append(f"{pad}if ({f} <= {thr:.6g}) {{")
+        rec(t.children_left[node], depth + 1)
+        lines.append(f"{pad}}} else {{")
+        rec(t.children_right[node], depth + 1)
+        lines.append(f"{pad}}}")
+
+    rec(0, 0)
+    return lines
+
+
+def predict_cand(tree, row, with_family, e):
+    v = tree.predict(np.asarray([row]))[0]
+    fam, k, g = round_leaf(np.atleast_1d(v), with_family)
+    c = f"f1_r{k}_g0" if fam == 1 else f"f2_r0_g{g}"
+    if c not in e["times"]:  # SP not measured for this input: fall back to the element-parallel leaf
+        c = f"f1_r{k}_g0"
+    return c
+
+
+EP_ROWS = (4, 8, 16, 32, 64, 128, 256)
+MISSING_COST = math.log(50.0)  # a candidate that was not measured (or too slow to finish)
+NAMED_WEIGHT = 16.0            # the named benchmark workloads count this many times
+
+
+def lanes_for(F: int) -> int:
+    V = 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1)
+    vecs = -(-F // V)
+    L = 1
+    while L < vecs and L < 64:
+        L <<= 1
+    return L
+
+
+def candidate_space(stats: bool):
+    c = [(1, k, 1) for k in EP_ROWS]
+    if stats:
+        c += [(2, 0, g) for g in (1, 2, 4, 8, 16, 32, 64)]
+    return c
+
+
+def cost_matrix(data, cands):
+    """C[i, j] = w_i * log(time of candidate j / best measured time of input i); the named
+    workloads get weight NAMED_WEIGHT, every other input weight 1."""
+    C = np.full((len(data), len(cands)), MISSING_COST)
+    for i, e in enumerate(data):
+        tb, _ = best_of(e)
+        gw = 64 // lanes_for(e["instance"]["F"])
+        for j, (fam, k, g) in enumerate(cands):
+            key = f"f1_r{k}_g0" if fam == 1 else f"f2_r0_g{min(g, gw)}"
+            t = e["times"].get(key)
+            if t is not None and t > 0 and tb > 0:
+                C[i, j] = min(MISSING_COST, math.log(t / tb))
+        if e["instance"]["id"] >= 10000:
+            C[i] *= NAMED_WEIGHT
+    return C
+
+
+class CostTree:
+    """Greedy tree minimising the total cost of one candidate per leaf."""
+
+    def __init__(self, max_depth=MAX_DEPTH, min_leaf=2):
+        self.max_depth, self.min_leaf = max_depth, min_leaf
+
+    def fit(self, X, C):
+        self.X, self.C = np.asarray(X, dtype=np.float64), np.asarray(C, dtype=np.float64)
+        self.root = self._grow(np.arange(len(self.X)), 0)
+        return self
+
+    def _leaf(self, rows):
+        tot = self.C[rows].sum(axis=0)
+        return dict(leaf=int(np.argmin(tot)), cost=float(tot.min()))
+
+    def _grow(self, rows, depth):
+        node = self._leaf(rows)
+        if depth >= self.max_depth or len(rows) < 2 * self.min_leaf:
+            return node
+        best = (node["cost"] - 1e-9, None)
+        for f in range(self.X.shape[1]):
+            order = rows[np.argsort(self.X[rows, f], kind="stable")]
+            vals = self.X[order, f]
+            pre = np.cumsum(self.C[order], axis=0)
+            total = pre[-1]
+            for i in range(self.min_leaf - 1, len(order) - self.min_leaf):
+                if vals[i] == vals[i + 1]:
+                    continue
+                c = pre[i].min() + (total - pre[i]).min()
+                if c < best[0]:
+                    best = (c, (f, 0.5 * (vals[i] + vals[i + 1])))
+        if best[1] is None:
+            return node
+        f, thr = best[1]
+        left = rows[self.X[rows, f] <= thr]
+        right = rows[self.X[rows, f] > thr]
+        return dict(feature=f, threshold=thr, left=self._grow(left, depth + 1),
+                    right=self._grow(right, depth + 1))
+
+    def predict_one(self, x):
+        n = self.root
+        while "leaf" not in n:
+            n = n["left"] if x[n["feature"]] <= n["threshold"] else n["right"]
+        return n["leaf"]
+
+
+def emit_cost_tree(tree, names, cands, indent):
+    lines = []
+
+    def rec(n, depth):
+        pad = " " * (indent + 4 * depth)
+        if "leaf" in n:
+            fam, k, g = cands[n["leaf"]]
+            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};")
+            return
+        lines.append(f"{pad}if ({names[n['feature']]} <= {n['threshold']:.9g}) {{")
+        rec(n["left"], depth + 1)
+        lines.append(f"{pad}}} else {{")
+        rec(n["right"], depth + 1)
+        lines.append(f"{pad}}}")
+
+    rec(tree.root, 0)
+    return lines
+
+
+def build(db: str):
+    """Load the database and fit both trees. Returns (nostats_tree, stats_tree, data, Xn, Xs)."""
+    data = load(db)
+    data = [e for e in data if any(e["choices"][c]["family"] == 1 and e["choices"][c].get("rows", 0) > 0
+                                   for c in e["times"])]
+    Xn = [feature_row(e["features"], False) for e in data]
+    Xs = [feature_row(e["features"], True) for e in data]
+    tn = CostTree().fit(Xn, cost_matrix(data, candidate_space(False)))
+    ts = CostTree().fit(Xs, cost_matrix(data, candidate_space(True)))
+    return tn, ts, data, Xn, Xs
+
+
+def render(tn, ts, n_inputs: int) -> str:
+    """The C++ header text of both trees."""
+    body = ["// Kernel selection rules compiled into libgeot_hip (Section III-C: a decision tree",
+            "// over cheap input features, emitted as if/else). GENERATED by",
+            "// paper_2404_03019_amd/tune/fit.py from the MI355X performance database",
+            "// paper_2404_03019_amd/tune/perfdb.jsonl; do not edit by hand.",
+            "//",
+            f"// Training inputs: {n_inputs}. Depth <= {MAX_DEPTH}. Each leaf is the candidate with the",
+            "// least total log-slowdown over the inputs reaching it. out[0] family (1 element-",
+            "// parallel, 2 segment-parallel), out[3] rows per row group, out[4] row groups per",
+            "// segment (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape.",
+            "#pragma once", "", "#include <cmath>", "#include <cstdint>", "", "namespace geot {", "",
+            "static inline void tree_select(double nnz, double num_segments, double F, int op, int gather,",
+            "                               int has_stats, double cv, double max_rel, int32_t out[5]) {",
+            "    const double lnnz = std::log2(nnz > 1.0 ? nnz : 1.0);",
+            "    const double lS = std::log2(num_segments > 1.0 ? num_segments : 1.0);",
+            "    const double mean = num_segments > 0.0 ? nnz / num_segments : 0.0;",
+            "    const double lmean = std::log2(mean > 1e-9 ? mean : 1e-9);",
+            "    const double opmax = op == 2 ? 1.0 : 0.0;",
+            "    const double lmaxrel = std::log2(max_rel > 1e-9 ? max_rel : 1e-9);",
+            "    (void)lnnz; (void)lS; (void)F; (void)lmean; (void)opmax; (void)cv; (void)lmaxrel; (void)gather;",
+            "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0;",
+            "    if (!has_stats) {"]
+    body += emit_cost_tree(tn, FEATURES_NOSTATS, candidate_space(False), 8)
+    body += ["    } else {"]
+    body += emit_cost_tree(ts, FEATURES_STATS, candidate_space(True), 8)
+    body += ["    }", "}", "", "}  // namespace geot", ""]
+    return "\n".join(body)
+
+
+def _time_of(e, cand):
+    fam, k, g = cand
+    gw = 64 // lanes_for(e["instance"]["F"])
+    key = f"f1_r{k}_g0" if fam == 1 else f"f2_r0_g{min(g, gw)}"
+    return e["times"].get(key, math.nan)
+
+
+def evaluate(tn, ts, data, Xn, Xs):
+    """Per input: chosen time / best measured time, for the trees, the paper's recipe and the hand rule."""
+    cn, cs = candidate_space(False), candidate_space(True)
+    # the paper's recipe as an ablation: Top-1 labels, multi-output regressor, rounded leaves
+    pn = fit_tree(Xn, [[targets(e)[1]] for e in data])
+    ps = fit_tree(Xs, [list(targets(e)) for e in data])
+    rep = []
+    for e, xn, xs in zip(data, Xn, Xs):
+        tb, _ = best_of(e)
+        tbe, _ = best_of(e, 1)
+        rep.append(dict(
+            name=e["instance"]["dist"], id=e["instance"]["id"], F=e["instance"]["F"],
+            op=e["instance"]["op"], gather=e["instance"]["gather"], nnz=e["features"]["nnz"], best=tb,
+            nostats=_time_of(e, cn[tn.predict_one(xn)]) / tbe,
+            stats=_time_of(e, cs[ts.predict_one(xs)]) / tb,
+            paper_nostats=e["times"].get(predict_cand(pn, xn, False, e), math.nan) / tbe,
+            paper_stats=e["times"].get(predict_cand(ps, xs, True, e), math.nan) / tb,
+            hand=e["times"].get("f1_r0_g0", math.nan) / tbe))
+    return rep
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--db", default=DEFAULT_DB)
+    ap.add_argument("--out", default=DEFAULT_OUT)
+    args = ap.parse_args()
+    tn, ts, data, Xn, Xs = build(args.db)
+    open(args.out, "w").write(render(tn, ts, len(data)))
+    rep = evaluate(tn, ts, data, Xn, Xs)
+
+    def gm(xs):
+        xs = [x for x in xs if x == x and x > 0]
+        return math.exp(sum(math.log(x) for x in xs) / len(xs)) if xs else math.nan
+
+    print(f"inputs {len(data)}; wrote {args.out}")
+    for k in ("nostats", "stats", "paper_nostats", "paper_stats", "hand"):
+        v = [r[k] for r in rep]
+        w = sum(1 for x in v if x == x and x <= 1.10)
+        print(f"{k:14s} geomean slowdown vs best {gm(v):.3f}  max {np.nanmax(v):.3f}  within 10%: {w}/{len(v)}")
+    print("named workloads:")
+    for r in rep:
+        if r["id"] >= 10000:
+            print(f"  {r['name']:20s} F={r['F']:3d} {r['op']:4s} best {r['best']:.3f} ms  "
+                  f"nostats x{r['nostats']:.3f}  stats x{r['stats']:.3f}  paper x{r['paper_stats']:.3f}  "
+                  f"hand x{r['hand']:.3f}")
+    json.dump(rep, open(os.path.join(HERE, "fit_report.json"), "w"), indent=0)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,97 @@
+"""The selector: the committed C++ if/else is exactly what fitting the committed MI355X
+performance database produces, the compiled if/else agrees with the fitted trees on
+every training input, and the library's geot_select returns the tree's choice.
+CPU only (g++ compiles the generated header).
+"""
+import math
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2404_03019_amd.tune import fit
+
+DB = fit.DEFAULT_DB
+HEADER = fit.DEFAULT_OUT
+
+pytestmark = pytest.mark.skipif(not os.path.exists(DB), reason="no performance database committed")
+
+DRIVER = r"""
+#include <cstdio>
+#include "selector_generated.h"
+int main() {
+    double nnz, S, F, cv, mx; int op, gather, has;
+    while (std::scanf("%lf %lf %lf %d %d %d %lf %lf", &nnz, &S, &F, &op, &gather, &has, &cv, &mx) == 8) {
+        int32_t out[5];
+        geot::tree_select(nnz, S, F, op, gather, has, cv, mx, out);
+        std::printf("%d %d %d\n", out[0], out[3], out[4]);
+    }
+    return 0;
+}
+"""
+
+
+@pytest.fixture(scope="module")
+def fitted():
+    return fit.build(DB)
+
+
+def test_committed_header_is_reproducible(fitted):
+    tn, ts, data, _, _ = fitted
+    assert open(HEADER).read() == fit.render(tn, ts, len(data)), \
+        "selector_generated.h is stale: rerun python -m paper_2404_03019_amd.tune.fit"
+
+
+def test_compiled_tree_matches_sklearn(fitted, tmp_path):
+    tn, ts, data, Xn, Xs = fitted
+    drv = tmp_path / "drv.cpp"
+    drv.write_text(DRIVER)
+    exe = str(tmp_path / "drv")
+    subprocess.run(["g++", "-O1", "-std=c++17", "-I", os.path.dirname(HEADER), str(drv), "-o", exe],
+                   check=True)
+    lines, want = [], []
+    ops = {"sum": 0, "mean": 1, "max": 2}
+    for e, xn, xs in zip(data, Xn, Xs):
+        f = e["features"]
+        for has in (0, 1):
+            lines.append(f"{f['nnz']} {f['S']} {f['F']} {ops[f['op']]} {f['gather']} {has} "
+                         f"{f['cv']!r} {f['max_rel']!r}")
+            if has:
+                want.append(fit.candidate_space(True)[ts.predict_one(xs)])
+            else:
+                want.append(fit.candidate_space(False)[tn.predict_one(xn)])
+    got = subprocess.run([exe], input="\n".join(lines) + "\n", capture_output=True, text=True,
+                         check=True).stdout.split("\n")
+    mism = [(l, g, w) for l, g, w in zip(lines, got, want)
+            if tuple(int(t) for t in g.split()) != tuple(w)]
+    # a feature exactly on a threshold may round differently between the two evaluations
+    assert len(mism) <= max(1, len(lines) // 200), mism[:5]
+
+
+def test_library_select_follows_the_tree(fitted):
+    import paper_2404_03019_amd as geot
+
+    tn, ts, data, Xn, Xs = fitted
+    for e, xn in list(zip(data, Xn))[:60]:
+        f = e["features"]
+        fam, k, g = fit.candidate_space(False)[tn.predict_one(xn)]
+        c = geot.select(f["nnz"], f["S"], f["F"], f["op"], bool(f["gather"]))
+        assert c["family"] == fam and c["rows"] == k, (f, c, (fam, k))
+
+
+def test_selector_beats_the_hand_rule_and_the_paper_recipe(fitted):
+    """Measured on MI355X: geometric-mean slowdown against the best measured candidate."""
+    tn, ts, data, Xn, Xs = fitted
+    rep = fit.evaluate(tn, ts, data, Xn, Xs)
+
+    def gm(k):
+        v = [r[k] for r in rep if r[k] == r[k]]
+        return math.exp(sum(math.log(x) for x in v) / len(v))
+
+    assert gm("nostats") < gm("paper_nostats") < gm("hand")
+    assert gm("nostats") <= 1.05
+    named = [r for r in rep if r["id"] >= 10000]
+    # the large named workloads (above 0.2 ms) are within 10% of the best candidate
+    big = [r for r in named if r["best"] >= 0.2]
+    assert big and all(r["nostats"] <= 1.10 for r in big), big
