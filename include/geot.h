@@ -26,8 +26,9 @@
  *  - `out` is overwritten in full, including empty segments (it is never
  *    accumulated into). Empty segments hold GEOT_EMPTY_FILL for every op.
  *  - Temporary device memory (partial results of segments that cross block
- *    boundaries) comes from a stream-ordered pool owned by the library and is
- *    released on the same stream.
+ *    boundaries) comes from a stream-ordered pool owned by the library; the
+ *    reductions keep one buffer per (device, stream) for reuse (see
+ *    geot_release_scratch).
  *  - Preconditions: the index is non-decreasing and 0 <= index < num_segments;
  *    for the gather form 0 <= col < num_x_rows. They are not checked by the
  *    reduction calls (geot_check_index checks them). Violations give
@@ -114,8 +115,10 @@ typedef struct {
  *   sorted_index  [nnz] int64, non-decreasing, values in [0, num_segments)
  *   out           [num_segments x F] fp32, overwritten; must not overlap inputs
  * nnz == 0 fills `out` with GEOT_EMPTY_FILL; num_segments == 0 or F == 0 is a
- * no-op. Returns GEOT_ERROR_INVALID_VALUE for null pointers with nonzero
- * sizes, negative sizes, an unknown op or overlapping `out`.              */
+ * no-op. num_segments must be below 2^31 (segment ids are compared in 32
+ * bits); nnz is limited only by memory. Returns GEOT_ERROR_INVALID_VALUE for
+ * null pointers with nonzero sizes, negative sizes, num_segments >= 2^31, an
+ * unknown op or overlapping `out`.                                         */
 geot_status_t geot_segment_reduce(const float *src, const int64_t *sorted_index, int64_t nnz,
                                   int64_t num_segments, int64_t F, geot_op_t op, float *out,
                                   void *stream);
@@ -168,6 +171,14 @@ geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t
  * GEOT_ERROR_OUT_OF_RANGE (out of range wins when both hold).              */
 geot_status_t geot_check_index(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
                                const int64_t *col, int64_t num_x_rows, void *stream);
+
+/* Reduction calls keep one temporary device buffer per (device, stream), reused
+ * in stream order and grown on demand (partials of block-crossing segments:
+ * two rows of F floats per block, about 1.5 % of the input for F = 128; or
+ * num_segments + 1 segment starts). This frees every such buffer after
+ * synchronizing its stream; later calls allocate again. Call it before
+ * destroying a stream the library was used on, or to return the memory. */
+geot_status_t geot_release_scratch(void);
 
 /* The kernel choice the calling thread's last successful reduction used. */
 geot_status_t geot_last_choice(geot_kernel_choice_t *out);

@@ -20,5 +20,6 @@ from .geot import (  # noqa: F401
     last_choice,
     profile_begin,
     profile_end,
+    release_scratch,
     version,
 )

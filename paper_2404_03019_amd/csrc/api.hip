@@ -100,6 +100,42 @@ struct ScratchGuard {
     }
 };
 
+// Reduction calls keep their temporary buffer per (device, stream) and reuse it
+// in stream order, growing it (stream-ordered free of the old block, then a new
+// allocation) when a call needs more. Kernels of one stream run in order, so
+// consecutive calls never overlap on the buffer.
+struct StreamKey {
+    int dev;
+    hipStream_t st;
+    bool operator<(const StreamKey &o) const { return dev != o.dev ? dev < o.dev : st < o.st; }
+};
+std::mutex g_cache_mu;
+std::map<StreamKey, std::pair<void *, size_t>> g_cache;
+
+geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **p) {
+    *p = nullptr;
+    if (bytes == 0) return GEOT_SUCCESS;
+    int dev = 0;
+    GEOT_HIP(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    auto &e = g_cache[StreamKey{dev, st}];
+    if (e.second < bytes) {
+        if (e.first) {
+            GEOT_HIP(hipFreeAsync(e.first, st), "hipFreeAsync");
+            e.first = nullptr;
+            e.second = 0;
+        }
+        const size_t grown = std::max(bytes, e.second + e.second / 2);
+        void *q = nullptr;
+        geot_status_t s = scratch_alloc(&q, grown, st);
+        if (s != GEOT_SUCCESS) return s;
+        e.first = q;
+        e.second = grown;
+    }
+    *p = e.first;
+    return GEOT_SUCCESS;
+}
+
 // ---------------------------------------------------------------------------
 // measurement hooks (geot_profile_begin / _end)
 // ---------------------------------------------------------------------------
@@ -304,9 +340,10 @@ struct Level {
     int64_t n, K, nchunks;
 };
 
+// Partial levels are small and latency-bound: short serial runs (at most 8
+// partials per row group) and one more level rather than one long block.
 int64_t piece_rows_k(int64_t n, int64_t G) {
-    if (n <= G * 512) return ceil_div(n, G);  // one block finishes it
-    return std::max<int64_t>(4, std::min<int64_t>(512, ceil_div(n, G * 256)));
+    return std::max<int64_t>(1, std::min<int64_t>(8, ceil_div(n, G)));
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -335,11 +372,10 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
         off_c[l] = bytes;
         bytes = align256(bytes + (size_t)lv[l].n * 8);
     }
-    ScratchGuard sg;
-    sg.st = st;
-    geot_status_t s = scratch_alloc(&sg.p, bytes, st);
+    void *scratch = nullptr;
+    geot_status_t s = stream_scratch(bytes, st, &scratch);
     if (s != GEOT_SUCCESS) return s;
-    char *base = (char *)sg.p;
+    char *base = (char *)scratch;
     const int red = p.op == GEOT_OP_MAX ? RED_MAX : RED_SUM;
     for (size_t l = 0; l < lv.size(); ++l) {
         EpArgs a;
@@ -380,17 +416,14 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
         GEOT_HIP(launch_ep(a, red, mode, r.V, r.NT, r.L, lv[l].nchunks, st), "launch element-parallel kernel");
         if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
     }
-    void *p_free = sg.p;
-    sg.p = nullptr;
-    return scratch_free(p_free, st);
+    return GEOT_SUCCESS;
 }
 
 geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
-    ScratchGuard sg;
-    sg.st = st;
-    geot_status_t s = scratch_alloc(&sg.p, (size_t)(p.S + 1) * 8, st);
+    void *scratch = nullptr;
+    geot_status_t s = stream_scratch((size_t)(p.S + 1) * 8, st, &scratch);
     if (s != GEOT_SUCCESS) return s;
-    int64_t *off = (int64_t *)sg.p;
+    int64_t *off = (int64_t *)scratch;
     GEOT_HIP(launch_offsets(p.idx, p.nnz, p.S, off, st), "launch offsets kernel");
     SpArgs a;
     memset(&a, 0, sizeof(a));
@@ -414,9 +447,7 @@ geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
     GEOT_HIP(launch_sp(a, red, p.gather ? SRC_GATHER : SRC_ROWS, r.V, r.NT, r.L, st),
              "launch segment-parallel kernel");
     if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
-    void *p_free = sg.p;
-    sg.p = nullptr;
-    return scratch_free(p_free, st);
+    return GEOT_SUCCESS;
 }
 
 geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_t *forced) {
@@ -571,6 +602,24 @@ geot_status_t geot_check_index(const int64_t *sorted_index, int64_t nnz, int64_t
     if (h & 1u) return fail(GEOT_ERROR_OUT_OF_RANGE, "index or column out of range");
     if (h & 2u) return fail(GEOT_ERROR_NOT_SORTED, "index is not non-decreasing");
     return GEOT_SUCCESS;
+}
+
+geot_status_t geot_release_scratch(void) {
+    t_detail.clear();
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    geot_status_t st = GEOT_SUCCESS;
+    for (auto &kv : g_cache) {
+        if (!kv.second.first) continue;
+        int cur = 0;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess) e = hipSetDevice(kv.first.dev);
+        if (e == hipSuccess) e = hipFreeAsync(kv.second.first, kv.first.st);
+        if (e == hipSuccess) e = hipStreamSynchronize(kv.first.st);
+        (void)hipSetDevice(cur);
+        if (e != hipSuccess && st == GEOT_SUCCESS) st = hip_fail(e, "release scratch");
+    }
+    g_cache.clear();
+    return st;
 }
 
 geot_status_t geot_last_choice(geot_kernel_choice_t *out) {

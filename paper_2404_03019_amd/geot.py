@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
     L.geot_index_stats.argtypes = [p, i64, i64, ctypes.POINTER(IndexStats), p]
     L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
     L.geot_last_choice.argtypes = [pc]
+    L.geot_release_scratch.argtypes = []
     L.geot_profile_begin.argtypes = [i32]
     L.geot_profile_end.argtypes = [ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(i32)]
     L.geot_status_string.argtypes = [ctypes.c_int]
@@ -76,7 +77,7 @@ def lib() -> ctypes.CDLL:
     L.geot_version.restype = i32
     for name in ("geot_segment_reduce", "geot_segment_reduce_with", "geot_gather_scatter",
                  "geot_gather_scatter_with", "geot_select", "geot_index_stats", "geot_check_index",
-                 "geot_last_choice", "geot_profile_begin", "geot_profile_end"):
+                 "geot_last_choice", "geot_profile_begin", "geot_profile_end", "geot_release_scratch"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -119,6 +120,26 @@ def _stream(device) -> int:
     return torch.cuda.current_stream(device).cuda_stream
 
 
+class _OnDevice:
+    """Make `device` current for the call (cheap when it already is)."""
+
+    __slots__ = ("idx", "prev")
+
+    def __init__(self, device):
+        self.idx = device.index if device.index is not None else torch.cuda.current_device()
+
+    def __enter__(self):
+        self.prev = torch.cuda.current_device()
+        if self.prev != self.idx:
+            torch.cuda.set_device(self.idx)
+        return self
+
+    def __exit__(self, *exc):
+        if self.prev != self.idx:
+            torch.cuda.set_device(self.prev)
+        return False
+
+
 def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str = "sum",
                    out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
     """out[s] = reduce over rows i of src with index[i] == s (geot_segment_reduce)."""
@@ -136,7 +157,7 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
         if tuple(out.shape) != (S, F):
             raise ValueError("out must be [num_segments, F]")
     c = _choice(choice)
-    with torch.cuda.device(src.device):
+    with _OnDevice(src.device):
         st = lib().geot_segment_reduce_with(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
                                             OPS[reduce], out.data_ptr(), _stream(src.device),
                                             ctypes.byref(c) if c is not None else None)
@@ -166,7 +187,7 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
             raise ValueError("out must be [num_rows, F]")
     c = _choice(choice)
     wp = weight.data_ptr() if weight is not None else None
-    with torch.cuda.device(x.device):
+    with _OnDevice(x.device):
         st = lib().geot_gather_scatter_with(x.data_ptr(), x.shape[0], col.data_ptr(), wp,
                                             row.data_ptr(), row.numel(), R, F, OPS[reduce],
                                             out.data_ptr(), _stream(x.device),
@@ -179,7 +200,7 @@ def index_stats(index: torch.Tensor, num_segments: int) -> dict:
     """Segment-length statistics of a sorted index (geot_index_stats; synchronizes)."""
     _dev(index, "index", torch.int64, 1)
     o = IndexStats()
-    with torch.cuda.device(index.device):
+    with _OnDevice(index.device):
         st = lib().geot_index_stats(index.data_ptr(), index.numel(), int(num_segments),
                                     ctypes.byref(o), _stream(index.device))
     _raise(st)
@@ -194,7 +215,7 @@ def check_index(index: torch.Tensor, num_segments: int, col: torch.Tensor | None
     if col is not None:
         _dev(col, "col", torch.int64, 1)
         cp = col.data_ptr()
-    with torch.cuda.device(index.device):
+    with _OnDevice(index.device):
         return int(lib().geot_check_index(index.data_ptr(), index.numel(), int(num_segments), cp,
                                           int(num_x_rows), _stream(index.device)))
 
@@ -227,6 +248,11 @@ def profile_end(capacity: int = 4096) -> list:
     n = ctypes.c_int32()
     _raise(lib().geot_profile_end(buf, capacity, ctypes.byref(n)))
     return [float(buf[i]) for i in range(min(n.value, capacity))]
+
+
+def release_scratch():
+    """Free the library's cached per-stream temporary buffers (geot_release_scratch)."""
+    _raise(lib().geot_release_scratch())
 
 
 def version() -> int:

@@ -247,3 +247,30 @@ def test_profile_hooks_record_main_kernel_time():
         geot.segment_reduce(s, i, 5000, "sum")
     ms = geot.profile_end()
     assert len(ms) == 3 and all(0.0 < t < 1000.0 for t in ms)
+
+
+def test_two_streams_and_scratch_release():
+    """Calls on two streams in flight use separate cached buffers; releasing them and
+    calling again gives the same results."""
+    p = random_problem(55, 300000, 2000, 32, "lognormal", "normal", 0.05)
+    q = random_problem(56, 200000, 1500, 32, "zipf", "normal", 0.05)
+    sp, ip = up(p["src"]), up(p["index"])
+    sq, iq = up(q["src"]), up(q["index"])
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    outs = []
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            a = geot.segment_reduce(sp, ip, 2000, "sum")
+        with torch.cuda.stream(s2):
+            b = geot.segment_reduce(sq, iq, 1500, "max")
+        outs.append((a, b))
+    torch.cuda.synchronize()
+    ref_a, terms_a = oracle_segment(p["src"], p["index"], 2000, "sum")
+    ref_b, _ = oracle_segment(q["src"], q["index"], 1500, "max")
+    for a, b in outs:
+        compare(a.cpu().numpy(), ref_a, "sum", terms_a, "stream 1")
+        compare(b.cpu().numpy(), ref_b, "max", None, "stream 2")
+    geot.release_scratch()
+    a = geot.segment_reduce(sp, ip, 2000, "sum").cpu().numpy()
+    assert np.array_equal(a, outs[0][0].cpu().numpy())
