@@ -71,14 +71,20 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         if (MODE == SRC_PIECES && n == 0) return;     // only empty partials: stored elsewhere
         if (seg < 0 || (int64_t)seg >= a.S) return;   // out-of-range id: skip the store
         float *o = a.out + (int64_t)seg * a.ld_out;
-        const float fn = (float)n;
+        if (a.mean) {  // uniform across the grid: a scalar branch, no division on the sum path
+            const float fn = (float)n;
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-            if (!cv[j]) continue;
-            float t[V];
+            for (int j = 0; j < NT; ++j) {
+                if (!cv[j]) continue;
+                float t[V];
 #pragma unroll
-            for (int k = 0; k < V; ++k) t[k] = a.mean ? v[j * V + k] / fn : v[j * V + k];
-            store_vec<V>(o + cb[j], t);
+                for (int k = 0; k < V; ++k) t[k] = v[j * V + k] / fn;
+                store_vec<V>(o + cb[j], t);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                if (cv[j]) store_vec<V>(o + cb[j], v + j * V);
         }
     };
     auto fill_empty = [&](int64_t s_lo, int64_t s_hi) {  // segments [s_lo, s_hi) have no rows
@@ -208,12 +214,17 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                         wt[u] = nw[u];
                         c = nc[u];
                     }
+                    // an out-of-range column reads row 0 and contributes the neutral value
                     const bool ok = (uint64_t)c < (uint64_t)a.num_x_rows;
-                    const float *p = a.src + c * a.ld_src;
+                    const float *p = a.src + (ok ? c : 0) * a.ld_src;
 #pragma unroll
                     for (int j = 0; j < NT; ++j) {
-                        if (cv[j] && ok) {
+                        if (cv[j]) {
                             load_vec<V>(p + cb[j], x[u] + j * V);
+                            if (!ok) {
+#pragma unroll
+                                for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
+                            }
                         } else {
 #pragma unroll
                             for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
