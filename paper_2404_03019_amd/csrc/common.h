@@ -68,6 +68,45 @@ __device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int delta) {
 __device__ __forceinline__ int32_t shfl_up_cnt(int32_t v, int delta) { return shfl_up_i(v, delta); }
 __device__ __forceinline__ int64_t shfl_up_cnt(int64_t v, int delta) { return shfl_up_i64(v, delta); }
 
+// DPP lane moves (GFX9 encodings): row_shr:S shifts within each 16-lane row;
+// row_bcast:15 / row_bcast:31 broadcast lane 15 of a row (lane 31) to the
+// next row (rows 2 and 3). Lanes whose source does not exist keep their own
+// value; callers decide by lane position which lanes use the result.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(v, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __int_as_float(dpp_i<CTRL, ROW_MASK>(__float_as_int(v)));
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int32_t dpp_cnt(int32_t v) {
+    return dpp_i<CTRL, ROW_MASK>(v);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int64_t dpp_cnt(int64_t v) {
+    const int lo = dpp_i<CTRL, ROW_MASK>((int)(uint32_t)(uint64_t)v);
+    const int hi = dpp_i<CTRL, ROW_MASK>((int)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+}
+
+constexpr int kDppRowShr = 0x110;     // + shift (1..15)
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+__device__ __forceinline__ float shfl_f(float v, int src) { return __shfl(v, src, 64); }
+__device__ __forceinline__ int shfl_i(int v, int src) { return __shfl(v, src, 64); }
+__device__ __forceinline__ int32_t shfl_cnt(int32_t v, int src) { return __shfl(v, src, 64); }
+__device__ __forceinline__ int64_t shfl_cnt(int64_t v, int src) {
+    const int lo = __shfl((int)(uint32_t)(uint64_t)v, src, 64);
+    const int hi = __shfl((int)(uint32_t)((uint64_t)v >> 32), src, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+}
+
 __device__ __forceinline__ float shfl_down_f(float v, int delta) {
     return __shfl_down(v, (unsigned)delta, 64);
 }

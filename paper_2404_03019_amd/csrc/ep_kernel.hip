@@ -10,8 +10,10 @@
 // Section III-B, with the N-loop held in registers). The first and last
 // segment of each run are then combined across the row groups of the block
 // by a segmented scan (the paper's parallel reduction, Algorithm 1, recast):
-// a Hillis-Steele scan over row groups inside each wave with lane shuffles,
-// and across the four waves through LDS. A segment that crosses the block's
+// inside each wave, DPP row shifts scan the groups of every 16-lane row and
+// DPP row broadcasts (or lane shuffles, when a group spans several lanes)
+// carry the rows into each other; across the four waves the scan goes
+// through LDS. A segment that crosses the block's
 // first or last row leaves one partial per block side ("lo" and "hi"); these
 // partials are themselves a sorted list of rows with counts, and the same
 // kernel reduces them at the next level until one block remains. No atomics,
@@ -302,20 +304,74 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     Cnt n = has_rows ? accn : 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) v[k] = acc[k];
-#pragma unroll
-    for (int d = 1; d < GW; d <<= 1) {
-        const int fo = shfl_up_i((int)f, d * L);
-        const Cnt no = shfl_up_cnt(n, d * L);
-        float vo[NV];
-#pragma unroll
-        for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], d * L);
-        if (gw >= d) {
+    // (f, v, n) absorbs the element (fo, vo, no) of an earlier group when `take`
+    auto absorb = [&](bool take, int fo, const float *vo, Cnt no) {
+        if (take) {
             if (!f) {
 #pragma unroll
                 for (int k = 0; k < NV; ++k) v[k] = red_apply<RED>(vo[k], v[k]);
                 n += no;
             }
-            f = f || fo;
+            f = f || (fo != 0);
+        }
+    };
+    // DPP step inside 16-lane rows: take the group S lanes below, if it is in this row
+    auto dpp_row_step = [&](auto shift_tag) {
+        constexpr int S = decltype(shift_tag)::value;
+        float vo[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowShr + S, 0xf>(v[k]);
+        const int fo = dpp_i<kDppRowShr + S, 0xf>((int)f);
+        const Cnt no = dpp_cnt<kDppRowShr + S, 0xf>(n);
+        absorb((lane & 15) >= S, fo, vo, no);
+    };
+    if constexpr (L < 16) {
+        // 1. segmented scan of the groups of each 16-lane row with DPP row shifts
+        if constexpr (1 * L < 16) dpp_row_step(std::integral_constant<int, 1 * L>{});
+        if constexpr (2 * L < 16) dpp_row_step(std::integral_constant<int, 2 * L>{});
+        if constexpr (4 * L < 16) dpp_row_step(std::integral_constant<int, 4 * L>{});
+        if constexpr (8 * L < 16) dpp_row_step(std::integral_constant<int, 8 * L>{});
+        // 2. rows absorb the last group of earlier rows
+        const int row = lane >> 4;
+        if constexpr (L == 1) {
+            {   // lane 15 -> row 1, lane 47 -> row 3
+                float vo[NV];
+#pragma unroll
+                for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowBcast15, 0xa>(v[k]);
+                const int fo = dpp_i<kDppRowBcast15, 0xa>((int)f);
+                const Cnt no = dpp_cnt<kDppRowBcast15, 0xa>(n);
+                absorb((row & 1) != 0, fo, vo, no);
+            }
+            {   // lane 31 -> rows 2 and 3
+                float vo[NV];
+#pragma unroll
+                for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowBcast31, 0xc>(v[k]);
+                const int fo = dpp_i<kDppRowBcast31, 0xc>((int)f);
+                const Cnt no = dpp_cnt<kDppRowBcast31, 0xc>(n);
+                absorb(row >= 2, fo, vo, no);
+            }
+        } else {
+#pragma unroll
+            for (int dr = 1; dr <= 2; dr <<= 1) {   // previous row, then two rows back
+                const int src = max(row - dr, 0) * 16 + 16 - L + gl;
+                float vo[NV];
+#pragma unroll
+                for (int k = 0; k < NV; ++k) vo[k] = shfl_f(v[k], src);
+                const int fo = shfl_i((int)f, src);
+                const Cnt no = shfl_cnt(n, src);
+                absorb(row >= dr, fo, vo, no);
+            }
+        }
+    } else {
+        // groups of 16 or more lanes: Hillis-Steele over groups with lane shuffles
+#pragma unroll
+        for (int d = 1; d < GW; d <<= 1) {
+            const int fo = shfl_up_i((int)f, d * L);
+            const Cnt no = shfl_up_cnt(n, d * L);
+            float vo[NV];
+#pragma unroll
+            for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], d * L);
+            absorb(gw >= d, fo, vo, no);
         }
     }
     if (gw == GW - 1) {

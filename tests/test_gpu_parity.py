@@ -274,3 +274,23 @@ def test_two_streams_and_scratch_release():
     geot.release_scratch()
     a = geot.segment_reduce(sp, ip, 2000, "sum").cpu().numpy()
     assert np.array_equal(a, outs[0][0].cpu().numpy())
+
+
+@pytest.mark.parametrize("lanes", [1, 2, 4, 8, 16, 32, 64])
+def test_scan_every_lane_width_exact(lanes):
+    """One row per row group and very short segments: every lane of every wave sits next to
+    a segment boundary, so the segmented scan (DPP row shifts and broadcasts for narrow
+    groups, lane shuffles for wide ones), the cross-wave LDS step and the partial levels
+    are all exercised. Integer values make sums exact: results must be bit-identical."""
+    rng = np.random.default_rng(200 + lanes)
+    for trial in range(3):
+        L = rng.integers(0, 4, size=6000)            # lengths 0..3: empties everywhere
+        idx = np.repeat(np.arange(L.size, dtype=np.int64), L)
+        F = 4 * lanes if trial == 0 else lanes      # vec 4, then vec 1 (F = lanes)
+        src = rng.integers(-8, 9, size=(idx.size, F)).astype(np.float32)
+        for op in ("sum", "max"):
+            ref = oracle.segment_reduce(src, idx, L.size, op)
+            for rows in (1, 2, 5):
+                ch = dict(family="ep", lanes=lanes, rows=rows)
+                got = run_sr(src, idx, L.size, op, ch)
+                assert np.array_equal(got, ref), f"lanes={lanes} F={F} rows={rows} {op}"
