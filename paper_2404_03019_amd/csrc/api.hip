@@ -103,37 +103,71 @@ struct ScratchGuard {
 // Reduction calls keep their temporary buffer per (device, stream) and reuse it
 // in stream order, growing it (stream-ordered free of the old block, then a new
 // allocation) when a call needs more. Kernels of one stream run in order, so
-// consecutive calls never overlap on the buffer.
+// consecutive calls never overlap on the buffer. The buffer starts with the
+// gap list (two counters and kGapCap records); the counters are zeroed when
+// the buffer is allocated and, after that, by the fill passes themselves.
 struct StreamKey {
     int dev;
     hipStream_t st;
     bool operator<(const StreamKey &o) const { return dev != o.dev ? dev < o.dev : st < o.st; }
 };
+struct StreamCtx {
+    void *p = nullptr;
+    size_t bytes = 0;
+    int parity = 0;
+    bool dirty = false;  // a launch failed after the gap list was handed out
+};
 std::mutex g_cache_mu;
-std::map<StreamKey, std::pair<void *, size_t>> g_cache;
+std::map<StreamKey, StreamCtx> g_cache;
 
-geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **p) {
-    *p = nullptr;
-    if (bytes == 0) return GEOT_SUCCESS;
+constexpr size_t kGapHeader = 256;
+constexpr size_t kGapArea = kGapHeader + (size_t)kGapCap * 3 * sizeof(int64_t);
+
+// `user` gets `bytes` of scratch after the gap list; `g` the list of this call.
+geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList *g,
+                             StreamCtx **ctx_out) {
+    *user = nullptr;
     int dev = 0;
     GEOT_HIP(hipGetDevice(&dev), "hipGetDevice");
     std::lock_guard<std::mutex> lk(g_cache_mu);
-    auto &e = g_cache[StreamKey{dev, st}];
-    if (e.second < bytes) {
-        if (e.first) {
-            GEOT_HIP(hipFreeAsync(e.first, st), "hipFreeAsync");
-            e.first = nullptr;
-            e.second = 0;
+    StreamCtx &e = g_cache[StreamKey{dev, st}];
+    const size_t need = kGapArea + ((bytes + 255) & ~(size_t)255);
+    bool fresh = false;
+    if (e.bytes < need) {
+        if (e.p) {
+            GEOT_HIP(hipFreeAsync(e.p, st), "hipFreeAsync");
+            e.p = nullptr;
+            e.bytes = 0;
         }
-        const size_t grown = std::max(bytes, e.second + e.second / 2);
+        const size_t grown = std::max(need, e.bytes + e.bytes / 2);
         void *q = nullptr;
         geot_status_t s = scratch_alloc(&q, grown, st);
         if (s != GEOT_SUCCESS) return s;
-        e.first = q;
-        e.second = grown;
+        e.p = q;
+        e.bytes = grown;
+        fresh = true;
     }
-    *p = e.first;
+    if (fresh || e.dirty) {
+        GEOT_HIP(launch_zero_u64((unsigned long long *)e.p, kGapHeader / 8, st), "launch zero kernel");
+        e.dirty = false;
+    }
+    unsigned *ctrl = (unsigned *)e.p;
+    g->count = ctrl + e.parity;
+    g->other = ctrl + (1 - e.parity);
+    g->rec = (int64_t *)((char *)e.p + kGapHeader);
+    e.parity ^= 1;
+    *user = bytes ? (char *)e.p + kGapArea : nullptr;
+    *ctx_out = &e;
     return GEOT_SUCCESS;
+}
+
+// Marks the context so the next call re-zeroes the gap counters.
+geot_status_t poison(StreamCtx *ctx, geot_status_t s) {
+    if (s != GEOT_SUCCESS && ctx) {
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        ctx->dirty = true;
+    }
+    return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -348,6 +382,11 @@ int64_t piece_rows_k(int64_t n, int64_t G) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
+                            char *base, const std::vector<size_t> &off_v,
+                            const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
+                            int64_t ld_p, GapList gaps, hipStream_t st);
+
 geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
     const int64_t G = kBlock / r.L;
     const int64_t TW = (int64_t)r.L * r.V * r.NT;
@@ -373,9 +412,18 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
         bytes = align256(bytes + (size_t)lv[l].n * 8);
     }
     void *scratch = nullptr;
-    geot_status_t s = stream_scratch(bytes, st, &scratch);
+    GapList gaps;
+    StreamCtx *ctx = nullptr;
+    geot_status_t s = stream_scratch(bytes, st, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
-    char *base = (char *)scratch;
+    s = poison(ctx, run_ep_levels(p, r, lv, (char *)scratch, off_v, off_s, off_c, ld_p, gaps, st));
+    return s;
+}
+
+geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
+                            char *base, const std::vector<size_t> &off_v,
+                            const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
+                            int64_t ld_p, GapList gaps, hipStream_t st) {
     const int red = p.op == GEOT_OP_MAX ? RED_MAX : RED_SUM;
     for (size_t l = 0; l < lv.size(); ++l) {
         EpArgs a;
@@ -388,6 +436,7 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
             a.w = p.w;
             a.num_x_rows = p.num_x_rows;
             a.fill_gaps = 1;
+            a.gaps = gaps;
         } else {
             a.src = (const float *)(base + off_v[l]);
             a.ld_src = ld_p;
@@ -415,16 +464,29 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
         if (prof) GEOT_HIP(hipEventRecord(e0, st), "hipEventRecord");
         GEOT_HIP(launch_ep(a, red, mode, r.V, r.NT, r.L, lv[l].nchunks, st), "launch element-parallel kernel");
         if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
+        if (l == 0)
+            GEOT_HIP(launch_gap_fill_rows(p.out, p.F, p.F, r.V, (int64_t)r.L * r.V * r.NT, p.S, gaps, st),
+                     "launch gap fill kernel");
     }
     return GEOT_SUCCESS;
 }
 
+geot_status_t run_sp_kernels(const Problem &p, const Resolved &r, int64_t *off, GapList gaps,
+                             hipStream_t st);
+
 geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
     void *scratch = nullptr;
-    geot_status_t s = stream_scratch((size_t)(p.S + 1) * 8, st, &scratch);
+    GapList gaps;
+    StreamCtx *ctx = nullptr;
+    geot_status_t s = stream_scratch((size_t)(p.S + 1) * 8, st, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
-    int64_t *off = (int64_t *)scratch;
-    GEOT_HIP(launch_offsets(p.idx, p.nnz, p.S, off, st), "launch offsets kernel");
+    return poison(ctx, run_sp_kernels(p, r, (int64_t *)scratch, gaps, st));
+}
+
+geot_status_t run_sp_kernels(const Problem &p, const Resolved &r, int64_t *off, GapList gaps,
+                             hipStream_t st) {
+    GEOT_HIP(launch_offsets(p.idx, p.nnz, p.S, off, gaps, st), "launch offsets kernel");
+    GEOT_HIP(launch_gap_fill_i64(off, p.S + 1, gaps, st), "launch gap fill kernel");
     SpArgs a;
     memset(&a, 0, sizeof(a));
     a.src = p.src;
@@ -550,23 +612,25 @@ geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t
         return GEOT_SUCCESS;
     }
     hipStream_t st = (hipStream_t)stream;
-    ScratchGuard sg;
-    sg.st = st;
     const size_t off_bytes = align256((size_t)(num_segments + 1) * 8);
-    geot_status_t s = scratch_alloc(&sg.p, off_bytes + 64, st);
+    void *scratch = nullptr;
+    GapList gaps;
+    StreamCtx *ctx = nullptr;
+    geot_status_t s = stream_scratch(off_bytes + 64, st, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
-    int64_t *off = (int64_t *)sg.p;
-    unsigned long long *acc = (unsigned long long *)((char *)sg.p + off_bytes);
-    GEOT_HIP(launch_offsets(sorted_index, nnz, num_segments, off, st), "launch offsets kernel");
-    GEOT_HIP(launch_zero_u64(acc, 3, st), "launch zero kernel");
-    GEOT_HIP(launch_len_stats(off, num_segments, acc, st), "launch length statistics kernel");
+    int64_t *off = (int64_t *)scratch;
+    unsigned long long *acc = (unsigned long long *)((char *)scratch + off_bytes);
     unsigned long long h[3] = {0, 0, 0};
-    GEOT_HIP(hipMemcpyAsync(h, acc, sizeof(h), hipMemcpyDeviceToHost, st), "hipMemcpyAsync");
-    void *p_free = sg.p;
-    sg.p = nullptr;
-    s = scratch_free(p_free, st);
+    s = poison(ctx, [&]() -> geot_status_t {
+        GEOT_HIP(launch_offsets(sorted_index, nnz, num_segments, off, gaps, st), "launch offsets kernel");
+        GEOT_HIP(launch_gap_fill_i64(off, num_segments + 1, gaps, st), "launch gap fill kernel");
+        GEOT_HIP(launch_zero_u64(acc, 3, st), "launch zero kernel");
+        GEOT_HIP(launch_len_stats(off, num_segments, acc, st), "launch length statistics kernel");
+        GEOT_HIP(hipMemcpyAsync(h, acc, sizeof(h), hipMemcpyDeviceToHost, st), "hipMemcpyAsync");
+        GEOT_HIP(hipStreamSynchronize(st), "hipStreamSynchronize");
+        return GEOT_SUCCESS;
+    }());
     if (s != GEOT_SUCCESS) return s;
-    GEOT_HIP(hipStreamSynchronize(st), "hipStreamSynchronize");
     o.sum_len_sq = (int64_t)h[0];
     o.max_len = (int64_t)h[1];
     o.num_empty = (int64_t)h[2];
@@ -609,11 +673,11 @@ geot_status_t geot_release_scratch(void) {
     std::lock_guard<std::mutex> lk(g_cache_mu);
     geot_status_t st = GEOT_SUCCESS;
     for (auto &kv : g_cache) {
-        if (!kv.second.first) continue;
+        if (!kv.second.p) continue;
         int cur = 0;
         hipError_t e = hipGetDevice(&cur);
         if (e == hipSuccess) e = hipSetDevice(kv.first.dev);
-        if (e == hipSuccess) e = hipFreeAsync(kv.second.first, kv.first.st);
+        if (e == hipSuccess) e = hipFreeAsync(kv.second.p, kv.first.st);
         if (e == hipSuccess) e = hipStreamSynchronize(kv.first.st);
         (void)hipSetDevice(cur);
         if (e != hipSuccess && st == GEOT_SUCCESS) st = hip_fail(e, "release scratch");

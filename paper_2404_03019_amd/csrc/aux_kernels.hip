@@ -18,17 +18,59 @@ __global__ __launch_bounds__(256) void fill_kernel(float *out, int64_t rows, int
 
 // off[s] = first row i with idx[i] >= s. Row i writes the starts of every
 // segment in (idx[i-1], idx[i]] (so empty segments get the next start), and
-// the last row also writes (idx[n-1], S] = n.
+// the last row also writes (idx[n-1], S] = n. Runs longer than kGapRun go to
+// the gap list instead (value = the row they start at).
 __global__ __launch_bounds__(256) void offsets_kernel(const int64_t *idx, int64_t n, int64_t S,
-                                                      int64_t *off) {
+                                                      int64_t *off, GapList gaps) {
+    auto put = [&](int64_t lo, int64_t hi, int64_t row) {  // off[lo, hi) = row
+        lo = max(lo, (int64_t)0);
+        hi = min(hi, S + 1);
+        if (hi - lo > kGapRun && gap_push(gaps, lo, hi, row, 0, 0, 1)) return;
+        for (int64_t t = lo; t < hi; ++t) off[t] = row;
+    };
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t s = idx[i];
         const int64_t sp = i > 0 ? idx[i - 1] : -1;
-        const int64_t hi = min(s, S);
-        for (int64_t t = max(sp + 1, (int64_t)0); t <= hi; ++t) off[t] = i;
-        if (i == n - 1)
-            for (int64_t t = max(s + 1, (int64_t)0); t <= S; ++t) off[t] = n;
+        if (s != sp) put(sp + 1, s + 1, i);
+        if (i == n - 1) put(s + 1, S + 1, n);
+    }
+}
+
+// One block per record at a time: rows [first, end) of the record's column tile = 0.
+template <int V>
+__global__ __launch_bounds__(256) void gap_fill_rows_kernel(float *out, int64_t F, int64_t ld,
+                                                            int64_t tw, int64_t rows, GapList g) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *g.other = 0u;
+    const unsigned cnt = min(*g.count, kGapCap);
+    float z[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) z[k] = 0.0f;
+    for (unsigned q = blockIdx.x; q < cnt; q += gridDim.x) {
+        const int64_t *r = g.rec + 3 * (int64_t)q;
+        const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], rows);
+        const int64_t c0 = r[2] * tw;
+        const int64_t ncol = min(tw, F - c0);
+        if (hi <= lo || c0 < 0 || ncol <= 0) continue;
+        const int nvec = (int)((ncol + V - 1) / V);
+        int tpr = 1;                                  // threads per row (power of two)
+        while (tpr < nvec && tpr < 256) tpr <<= 1;
+        const int rows_per_pass = 256 / tpr;
+        const int j0 = threadIdx.x % tpr;
+        for (int64_t row = lo + threadIdx.x / tpr; row < hi; row += rows_per_pass) {
+            float *o = out + row * ld + c0;
+            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void gap_fill_i64_kernel(int64_t *arr, int64_t len, GapList g) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *g.other = 0u;
+    const unsigned cnt = min(*g.count, kGapCap);
+    for (unsigned q = blockIdx.x; q < cnt; q += gridDim.x) {
+        const int64_t *r = g.rec + 3 * (int64_t)q;
+        const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], len), v = r[2];
+        for (int64_t t = lo + threadIdx.x; t < hi; t += 256) arr[t] = v;
     }
 }
 
@@ -110,11 +152,29 @@ hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float va
     return hipGetLastError();
 }
 
-hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off,
+hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
                           hipStream_t stream) {
     if (n <= 0) return hipErrorInvalidValue;
     hipLaunchKernelGGL(offsets_kernel, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
-                       idx, n, S, off);
+                       idx, n, S, off, gaps);
+    return hipGetLastError();
+}
+
+// 1024 blocks: a list with many records keeps the chip busy, an empty list
+// costs one counter read per block.
+hipError_t launch_gap_fill_rows(float *out, int64_t F, int64_t ld, int V, int64_t tw, int64_t rows,
+                                GapList gaps, hipStream_t stream) {
+    if (V == 4)
+        hipLaunchKernelGGL(gap_fill_rows_kernel<4>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+    else if (V == 2)
+        hipLaunchKernelGGL(gap_fill_rows_kernel<2>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+    else
+        hipLaunchKernelGGL(gap_fill_rows_kernel<1>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+    return hipGetLastError();
+}
+
+hipError_t launch_gap_fill_i64(int64_t *arr, int64_t len, GapList gaps, hipStream_t stream) {
+    hipLaunchKernelGGL(gap_fill_i64_kernel, dim3(1024), dim3(256), 0, stream, arr, len, gaps);
     return hipGetLastError();
 }
 

@@ -68,6 +68,30 @@ __device__ __forceinline__ int64_t shfl_up_i64(int64_t v, int delta) {
 __device__ __forceinline__ int32_t shfl_up_cnt(int32_t v, int delta) { return shfl_up_i(v, delta); }
 __device__ __forceinline__ int64_t shfl_up_cnt(int64_t v, int delta) { return shfl_up_i64(v, delta); }
 
+// Appends the run of segments [lo, hi) (value carried along) to a gap list,
+// cut into records of at most kGapChunk segments. `lanes` lanes starting at
+// lane `lead` (all in the same state) call it together; the lead lane takes
+// the slots and the lanes share the writes. Returns false when the list is
+// full: the caller then writes the run itself (the slots it took hold empty
+// records).
+__device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t hi, int64_t value,
+                                         int lead, int lane_in, int lanes) {
+    const int64_t nrec = (hi - lo + kGapChunk - 1) / kGapChunk;
+    unsigned base = 0;
+    if (lane_in == 0) base = atomicAdd(g.count, (unsigned)nrec);
+    if (lanes > 1) base = (unsigned)__shfl((int)base, lead, 64);
+    const bool fits = (int64_t)base + nrec <= (int64_t)kGapCap;
+    const int64_t end = fits ? nrec : ((int64_t)kGapCap > (int64_t)base ? (int64_t)kGapCap - base : 0);
+    for (int64_t q = lane_in; q < end; q += lanes) {
+        int64_t *r = g.rec + 3 * ((int64_t)base + q);
+        const int64_t a = fits ? lo + q * kGapChunk : 0;
+        r[0] = a;
+        r[1] = fits ? min(hi, a + kGapChunk) : 0;
+        r[2] = value;
+    }
+    return fits;
+}
+
 // DPP lane moves (GFX9 encodings): row_shr:S shifts within each 16-lane row;
 // row_bcast:15 / row_bcast:31 broadcast lane 15 of a row (lane 31) to the
 // next row (rows 2 and 3). Lanes whose source does not exist keep their own

@@ -89,9 +89,14 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 if (cv[j]) store_vec<V>(o + cb[j], v + j * V);
         }
     };
-    auto fill_empty = [&](int64_t s_lo, int64_t s_hi) {  // segments [s_lo, s_hi) have no rows
+    // Segments [s_lo, s_hi) have no rows. Short runs are written here by the row
+    // group; a longer run goes to the gap list (written afterwards by a grid-wide
+    // pass). All lanes of a row group take the same path.
+    const int gbase_fill = gw * L;
+    auto fill_empty = [&](int64_t s_lo, int64_t s_hi) {
         s_lo = max(s_lo, (int64_t)0);
         s_hi = min(s_hi, a.S);
+        if (s_hi - s_lo > kGapRun && gap_push(a.gaps, s_lo, s_hi, tile, gbase_fill, gl, L)) return;
         float z[V];
 #pragma unroll
         for (int k = 0; k < V; ++k) z[k] = 0.0f;

@@ -18,6 +18,21 @@ enum SrcMode : int {
 
 enum RedOp : int { RED_SUM = 0, RED_MAX = 1 };  // mean = sum, divided by the count on store
 
+// Runs of empty segments longer than kGapRun segments are not written by the
+// kernel that finds them: it appends them to a device list, cut into records
+// of at most kGapChunk segments, and a grid-wide pass writes them afterwards.
+// The list counter alternates between two words from call to call; the fill
+// pass of one call zeroes the other word, so no memset is ever needed.
+constexpr int kGapRun = 32;
+constexpr int64_t kGapChunk = 8192;
+constexpr unsigned kGapCap = 8192;
+
+struct GapList {
+    unsigned int *count;   // records appended in this call
+    unsigned int *other;   // the counter of the next call (zeroed by this call's fill pass)
+    int64_t *rec;          // [kGapCap][3]: first segment, end segment, value
+};
+
 // Arguments of one element-parallel pass (level 0 over the input rows, or a
 // later level over the partials of segments that crossed block boundaries).
 struct EpArgs {
@@ -41,6 +56,7 @@ struct EpArgs {
     int32_t ntiles;         // column tiles (blocks per chunk)
     int32_t mean;           // divide by the count when a segment is stored
     int32_t fill_gaps;      // write empty segments (level 0 only)
+    GapList gaps;           // long runs of empty segments (level 0 only)
 };
 
 hipError_t launch_ep(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
@@ -66,7 +82,17 @@ struct SpArgs {
 hipError_t launch_sp(const SpArgs &a, int red, int mode, int V, int NT, int L, hipStream_t stream);
 
 // off[s] = first row with idx >= s for s in [0, S]; one pass over the index.
-hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, hipStream_t stream);
+// Long runs go to `gaps` (value = the row they start at): run launch_gap_fill_i64 after.
+hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
+                          hipStream_t stream);
+
+// Grid-wide passes over a gap list: out rows [first, end) = 0 in the columns of
+// tile `value` (tiles of `tw` columns), or arr[first, end) = value. Both zero
+// the other call's counter.
+// Records are clamped to the `rows` (or `len`) of the current call.
+hipError_t launch_gap_fill_rows(float *out, int64_t F, int64_t ld, int V, int64_t tw, int64_t rows,
+                                GapList gaps, hipStream_t stream);
+hipError_t launch_gap_fill_i64(int64_t *arr, int64_t len, GapList gaps, hipStream_t stream);
 
 // out[0 .. rows*ld) = value for the first F columns of each row.
 hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float value, hipStream_t stream);

@@ -294,3 +294,26 @@ def test_scan_every_lane_width_exact(lanes):
                 ch = dict(family="ep", lanes=lanes, rows=rows)
                 got = run_sr(src, idx, L.size, op, ch)
                 assert np.array_equal(got, ref), f"lanes={lanes} F={F} rows={rows} {op}"
+
+
+def test_long_runs_of_empty_segments():
+    """Outputs that are mostly empty: long leading, interior and trailing runs of empty
+    segments (filled by whole blocks), and blocks with more long runs than their queue
+    holds (the rest filled by the row group)."""
+    rng = np.random.default_rng(57)
+    cases = []
+    # few rows over many segments, one huge trailing run
+    cases.append((np.sort(rng.integers(1000, 5000, 3000)).astype(np.int64), 400000, 8))
+    # rows spaced ~40 segments apart: every boundary is a long run
+    cases.append((np.cumsum(rng.integers(33, 48, 20000)).astype(np.int64), 1000000, 4))
+    # one row in the middle of a million segments
+    cases.append((np.array([500000], dtype=np.int64), 1000000, 32))
+    for idx, S, F in cases:
+        src = rng.standard_normal((idx.size, F)).astype(np.float32)
+        for op in ("sum", "max"):
+            ref, terms = oracle_segment(src, idx, S, op)
+            for ch in (None, dict(family="ep", lanes=1, rows=1), dict(family="ep", rows=1),
+                       dict(family="ep", rows=64), dict(family="sp")):
+                say(f"gaps S={S} nnz={idx.size} F={F} op={op} choice={ch}")
+                got = run_sr(src, idx, S, op, ch)
+                compare(got, ref, op, terms, f"gaps S={S} F={F} {op} {ch}")
