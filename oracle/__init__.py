@@ -16,4 +16,6 @@ from .oracle import (  # noqa: F401
     gather_scatter,
     abs_term_sum,
     index_stats,
+    segment_reduce_backward,
+    gather_scatter_backward,
 )

@@ -26,6 +26,21 @@
  *    without weights the term is x itself;
  *  - the output is overwritten in full (not accumulated into).
  *
+ * Gradients (Section VI names training support as future work; these are the
+ * derivatives of the definition above, written out):
+ *  - segment reduction w.r.t. src: sum copies grad_out[idx[i]] to row i; mean
+ *    divides it by the segment length (fp64 division, rounded once); max
+ *    routes grad_out[s, f] to the first row of segment s (lowest index) whose
+ *    src[i, f] equals out[s, f], every other row gets 0;
+ *  - fused form w.r.t. X: grad_X[c] = sum over edges e with col[e] == c of
+ *    coef(e) * grad_out[row[e]] with coef = w[e] (1 without weights), divided
+ *    by the row's edge count for mean; for max only the first edge of each
+ *    (row, feature) whose rounded product equals out[row, f] contributes;
+ *  - fused form w.r.t. the weights: grad_w[e] = sum over f of
+ *    grad_out[row[e], f] * X[col[e], f] (divided by the count for mean;
+ *    restricted to the features where e is that first edge for max).
+ *  Both accumulate in fp64 and return fp64.
+ *
  * Build: gcc -O2 -fno-fast-math -ffp-contract=off -shared -fPIC.
  * Error codes: 0 ok, 1 invalid argument, 2 index not sorted, 3 index (or
  * column) out of range.
@@ -194,6 +209,99 @@ int oracle_index_stats(const int64_t *idx, int64_t nnz, int64_t S, double *mean,
     *max_len = mx;
     *num_empty = ne;
     *sum_len_sq = sq;
+    free(start);
+    return OR_OK;
+}
+
+/* Gradient of segment reduction w.r.t. src (see the header). src and out are
+ * read for max only. */
+int oracle_segment_reduce_backward(const float *grad_out, const int64_t *idx, int64_t nnz,
+                                   int64_t S, int64_t F, int op, const float *src,
+                                   const float *out, float *grad_src)
+{
+    if (nnz < 0 || S < 0 || F < 0 || op < OR_SUM || op > OR_MAX) return OR_INVALID;
+    if (nnz == 0 || F == 0) return OR_OK;
+    int rc = oracle_check_index(idx, nnz, S);
+    if (rc != OR_OK) return rc;
+    int64_t *start = (int64_t *)malloc((size_t)(S + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(idx, nnz, S, start);
+    for (int64_t s = 0; s < S; ++s) {
+        int64_t b = start[s], e = start[s + 1];
+        for (int64_t f = 0; f < F; ++f) {
+            double g = (double)grad_out[s * F + f];
+            int found = 0;
+            for (int64_t i = b; i < e; ++i) {
+                float r;
+                if (op == OR_SUM) {
+                    r = (float)g;
+                } else if (op == OR_MEAN) {
+                    r = (float)(g / (double)(e - b));
+                } else if (!found && src[i * F + f] == out[s * F + f]) {
+                    r = (float)g;
+                    found = 1;
+                } else {
+                    r = 0.0f;
+                }
+                grad_src[i * F + f] = r;
+            }
+        }
+    }
+    free(start);
+    return OR_OK;
+}
+
+/* Gradients of the fused form w.r.t. X (grad_X, [n_x x F]) and the weights
+ * (grad_w, [nnz]); either may be NULL. With absolute != 0 every term is
+ * replaced by its absolute value (the sums of |terms| that state the
+ * floating-point bound). out is read for max only. */
+int oracle_gather_scatter_backward(const float *X, int64_t n_x, const int64_t *col, const float *w,
+                                   const int64_t *row, int64_t nnz, int64_t R, int64_t F, int op,
+                                   const float *grad_out, const float *out, int absolute,
+                                   double *grad_X, double *grad_w)
+{
+    if (nnz < 0 || R < 0 || F < 0 || n_x < 0 || op < OR_SUM || op > OR_MAX) return OR_INVALID;
+    if (grad_X)
+        for (int64_t i = 0; i < n_x * F; ++i) grad_X[i] = 0.0;
+    if (grad_w)
+        for (int64_t e = 0; e < nnz; ++e) grad_w[e] = 0.0;
+    if (nnz == 0 || F == 0) return OR_OK;
+    int rc = oracle_check_index(row, nnz, R);
+    if (rc != OR_OK) return rc;
+    for (int64_t e = 0; e < nnz; ++e)
+        if (col[e] < 0 || col[e] >= n_x) return OR_OUT_OF_RANGE;
+    int64_t *start = (int64_t *)malloc((size_t)(R + 1) * sizeof(int64_t));
+    if (!start) return OR_INVALID;
+    segment_starts(row, nnz, R, start);
+    for (int64_t r = 0; r < R; ++r) {
+        int64_t b = start[r], e_end = start[r + 1];
+        double cnt = (double)(e_end - b);
+        for (int64_t f = 0; f < F; ++f) {
+            double g = (double)grad_out[r * F + f];
+            int found = 0;
+            for (int64_t e = b; e < e_end; ++e) {
+                double x = (double)X[col[e] * F + f];
+                double coef = w ? (double)w[e] : 1.0;
+                int use = 1;
+                if (op == OR_MAX) {
+                    use = !found && term(X, F, col, w, e, f) == out[r * F + f];
+                    if (use) found = 1;
+                }
+                if (!use) continue;
+                double tx = coef * g, tw = g * x;
+                if (op == OR_MEAN) {
+                    tx /= cnt;
+                    tw /= cnt;
+                }
+                if (absolute) {
+                    tx = fabs(tx);
+                    tw = fabs(tw);
+                }
+                if (grad_X) grad_X[col[e] * F + f] += tx;
+                if (grad_w) grad_w[e] += tw;
+            }
+        }
+    }
     free(start);
     return OR_OK;
 }

@@ -65,8 +65,12 @@ class OracleLib:
         lib.oracle_gather_scatter.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p]
         lib.oracle_abs_term_sum.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p]
         lib.oracle_index_stats.argtypes = [p, i64, i64, p, p, p, p, p]
+        lib.oracle_segment_reduce_backward.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, p]
+        lib.oracle_gather_scatter_backward.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int,
+                                                       p, p, ctypes.c_int, p, p]
         for name in ("oracle_check_index", "oracle_segment_reduce", "oracle_gather_scatter",
-                     "oracle_abs_term_sum", "oracle_index_stats"):
+                     "oracle_abs_term_sum", "oracle_index_stats", "oracle_segment_reduce_backward",
+                     "oracle_gather_scatter_backward"):
             getattr(lib, name).restype = ctypes.c_int
         self._lib = lib
         self.path = path
@@ -121,6 +125,39 @@ class OracleLib:
                                              OPS[op], _ptr(out)))
         return out
 
+    def segment_reduce_backward(self, grad_out, index, op: str = "sum", src=None, out=None):
+        """grad_src of segment_reduce given grad_out [S x F] (src and out needed for max)."""
+        grad_out = _f32(grad_out)
+        index = _i64(index)
+        S, F = grad_out.shape
+        g = np.empty((index.size, F), dtype=np.float32)
+        s_ = None if src is None else _f32(src)
+        o_ = None if out is None else _f32(out)
+        if op == "max" and (s_ is None or o_ is None):
+            raise ValueError("max needs src and out")
+        _check(self._lib.oracle_segment_reduce_backward(_ptr(grad_out), _ptr(index), index.size, S, F,
+                                                        OPS[op], _ptr(s_), _ptr(o_), _ptr(g)))
+        return g
+
+    def gather_scatter_backward(self, X, col, weight, row, grad_out, op: str = "sum", out=None,
+                                absolute: bool = False):
+        """(grad_X [n_x x F] fp64, grad_w [nnz] fp64 or None) of gather_scatter."""
+        X = _f32(X)
+        col = _i64(col)
+        row = _i64(row)
+        w = None if weight is None else _f32(weight)
+        grad_out = _f32(grad_out)
+        o_ = None if out is None else _f32(out)
+        if op == "max" and o_ is None:
+            raise ValueError("max needs out")
+        R, F = grad_out.shape
+        gX = np.empty(X.shape, dtype=np.float64)
+        gw = np.empty(row.size, dtype=np.float64) if w is not None else None
+        _check(self._lib.oracle_gather_scatter_backward(_ptr(X), X.shape[0], _ptr(col), _ptr(w), _ptr(row),
+                                                        row.size, R, F, OPS[op], _ptr(grad_out), _ptr(o_),
+                                                        int(absolute), _ptr(gX), _ptr(gw)))
+        return gX, gw
+
     def index_stats(self, index, num_segments: int) -> dict:
         """mean, population variance, max length, empty count and sum of squared lengths."""
         index = _i64(index)
@@ -164,3 +201,11 @@ def abs_term_sum(rows, index, num_segments, op="sum", col=None, weight=None):
 
 def index_stats(index, num_segments):
     return default().index_stats(index, num_segments)
+
+
+def segment_reduce_backward(grad_out, index, op="sum", src=None, out=None):
+    return default().segment_reduce_backward(grad_out, index, op, src, out)
+
+
+def gather_scatter_backward(X, col, weight, row, grad_out, op="sum", out=None, absolute=False):
+    return default().gather_scatter_backward(X, col, weight, row, grad_out, op, out, absolute)

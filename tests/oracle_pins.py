@@ -307,6 +307,144 @@ def pin_index_stats(impl):
         assert abs(st["var_len"] - L.var()) <= 1e-9 * max(L.var(), 1.0)
 
 
+# ----------------------------------------------------------------------------
+# gradients
+# ----------------------------------------------------------------------------
+def _fd_loss(impl, g, fwd):
+    return float((g.astype(np.float64) * fwd().astype(np.float64)).sum())
+
+
+def pin_backward_finite_differences(impl):
+    """grad = d/d input of sum(grad_out * forward(input)), by central differences of the
+    (independently pinned) forward oracle. Integer data and half steps keep sum exact;
+    mean adds one fp32 rounding; max uses well-separated values so the step never
+    changes which member is largest."""
+    rng = np.random.default_rng(91)
+    for S, F in ((5, 2), (7, 3)):
+        L = rng.integers(0, 5, size=S)
+        idx = np.repeat(np.arange(S), L).astype(np.int64)
+        n = idx.size
+        g = rng.integers(-3, 4, size=(S, F)).astype(np.float32)
+        for op in ("sum", "mean", "max"):
+            if op == "max":
+                src = (rng.permutation(n * F).reshape(n, F) * 4.0).astype(np.float32)
+            else:
+                src = rng.integers(-8, 9, size=(n, F)).astype(np.float32)
+            out = impl.segment_reduce(src, idx, S, op)
+            got = impl.segment_reduce_backward(g, idx, op, src, out)
+            h = 0.5
+            for i in range(n):
+                for f in range(F):
+                    sp, sm = src.copy(), src.copy()
+                    sp[i, f] += h
+                    sm[i, f] -= h
+                    fd = (_fd_loss(impl, g, lambda: impl.segment_reduce(sp, idx, S, op)) -
+                          _fd_loss(impl, g, lambda: impl.segment_reduce(sm, idx, S, op))) / (2 * h)
+                    tol = 1e-6 * (1 + abs(fd)) if op == "mean" else 0.0
+                    assert abs(fd - float(got[i, f])) <= tol, f"segment backward {op} ({i},{f})"
+    # fused form: w.r.t. X and weights (quarter-step weights, integer X: exact products)
+    for weighted in (True, False):
+        R, nx, F = 4, 3, 2
+        L = rng.integers(0, 4, size=R)
+        row = np.repeat(np.arange(R), L).astype(np.int64)
+        n = row.size
+        col = rng.integers(0, nx, n).astype(np.int64)
+        g = rng.integers(-3, 4, size=(R, F)).astype(np.float32)
+        for op in ("sum", "mean", "max"):
+            if op == "max":
+                X = (rng.permutation(nx * F).reshape(nx, F) * 8.0 + 1.0).astype(np.float32)
+                w = (rng.permutation(n) + 1.0).astype(np.float32) if weighted else None
+            else:
+                X = rng.integers(-8, 9, size=(nx, F)).astype(np.float32)
+                w = (rng.integers(-4, 5, n) / 4.0).astype(np.float32) if weighted else None
+            out = impl.gather_scatter(X, col, w, row, R, op)
+            gX, gw = impl.gather_scatter_backward(X, col, w, row, g, op, out)
+            fwd = lambda Xv, wv: impl.gather_scatter(Xv, col, wv, row, R, op)
+            h = 0.125 if op == "max" else 0.5
+            for c in range(nx):
+                for f in range(F):
+                    Xp, Xm = X.copy(), X.copy()
+                    Xp[c, f] += h
+                    Xm[c, f] -= h
+                    fd = (_fd_loss(impl, g, lambda: fwd(Xp, w)) - _fd_loss(impl, g, lambda: fwd(Xm, w))) / (2 * h)
+                    assert abs(fd - gX[c, f]) <= 1e-6 * (1 + abs(fd)), f"gather grad_X {op} ({c},{f})"
+            if weighted:
+                hw = 1.0 / 64 if op == "max" else 0.25
+                for e in range(n):
+                    wp, wm = w.copy(), w.copy()
+                    wp[e] += hw
+                    wm[e] -= hw
+                    fd = (_fd_loss(impl, g, lambda: fwd(X, wp)) - _fd_loss(impl, g, lambda: fwd(X, wm))) / (2 * hw)
+                    assert abs(fd - gw[e]) <= 1e-6 * (1 + abs(fd)), f"gather grad_w {op} e={e}"
+
+
+def pin_backward_max_ties(impl):
+    """With ties, the max gradient is a subgradient: per (segment, feature) it sums to
+    grad_out, goes to one member that attains the max, and (the tie reading) to the
+    lowest-indexed such member. The same for the fused form's X gradient."""
+    rng = np.random.default_rng(95)
+    p = random_problem(96, 4000, 300, 3, "zipf", "int", 0.1)  # values in [-8, 8]: many ties
+    src, idx, S, L = p["src"], p["index"], p["num_segments"], p["lengths"]
+    g = rng.integers(1, 5, size=(S, 3)).astype(np.float32)
+    out = impl.segment_reduce(src, idx, S, "max")
+    got = impl.segment_reduce_backward(g, idx, "max", src, out)
+    starts = np.concatenate([[0], np.cumsum(L)])
+    for s_ in np.flatnonzero(L > 0):
+        seg = src[starts[s_]:starts[s_ + 1]]
+        gs = got[starts[s_]:starts[s_ + 1]]
+        for f in range(3):
+            nz = np.flatnonzero(gs[:, f])
+            assert nz.size == 1 and gs[nz[0], f] == g[s_, f], f"one recipient seg {s_} f {f}"
+            assert seg[nz[0], f] == out[s_, f], f"recipient attains the max seg {s_}"
+            assert nz[0] == np.flatnonzero(seg[:, f] == out[s_, f])[0], f"lowest index seg {s_}"
+    q = random_gather_problem(97, 3000, 200, 40, 2, "zipf", "int", True, 0.1)
+    X, col, w, row, R = q["X"], q["col"], q["weight"], q["index"], q["num_segments"]
+    g = rng.integers(1, 5, size=(R, 2)).astype(np.float32)
+    out = impl.gather_scatter(X, col, w, row, R, "max")
+    gX, gw = impl.gather_scatter_backward(X, col, w, row, g, "max", out)
+    # every (row, feature) routes exactly one term: total |dX| mass = sum_r,f |w_e*| g
+    nonempty = np.bincount(row, minlength=R) > 0
+    msgs = (w[:, None] * X[col]).astype(np.float32)
+    want_total = 0.0
+    starts = np.concatenate([[0], np.cumsum(q["lengths"])])
+    for r in np.flatnonzero(nonempty):
+        for f in range(2):
+            e = starts[r] + np.flatnonzero(msgs[starts[r]:starts[r + 1], f] == out[r, f])[0]
+            want_total += float(w[e]) * float(g[r, f])
+    assert abs(gX.sum() - want_total) <= 1e-9 * max(1.0, abs(want_total)), "fused max recipients"
+
+
+def pin_backward_torch_autograd(impl):
+    """torch's autograd of scatter_reduce / index_select on the CPU (tie-free data)."""
+    import torch
+
+    rng = np.random.default_rng(92)
+    p = random_problem(93, 3000, 200, 5, "zipf", "normal", 0.1)
+    src, idx, S = p["src"], p["index"], p["num_segments"]
+    g = rng.standard_normal((S, 5)).astype(np.float32)
+    for op, tname in (("sum", "sum"), ("mean", "mean"), ("max", "amax")):
+        ts = torch.from_numpy(src.astype(np.float64)).requires_grad_(True)
+        ti = torch.from_numpy(idx)[:, None].expand(-1, 5)
+        o = torch.zeros(S, 5, dtype=torch.float64).scatter_reduce(0, ti, ts, tname, include_self=False)
+        (o * torch.from_numpy(g.astype(np.float64))).sum().backward()
+        out = impl.segment_reduce(src, idx, S, op)
+        got = impl.segment_reduce_backward(g, idx, op, src, out)
+        assert np.allclose(got, ts.grad.numpy(), rtol=1e-6, atol=1e-7), f"torch autograd {op}"
+    q = random_gather_problem(94, 2000, 150, 120, 4, "lognormal", "normal", True, 0.1)
+    X, col, w, row, R = q["X"], q["col"], q["weight"], q["index"], q["num_segments"]
+    g = rng.standard_normal((R, 4)).astype(np.float32)
+    for op, tname in (("sum", "sum"), ("mean", "mean")):
+        tX = torch.from_numpy(X.astype(np.float64)).requires_grad_(True)
+        tw = torch.from_numpy(w.astype(np.float64)).requires_grad_(True)
+        msg = tX[torch.from_numpy(col)] * tw[:, None]
+        ti = torch.from_numpy(row)[:, None].expand(-1, 4)
+        o = torch.zeros(R, 4, dtype=torch.float64).scatter_reduce(0, ti, msg, tname, include_self=False)
+        (o * torch.from_numpy(g.astype(np.float64))).sum().backward()
+        gX, gw = impl.gather_scatter_backward(X, col, w, row, g, op)
+        assert np.allclose(gX, tX.grad.numpy(), rtol=1e-9, atol=1e-9), f"torch grad_X {op}"
+        assert np.allclose(gw, tw.grad.numpy(), rtol=1e-9, atol=1e-9), f"torch grad_w {op}"
+
+
 ALL_PINS = (
     pin_golden,
     pin_bruteforce_segment,
@@ -320,4 +458,7 @@ ALL_PINS = (
     pin_errors,
     pin_abs_term_sum,
     pin_index_stats,
+    pin_backward_finite_differences,
+    pin_backward_max_ties,
+    pin_backward_torch_autograd,
 )

@@ -36,6 +36,12 @@ MUTANTS = {
                          "out[s * F + (F - 1 - f)] = result;"),
     "max_keeps_first": ("if (t > m) m = t;", "if (t > m && i == b) m = t;"),
     "stats_var_unsquared": ("v += d * d;", "v += d;"),
+    "bwd_mean_no_divide": ("r = (float)(g / (double)(e - b));", "r = (float)g;"),
+    "bwd_max_last_member": ("} else if (!found && src[i * F + f] == out[s * F + f]) {",
+                            "} else if (src[i * F + f] == out[s * F + f]) {"),
+    "bwd_grad_w_wrong_factor": ("double tx = coef * g, tw = g * x;", "double tx = coef * g, tw = coef * x;"),
+    "bwd_grad_x_by_row": ("if (grad_X) grad_X[col[e] * F + f] += tx;",
+                          "if (grad_X) grad_X[(r % n_x) * F + f] += tx;"),
 }
 
 RUNNER = r"""
