@@ -149,6 +149,53 @@ geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const
                                        int64_t num_rows, int64_t F, geot_op_t op, float *out,
                                        void *stream, const geot_kernel_choice_t *choice);
 
+/* Gradient of geot_segment_reduce w.r.t. src, for training (Section VI lists
+ * autograd support as future work; this is the derivative of the definition).
+ *   grad_out  [num_segments x F] fp32: gradient of the loss w.r.t. out
+ *   grad_src  [nnz x F] fp32, overwritten
+ *   sum:  grad_src[i, :] = grad_out[sorted_index[i], :]
+ *   mean: grad_src[i, :] = grad_out[s, :] / (rows of segment s), s = sorted_index[i]
+ *   max:  grad_out[s, f] goes to the first row i of segment s (lowest index)
+ *         with src[i, f] == out[s, f]; every other element of grad_src is 0.
+ *         src and out (the forward result) are read for max only (may be NULL
+ *         otherwise).
+ * Sum and max copy values (exact); mean divides once in fp32. Deterministic.
+ * Same argument checks as geot_segment_reduce; grad_src must not overlap the
+ * inputs. Temporary memory: (num_segments + 1) int64 for mean, num_segments *
+ * F uint64 for max, from the per-stream buffer.                              */
+geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
+                                           int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
+                                           const float *src, const float *out, float *grad_src,
+                                           void *stream);
+
+/* Gradients of geot_gather_scatter w.r.t. X and the edge weights. The caller
+ * keeps only the row-sorted edge list: for the X gradient of sum and mean the
+ * library counting-sorts the edges by column into a temporary transposed list
+ * (20 bytes per edge and 12 per X row, from its stream-ordered pool) and runs
+ * the forward gather kernel over it, so every row of grad_X is written without
+ * float atomics; for max only the recipients' terms are added, atomically.
+ *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
+ *   out          [num_rows x F]: the forward result (read for max only)
+ *   grad_X       [num_x_rows x F] fp32 or NULL (skipped), overwritten:
+ *                grad_X[c, :] = sum over edges e with col[e] == c of
+ *                coef(e) * grad_out[sorted_row[e], :], coef = weight[e] (1 when
+ *                weight is NULL), divided by the row's edge count for mean
+ *   grad_weight  [nnz] fp32 or NULL (skipped; must be NULL when weight is
+ *                NULL), overwritten: grad_weight[e] = sum over f of
+ *                grad_out[sorted_row[e], f] * X[col[e], f] (divided by the
+ *                count for mean)
+ *   max: only the first edge of each (row, feature) whose rounded product
+ *        weight[e] * X[col[e], f] equals out[row, f] contributes, in both.
+ * grad_X sums in fp32; the order of the edges inside one column comes from
+ * atomic slot allocation, so it is not bitwise reproducible (within
+ * 1e-5 * sum|terms| + 1e-6). grad_weight is deterministic. X is needed for
+ * grad_weight and for max.                                                   */
+geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,
+                                           const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                           int64_t num_rows, int64_t F, geot_op_t op,
+                                           const float *grad_out, const float *out, float *grad_X,
+                                           float *grad_weight, void *stream);
+
 /* The selector (Section III-C: a decision tree over O(1) input features,
  * compiled to if/else). Pure host function: no device access.
  *   gather  nonzero for geot_gather_scatter, zero for geot_segment_reduce

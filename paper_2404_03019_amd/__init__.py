@@ -14,6 +14,8 @@ from .geot import (  # noqa: F401
     lib,
     segment_reduce,
     gather_scatter,
+    segment_reduce_backward,
+    gather_scatter_backward,
     index_stats,
     check_index,
     select,

@@ -123,7 +123,9 @@ std::map<StreamKey, StreamCtx> g_cache;
 constexpr size_t kGapHeader = 256;
 constexpr size_t kGapArea = kGapHeader + (size_t)kGapCap * 3 * sizeof(int64_t);
 
-// `user` gets `bytes` of scratch after the gap list; `g` the list of this call.
+// `user` gets `bytes` of scratch after the gap list; `g` the list of this call
+// (NULL when the call runs no gap-fill pass: only a call that runs one may take
+// the list, since its fill pass zeroes the next call's counter).
 geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList *g,
                              StreamCtx **ctx_out) {
     *user = nullptr;
@@ -151,11 +153,13 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
         GEOT_HIP(launch_zero_u64((unsigned long long *)e.p, kGapHeader / 8, st), "launch zero kernel");
         e.dirty = false;
     }
-    unsigned *ctrl = (unsigned *)e.p;
-    g->count = ctrl + e.parity;
-    g->other = ctrl + (1 - e.parity);
-    g->rec = (int64_t *)((char *)e.p + kGapHeader);
-    e.parity ^= 1;
+    if (g) {
+        unsigned *ctrl = (unsigned *)e.p;
+        g->count = ctrl + e.parity;
+        g->other = ctrl + (1 - e.parity);
+        g->rec = (int64_t *)((char *)e.p + kGapHeader);
+        e.parity ^= 1;
+    }
     *user = bytes ? (char *)e.p + kGapArea : nullptr;
     *ctx_out = &e;
     return GEOT_SUCCESS;
@@ -570,6 +574,161 @@ geot_status_t geot_gather_scatter(const float *X, int64_t num_x_rows, const int6
                                   void *stream) {
     return geot_gather_scatter_with(X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, op,
                                     out, stream, nullptr);
+}
+
+geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
+                                           int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
+                                           const float *src, const float *out, float *grad_src,
+                                           void *stream) {
+    t_detail.clear();
+    if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
+    if (nnz < 0 || num_segments < 0 || F < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (nnz == 0 || F == 0) return GEOT_SUCCESS;
+    if (num_segments == 0) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments is 0 but nnz > 0");
+    if (num_segments > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments must be < 2^31");
+    const int64_t kMax = (int64_t)1 << 62;
+    if (F > ((int64_t)1 << 31) || num_segments > kMax / F || nnz > kMax / F)
+        return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
+    if (!grad_out || !sorted_index || !grad_src) return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
+    if (op == GEOT_OP_MAX && (!src || !out)) return fail(GEOT_ERROR_INVALID_VALUE, "max needs src and out");
+    const size_t gb = (size_t)(nnz * F) * 4;
+    if (overlaps(grad_src, gb, grad_out, (size_t)(num_segments * F) * 4) ||
+        overlaps(grad_src, gb, sorted_index, (size_t)nnz * 8) || overlaps(grad_src, gb, src, gb) ||
+        overlaps(grad_src, gb, out, op == GEOT_OP_MAX ? (size_t)(num_segments * F) * 4 : 0))
+        return fail(GEOT_ERROR_INVALID_VALUE, "grad_src overlaps an input");
+    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)grad_src |
+                           (op == GEOT_OP_MAX ? ((uintptr_t)src | (uintptr_t)out) : 0);
+    const int V = (F % 4 == 0 && (ptrs & 15) == 0) ? 4 : ((F % 2 == 0 && (ptrs & 7) == 0) ? 2 : 1);
+    hipStream_t st = (hipStream_t)stream;
+    void *scratch = nullptr;
+    StreamCtx *ctx = nullptr;
+    if (op == GEOT_OP_MAX) {
+        geot_status_t s = stream_scratch((size_t)(num_segments * F) * 8, st, &scratch, nullptr, &ctx);
+        if (s != GEOT_SUCCESS) return s;
+        GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, src, out, nnz, num_segments, F, V,
+                                    (unsigned long long *)scratch, grad_src, st),
+                 "launch max backward kernels");
+        return GEOT_SUCCESS;
+    }
+    if (op == GEOT_OP_SUM) {
+        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, nullptr, nnz, num_segments, F, V, false,
+                                      grad_src, st),
+                 "launch backward kernel");
+        return GEOT_SUCCESS;
+    }
+    GapList gaps;
+    geot_status_t s = stream_scratch((size_t)(num_segments + 1) * 8, st, &scratch, &gaps, &ctx);
+    if (s != GEOT_SUCCESS) return s;
+    int64_t *off = (int64_t *)scratch;
+    return poison(ctx, [&]() -> geot_status_t {
+        GEOT_HIP(launch_offsets(sorted_index, nnz, num_segments, off, gaps, st), "launch offsets kernel");
+        GEOT_HIP(launch_gap_fill_i64(off, num_segments + 1, gaps, st), "launch gap fill kernel");
+        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, off, nnz, num_segments, F, V, true,
+                                      grad_src, st),
+                 "launch backward kernel");
+        return GEOT_SUCCESS;
+    }());
+}
+
+geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,
+                                           const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                           int64_t num_rows, int64_t F, geot_op_t op,
+                                           const float *grad_out, const float *out, float *grad_X,
+                                           float *grad_weight, void *stream) {
+    t_detail.clear();
+    if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
+    if (nnz < 0 || num_rows < 0 || F < 0 || num_x_rows < 0)
+        return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (grad_weight && !weight) return fail(GEOT_ERROR_INVALID_VALUE, "grad_weight needs weight");
+    if (num_rows > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_rows must be < 2^31");
+    const int64_t kMax = (int64_t)1 << 62;
+    if (F > ((int64_t)1 << 31) || num_rows > kMax / F || nnz > kMax / F || num_x_rows > kMax / (F ? F : 1))
+        return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
+    hipStream_t st = (hipStream_t)stream;
+    if (F == 0) return GEOT_SUCCESS;
+    if (nnz == 0) {  // no edge: every gradient is zero
+        if (grad_X) GEOT_HIP(launch_fill(grad_X, num_x_rows, F, F, 0.0f, st), "launch fill kernel");
+        return GEOT_SUCCESS;
+    }
+    if (num_rows == 0 || num_x_rows == 0) return fail(GEOT_ERROR_INVALID_VALUE, "empty row or X range with nnz > 0");
+    if (!col || !sorted_row || !grad_out) return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
+    if ((grad_weight || op == GEOT_OP_MAX) && !X) return fail(GEOT_ERROR_INVALID_VALUE, "X is NULL");
+    if (op == GEOT_OP_MAX && !out) return fail(GEOT_ERROR_INVALID_VALUE, "max needs out");
+    const size_t xb = (size_t)(num_x_rows * F) * 4;
+    if (grad_X && (overlaps(grad_X, xb, X, xb) || overlaps(grad_X, xb, grad_out, (size_t)(num_rows * F) * 4) ||
+                   overlaps(grad_X, xb, col, (size_t)nnz * 8) || overlaps(grad_X, xb, sorted_row, (size_t)nnz * 8) ||
+                   overlaps(grad_X, xb, weight, weight ? (size_t)nnz * 4 : 0) ||
+                   overlaps(grad_X, xb, grad_weight, grad_weight ? (size_t)nnz * 4 : 0)))
+        return fail(GEOT_ERROR_INVALID_VALUE, "grad_X overlaps another array");
+    if (grad_weight && (overlaps(grad_weight, (size_t)nnz * 4, weight, (size_t)nnz * 4) ||
+                        overlaps(grad_weight, (size_t)nnz * 4, col, (size_t)nnz * 8) ||
+                        overlaps(grad_weight, (size_t)nnz * 4, sorted_row, (size_t)nnz * 8)))
+        return fail(GEOT_ERROR_INVALID_VALUE, "grad_weight overlaps an input");
+    if (!grad_X && !grad_weight) return GEOT_SUCCESS;
+    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)X | (uintptr_t)grad_X | (uintptr_t)out;
+    const int V = (F % 4 == 0 && (ptrs & 15) == 0) ? 4 : ((F % 2 == 0 && (ptrs & 7) == 0) ? 2 : 1);
+    // temporaries from the stream-ordered pool (the forward call below uses the per-stream buffer):
+    // row starts (mean), max recipients (max), the transposed edge list (grad_X for sum and mean)
+    const bool mean = op == GEOT_OP_MEAN, mx = op == GEOT_OP_MAX;
+    const bool transpose = grad_X && !mx;
+    size_t at = 0;
+    auto take = [&](size_t b) { const size_t o = at; at = align256(at + b); return o; };
+    const size_t o_roff = mean ? take((size_t)(num_rows + 1) * 8) : 0;
+    const size_t o_arg = mx ? take((size_t)(num_rows * F) * 8) : 0;
+    const int64_t nx = num_x_rows;
+    const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
+    const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
+    const size_t o_sums = transpose ? take((size_t)((nx + 4095) / 4096 + 1) * 8) : 0;
+    const size_t o_key = transpose ? take((size_t)nnz * 8) : 0;
+    const size_t o_row = transpose ? take((size_t)nnz * 8) : 0;
+    const size_t o_w = transpose ? take((size_t)nnz * 4) : 0;
+    ScratchGuard sg;
+    sg.st = st;
+    geot_status_t s = scratch_alloc(&sg.p, at, st);
+    if (s != GEOT_SUCCESS) return s;
+    char *base = (char *)sg.p;
+    int64_t *roff = mean ? (int64_t *)(base + o_roff) : nullptr;
+    unsigned long long *arg = mx ? (unsigned long long *)(base + o_arg) : nullptr;
+    if (mean) {
+        void *unused = nullptr;
+        GapList gaps;
+        StreamCtx *ctx = nullptr;
+        s = stream_scratch(0, st, &unused, &gaps, &ctx);
+        if (s != GEOT_SUCCESS) return s;
+        s = poison(ctx, [&]() -> geot_status_t {
+            GEOT_HIP(launch_offsets(sorted_row, nnz, num_rows, roff, gaps, st), "launch offsets kernel");
+            GEOT_HIP(launch_gap_fill_i64(roff, num_rows + 1, gaps, st), "launch gap fill kernel");
+            return GEOT_SUCCESS;
+        }());
+        if (s != GEOT_SUCCESS) return s;
+    }
+    const int bop = op == GEOT_OP_SUM ? GEOT_BWD_SUM : (mean ? GEOT_BWD_MEAN : GEOT_BWD_MAX);
+    // weights (and, for max, X through atomic adds of the recipients only)
+    GEOT_HIP(launch_gs_bwd(X, num_x_rows, col, weight, sorted_row, roff, out, grad_out, nnz, num_rows, F,
+                           V, bop, arg, mx ? grad_X : nullptr, grad_weight, st),
+             "launch fused backward kernels");
+    if (transpose) {
+        // grad_X = gather_scatter of grad_out over the edges sorted by col (sum of coef * grad_out rows)
+        int64_t *key_t = (int64_t *)(base + o_key);
+        int64_t *row_t = (int64_t *)(base + o_row);
+        float *w_t = (float *)(base + o_w);
+        GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
+                                  (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, st),
+                 "launch transpose kernels");
+        Problem tp{true, grad_out, num_rows, row_t, w_t, key_t, nnz, nx, F, GEOT_OP_SUM, grad_X};
+        geot_kernel_choice_t c;
+        select_raw(nnz, nx, F, GEOT_OP_SUM, 1, nullptr, &c);
+        Resolved r;
+        s = resolve(tp, c, &r, true);
+        if (s != GEOT_SUCCESS) return s;
+        s = run_ep(tp, r, st);
+        if (s != GEOT_SUCCESS) return s;
+    }
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    return scratch_free(p_free, st);
 }
 
 geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, int32_t gather,

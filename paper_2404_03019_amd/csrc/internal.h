@@ -107,4 +107,32 @@ hipError_t launch_check(const int64_t *idx, int64_t n, int64_t S, const int64_t 
 
 hipError_t launch_zero_u64(unsigned long long *p, int64_t n, hipStream_t stream);
 
+// ---- gradients (bwd_kernels.hip) ------------------------------------------
+enum BwdOp : int { GEOT_BWD_SUM = 0, GEOT_BWD_MEAN = 1, GEOT_BWD_MAX = 2 };
+
+hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long v, hipStream_t st);
+
+// Counting sort of the edges by col: key_t (sorted col), row_t and w_t (weight, divided by
+// the row's edge count for mean; roff = row starts) of the transposed problem.
+// counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
+hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
+                            const int64_t *roff, bool mean, int64_t n, unsigned *counts, int64_t *off,
+                            int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, hipStream_t st);
+
+// grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean)
+hipError_t launch_seg_bwd_bcast(const float *gout, const int64_t *idx, const int64_t *off, int64_t n,
+                                int64_t S, int64_t F, int V, bool mean, float *gsrc, hipStream_t st);
+
+// max: arg [S x F] scratch; grad_src gets grad_out at the first attaining row of each (s, f)
+hipError_t launch_seg_bwd_max(const float *gout, const int64_t *idx, const float *src, const float *out,
+                              int64_t n, int64_t S, int64_t F, int V, unsigned long long *arg, float *gsrc,
+                              hipStream_t st);
+
+// fused form: grad_X (zero-filled here, then atomic adds) and/or grad_w; off = row starts
+// (mean), arg [R x F] scratch (max).
+hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const float *w, const int64_t *row,
+                         const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
+                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw,
+                         hipStream_t st);
+
 }  // namespace geot

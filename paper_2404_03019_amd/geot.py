@@ -66,6 +66,8 @@ def lib() -> ctypes.CDLL:
     L.geot_select.argtypes = [i64, i64, i64, ctypes.c_int, i32, ctypes.POINTER(IndexStats), pc]
     L.geot_index_stats.argtypes = [p, i64, i64, ctypes.POINTER(IndexStats), p]
     L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
+    L.geot_segment_reduce_backward.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, p, p]
+    L.geot_gather_scatter_backward.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, p, p, p]
     L.geot_last_choice.argtypes = [pc]
     L.geot_release_scratch.argtypes = []
     L.geot_profile_begin.argtypes = [i32]
@@ -77,7 +79,8 @@ def lib() -> ctypes.CDLL:
     L.geot_version.restype = i32
     for name in ("geot_segment_reduce", "geot_segment_reduce_with", "geot_gather_scatter",
                  "geot_gather_scatter_with", "geot_select", "geot_index_stats", "geot_check_index",
-                 "geot_last_choice", "geot_profile_begin", "geot_profile_end", "geot_release_scratch"):
+                 "geot_last_choice", "geot_profile_begin", "geot_profile_end", "geot_release_scratch",
+                 "geot_segment_reduce_backward", "geot_gather_scatter_backward"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -194,6 +197,59 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
                                             ctypes.byref(c) if c is not None else None)
     _raise(st)
     return out
+
+
+def segment_reduce_backward(grad_out: torch.Tensor, index: torch.Tensor, reduce: str = "sum",
+                            src: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                            grad_src: torch.Tensor | None = None) -> torch.Tensor:
+    """Gradient of segment_reduce w.r.t. src (geot_segment_reduce_backward)."""
+    _dev(grad_out, "grad_out", torch.float32, 2)
+    _dev(index, "index", torch.int64, 1)
+    S, F = grad_out.shape
+    if reduce == "max":
+        if src is None or out is None:
+            raise ValueError("max needs src and out")
+        _dev(src, "src", torch.float32, 2)
+        _dev(out, "out", torch.float32, 2)
+    if grad_src is None:
+        grad_src = torch.empty((index.numel(), F), dtype=torch.float32, device=grad_out.device)
+    else:
+        _dev(grad_src, "grad_src", torch.float32, 2)
+    with _OnDevice(grad_out.device):
+        st = lib().geot_segment_reduce_backward(
+            grad_out.data_ptr(), index.data_ptr(), index.numel(), S, F, OPS[reduce],
+            src.data_ptr() if src is not None else None, out.data_ptr() if out is not None else None,
+            grad_src.data_ptr(), _stream(grad_out.device))
+    _raise(st)
+    return grad_src
+
+
+def gather_scatter_backward(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
+                            row: torch.Tensor, grad_out: torch.Tensor, reduce: str = "sum",
+                            out: torch.Tensor | None = None, need_x: bool = True,
+                            need_weight: bool = True):
+    """(grad_x or None, grad_weight or None) of gather_scatter (geot_gather_scatter_backward)."""
+    _dev(x, "x", torch.float32, 2)
+    _dev(col, "col", torch.int64, 1)
+    _dev(row, "row", torch.int64, 1)
+    _dev(grad_out, "grad_out", torch.float32, 2)
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+    if reduce == "max":
+        if out is None:
+            raise ValueError("max needs out")
+        _dev(out, "out", torch.float32, 2)
+    R, F = grad_out.shape
+    gx = torch.empty_like(x) if need_x else None
+    gw = torch.empty_like(weight) if (need_weight and weight is not None) else None
+    with _OnDevice(x.device):
+        st = lib().geot_gather_scatter_backward(
+            x.data_ptr(), x.shape[0], col.data_ptr(), weight.data_ptr() if weight is not None else None,
+            row.data_ptr(), row.numel(), R, F, OPS[reduce], grad_out.data_ptr(),
+            out.data_ptr() if out is not None else None, gx.data_ptr() if gx is not None else None,
+            gw.data_ptr() if gw is not None else None, _stream(x.device))
+    _raise(st)
+    return gx, gw
 
 
 def index_stats(index: torch.Tensor, num_segments: int) -> dict:

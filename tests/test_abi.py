@@ -128,3 +128,21 @@ def test_selector_uses_stats_when_given():
                 sum_len_sq=9000 ** 2, mean_len=16.0, var_len=8.0e4)
     assert geot.select(16000, 1000, 64, "mean", stats=skew)["family"] == 1
     assert geot.select(16000, 1000, 64, "mean", stats=even)["family"] in (1, 2)
+
+
+def test_backward_arguments_are_checked_on_the_host():
+    L = lib()
+    g, idx, out, gs = FAKE, FAKE + (1 << 26), FAKE + (1 << 27), FAKE + (1 << 30)
+    # unknown op, negative sizes, max without src/out, overlap, no rows = no-op
+    assert L.geot_segment_reduce_backward(g, idx, 10, 4, 3, 9, None, None, gs, None) == INVALID
+    assert L.geot_segment_reduce_backward(g, idx, -1, 4, 3, 0, None, None, gs, None) == INVALID
+    assert L.geot_segment_reduce_backward(g, idx, 10, 4, 3, 2, None, out, gs, None) == INVALID
+    assert L.geot_segment_reduce_backward(g, idx, 10, 4, 8, 0, None, None, g + 16, None) == INVALID
+    assert L.geot_segment_reduce_backward(g, idx, 10, 0, 3, 0, None, None, gs, None) == INVALID
+    assert L.geot_segment_reduce_backward(None, None, 0, 4, 3, 0, None, None, None, None) == SUCCESS
+    X, col, row, gx, gw = FAKE, FAKE + (1 << 25), FAKE + (1 << 26), FAKE + (1 << 31), FAKE + (1 << 32)
+    # grad_weight without weight, max without out, nothing requested = no-op
+    assert L.geot_gather_scatter_backward(X, 10, col, None, row, 5, 3, 4, 0, g, None, gx, gw, None) == INVALID
+    assert L.geot_gather_scatter_backward(X, 10, col, None, row, 5, 3, 4, 2, g, None, gx, None, None) == INVALID
+    assert L.geot_gather_scatter_backward(X, 10, None, None, row, 5, 3, 4, 0, g, None, gx, None, None) == INVALID
+    assert L.geot_gather_scatter_backward(X, 10, col, None, row, 5, 3, 4, 0, g, None, None, None, None) == SUCCESS

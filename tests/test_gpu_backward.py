@@ -1,0 +1,116 @@
+"""GPU parity of the gradients (geot_segment_reduce_backward, geot_gather_scatter_backward)
+against the CPU oracle.
+
+Bar: segment sum and max gradients copy values, so they are bit-exact; mean is one
+division (within the fp32 bound); the fused gradients are sums within
+1e-5 * sum|terms| + 1e-6 per element, with sum|terms| from the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2404_03019_amd as geot
+from gpu_util import say
+from workloads import random_gather_problem, random_problem
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def up(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def within(got, ref, terms, what):
+    err = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    lim = 1e-5 * terms + 1e-6
+    bad = ~(err <= lim)
+    assert not bad.any(), f"{what}: {int(bad.sum())} elements, first at {np.argwhere(bad)[0]}"
+
+
+SEG_CASES = [
+    (1, 20000, 900, 1, "zipf", "normal", 0.1),
+    (2, 30000, 1500, 3, "lognormal", "normal", 0.05),
+    (3, 25000, 700, 32, "uniform", "int", 0.2),
+    (4, 8000, 400, 33, "one_heavy", "normal", 0.1),
+    (5, 6000, 300, 256, "zipf", "normal", 0.0),
+]
+
+
+@pytest.mark.parametrize("case", SEG_CASES, ids=lambda c: f"seed{c[0]}-F{c[3]}")
+def test_segment_backward_parity(case):
+    seed, nnz, S, F, dist, values, ef = case
+    p = random_problem(seed, nnz, S, F, dist, values, ef)
+    src, idx = p["src"], p["index"]
+    g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
+    for op in ("sum", "mean", "max"):
+        say(f"segment backward seed={seed} F={F} {op}")
+        out_gpu = geot.segment_reduce(up(src), up(idx), S, op)
+        out_np = out_gpu.cpu().numpy()
+        got = geot.segment_reduce_backward(up(g), up(idx), op, up(src), out_gpu).cpu().numpy()
+        ref = oracle.segment_reduce_backward(g, idx, op, src, out_np)
+        if op == "mean":
+            terms = np.abs(ref.astype(np.float64))
+            within(got, ref, terms, f"segment backward mean seed={seed}")
+        else:
+            assert np.array_equal(got, ref), f"segment backward {op} seed={seed} F={F}"
+
+
+GS_CASES = [
+    (11, 20000, 1200, 900, 32, "zipf", "normal", True),
+    (12, 15000, 800, 2000, 3, "lognormal", "normal", True),
+    (13, 10000, 500, 700, 64, "uniform", "normal", False),
+    (14, 8000, 300, 3000, 128, "one_heavy", "normal", True),
+    (15, 5000, 400, 400, 17, "poisson", "int", True),
+]
+
+
+@pytest.mark.parametrize("case", GS_CASES, ids=lambda c: f"seed{c[0]}-F{c[4]}-w{int(c[7])}")
+def test_gather_backward_parity(case):
+    seed, nnz, R, nx, F, dist, values, weighted = case
+    q = random_gather_problem(seed, nnz, R, nx, F, dist, values, weighted, 0.05)
+    X, col, w, row = q["X"], q["col"], q["weight"], q["index"]
+    g = np.random.default_rng(seed).standard_normal((R, F)).astype(np.float32)
+    for op in ("sum", "mean", "max"):
+        say(f"gather backward seed={seed} F={F} {op}")
+        out_gpu = geot.gather_scatter(up(X), up(col), up(w), up(row), R, op)
+        out_np = out_gpu.cpu().numpy()
+        gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op, out_gpu)
+        rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, op, out_np)
+        ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, op, out_np, absolute=True)
+        within(gx.cpu().numpy(), rx, ax, f"grad_X {op} seed={seed}")
+        if weighted:
+            within(gw.cpu().numpy(), rw, aw, f"grad_w {op} seed={seed}")
+        else:
+            assert gw is None
+
+
+def test_backward_edge_cases():
+    # no rows: grad_src is empty; fused form with no edges: grad_X is all zeros
+    g = up(np.ones((4, 3), dtype=np.float32))
+    e = geot.segment_reduce_backward(g, up(np.zeros(0, dtype=np.int64)), "sum")
+    assert e.shape == (0, 3)
+    X = up(np.ones((5, 3), dtype=np.float32))
+    gx, _ = geot.gather_scatter_backward(X, up(np.zeros(0, dtype=np.int64)), None,
+                                         up(np.zeros(0, dtype=np.int64)), g, "sum", need_weight=False)
+    assert torch.all(gx == 0)
+    with pytest.raises(ValueError):
+        geot.segment_reduce_backward(g, up(np.zeros(2, dtype=np.int64)), "max")
+
+
+def test_gradients_match_a_torch_training_step():
+    """A GNN-style step: loss = sum(out * t) with out = gather_scatter(X, w); the library's
+    gradients equal torch autograd of the same expression in fp64 on the GPU."""
+    q = random_gather_problem(16, 40000, 2000, 2000, 16, "zipf", "normal", True, 0.0)
+    X, col, w, row, R = q["X"], q["col"], q["weight"], q["index"], q["num_segments"]
+    t = np.random.default_rng(17).standard_normal((R, 16)).astype(np.float32)
+    tX = torch.from_numpy(X).to(DEV).double().requires_grad_(True)
+    tw = torch.from_numpy(w).to(DEV).double().requires_grad_(True)
+    msg = tX[up(col)] * tw[:, None]
+    o = torch.zeros(R, 16, dtype=torch.float64, device=DEV).index_add(0, up(row), msg)
+    (o * up(t).double()).sum().backward()
+    gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(t), "sum")
+    ax, aw = oracle.gather_scatter_backward(X, col, w, row, t, "sum", absolute=True)
+    within(gx.cpu().numpy(), tX.grad.cpu().numpy(), ax, "grad_X vs torch")
+    within(gw.cpu().numpy(), tw.grad.cpu().numpy(), aw, "grad_w vs torch")
