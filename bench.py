@@ -131,6 +131,137 @@ def copy_probe(n: int):
                       "GB/s": round(2 * (1 << 31) / dt / 1e9, 1)}), flush=True)
 
 
+def suite(reps: int):
+    """One JSON line per measurement: every named workload and op, the gradients on the two
+    large workloads, and a two-layer graph-convolution training step (library autograd vs the
+    same model with torch's index_add). Median over `reps` HIP-event timings per entry; for
+    inputs under 1 GB a 512 MB write flushes the MALL before each repetition."""
+    import numpy as np
+    import torch
+
+    import paper_2404_03019_amd as geot
+    import paper_2404_03019_amd.autograd as ga
+    from workloads import make_config
+    from workloads.generators import C2_FEATURES
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    geot.lib()
+    flush = torch.empty(1 << 27, device=dev)
+
+    def timed(fn, nbytes_in):
+        cold = nbytes_in < (1 << 30)
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            if cold:
+                flush.fill_(1.0)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts)), cold
+
+    def emit(name, ms, nbytes, cold, **extra):
+        rec = {"suite": name, "ms": round(ms, 4), "algorithmic_bytes": nbytes,
+               "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+               "pct_of_hbm_peak": round(100 * nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 1),
+               "mall_flushed": cold, "choice": geot.last_choice()}
+        rec.update(extra)
+        print(json.dumps(rec), flush=True)
+
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    # segment reductions
+    c = make_config("c1_zipf_small")
+    src, idx = up(c["src"]), up(c["index"])
+    b = seg_bytes(idx.numel(), c["num_segments"], 32)
+    ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], "sum"), b)
+    emit("c1_zipf_small sum", ms, b, cold)
+    c = make_config("c2_poisson_fsweep", F=256)
+    idx = up(c["index"])
+    for F in C2_FEATURES:
+        src = up(c["src"][:, :F])
+        b = seg_bytes(idx.numel(), c["num_segments"], F)
+        for op in ("sum", "mean", "max"):
+            ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], op), b)
+            emit(f"c2_poisson_fsweep F={F} {op}", ms, b, cold)
+        del src
+    del c
+    c = make_config("c5_pointcloud_knn")
+    src, idx = up(c["src"]), up(c["index"])
+    b = seg_bytes(idx.numel(), c["num_segments"], 64)
+    for op in ("mean", "max"):
+        ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], op), b)
+        emit(f"c5_pointcloud_knn {op}", ms, b, cold)
+    del src, idx, c
+    torch.cuda.empty_cache()
+    # the two large workloads, forward and gradients
+    c3 = make_config("c3_powerlaw_graph")
+    S3 = c3["num_segments"]
+    src, idx = up(c3["src"]), up(c3["index"])
+    n3 = idx.numel()
+    b = seg_bytes(n3, S3, 32)
+    ms, cold = timed(lambda: geot.segment_reduce(src, idx, S3, "sum"), b)
+    emit("c3_powerlaw_graph sum", ms, b, cold)
+    g3 = torch.randn(S3, 32, device=dev)
+    gsrc = torch.empty_like(src)
+    for op in ("sum", "mean", "max"):
+        out = geot.segment_reduce(src, idx, S3, op)
+        # bytes: index + grad_src written + grad_out read; max also reads src and out per row
+        b = n3 * 8 + n3 * 128 + S3 * 128 + (n3 * 128 + S3 * 128 if op == "max" else 0)
+        ms, cold = timed(lambda: geot.segment_reduce_backward(g3, idx, op, src, out, grad_src=gsrc), b)
+        emit(f"c3_powerlaw_graph backward {op}", ms, b, cold)
+    del src, idx, g3, gsrc, c3
+    torch.cuda.empty_cache()
+    c4 = make_config("c4_spmm")
+    R4 = c4["num_segments"]
+    X, col, w, row = up(c4["X"]), up(c4["col"]), up(c4["weight"]), up(c4["index"])
+    n4 = row.numel()
+    b = gather_bytes(n4, R4, 128)
+    ms, cold = timed(lambda: geot.gather_scatter(X, col, w, row, R4, "sum"), b)
+    emit("c4_spmm sum", ms, b, cold)
+    g4 = torch.randn(R4, 128, device=dev)
+    # grad_X: edge metadata + one gathered grad_out row per edge + grad_X written
+    b = n4 * 20 + n4 * 512 + R4 * 512
+    ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_weight=False), b)
+    emit("c4_spmm backward grad_X", ms, b, cold)
+    # grad_w: col, row (the weight is not read for sum) + one gathered X row per edge + each
+    # grad_out row once (edges are sorted by row) + grad_w written; same count as the forward
+    b = n4 * 20 + n4 * 512 + R4 * 512
+    ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_x=False), b)
+    emit("c4_spmm backward grad_weight", ms, b, cold)
+    del g4
+    # two-layer graph convolution training step on the SpMM graph (128 -> 128 -> 64)
+    torch.manual_seed(0)
+    layers = torch.nn.ModuleList([ga.GraphConv(128, 128), ga.GraphConv(128, 64)]).to(dev)
+    target = torch.randn(R4, 64, device=dev)
+
+    def step_geot():
+        layers.zero_grad(set_to_none=True)
+        h = torch.relu(layers[0](X, col, row, R4, w))
+        loss = ((layers[1](h, col, row, R4, w) - target) ** 2).mean()
+        loss.backward()
+
+    def agg_torch(z):
+        return torch.zeros(R4, z.shape[1], device=dev).index_add_(0, row, z[col] * w[:, None])
+
+    def step_torch():
+        layers.zero_grad(set_to_none=True)
+        h = torch.relu(agg_torch(layers[0].lin(X)) + layers[0].bias)
+        loss = ((agg_torch(layers[1].lin(h)) + layers[1].bias - target) ** 2).mean()
+        loss.backward()
+
+    ms_g, _ = timed(step_geot, 1 << 40)
+    ms_t, _ = timed(step_torch, 1 << 40)
+    print(json.dumps({"suite": "graphconv 2-layer training step (SpMM graph, 128-128-64)",
+                      "ms": round(ms_g, 3), "torch_index_add_ms": round(ms_t, 3),
+                      "speedup_vs_torch": round(ms_t / ms_g, 2)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,9 +272,14 @@ def main():
                     help="approximate host seconds of oracle work for cpu_baseline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="N",
                     help="only run N plain device copies of 2 GiB (calibrates HBM byte counters)")
+    ap.add_argument("--suite", action="store_true",
+                    help="instead of the headline line: one line per workload, op and gradient")
     args = ap.parse_args()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.suite:
+        suite(max(3, args.steps))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the path does not shard across GPUs); "

@@ -1,0 +1,93 @@
+"""Autograd and a message-passing layer on top of libgeot_hip.
+
+The functions here are torch.autograd.Function wrappers: their forward calls
+geot_segment_reduce / geot_gather_scatter and their backward calls
+geot_segment_reduce_backward / geot_gather_scatter_backward. The only torch
+arithmetic is in the layer's dense transform (a plain matrix product) and
+bias, as in the GNN layers of the paper's end-to-end setting (Section V-F:
+message and aggregation fused into one operator, update by a dense layer).
+"""
+from __future__ import annotations
+
+import torch
+
+from . import geot
+
+
+class SegmentReduce(torch.autograd.Function):
+    """out = segment_reduce(src, index, num_segments, reduce); differentiable in src."""
+
+    @staticmethod
+    def forward(ctx, src, index, num_segments: int, reduce: str = "sum"):
+        out = geot.segment_reduce(src.contiguous(), index, num_segments, reduce)
+        ctx.reduce = reduce
+        if reduce == "max":
+            ctx.save_for_backward(index, src, out)
+        else:
+            ctx.save_for_backward(index)
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        if ctx.reduce == "max":
+            index, src, out = ctx.saved_tensors
+        else:
+            (index,) = ctx.saved_tensors
+            src = out = None
+        g = geot.segment_reduce_backward(grad_out.contiguous(), index, ctx.reduce, src, out)
+        return g, None, None, None
+
+
+class GatherScatter(torch.autograd.Function):
+    """out = gather_scatter(x, col, weight, row, num_rows, reduce); differentiable in x and weight."""
+
+    @staticmethod
+    def forward(ctx, x, col, weight, row, num_rows: int, reduce: str = "sum"):
+        x = x.contiguous()
+        out = geot.gather_scatter(x, col, weight, row, num_rows, reduce)
+        ctx.reduce = reduce
+        ctx.save_for_backward(x, col, weight if weight is not None else torch.empty(0), row,
+                              out if reduce == "max" else torch.empty(0))
+        ctx.has_weight = weight is not None
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        x, col, weight, row, out = ctx.saved_tensors
+        weight = weight if ctx.has_weight else None
+        need_x = ctx.needs_input_grad[0]
+        need_w = ctx.has_weight and ctx.needs_input_grad[2]
+        gx, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out.contiguous(), ctx.reduce,
+                                              out if ctx.reduce == "max" else None,
+                                              need_x=need_x, need_weight=need_w)
+        return gx, None, gw, None, None, None
+
+
+def segment_reduce(src, index, num_segments, reduce="sum"):
+    """Differentiable segment reduction (gradient w.r.t. src)."""
+    return SegmentReduce.apply(src, index, num_segments, reduce)
+
+
+def gather_scatter(x, col, weight, row, num_rows, reduce="sum"):
+    """Differentiable fused gather-weight-scatter (gradients w.r.t. x and weight)."""
+    return GatherScatter.apply(x, col, weight, row, num_rows, reduce)
+
+
+class GraphConv(torch.nn.Module):
+    """h' = aggregate_{e: row[e] = v} w_e * (h W)[col[e]] + b, with the aggregation fused.
+
+    With w_e = 1 / sqrt(deg(row[e]) * deg(col[e])) and self-loops in the edge
+    list this is a GCN layer; with reduce="mean" and no weights a GraphSAGE-style
+    mean aggregation. The edge list is sorted by row (the destination).
+    """
+
+    def __init__(self, in_features: int, out_features: int, reduce: str = "sum", bias: bool = True):
+        super().__init__()
+        self.lin = torch.nn.Linear(in_features, out_features, bias=False)
+        self.bias = torch.nn.Parameter(torch.zeros(out_features)) if bias else None
+        self.reduce = reduce
+
+    def forward(self, h, col, row, num_nodes: int, weight=None):
+        z = self.lin(h)
+        out = gather_scatter(z, col, weight, row, num_nodes, self.reduce)
+        return out + self.bias if self.bias is not None else out
