@@ -33,8 +33,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "segment_reduce / gather_scatter effective HBM GB/s and % of MI355X HBM peak"
-KERNEL_SOURCES = ("paper_2404_03019_amd/csrc/ep_kernel.hip", "paper_2404_03019_amd/csrc/common.h",
-                  "paper_2404_03019_amd/csrc/internal.h")
+KERNEL_SOURCES = ("paper_2404_03019_amd/csrc/ep_kernel.h", "paper_2404_03019_amd/csrc/ep_f32_i64.hip",
+                  "paper_2404_03019_amd/csrc/common.h", "paper_2404_03019_amd/csrc/internal.h")
 
 
 def log(*a):
@@ -49,12 +49,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def seg_bytes(nnz, S, F):
-    return nnz * F * 4 + nnz * 8 + S * F * 4
+def seg_bytes(nnz, S, F, esize=4, isize=8):
+    """src + index + out; esize / isize: bytes per stored element / per id"""
+    return nnz * F * esize + nnz * isize + S * F * 4
 
 
-def gather_bytes(nnz, R, F):
-    return nnz * (8 + 4 + 8) + nnz * F * 4 + R * F * 4
+def gather_bytes(nnz, R, F, esize=4, isize=8):
+    """col + weight + row per edge, one gathered X row per edge, out"""
+    return nnz * (isize + 4 + isize) + nnz * F * esize + R * F * 4
 
 
 def load_traffic(kernel_key: str):
@@ -207,6 +209,12 @@ def suite(reps: int):
     b = seg_bytes(n3, S3, 32)
     ms, cold = timed(lambda: geot.segment_reduce(src, idx, S3, "sum"), b)
     emit("c3_powerlaw_graph sum", ms, b, cold)
+    # the same reduction with bf16 storage and int32 ids (fp32 accumulation and output)
+    src16, idx32 = src.to(torch.bfloat16), idx.to(torch.int32)
+    b = seg_bytes(n3, S3, 32, 2, 4)
+    ms, cold = timed(lambda: geot.segment_reduce(src16, idx32, S3, "sum"), b)
+    emit("c3_powerlaw_graph sum bf16 int32", ms, b, cold)
+    del src16, idx32
     g3 = torch.randn(S3, 32, device=dev)
     gsrc = torch.empty_like(src)
     for op in ("sum", "mean", "max"):
@@ -224,6 +232,20 @@ def suite(reps: int):
     b = gather_bytes(n4, R4, 128)
     ms, cold = timed(lambda: geot.gather_scatter(X, col, w, row, R4, "sum"), b)
     emit("c4_spmm sum", ms, b, cold)
+    X16, col32, row32 = X.to(torch.bfloat16), col.to(torch.int32), row.to(torch.int32)
+    b = gather_bytes(n4, R4, 128, 2, 4)
+    ms, cold = timed(lambda: geot.gather_scatter(X16, col32, w, row32, R4, "sum"), b)
+    emit("c4_spmm sum bf16 int32", ms, b, cold)
+    # unfused: materialise the weighted messages with torch, then reduce them (the paper's
+    # motivation for fusing: the message tensor is written and read back once)
+    b = gather_bytes(n4, R4, 128)
+
+    def unfused():
+        msg = torch.index_select(X, 0, col).mul_(w[:, None])
+        geot.segment_reduce(msg, row, R4, "sum")
+    ms_u, _ = timed(unfused, b)
+    emit("c4_spmm sum unfused (torch gather + segment_reduce)", ms_u, b, False)
+    del X16, col32, row32
     g4 = torch.randn(R4, 128, device=dev)
     # grad_X: edge metadata + one gathered grad_out row per edge + grad_X written
     b = n4 * 20 + n4 * 512 + R4 * 512

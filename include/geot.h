@@ -149,6 +149,42 @@ geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const
                                        int64_t num_rows, int64_t F, geot_op_t op, float *out,
                                        void *stream, const geot_kernel_choice_t *choice);
 
+/* Storage types of the reduced data, and index types. Not in the paper: a
+ * 16-bit storage type halves the bytes of the stream that dominates every
+ * reduction, and int32 ids halve the index stream. */
+typedef enum {
+    GEOT_DTYPE_F32 = 0,  /* IEEE binary32 */
+    GEOT_DTYPE_BF16 = 1, /* bfloat16: the upper 16 bits of a binary32 */
+    GEOT_DTYPE_F16 = 2   /* IEEE binary16 */
+} geot_dtype_t;
+typedef enum { GEOT_INDEX_I64 = 0, GEOT_INDEX_I32 = 1 } geot_index_type_t;
+
+/* geot_segment_reduce_with / geot_gather_scatter_with with the storage type of
+ * src (X) and the type of the ids given:
+ *   src / X               fp32, bf16 or fp16 (`src_type` / `x_type`), row-major
+ *   sorted_index, col,
+ *   sorted_row            int64 or int32 (`index_type`, the same for col and row)
+ *   weight                fp32 or NULL, as before
+ *   out                   fp32, overwritten, as before
+ * Every element is widened to fp32 exactly when loaded and accumulated in fp32,
+ * so the result is the fp32 call's result on the widened data (same
+ * tolerance; max exact). These calls run the element-parallel family: a
+ * choice with family GEOT_FAMILY_SP returns GEOT_ERROR_UNSUPPORTED, and
+ * where the selector names the segment-parallel family the element-parallel
+ * one runs with shape-derived parameters. A 16-bit type with vec 4 reads
+ * 8-byte vectors, so vec is clamped to what F and the src alignment allow in
+ * elements. An unknown type is GEOT_ERROR_INVALID_VALUE. Other checks and
+ * errors as geot_segment_reduce.                                            */
+geot_status_t geot_segment_reduce_typed(const void *src, geot_dtype_t src_type, const void *sorted_index,
+                                        geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                        int64_t F, geot_op_t op, float *out, void *stream,
+                                        const geot_kernel_choice_t *choice);
+geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows, const void *col,
+                                        const float *weight, const void *sorted_row,
+                                        geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                        geot_op_t op, float *out, void *stream,
+                                        const geot_kernel_choice_t *choice);
+
 /* Gradient of geot_segment_reduce w.r.t. src, for training (Section VI lists
  * autograd support as future work; this is the derivative of the definition).
  *   grad_out  [num_segments x F] fp32: gradient of the loss w.r.t. out

@@ -34,6 +34,10 @@ class SegmentReduce(torch.autograd.Function):
         else:
             (index,) = ctx.saved_tensors
             src = out = None
+        # the gradient kernels take fp32 data and int64 ids; a 16-bit src gets its
+        # gradient cast back by autograd
+        index = index.long()
+        src = src.float() if src is not None else None
         g = geot.segment_reduce_backward(grad_out.contiguous(), index, ctx.reduce, src, out)
         return g, None, None, None
 
@@ -57,6 +61,7 @@ class GatherScatter(torch.autograd.Function):
         weight = weight if ctx.has_weight else None
         need_x = ctx.needs_input_grad[0]
         need_w = ctx.has_weight and ctx.needs_input_grad[2]
+        x, col, row = x.float(), col.long(), row.long()  # the gradient kernels take fp32 and int64
         gx, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out.contiguous(), ctx.reduce,
                                               out if ctx.reduce == "max" else None,
                                               need_x=need_x, need_weight=need_w)

@@ -202,14 +202,19 @@ bool prof_take(hipEvent_t *a, hipEvent_t *b) {
 // ---------------------------------------------------------------------------
 struct Problem {
     bool gather;
-    const float *src;      // rows or X
+    const void *src;       // rows or X, of type elem
     int64_t num_x_rows;
-    const int64_t *col;
+    const void *col;       // int32 when idx32, else int64 (as idx)
     const float *w;
-    const int64_t *idx;
+    const void *idx;
     int64_t nnz, S, F;
     geot_op_t op;
     float *out;
+    int elem = ELEM_F32;   // storage type of src / X
+    int idx32 = 0;         // idx and col hold int32
+    size_t esize() const { return elem == ELEM_F32 ? 4 : 2; }
+    size_t isize() const { return idx32 ? 4 : 8; }
+    bool typed() const { return elem != ELEM_F32 || idx32 != 0; }
 };
 
 struct Resolved {
@@ -236,9 +241,9 @@ void auto_lanes(int64_t F, int V, int *L, int *NT) {
     }
 }
 
-int auto_rows(int64_t nnz, int L, int V, int NT, int ntiles) {
+int auto_rows(int64_t nnz, int L, int V, int NT, int ntiles, int64_t esize) {
     const int64_t G = kBlock / L;
-    const int64_t row_bytes = (int64_t)L * V * NT * 4;
+    const int64_t row_bytes = (int64_t)L * V * NT * esize;
     const int64_t target_rows = std::max<int64_t>(512, (256 * 1024) / row_bytes);
     int64_t K = ceil_div(target_rows, G);
     // keep at least ~1024 blocks in flight when the input allows it
@@ -249,9 +254,9 @@ int auto_rows(int64_t nnz, int L, int V, int NT, int ntiles) {
 
 int widest_vec(const Problem &p) {
     auto aligned = [&](int V) {
-        const uintptr_t m = (uintptr_t)(4 * V - 1);
+        const uintptr_t ms = (uintptr_t)(p.esize() * V - 1), mo = (uintptr_t)(4 * V - 1);
         if (p.F % V != 0) return false;
-        if (((uintptr_t)p.src & m) != 0 || ((uintptr_t)p.out & m) != 0) return false;
+        if (((uintptr_t)p.src & ms) != 0 || ((uintptr_t)p.out & mo) != 0) return false;
         return true;
     };
     if (aligned(4)) return 4;
@@ -265,6 +270,8 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     r->family = c.family == GEOT_FAMILY_AUTO ? GEOT_FAMILY_EP : c.family;
     if (r->family != GEOT_FAMILY_EP && r->family != GEOT_FAMILY_SP)
         return fail(GEOT_ERROR_UNSUPPORTED, "unknown kernel family %d", c.family);
+    if (r->family == GEOT_FAMILY_SP && p.typed())
+        return fail(GEOT_ERROR_UNSUPPORTED, "the segment-parallel family takes fp32 data with int64 ids only");
     const int vmax = widest_vec(p);
     int V = c.vec == 0 ? vmax : c.vec;
     if (!(V == 1 || V == 2 || V == 4)) return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2 or 4");
@@ -286,7 +293,7 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     if (ntiles > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "F too large for lanes*vec");
     r->ntiles = (int)ntiles;
     if (c.rows < 0 || c.rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
-    r->K = c.rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles) : c.rows;
+    r->K = c.rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles, (int64_t)p.esize()) : c.rows;
     const int GW = 64 / L;
     geot_kernel_choice_t cc = c;
     if (from_selector && cc.groups > GW) cc.groups = GW;  // tree leaves are shape-independent
@@ -344,6 +351,10 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
 geot_status_t check_args(const Problem &p) {
     if (p.op != GEOT_OP_SUM && p.op != GEOT_OP_MEAN && p.op != GEOT_OP_MAX)
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)p.op);
+    if (p.elem != ELEM_F32 && p.elem != ELEM_BF16 && p.elem != ELEM_F16)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown data type %d", p.elem);
+    if (p.idx32 != 0 && p.idx32 != 1)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown index type %d", p.idx32);
     if (p.nnz < 0 || p.S < 0 || p.F < 0 || (p.gather && p.num_x_rows < 0))
         return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
     if (p.S == 0 || p.F == 0) return GEOT_SUCCESS;
@@ -362,9 +373,9 @@ geot_status_t check_args(const Problem &p) {
             if (p.num_x_rows == 0) return fail(GEOT_ERROR_INVALID_VALUE, "X has no rows but nnz > 0");
         }
         const size_t src_rows = (size_t)(p.gather ? p.num_x_rows : p.nnz);
-        if (overlaps(p.out, out_bytes, p.src, src_rows * (size_t)p.F * 4) ||
-            overlaps(p.out, out_bytes, p.idx, (size_t)p.nnz * 8) ||
-            overlaps(p.out, out_bytes, p.col, p.gather ? (size_t)p.nnz * 8 : 0) ||
+        if (overlaps(p.out, out_bytes, p.src, src_rows * (size_t)p.F * p.esize()) ||
+            overlaps(p.out, out_bytes, p.idx, (size_t)p.nnz * p.isize()) ||
+            overlaps(p.out, out_bytes, p.col, p.gather ? (size_t)p.nnz * p.isize() : 0) ||
             overlaps(p.out, out_bytes, p.w, p.gather ? (size_t)p.nnz * 4 : 0))
             return fail(GEOT_ERROR_INVALID_VALUE, "out overlaps an input");
     }
@@ -441,6 +452,8 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.num_x_rows = p.num_x_rows;
             a.fill_gaps = 1;
             a.gaps = gaps;
+            a.elem = p.elem;
+            a.idx32 = p.idx32;
         } else {
             a.src = (const float *)(base + off_v[l]);
             a.ld_src = ld_p;
@@ -489,14 +502,15 @@ geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
 
 geot_status_t run_sp_kernels(const Problem &p, const Resolved &r, int64_t *off, GapList gaps,
                              hipStream_t st) {
-    GEOT_HIP(launch_offsets(p.idx, p.nnz, p.S, off, gaps, st), "launch offsets kernel");
+    if (p.typed()) return fail(GEOT_ERROR_UNSUPPORTED, "internal: typed problem in the segment-parallel path");
+    GEOT_HIP(launch_offsets(static_cast<const int64_t *>(p.idx), p.nnz, p.S, off, gaps, st), "launch offsets kernel");
     GEOT_HIP(launch_gap_fill_i64(off, p.S + 1, gaps, st), "launch gap fill kernel");
     SpArgs a;
     memset(&a, 0, sizeof(a));
-    a.src = p.src;
+    a.src = static_cast<const float *>(p.src);
     a.ld_src = p.F;
     a.off = off;
-    a.col = p.col;
+    a.col = static_cast<const int64_t *>(p.col);
     a.w = p.w;
     a.num_x_rows = p.num_x_rows;
     a.S = p.S;
@@ -531,6 +545,7 @@ geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_
         c = *forced;
     } else {
         select_raw(p.nnz, p.S, p.F, p.op, p.gather ? 1 : 0, nullptr, &c);
+        if (p.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
     }
     Resolved r;
     s = resolve(p, c, &r, forced == nullptr);
@@ -629,6 +644,27 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
                  "launch backward kernel");
         return GEOT_SUCCESS;
     }());
+}
+
+geot_status_t geot_segment_reduce_typed(const void *src, geot_dtype_t src_type, const void *sorted_index,
+                                        geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                        int64_t F, geot_op_t op, float *out, void *stream,
+                                        const geot_kernel_choice_t *choice) {
+    Problem p{false, src, 0, nullptr, nullptr, sorted_index, nnz, num_segments, F, op, out};
+    p.elem = (int)src_type;
+    p.idx32 = (int)index_type;
+    return reduce(p, (hipStream_t)stream, choice);
+}
+
+geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows, const void *col,
+                                        const float *weight, const void *sorted_row,
+                                        geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                        geot_op_t op, float *out, void *stream,
+                                        const geot_kernel_choice_t *choice) {
+    Problem p{true, X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, op, out};
+    p.elem = (int)x_type;
+    p.idx32 = (int)index_type;
+    return reduce(p, (hipStream_t)stream, choice);
 }
 
 geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,

@@ -49,6 +49,46 @@ __device__ __forceinline__ void store_vec(float *p, const float *x) {
     }
 }
 
+// Storage types: src / X elements are widened to fp32 when loaded. A bf16 value
+// is the upper half of the fp32 with the same value; fp16 converts exactly.
+template <int E> struct ElemT;
+template <> struct ElemT<ELEM_F32> { using T = float; };
+template <> struct ElemT<ELEM_BF16> { using T = uint16_t; };
+template <> struct ElemT<ELEM_F16> { using T = _Float16; };
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// V consecutive elements at p (aligned to V elements) as fp32
+template <int E, int V>
+__device__ __forceinline__ void load_cvt(const typename ElemT<E>::T *p, float *x) {
+    if constexpr (E == ELEM_F32) {
+        load_vec<V>(p, x);
+    } else if constexpr (E == ELEM_BF16) {
+        if constexpr (V == 4) {
+            const uint2 t = *reinterpret_cast<const uint2 *>(p);
+            x[0] = bf16_lo(t.x); x[1] = bf16_hi(t.x); x[2] = bf16_lo(t.y); x[3] = bf16_hi(t.y);
+        } else if constexpr (V == 2) {
+            const uint32_t t = *reinterpret_cast<const uint32_t *>(p);
+            x[0] = bf16_lo(t); x[1] = bf16_hi(t);
+        } else {
+            x[0] = bf16_lo((uint32_t)*p);
+        }
+    } else {
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+        if constexpr (V == 4) {
+            const h4 t = *reinterpret_cast<const h4 *>(p);
+            x[0] = (float)t.x; x[1] = (float)t.y; x[2] = (float)t.z; x[3] = (float)t.w;
+        } else if constexpr (V == 2) {
+            const h2 t = *reinterpret_cast<const h2 *>(p);
+            x[0] = (float)t.x; x[1] = (float)t.y;
+        } else {
+            x[0] = (float)*p;
+        }
+    }
+}
+
 // Value of `v` held by lane (lane - delta) of the wave; lanes below `delta`
 // get their own value back (callers mask them). ds_bpermute underneath.
 __device__ __forceinline__ float shfl_up_f(float v, int delta) {

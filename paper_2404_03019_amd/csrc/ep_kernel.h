@@ -18,6 +18,14 @@
 // partials are themselves a sorted list of rows with counts, and the same
 // kernel reduces them at the next level until one block remains. No atomics,
 // no output memset, and the result does not depend on timing.
+//
+// src / X may be stored as fp32, bf16 or fp16 and the index (and col) as int64
+// or int32: the first pass widens on load and reduces in fp32; later passes
+// read the fp32 partials. Each (storage, index) pair is instantiated in a
+// translation unit of its own (ep_<storage>_<index>.hip), which this header
+// is included into.
+#pragma once
+
 #include <type_traits>
 
 #include "common.h"
@@ -26,7 +34,7 @@ namespace geot {
 
 namespace {
 
-template <int RED, int MODE, int V, int NT, int L>
+template <int RED, int MODE, int V, int NT, int L, int E, typename I>
 __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     constexpr int NV = V * NT;        // floats per lane
     constexpr int GW = 64 / L;        // row groups per wave
@@ -38,6 +46,12 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     // Segment ids fit 32 bits (the host rejects num_segments >= 2^31). Row counts
     // of one block fit 32 bits; partial levels add counts of many blocks: 64 bits.
     using Cnt = typename std::conditional<MODE == SRC_PIECES, int64_t, int32_t>::type;
+    static_assert(MODE != SRC_PIECES || (E == ELEM_F32 && std::is_same<I, int64_t>::value),
+                  "partials are fp32 with int64 segment ids");
+    using T = typename ElemT<E>::T;
+    const T *src = static_cast<const T *>(a.src);
+    const I *idx = static_cast<const I *>(a.idx);
+    const I *col = static_cast<const I *>(a.col);
 
     __shared__ float s_v[NW][TW];
     __shared__ Cnt s_n[NW];
@@ -124,15 +138,15 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     auto load_term = [&](int64_t r, float *x, Cnt &c) {
         if constexpr (MODE == SRC_ROWS) {
             c = 1;
-            const float *p = a.src + r * a.ld_src;
+            const T *p = src + r * a.ld_src;
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
-                if (cv[j]) load_vec<V>(p + cb[j], x + j * V);
+                if (cv[j]) load_cvt<E, V>(p + cb[j], x + j * V);
                 else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
             }
         } else if constexpr (MODE == SRC_PIECES) {
             c = (Cnt)a.cnt[r];
-            const float *p = a.src + r * a.ld_src;
+            const T *p = src + r * a.ld_src;
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
                 if (cv[j] && c > 0) load_vec<V>(p + cb[j], x + j * V);
@@ -173,10 +187,10 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
 
     int32_t prev = -1, next = -1;
     if (has_rows) {
-        first_seg = (int32_t)a.idx[r0];
+        first_seg = (int32_t)idx[r0];
         cur = first_seg;
-        prev = r0 > 0 ? (int32_t)a.idx[r0 - 1] : -1;
-        next = r1 < a.n ? (int32_t)a.idx[r1] : -1;
+        prev = r0 > 0 ? (int32_t)idx[r0 - 1] : -1;
+        next = r1 < a.n ? (int32_t)idx[r1] : -1;
         if (a.fill_gaps) fill_empty((int64_t)prev + 1, (int64_t)first_seg);
 
         if constexpr (MODE == SRC_GATHER) {
@@ -191,14 +205,14 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             constexpr int UM = kShared ? 1 : UG;
             const int gbase = gw * L;
             int32_t ns[UM];
-            int64_t nc[UM];
+            I nc[UM];
             float nw[UM];
             auto load_meta = [&](int64_t rb) {
 #pragma unroll
                 for (int m = 0; m < UM; ++m) {
                     const int64_t rr = min(rb + (kShared ? (int64_t)min(gl, UG - 1) : (int64_t)m), r1 - 1);
-                    ns[m] = (int32_t)a.idx[rr];
-                    nc[m] = a.col[rr];
+                    ns[m] = (int32_t)idx[rr];
+                    nc[m] = col[rr];
                     nw[m] = a.w ? a.w[rr] : 1.0f;
                 }
             };
@@ -213,21 +227,25 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                     if constexpr (kShared) {
                         s[u] = __shfl(ns[0], gbase + u, 64);
                         wt[u] = __shfl(nw[0], gbase + u, 64);
-                        const int lo = __shfl((int)(uint32_t)(uint64_t)nc[0], gbase + u, 64);
-                        const int hi = __shfl((int)(uint32_t)((uint64_t)nc[0] >> 32), gbase + u, 64);
-                        c = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+                        if constexpr (sizeof(I) == 8) {
+                            const int lo = __shfl((int)(uint32_t)(uint64_t)nc[0], gbase + u, 64);
+                            const int hi = __shfl((int)(uint32_t)((uint64_t)nc[0] >> 32), gbase + u, 64);
+                            c = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+                        } else {
+                            c = (int64_t)__shfl((int)nc[0], gbase + u, 64);
+                        }
                     } else {
                         s[u] = ns[u];
                         wt[u] = nw[u];
-                        c = nc[u];
+                        c = (int64_t)nc[u];
                     }
                     // an out-of-range column reads row 0 and contributes the neutral value
                     const bool ok = (uint64_t)c < (uint64_t)a.num_x_rows;
-                    const float *p = a.src + (ok ? c : 0) * a.ld_src;
+                    const T *p = src + (ok ? c : 0) * a.ld_src;
 #pragma unroll
                     for (int j = 0; j < NT; ++j) {
                         if (cv[j]) {
-                            load_vec<V>(p + cb[j], x[u] + j * V);
+                            load_cvt<E, V>(p + cb[j], x[u] + j * V);
                             if (!ok) {
 #pragma unroll
                                 for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
@@ -254,14 +272,14 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             // back with lane shuffles. Rows past r1 are clamped and not reduced.
             const int gbase = gw * L;
             const int lu = min(gl, U - 1);
-            int32_t nid = (int32_t)a.idx[min(r0 + lu, r1 - 1)];
+            int32_t nid = (int32_t)idx[min(r0 + lu, r1 - 1)];
             for (int64_t r = r0; r < r1; r += U) {
                 const int32_t id = nid;
                 float x[U][NV];
                 Cnt c;
 #pragma unroll
                 for (int u = 0; u < U; ++u) load_term(min(r + u, r1 - 1), x[u], c);
-                if (r + U < r1) nid = (int32_t)a.idx[min(r + U + lu, r1 - 1)];
+                if (r + U < r1) nid = (int32_t)idx[min(r + U + lu, r1 - 1)];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int32_t su = __shfl(id, gbase + u, 64);
@@ -275,7 +293,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 Cnt c[U];
                 float x[U][NV];
 #pragma unroll
-                for (int u = 0; u < U; ++u) s[u] = (int32_t)a.idx[r + u];
+                for (int u = 0; u < U; ++u) s[u] = (int32_t)idx[r + u];
 #pragma unroll
                 for (int u = 0; u < U; ++u) load_term(r + u, x[u], c[u]);
 #pragma unroll
@@ -284,7 +302,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             for (; r < r1; ++r) {
                 float x[NV];
                 Cnt c;
-                const int32_t s = (int32_t)a.idx[r];
+                const int32_t s = (int32_t)idx[r];
                 load_term(r, x, c);
                 step(s, x, c);
             }
@@ -473,60 +491,64 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     }
 }
 
-template <int RED, int MODE, int V, int NT, int L>
+template <int RED, int MODE, int V, int NT, int L, int E, typename I>
 hipError_t launch_one(const EpArgs &a, int64_t nchunks, hipStream_t stream) {
     const int64_t blocks = nchunks * a.ntiles;
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((ep_kernel<RED, MODE, V, NT, L>), dim3((unsigned)blocks), dim3(kBlock), 0,
+    hipLaunchKernelGGL((ep_kernel<RED, MODE, V, NT, L, E, I>), dim3((unsigned)blocks), dim3(kBlock), 0,
                        stream, a);
     return hipGetLastError();
 }
 
-template <int RED, int MODE, int V, int NT>
+template <int RED, int MODE, int V, int NT, int E, typename I>
 hipError_t by_lanes(const EpArgs &a, int L, int64_t nchunks, hipStream_t st) {
     if constexpr (NT > 1) {
         if (L != 64) return hipErrorInvalidValue;
-        return launch_one<RED, MODE, V, NT, 64>(a, nchunks, st);
+        return launch_one<RED, MODE, V, NT, 64, E, I>(a, nchunks, st);
     } else {
         switch (L) {
-            case 1: return launch_one<RED, MODE, V, 1, 1>(a, nchunks, st);
-            case 2: return launch_one<RED, MODE, V, 1, 2>(a, nchunks, st);
-            case 4: return launch_one<RED, MODE, V, 1, 4>(a, nchunks, st);
-            case 8: return launch_one<RED, MODE, V, 1, 8>(a, nchunks, st);
-            case 16: return launch_one<RED, MODE, V, 1, 16>(a, nchunks, st);
-            case 32: return launch_one<RED, MODE, V, 1, 32>(a, nchunks, st);
-            case 64: return launch_one<RED, MODE, V, 1, 64>(a, nchunks, st);
+            case 1: return launch_one<RED, MODE, V, 1, 1, E, I>(a, nchunks, st);
+            case 2: return launch_one<RED, MODE, V, 1, 2, E, I>(a, nchunks, st);
+            case 4: return launch_one<RED, MODE, V, 1, 4, E, I>(a, nchunks, st);
+            case 8: return launch_one<RED, MODE, V, 1, 8, E, I>(a, nchunks, st);
+            case 16: return launch_one<RED, MODE, V, 1, 16, E, I>(a, nchunks, st);
+            case 32: return launch_one<RED, MODE, V, 1, 32, E, I>(a, nchunks, st);
+            case 64: return launch_one<RED, MODE, V, 1, 64, E, I>(a, nchunks, st);
             default: return hipErrorInvalidValue;
         }
     }
 }
 
-template <int RED, int MODE>
+template <int RED, int MODE, int E, typename I>
 hipError_t by_shape(const EpArgs &a, int V, int NT, int L, int64_t nchunks, hipStream_t st) {
-    if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1>(a, L, nchunks, st);
-    if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1>(a, L, nchunks, st);
-    if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2>(a, L, nchunks, st);
-    if (V == 1 && NT == 1) return by_lanes<RED, MODE, 1, 1>(a, L, nchunks, st);
-    if (V == 1 && NT == 2) return by_lanes<RED, MODE, 1, 2>(a, L, nchunks, st);
-    if (V == 1 && NT == 4) return by_lanes<RED, MODE, 1, 4>(a, L, nchunks, st);
+    if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1, E, I>(a, L, nchunks, st);
+    if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1, E, I>(a, L, nchunks, st);
+    if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2, E, I>(a, L, nchunks, st);
+    if (V == 1 && NT == 1) return by_lanes<RED, MODE, 1, 1, E, I>(a, L, nchunks, st);
+    if (V == 1 && NT == 2) return by_lanes<RED, MODE, 1, 2, E, I>(a, L, nchunks, st);
+    if (V == 1 && NT == 4) return by_lanes<RED, MODE, 1, 4, E, I>(a, L, nchunks, st);
     return hipErrorInvalidValue;
 }
 
-}  // namespace
-
-hipError_t launch_ep(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
-                     hipStream_t stream) {
+// The first-pass modes (rows, gather) for storage E and index I; the partial
+// levels (fp32 partials, int64 ids) only where PIECES is set.
+template <int E, typename I, bool PIECES>
+hipError_t ep_dispatch(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
+                       hipStream_t st) {
     if (red == RED_SUM) {
-        if (mode == SRC_ROWS) return by_shape<RED_SUM, SRC_ROWS>(a, V, NT, L, nchunks, stream);
-        if (mode == SRC_GATHER) return by_shape<RED_SUM, SRC_GATHER>(a, V, NT, L, nchunks, stream);
-        if (mode == SRC_PIECES) return by_shape<RED_SUM, SRC_PIECES>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_ROWS) return by_shape<RED_SUM, SRC_ROWS, E, I>(a, V, NT, L, nchunks, st);
+        if (mode == SRC_GATHER) return by_shape<RED_SUM, SRC_GATHER, E, I>(a, V, NT, L, nchunks, st);
+        if constexpr (PIECES)
+            if (mode == SRC_PIECES) return by_shape<RED_SUM, SRC_PIECES, E, I>(a, V, NT, L, nchunks, st);
     } else if (red == RED_MAX) {
-        if (mode == SRC_ROWS) return by_shape<RED_MAX, SRC_ROWS>(a, V, NT, L, nchunks, stream);
-        if (mode == SRC_GATHER) return by_shape<RED_MAX, SRC_GATHER>(a, V, NT, L, nchunks, stream);
-        if (mode == SRC_PIECES) return by_shape<RED_MAX, SRC_PIECES>(a, V, NT, L, nchunks, stream);
+        if (mode == SRC_ROWS) return by_shape<RED_MAX, SRC_ROWS, E, I>(a, V, NT, L, nchunks, st);
+        if (mode == SRC_GATHER) return by_shape<RED_MAX, SRC_GATHER, E, I>(a, V, NT, L, nchunks, st);
+        if constexpr (PIECES)
+            if (mode == SRC_PIECES) return by_shape<RED_MAX, SRC_PIECES, E, I>(a, V, NT, L, nchunks, st);
     }
     return hipErrorInvalidValue;
 }
 
+}  // namespace
 }  // namespace geot

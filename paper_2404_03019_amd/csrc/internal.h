@@ -18,6 +18,10 @@ enum SrcMode : int {
 
 enum RedOp : int { RED_SUM = 0, RED_MAX = 1 };  // mean = sum, divided by the count on store
 
+// Storage type of src / X at level 0 (partials are always fp32 with int64 ids).
+// Elements are widened to fp32 on load, which is exact for all three types.
+enum ElemType : int { ELEM_F32 = 0, ELEM_BF16 = 1, ELEM_F16 = 2 };
+
 // Runs of empty segments longer than kGapRun segments are not written by the
 // kernel that finds them: it appends them to a device list, cut into records
 // of at most kGapChunk segments, and a grid-wide pass writes them afterwards.
@@ -36,11 +40,11 @@ struct GapList {
 // Arguments of one element-parallel pass (level 0 over the input rows, or a
 // later level over the partials of segments that crossed block boundaries).
 struct EpArgs {
-    const float *src;       // rows (SRC_ROWS / SRC_PIECES) or X (SRC_GATHER)
-    int64_t ld_src;         // row stride of src in floats
-    const int64_t *idx;     // sorted segment id of each row
+    const void *src;        // rows (SRC_ROWS / SRC_PIECES) or X (SRC_GATHER), of type `elem`
+    int64_t ld_src;         // row stride of src in elements
+    const void *idx;        // sorted segment id of each row (int32 when idx32, else int64)
     const int64_t *cnt;     // SRC_PIECES: rows represented by each partial
-    const int64_t *col;     // SRC_GATHER: source row of each edge
+    const void *col;        // SRC_GATHER: source row of each edge (same type as idx)
     const float *w;         // SRC_GATHER: edge weight or nullptr
     int64_t num_x_rows;     // SRC_GATHER: rows of X
     int64_t n;              // rows (edges, partials) of this pass
@@ -57,10 +61,22 @@ struct EpArgs {
     int32_t mean;           // divide by the count when a segment is stored
     int32_t fill_gaps;      // write empty segments (level 0 only)
     GapList gaps;           // long runs of empty segments (level 0 only)
+    int32_t elem;           // ElemType of src (SRC_PIECES: ELEM_F32)
+    int32_t idx32;          // idx and col hold int32 (SRC_PIECES: 0)
 };
 
+// Dispatches on (elem, idx32) to the translation unit holding those instantiations.
 hipError_t launch_ep(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks,
                      hipStream_t stream);
+#define GEOT_EP_LAUNCHER(NAME)                                                                  \
+    hipError_t NAME(const EpArgs &a, int red, int mode, int V, int NT, int L, int64_t nchunks, \
+                    hipStream_t stream)
+GEOT_EP_LAUNCHER(launch_ep_f32_i64);
+GEOT_EP_LAUNCHER(launch_ep_f32_i32);
+GEOT_EP_LAUNCHER(launch_ep_bf16_i64);
+GEOT_EP_LAUNCHER(launch_ep_bf16_i32);
+GEOT_EP_LAUNCHER(launch_ep_f16_i64);
+GEOT_EP_LAUNCHER(launch_ep_f16_i32);
 
 // Segment-parallel pass: segment s covers rows off[s] .. off[s+1]-1.
 struct SpArgs {

@@ -63,6 +63,10 @@ def lib() -> ctypes.CDLL:
     L.geot_segment_reduce_with.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, pc]
     L.geot_gather_scatter.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p]
     L.geot_gather_scatter_with.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, pc]
+    L.geot_segment_reduce_typed.argtypes = [p, ctypes.c_int, p, ctypes.c_int, i64, i64, i64, ctypes.c_int,
+                                            p, p, pc]
+    L.geot_gather_scatter_typed.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64, i64,
+                                            ctypes.c_int, p, p, pc]
     L.geot_select.argtypes = [i64, i64, i64, ctypes.c_int, i32, ctypes.POINTER(IndexStats), pc]
     L.geot_index_stats.argtypes = [p, i64, i64, ctypes.POINTER(IndexStats), p]
     L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
@@ -110,7 +114,7 @@ def _dev(t: torch.Tensor, name: str, dtype, ndim):
         raise TypeError(f"{name} must be a torch tensor")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on the GPU")
-    if t.dtype != dtype:
+    if t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
         raise TypeError(f"{name} must be {dtype}")
     if t.dim() != ndim:
         raise ValueError(f"{name} must have {ndim} dimensions")
@@ -143,11 +147,19 @@ class _OnDevice:
         return False
 
 
+# storage types of src / x and index types accepted by the typed entry points
+DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
+INDEX_TYPES = {torch.int64: 0, torch.int32: 1}
+
+
 def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str = "sum",
                    out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
-    """out[s] = reduce over rows i of src with index[i] == s (geot_segment_reduce)."""
-    _dev(src, "src", torch.float32, 2)
-    _dev(index, "index", torch.int64, 1)
+    """out[s] = reduce over rows i of src with index[i] == s (geot_segment_reduce).
+
+    src may be fp32, bf16 or fp16 and index int64 or int32 (geot_segment_reduce_typed);
+    out is fp32 in every case."""
+    _dev(src, "src", tuple(DTYPES), 2)
+    _dev(index, "index", tuple(INDEX_TYPES), 1)
     if index.numel() != src.shape[0]:
         raise ValueError("index must have one entry per row of src")
     if index.device != src.device:
@@ -160,10 +172,15 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
         if tuple(out.shape) != (S, F):
             raise ValueError("out must be [num_segments, F]")
     c = _choice(choice)
+    cp = ctypes.byref(c) if c is not None else None
     with _OnDevice(src.device):
-        st = lib().geot_segment_reduce_with(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
-                                            OPS[reduce], out.data_ptr(), _stream(src.device),
-                                            ctypes.byref(c) if c is not None else None)
+        if src.dtype == torch.float32 and index.dtype == torch.int64:
+            st = lib().geot_segment_reduce_with(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
+                                                OPS[reduce], out.data_ptr(), _stream(src.device), cp)
+        else:
+            st = lib().geot_segment_reduce_typed(src.data_ptr(), DTYPES[src.dtype], index.data_ptr(),
+                                                 INDEX_TYPES[index.dtype], index.numel(), S, F,
+                                                 OPS[reduce], out.data_ptr(), _stream(src.device), cp)
     _raise(st)
     return out
 
@@ -171,10 +188,13 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
 def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
                    row: torch.Tensor, num_rows: int, reduce: str = "sum",
                    out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
-    """out[r] = reduce over edges e with row[e] == r of weight[e] * x[col[e]] (geot_gather_scatter)."""
-    _dev(x, "x", torch.float32, 2)
-    _dev(col, "col", torch.int64, 1)
-    _dev(row, "row", torch.int64, 1)
+    """out[r] = reduce over edges e with row[e] == r of weight[e] * x[col[e]] (geot_gather_scatter).
+
+    x may be fp32, bf16 or fp16 and col / row int64 or int32 (both the same;
+    geot_gather_scatter_typed); weight and out are fp32."""
+    _dev(x, "x", tuple(DTYPES), 2)
+    _dev(col, "col", tuple(INDEX_TYPES), 1)
+    _dev(row, "row", (col.dtype,), 1)
     if weight is not None:
         _dev(weight, "weight", torch.float32, 1)
         if weight.numel() != row.numel():
@@ -190,11 +210,16 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
             raise ValueError("out must be [num_rows, F]")
     c = _choice(choice)
     wp = weight.data_ptr() if weight is not None else None
+    cp = ctypes.byref(c) if c is not None else None
     with _OnDevice(x.device):
-        st = lib().geot_gather_scatter_with(x.data_ptr(), x.shape[0], col.data_ptr(), wp,
-                                            row.data_ptr(), row.numel(), R, F, OPS[reduce],
-                                            out.data_ptr(), _stream(x.device),
-                                            ctypes.byref(c) if c is not None else None)
+        if x.dtype == torch.float32 and col.dtype == torch.int64:
+            st = lib().geot_gather_scatter_with(x.data_ptr(), x.shape[0], col.data_ptr(), wp,
+                                                row.data_ptr(), row.numel(), R, F, OPS[reduce],
+                                                out.data_ptr(), _stream(x.device), cp)
+        else:
+            st = lib().geot_gather_scatter_typed(x.data_ptr(), DTYPES[x.dtype], x.shape[0], col.data_ptr(),
+                                                 wp, row.data_ptr(), INDEX_TYPES[col.dtype], row.numel(),
+                                                 R, F, OPS[reduce], out.data_ptr(), _stream(x.device), cp)
     _raise(st)
     return out
 

@@ -146,3 +146,24 @@ def test_backward_arguments_are_checked_on_the_host():
     assert L.geot_gather_scatter_backward(X, 10, col, None, row, 5, 3, 4, 2, g, None, gx, None, None) == INVALID
     assert L.geot_gather_scatter_backward(X, 10, None, None, row, 5, 3, 4, 0, g, None, gx, None, None) == INVALID
     assert L.geot_gather_scatter_backward(X, 10, col, None, row, 5, 3, 4, 0, g, None, None, None, None) == SUCCESS
+
+
+def test_typed_arguments_are_checked_on_the_host():
+    L = lib()
+    src, idx, out = FAKE, FAKE + (1 << 28), FAKE + (1 << 30)
+    sp = geot.geot._choice(dict(family="sp"))
+    # unknown storage or index type
+    assert L.geot_segment_reduce_typed(src, 3, idx, 0, 10, 4, 8, 0, out, None, None) == INVALID
+    assert "data type" in _detail()
+    assert L.geot_segment_reduce_typed(src, 1, idx, 2, 10, 4, 8, 0, out, None, None) == INVALID
+    assert "index type" in _detail()
+    assert L.geot_gather_scatter_typed(src, 5, 10, idx, None, idx + 4096, 0, 5, 3, 4, 0, out, None,
+                                       None) == INVALID
+    # overlap is judged with the element sizes: 100 x 8 bf16 = 1600 bytes, 100 int32 ids = 400 bytes
+    assert L.geot_segment_reduce_typed(src, 1, idx, 1, 100, 4, 8, 0, src + 1500, None, None) == INVALID
+    assert L.geot_segment_reduce_typed(src, 1, idx, 1, 100, 4, 8, 0, idx + 396, None, None) == INVALID
+    # the segment-parallel family takes fp32 with int64 ids only
+    assert L.geot_segment_reduce_typed(src, 1, idx, 0, 1000, 10, 32, 0, out, None, ctypes.byref(sp)) == UNSUPPORTED
+    assert L.geot_segment_reduce_typed(src, 0, idx, 1, 1000, 10, 32, 0, out, None, ctypes.byref(sp)) == UNSUPPORTED
+    # no-ops as in the fp32 call
+    assert L.geot_segment_reduce_typed(None, 1, None, 1, 0, 0, 5, 0, None, None, None) == SUCCESS

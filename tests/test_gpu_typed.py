@@ -1,0 +1,182 @@
+"""GPU parity of the typed entry points: bf16 / fp16 storage and int32 ids.
+
+A bf16 or fp16 value widens to fp32 exactly, so the oracle runs on the widened
+fp32 copy of the very data the GPU reads (rounded to the storage type on the
+host by torch, then widened on the host): the typed call meets the fp32 bar on
+it, max exact and sum / mean within 1e-5 * sum|terms| + 1e-6. int32 ids are the
+int64 ids narrowed, which changes nothing the oracle sees.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2404_03019_amd as geot
+from gpu_util import compare, oracle_gather, oracle_segment, say
+from workloads import make_config, random_gather_problem, random_problem
+
+pytestmark = pytest.mark.gpu
+OPS = ("sum", "mean", "max")
+DEV = "cuda:0"
+DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
+IT = {"i64": torch.int64, "i32": torch.int32}
+
+
+def stored(a, dt):
+    """(host tensor in the storage type, its exact fp32 widening as numpy)."""
+    t = torch.from_numpy(np.ascontiguousarray(a)).to(DT[dt])
+    return t, t.float().numpy()
+
+
+def ids(a, it):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(IT[it]).to(DEV)
+
+
+CHOICES = [
+    None,
+    dict(family="ep", lanes=64, vec=1, rows=2),   # many blocks: several partial levels
+    dict(family="ep", lanes=1, rows=3),
+    dict(family="ep", lanes=4, vec=2, rows=7),
+]
+
+CASES = [
+    # seed, nnz, S, F, dist, values, empty_frac
+    (11, 30000, 2000, 32, "zipf", "uniform", 0.05),
+    (12, 25000, 400, 1, "lognormal", "normal", 0.1),
+    (13, 20000, 3000, 3, "uniform", "normal", 0.2),
+    (14, 40000, 50, 64, "one_heavy", "normal", 0.3),
+    (15, 9000, 700, 130, "poisson", "uniform", 0.0),
+    (16, 5000, 6000, 8, "uniform", "negative", 0.5),   # more segments than rows, all-negative max
+]
+
+
+@pytest.mark.parametrize("dt,it", [("bf16", "i64"), ("bf16", "i32"), ("f16", "i64"), ("f16", "i32"),
+                                   ("f32", "i32")])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: f"seed{c[0]}_F{c[3]}")
+def test_segment_reduce_typed(dt, it, case):
+    seed, nnz, S, F, dist, values, ef = case
+    p = random_problem(seed, nnz, S, F, dist, values, ef)
+    t, wide = stored(p["src"], dt)
+    s, i = t.to(DEV), ids(p["index"], it)
+    for op in OPS:
+        ref, terms = oracle_segment(wide, p["index"], S, op)
+        for ch in CHOICES:
+            say(f"typed segment {dt}/{it} seed={seed} F={F} {op} choice={ch}")
+            got = geot.segment_reduce(s, i, S, op, choice=ch).cpu().numpy()
+            compare(got, ref, op, terms, f"{dt}/{it} seed={seed} {op} choice={ch}")
+
+
+GATHER_CASES = [
+    # seed, nnz, R, n_x, F, dist, weighted, empty_frac
+    (21, 30000, 1500, 900, 32, "zipf", True, 0.05),
+    (22, 20000, 800, 5000, 5, "lognormal", False, 0.1),
+    (23, 15000, 3000, 64, 128, "uniform", True, 0.0),
+    (24, 8000, 9000, 300, 2, "one_heavy", True, 0.4),
+]
+
+
+@pytest.mark.parametrize("dt,it", [("bf16", "i32"), ("f16", "i64"), ("f32", "i32"), ("bf16", "i64")])
+@pytest.mark.parametrize("case", GATHER_CASES, ids=lambda c: f"seed{c[0]}_F{c[4]}")
+def test_gather_scatter_typed(dt, it, case):
+    seed, nnz, R, nx, F, dist, weighted, ef = case
+    p = random_gather_problem(seed, nnz, R, nx, F, dist, "normal", weighted, ef)
+    t, wide = stored(p["X"], dt)
+    X = t.to(DEV)
+    col, row = ids(p["col"], it), ids(p["index"], it)
+    w = torch.from_numpy(p["weight"]).to(DEV) if p["weight"] is not None else None
+    for op in OPS:
+        ref, terms = oracle_gather(wide, p["col"], p["weight"], p["index"], R, op)
+        for ch in CHOICES:
+            say(f"typed gather {dt}/{it} seed={seed} F={F} {op} choice={ch}")
+            got = geot.gather_scatter(X, col, w, row, R, op, choice=ch).cpu().numpy()
+            compare(got, ref, op, terms, f"gather {dt}/{it} seed={seed} {op} choice={ch}")
+
+
+def test_typed_exact_arithmetic():
+    """Values in {-1, 0, 1} are exact in every storage type and every partial sum
+    is an integer below 2^24: sums are bit-exact at any kernel choice."""
+    p = random_problem(31, 200000, 300, 16, "lognormal", "ternary", 0.1)
+    ref = oracle.segment_reduce(p["src"], p["index"], 300, "sum")
+    for dt in ("bf16", "f16"):
+        t, wide = stored(p["src"], dt)
+        assert np.array_equal(wide, p["src"])
+        for it in ("i64", "i32"):
+            for ch in CHOICES:
+                got = geot.segment_reduce(t.to(DEV), ids(p["index"], it), 300, "sum", choice=ch)
+                assert np.array_equal(got.cpu().numpy(), ref), f"{dt}/{it} choice={ch}"
+
+
+def test_typed_misaligned_storage_and_empty_input():
+    """A bf16 view that starts 2 bytes into its buffer only allows 2-byte loads;
+    nnz == 0 fills zeros as the fp32 call does."""
+    p = random_problem(32, 7000, 500, 4, "zipf", "normal", 0.1)
+    t, wide = stored(p["src"], "bf16")
+    buf = torch.empty(t.numel() + 1, dtype=torch.bfloat16, device=DEV)
+    view = buf[1:].view(t.shape)
+    view.copy_(t.to(DEV))
+    assert view.data_ptr() % 4 == 2
+    for op in OPS:
+        ref, terms = oracle_segment(wide, p["index"], 500, op)
+        got = geot.segment_reduce(view, ids(p["index"], "i32"), 500, op)
+        assert geot.last_choice()["vec"] == 1
+        compare(got.cpu().numpy(), ref, op, terms, f"misaligned bf16 {op}")
+    empty = torch.empty((0, 4), dtype=torch.float16, device=DEV)
+    out = torch.full((9, 4), 7.0, device=DEV)
+    geot.segment_reduce(empty, torch.empty(0, dtype=torch.int32, device=DEV), 9, "max", out=out)
+    assert torch.count_nonzero(out).item() == 0
+
+
+def test_typed_selector_never_runs_segment_parallel():
+    """Where the tree picks the segment-parallel family (fp32, int64), a typed call
+    of the same shape runs the element-parallel family and still matches."""
+    p = random_problem(33, 2_000_000, 100_000, 8, "poisson", "normal", 0.0)
+    geot.segment_reduce(torch.from_numpy(p["src"]).to(DEV), torch.from_numpy(p["index"]).to(DEV),
+                        100_000, "mean")
+    say("fp32 choice", geot.last_choice())
+    t, wide = stored(p["src"], "bf16")
+    got = geot.segment_reduce(t.to(DEV), ids(p["index"], "i32"), 100_000, "mean").cpu().numpy()
+    assert geot.last_choice()["family"] == 1
+    ref, terms = oracle_segment(wide, p["index"], 100_000, "mean")
+    compare(got, ref, "mean", terms, "typed mean, fp32 shape")
+
+
+def _sample_segments(lengths, k, seed):
+    rng = np.random.default_rng(seed)
+    S = lengths.size
+    picks = {0, S - 1, int(np.argmax(lengths)), int(np.argmin(lengths))}
+    picks.update(int(x) for x in np.argsort(lengths)[-8:])
+    picks.update(int(x) for x in rng.choice(S, size=k, replace=False))
+    return np.array(sorted(picks), dtype=np.int64)
+
+
+def test_c3_powerlaw_graph_bf16_i32_sampled():
+    """The power-law workload (114,615,892 x 32) stored as bf16 with int32 ids."""
+    c = make_config("c3_powerlaw_graph")
+    src, idx, S, L = c["src"], c["index"], c["num_segments"], c["lengths"]
+    s = torch.from_numpy(src).to(DEV).to(torch.bfloat16)
+    say("c3 bf16 uploaded")
+    got = geot.segment_reduce(s, ids(idx, "i32"), S, "sum").cpu().numpy()
+    starts = np.concatenate([[0], np.cumsum(L)])
+    for seg in _sample_segments(L, 200, 4):
+        a, b = starts[seg], starts[seg + 1]
+        sub = s[a:b].cpu().float().numpy()   # the stored rows, widened on the host
+        z = np.zeros(b - a, dtype=np.int64)
+        ref = oracle.segment_reduce(sub, z, 1, "sum")
+        compare(got[seg:seg + 1], ref, "sum", oracle.abs_term_sum(sub, z, 1, "sum"),
+                f"c3 bf16 segment {seg} (len {b - a})")
+
+
+def test_c4_spmm_bf16_i32_sampled():
+    """The SpMM workload with X stored as bf16 and int32 col / row."""
+    c = make_config("c4_spmm")
+    X, col, w, row, R, L = c["X"], c["col"], c["weight"], c["index"], c["num_segments"], c["lengths"]
+    t, wide = stored(X, "bf16")
+    say("c4 bf16 uploaded")
+    got = geot.gather_scatter(t.to(DEV), ids(col, "i32"), torch.from_numpy(w).to(DEV), ids(row, "i32"),
+                              R, "sum").cpu().numpy()
+    starts = np.concatenate([[0], np.cumsum(L)])
+    for r in _sample_segments(L, 200, 5):
+        a, b = starts[r], starts[r + 1]
+        z = np.zeros(b - a, dtype=np.int64)
+        ref, terms = oracle_gather(wide, col[a:b], w[a:b], z, 1, "sum")
+        compare(got[r:r + 1], ref, "sum", terms, f"c4 bf16 row {r} (len {b - a})")
