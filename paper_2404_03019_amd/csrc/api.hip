@@ -224,15 +224,19 @@ struct Resolved {
 int max_nt(int V) { return V == 4 ? 1 : (V == 2 ? 2 : 4); }
 
 bool valid_shape(int V, int NT, int L) {
-    if (!(V == 1 || V == 2 || V == 4)) return false;
+    if (!(V == 1 || V == 2 || V == 4 || V == 8)) return false;
     if (!is_pow2(L) || L > 64) return false;
+    if (V == 8) return NT == 1 && L <= 32;
     if (NT == 1) return true;
     return L == 64 && NT <= max_nt(V) && is_pow2(NT);
 }
 
 void auto_lanes(int64_t F, int V, int *L, int *NT) {
     const int64_t vecs = ceil_div(F, V);
-    if (vecs <= 64) {
+    if (V == 8) {  // 16-bit storage: at most 32 lanes, more column tiles beyond 256 columns
+        *L = (int)std::min<int64_t>(32, pow2ceil(vecs));
+        *NT = 1;
+    } else if (vecs <= 64) {
         *L = pow2ceil(vecs);
         *NT = 1;
     } else {
@@ -253,12 +257,14 @@ int auto_rows(int64_t nnz, int L, int V, int NT, int ntiles, int64_t esize) {
 }
 
 int widest_vec(const Problem &p) {
+    // src loads of V elements; fp32 stores of at most 4 floats (V = 8 stores 2 x 4)
     auto aligned = [&](int V) {
-        const uintptr_t ms = (uintptr_t)(p.esize() * V - 1), mo = (uintptr_t)(4 * V - 1);
+        const uintptr_t ms = (uintptr_t)(p.esize() * V - 1), mo = (uintptr_t)(4 * std::min(V, 4) - 1);
         if (p.F % V != 0) return false;
         if (((uintptr_t)p.src & ms) != 0 || ((uintptr_t)p.out & mo) != 0) return false;
         return true;
     };
+    if (p.esize() == 2 && aligned(8)) return 8;
     if (aligned(4)) return 4;
     if (aligned(2)) return 2;
     return 1;
@@ -274,14 +280,24 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
         return fail(GEOT_ERROR_UNSUPPORTED, "the segment-parallel family takes fp32 data with int64 ids only");
     const int vmax = widest_vec(p);
     int V = c.vec == 0 ? vmax : c.vec;
-    if (!(V == 1 || V == 2 || V == 4)) return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2 or 4");
+    int lanes = c.lanes, rows = c.rows;
+    if (from_selector && p.esize() == 2 && c.vec != 0 && vmax > c.vec) {
+        // tree leaves are fit on fp32 shapes: load as wide as the 16-bit storage allows,
+        // keep the columns of one row group and the bytes it reads (rows grow as lanes shrink)
+        V = vmax;
+        if (lanes != 0) lanes = std::max(1, lanes * c.vec / V);
+        if (rows != 0) rows = std::min(4096, rows * V / c.vec);
+    }
+    if (!(V == 1 || V == 2 || V == 4 || V == 8))
+        return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2, 4 or (16-bit storage) 8");
+    if (V == 8 && p.esize() != 2) return fail(GEOT_ERROR_UNSUPPORTED, "vec 8 needs 16-bit storage");
     while (V > vmax) V >>= 1;  // clamp to what F and the pointers allow
     int L, NT;
     auto_lanes(p.F, V, &L, &NT);
-    if (c.lanes != 0) {
-        if (!is_pow2(c.lanes) || c.lanes > 64)
+    if (lanes != 0) {
+        if (!is_pow2(lanes) || lanes > 64)
             return fail(GEOT_ERROR_UNSUPPORTED, "lanes must be a power of two <= 64");
-        L = c.lanes;
+        L = V == 8 ? std::min(lanes, 32) : lanes;
         if (L != 64) NT = 1;
     }
     if (!valid_shape(V, NT, L)) NT = 1;
@@ -292,8 +308,8 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     const int64_t ntiles = ceil_div(p.F, TW);
     if (ntiles > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "F too large for lanes*vec");
     r->ntiles = (int)ntiles;
-    if (c.rows < 0 || c.rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
-    r->K = c.rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles, (int64_t)p.esize()) : c.rows;
+    if (rows < 0 || rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
+    r->K = rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles, (int64_t)p.esize()) : rows;
     const int GW = 64 / L;
     geot_kernel_choice_t cc = c;
     if (from_selector && cc.groups > GW) cc.groups = GW;  // tree leaves are shape-independent
@@ -402,19 +418,27 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
                             const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
                             int64_t ld_p, GapList gaps, hipStream_t st);
 
+// Shape of the passes over fp32 partials: 8-element vectors (16-bit storage)
+// become 4-element vectors over twice the lanes, so the column tiles match.
+void piece_shape(const Resolved &r, int *V, int *L) {
+    *V = r.V == 8 ? 4 : r.V;
+    *L = r.V == 8 ? 2 * r.L : r.L;
+}
+
 geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
     const int64_t G = kBlock / r.L;
-    const int64_t TW = (int64_t)r.L * r.V * r.NT;
+    int Vp, Lp;
+    piece_shape(r, &Vp, &Lp);
+    const int64_t Gp = kBlock / Lp;
     const int64_t ld_p = ceil_div(p.F, 4) * 4;
     std::vector<Level> lv;
     lv.push_back({p.nnz, r.K, ceil_div(p.nnz, G * r.K)});
     while (lv.back().nchunks > 1) {
         const int64_t n = 2 * lv.back().nchunks;
-        const int64_t K = piece_rows_k(n, G);
-        lv.push_back({n, K, ceil_div(n, G * K)});
+        const int64_t K = piece_rows_k(n, Gp);
+        lv.push_back({n, K, ceil_div(n, Gp * K)});
         if (lv.size() > 64) return fail(GEOT_ERROR_HIP, "internal: level count");
     }
-    (void)TW;
     // partial buffers of levels 1..: values, segment ids, counts
     std::vector<size_t> off_v(lv.size(), 0), off_s(lv.size(), 0), off_c(lv.size(), 0);
     size_t bytes = 0;
@@ -479,10 +503,13 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
         hipEvent_t e0 = nullptr, e1 = nullptr;
         const bool prof = l == 0 && prof_take(&e0, &e1);
         if (prof) GEOT_HIP(hipEventRecord(e0, st), "hipEventRecord");
-        GEOT_HIP(launch_ep(a, red, mode, r.V, r.NT, r.L, lv[l].nchunks, st), "launch element-parallel kernel");
+        int V = r.V, L = r.L;
+        if (l > 0) piece_shape(r, &V, &L);
+        GEOT_HIP(launch_ep(a, red, mode, V, r.NT, L, lv[l].nchunks, st), "launch element-parallel kernel");
         if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
         if (l == 0)
-            GEOT_HIP(launch_gap_fill_rows(p.out, p.F, p.F, r.V, (int64_t)r.L * r.V * r.NT, p.S, gaps, st),
+            GEOT_HIP(launch_gap_fill_rows(p.out, p.F, p.F, std::min(r.V, 4), (int64_t)r.L * r.V * r.NT, p.S,
+                                          gaps, st),
                      "launch gap fill kernel");
     }
     return GEOT_SUCCESS;

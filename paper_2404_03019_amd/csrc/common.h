@@ -40,7 +40,10 @@ __device__ __forceinline__ void load_vec(const float *p, float *x) {
 
 template <int V>
 __device__ __forceinline__ void store_vec(float *p, const float *x) {
-    if constexpr (V == 4) {
+    if constexpr (V == 8) {  // 16-bit storage loads 8 elements per lane; fp32 results go out as 2 x 16 B
+        *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<float4 *>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+    } else if constexpr (V == 4) {
         *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
     } else if constexpr (V == 2) {
         *reinterpret_cast<float2 *>(p) = make_float2(x[0], x[1]);
@@ -59,32 +62,44 @@ template <> struct ElemT<ELEM_F16> { using T = _Float16; };
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// V consecutive elements at p (aligned to V elements) as fp32
+// V consecutive elements as loaded: the fp32 values themselves, or the 32-bit
+// words that hold 16-bit elements. Loads fill these; rows are widened where
+// they are reduced, so only the loaded words occupy registers while loads are
+// in flight.
+template <int E, int V> struct Raw { float v[V]; };
+template <int V> struct Raw<ELEM_BF16, V> { uint32_t w[(V + 1) / 2]; };
+template <int V> struct Raw<ELEM_F16, V> { uint32_t w[(V + 1) / 2]; };
+
+// V consecutive elements at p (aligned to V elements)
 template <int E, int V>
-__device__ __forceinline__ void load_cvt(const typename ElemT<E>::T *p, float *x) {
+__device__ __forceinline__ void load_raw(const typename ElemT<E>::T *p, Raw<E, V> &r) {
     if constexpr (E == ELEM_F32) {
-        load_vec<V>(p, x);
-    } else if constexpr (E == ELEM_BF16) {
-        if constexpr (V == 4) {
-            const uint2 t = *reinterpret_cast<const uint2 *>(p);
-            x[0] = bf16_lo(t.x); x[1] = bf16_hi(t.x); x[2] = bf16_lo(t.y); x[3] = bf16_hi(t.y);
-        } else if constexpr (V == 2) {
-            const uint32_t t = *reinterpret_cast<const uint32_t *>(p);
-            x[0] = bf16_lo(t); x[1] = bf16_hi(t);
-        } else {
-            x[0] = bf16_lo((uint32_t)*p);
-        }
+        load_vec<V>(p, r.v);
+    } else if constexpr (V == 8) {
+        const uint4 t = *reinterpret_cast<const uint4 *>(p);
+        r.w[0] = t.x; r.w[1] = t.y; r.w[2] = t.z; r.w[3] = t.w;
+    } else if constexpr (V == 4) {
+        const uint2 t = *reinterpret_cast<const uint2 *>(p);
+        r.w[0] = t.x; r.w[1] = t.y;
+    } else if constexpr (V == 2) {
+        r.w[0] = *reinterpret_cast<const uint32_t *>(p);
     } else {
-        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-        if constexpr (V == 4) {
-            const h4 t = *reinterpret_cast<const h4 *>(p);
-            x[0] = (float)t.x; x[1] = (float)t.y; x[2] = (float)t.z; x[3] = (float)t.w;
-        } else if constexpr (V == 2) {
-            const h2 t = *reinterpret_cast<const h2 *>(p);
-            x[0] = (float)t.x; x[1] = (float)t.y;
+        r.w[0] = (uint32_t)*reinterpret_cast<const uint16_t *>(p);
+    }
+}
+
+// element k of a word pair: the low half comes first in memory
+template <int E, int V>
+__device__ __forceinline__ void widen(const Raw<E, V> &r, float *x) {
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        if constexpr (E == ELEM_F32) {
+            x[k] = r.v[k];
+        } else if constexpr (E == ELEM_BF16) {
+            x[k] = (k & 1) ? bf16_hi(r.w[k / 2]) : bf16_lo(r.w[k / 2]);
         } else {
-            x[0] = (float)*p;
+            const uint16_t h = (uint16_t)((k & 1) ? (r.w[k / 2] >> 16) : (r.w[k / 2] & 0xffffu));
+            x[k] = (float)__builtin_bit_cast(_Float16, h);
         }
     }
 }

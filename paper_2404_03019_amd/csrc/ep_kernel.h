@@ -135,23 +135,30 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             a.pcnt[row] = (int64_t)n;
         }
     };
-    auto load_term = [&](int64_t r, float *x, Cnt &c) {
-        if constexpr (MODE == SRC_ROWS) {
-            c = 1;
-            const T *p = src + r * a.ld_src;
-#pragma unroll
-            for (int j = 0; j < NT; ++j) {
-                if (cv[j]) load_cvt<E, V>(p + cb[j], x + j * V);
-                else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
-            }
-        } else if constexpr (MODE == SRC_PIECES) {
+    // Loads of one row's columns in this tile, as loaded (see Raw); columns
+    // outside the tile are not loaded, and widen_term makes them neutral.
+    using RV = Raw<E, V>;
+    auto load_term = [&](int64_t r, RV *xr, Cnt &c) {
+        const T *p = src + r * a.ld_src;
+        if constexpr (MODE == SRC_PIECES) {
             c = (Cnt)a.cnt[r];
-            const T *p = src + r * a.ld_src;
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
-                if (cv[j] && c > 0) load_vec<V>(p + cb[j], x + j * V);
-                else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
+                if (cv[j] && c > 0) load_raw<E, V>(p + cb[j], xr[j]);
+                else for (int k = 0; k < V; ++k) xr[j].v[k] = neutral;  // partials are fp32
             }
+        } else {
+            c = 1;
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+                if (cv[j]) load_raw<E, V>(p + cb[j], xr[j]);
+        }
+    };
+    auto widen_term = [&](const RV *xr, float *x) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            if (cv[j]) widen<E, V>(xr[j], x + j * V);
+            else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
         }
     };
 
@@ -220,7 +227,8 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             for (int64_t r = r0; r < r1; r += UG) {
                 int32_t s[UG];
                 float wt[UG];
-                float x[UG][NV];
+                bool okv[UG];
+                RV xr[UG][NT];
 #pragma unroll
                 for (int u = 0; u < UG; ++u) {
                     int64_t c;
@@ -240,29 +248,21 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                         c = (int64_t)nc[u];
                     }
                     // an out-of-range column reads row 0 and contributes the neutral value
-                    const bool ok = (uint64_t)c < (uint64_t)a.num_x_rows;
-                    const T *p = src + (ok ? c : 0) * a.ld_src;
+                    okv[u] = (uint64_t)c < (uint64_t)a.num_x_rows;
+                    const T *p = src + (okv[u] ? c : 0) * a.ld_src;
 #pragma unroll
-                    for (int j = 0; j < NT; ++j) {
-                        if (cv[j]) {
-                            load_cvt<E, V>(p + cb[j], x[u] + j * V);
-                            if (!ok) {
-#pragma unroll
-                                for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
-                            }
-                        } else {
-#pragma unroll
-                            for (int k = 0; k < V; ++k) x[u][j * V + k] = neutral;
-                        }
-                    }
+                    for (int j = 0; j < NT; ++j)
+                        if (cv[j]) load_raw<E, V>(p + cb[j], xr[u][j]);
                 }
                 if (r + UG < r1) load_meta(r + UG);
 #pragma unroll
                 for (int u = 0; u < UG; ++u) {
                     if (r + u < r1) {
+                        float x[NV];
+                        widen_term(xr[u], x);
 #pragma unroll
-                        for (int k = 0; k < NV; ++k) x[u][k] = wt[u] * x[u][k];
-                        step(s[u], x[u], 1);
+                        for (int k = 0; k < NV; ++k) x[k] = okv[u] ? wt[u] * x[k] : neutral;
+                        step(s[u], x, 1);
                     }
                 }
             }
@@ -275,15 +275,19 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             int32_t nid = (int32_t)idx[min(r0 + lu, r1 - 1)];
             for (int64_t r = r0; r < r1; r += U) {
                 const int32_t id = nid;
-                float x[U][NV];
+                RV xr[U][NT];
                 Cnt c;
 #pragma unroll
-                for (int u = 0; u < U; ++u) load_term(min(r + u, r1 - 1), x[u], c);
+                for (int u = 0; u < U; ++u) load_term(min(r + u, r1 - 1), xr[u], c);
                 if (r + U < r1) nid = (int32_t)idx[min(r + U + lu, r1 - 1)];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int32_t su = __shfl(id, gbase + u, 64);
-                    if (r + u < r1) step(su, x[u], 1);
+                    if (r + u < r1) {
+                        float x[NV];
+                        widen_term(xr[u], x);
+                        step(su, x, 1);
+                    }
                 }
             }
         } else {
@@ -291,19 +295,25 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             for (; r + U <= r1; r += U) {
                 int32_t s[U];
                 Cnt c[U];
-                float x[U][NV];
+                RV xr[U][NT];
 #pragma unroll
                 for (int u = 0; u < U; ++u) s[u] = (int32_t)idx[r + u];
 #pragma unroll
-                for (int u = 0; u < U; ++u) load_term(r + u, x[u], c[u]);
+                for (int u = 0; u < U; ++u) load_term(r + u, xr[u], c[u]);
 #pragma unroll
-                for (int u = 0; u < U; ++u) step(s[u], x[u], c[u]);
+                for (int u = 0; u < U; ++u) {
+                    float x[NV];
+                    widen_term(xr[u], x);
+                    step(s[u], x, c[u]);
+                }
             }
             for (; r < r1; ++r) {
+                RV xr[NT];
                 float x[NV];
                 Cnt c;
                 const int32_t s = (int32_t)idx[r];
-                load_term(r, x, c);
+                load_term(r, xr, c);
+                widen_term(xr, x);
                 step(s, x, c);
             }
         }
@@ -514,7 +524,9 @@ hipError_t by_lanes(const EpArgs &a, int L, int64_t nchunks, hipStream_t st) {
             case 8: return launch_one<RED, MODE, V, 1, 8, E, I>(a, nchunks, st);
             case 16: return launch_one<RED, MODE, V, 1, 16, E, I>(a, nchunks, st);
             case 32: return launch_one<RED, MODE, V, 1, 32, E, I>(a, nchunks, st);
-            case 64: return launch_one<RED, MODE, V, 1, 64, E, I>(a, nchunks, st);
+            case 64:
+                if constexpr (V == 8) return hipErrorInvalidValue;
+                else return launch_one<RED, MODE, V, 1, 64, E, I>(a, nchunks, st);
             default: return hipErrorInvalidValue;
         }
     }
@@ -522,6 +534,12 @@ hipError_t by_lanes(const EpArgs &a, int L, int64_t nchunks, hipStream_t st) {
 
 template <int RED, int MODE, int E, typename I>
 hipError_t by_shape(const EpArgs &a, int V, int NT, int L, int64_t nchunks, hipStream_t st) {
+    if constexpr (E != ELEM_F32) {  // 16-byte loads of 16-bit storage, at most 32 lanes
+        if (V == 8 && NT == 1) {
+            if (L > 32) return hipErrorInvalidValue;
+            return by_lanes<RED, MODE, 8, 1, E, I>(a, L, nchunks, st);
+        }
+    }
     if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1, E, I>(a, L, nchunks, st);
     if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1, E, I>(a, L, nchunks, st);
     if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2, E, I>(a, L, nchunks, st);

@@ -97,7 +97,7 @@ def test_gather_arguments_are_checked():
 
 @pytest.mark.parametrize("choice", [
     dict(family=7), dict(vec=3), dict(lanes=3), dict(lanes=128), dict(rows=-1), dict(rows=5000),
-    dict(family=2, lanes=16, groups=8), dict(family=2, groups=3), dict(flags=1),
+    dict(family=2, lanes=16, groups=8), dict(family=2, groups=3), dict(flags=1), dict(vec=8),
 ])
 def test_impossible_forced_choices_are_unsupported(choice):
     c = geot.geot._choice(choice)

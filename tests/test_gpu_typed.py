@@ -37,7 +37,14 @@ CHOICES = [
     dict(family="ep", lanes=64, vec=1, rows=2),   # many blocks: several partial levels
     dict(family="ep", lanes=1, rows=3),
     dict(family="ep", lanes=4, vec=2, rows=7),
+    dict(family="ep", lanes=2, vec=8, rows=5),    # 16-byte loads of 16-bit storage
+    dict(family="ep", lanes=64, vec=8, rows=1),   # lanes capped at 32; partial levels run 4-wide on 64 lanes
 ]
+
+
+def choices(dt):
+    """vec 8 is for 16-bit storage only (fp32 data with vec 8 is refused)."""
+    return [c for c in CHOICES if dt != "f32" or c is None or c.get("vec") != 8]
 
 CASES = [
     # seed, nnz, S, F, dist, values, empty_frac
@@ -47,6 +54,7 @@ CASES = [
     (14, 40000, 50, 64, "one_heavy", "normal", 0.3),
     (15, 9000, 700, 130, "poisson", "uniform", 0.0),
     (16, 5000, 6000, 8, "uniform", "negative", 0.5),   # more segments than rows, all-negative max
+    (17, 6000, 300, 512, "zipf", "normal", 0.1),       # two column tiles of 256 at vec 8
 ]
 
 
@@ -60,7 +68,7 @@ def test_segment_reduce_typed(dt, it, case):
     s, i = t.to(DEV), ids(p["index"], it)
     for op in OPS:
         ref, terms = oracle_segment(wide, p["index"], S, op)
-        for ch in CHOICES:
+        for ch in choices(dt):
             say(f"typed segment {dt}/{it} seed={seed} F={F} {op} choice={ch}")
             got = geot.segment_reduce(s, i, S, op, choice=ch).cpu().numpy()
             compare(got, ref, op, terms, f"{dt}/{it} seed={seed} {op} choice={ch}")
@@ -86,7 +94,7 @@ def test_gather_scatter_typed(dt, it, case):
     w = torch.from_numpy(p["weight"]).to(DEV) if p["weight"] is not None else None
     for op in OPS:
         ref, terms = oracle_gather(wide, p["col"], p["weight"], p["index"], R, op)
-        for ch in CHOICES:
+        for ch in choices(dt):
             say(f"typed gather {dt}/{it} seed={seed} F={F} {op} choice={ch}")
             got = geot.gather_scatter(X, col, w, row, R, op, choice=ch).cpu().numpy()
             compare(got, ref, op, terms, f"gather {dt}/{it} seed={seed} {op} choice={ch}")
@@ -156,6 +164,7 @@ def test_c3_powerlaw_graph_bf16_i32_sampled():
     s = torch.from_numpy(src).to(DEV).to(torch.bfloat16)
     say("c3 bf16 uploaded")
     got = geot.segment_reduce(s, ids(idx, "i32"), S, "sum").cpu().numpy()
+    assert geot.last_choice()["vec"] == 8
     starts = np.concatenate([[0], np.cumsum(L)])
     for seg in _sample_segments(L, 200, 4):
         a, b = starts[seg], starts[seg + 1]
