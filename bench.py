@@ -137,7 +137,8 @@ def suite(reps: int):
     """One JSON line per measurement: every named workload and op, the gradients on the two
     large workloads, and a two-layer graph-convolution training step (library autograd vs the
     same model with torch's index_add). Median over `reps` HIP-event timings per entry; for
-    inputs under 1 GB a 512 MB write flushes the MALL before each repetition."""
+    inputs under 1 GB a 512 MB read evicts them from the MALL before each repetition (a read,
+    so no dirty lines are written back inside the timed call)."""
     import numpy as np
     import torch
 
@@ -149,7 +150,7 @@ def suite(reps: int):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     geot.lib()
-    flush = torch.empty(1 << 27, device=dev)
+    flush = torch.ones(1 << 27, device=dev)
 
     def timed(fn, nbytes_in):
         cold = nbytes_in < (1 << 30)
@@ -158,7 +159,7 @@ def suite(reps: int):
         ts = []
         for _ in range(reps):
             if cold:
-                flush.fill_(1.0)
+                flush.sum()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record()

@@ -235,7 +235,10 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
 
 /* The selector (Section III-C: a decision tree over O(1) input features,
  * compiled to if/else). Pure host function: no device access.
- *   gather  nonzero for geot_gather_scatter, zero for geot_segment_reduce
+ *   gather  0 for geot_segment_reduce; for geot_gather_scatter 1 with edge
+ *           weights and 2 without (any other nonzero value counts as 1). The
+ *           two operations have trees of their own, and the fused one splits
+ *           on whether there are weights
  *   stats   optional (NULL allowed); when given, the length variance and the
  *           longest segment join the features
  * Writes a fully specified choice to *out.                                  */

@@ -281,12 +281,14 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     const int vmax = widest_vec(p);
     int V = c.vec == 0 ? vmax : c.vec;
     int lanes = c.lanes, rows = c.rows;
-    if (from_selector && p.esize() == 2 && c.vec != 0 && vmax > c.vec) {
-        // tree leaves are fit on fp32 shapes: load as wide as the 16-bit storage allows,
-        // keep the columns of one row group and the bytes it reads (rows grow as lanes shrink)
-        V = vmax;
-        if (lanes != 0) lanes = std::max(1, lanes * c.vec / V);
-        if (rows != 0) rows = std::min(4096, rows * V / c.vec);
+    if (from_selector && p.esize() == 2 && vmax == 8) {
+        // tree leaves are fit on fp32 shapes, which load 4 floats here (F % 8 == 0): load 8
+        // 16-bit elements instead, keeping the columns of one row group and the bytes it
+        // reads (half the lanes, twice the rows)
+        const int v32 = c.vec != 0 ? std::min(c.vec, 4) : 4;
+        V = 8;
+        if (lanes != 0) lanes = std::max(1, lanes * v32 / V);
+        if (rows != 0) rows = std::min(4096, rows * V / v32);
     }
     if (!(V == 1 || V == 2 || V == 4 || V == 8))
         return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2, 4 or (16-bit storage) 8");
@@ -571,7 +573,7 @@ geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_
     if (forced) {
         c = *forced;
     } else {
-        select_raw(p.nnz, p.S, p.F, p.op, p.gather ? 1 : 0, nullptr, &c);
+        select_raw(p.nnz, p.S, p.F, p.op, p.gather ? (p.w ? 1 : 2) : 0, nullptr, &c);
         if (p.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
     }
     Resolved r;
@@ -802,7 +804,7 @@ geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
     if (nnz < 0 || num_segments < 0 || F < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
     geot_kernel_choice_t c;
-    select_raw(nnz, num_segments, F, op, gather ? 1 : 0, stats, &c);
+    select_raw(nnz, num_segments, F, op, gather == 0 ? 0 : (gather == 2 ? 2 : 1), stats, &c);
     if (F == 0) {
         *out = c;
         return GEOT_SUCCESS;

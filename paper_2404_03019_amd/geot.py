@@ -302,15 +302,16 @@ def check_index(index: torch.Tensor, num_segments: int, col: torch.Tensor | None
 
 
 def select(nnz: int, num_segments: int, F: int, reduce: str = "sum", gather: bool = False,
-           stats: dict | None = None) -> dict:
-    """The selector's kernel choice for a shape (geot_select; host only)."""
+           stats: dict | None = None, weighted: bool = True) -> dict:
+    """The selector's kernel choice for a shape (geot_select; host only). `weighted`
+    says whether a fused gather has edge weights."""
     c = KernelChoice()
     sp = None
     if stats is not None:
         s = IndexStats(**{k: stats[k] for k, _ in IndexStats._fields_})
         sp = ctypes.byref(s)
-    _raise(lib().geot_select(int(nnz), int(num_segments), int(F), OPS[reduce], int(bool(gather)),
-                             sp, ctypes.byref(c)))
+    g = 0 if not gather else (1 if weighted else 2)
+    _raise(lib().geot_select(int(nnz), int(num_segments), int(F), OPS[reduce], g, sp, ctypes.byref(c)))
     return c.as_dict()
 
 

@@ -13,11 +13,17 @@ recipe (Top-1 labels and a scikit-learn multi-output regressor of depth 5,
 leaves rounded to valid parameters) is fitted too and reported as an
 ablation, beside the hand-written rule.
 
-Two trees, as the paper keeps two:
+Two trees per operation, as the paper keeps two, and one pair for each of the
+two operations (segment reduction, and the fused gather form, whose inputs
+also say whether edges carry weights), since their best configurations
+differ:
   * ``nostats``: O(1) features only (log2 nnz, log2 num_segments, F,
-    log2 mean length, op, gather); chooses among element-parallel row runs;
+    log2 mean length, op; for the fused form also weighted); chooses among
+    element-parallel row runs;
   * ``stats``: adds the length cv and log2(longest / mean) from
     geot_index_stats; chooses the family and its parameters.
+A single pair over both operations (with gather and weighted as features) is
+fitted too and reported as an ablation.
 
 Usage: python -m paper_2404_03019_amd.tune.fit [--db perfdb.jsonl] [--out ../csrc/selector_generated.h]
 """
@@ -48,16 +54,40 @@ def load(db: str):
     return list(inst.values())
 
 
-def feature_row(f: dict, stats: bool):
+KINDS = ("segment", "gather")
+
+
+def kind_of(e) -> str:
+    return "gather" if e["instance"]["gather"] else "segment"
+
+
+def weighted_of(e) -> int:
+    """Fused-form inputs of the first sweeps carry no flag: they all had weights."""
+    inst = e["instance"]
+    return int(inst.get("weighted", inst["gather"])) if inst["gather"] else 0
+
+
+def feature_row(e, stats: bool, kind: str | None = None):
+    """Features of input e for the trees of `kind` (None: the single-tree ablation)."""
+    f = e["features"]
     row = [math.log2(max(f["nnz"], 1)), math.log2(max(f["S"], 1)), float(f["F"]),
-           math.log2(max(f["mean"], 1e-9)), 1.0 if f["op"] == "max" else 0.0, float(f["gather"])]
+           math.log2(max(f["mean"], 1e-9)), 1.0 if f["op"] == "max" else 0.0]
+    if kind is None:
+        row += [float(f["gather"]), float(weighted_of(e))]
+    elif kind == "gather":
+        row += [float(weighted_of(e))]
     if stats:
         row += [float(f["cv"]), math.log2(max(f["max_rel"], 1e-9))]
     return row
 
 
-FEATURES_NOSTATS = ["lnnz", "lS", "F", "lmean", "opmax", "gather"]
-FEATURES_STATS = FEATURES_NOSTATS + ["cv", "lmaxrel"]
+def feature_names(stats: bool, kind: str | None = None):
+    names = ["lnnz", "lS", "F", "lmean", "opmax"]
+    if kind is None:
+        names += ["isgather", "weighted"]
+    elif kind == "gather":
+        names += ["weighted"]
+    return names + (["cv", "lmaxrel"] if stats else [])
 
 
 def best_of(e, fam=None):
@@ -158,7 +188,7 @@ def cost_matrix(data, cands):
             t = e["times"].get(key)
             if t is not None and t > 0 and tb > 0:
                 C[i, j] = min(MISSING_COST, math.log(t / tb))
-        if e["instance"]["id"] >= 10000:
+        if 10000 <= e["instance"]["id"] < 20000:
             C[i] *= NAMED_WEIGHT
     return C
 
@@ -228,29 +258,53 @@ def emit_cost_tree(tree, names, cands, indent):
     return lines
 
 
-def build(db: str):
-    """Load the database and fit both trees. Returns (nostats_tree, stats_tree, data, Xn, Xs)."""
+class Fitted:
+    """The four trees (kind x stats) fitted on the database, and the single-pair ablation."""
+
+    def __init__(self, data):
+        self.data = data
+        self.trees, self.single = {}, {}
+        for stats in (False, True):
+            cands = candidate_space(stats)
+            for kind in KINDS:
+                sub = [e for e in data if kind_of(e) == kind]
+                X = [feature_row(e, stats, kind) for e in sub]
+                self.trees[(kind, stats)] = CostTree().fit(X, cost_matrix(sub, cands))
+            self.single[stats] = CostTree().fit([feature_row(e, stats) for e in data],
+                                                cost_matrix(data, cands))
+
+    def choose(self, e, stats: bool):
+        """(family, rows, groups) the emitted selector gives input e."""
+        kind = kind_of(e)
+        return candidate_space(stats)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
+
+    def choose_single(self, e, stats: bool):
+        return candidate_space(stats)[self.single[stats].predict_one(feature_row(e, stats))]
+
+
+def build(db: str) -> Fitted:
+    """Load the database (inputs with at least one measured element-parallel row run) and fit."""
     data = load(db)
     data = [e for e in data if any(e["choices"][c]["family"] == 1 and e["choices"][c].get("rows", 0) > 0
                                    for c in e["times"])]
-    Xn = [feature_row(e["features"], False) for e in data]
-    Xs = [feature_row(e["features"], True) for e in data]
-    tn = CostTree().fit(Xn, cost_matrix(data, candidate_space(False)))
-    ts = CostTree().fit(Xs, cost_matrix(data, candidate_space(True)))
-    return tn, ts, data, Xn, Xs
+    return Fitted(data)
 
 
-def render(tn, ts, n_inputs: int) -> str:
-    """The C++ header text of both trees."""
+def render(fitted: Fitted) -> str:
+    """The C++ header text of the four trees."""
+    n_seg = sum(1 for e in fitted.data if kind_of(e) == "segment")
+    n_gat = len(fitted.data) - n_seg
     body = ["// Kernel selection rules compiled into libgeot_hip (Section III-C: a decision tree",
             "// over cheap input features, emitted as if/else). GENERATED by",
             "// paper_2404_03019_amd/tune/fit.py from the MI355X performance database",
             "// paper_2404_03019_amd/tune/perfdb.jsonl; do not edit by hand.",
             "//",
-            f"// Training inputs: {n_inputs}. Depth <= {MAX_DEPTH}. Each leaf is the candidate with the",
-            "// least total log-slowdown over the inputs reaching it. out[0] family (1 element-",
-            "// parallel, 2 segment-parallel), out[3] rows per row group, out[4] row groups per",
-            "// segment (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape.",
+            f"// Training inputs: {n_seg} segment reductions, {n_gat} fused gather forms. One pair of",
+            f"// trees per operation, depth <= {MAX_DEPTH}. Each leaf is the candidate with the least",
+            "// total log-slowdown over the inputs reaching it. out[0] family (1 element-parallel,",
+            "// 2 segment-parallel), out[3] rows per row group, out[4] row groups per segment",
+            "// (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape.",
+            "// gather: 0 segment reduction, 1 fused form with edge weights, 2 without.",
             "#pragma once", "", "#include <cmath>", "#include <cstdint>", "", "namespace geot {", "",
             "static inline void tree_select(double nnz, double num_segments, double F, int op, int gather,",
             "                               int has_stats, double cv, double max_rel, int32_t out[5]) {",
@@ -259,13 +313,16 @@ def render(tn, ts, n_inputs: int) -> str:
             "    const double mean = num_segments > 0.0 ? nnz / num_segments : 0.0;",
             "    const double lmean = std::log2(mean > 1e-9 ? mean : 1e-9);",
             "    const double opmax = op == 2 ? 1.0 : 0.0;",
+            "    const double weighted = gather == 1 ? 1.0 : 0.0;",
             "    const double lmaxrel = std::log2(max_rel > 1e-9 ? max_rel : 1e-9);",
-            "    (void)lnnz; (void)lS; (void)F; (void)lmean; (void)opmax; (void)cv; (void)lmaxrel; (void)gather;",
-            "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0;",
-            "    if (!has_stats) {"]
-    body += emit_cost_tree(tn, FEATURES_NOSTATS, candidate_space(False), 8)
-    body += ["    } else {"]
-    body += emit_cost_tree(ts, FEATURES_STATS, candidate_space(True), 8)
+            "    (void)lnnz; (void)lS; (void)F; (void)lmean; (void)opmax; (void)weighted; (void)cv; (void)lmaxrel;",
+            "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0;"]
+    for kind, cond, close in (("segment", "    if (gather == 0) {", None), ("gather", "    } else {", "    }")):
+        body += [cond, "        if (!has_stats) {"]
+        body += emit_cost_tree(fitted.trees[(kind, False)], feature_names(False, kind), candidate_space(False), 12)
+        body += ["        } else {"]
+        body += emit_cost_tree(fitted.trees[(kind, True)], feature_names(True, kind), candidate_space(True), 12)
+        body += ["        }"]
     body += ["    }", "}", "", "}  // namespace geot", ""]
     return "\n".join(body)
 
@@ -277,23 +334,33 @@ def _time_of(e, cand):
     return e["times"].get(key, math.nan)
 
 
-def evaluate(tn, ts, data, Xn, Xs):
-    """Per input: chosen time / best measured time, for the trees, the paper's recipe and the hand rule."""
+def evaluate(fitted: Fitted):
+    """Per input: chosen time / best measured time, for the per-operation trees, the single
+    pair (ablation), the paper's recipe (per operation, ablation) and the hand rule."""
     cn, cs = candidate_space(False), candidate_space(True)
-    # the paper's recipe as an ablation: Top-1 labels, multi-output regressor, rounded leaves
-    pn = fit_tree(Xn, [[targets(e)[1]] for e in data])
-    ps = fit_tree(Xs, [list(targets(e)) for e in data])
+    # the paper's recipe: Top-1 labels, multi-output regressor, rounded leaves
+    paper = {}
+    for kind in KINDS:
+        sub = [e for e in fitted.data if kind_of(e) == kind]
+        paper[(kind, False)] = fit_tree([feature_row(e, False, kind) for e in sub], [[targets(e)[1]] for e in sub])
+        paper[(kind, True)] = fit_tree([feature_row(e, True, kind) for e in sub], [list(targets(e)) for e in sub])
     rep = []
-    for e, xn, xs in zip(data, Xn, Xs):
+    for e in fitted.data:
         tb, _ = best_of(e)
         tbe, _ = best_of(e, 1)
+        kind = kind_of(e)
         rep.append(dict(
             name=e["instance"]["dist"], id=e["instance"]["id"], F=e["instance"]["F"],
-            op=e["instance"]["op"], gather=e["instance"]["gather"], nnz=e["features"]["nnz"], best=tb,
-            nostats=_time_of(e, cn[tn.predict_one(xn)]) / tbe,
-            stats=_time_of(e, cs[ts.predict_one(xs)]) / tb,
-            paper_nostats=e["times"].get(predict_cand(pn, xn, False, e), math.nan) / tbe,
-            paper_stats=e["times"].get(predict_cand(ps, xs, True, e), math.nan) / tb,
+            op=e["instance"]["op"], gather=e["instance"]["gather"], weighted=weighted_of(e),
+            nnz=e["features"]["nnz"], best=tb,
+            nostats=_time_of(e, fitted.choose(e, False)) / tbe,
+            stats=_time_of(e, fitted.choose(e, True)) / tb,
+            single_nostats=_time_of(e, fitted.choose_single(e, False)) / tbe,
+            single_stats=_time_of(e, fitted.choose_single(e, True)) / tb,
+            paper_nostats=e["times"].get(predict_cand(paper[(kind, False)], feature_row(e, False, kind), False, e),
+                                         math.nan) / tbe,
+            paper_stats=e["times"].get(predict_cand(paper[(kind, True)], feature_row(e, True, kind), True, e),
+                                       math.nan) / tb,
             hand=e["times"].get("f1_r0_g0", math.nan) / tbe))
     return rep
 
@@ -303,25 +370,33 @@ def main():
     ap.add_argument("--db", default=DEFAULT_DB)
     ap.add_argument("--out", default=DEFAULT_OUT)
     args = ap.parse_args()
-    tn, ts, data, Xn, Xs = build(args.db)
-    open(args.out, "w").write(render(tn, ts, len(data)))
-    rep = evaluate(tn, ts, data, Xn, Xs)
+    fitted = build(args.db)
+    open(args.out, "w").write(render(fitted))
+    rep = evaluate(fitted)
 
     def gm(xs):
         xs = [x for x in xs if x == x and x > 0]
         return math.exp(sum(math.log(x) for x in xs) / len(xs)) if xs else math.nan
 
-    print(f"inputs {len(data)}; wrote {args.out}")
-    for k in ("nostats", "stats", "paper_nostats", "paper_stats", "hand"):
-        v = [r[k] for r in rep]
-        w = sum(1 for x in v if x == x and x <= 1.10)
-        print(f"{k:14s} geomean slowdown vs best {gm(v):.3f}  max {np.nanmax(v):.3f}  within 10%: {w}/{len(v)}")
+    print(f"inputs {len(fitted.data)}; wrote {args.out}")
+    groups = [("all", lambda r: True), ("segment", lambda r: not r["gather"]),
+              ("gather weighted", lambda r: r["gather"] and r["weighted"]),
+              ("gather unweighted", lambda r: r["gather"] and not r["weighted"])]
+    for gname, sel in groups:
+        sub = [r for r in rep if sel(r)]
+        print(f"-- {gname} ({len(sub)} inputs)")
+        if not sub:
+            continue
+        for k in ("nostats", "stats", "single_nostats", "single_stats", "paper_nostats", "paper_stats", "hand"):
+            v = [r[k] for r in sub]
+            w = sum(1 for x in v if x == x and x <= 1.10)
+            print(f"   {k:15s} geomean slowdown vs best {gm(v):.3f}  max {np.nanmax(v):.3f}  within 10%: {w}/{len(v)}")
     print("named workloads:")
     for r in rep:
-        if r["id"] >= 10000:
-            print(f"  {r['name']:20s} F={r['F']:3d} {r['op']:4s} best {r['best']:.3f} ms  "
-                  f"nostats x{r['nostats']:.3f}  stats x{r['stats']:.3f}  paper x{r['paper_stats']:.3f}  "
-                  f"hand x{r['hand']:.3f}")
+        if r["id"] >= 10000 and r["id"] < 20000:
+            print(f"  {r['name']:20s} F={r['F']:3d} {r['op']:4s} w={r['weighted']} best {r['best']:.3f} ms  "
+                  f"nostats x{r['nostats']:.3f}  stats x{r['stats']:.3f}  single x{r['single_nostats']:.3f}  "
+                  f"paper x{r['paper_stats']:.3f}  hand x{r['hand']:.3f}")
     json.dump(rep, open(os.path.join(HERE, "fit_report.json"), "w"), indent=0)
 
 

@@ -1,7 +1,8 @@
 """Offline performance database for the kernel selector (Section III-C, "data-aware config rules").
 
 For every instance of a seeded synthetic family (length distribution, nnz,
-mean segment length, F, op, plain or fused gather) this times every
+mean segment length, F, op, plain or fused gather, with or without edge
+weights) this times every
 candidate kernel choice through the library's forced-choice entry points and
 appends one JSON line per (instance, candidate) to a performance database.
 Already-measured keys are skipped, so an interrupted sweep resumes.
@@ -75,8 +76,29 @@ def instances(n: int, seed: int):
     return out
 
 
+def gather_instances(n: int, seed: int):
+    """A seeded list of fused-form instances, half of them without edge weights
+    (the unweighted index_segment_reduce and the weighted SpMM form)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dist = DISTS[rng.integers(len(DISTS))]
+        F = int(FS[rng.integers(len(FS))])
+        weighted = int(rng.random() < 0.5)
+        u = rng.random()
+        op = "max" if u < 0.3 else ("mean" if u < 0.45 else "sum")
+        mean = float(2.0 ** rng.uniform(0.5, 10.0))
+        max_nnz = min(1.2e8, 3e9 / (4 * F + 20))
+        nnz = int(min(max_nnz, 10 ** rng.uniform(4.0, 8.1)))
+        S = max(1, int(round(nnz / mean)))
+        out.append(dict(id=20000 + i, dist=dist, nnz=nnz, S=S, F=F, op=op, gather=1, weighted=weighted,
+                        seed=seed * 100003 + i))
+    return out
+
+
 def named_instances():
-    """The five named workloads (lengths from their recipes), each op they are run with."""
+    """The five named workloads (lengths from their recipes), each op they are run with,
+    and the SpMM workload without weights and with max."""
     from workloads.generators import C2_FEATURES
 
     out = []
@@ -84,8 +106,12 @@ def named_instances():
              ("c4_spmm", 128, "sum", 1), ("c5_pointcloud_knn", 64, "mean", 0),
              ("c5_pointcloud_knn", 64, "max", 0)]
     specs += [("c2_poisson_fsweep", F, op, 0) for F in C2_FEATURES for op in ("sum", "max")]
-    for i, (name, F, op, gather) in enumerate(specs):
-        out.append(dict(id=10000 + i, dist=name, nnz=0, S=0, F=F, op=op, gather=gather, seed=i))
+    specs += [("c4_spmm", 128, "sum", 1, 0), ("c4_spmm", 128, "max", 1, 1)]
+    for i, spec in enumerate(specs):
+        name, F, op, gather = spec[:4]
+        weighted = spec[4] if len(spec) > 4 else gather
+        out.append(dict(id=10000 + i, dist=name, nnz=0, S=0, F=F, op=op, gather=gather, weighted=weighted,
+                        seed=i))
     return out
 
 
@@ -113,6 +139,8 @@ def main():
     ap.add_argument("--out", default=os.path.join(HERE, "perfdb.jsonl"))
     ap.add_argument("--n", type=int, default=240)
     ap.add_argument("--seed", type=int, default=2024)
+    ap.add_argument("--gather-n", type=int, default=120)
+    ap.add_argument("--gather-seed", type=int, default=4048)
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--budget-s", type=float, default=900.0, help="stop after this many seconds")
     args = ap.parse_args()
@@ -129,15 +157,20 @@ def main():
                 done.add((r["instance"]["id"], r["instance"]["seed"], r["cand"]))
             except (ValueError, KeyError):
                 pass
+    done_inst = {(i, s) for (i, s, _) in done}
     dev = torch.device("cuda:0")
     gen = torch.Generator(device=dev)
     t_start = time.time()
     with open(args.out, "a") as fout:
-        for inst in named_instances() + instances(args.n, args.seed):
+        for inst in named_instances() + instances(args.n, args.seed) + \
+                gather_instances(args.gather_n, args.gather_seed):
             if time.time() - t_start > args.budget_s:
                 print("budget reached", flush=True)
                 break
-            if inst["id"] >= 10000:
+            if (inst["id"], inst["seed"]) in done_inst:
+                continue
+            weighted = inst.get("weighted", inst["gather"])
+            if 10000 <= inst["id"] < 20000:  # a named workload: lengths from its recipe
                 from workloads import config_lengths
 
                 _, L = config_lengths(inst["dist"])
@@ -152,9 +185,9 @@ def main():
                 nx = max(1, S)
                 X = torch.randn(nx, F, device=dev, generator=gen)
                 col = torch.randint(0, nx, (nnz,), device=dev, generator=gen)
-                w = torch.rand(nnz, device=dev, generator=gen)
+                w = torch.rand(nnz, device=dev, generator=gen) if weighted else None
                 out = torch.empty(S, F, device=dev)
-                nbytes = nnz * (20 + 4 * F) + S * F * 4
+                nbytes = nnz * (16 + 4 * weighted + 4 * F) + S * F * 4
 
                 def call(c):
                     geot.gather_scatter(X, col, w, idx, S, inst["op"], out=out, choice=c)
@@ -167,7 +200,7 @@ def main():
                     geot.segment_reduce(src, idx, S, inst["op"], out=out, choice=c)
             st = geot.index_stats(idx, S)
             mean = nnz / S
-            feats = dict(nnz=nnz, S=S, F=F, mean=mean, op=inst["op"], gather=inst["gather"],
+            feats = dict(nnz=nnz, S=S, F=F, mean=mean, op=inst["op"], gather=inst["gather"], weighted=weighted,
                          cv=math.sqrt(st["var_len"]) / mean if mean > 0 else 0.0,
                          max_rel=st["max_len"] / mean if mean > 0 else 0.0)
             best = math.inf

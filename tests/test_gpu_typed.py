@@ -164,7 +164,9 @@ def test_c3_powerlaw_graph_bf16_i32_sampled():
     s = torch.from_numpy(src).to(DEV).to(torch.bfloat16)
     say("c3 bf16 uploaded")
     got = geot.segment_reduce(s, ids(idx, "i32"), S, "sum").cpu().numpy()
-    assert geot.last_choice()["vec"] == 8
+    # the fp32 leaf for this shape, loaded 8 wide: half the lanes, twice the rows
+    fp, lc = geot.select(idx.size, S, 32, "sum"), geot.last_choice()
+    assert (lc["vec"], lc["lanes"], lc["rows"]) == (8, fp["lanes"] // 2, 2 * fp["rows"]), (lc, fp)
     starts = np.concatenate([[0], np.cumsum(L)])
     for seg in _sample_segments(L, 200, 4):
         a, b = starts[seg], starts[seg + 1]

@@ -38,13 +38,11 @@ def fitted():
 
 
 def test_committed_header_is_reproducible(fitted):
-    tn, ts, data, _, _ = fitted
-    assert open(HEADER).read() == fit.render(tn, ts, len(data)), \
+    assert open(HEADER).read() == fit.render(fitted), \
         "selector_generated.h is stale: rerun python -m paper_2404_03019_amd.tune.fit"
 
 
-def test_compiled_tree_matches_sklearn(fitted, tmp_path):
-    tn, ts, data, Xn, Xs = fitted
+def test_compiled_tree_matches_the_fitted_trees(fitted, tmp_path):
     drv = tmp_path / "drv.cpp"
     drv.write_text(DRIVER)
     exe = str(tmp_path / "drv")
@@ -52,15 +50,13 @@ def test_compiled_tree_matches_sklearn(fitted, tmp_path):
                    check=True)
     lines, want = [], []
     ops = {"sum": 0, "mean": 1, "max": 2}
-    for e, xn, xs in zip(data, Xn, Xs):
+    for e in fitted.data:
         f = e["features"]
+        g = 0 if not f["gather"] else (1 if fit.weighted_of(e) else 2)
         for has in (0, 1):
-            lines.append(f"{f['nnz']} {f['S']} {f['F']} {ops[f['op']]} {f['gather']} {has} "
+            lines.append(f"{f['nnz']} {f['S']} {f['F']} {ops[f['op']]} {g} {has} "
                          f"{f['cv']!r} {f['max_rel']!r}")
-            if has:
-                want.append(fit.candidate_space(True)[ts.predict_one(xs)])
-            else:
-                want.append(fit.candidate_space(False)[tn.predict_one(xn)])
+            want.append(fitted.choose(e, bool(has)))
     got = subprocess.run([exe], input="\n".join(lines) + "\n", capture_output=True, text=True,
                          check=True).stdout.split("\n")
     mism = [(l, g, w) for l, g, w in zip(lines, got, want)
@@ -72,26 +68,30 @@ def test_compiled_tree_matches_sklearn(fitted, tmp_path):
 def test_library_select_follows_the_tree(fitted):
     import paper_2404_03019_amd as geot
 
-    tn, ts, data, Xn, Xs = fitted
-    for e, xn in list(zip(data, Xn))[:60]:
+    picks = [e for e in fitted.data if not e["features"]["gather"]][:40] + \
+        [e for e in fitted.data if e["features"]["gather"]][:40]
+    for e in picks:
         f = e["features"]
-        fam, k, g = fit.candidate_space(False)[tn.predict_one(xn)]
-        c = geot.select(f["nnz"], f["S"], f["F"], f["op"], bool(f["gather"]))
+        fam, k, g = fitted.choose(e, False)
+        c = geot.select(f["nnz"], f["S"], f["F"], f["op"], bool(f["gather"]), weighted=bool(fit.weighted_of(e)))
         assert c["family"] == fam and c["rows"] == k, (f, c, (fam, k))
 
 
 def test_selector_beats_the_hand_rule_and_the_paper_recipe(fitted):
-    """Measured on MI355X: geometric-mean slowdown against the best measured candidate."""
-    tn, ts, data, Xn, Xs = fitted
-    rep = fit.evaluate(tn, ts, data, Xn, Xs)
+    """Measured on MI355X: geometric-mean slowdown against the best measured candidate,
+    over all inputs and over the fused-form inputs alone."""
+    rep = fit.evaluate(fitted)
 
-    def gm(k):
-        v = [r[k] for r in rep if r[k] == r[k]]
+    def gm(k, sel=lambda r: True):
+        v = [r[k] for r in rep if r[k] == r[k] and sel(r)]
         return math.exp(sum(math.log(x) for x in v) / len(v))
 
     assert gm("nostats") < gm("paper_nostats") < gm("hand")
     assert gm("nostats") <= 1.05
-    named = [r for r in rep if r["id"] >= 10000]
+    fused = lambda r: r["gather"]
+    assert gm("nostats", fused) <= gm("single_nostats", fused) + 1e-9
+    assert gm("nostats", fused) <= 1.05
+    named = [r for r in rep if 10000 <= r["id"] < 20000]
     # the large named workloads (above 0.2 ms) are within 10% of the best candidate
     big = [r for r in named if r["best"] >= 0.2]
     assert big and all(r["nostats"] <= 1.10 for r in big), big
