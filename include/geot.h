@@ -95,8 +95,18 @@ typedef struct {
     int32_t lanes;  /* lanes sharing one row: 1, 2, 4, 8, 16, 32 or 64 */
     int32_t rows;   /* EP: consecutive rows per row group (1..4096) */
     int32_t groups; /* SP: row groups of one wave that cooperate on one segment (1..64/lanes) */
-    int32_t flags;  /* reserved, must be 0 */
+    int32_t flags;  /* 0, or one of the GEOT_FLAG_* load policies below */
 } geot_kernel_choice_t;
+
+/* Load policy of the streamed rows (element-parallel family, segment reduction).
+ * By default rows are loaded non-temporally when a row group's load and the row
+ * both span at least 128 bytes (whole cache lines read once), else with ordinary
+ * loads. NT_LOADS forces the non-temporal policy (GEOT_ERROR_UNSUPPORTED where
+ * the tile is narrower than 128 bytes, or for the gather form); CACHED_LOADS
+ * forces ordinary loads. A resolved choice (geot_select, geot_last_choice)
+ * reports NT_LOADS when it loads non-temporally. */
+#define GEOT_FLAG_NT_LOADS 1
+#define GEOT_FLAG_CACHED_LOADS 2
 
 /* Segment-length statistics of a sorted index (all lengths over
  * [0, num_segments), empties included). */

@@ -219,6 +219,7 @@ struct Problem {
 
 struct Resolved {
     int family, V, NT, L, K, groups, ntiles;
+    int nt_rows;  // EP rows mode: non-temporal row loads
 };
 
 int max_nt(int V) { return V == 4 ? 1 : (V == 2 ? 2 : 4); }
@@ -272,7 +273,9 @@ int widest_vec(const Problem &p) {
 
 geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r,
                       bool from_selector = false) {
-    if (c.flags != 0) return fail(GEOT_ERROR_UNSUPPORTED, "choice.flags must be 0");
+    const int known = GEOT_FLAG_NT_LOADS | GEOT_FLAG_CACHED_LOADS;
+    if ((c.flags & ~known) != 0 || (c.flags & known) == known)
+        return fail(GEOT_ERROR_UNSUPPORTED, "choice.flags: unknown bit, or both load policies");
     r->family = c.family == GEOT_FAMILY_AUTO ? GEOT_FAMILY_EP : c.family;
     if (r->family != GEOT_FAMILY_EP && r->family != GEOT_FAMILY_SP)
         return fail(GEOT_ERROR_UNSUPPORTED, "unknown kernel family %d", c.family);
@@ -311,6 +314,15 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     if (ntiles > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "F too large for lanes*vec");
     r->ntiles = (int)ntiles;
     if (rows < 0 || rows > 4096) return fail(GEOT_ERROR_UNSUPPORTED, "rows must be in 0..4096");
+    // Non-temporal row loads where a row group's load covers whole 128-byte lines: the
+    // element-parallel rows mode, a tile and a row of at least 128 bytes.
+    const bool nt_ok = r->family == GEOT_FAMILY_EP && !p.gather && TW * (int64_t)p.esize() >= 128;
+    if ((c.flags & GEOT_FLAG_NT_LOADS) && !nt_ok)
+        return fail(GEOT_ERROR_UNSUPPORTED, "non-temporal loads need the element-parallel rows mode and a "
+                                            "tile of at least 128 bytes");
+    r->nt_rows = (c.flags & GEOT_FLAG_NT_LOADS) ? 1
+                 : (c.flags & GEOT_FLAG_CACHED_LOADS) ? 0
+                 : (nt_ok && p.F * (int64_t)p.esize() >= 128 ? 1 : 0);
     r->K = rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles, (int64_t)p.esize()) : rows;
     const int GW = 64 / L;
     geot_kernel_choice_t cc = c;
@@ -335,7 +347,7 @@ geot_kernel_choice_t to_choice(const Resolved &r) {
     c.lanes = r.L;
     c.rows = r.K;
     c.groups = r.groups;
-    c.flags = 0;
+    c.flags = r.nt_rows ? GEOT_FLAG_NT_LOADS : 0;
     return c;
 }
 
@@ -480,6 +492,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.gaps = gaps;
             a.elem = p.elem;
             a.idx32 = p.idx32;
+            a.nt_rows = r.nt_rows;
         } else {
             a.src = (const float *)(base + off_v[l]);
             a.ld_src = ld_p;

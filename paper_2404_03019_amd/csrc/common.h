@@ -38,6 +38,34 @@ __device__ __forceinline__ void load_vec(const float *p, float *x) {
     }
 }
 
+// Non-temporal loads (the `nt` cache policy): for data read exactly once, such
+// as streamed rows and ids, which then does not displace data that is reused.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+template <bool NT, typename T>
+__device__ __forceinline__ T ld(const T *p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+
+template <int V, bool NT>
+__device__ __forceinline__ void load_vec_p(const float *p, float *x) {
+    if constexpr (!NT) {
+        load_vec<V>(p, x);
+    } else if constexpr (V == 4) {
+        const f32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p));
+        x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    } else if constexpr (V == 2) {
+        const f32x2_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x2_t *>(p));
+        x[0] = t.x; x[1] = t.y;
+    } else {
+        x[0] = __builtin_nontemporal_load(p);
+    }
+}
+
 template <int V>
 __device__ __forceinline__ void store_vec(float *p, const float *x) {
     if constexpr (V == 8) {  // 16-bit storage loads 8 elements per lane; fp32 results go out as 2 x 16 B
@@ -70,21 +98,21 @@ template <int E, int V> struct Raw { float v[V]; };
 template <int V> struct Raw<ELEM_BF16, V> { uint32_t w[(V + 1) / 2]; };
 template <int V> struct Raw<ELEM_F16, V> { uint32_t w[(V + 1) / 2]; };
 
-// V consecutive elements at p (aligned to V elements)
-template <int E, int V>
+// V consecutive elements at p (aligned to V elements); NT: non-temporal load
+template <int E, int V, bool NT = false>
 __device__ __forceinline__ void load_raw(const typename ElemT<E>::T *p, Raw<E, V> &r) {
     if constexpr (E == ELEM_F32) {
-        load_vec<V>(p, r.v);
+        load_vec_p<V, NT>(p, r.v);
     } else if constexpr (V == 8) {
-        const uint4 t = *reinterpret_cast<const uint4 *>(p);
+        const u32x4_t t = ld<NT>(reinterpret_cast<const u32x4_t *>(p));
         r.w[0] = t.x; r.w[1] = t.y; r.w[2] = t.z; r.w[3] = t.w;
     } else if constexpr (V == 4) {
-        const uint2 t = *reinterpret_cast<const uint2 *>(p);
+        const u32x2_t t = ld<NT>(reinterpret_cast<const u32x2_t *>(p));
         r.w[0] = t.x; r.w[1] = t.y;
     } else if constexpr (V == 2) {
-        r.w[0] = *reinterpret_cast<const uint32_t *>(p);
+        r.w[0] = ld<NT>(reinterpret_cast<const uint32_t *>(p));
     } else {
-        r.w[0] = (uint32_t)*reinterpret_cast<const uint16_t *>(p);
+        r.w[0] = (uint32_t)ld<NT>(reinterpret_cast<const uint16_t *>(p));
     }
 }
 

@@ -63,6 +63,7 @@ struct EpArgs {
     GapList gaps;           // long runs of empty segments (level 0 only)
     int32_t elem;           // ElemType of src (SRC_PIECES: ELEM_F32)
     int32_t idx32;          // idx and col hold int32 (SRC_PIECES: 0)
+    int32_t nt_rows;        // rows mode: non-temporal row loads (tiles of >= 128 bytes only)
 };
 
 // Dispatches on (elem, idx32) to the translation unit holding those instantiations.

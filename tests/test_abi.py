@@ -97,12 +97,26 @@ def test_gather_arguments_are_checked():
 
 @pytest.mark.parametrize("choice", [
     dict(family=7), dict(vec=3), dict(lanes=3), dict(lanes=128), dict(rows=-1), dict(rows=5000),
-    dict(family=2, lanes=16, groups=8), dict(family=2, groups=3), dict(flags=1), dict(vec=8),
+    dict(family=2, lanes=16, groups=8), dict(family=2, groups=3), dict(flags=4), dict(flags=3),
+    dict(vec=8), dict(flags=1, lanes=2),   # a 2-lane x 4-float tile is 32 bytes: no non-temporal rows
+    dict(flags=1, family=2),
 ])
 def test_impossible_forced_choices_are_unsupported(choice):
     c = geot.geot._choice(choice)
     out = FAKE + (1 << 30)
     assert _sr(FAKE, FAKE + (1 << 28), 1000, 10, 32, 0, out, c) == UNSUPPORTED
+
+
+def test_non_temporal_loads_are_refused_for_the_gather_form():
+    c = geot.geot._choice(dict(flags=1))
+    out = FAKE + (1 << 30)
+    assert _gs(FAKE, 10, FAKE + (1 << 27), None, FAKE + (1 << 26), 5, 3, 32, 0, out, c) == UNSUPPORTED
+
+
+def test_selector_reports_the_load_policy():
+    assert geot.select(114_615_892, 232_965, 32, "sum")["flags"] == 1       # 128-byte rows
+    assert geot.select(2_000_000, 100_000, 8, "sum")["flags"] == 0          # 32-byte rows
+    assert geot.select(61_859_140, 2_449_029, 128, "sum", gather=True)["flags"] == 0
 
 
 def test_selector_is_a_host_function():

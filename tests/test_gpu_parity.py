@@ -317,3 +317,32 @@ def test_long_runs_of_empty_segments():
                 say(f"gaps S={S} nnz={idx.size} F={F} op={op} choice={ch}")
                 got = run_sr(src, idx, S, op, ch)
                 compare(got, ref, op, terms, f"gaps S={S} F={F} {op} {ch}")
+
+
+@pytest.mark.parametrize("F", [32, 33, 64, 100, 128, 256, 300])
+def test_non_temporal_row_loads_match_ordinary_loads(F):
+    """The two load policies read the same values and reduce them in the same order:
+    outputs are bitwise identical, and both match the oracle."""
+    p = random_problem(900 + F, 40000, 700, F, "lognormal", "normal", 0.1)
+    s, i = up(p["src"]), up(p["index"])
+    for op in OPS:
+        ref, terms = oracle_segment(p["src"], p["index"], 700, op)
+        for base in (dict(family="ep"), dict(family="ep", rows=3), dict(family="ep", lanes=64, vec=1, rows=2)):
+            say(f"load policies F={F} {op} {base}")
+            cached = geot.segment_reduce(s, i, 700, op, choice=dict(base, flags=2))
+            assert geot.last_choice()["flags"] == 0
+            try:
+                nt = geot.segment_reduce(s, i, 700, op, choice=dict(base, flags=1))
+            except geot.GeotError as e:   # the tile of this shape is narrower than 128 bytes
+                assert e.status == 5, e
+                continue
+            assert geot.last_choice()["flags"] == 1
+            assert torch.equal(nt, cached), f"F={F} {op} {base}"
+            compare(nt.cpu().numpy(), ref, op, terms, f"non-temporal F={F} {op} {base}")
+    # 16-bit storage: 64 bf16 columns are 128 bytes
+    t = torch.from_numpy(p["src"][:, :64].copy()).to(torch.bfloat16)
+    s16 = t.to(DEV)
+    a = geot.segment_reduce(s16, i, 700, "sum", choice=dict(family="ep", flags=1)) if F >= 64 else None
+    if a is not None:
+        b = geot.segment_reduce(s16, i, 700, "sum", choice=dict(family="ep", flags=2))
+        assert torch.equal(a, b)
