@@ -206,7 +206,8 @@ geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int6
  *         with src[i, f] == out[s, f]; every other element of grad_src is 0.
  *         src and out (the forward result) are read for max only (may be NULL
  *         otherwise).
- * Sum and max copy values (exact); mean divides once in fp32. Deterministic.
+ * Sum and max copy values (exact); mean multiplies by the fp32 reciprocal of
+ * the count (two roundings, within 1e-5 relative). Deterministic.
  * Same argument checks as geot_segment_reduce; grad_src must not overlap the
  * inputs. Temporary memory: (num_segments + 1) int64 for mean, num_segments *
  * F uint64 for max, from the per-stream buffer.                              */
@@ -218,9 +219,10 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
 /* Gradients of geot_gather_scatter w.r.t. X and the edge weights. The caller
  * keeps only the row-sorted edge list: for the X gradient of sum and mean the
  * library counting-sorts the edges by column into a temporary transposed list
- * (20 bytes per edge and 12 per X row, from its stream-ordered pool) and runs
- * the forward gather kernel over it, so every row of grad_X is written without
- * float atomics; for max only the recipients' terms are added, atomically.
+ * (one 16-byte record per edge, 20 bytes when num_x_rows >= 2^31, and 12
+ * bytes per X row, from its stream-ordered pool) and runs the forward gather
+ * kernel over it, so every row of grad_X is written without float atomics; for
+ * max only the recipients' terms are added, atomically.
  *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
  *   out          [num_rows x F]: the forward result (read for max only)
  *   grad_X       [num_x_rows x F] fp32 or NULL (skipped), overwritten:

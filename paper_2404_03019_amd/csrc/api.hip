@@ -212,6 +212,7 @@ struct Problem {
     float *out;
     int elem = ELEM_F32;   // storage type of src / X
     int idx32 = 0;         // idx and col hold int32
+    int meta_stride = 1;   // gather: idx, col and w of edge e at [e * meta_stride] (internal records)
     size_t esize() const { return elem == ELEM_F32 ? 4 : 2; }
     size_t isize() const { return idx32 ? 4 : 8; }
     bool typed() const { return elem != ELEM_F32 || idx32 != 0; }
@@ -493,6 +494,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.elem = p.elem;
             a.idx32 = p.idx32;
             a.nt_rows = r.nt_rows;
+            a.meta_stride = p.meta_stride;
         } else {
             a.src = (const float *)(base + off_v[l]);
             a.ld_src = ld_p;
@@ -759,9 +761,13 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
     const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
     const size_t o_sums = transpose ? take((size_t)((nx + 4095) / 4096 + 1) * 8) : 0;
-    const size_t o_key = transpose ? take((size_t)nnz * 8) : 0;
-    const size_t o_row = transpose ? take((size_t)nnz * 8) : 0;
-    const size_t o_w = transpose ? take((size_t)nnz * 4) : 0;
+    // the transposed list: 16-byte records {col, row, coefficient, 0} with int32 ids, or
+    // (X with 2^31 rows or more) three arrays
+    const bool packed = nx <= (int64_t)INT32_MAX;
+    const size_t o_rec = transpose && packed ? take((size_t)nnz * 16) : 0;
+    const size_t o_key = transpose && !packed ? take((size_t)nnz * 8) : 0;
+    const size_t o_row = transpose && !packed ? take((size_t)nnz * 8) : 0;
+    const size_t o_w = transpose && !packed ? take((size_t)nnz * 4) : 0;
     ScratchGuard sg;
     sg.st = st;
     geot_status_t s = scratch_alloc(&sg.p, at, st);
@@ -789,15 +795,25 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
              "launch fused backward kernels");
     if (transpose) {
         // grad_X = gather_scatter of grad_out over the edges sorted by col (sum of coef * grad_out rows)
-        int64_t *key_t = (int64_t *)(base + o_key);
-        int64_t *row_t = (int64_t *)(base + o_row);
-        float *w_t = (float *)(base + o_w);
+        int64_t *key_t = packed ? nullptr : (int64_t *)(base + o_key);
+        int64_t *row_t = packed ? nullptr : (int64_t *)(base + o_row);
+        float *w_t = packed ? nullptr : (float *)(base + o_w);
+        int32_t *rec = packed ? (int32_t *)(base + o_rec) : nullptr;
         GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
-                                  (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, st),
+                                  (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, rec,
+                                  st),
                  "launch transpose kernels");
         Problem tp{true, grad_out, num_rows, row_t, w_t, key_t, nnz, nx, F, GEOT_OP_SUM, grad_X};
+        if (packed) {
+            tp.idx = rec;
+            tp.col = rec + 1;
+            tp.w = (const float *)(rec + 2);
+            tp.idx32 = 1;
+            tp.meta_stride = 4;
+        }
         geot_kernel_choice_t c;
         select_raw(nnz, nx, F, GEOT_OP_SUM, 1, nullptr, &c);
+        if (tp.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
         Resolved r;
         s = resolve(tp, c, &r, true);
         if (s != GEOT_SUCCESS) return s;

@@ -63,6 +63,8 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     const T *src = static_cast<const T *>(a.src);
     const I *idx = static_cast<const I *>(a.idx);
     const I *col = static_cast<const I *>(a.col);
+    // gather mode: edge e's id, column and weight sit at [e * ms] (records of ms words), else ms = 1
+    const int64_t ms = MODE == SRC_GATHER && a.meta_stride > 1 ? (int64_t)a.meta_stride : 1;
 
     __shared__ float s_v[NW][TW];
     __shared__ Cnt s_n[NW];
@@ -205,10 +207,10 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
 
     int32_t prev = -1, next = -1;
     if (has_rows) {
-        first_seg = (int32_t)idx[r0];
+        first_seg = (int32_t)idx[r0 * ms];
         cur = first_seg;
-        prev = r0 > 0 ? (int32_t)idx[r0 - 1] : -1;
-        next = r1 < a.n ? (int32_t)idx[r1] : -1;
+        prev = r0 > 0 ? (int32_t)idx[(r0 - 1) * ms] : -1;
+        next = r1 < a.n ? (int32_t)idx[r1 * ms] : -1;
         if (a.fill_gaps) fill_empty((int64_t)prev + 1, (int64_t)first_seg);
 
         if constexpr (MODE == SRC_GATHER) {
@@ -229,9 +231,9 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
 #pragma unroll
                 for (int m = 0; m < UM; ++m) {
                     const int64_t rr = min(rb + (kShared ? (int64_t)min(gl, UG - 1) : (int64_t)m), r1 - 1);
-                    ns[m] = (int32_t)idx[rr];
-                    nc[m] = col[rr];
-                    nw[m] = a.w ? a.w[rr] : 1.0f;
+                    ns[m] = (int32_t)idx[rr * ms];
+                    nc[m] = col[rr * ms];
+                    nw[m] = a.w ? a.w[rr * ms] : 1.0f;
                 }
             };
             load_meta(r0);

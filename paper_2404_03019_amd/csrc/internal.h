@@ -64,6 +64,7 @@ struct EpArgs {
     int32_t elem;           // ElemType of src (SRC_PIECES: ELEM_F32)
     int32_t idx32;          // idx and col hold int32 (SRC_PIECES: 0)
     int32_t nt_rows;        // rows mode: non-temporal row loads (tiles of >= 128 bytes only)
+    int32_t meta_stride;    // gather mode: idx, col and w of edge e at [e * meta_stride] (0 or 1: arrays)
 };
 
 // Dispatches on (elem, idx32) to the translation unit holding those instantiations.
@@ -132,9 +133,12 @@ hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long 
 // Counting sort of the edges by col: key_t (sorted col), row_t and w_t (weight, divided by
 // the row's edge count for mean; roff = row starts) of the transposed problem.
 // counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
+// With rec != nullptr (needs nx and the rows < 2^31) each edge is one 16-byte record
+// {int32 key, int32 row, float coefficient, 0} at rec[4 * slot] and key_t, row_t, w_t are unused.
 hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
                             const int64_t *roff, bool mean, int64_t n, unsigned *counts, int64_t *off,
-                            int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, hipStream_t st);
+                            int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
+                            hipStream_t st);
 
 // grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean)
 hipError_t launch_seg_bwd_bcast(const float *gout, const int64_t *idx, const int64_t *off, int64_t n,
