@@ -252,7 +252,9 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
  *           two operations have trees of their own, and the fused one splits
  *           on whether there are weights
  *   stats   optional (NULL allowed); when given, the length variance and the
- *           longest segment join the features
+ *           longest segment join the features, and the segment-parallel
+ *           family is never chosen when the longest segment exceeds 256x the
+ *           mean length
  * Writes a fully specified choice to *out.                                  */
 geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, int32_t gather,
                           const geot_index_stats_t *stats, geot_kernel_choice_t *out);

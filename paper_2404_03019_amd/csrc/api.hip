@@ -362,6 +362,10 @@ void select_raw(int64_t nnz, int64_t S, int64_t F, geot_op_t op, int gather,
     }
     int32_t o[5];
     tree_select((double)nnz, (double)S, (double)F, (int)op, gather, stats != nullptr, cv, max_rel, o);
+    // One segment-parallel team owns a whole segment: never used where the longest segment
+    // exceeds 256x the mean (the range the trees were fitted on leaves it unmeasured there)
+    if (o[0] == GEOT_FAMILY_SP && max_rel > 256.0)
+        tree_select((double)nnz, (double)S, (double)F, (int)op, gather, 0, cv, max_rel, o);
     c->family = o[0];
     c->vec = o[1];
     c->lanes = o[2];

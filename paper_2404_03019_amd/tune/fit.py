@@ -278,6 +278,14 @@ class Fitted:
         kind = kind_of(e)
         return candidate_space(stats)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
 
+    def choose_as_library(self, e, stats: bool):
+        """What geot_select returns: the tree's choice, except that the segment-parallel
+        family is never used where the longest segment exceeds 256x the mean."""
+        c = self.choose(e, stats)
+        if stats and c[0] == 2 and e["features"]["max_rel"] > 256.0:
+            c = self.choose(e, False)
+        return c
+
     def choose_single(self, e, stats: bool):
         return candidate_space(stats)[self.single[stats].predict_one(feature_row(e, stats))]
 
@@ -354,7 +362,7 @@ def evaluate(fitted: Fitted):
             op=e["instance"]["op"], gather=e["instance"]["gather"], weighted=weighted_of(e),
             nnz=e["features"]["nnz"], best=tb,
             nostats=_time_of(e, fitted.choose(e, False)) / tbe,
-            stats=_time_of(e, fitted.choose(e, True)) / tb,
+            stats=_time_of(e, fitted.choose_as_library(e, True)) / tb,
             single_nostats=_time_of(e, fitted.choose_single(e, False)) / tbe,
             single_stats=_time_of(e, fitted.choose_single(e, True)) / tb,
             paper_nostats=e["times"].get(predict_cand(paper[(kind, False)], feature_row(e, False, kind), False, e),

@@ -1,0 +1,103 @@
+"""GPU parity at the size limits: more than 2^31 rows (64-bit row and chunk
+arithmetic, 64-bit counts in the partial levels), one segment of more than
+2^31 rows, and a fused call over more than 2^31 edges.
+
+Inputs are built on the GPU with torch's seeded generator (ternary values, so
+every partial sum below 2^24 is exact in fp32); the oracle runs on the rows of
+sampled segments copied back to the host.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2404_03019_amd as geot
+from gpu_util import compare, say
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+BIG = (1 << 31) + 999_999
+
+
+def lengths(seed, S, total):
+    rng = np.random.default_rng(seed)
+    w = rng.lognormal(0.0, 0.6, S)
+    L = np.floor(w / w.sum() * total).astype(np.int64)
+    L[: total - int(L.sum())] += 1
+    assert int(L.sum()) == total
+    return L
+
+
+def ternary(n, F, seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return torch.randint(-1, 2, (n, F), dtype=torch.int8, device=DEV, generator=g).float()
+
+
+def sample(L, k, seed):
+    rng = np.random.default_rng(seed)
+    picks = {0, L.size - 1, int(np.argmax(L)), int(np.argmin(L))}
+    picks.update(int(x) for x in rng.choice(L.size, size=k, replace=False))
+    return sorted(picks)
+
+
+def test_more_than_2_31_rows():
+    S, F = 3000, 1
+    L = lengths(7, S, BIG)
+    starts = np.concatenate([[0], np.cumsum(L)])
+    idx = torch.repeat_interleave(torch.arange(S, device=DEV), torch.from_numpy(L).to(DEV))
+    src = ternary(BIG, F, 7)
+    say("limits: 2^31+ rows uploaded")
+    for itype in (torch.int64, torch.int32):
+        ix = idx if itype == torch.int64 else idx.to(torch.int32)
+        outs = {op: geot.segment_reduce(src, ix, S, op).cpu().numpy() for op in ("sum", "mean", "max")}
+        say(f"limits: 2^31+ rows reduced ({itype})")
+        for s in sample(L, 12, 8):
+            a, b = int(starts[s]), int(starts[s + 1])
+            rows = src[a:b].cpu().numpy()
+            z = np.zeros(b - a, dtype=np.int64)
+            for op in ("sum", "max"):   # partial sums are integers below 2^24: exact
+                ref = oracle.segment_reduce(rows, z, 1, op)
+                assert np.array_equal(outs[op][s:s + 1], ref), (itype, op, s)
+            ref = oracle.segment_reduce(rows, z, 1, "mean")
+            compare(outs["mean"][s:s + 1], ref, "mean", oracle.abs_term_sum(rows, z, 1, "mean"),
+                    f"limits mean segment {s}")
+        del ix
+    # per-feature conservation over every row (fp64 totals of exact integers)
+    tot = torch.sum(src, dim=0, dtype=torch.float64).cpu().numpy()
+    assert np.array_equal(np.sum(outs["sum"].astype(np.float64), axis=0), tot)
+
+
+def test_one_segment_of_more_than_2_31_rows():
+    """The count of the only segment exceeds 32 bits; sums pass 2^24, so they are
+    compared within the bound (terms = the row count)."""
+    F = 2
+    src = torch.ones((BIG, F), device=DEV)
+    idx = torch.zeros(BIG, dtype=torch.int64, device=DEV)
+    say("limits: one 2^31+ segment uploaded")
+    got = {op: geot.segment_reduce(src, idx, 1, op).cpu().numpy() for op in ("sum", "mean", "max")}
+    terms = np.full((1, F), float(BIG))
+    compare(got["sum"], np.full((1, F), float(BIG), dtype=np.float32), "sum", terms, "one segment sum")
+    compare(got["mean"], np.ones((1, F), dtype=np.float32), "mean", np.ones((1, F)), "one segment mean")
+    assert np.array_equal(got["max"], np.ones((1, F), dtype=np.float32))
+
+
+def test_fused_more_than_2_31_edges():
+    R, nx, F = 1500, 4000, 2
+    L = lengths(9, R, BIG)
+    starts = np.concatenate([[0], np.cumsum(L)])
+    row = torch.repeat_interleave(torch.arange(R, device=DEV), torch.from_numpy(L).to(DEV))
+    g = torch.Generator(device=DEV)
+    g.manual_seed(9)
+    col = torch.randint(0, nx, (BIG,), device=DEV, generator=g)
+    X = ternary(nx, F, 10)
+    say("limits: 2^31+ edges uploaded")
+    got = {op: geot.gather_scatter(X, col, None, row, R, op).cpu().numpy() for op in ("sum", "max")}
+    Xh = X.cpu().numpy()
+    for r in sample(L, 8, 11):
+        a, b = int(starts[r]), int(starts[r + 1])
+        c = col[a:b].cpu().numpy()
+        z = np.zeros(b - a, dtype=np.int64)
+        for op in ("sum", "max"):
+            ref = oracle.gather_scatter(Xh, c, None, z, 1, op)
+            assert np.array_equal(got[op][r:r + 1], ref), (op, r)
