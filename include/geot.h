@@ -17,8 +17,9 @@
  *
  * Conventions shared by every call:
  *  - Array arguments are DEVICE pointers owned by the caller: fp32 values and
- *    int64 indices, contiguous and row-major. The library never frees them
- *    and keeps no reference after the call returns.
+ *    int64 indices (the *_typed calls also take bf16 / fp16 values and int32
+ *    indices), contiguous and row-major. The library never frees them and
+ *    keeps no reference after the call returns.
  *  - `stream` is a hipStream_t passed as void*; NULL is the default stream.
  *    Calls are asynchronous: they return after the kernels are enqueued, and
  *    device faults surface at the caller's next synchronisation. Calls that
