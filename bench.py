@@ -210,6 +210,8 @@ def suite(reps: int):
     b = seg_bytes(n3, S3, 32)
     ms, cold = timed(lambda: geot.segment_reduce(src, idx, S3, "sum"), b)
     emit("c3_powerlaw_graph sum", ms, b, cold)
+    ms, _ = timed(lambda: geot.index_stats(idx, S3), 1 << 40)
+    emit("c3_powerlaw_graph index statistics (geot_index_stats, synchronizing)", ms, n3 * 8 + (S3 + 1) * 8, False)
     # the same reduction with bf16 storage and int32 ids (fp32 accumulation and output)
     src16, idx32 = src.to(torch.bfloat16), idx.to(torch.int32)
     b = seg_bytes(n3, S3, 32, 2, 4)
@@ -278,11 +280,31 @@ def suite(reps: int):
         loss = ((agg_torch(layers[1].lin(h)) + layers[1].bias - target) ** 2).mean()
         loss.backward()
 
+    # index statistics pass (the optional selector features): one read of the index
+    for name, ix, S_ in (("c4_spmm", row, R4),):
+        ms, _ = timed(lambda: geot.index_stats(ix, S_), 1 << 40)
+        emit(f"{name} index statistics (geot_index_stats, synchronizing)", ms, ix.numel() * 8 + (S_ + 1) * 8,
+             False)
     ms_g, _ = timed(step_geot, 1 << 40)
     ms_t, _ = timed(step_torch, 1 << 40)
     print(json.dumps({"suite": "graphconv 2-layer training step (SpMM graph, 128-128-64)",
                       "ms": round(ms_g, 3), "torch_index_add_ms": round(ms_t, 3),
                       "speedup_vs_torch": round(ms_t / ms_g, 2)}), flush=True)
+    host_probe()
+
+
+def host_probe():
+    """Selector host cost per call and the HBM peak from device properties (a small host
+    program linked against the library, built here with hipcc)."""
+    import subprocess
+    exe = os.path.join(ROOT, "_build", "host_probe")
+    os.makedirs(os.path.dirname(exe), exist_ok=True)
+    lib_dir = os.path.join(ROOT, "paper_2404_03019_amd")
+    subprocess.run(["/opt/rocm/bin/hipcc", "-O2", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+                    os.path.join(lib_dir, "tune", "host_probe.cpp"), f"-L{lib_dir}", "-lgeot_hip",
+                    f"-Wl,-rpath,{lib_dir}", "-o", exe], check=True, capture_output=True)
+    r = subprocess.run([exe], check=True, capture_output=True, text=True)
+    print(r.stdout.strip(), flush=True)
 
 
 def main():
