@@ -29,7 +29,10 @@
  *  - Temporary device memory (partial results of segments that cross block
  *    boundaries) comes from a stream-ordered pool owned by the library; the
  *    reductions keep one buffer per (device, stream) for reuse (see
- *    geot_release_scratch).
+ *    geot_release_scratch). Any thread may call the library, but calls that
+ *    share one stream must be issued one after the other: two host threads
+ *    enqueuing on the same stream at once would interleave their kernels
+ *    over that stream's buffer. Different streams are independent.
  *  - Preconditions: the index is non-decreasing and 0 <= index < num_segments;
  *    for the gather form 0 <= col < num_x_rows. They are not checked by the
  *    reduction calls (geot_check_index checks them). Violations give

@@ -136,12 +136,12 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
     const size_t need = kGapArea + ((bytes + 255) & ~(size_t)255);
     bool fresh = false;
     if (e.bytes < need) {
+        const size_t grown = std::max(need, e.bytes + e.bytes / 2);  // grow by half at least
         if (e.p) {
             GEOT_HIP(hipFreeAsync(e.p, st), "hipFreeAsync");
             e.p = nullptr;
             e.bytes = 0;
         }
-        const size_t grown = std::max(need, e.bytes + e.bytes / 2);
         void *q = nullptr;
         geot_status_t s = scratch_alloc(&q, grown, st);
         if (s != GEOT_SUCCESS) return s;
