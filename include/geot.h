@@ -249,6 +249,29 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
                                            const float *grad_out, const float *out, float *grad_X,
                                            float *grad_weight, void *stream);
 
+/* The edge list sorted by source column instead of destination row: the
+ * transposed problem whose fused gather gives the X gradient of sum and mean
+ * (Section VI: training), kept by callers whose graph does not change between
+ * calls (every training step of a static graph), so the gradient w.r.t. X is
+ * one forward call:
+ *   grad_X = geot_gather_scatter(grad_out, num_rows, row_out, coef_out,
+ *                                sorted_col_out, nnz, num_x_rows, F, GEOT_OP_SUM)
+ *   sorted_col_out [nnz] int64: the columns, non-decreasing
+ *   row_out        [nnz] int64: the destination row of each edge
+ *   coef_out       [nnz] fp32: the edge's coefficient, weight[e] (1 when weight
+ *                  is NULL), divided by its row's edge count for GEOT_OP_MEAN
+ * The order of the edges inside one column depends on timing (placement by an
+ * atomic cursor); any order is a valid input to the gather. op must be sum or
+ * mean (the max gradient depends on the forward result). Edges whose column is
+ * out of range are left out, and the tail of the outputs is then unspecified.
+ * Temporary memory: 12 bytes per X row (and 8 per row for mean), from the
+ * library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
+ * sizes, num_rows >= 2^31, another op, or outputs that overlap the inputs or
+ * each other.                                                               */
+geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,
+                                   const int64_t *sorted_row, int64_t nnz, int64_t num_rows, geot_op_t op,
+                                   int64_t *sorted_col_out, int64_t *row_out, float *coef_out, void *stream);
+
 /* The selector (Section III-C: a decision tree over O(1) input features,
  * compiled to if/else). Pure host function: no device access.
  *   gather  0 for geot_segment_reduce; for geot_gather_scatter 1 with edge

@@ -17,6 +17,7 @@ from .geot import (  # noqa: F401
     segment_reduce_backward,
     gather_scatter_backward,
     index_stats,
+    transpose_edges,
     check_index,
     select,
     last_choice,

@@ -42,14 +42,44 @@ class SegmentReduce(torch.autograd.Function):
         return g, None, None, None
 
 
+class Graph:
+    """A static edge list: edge e goes from source node col[e] to destination
+    row[e] (sorted), with an optional weight, over num_nodes destinations and
+    num_src sources (default num_nodes).
+
+    The same edges sorted by source (geot_transpose_edges) turn the gradient
+    w.r.t. the source features of sum and mean into one forward gather. That
+    copy is built on first use and kept while the weights are unchanged (it is
+    rebuilt when an in-place update bumps the weight tensor's version)."""
+
+    def __init__(self, col, row, num_nodes: int, weight=None, num_src: int | None = None):
+        self.col, self.row, self.weight = col, row, weight
+        self.num_nodes = int(num_nodes)
+        self.num_src = int(num_src if num_src is not None else num_nodes)
+        self._transposed = {}
+
+    def transposed(self, reduce: str):
+        """(sorted_col, row_t, coef) for `reduce` in sum / mean."""
+        version = self.weight._version if self.weight is not None else 0
+        hit = self._transposed.get(reduce)
+        if hit is None or hit[0] != version:
+            w = self.weight.detach() if self.weight is not None else None
+            hit = (version, geot.transpose_edges(self.col, w, self.row, self.num_src, self.num_nodes, reduce))
+            self._transposed[reduce] = hit
+        return hit[1]
+
+
 class GatherScatter(torch.autograd.Function):
-    """out = gather_scatter(x, col, weight, row, num_rows, reduce); differentiable in x and weight."""
+    """out = gather_scatter(x, col, weight, row, num_rows, reduce); differentiable in x and weight.
+    With a Graph of the same edges, the gradient w.r.t. x of sum and mean is one forward
+    gather over its cached transposed list."""
 
     @staticmethod
-    def forward(ctx, x, col, weight, row, num_rows: int, reduce: str = "sum"):
+    def forward(ctx, x, col, weight, row, num_rows: int, reduce: str = "sum", graph=None):
         x = x.contiguous()
         out = geot.gather_scatter(x, col, weight, row, num_rows, reduce)
         ctx.reduce = reduce
+        ctx.graph = graph
         ctx.save_for_backward(x, col, weight if weight is not None else torch.empty(0), row,
                               out if reduce == "max" else torch.empty(0))
         ctx.has_weight = weight is not None
@@ -62,10 +92,16 @@ class GatherScatter(torch.autograd.Function):
         need_x = ctx.needs_input_grad[0]
         need_w = ctx.has_weight and ctx.needs_input_grad[2]
         x, col, row = x.float(), col.long(), row.long()  # the gradient kernels take fp32 and int64
-        gx, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out.contiguous(), ctx.reduce,
-                                              out if ctx.reduce == "max" else None,
-                                              need_x=need_x, need_weight=need_w)
-        return gx, None, gw, None, None, None
+        grad_out = grad_out.contiguous()
+        gx = None
+        if need_x and ctx.graph is not None and ctx.reduce in ("sum", "mean"):
+            sorted_col, row_t, coef = ctx.graph.transposed(ctx.reduce)
+            gx = geot.gather_scatter(grad_out, row_t, coef, sorted_col, x.shape[0], "sum")
+            need_x = False
+        gx2, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out, ctx.reduce,
+                                               out if ctx.reduce == "max" else None,
+                                               need_x=need_x, need_weight=need_w)
+        return (gx if gx is not None else gx2), None, gw, None, None, None, None
 
 
 def segment_reduce(src, index, num_segments, reduce="sum"):
@@ -73,9 +109,10 @@ def segment_reduce(src, index, num_segments, reduce="sum"):
     return SegmentReduce.apply(src, index, num_segments, reduce)
 
 
-def gather_scatter(x, col, weight, row, num_rows, reduce="sum"):
-    """Differentiable fused gather-weight-scatter (gradients w.r.t. x and weight)."""
-    return GatherScatter.apply(x, col, weight, row, num_rows, reduce)
+def gather_scatter(x, col, weight, row, num_rows, reduce="sum", graph=None):
+    """Differentiable fused gather-weight-scatter (gradients w.r.t. x and weight); `graph`
+    (a Graph of the same edges) caches the transposed list for the gradient w.r.t. x."""
+    return GatherScatter.apply(x, col, weight, row, num_rows, reduce, graph)
 
 
 class GraphConv(torch.nn.Module):
@@ -92,7 +129,12 @@ class GraphConv(torch.nn.Module):
         self.bias = torch.nn.Parameter(torch.zeros(out_features)) if bias else None
         self.reduce = reduce
 
-    def forward(self, h, col, row, num_nodes: int, weight=None):
+    def forward(self, h, col, row=None, num_nodes: int | None = None, weight=None):
+        """forward(h, graph) with a Graph, or forward(h, col, row, num_nodes, weight)."""
+        graph = None
+        if isinstance(col, Graph):
+            graph = col
+            col, row, num_nodes, weight = graph.col, graph.row, graph.num_nodes, graph.weight
         z = self.lin(h)
-        out = gather_scatter(z, col, weight, row, num_nodes, self.reduce)
+        out = gather_scatter(z, col, weight, row, num_nodes, self.reduce, graph)
         return out + self.bias if self.bias is not None else out

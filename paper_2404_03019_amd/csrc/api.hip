@@ -829,6 +829,67 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     return scratch_free(p_free, st);
 }
 
+geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,
+                                   const int64_t *sorted_row, int64_t nnz, int64_t num_rows, geot_op_t op,
+                                   int64_t *sorted_col_out, int64_t *row_out, float *coef_out, void *stream) {
+    t_detail.clear();
+    if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN)
+        return fail(GEOT_ERROR_INVALID_VALUE, "a transposed list serves sum and mean only");
+    if (nnz < 0 || num_rows < 0 || num_x_rows < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (nnz == 0) return GEOT_SUCCESS;
+    if (num_rows == 0 || num_x_rows == 0) return fail(GEOT_ERROR_INVALID_VALUE, "empty row or X range with nnz > 0");
+    if (num_rows > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_rows must be < 2^31");
+    if (nnz > ((int64_t)1 << 60)) return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
+    if (!col || !sorted_row || !sorted_col_out || !row_out || !coef_out)
+        return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
+    const size_t n8 = (size_t)nnz * 8, n4 = (size_t)nnz * 4;
+    const void *outs[3] = {sorted_col_out, row_out, coef_out};
+    const size_t out_b[3] = {n8, n8, n4};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(outs[i], out_b[i], col, n8) || overlaps(outs[i], out_b[i], sorted_row, n8) ||
+            overlaps(outs[i], out_b[i], weight, weight ? n4 : 0))
+            return fail(GEOT_ERROR_INVALID_VALUE, "an output overlaps an input");
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], out_b[i], outs[j], out_b[j]))
+                return fail(GEOT_ERROR_INVALID_VALUE, "the outputs overlap");
+    }
+    hipStream_t st = (hipStream_t)stream;
+    const bool mean = op == GEOT_OP_MEAN;
+    const int64_t nx = num_x_rows;
+    size_t at = 0;
+    auto take = [&](size_t b) { const size_t o = at; at = align256(at + b); return o; };
+    const size_t o_roff = mean ? take((size_t)(num_rows + 1) * 8) : 0;
+    const size_t o_cnt = take((size_t)((nx + 1) & ~(int64_t)1) * 4);
+    const size_t o_off = take((size_t)(nx + 1) * 8);
+    const size_t o_sums = take((size_t)((nx + 4095) / 4096 + 1) * 8);
+    ScratchGuard sg;
+    sg.st = st;
+    geot_status_t s = scratch_alloc(&sg.p, at, st);
+    if (s != GEOT_SUCCESS) return s;
+    char *base = (char *)sg.p;
+    int64_t *roff = mean ? (int64_t *)(base + o_roff) : nullptr;
+    if (mean) {
+        void *unused = nullptr;
+        GapList gaps;
+        StreamCtx *ctx = nullptr;
+        s = stream_scratch(0, st, &unused, &gaps, &ctx);
+        if (s != GEOT_SUCCESS) return s;
+        s = poison(ctx, [&]() -> geot_status_t {
+            GEOT_HIP(launch_offsets(sorted_row, nnz, num_rows, roff, gaps, st), "launch offsets kernel");
+            GEOT_HIP(launch_gap_fill_i64(roff, num_rows + 1, gaps, st), "launch gap fill kernel");
+            return GEOT_SUCCESS;
+        }());
+        if (s != GEOT_SUCCESS) return s;
+    }
+    GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
+                              (int64_t *)(base + o_off), (int64_t *)(base + o_sums), sorted_col_out, row_out,
+                              coef_out, nullptr, st),
+             "launch transpose kernels");
+    void *p_free = sg.p;
+    sg.p = nullptr;
+    return scratch_free(p_free, st);
+}
+
 geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, int32_t gather,
                           const geot_index_stats_t *stats, geot_kernel_choice_t *out) {
     t_detail.clear();

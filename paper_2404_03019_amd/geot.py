@@ -72,6 +72,7 @@ def lib() -> ctypes.CDLL:
     L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
     L.geot_segment_reduce_backward.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, p, p]
     L.geot_gather_scatter_backward.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, p, p, p]
+    L.geot_transpose_edges.argtypes = [p, i64, p, p, i64, i64, ctypes.c_int, p, p, p, p]
     L.geot_last_choice.argtypes = [pc]
     L.geot_release_scratch.argtypes = []
     L.geot_profile_begin.argtypes = [i32]
@@ -275,6 +276,33 @@ def gather_scatter_backward(x: torch.Tensor, col: torch.Tensor, weight: torch.Te
             gw.data_ptr() if gw is not None else None, _stream(x.device))
     _raise(st)
     return gx, gw
+
+
+def transpose_edges(col: torch.Tensor, weight: torch.Tensor | None, row: torch.Tensor, num_x_rows: int,
+                    num_rows: int, reduce: str = "sum"):
+    """The edge list sorted by column (geot_transpose_edges): (sorted_col, row_t, coef).
+
+    gather_scatter(grad_out, row_t, coef, sorted_col, num_x_rows, "sum") is then the
+    gradient w.r.t. x of gather_scatter(x, col, weight, row, num_rows, reduce)."""
+    _dev(col, "col", torch.int64, 1)
+    _dev(row, "row", torch.int64, 1)
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+        if weight.numel() != row.numel():
+            raise ValueError("weight must have one entry per edge")
+    if col.numel() != row.numel():
+        raise ValueError("col and row must have one entry per edge")
+    n = row.numel()
+    sc = torch.empty(n, dtype=torch.int64, device=row.device)
+    rt = torch.empty(n, dtype=torch.int64, device=row.device)
+    cf = torch.empty(n, dtype=torch.float32, device=row.device)
+    wp = weight.data_ptr() if weight is not None else None
+    with _OnDevice(row.device):
+        st = lib().geot_transpose_edges(col.data_ptr(), int(num_x_rows), wp, row.data_ptr(), n, int(num_rows),
+                                        OPS[reduce], sc.data_ptr(), rt.data_ptr(), cf.data_ptr(),
+                                        _stream(row.device))
+    _raise(st)
+    return sc, rt, cf
 
 
 def index_stats(index: torch.Tensor, num_segments: int) -> dict:

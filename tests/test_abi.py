@@ -181,3 +181,15 @@ def test_typed_arguments_are_checked_on_the_host():
     assert L.geot_segment_reduce_typed(src, 0, idx, 1, 1000, 10, 32, 0, out, None, ctypes.byref(sp)) == UNSUPPORTED
     # no-ops as in the fp32 call
     assert L.geot_segment_reduce_typed(None, 1, None, 1, 0, 0, 5, 0, None, None, None) == SUCCESS
+
+
+def test_transpose_arguments_are_checked_on_the_host():
+    L = lib()
+    col, row, w = FAKE, FAKE + (1 << 26), FAKE + (1 << 27)
+    a, b, c = FAKE + (1 << 30), FAKE + (1 << 31), FAKE + (1 << 32)
+    assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 2, a, b, c, None) == INVALID   # max
+    assert L.geot_transpose_edges(col, 10, w, row, -1, 5, 0, a, b, c, None) == INVALID
+    assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 0, None, b, c, None) == INVALID
+    assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 0, col + 8, b, c, None) == INVALID  # overlap
+    assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 0, a, a + 64, c, None) == INVALID  # outputs overlap
+    assert L.geot_transpose_edges(None, 10, None, None, 0, 5, 0, None, None, None, None) == SUCCESS

@@ -114,3 +114,30 @@ def test_gradients_match_a_torch_training_step():
     ax, aw = oracle.gather_scatter_backward(X, col, w, row, t, "sum", absolute=True)
     within(gx.cpu().numpy(), tX.grad.cpu().numpy(), ax, "grad_X vs torch")
     within(gw.cpu().numpy(), tw.grad.cpu().numpy(), aw, "grad_w vs torch")
+
+
+@pytest.mark.parametrize("weighted", [True, False])
+@pytest.mark.parametrize("op", ["sum", "mean"])
+def test_transpose_edges(weighted, op):
+    """geot_transpose_edges: the same (column, row, coefficient) triples, sorted by column
+    (the order inside a column is free, so both sides are compared in a canonical order),
+    and the forward gather over them equals the oracle's gradient w.r.t. X."""
+    p = random_gather_problem(41, 30000, 1200, 1700, 24, "zipf", "normal", weighted, 0.1)
+    X, col, w, row = p["X"], p["col"], p["weight"], p["index"]
+    n = row.size
+    sc, rt, cf = geot.transpose_edges(up(col), up(w), up(row), 1700, 1200, op)
+    sc, rt, cf = sc.cpu().numpy(), rt.cpu().numpy(), cf.cpu().numpy()
+    assert np.all(np.diff(sc) >= 0)
+    coef = w.copy() if w is not None else np.ones(n, dtype=np.float32)
+    if op == "mean":
+        deg = np.bincount(row, minlength=1200).astype(np.float32)
+        coef = (coef / deg[row]).astype(np.float32)   # one fp32 division, as the library
+    want = np.lexsort((coef.view(np.uint32), row, col))
+    got = np.lexsort((cf.view(np.uint32), rt, sc))
+    assert np.array_equal(sc[got], col[want]) and np.array_equal(rt[got], row[want])
+    assert np.array_equal(cf[got].view(np.uint32), coef[want].view(np.uint32))
+    g = np.random.default_rng(42).standard_normal((1200, 24)).astype(np.float32)
+    gx = geot.gather_scatter(up(g), up(rt), up(cf), up(sc), 1700, "sum").cpu().numpy()
+    rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op)
+    tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, absolute=True)
+    within(gx, rx, tx, f"transposed gather grad_X {op} weighted={weighted}")

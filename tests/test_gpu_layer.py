@@ -16,8 +16,10 @@ def gcn_norm(row, col, n):
     return (1.0 / np.sqrt(np.maximum(deg[row], 1) * np.maximum(deg[col], 1))).astype(np.float32)
 
 
-@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
-def test_two_layer_training_step(reduce):
+@pytest.mark.parametrize("reduce,cached", [("sum", False), ("mean", False), ("max", False),
+                                           ("sum", True), ("mean", True)])
+def test_two_layer_training_step(reduce, cached):
+    """cached: the layers take a Graph, whose transposed edge list serves the gradient."""
     n, F, H, C = 3000, 24, 32, 5
     q = random_gather_problem(301, 40000, n, n, F, "zipf", "normal", True, 0.0)
     row, col, X = q["index"], q["col"], q["X"]
@@ -33,8 +35,13 @@ def test_two_layer_training_step(reduce):
     # library path on the GPU
     rt, ct = torch.from_numpy(row).to(DEV), torch.from_numpy(col).to(DEV)
     wt = torch.from_numpy(w).to(DEV) if w is not None else None
-    h = torch.relu(m[0](torch.from_numpy(X).to(DEV), ct, rt, n, wt))
-    logits = m[1](h, ct, rt, n, wt)
+    if cached:
+        g = ga.Graph(ct, rt, n, wt)
+        h = torch.relu(m[0](torch.from_numpy(X).to(DEV), g))
+        logits = m[1](h, g)
+    else:
+        h = torch.relu(m[0](torch.from_numpy(X).to(DEV), ct, rt, n, wt))
+        logits = m[1](h, ct, rt, n, wt)
     loss = torch.nn.functional.cross_entropy(logits, torch.from_numpy(y).to(DEV))
     loss.backward()
     # reference: plain torch, fp64, CPU
@@ -57,3 +64,17 @@ def test_two_layer_training_step(reduce):
         ga_ = a.lin.weight.grad.double().cpu()
         gb_ = b.weight.grad
         assert torch.allclose(ga_, gb_, rtol=2e-3, atol=2e-5), (reduce, (ga_ - gb_).abs().max())
+
+
+def test_graph_cache_follows_weight_updates():
+    """A Graph rebuilds its transposed list when its weight tensor changes in place."""
+    n = 500
+    q = random_gather_problem(311, 6000, n, n, 4, "uniform", "normal", True, 0.0)
+    ct, rt = torch.from_numpy(q["col"]).to(DEV), torch.from_numpy(q["index"]).to(DEV)
+    w = torch.from_numpy(q["weight"]).to(DEV)
+    g = ga.Graph(ct, rt, n, w)
+    a = g.transposed("sum")[2].clone()
+    assert g.transposed("sum")[2] is g.transposed("sum")[2]   # reused while unchanged
+    w.mul_(2.0)
+    b = g.transposed("sum")[2]
+    assert torch.equal(torch.sort(b).values, torch.sort(2.0 * a).values)
