@@ -432,6 +432,9 @@ int64_t piece_rows_k(int64_t n, int64_t G) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// blocks that write the gap list, as a pass of their own or riding on the final partial level
+constexpr int kFoldedGapBlocks = 1024;
+
 geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
                             char *base, const std::vector<size_t> &off_v,
                             const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
@@ -517,6 +520,10 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.pcnt = (int64_t *)(base + off_c[l + 1]);
             a.ld_p = ld_p;
         }
+        if (l + 1 == lv.size() && l > 0) {  // the final level also fills the gap list of level 0
+            a.gaps = gaps;
+            a.gap_blocks = kFoldedGapBlocks;
+        }
         a.K = (int32_t)lv[l].K;
         a.ntiles = r.ntiles;
         a.mean = p.op == GEOT_OP_MEAN ? 1 : 0;
@@ -528,7 +535,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
         if (l > 0) piece_shape(r, &V, &L);
         GEOT_HIP(launch_ep(a, red, mode, V, r.NT, L, lv[l].nchunks, st), "launch element-parallel kernel");
         if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
-        if (l == 0)
+        if (l == 0 && lv.size() == 1)  // one level: a pass of its own (else the final level's extra blocks)
             GEOT_HIP(launch_gap_fill_rows(p.out, p.F, p.F, std::min(r.V, 4), (int64_t)r.L * r.V * r.NT, p.S,
                                           gaps, st),
                      "launch gap fill kernel");

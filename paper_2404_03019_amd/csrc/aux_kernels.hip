@@ -41,27 +41,7 @@ __global__ __launch_bounds__(256) void offsets_kernel(const int64_t *idx, int64_
 template <int V>
 __global__ __launch_bounds__(256) void gap_fill_rows_kernel(float *out, int64_t F, int64_t ld,
                                                             int64_t tw, int64_t rows, GapList g) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) *g.other = 0u;
-    const unsigned cnt = min(*g.count, kGapCap);
-    float z[V];
-#pragma unroll
-    for (int k = 0; k < V; ++k) z[k] = 0.0f;
-    for (unsigned q = blockIdx.x; q < cnt; q += gridDim.x) {
-        const int64_t *r = g.rec + 3 * (int64_t)q;
-        const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], rows);
-        const int64_t c0 = r[2] * tw;
-        const int64_t ncol = min(tw, F - c0);
-        if (hi <= lo || c0 < 0 || ncol <= 0) continue;
-        const int nvec = (int)((ncol + V - 1) / V);
-        int tpr = 1;                                  // threads per row (power of two)
-        while (tpr < nvec && tpr < 256) tpr <<= 1;
-        const int rows_per_pass = 256 / tpr;
-        const int j0 = threadIdx.x % tpr;
-        for (int64_t row = lo + threadIdx.x / tpr; row < hi; row += rows_per_pass) {
-            float *o = out + row * ld + c0;
-            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
-        }
-    }
+    gap_fill_rows_body<V>(out, F, ld, tw, rows, g, blockIdx.x, gridDim.x);
 }
 
 __global__ __launch_bounds__(256) void gap_fill_i64_kernel(int64_t *arr, int64_t len, GapList g) {

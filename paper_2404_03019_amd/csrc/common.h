@@ -175,6 +175,35 @@ __device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t h
     return fits;
 }
 
+// One block's share of the gap-list fill: records q = blk, blk + nblk, ...;
+// rows [first, end) of record q's column tile (tiles of `tw` columns) = 0,
+// clamped to `rows`. Block 0 zeroes the next call's counter.
+template <int V>
+__device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_t ld, int64_t tw, int64_t rows,
+                                                   const GapList &g, int64_t blk, int64_t nblk) {
+    if (blk == 0 && threadIdx.x == 0) *g.other = 0u;
+    const unsigned cnt = min(*g.count, kGapCap);
+    float z[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) z[k] = 0.0f;
+    for (int64_t q = blk; q < (int64_t)cnt; q += nblk) {
+        const int64_t *r = g.rec + 3 * q;
+        const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], rows);
+        const int64_t c0 = r[2] * tw;
+        const int64_t ncol = min(tw, F - c0);
+        if (hi <= lo || c0 < 0 || ncol <= 0) continue;
+        const int nvec = (int)((ncol + V - 1) / V);
+        int tpr = 1;  // threads per row (power of two)
+        while (tpr < nvec && tpr < 256) tpr <<= 1;
+        const int rows_per_pass = 256 / tpr;
+        const int j0 = threadIdx.x % tpr;
+        for (int64_t row = lo + threadIdx.x / tpr; row < hi; row += rows_per_pass) {
+            float *o = out + row * ld + c0;
+            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
+        }
+    }
+}
+
 // DPP lane moves (GFX9 encodings): row_shr:S shifts within each 16-lane row;
 // row_bcast:15 / row_bcast:31 broadcast lane 15 of a row (lane 31) to the
 // next row (rows 2 and 3). Lanes whose source does not exist keep their own

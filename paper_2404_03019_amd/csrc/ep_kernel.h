@@ -77,6 +77,15 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     const int gl = lane - gw * L;     // lane within the row group
     const int g = wave * GW + gw;     // row group within the block
 
+    if constexpr (MODE == SRC_PIECES) {
+        // the final level's extra blocks write the runs of empty segments level 0 listed
+        const int64_t main_blocks = (int64_t)gridDim.x - a.gap_blocks;
+        if (a.gap_blocks > 0 && (int64_t)blockIdx.x >= main_blocks) {
+            gap_fill_rows_body<V>(a.out, a.F, a.ld_out, (int64_t)TW, a.S, a.gaps, blockIdx.x - main_blocks,
+                                  a.gap_blocks);
+            return;
+        }
+    }
     const int64_t chunk = blockIdx.x / a.ntiles;
     const int tile = (int)(blockIdx.x - chunk * a.ntiles);
     const int64_t bsize = (int64_t)G * a.K;
@@ -516,7 +525,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
 
 template <int RED, int MODE, int V, int NT, int L, int E, typename I>
 hipError_t launch_one(const EpArgs &a, int64_t nchunks, hipStream_t stream) {
-    const int64_t blocks = nchunks * a.ntiles;
+    const int64_t blocks = nchunks * a.ntiles + (MODE == SRC_PIECES ? (int64_t)a.gap_blocks : 0);
     if (blocks <= 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     if (a.nt_rows) {

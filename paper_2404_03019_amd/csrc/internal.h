@@ -65,6 +65,8 @@ struct EpArgs {
     int32_t idx32;          // idx and col hold int32 (SRC_PIECES: 0)
     int32_t nt_rows;        // rows mode: non-temporal row loads (tiles of >= 128 bytes only)
     int32_t meta_stride;    // gather mode: idx, col and w of edge e at [e * meta_stride] (0 or 1: arrays)
+    int32_t gap_blocks;     // SRC_PIECES, final level: this many extra blocks fill the gap list `gaps`
+                            // (written by level 0, which has finished), in tiles of the level's width
 };
 
 // Dispatches on (elem, idx32) to the translation unit holding those instantiations.
