@@ -152,14 +152,16 @@ __device__ __forceinline__ int32_t shfl_up_cnt(int32_t v, int delta) { return sh
 __device__ __forceinline__ int64_t shfl_up_cnt(int64_t v, int delta) { return shfl_up_i64(v, delta); }
 
 // Appends the run of segments [lo, hi) (value carried along) to a gap list,
-// cut into records of at most kGapChunk segments. `lanes` lanes starting at
-// lane `lead` (all in the same state) call it together; the lead lane takes
-// the slots and the lanes share the writes. Returns false when the list is
-// full: the caller then writes the run itself (the slots it took hold empty
-// records).
+// cut into records of kGapChunk segments, or into kGapMaxRecs longer ones for
+// a run longer than that many chunks (so no run needs more than kGapMaxRecs
+// slots). `lanes` lanes starting at lane `lead` (all in the same state) call it
+// together; the lead lane takes the slots and the lanes share the writes.
+// Returns false when the list is full: the caller then writes the run itself
+// (the slots it took hold empty records).
 __device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t hi, int64_t value,
                                          int lead, int lane_in, int lanes) {
-    const int64_t nrec = (hi - lo + kGapChunk - 1) / kGapChunk;
+    const int64_t chunk = max(kGapChunk, (hi - lo + kGapMaxRecs - 1) / kGapMaxRecs);
+    const int64_t nrec = (hi - lo + chunk - 1) / chunk;
     unsigned base = 0;
     if (lane_in == 0) base = atomicAdd(g.count, (unsigned)nrec);
     if (lanes > 1) base = (unsigned)__shfl((int)base, lead, 64);
@@ -167,9 +169,9 @@ __device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t h
     const int64_t end = fits ? nrec : ((int64_t)kGapCap > (int64_t)base ? (int64_t)kGapCap - base : 0);
     for (int64_t q = lane_in; q < end; q += lanes) {
         int64_t *r = g.rec + 3 * ((int64_t)base + q);
-        const int64_t a = fits ? lo + q * kGapChunk : 0;
+        const int64_t a = fits ? lo + q * chunk : 0;
         r[0] = a;
-        r[1] = fits ? min(hi, a + kGapChunk) : 0;
+        r[1] = fits ? min(hi, a + chunk) : 0;
         r[2] = value;
     }
     return fits;

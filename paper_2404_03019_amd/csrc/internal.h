@@ -24,12 +24,14 @@ enum ElemType : int { ELEM_F32 = 0, ELEM_BF16 = 1, ELEM_F16 = 2 };
 
 // Runs of empty segments longer than kGapRun segments are not written by the
 // kernel that finds them: it appends them to a device list, cut into records
-// of at most kGapChunk segments, and a grid-wide pass writes them afterwards.
+// of kGapChunk segments (at most kGapMaxRecs records per run), and a grid-wide
+// pass writes them afterwards.
 // The list counter alternates between two words from call to call; the fill
 // pass of one call zeroes the other word, so no memset is ever needed.
 constexpr int kGapRun = 32;
-constexpr int64_t kGapChunk = 8192;
-constexpr unsigned kGapCap = 8192;
+constexpr int64_t kGapChunk = 8192;     // segments per record (longer when a run would need more records)
+constexpr int64_t kGapMaxRecs = 64;     // records one run takes at most
+constexpr unsigned kGapCap = 65536;     // records in the list (24 bytes each)
 
 struct GapList {
     unsigned int *count;   // records appended in this call

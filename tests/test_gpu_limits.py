@@ -101,3 +101,24 @@ def test_fused_more_than_2_31_edges():
         for op in ("sum", "max"):
             ref = oracle.gather_scatter(Xh, c, None, z, 1, op)
             assert np.array_equal(got[op][r:r + 1], ref), (op, r)
+
+
+def test_most_segments():
+    """num_segments = 2^31 - 1 (the largest accepted) with 1,000 rows: runs of empty
+    segments of about 2.1 M each and one of about 10^9 after the last row, more records
+    than the gap list holds (the rest are written by their row groups)."""
+    S, F, n = (1 << 31) - 1, 1, 1000
+    rng = np.random.default_rng(12)
+    idx = np.unique(rng.integers(0, S // 2, size=n)).astype(np.int64)   # sorted, distinct
+    idx[-1] = S // 2 + 12345
+    n = idx.size
+    src = rng.integers(-8, 9, size=(n, F)).astype(np.float32)
+    out = torch.full((S, F), 7.0, device=DEV)
+    say("limits: 2^31-1 segments")
+    geot.segment_reduce(torch.from_numpy(src).to(DEV), torch.from_numpy(idx).to(DEV), S, "sum", out=out)
+    torch.cuda.synchronize()
+    seg, first = np.unique(idx, return_index=True)
+    want = np.add.reduceat(src[:, 0].astype(np.float64), first).astype(np.float32)
+    got = out[torch.from_numpy(seg).to(DEV), 0].cpu().numpy()
+    assert np.array_equal(got, want)
+    assert int(torch.count_nonzero(out).item()) == int(np.count_nonzero(want))
