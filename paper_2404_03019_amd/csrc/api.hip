@@ -114,7 +114,6 @@ struct StreamKey {
 struct StreamCtx {
     void *p = nullptr;
     size_t bytes = 0;
-    int parity = 0;
     bool dirty = false;  // a launch failed after the gap list was handed out
 };
 std::mutex g_cache_mu;
@@ -125,7 +124,7 @@ constexpr size_t kGapArea = kGapHeader + (size_t)kGapCap * 3 * sizeof(int64_t);
 
 // `user` gets `bytes` of scratch after the gap list; `g` the list of this call
 // (NULL when the call runs no gap-fill pass: only a call that runs one may take
-// the list, since its fill pass zeroes the next call's counter).
+// the list, since its fill pass is what empties it again).
 geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList *g,
                              StreamCtx **ctx_out) {
     *user = nullptr;
@@ -155,10 +154,9 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
     }
     if (g) {
         unsigned *ctrl = (unsigned *)e.p;
-        g->count = ctrl + e.parity;
-        g->other = ctrl + (1 - e.parity);
+        g->count = ctrl;
+        g->ticket = ctrl + 1;
         g->rec = (int64_t *)((char *)e.p + kGapHeader);
-        e.parity ^= 1;
     }
     *user = bytes ? (char *)e.p + kGapArea : nullptr;
     *ctx_out = &e;

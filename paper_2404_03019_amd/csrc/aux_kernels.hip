@@ -45,13 +45,13 @@ __global__ __launch_bounds__(256) void gap_fill_rows_kernel(float *out, int64_t 
 }
 
 __global__ __launch_bounds__(256) void gap_fill_i64_kernel(int64_t *arr, int64_t len, GapList g) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) *g.other = 0u;
-    const unsigned cnt = min(*g.count, kGapCap);
+    const unsigned cnt = gap_count(g);
     for (unsigned q = blockIdx.x; q < cnt; q += gridDim.x) {
         const int64_t *r = g.rec + 3 * (int64_t)q;
         const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], len), v = r[2];
         for (int64_t t = lo + threadIdx.x; t < hi; t += 256) arr[t] = v;
     }
+    gap_done(g, gridDim.x);
 }
 
 __global__ __launch_bounds__(256) void len_stats_kernel(const int64_t *off, int64_t S,

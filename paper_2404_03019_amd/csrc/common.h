@@ -177,14 +177,36 @@ __device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t h
     return fits;
 }
 
+// A fill block's record count: read once per block, before the block takes
+// its ticket (so before the list can be reset).
+__device__ __forceinline__ unsigned gap_count(const GapList &g) {
+    __shared__ unsigned s_cnt;
+    if (threadIdx.x == 0) s_cnt = min(*g.count, kGapCap);
+    __syncthreads();
+    return s_cnt;
+}
+
+// A fill block is done: the last of the pass's `nblk` blocks empties the list
+// (every block read the count before taking its ticket).
+__device__ __forceinline__ void gap_done(const GapList &g, int64_t nblk) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        const unsigned t = atomicAdd(g.ticket, 1u);
+        if ((int64_t)t == nblk - 1) {
+            atomicExch(g.count, 0u);
+            atomicExch(g.ticket, 0u);
+        }
+    }
+}
+
 // One block's share of the gap-list fill: records q = blk, blk + nblk, ...;
 // rows [first, end) of record q's column tile (tiles of `tw` columns) = 0,
-// clamped to `rows`. Block 0 zeroes the next call's counter.
+// clamped to `rows`. The pass's last block empties the list.
 template <int V>
 __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_t ld, int64_t tw, int64_t rows,
                                                    const GapList &g, int64_t blk, int64_t nblk) {
-    if (blk == 0 && threadIdx.x == 0) *g.other = 0u;
-    const unsigned cnt = min(*g.count, kGapCap);
+    const unsigned cnt = gap_count(g);
     float z[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) z[k] = 0.0f;
@@ -204,6 +226,7 @@ __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_
             for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
         }
     }
+    gap_done(g, nblk);
 }
 
 // DPP lane moves (GFX9 encodings): row_shr:S shifts within each 16-lane row;

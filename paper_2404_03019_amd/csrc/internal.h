@@ -26,8 +26,11 @@ enum ElemType : int { ELEM_F32 = 0, ELEM_BF16 = 1, ELEM_F16 = 2 };
 // kernel that finds them: it appends them to a device list, cut into records
 // of kGapChunk segments (at most kGapMaxRecs records per run), and a grid-wide
 // pass writes them afterwards.
-// The list counter alternates between two words from call to call; the fill
-// pass of one call zeroes the other word, so no memset is ever needed.
+// The fill pass resets the list itself: each of its blocks reads the count
+// once and then takes a ticket, and the block that takes the last ticket
+// zeroes the count and the ticket. The list is therefore empty whenever no
+// call is running (no memset, no host-side state: calls captured in a HIP
+// graph replay correctly).
 constexpr int kGapRun = 32;
 constexpr int64_t kGapChunk = 8192;     // segments per record (longer when a run would need more records)
 constexpr int64_t kGapMaxRecs = 64;     // records one run takes at most
@@ -35,7 +38,7 @@ constexpr unsigned kGapCap = 65536;     // records in the list (24 bytes each)
 
 struct GapList {
     unsigned int *count;   // records appended in this call
-    unsigned int *other;   // the counter of the next call (zeroed by this call's fill pass)
+    unsigned int *ticket;  // fill blocks done (the last one resets count and ticket)
     int64_t *rec;          // [kGapCap][3]: first segment, end segment, value
 };
 
@@ -109,8 +112,8 @@ hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off
                           hipStream_t stream);
 
 // Grid-wide passes over a gap list: out rows [first, end) = 0 in the columns of
-// tile `value` (tiles of `tw` columns), or arr[first, end) = value. Both zero
-// the other call's counter.
+// tile `value` (tiles of `tw` columns), or arr[first, end) = value. Both leave
+// the list empty.
 // Records are clamped to the `rows` (or `len`) of the current call.
 hipError_t launch_gap_fill_rows(float *out, int64_t F, int64_t ld, int V, int64_t tw, int64_t rows,
                                 GapList gaps, hipStream_t stream);
