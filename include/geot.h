@@ -33,9 +33,12 @@
  *    share one stream must be issued one after the other: two host threads
  *    enqueuing on the same stream at once would interleave their kernels
  *    over that stream's buffer. Different streams are independent.
- *  - Calls can be captured in a HIP graph and replayed (they keep no per-call
- *    host state and issue no memset). Make one call of the same shapes on the
- *    capture stream first, so the stream's buffer exists before the capture.
+ *  - The reduction calls (forward) can be captured in a HIP graph and replayed:
+ *    they keep no per-call host state and issue no memset. Make one call of the
+ *    same shapes on the capture stream first, so the stream's buffer exists
+ *    before the capture. The gradient calls and geot_transpose_edges take
+ *    their temporaries from the pool on every call (stream-ordered
+ *    allocations); their capture is not covered by the tests.
  *  - Preconditions: the index is non-decreasing and 0 <= index < num_segments;
  *    for the gather form 0 <= col < num_x_rows. They are not checked by the
  *    reduction calls (geot_check_index checks them). Violations give
