@@ -270,8 +270,8 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
  * atomic cursor); any order is a valid input to the gather. op must be sum or
  * mean (the max gradient depends on the forward result). Edges whose column is
  * out of range are left out, and the tail of the outputs is then unspecified.
- * Temporary memory: 12 bytes per X row (and 8 per row for mean), from the
- * library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
+ * Temporary memory: 16 bytes per edge (when num_x_rows < 2^31) and 12 per X
+ * row (and 8 per row for mean), from the library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
  * sizes, num_rows >= 2^31, another op, or outputs that overlap the inputs or
  * each other.                                                               */
 geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,

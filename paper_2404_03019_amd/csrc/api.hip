@@ -867,12 +867,16 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
     const size_t o_cnt = take((size_t)((nx + 1) & ~(int64_t)1) * 4);
     const size_t o_off = take((size_t)(nx + 1) * 8);
     const size_t o_sums = take((size_t)((nx + 4095) / 4096 + 1) * 8);
+    // placed as 16-byte records (one random store per edge), then split into the outputs
+    const bool packed = nx <= (int64_t)INT32_MAX;
+    const size_t o_rec = packed ? take((size_t)nnz * 16) : 0;
     ScratchGuard sg;
     sg.st = st;
     geot_status_t s = scratch_alloc(&sg.p, at, st);
     if (s != GEOT_SUCCESS) return s;
     char *base = (char *)sg.p;
     int64_t *roff = mean ? (int64_t *)(base + o_roff) : nullptr;
+    int32_t *rec = packed ? (int32_t *)(base + o_rec) : nullptr;
     if (mean) {
         void *unused = nullptr;
         GapList gaps;
@@ -888,8 +892,9 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
     }
     GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
                               (int64_t *)(base + o_off), (int64_t *)(base + o_sums), sorted_col_out, row_out,
-                              coef_out, nullptr, st),
+                              coef_out, rec, st),
              "launch transpose kernels");
+    if (packed) GEOT_HIP(launch_unpack(rec, nnz, sorted_col_out, row_out, coef_out, st), "launch unpack kernel");
     void *p_free = sg.p;
     sg.p = nullptr;
     return scratch_free(p_free, st);

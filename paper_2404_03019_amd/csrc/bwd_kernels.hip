@@ -374,6 +374,19 @@ __global__ __launch_bounds__(256) void place_kernel(const int64_t *col, int64_t 
     }
 }
 
+// the 16-byte records {col, row, coefficient, 0} as three arrays (one streaming pass)
+__global__ __launch_bounds__(256) void unpack_kernel(const int32_t *rec, int64_t n, int64_t *key_t,
+                                                     int64_t *row_t, float *w_t) {
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
+        if (e >= n) break;
+        const int4 v = *reinterpret_cast<const int4 *>(rec + 4 * e);
+        key_t[e] = (int64_t)v.x;
+        row_t[e] = (int64_t)v.y;
+        w_t[e] = __int_as_float(v.z);
+    }
+}
+
 __global__ __launch_bounds__(256) void fill_u64_kernel(unsigned long long *p, int64_t n,
                                                        unsigned long long v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -417,6 +430,15 @@ hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, 
     else
         hipLaunchKernelGGL(place_kernel<false>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, mean ? 1 : 0,
                            n, off, counts, key_t, row_t, w_t, rec);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t *row_t, float *w_t,
+                         hipStream_t st) {
+    if (n <= 0) return hipSuccess;
+    const int64_t b = (n + 256 * kPasses - 1) / (256 * kPasses);
+    if (b > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(unpack_kernel, dim3((unsigned)b), dim3(256), 0, st, rec, n, key_t, row_t, w_t);
     return hipGetLastError();
 }
 

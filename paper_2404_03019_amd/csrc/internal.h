@@ -137,6 +137,10 @@ enum BwdOp : int { GEOT_BWD_SUM = 0, GEOT_BWD_MEAN = 1, GEOT_BWD_MAX = 2 };
 
 hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long v, hipStream_t st);
 
+// records {int32 key, int32 row, float coefficient, 0} -> key_t, row_t, w_t
+hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t *row_t, float *w_t,
+                         hipStream_t st);
+
 // Counting sort of the edges by col: key_t (sorted col), row_t and w_t (weight, divided by
 // the row's edge count for mean; roff = row starts) of the transposed problem.
 // counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
