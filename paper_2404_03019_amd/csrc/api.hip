@@ -774,6 +774,8 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     // (X with 2^31 rows or more) three arrays
     const bool packed = nx <= (int64_t)INT32_MAX;
     const size_t o_rec = transpose && packed ? take((size_t)nnz * 16) : 0;
+    const size_t bucket_b = transpose ? transpose_scratch_bytes(nnz, nx) : 0;
+    const size_t o_bucket = bucket_b ? take(bucket_b) : 0;
     const size_t o_key = transpose && !packed ? take((size_t)nnz * 8) : 0;
     const size_t o_row = transpose && !packed ? take((size_t)nnz * 8) : 0;
     const size_t o_w = transpose && !packed ? take((size_t)nnz * 4) : 0;
@@ -808,9 +810,9 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
         int64_t *row_t = packed ? nullptr : (int64_t *)(base + o_row);
         float *w_t = packed ? nullptr : (float *)(base + o_w);
         int32_t *rec = packed ? (int32_t *)(base + o_rec) : nullptr;
-        GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
+        GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                                   (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, rec,
-                                  st),
+                                  bucket_b ? base + o_bucket : nullptr, st),
                  "launch transpose kernels");
         Problem tp{true, grad_out, num_rows, row_t, w_t, key_t, nnz, nx, F, GEOT_OP_SUM, grad_X};
         if (packed) {
@@ -867,7 +869,10 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
     const size_t o_cnt = take((size_t)((nx + 1) & ~(int64_t)1) * 4);
     const size_t o_off = take((size_t)(nx + 1) * 8);
     const size_t o_sums = take((size_t)((nx + 4095) / 4096 + 1) * 8);
-    // placed as 16-byte records (one random store per edge), then split into the outputs
+    // placed as 16-byte records (one store per edge; grouped by buckets of columns first for
+    // large inputs) and split into the outputs by one streaming pass
+    const size_t bucket_b = transpose_scratch_bytes(nnz, nx);
+    const size_t o_bucket = bucket_b ? take(bucket_b) : 0;
     const bool packed = nx <= (int64_t)INT32_MAX;
     const size_t o_rec = packed ? take((size_t)nnz * 16) : 0;
     ScratchGuard sg;
@@ -890,9 +895,9 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
         }());
         if (s != GEOT_SUCCESS) return s;
     }
-    GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, mean, nnz, (unsigned *)(base + o_cnt),
+    GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                               (int64_t *)(base + o_off), (int64_t *)(base + o_sums), sorted_col_out, row_out,
-                              coef_out, rec, st),
+                              coef_out, rec, bucket_b ? base + o_bucket : nullptr, st),
              "launch transpose kernels");
     if (packed) GEOT_HIP(launch_unpack(rec, nnz, sorted_col_out, row_out, coef_out, st), "launch unpack kernel");
     void *p_free = sg.p;

@@ -352,7 +352,7 @@ __global__ __launch_bounds__(256) void scan_add_kernel(int64_t *off, int64_t n, 
 // random, and every store touches its own cache line)
 template <bool PACKED>
 __global__ __launch_bounds__(256) void place_kernel(const int64_t *col, int64_t nx, const int64_t *row,
-                                                    const float *w, const int64_t *roff, int mean,
+                                                    const float *w, const int64_t *roff, int64_t nrows, int mean,
                                                     int64_t n, const int64_t *off, unsigned *cursor,
                                                     int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec) {
     for (int q = 0; q < kPasses; ++q) {
@@ -363,13 +363,180 @@ __global__ __launch_bounds__(256) void place_kernel(const int64_t *col, int64_t 
         const int64_t pos = off[c] + (int64_t)atomicSub(cursor + c, 1u) - 1;
         const int64_t r = row[e];
         float coef = w ? w[e] : 1.0f;
-        if (mean) coef = coef / (float)(roff[r + 1] - roff[r]);
+        if (mean && (uint64_t)r < (uint64_t)nrows) coef = coef / (float)(roff[r + 1] - roff[r]);
         if constexpr (PACKED) {
             *reinterpret_cast<int4 *>(rec + 4 * pos) = make_int4((int)c, (int)r, __float_as_int(coef), 0);
         } else {
             key_t[pos] = c;
             row_t[pos] = r;
             w_t[pos] = coef;
+        }
+    }
+}
+
+// ---- the transposition in buckets of columns (large inputs) ---------------
+// The edges are first grouped by buckets of at most kBucketCols consecutive
+// columns (block-local counts in LDS, a scan, a scatter with LDS cursors) as
+// 16-byte records; then one block per bucket counts, scans and places the
+// bucket's records by column in LDS. No pass takes a global atomic per edge
+// (on MI355X those run at about 33 G/s, local or not, and bound the direct
+// transposition).
+constexpr int kBucketChunk = 128 * 256;  // edges per block in the bucket passes
+constexpr int64_t kBucketTarget = 1 << 16;  // records per bucket aimed at
+constexpr int kMaxBuckets = 4096;
+constexpr int kBucketCols = 2048;  // columns per bucket sorted in LDS
+constexpr int64_t kBucketMinEdges = 1 << 20;  // below this the direct transposition is as fast
+
+// counts of the block's edges per bucket, bucket-major: bcnt[b * nblk + block]
+__global__ __launch_bounds__(256) void bucket_count_kernel(const int64_t *col, int64_t n, int64_t nx, int shift,
+                                                           int nbuckets, int64_t nblk, unsigned *bcnt) {
+    __shared__ unsigned h[kMaxBuckets];
+    for (int b = threadIdx.x; b < nbuckets; b += 256) h[b] = 0;
+    __syncthreads();
+    const int64_t e0 = (int64_t)blockIdx.x * kBucketChunk;
+    for (int k = 0; k < kBucketChunk / 256; ++k) {
+        const int64_t e = e0 + (int64_t)k * 256 + threadIdx.x;
+        if (e >= n) break;
+        const int64_t c = col[e];
+        if ((uint64_t)c < (uint64_t)nx) atomicAdd(&h[(int)(c >> shift)], 1u);
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b < nbuckets; b += 256) bcnt[(int64_t)b * nblk + blockIdx.x] = h[b];
+}
+
+// total[0] = off[len - 1] + cnt[len - 1]: the records the scatter writes
+__global__ void scan_total_kernel(const int64_t *off, const unsigned *cnt, int64_t len, int64_t *total) {
+    if (threadIdx.x == 0 && blockIdx.x == 0) total[0] = off[len - 1] + (int64_t)cnt[len - 1];
+}
+
+// the block's edges as 16-byte records {col, row, coefficient, 0} into bucket order; the
+// cursors hold absolute record positions (n < 2^32 on this path). Each thread loads kU
+// edges before it places them.
+__global__ __launch_bounds__(256) void bucket_scatter_kernel(const int64_t *col, int64_t nx, const int64_t *row,
+                                                             const float *w, const int64_t *roff, int64_t nrows,
+                                                             int mean, int64_t n, int shift, int nbuckets, int64_t nblk,
+                                                             const int64_t *boff, int32_t *tmp) {
+    constexpr int kU = 4;
+    __shared__ unsigned cur[kMaxBuckets];
+    for (int b = threadIdx.x; b < nbuckets; b += 256) cur[b] = (unsigned)boff[(int64_t)b * nblk + blockIdx.x];
+    __syncthreads();
+    const int64_t e0 = (int64_t)blockIdx.x * kBucketChunk;
+    const int64_t e1 = min(e0 + (int64_t)kBucketChunk, n);
+    for (int64_t b0 = e0; b0 < e1; b0 += 256 * kU) {
+        int64_t c[kU], r[kU];
+        float wt[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int64_t e = b0 + u * 256 + threadIdx.x;
+            const bool in = e < e1;
+            c[u] = in ? col[e] : -1;
+            r[u] = in ? row[e] : 0;
+            wt[u] = in && w ? w[e] : 1.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            if ((uint64_t)c[u] >= (uint64_t)nx) continue;
+            const unsigned pos = atomicAdd(&cur[(int)(c[u] >> shift)], 1u);
+            float coef = wt[u];
+            if (mean && (uint64_t)r[u] < (uint64_t)nrows) coef = coef / (float)(roff[r[u] + 1] - roff[r[u]]);
+            *reinterpret_cast<int4 *>(tmp + 4 * (int64_t)pos) =
+                make_int4((int)c[u], (int)r[u], __float_as_int(coef), 0);
+        }
+    }
+}
+
+// One block per bucket: its records tmp[start, end) (columns b << shift ..) are
+// counted per column, scanned and placed within the bucket's output range, all
+// in LDS. A wave whose lanes share lane 0's column takes their slots with one
+// LDS atomic (so a column holding most of a bucket does not serialise).
+template <bool PACKED>
+__global__ __launch_bounds__(256) void bucket_sort_kernel(const int32_t *tmp, const int64_t *boff, int64_t nblk,
+                                                          const int64_t *total, int shift, int nbuckets,
+                                                          int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec) {
+    constexpr int kU = 8;
+    __shared__ unsigned h[kBucketCols];
+    __shared__ unsigned s_t[256];
+    const int b = blockIdx.x;
+    const int64_t lo = boff[(int64_t)b * nblk];
+    const int64_t hi = b + 1 < nbuckets ? boff[(int64_t)(b + 1) * nblk] : *total;
+    const int ncols = 1 << shift;
+    const unsigned mask = (unsigned)ncols - 1u;
+    const int lane = threadIdx.x & 63;
+    for (int c = threadIdx.x; c < ncols; c += 256) h[c] = 0;
+    __syncthreads();
+    // slot of this lane's record among its column's (claims from h, aggregating lane 0's column)
+    auto claim = [&](unsigned key, bool valid) -> unsigned {
+        const unsigned k0 = (unsigned)__shfl((int)key, 0, 64);
+        const bool same = valid && key == k0;
+        const unsigned long long m = __ballot(same);
+        const int leader = m ? __ffsll((long long)m) - 1 : 0;
+        unsigned base = 0;
+        if (same && lane == leader) base = atomicAdd(&h[k0], (unsigned)__popcll(m));
+        base = (unsigned)__shfl((int)base, leader, 64);
+        unsigned r = 0;
+        if (same) r = base + (unsigned)__popcll(m & ((1ull << lane) - 1ull));
+        else if (valid) r = atomicAdd(&h[key], 1u);
+        return r;
+    };
+    // kU records per thread in flight: a bucket is walked by its one block
+    for (int64_t i0 = lo; i0 < hi; i0 += 256 * kU) {
+        unsigned key[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int64_t i = i0 + u * 256 + threadIdx.x;
+            key[u] = i < hi ? ((unsigned)tmp[4 * i] & mask) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) (void)claim(key[u], i0 + u * 256 + threadIdx.x < hi);
+    }
+    __syncthreads();
+    // exclusive scan of h[0, ncols): 8 columns per thread, then across the threads
+    constexpr int kPer = kBucketCols / 256;
+    unsigned v[kPer];
+    unsigned t = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int c = threadIdx.x * kPer + k;
+        v[k] = c < ncols ? h[c] : 0u;
+        t += v[k];
+    }
+    s_t[threadIdx.x] = t;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {
+        const unsigned o = threadIdx.x >= (unsigned)d ? s_t[threadIdx.x - d] : 0u;
+        __syncthreads();
+        s_t[threadIdx.x] += o;
+        __syncthreads();
+    }
+    unsigned run = s_t[threadIdx.x] - t;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int c = threadIdx.x * kPer + k;
+        if (c < ncols) h[c] = run;
+        run += v[k];
+    }
+    __syncthreads();
+    for (int64_t i0 = lo; i0 < hi; i0 += 256 * kU) {
+        int4 rv[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int64_t i = i0 + u * 256 + threadIdx.x;
+            rv[u] = i < hi ? *reinterpret_cast<const int4 *>(tmp + 4 * i) : make_int4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const bool valid = i0 + u * 256 + threadIdx.x < hi;
+            const unsigned r = claim((unsigned)rv[u].x & mask, valid);
+            if (valid) {
+                const int64_t pos = lo + (int64_t)r;
+                if constexpr (PACKED) {
+                    *reinterpret_cast<int4 *>(rec + 4 * pos) = rv[u];
+                } else {
+                    key_t[pos] = (int64_t)rv[u].x;
+                    row_t[pos] = (int64_t)rv[u].y;
+                    w_t[pos] = __int_as_float(rv[u].z);
+                }
+            }
         }
     }
 }
@@ -403,13 +570,93 @@ int64_t grid_rows(int64_t rows, int nvec) {
     return b < 1 ? 1 : b;
 }
 
+// exclusive scan of len unsigned counts into off (sums: ceil(len / kScanTile) scratch); off[len] = last
+hipError_t scan_counts(const unsigned *counts, int64_t len, int64_t *off, int64_t *sums, int64_t last,
+                       hipStream_t st) {
+    const int64_t ntiles = (len + kScanTile - 1) / kScanTile;
+    if (ntiles > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(scan_tiles_kernel, dim3((unsigned)ntiles), dim3(256), 0, st, counts, len, off, sums);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(256), 0, st, sums, ntiles);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_add_kernel, dim3((unsigned)((len + 255) / 256)), dim3(256), 0, st, off, len, sums, last);
+    return hipGetLastError();
+}
+
+// bucket layout: 2^bb buckets of 2^shift columns: at most kBucketCols columns (nx <= 2^23),
+// at most about kBucketTarget records (on average) per bucket, and at least 1024 buckets
+// where the columns allow, so the per-bucket sort has blocks for every CU; nblk blocks of
+// kBucketChunk edges in the grouping passes
+int64_t bucket_words(int64_t n, int64_t nx, int *shift, int *nbuckets, int64_t *nblk) {
+    int nb = 1;
+    while (nb < 23 && ((int64_t)1 << nb) < nx) ++nb;     // bits of the largest column
+    int by_rows = 0;
+    while (by_rows < 12 && (kBucketTarget << by_rows) < n) ++by_rows;
+    const int bb = std::min({nb, 12, std::max({nb - 11, by_rows, 10})});
+    *shift = nb - bb;
+    *nbuckets = 1 << bb;
+    *nblk = (n + kBucketChunk - 1) / kBucketChunk;
+    return (int64_t)*nbuckets * *nblk;
+}
+
+}  // namespace
+
+size_t transpose_scratch_bytes(int64_t n, int64_t nx) {
+    // per-bucket counts are 32-bit: n < 2^32
+    // and at least 256 buckets (nx > 128)
+    if (n < kBucketMinEdges || n > (int64_t)UINT32_MAX || nx > ((int64_t)1 << 23) || nx <= 128) return 0;
+    int shift, nb;
+    int64_t nblk;
+    const int64_t len = bucket_words(n, nx, &shift, &nb, &nblk);
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    return a256((size_t)len * 4) + a256((size_t)(len + 1) * 8) + a256((size_t)((len + kScanTile - 1) / kScanTile + 1) * 8) +
+           a256(64) + a256((size_t)n * 16);
+}
+
+namespace {
+
+hipError_t launch_transpose_bucketed(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
+                                     const int64_t *roff, int64_t nrows, bool mean, int64_t n, int64_t *key_t, int64_t *row_t,
+                                     float *w_t, int32_t *rec, char *scratch, hipStream_t st) {
+    int shift, nb;
+    int64_t nblk;
+    const int64_t len = bucket_words(n, nx, &shift, &nb, &nblk);
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    unsigned *bcnt = (unsigned *)scratch;
+    int64_t *boff = (int64_t *)(scratch + a256((size_t)len * 4));
+    int64_t *bsums = (int64_t *)((char *)boff + a256((size_t)(len + 1) * 8));
+    int64_t *total = (int64_t *)((char *)bsums + a256((size_t)((len + kScanTile - 1) / kScanTile + 1) * 8));
+    int32_t *tmp = (int32_t *)((char *)total + a256(64));
+    if (nblk > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(bucket_count_kernel, dim3((unsigned)nblk), dim3(256), 0, st, col, n, nx, shift, nb, nblk, bcnt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = scan_counts(bcnt, len, boff, bsums, 0, st)) != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_total_kernel, dim3(1), dim3(64), 0, st, boff, bcnt, len, total);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(bucket_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+                       mean ? 1 : 0, n, shift, nb, nblk, boff, tmp);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (rec)
+        hipLaunchKernelGGL(bucket_sort_kernel<true>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
+                           shift, nb, key_t, row_t, w_t, rec);
+    else
+        hipLaunchKernelGGL(bucket_sort_kernel<false>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
+                           shift, nb, key_t, row_t, w_t, rec);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
-                            const int64_t *roff, bool mean, int64_t n, unsigned *counts, int64_t *off,
+                            const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                             int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                            hipStream_t st) {
+                            char *bucket_scratch, hipStream_t st) {
     if (n <= 0 || nx <= 0) return hipSuccess;
+    if (bucket_scratch && transpose_scratch_bytes(n, nx) > 0)
+        return launch_transpose_bucketed(col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec, bucket_scratch,
+                                         st);
     hipError_t e = launch_zero_u64((unsigned long long *)counts, (nx + 1) / 2, st);
     if (e != hipSuccess) return e;
     const int64_t geb = (n + 256 * kPasses - 1) / (256 * kPasses);
@@ -417,18 +664,14 @@ hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, 
     const unsigned ge = (unsigned)geb;
     hipLaunchKernelGGL(hist_kernel, dim3(ge), dim3(256), 0, st, col, n, nx, counts);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t ntiles = (nx + kScanTile - 1) / kScanTile;
-    hipLaunchKernelGGL(scan_tiles_kernel, dim3((unsigned)ntiles), dim3(256), 0, st, counts, nx, off, sums);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(256), 0, st, sums, ntiles);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_add_kernel, dim3((unsigned)((nx + 255) / 256)), dim3(256), 0, st, off, nx, sums, n);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = scan_counts(counts, nx, off, sums, n, st)) != hipSuccess) return e;
     if (rec)
-        hipLaunchKernelGGL(place_kernel<true>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, mean ? 1 : 0, n,
+        hipLaunchKernelGGL(place_kernel<true>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+                           mean ? 1 : 0, n,
                            off, counts, key_t, row_t, w_t, rec);
     else
-        hipLaunchKernelGGL(place_kernel<false>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, mean ? 1 : 0,
+        hipLaunchKernelGGL(place_kernel<false>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+                           mean ? 1 : 0,
                            n, off, counts, key_t, row_t, w_t, rec);
     return hipGetLastError();
 }

@@ -146,10 +146,15 @@ hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t 
 // counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
 // With rec != nullptr (needs nx and the rows < 2^31) each edge is one 16-byte record
 // {int32 key, int32 row, float coefficient, 0} at rec[4 * slot] and key_t, row_t, w_t are unused.
+// bucket_scratch (transpose_scratch_bytes(n, nx) bytes, or nullptr) lets large inputs group the
+// edges by buckets of columns and sort each bucket in LDS (no global atomic per edge); counts,
+// off and sums are then unused.
 hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
-                            const int64_t *roff, bool mean, int64_t n, unsigned *counts, int64_t *off,
+                            const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                             int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                            hipStream_t st);
+                            char *bucket_scratch, hipStream_t st);
+// scratch of the bucketed transposition (0: the input takes the direct one)
+size_t transpose_scratch_bytes(int64_t n, int64_t nx);
 
 // grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean)
 hipError_t launch_seg_bwd_bcast(const float *gout, const int64_t *idx, const int64_t *off, int64_t n,

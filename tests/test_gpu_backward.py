@@ -141,3 +141,62 @@ def test_transpose_edges(weighted, op):
     rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op)
     tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, absolute=True)
     within(gx, rx, tx, f"transposed gather grad_X {op} weighted={weighted}")
+
+
+@pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True)])
+def test_transpose_edges_in_buckets(nx, hub):
+    """Inputs of over 2^20 edges group the edges by buckets of columns, then sort each bucket
+    by column in LDS (1,024 buckets of 512 columns for 300,000 columns, 4,096 of 2,048 for 5,000,000;
+    `hub` sends 40 % of the edges to one column, so one bucket holds most of them). Same
+    canonical comparison as above, sum and mean, and the gradient w.r.t. X through the
+    library's own transposition against the oracle."""
+    n, R, F = 1_300_000, 200_000, 4
+    rng = np.random.default_rng(43)
+    row = np.sort(rng.integers(0, R, n)).astype(np.int64)
+    col = rng.integers(0, nx, n).astype(np.int64)
+    if hub:
+        col[rng.random(n) < 0.4] = 12345
+    w = rng.random(n, dtype=np.float32)
+    for op in ("sum", "mean"):
+        say(f"bucketed transpose nx={nx} hub={hub} {op}")
+        sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, op))
+        assert np.all(np.diff(sc) >= 0)
+        coef = w.copy()
+        if op == "mean":
+            deg = np.bincount(row, minlength=R).astype(np.float32)
+            coef = (coef / deg[row]).astype(np.float32)
+        want = np.lexsort((coef.view(np.uint32), row, col))
+        got = np.lexsort((cf.view(np.uint32), rt, sc))
+        assert np.array_equal(sc[got], col[want]) and np.array_equal(rt[got], row[want])
+        assert np.array_equal(cf[got].view(np.uint32), coef[want].view(np.uint32))
+    X = rng.standard_normal((nx, F)).astype(np.float32)
+    g = rng.standard_normal((R, F)).astype(np.float32)
+    for op in ("sum", "mean"):
+        gx, _ = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op, need_weight=False)
+        rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op)
+        tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, absolute=True)
+        within(gx.cpu().numpy(), rx, tx, f"bucketed grad_X nx={nx} hub={hub} {op}")
+
+
+@pytest.mark.parametrize("n", [30_000, 1_300_000])
+def test_transpose_mean_with_rows_out_of_range(n):
+    """Row ids outside [0, num_rows) break the precondition: their values are unspecified,
+    but the mean coefficient must not read row starts out of bounds (the edges' rows are
+    checked before the division). The edges with rows in range still carry weight / the
+    in-range edge count of their row. Direct placement (30,000 edges) and buckets (1.3 M)."""
+    R, nx = 5000, 40_000
+    rng = np.random.default_rng(44)
+    row = np.sort(rng.integers(-50, R + 50, n)).astype(np.int64)
+    col = rng.integers(0, nx, n).astype(np.int64)
+    w = rng.random(n, dtype=np.float32)
+    say(f"transpose mean, rows out of range, n={n}")
+    sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, "mean"))
+    assert np.array_equal(sc, np.sort(col))
+    ok = (row >= 0) & (row < R)
+    deg = np.bincount(row[ok], minlength=R).astype(np.float32)
+    coef = (w[ok] / deg[row[ok]]).astype(np.float32)
+    keep = (rt >= 0) & (rt < R)
+    want = np.lexsort((coef.view(np.uint32), row[ok], col[ok]))
+    got = np.lexsort((cf[keep].view(np.uint32), rt[keep], sc[keep]))
+    assert np.array_equal(rt[keep][got], row[ok][want]) and np.array_equal(sc[keep][got], col[ok][want])
+    assert np.array_equal(cf[keep][got].view(np.uint32), coef[want].view(np.uint32))
