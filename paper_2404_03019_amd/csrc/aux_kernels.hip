@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void gap_fill_i64_kernel(int64_t *arr, int64_t
         const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], len), v = r[2];
         for (int64_t t = lo + threadIdx.x; t < hi; t += 256) arr[t] = v;
     }
-    gap_done(g, gridDim.x);
+    gap_done(g, blockIdx.x, gridDim.x, cnt);
 }
 
 __global__ __launch_bounds__(256) void len_stats_kernel(const int64_t *off, int64_t S,

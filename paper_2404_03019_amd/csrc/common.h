@@ -186,14 +186,19 @@ __device__ __forceinline__ unsigned gap_count(const GapList &g) {
     return s_cnt;
 }
 
-// A fill block is done: the last of the pass's `nblk` blocks empties the list
-// (every block read the count before taking its ticket).
-__device__ __forceinline__ void gap_done(const GapList &g, int64_t nblk) {
+// A fill block is done. Only the blocks that read records (blk < cnt: the
+// first min(cnt, nblk) of the pass) take a ticket, and the last of them empties
+// the list; each read the count before taking its ticket, so before the reset.
+// A block that reads the count after the reset sees 0, and is one with no
+// record under the true count either. An empty list costs no atomic.
+__device__ __forceinline__ void gap_done(const GapList &g, int64_t blk, int64_t nblk, unsigned cnt) {
+    if (blk >= (int64_t)cnt) return;
+    const int64_t parts = min((int64_t)cnt, nblk);
     __syncthreads();
     if (threadIdx.x == 0) {
         __threadfence();
         const unsigned t = atomicAdd(g.ticket, 1u);
-        if ((int64_t)t == nblk - 1) {
+        if ((int64_t)t == parts - 1) {
             atomicExch(g.count, 0u);
             atomicExch(g.ticket, 0u);
         }
@@ -226,7 +231,7 @@ __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_
             for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
         }
     }
-    gap_done(g, nblk);
+    gap_done(g, blk, nblk, cnt);
 }
 
 // DPP lane moves (GFX9 encodings): row_shr:S shifts within each 16-lane row;
