@@ -105,7 +105,7 @@ typedef struct {
     int32_t lanes;  /* lanes sharing one row: 1, 2, 4, 8, 16, 32 or 64 */
     int32_t rows;   /* EP: consecutive rows per row group (1..4096) */
     int32_t groups; /* SP: row groups of one wave that cooperate on one segment (1..64/lanes) */
-    int32_t flags;  /* 0, or one of the GEOT_FLAG_* load policies below */
+    int32_t flags;  /* 0, or GEOT_FLAG_* bits below: one load policy, and the tile order */
 } geot_kernel_choice_t;
 
 /* Load policy of the streamed rows (element-parallel family, segment reduction).
@@ -117,6 +117,13 @@ typedef struct {
  * reports NT_LOADS when it loads non-temporally. */
 #define GEOT_FLAG_NT_LOADS 1
 #define GEOT_FLAG_CACHED_LOADS 2
+/* Block order of the element-parallel family when F spans several column tiles:
+ * TILE_MAJOR runs every chunk of rows for tile 0, then tile 1, and so on, so the
+ * blocks in flight read one slab of columns (for the gather form, a slab of X,
+ * which caches better) at the price of reading the ids once per tile. Without it
+ * the tiles of one chunk are adjacent blocks. Ignored with one tile; may be
+ * combined with either load policy. */
+#define GEOT_FLAG_TILE_MAJOR 4
 
 /* Segment-length statistics of a sorted index (all lengths over
  * [0, num_segments), empties included). */

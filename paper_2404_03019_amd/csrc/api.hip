@@ -218,7 +218,8 @@ struct Problem {
 
 struct Resolved {
     int family, V, NT, L, K, groups, ntiles;
-    int nt_rows;  // EP rows mode: non-temporal row loads
+    int nt_rows;     // EP rows mode: non-temporal row loads
+    int tile_major;  // EP level 0: column tiles in sequence (blocks of one tile together)
 };
 
 int max_nt(int V) { return V == 4 ? 1 : (V == 2 ? 2 : 4); }
@@ -272,8 +273,9 @@ int widest_vec(const Problem &p) {
 
 geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r,
                       bool from_selector = false) {
-    const int known = GEOT_FLAG_NT_LOADS | GEOT_FLAG_CACHED_LOADS;
-    if ((c.flags & ~known) != 0 || (c.flags & known) == known)
+    const int loads = GEOT_FLAG_NT_LOADS | GEOT_FLAG_CACHED_LOADS;
+    const int known = loads | GEOT_FLAG_TILE_MAJOR;
+    if ((c.flags & ~known) != 0 || (c.flags & loads) == loads)
         return fail(GEOT_ERROR_UNSUPPORTED, "choice.flags: unknown bit, or both load policies");
     r->family = c.family == GEOT_FAMILY_AUTO ? GEOT_FAMILY_EP : c.family;
     if (r->family != GEOT_FAMILY_EP && r->family != GEOT_FAMILY_SP)
@@ -322,6 +324,7 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     r->nt_rows = (c.flags & GEOT_FLAG_NT_LOADS) ? 1
                  : (c.flags & GEOT_FLAG_CACHED_LOADS) ? 0
                  : (nt_ok && p.F * (int64_t)p.esize() >= 128 ? 1 : 0);
+    r->tile_major = (c.flags & GEOT_FLAG_TILE_MAJOR) != 0 && r->family == GEOT_FAMILY_EP && ntiles > 1;
     r->K = rows == 0 ? auto_rows(p.nnz, L, V, NT, r->ntiles, (int64_t)p.esize()) : rows;
     const int GW = 64 / L;
     geot_kernel_choice_t cc = c;
@@ -346,7 +349,7 @@ geot_kernel_choice_t to_choice(const Resolved &r) {
     c.lanes = r.L;
     c.rows = r.K;
     c.groups = r.groups;
-    c.flags = r.nt_rows ? GEOT_FLAG_NT_LOADS : 0;
+    c.flags = (r.nt_rows ? GEOT_FLAG_NT_LOADS : 0) | (r.tile_major ? GEOT_FLAG_TILE_MAJOR : 0);
     return c;
 }
 
@@ -358,7 +361,7 @@ void select_raw(int64_t nnz, int64_t S, int64_t F, geot_op_t op, int gather,
         cv = stats->var_len > 0 ? std::sqrt(stats->var_len) / mean : 0.0;
         max_rel = (double)stats->max_len / mean;
     }
-    int32_t o[5];
+    int32_t o[6];
     tree_select((double)nnz, (double)S, (double)F, (int)op, gather, stats != nullptr, cv, max_rel, o);
     // One segment-parallel team owns a whole segment: never used where the longest segment
     // exceeds 256x the mean (the range the trees were fitted on leaves it unmeasured there)
@@ -370,6 +373,15 @@ void select_raw(int64_t nnz, int64_t S, int64_t F, geot_op_t op, int gather,
     c->rows = o[3];
     c->groups = o[4];
     c->flags = 0;
+    if (o[0] == GEOT_FAMILY_EP && o[5] > 1 && F % 4 == 0) {
+        // o[5] column tiles run one after another: the lanes of the 4-wide shape of F, divided
+        // (leaves are fit on fp32 shapes; 16-bit storage halves them again in resolve)
+        const int64_t vecs = F / 4;
+        int L = 1;
+        while (L < vecs && L < 64) L <<= 1;
+        c->lanes = std::max(1, L / o[5]);
+        c->flags = GEOT_FLAG_TILE_MAJOR;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -500,6 +512,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.idx32 = p.idx32;
             a.nt_rows = r.nt_rows;
             a.meta_stride = p.meta_stride;
+            a.tile_major = r.tile_major;
         } else {
             a.src = (const float *)(base + off_v[l]);
             a.ld_src = ld_p;

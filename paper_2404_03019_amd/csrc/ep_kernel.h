@@ -86,8 +86,18 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
             return;
         }
     }
-    const int64_t chunk = blockIdx.x / a.ntiles;
-    const int tile = (int)(blockIdx.x - chunk * a.ntiles);
+    // tile-major: the blocks in flight share one column tile, so a gather reads one
+    // slab of X at a time (the metadata is read once per tile)
+    int64_t chunk;
+    int tile;
+    if (a.tile_major) {
+        const int64_t nch = ((int64_t)gridDim.x - (MODE == SRC_PIECES ? (int64_t)a.gap_blocks : 0)) / a.ntiles;
+        tile = (int)(blockIdx.x / nch);
+        chunk = blockIdx.x - (int64_t)tile * nch;
+    } else {
+        chunk = blockIdx.x / a.ntiles;
+        tile = (int)(blockIdx.x - chunk * a.ntiles);
+    }
     const int64_t bsize = (int64_t)G * a.K;
     const int64_t bstart = chunk * bsize;
     const int64_t bend = min(bstart + bsize, a.n);

@@ -72,6 +72,8 @@ struct EpArgs {
     int32_t meta_stride;    // gather mode: idx, col and w of edge e at [e * meta_stride] (0 or 1: arrays)
     int32_t gap_blocks;     // SRC_PIECES, final level: this many extra blocks fill the gap list `gaps`
                             // (written by level 0, which has finished), in tiles of the level's width
+    int32_t tile_major;     // block b takes column tile b / chunks and chunk b % chunks (else the
+                            // ntiles tiles of a chunk are adjacent blocks)
 };
 
 // Dispatches on (elem, idx32) to the translation unit holding those instantiations.

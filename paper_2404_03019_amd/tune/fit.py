@@ -156,6 +156,7 @@ def predict_cand(tree, row, with_family, e):
 
 
 EP_ROWS = (4, 8, 16, 32, 64, 128, 256)
+TILE_ROWS = (16, 32, 64, 128)  # row runs timed with the columns in 2 or 4 tiles, one after another
 MISSING_COST = math.log(50.0)  # a candidate that was not measured (or too slow to finish)
 NAMED_WEIGHT = 16.0            # the named benchmark workloads count this many times
 
@@ -169,11 +170,23 @@ def lanes_for(F: int) -> int:
     return L
 
 
-def candidate_space(stats: bool):
-    c = [(1, k, 1) for k in EP_ROWS]
+def candidate_space(stats: bool, kind: str | None = None):
+    """(family, rows, groups, tiles): tiles > 1 runs the element-parallel kernel over that many
+    column tiles in sequence (tile-major blocks; fused form only)."""
+    c = [(1, k, 1, 1) for k in EP_ROWS]
+    if kind != "segment":
+        c += [(1, k, 1, t) for t in (2, 4) for k in TILE_ROWS]
     if stats:
-        c += [(2, 0, g) for g in (1, 2, 4, 8, 16, 32, 64)]
+        c += [(2, 0, g, 1) for g in (1, 2, 4, 8, 16, 32, 64)]
     return c
+
+
+def cand_key(cand, F: int) -> str:
+    """The database key of a candidate for an input with F columns."""
+    fam, k, g, t = cand
+    if fam == 1:
+        return f"f1_r{k}_g0" + (f"_t{t}" if t > 1 else "")
+    return f"f2_r0_g{min(g, 64 // lanes_for(F))}"
 
 
 def cost_matrix(data, cands):
@@ -182,10 +195,8 @@ def cost_matrix(data, cands):
     C = np.full((len(data), len(cands)), MISSING_COST)
     for i, e in enumerate(data):
         tb, _ = best_of(e)
-        gw = 64 // lanes_for(e["instance"]["F"])
-        for j, (fam, k, g) in enumerate(cands):
-            key = f"f1_r{k}_g0" if fam == 1 else f"f2_r0_g{min(g, gw)}"
-            t = e["times"].get(key)
+        for j, cand in enumerate(cands):
+            t = e["times"].get(cand_key(cand, e["instance"]["F"]))
             if t is not None and t > 0 and tb > 0:
                 C[i, j] = min(MISSING_COST, math.log(t / tb))
         if 10000 <= e["instance"]["id"] < 20000:
@@ -245,8 +256,8 @@ def emit_cost_tree(tree, names, cands, indent):
     def rec(n, depth):
         pad = " " * (indent + 4 * depth)
         if "leaf" in n:
-            fam, k, g = cands[n["leaf"]]
-            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};")
+            fam, k, g, t = cands[n["leaf"]]
+            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};" + (f" out[5] = {t};" if t > 1 else ""))
             return
         lines.append(f"{pad}if ({names[n['feature']]} <= {n['threshold']:.9g}) {{")
         rec(n["left"], depth + 1)
@@ -265,18 +276,17 @@ class Fitted:
         self.data = data
         self.trees, self.single = {}, {}
         for stats in (False, True):
-            cands = candidate_space(stats)
             for kind in KINDS:
                 sub = [e for e in data if kind_of(e) == kind]
                 X = [feature_row(e, stats, kind) for e in sub]
-                self.trees[(kind, stats)] = CostTree().fit(X, cost_matrix(sub, cands))
+                self.trees[(kind, stats)] = CostTree().fit(X, cost_matrix(sub, candidate_space(stats, kind)))
             self.single[stats] = CostTree().fit([feature_row(e, stats) for e in data],
-                                                cost_matrix(data, cands))
+                                                cost_matrix(data, candidate_space(stats)))
 
     def choose(self, e, stats: bool):
-        """(family, rows, groups) the emitted selector gives input e."""
+        """(family, rows, groups, tiles) the emitted selector gives input e."""
         kind = kind_of(e)
-        return candidate_space(stats)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
+        return candidate_space(stats, kind)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
 
     def choose_as_library(self, e, stats: bool):
         """What geot_select returns: the tree's choice, except that the segment-parallel
@@ -311,11 +321,12 @@ def render(fitted: Fitted) -> str:
             f"// trees per operation, depth <= {MAX_DEPTH}. Each leaf is the candidate with the least",
             "// total log-slowdown over the inputs reaching it. out[0] family (1 element-parallel,",
             "// 2 segment-parallel), out[3] rows per row group, out[4] row groups per segment",
-            "// (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape.",
+            "// (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape; out[5] column",
+            "// tiles run one after another (1: the columns' own tiling, in adjacent blocks).",
             "// gather: 0 segment reduction, 1 fused form with edge weights, 2 without.",
             "#pragma once", "", "#include <cmath>", "#include <cstdint>", "", "namespace geot {", "",
             "static inline void tree_select(double nnz, double num_segments, double F, int op, int gather,",
-            "                               int has_stats, double cv, double max_rel, int32_t out[5]) {",
+            "                               int has_stats, double cv, double max_rel, int32_t out[6]) {",
             "    const double lnnz = std::log2(nnz > 1.0 ? nnz : 1.0);",
             "    const double lS = std::log2(num_segments > 1.0 ? num_segments : 1.0);",
             "    const double mean = num_segments > 0.0 ? nnz / num_segments : 0.0;",
@@ -324,22 +335,20 @@ def render(fitted: Fitted) -> str:
             "    const double weighted = gather == 1 ? 1.0 : 0.0;",
             "    const double lmaxrel = std::log2(max_rel > 1e-9 ? max_rel : 1e-9);",
             "    (void)lnnz; (void)lS; (void)F; (void)lmean; (void)opmax; (void)weighted; (void)cv; (void)lmaxrel;",
-            "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0;"]
+            "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0; out[5] = 1;"]
     for kind, cond, close in (("segment", "    if (gather == 0) {", None), ("gather", "    } else {", "    }")):
         body += [cond, "        if (!has_stats) {"]
-        body += emit_cost_tree(fitted.trees[(kind, False)], feature_names(False, kind), candidate_space(False), 12)
+        body += emit_cost_tree(fitted.trees[(kind, False)], feature_names(False, kind),
+                               candidate_space(False, kind), 12)
         body += ["        } else {"]
-        body += emit_cost_tree(fitted.trees[(kind, True)], feature_names(True, kind), candidate_space(True), 12)
+        body += emit_cost_tree(fitted.trees[(kind, True)], feature_names(True, kind), candidate_space(True, kind), 12)
         body += ["        }"]
     body += ["    }", "}", "", "}  // namespace geot", ""]
     return "\n".join(body)
 
 
 def _time_of(e, cand):
-    fam, k, g = cand
-    gw = 64 // lanes_for(e["instance"]["F"])
-    key = f"f1_r{k}_g0" if fam == 1 else f"f2_r0_g{min(g, gw)}"
-    return e["times"].get(key, math.nan)
+    return e["times"].get(cand_key(cand, e["instance"]["F"]), math.nan)
 
 
 def evaluate(fitted: Fitted):

@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 DISTS = ("fixed", "poisson", "uniform", "zipf", "lognormal_narrow", "lognormal_wide", "one_heavy")
 FS = (1, 2, 3, 4, 8, 16, 32, 64, 128, 256)
 EP_ROWS = (4, 8, 16, 32, 64, 128, 256)
+TILE_ROWS = (16, 32, 64, 128)  # row runs also timed over 2 and 4 column tiles in sequence (fused form)
 
 
 def draw_lengths(rng, dist: str, S: int, nnz: int) -> np.ndarray:
@@ -115,14 +116,21 @@ def named_instances():
     return out
 
 
-def candidates(F: int, allow_sp: bool):
+def lanes_for(F: int) -> int:
+    V = 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1)
+    vecs = -(-F // V)
+    L = 1
+    while L < vecs and L < 64:
+        L <<= 1
+    return L
+
+
+def candidates(F: int, allow_sp: bool, gather: bool = False):
     c = [dict(family=1, rows=0)] + [dict(family=1, rows=k) for k in EP_ROWS]
+    if gather and F >= 64 and F % 4 == 0:  # column tiles in sequence (tile-major blocks)
+        c += [dict(family=1, rows=k, lanes=lanes_for(F) // t, flags=4, tiles=t) for t in (2, 4) for k in TILE_ROWS]
     if allow_sp:
-        V = 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1)
-        vecs = -(-F // V)
-        L = 1
-        while L < vecs and L < 64:
-            L <<= 1
+        L = lanes_for(F)
         g = 1
         while g <= 64 // L:
             c.append(dict(family=2, groups=g))
@@ -131,7 +139,13 @@ def candidates(F: int, allow_sp: bool):
 
 
 def ckey(c: dict) -> str:
-    return f"f{c['family']}_r{c.get('rows', 0)}_g{c.get('groups', 0)}"
+    t = c.get("tiles", 1)
+    return f"f{c['family']}_r{c.get('rows', 0)}_g{c.get('groups', 0)}" + (f"_t{t}" if t > 1 else "")
+
+
+def as_choice(c: dict) -> dict:
+    """The library's choice for candidate c (its `tiles` is a database label only)."""
+    return {k: v for k, v in c.items() if k != "tiles"}
 
 
 def main():
@@ -167,9 +181,11 @@ def main():
             if time.time() - t_start > args.budget_s:
                 print("budget reached", flush=True)
                 break
-            if (inst["id"], inst["seed"]) in done_inst:
-                continue
             weighted = inst.get("weighted", inst["gather"])
+            if (inst["id"], inst["seed"]) in done_inst and all(
+                    (inst["id"], inst["seed"], ckey(c)) in done
+                    for c in candidates(inst["F"], False, bool(inst["gather"]))):
+                continue  # every candidate but possibly SP done (SP is skipped on heavy tails)
             if 10000 <= inst["id"] < 20000:  # a named workload: lengths from its recipe
                 from workloads import config_lengths
 
@@ -190,14 +206,14 @@ def main():
                 nbytes = nnz * (16 + 4 * weighted + 4 * F) + S * F * 4
 
                 def call(c):
-                    geot.gather_scatter(X, col, w, idx, S, inst["op"], out=out, choice=c)
+                    geot.gather_scatter(X, col, w, idx, S, inst["op"], out=out, choice=as_choice(c))
             else:
                 src = torch.randn(nnz, F, device=dev, generator=gen)
                 out = torch.empty(S, F, device=dev)
                 nbytes = nnz * (8 + 4 * F) + S * F * 4
 
                 def call(c):
-                    geot.segment_reduce(src, idx, S, inst["op"], out=out, choice=c)
+                    geot.segment_reduce(src, idx, S, inst["op"], out=out, choice=as_choice(c))
             st = geot.index_stats(idx, S)
             mean = nnz / S
             feats = dict(nnz=nnz, S=S, F=F, mean=mean, op=inst["op"], gather=inst["gather"], weighted=weighted,
@@ -205,7 +221,7 @@ def main():
                          max_rel=st["max_len"] / mean if mean > 0 else 0.0)
             best = math.inf
             # a segment-parallel team owns a whole segment: hopeless on very heavy tails
-            for c in candidates(F, feats["max_rel"] <= 256.0):
+            for c in candidates(F, feats["max_rel"] <= 256.0, bool(inst["gather"])):
                 key = (inst["id"], inst["seed"], ckey(c))
                 if key in done:
                     continue

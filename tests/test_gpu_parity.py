@@ -95,6 +95,7 @@ RANDOM_CHOICES = [
     dict(family="ep", lanes=64, rows=1),
     dict(family="ep", lanes=2, vec=1, rows=7),
     dict(family="ep", rows=33),
+    dict(family="ep", lanes=4, rows=9, flags=4),   # 16-column tiles, one tile after another
     dict(family="sp"),
     dict(family="sp", lanes=16, groups=2),
 ]
@@ -346,3 +347,41 @@ def test_non_temporal_row_loads_match_ordinary_loads(F):
     if a is not None:
         b = geot.segment_reduce(s16, i, 700, "sum", choice=dict(family="ep", flags=2))
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("F", [33, 64, 128, 256, 300])
+def test_tile_major_order_matches_adjacent_tiles(F):
+    """Tile-major block order changes which blocks run together, not what a block reduces:
+    outputs are bitwise identical to the adjacent order, for the gather and rows modes, with
+    several partial levels (small row runs) and long runs of empty segments."""
+    R, nx = 3000, 2500
+    p = random_gather_problem(950 + F, 30000, R, nx, F, "zipf", "normal", True, 0.3)
+    X, col, w, row = up(p["X"]), up(p["col"]), up(p["weight"]), up(p["index"])
+    q = random_problem(960 + F, 30000, 5000, F, "lognormal", "normal", 0.4)
+    s, i = up(q["src"]), up(q["index"])
+    for op in OPS:
+        gref, gterms = oracle_gather(p["X"], p["col"], p["weight"], p["index"], R, op)
+        sref, sterms = oracle_segment(q["src"], q["index"], 5000, op)
+        for base in (dict(family="ep", lanes=16, rows=64), dict(family="ep", lanes=8, rows=3),
+                     dict(family="ep", lanes=2, vec=2, rows=17)):
+            say(f"tile-major F={F} {op} {base}")
+            a = geot.gather_scatter(X, col, w, row, R, op, choice=base)
+            b = geot.gather_scatter(X, col, w, row, R, op, choice=dict(base, flags=4))
+            tiled = geot.last_choice()["flags"] & 4
+            V = min(base.get("vec", 4), 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1))
+            assert bool(tiled) == (F > base["lanes"] * V), geot.last_choice()   # reported when tiles > 1
+            assert torch.equal(a, b), f"gather F={F} {op} {base}"
+            compare(b.cpu().numpy(), gref, op, gterms, f"tile-major gather F={F} {op} {base}")
+            a = geot.segment_reduce(s, i, 5000, op, choice=base)
+            b = geot.segment_reduce(s, i, 5000, op, choice=dict(base, flags=4))
+            assert torch.equal(a, b), f"rows F={F} {op} {base}"
+            compare(b.cpu().numpy(), sref, op, sterms, f"tile-major rows F={F} {op} {base}")
+    # 16-bit X with int32 ids: 8-wide loads, tiles of 8 * lanes columns
+    Xb = up(p["X"]).to(torch.bfloat16)
+    c32, r32 = col.to(torch.int32), row.to(torch.int32)
+    base = dict(family="ep", lanes=4, vec=8, rows=32)
+    if F % 8 == 0:
+        a = geot.gather_scatter(Xb, c32, w, r32, R, "sum", choice=base)
+        b = geot.gather_scatter(Xb, c32, w, r32, R, "sum", choice=dict(base, flags=4))
+        assert geot.last_choice()["flags"] & 4
+        assert torch.equal(a, b), f"bf16 gather F={F}"

@@ -23,9 +23,9 @@ DRIVER = r"""
 int main() {
     double nnz, S, F, cv, mx; int op, gather, has;
     while (std::scanf("%lf %lf %lf %d %d %d %lf %lf", &nnz, &S, &F, &op, &gather, &has, &cv, &mx) == 8) {
-        int32_t out[5];
+        int32_t out[6];
         geot::tree_select(nnz, S, F, op, gather, has, cv, mx, out);
-        std::printf("%d %d %d\n", out[0], out[3], out[4]);
+        std::printf("%d %d %d %d\n", out[0], out[3], out[4], out[5]);
     }
     return 0;
 }
@@ -72,9 +72,14 @@ def test_library_select_follows_the_tree(fitted):
         [e for e in fitted.data if e["features"]["gather"]][:40]
     for e in picks:
         f = e["features"]
-        fam, k, g = fitted.choose(e, False)
+        fam, k, g, t = fitted.choose(e, False)
         c = geot.select(f["nnz"], f["S"], f["F"], f["op"], bool(f["gather"]), weighted=bool(fit.weighted_of(e)))
         assert c["family"] == fam and c["rows"] == k, (f, c, (fam, k))
+        # column tiles in sequence: lanes of the 4-wide shape divided by the tiles, tile-major order
+        tiled = t > 1 and f["F"] % 4 == 0
+        assert bool(c["flags"] & 4) == (tiled and f["F"] > 4 * fit.lanes_for(f["F"]) // t), (f, c, t)
+        if tiled:
+            assert c["lanes"] == max(1, fit.lanes_for(f["F"]) // t), (f, c, t)
 
 
 def test_selector_beats_the_hand_rule_and_the_paper_recipe(fitted):
