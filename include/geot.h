@@ -306,7 +306,9 @@ geot_status_t geot_select(int64_t nnz, int64_t num_segments, int64_t F, geot_op_
 /* Segment-length statistics of a sorted index (one pass over the index on
  * the device). Synchronizes `stream`; writes the host struct *host_out.
  * Precondition as for the reductions; results for an unsorted index are
- * unspecified.                                                              */
+ * unspecified. Returns GEOT_ERROR_INVALID_VALUE for a NULL host_out, nnz < 0,
+ * num_segments <= 0 or >= 2^31 (as the reductions), or a NULL index with
+ * nnz > 0.                                                                  */
 geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t num_segments,
                                geot_index_stats_t *host_out, void *stream);
 

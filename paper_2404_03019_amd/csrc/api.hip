@@ -962,6 +962,7 @@ geot_status_t geot_index_stats(const int64_t *sorted_index, int64_t nnz, int64_t
     t_detail.clear();
     if (!host_out) return fail(GEOT_ERROR_INVALID_VALUE, "host_out is NULL");
     if (nnz < 0 || num_segments <= 0) return fail(GEOT_ERROR_INVALID_VALUE, "need nnz >= 0 and num_segments > 0");
+    if (num_segments > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments must be < 2^31");
     if (nnz > 0 && !sorted_index) return fail(GEOT_ERROR_INVALID_VALUE, "index is NULL");
     geot_index_stats_t o;
     memset(&o, 0, sizeof(o));

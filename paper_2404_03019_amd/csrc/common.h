@@ -152,26 +152,29 @@ __device__ __forceinline__ int32_t shfl_up_cnt(int32_t v, int delta) { return sh
 __device__ __forceinline__ int64_t shfl_up_cnt(int64_t v, int delta) { return shfl_up_i64(v, delta); }
 
 // Appends the run of segments [lo, hi) (value carried along) to a gap list,
-// cut into records of kGapChunk segments, or into kGapMaxRecs longer ones for
-// a run longer than that many chunks (so no run needs more than kGapMaxRecs
-// slots). `lanes` lanes starting at lane `lead` (all in the same state) call it
-// together; the lead lane takes the slots and the lanes share the writes.
-// Returns false when the list is full: the caller then writes the run itself
-// (the slots it took hold empty records).
+// cut into records of 2^kGapChunkLog2 segments, or of the least power of two
+// that cuts it into at most 2^kGapMaxRecsLog2 records (so no run needs more
+// slots than that). Runs are shorter than 2^31 (num_segments < 2^31) and longer
+// than kGapRun, so the cut takes 32-bit shifts, no division (which would hold
+// registers in the loops this is inlined into). `lanes` lanes starting at lane
+// `lead` (all in the same state) call it together; the lead lane takes the
+// slots and the lanes share the writes. Returns false when the list is full:
+// the caller then writes the run itself (the slots it took hold empty records).
 __device__ __forceinline__ bool gap_push(const GapList &g, int64_t lo, int64_t hi, int64_t value,
                                          int lead, int lane_in, int lanes) {
-    const int64_t chunk = max(kGapChunk, (hi - lo + kGapMaxRecs - 1) / kGapMaxRecs);
-    const int64_t nrec = (hi - lo + chunk - 1) / chunk;
+    const unsigned len = (unsigned)(hi - lo);
+    const int sh = max(kGapChunkLog2, (32 - __clz((int)(len - 1u))) - kGapMaxRecsLog2);  // ceil(log2 len) - 6
+    const unsigned nrec = (unsigned)(((uint64_t)len + ((uint64_t)1 << sh) - 1u) >> sh);
     unsigned base = 0;
-    if (lane_in == 0) base = atomicAdd(g.count, (unsigned)nrec);
+    if (lane_in == 0) base = atomicAdd(g.count, nrec);
     if (lanes > 1) base = (unsigned)__shfl((int)base, lead, 64);
-    const bool fits = (int64_t)base + nrec <= (int64_t)kGapCap;
-    const int64_t end = fits ? nrec : ((int64_t)kGapCap > (int64_t)base ? (int64_t)kGapCap - base : 0);
-    for (int64_t q = lane_in; q < end; q += lanes) {
+    const bool fits = (uint64_t)base + nrec <= (uint64_t)kGapCap;
+    const unsigned end = fits ? nrec : (kGapCap > base ? kGapCap - base : 0u);
+    for (unsigned q = (unsigned)lane_in; q < end; q += (unsigned)lanes) {
         int64_t *r = g.rec + 3 * ((int64_t)base + q);
-        const int64_t a = fits ? lo + q * chunk : 0;
+        const int64_t a = fits ? lo + ((int64_t)q << sh) : 0;
         r[0] = a;
-        r[1] = fits ? min(hi, a + chunk) : 0;
+        r[1] = fits ? min(hi, a + ((int64_t)1 << sh)) : 0;
         r[2] = value;
     }
     return fits;

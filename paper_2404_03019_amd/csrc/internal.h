@@ -32,8 +32,8 @@ enum ElemType : int { ELEM_F32 = 0, ELEM_BF16 = 1, ELEM_F16 = 2 };
 // call is running (no memset, no host-side state: calls captured in a HIP
 // graph replay correctly).
 constexpr int kGapRun = 32;
-constexpr int64_t kGapChunk = 8192;     // segments per record (longer when a run would need more records)
-constexpr int64_t kGapMaxRecs = 64;     // records one run takes at most
+constexpr int kGapChunkLog2 = 13;       // records of 2^13 = 8192 segments, or of the least power of two
+constexpr int kGapMaxRecsLog2 = 6;      // that cuts the run into at most 2^6 = 64 records
 constexpr unsigned kGapCap = 65536;     // records in the list (24 bytes each)
 
 struct GapList {

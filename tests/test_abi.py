@@ -68,6 +68,8 @@ def _detail():
 def test_invalid_arguments_are_rejected_on_the_host():
     out = FAKE + (1 << 30)
     assert _sr(FAKE, FAKE + (1 << 28), 10, 4, 3, 7, out) == INVALID and "op" in _detail()
+    st = geot.geot.IndexStats()
+    assert lib().geot_index_stats(FAKE, 10, 1 << 31, ctypes.byref(st), None) == INVALID and "2^31" in _detail()
     assert _sr(FAKE, FAKE + (1 << 28), -1, 4, 3, 0, out) == INVALID
     assert _sr(FAKE, FAKE + (1 << 28), 10, -4, 3, 0, out) == INVALID
     assert _sr(FAKE, FAKE + (1 << 28), 10, 4, -3, 0, out) == INVALID
