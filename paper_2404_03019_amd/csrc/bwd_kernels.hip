@@ -59,6 +59,17 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
         const int64_t i = m.row(q);
         seg[q] = i < n ? idx[i] : -1;
     }
+    // mean: every pass's segment starts load together, branchless (a segment out of range
+    // reads segment 0's), before the first gradient row
+    int64_t o0[kPasses], o1[kPasses];
+    if (MEAN) {
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t s = (uint64_t)seg[q] < (uint64_t)S ? seg[q] : 0;
+            o0[q] = off[s];
+            o1[q] = off[s + 1];
+        }
+    }
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
@@ -66,7 +77,7 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
             const int64_t s = seg[q];
             const bool ok = (uint64_t)s < (uint64_t)S;
             float inv = 1.0f;
-            if (MEAN && ok) inv = 1.0f / (float)(off[s + 1] - off[s]);
+            if (MEAN && ok) inv = 1.0f / (float)(o1[q] - o0[q]);
             for (int j = m.j0; j < nvec; j += m.tpr) {
                 float x[V];
                 if (ok) {
@@ -192,9 +203,10 @@ __global__ __launch_bounds__(256) void gs_bwd_x_kernel(const int64_t *col, int64
     }
 }
 
-// fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max).
-// Every thread runs all passes (the group reduction is uniform); the edges'
-// ids load first, then both operand rows of every pass, then the products.
+// fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
+// mean divides afterwards, in scale_by_count_kernel). Every thread runs all passes (the group
+// reduction is uniform); the edges' ids load first, then both operand rows of every pass, then
+// the products.
 template <int V, int OP>
 __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__ X, int64_t nx,
                                                        const int64_t *__restrict__ col,
@@ -216,6 +228,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
 #pragma unroll
     for (int q = 0; q < kPasses; ++q)
         ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx;
+    static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
     float acc[kPasses];
     if (nvec <= m.tpr) {  // one vector per thread and row: all loads of the block's passes in flight together
         float g[kPasses][V], x[kPasses][V];
@@ -265,10 +278,36 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
         for (int d = m.tpr / 2; d >= 1; d >>= 1) a += __shfl_xor(a, d, 64);
         const int64_t e = m.row(q);
         if (e < n && m.j0 == 0) {
-            float v = ok[q] ? a : 0.0f;
-            if (ok[q] && OP == GEOT_BWD_MEAN) v = v / (float)(off[rr[q] + 1] - off[rr[q]]);
-            gw[e] = v;
+            gw[e] = ok[q] ? a : 0.0f;
         }
+    }
+}
+
+// mean: grad_w[e] /= the edge count of row[e]. A pass of its own: inside the dot-product
+// kernel the row starts either waited after the reduction (one more memory latency per
+// block) or held registers through it (5 waves per SIMD instead of 7); both cost C4 1.5 ms,
+// this pass about 0.2. Rows of all passes load first, then their starts and the values.
+__global__ __launch_bounds__(256) void scale_by_count_kernel(float *__restrict__ gw, const int64_t *__restrict__ row,
+                                                             const int64_t *__restrict__ off, int64_t n, int64_t R) {
+    int64_t r[kPasses];
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
+        r[q] = e < n ? row[e] : -1;
+    }
+    float v[kPasses], c[kPasses];
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
+        const bool ok = (uint64_t)r[q] < (uint64_t)R;
+        const int64_t rs = ok ? r[q] : 0;
+        c[q] = (float)(off[rs + 1] - off[rs]);
+        v[q] = e < n ? gw[e] : 0.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
+        if (e < n && (uint64_t)r[q] < (uint64_t)R) gw[e] = v[q] / c[q];
     }
 }
 
@@ -766,17 +805,21 @@ hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const f
         if (e != hipSuccess) return e;
     }
     if (gw) {
-        if (op == GEOT_BWD_SUM)
+        if (op == GEOT_BWD_SUM || op == GEOT_BWD_MEAN)
             GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st,
                                             X, nx, col, row, off, arg, gout, n, R, F, gw));
-        else if (op == GEOT_BWD_MEAN)
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_MEAN>), dim3(g), dim3(256), 0,
-                                            st, X, nx, col, row, off, arg, gout, n, R, F, gw));
         else
             GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st,
                                             X, nx, col, row, off, arg, gout, n, R, F, gw));
         e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if (op == GEOT_BWD_MEAN) {
+            const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
+            if (sb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+            hipLaunchKernelGGL(scale_by_count_kernel, dim3((unsigned)sb), dim3(256), 0, st, gw, row, off, n, R);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
     }
     return hipSuccess;
 }

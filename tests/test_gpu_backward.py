@@ -143,11 +143,13 @@ def test_transpose_edges(weighted, op):
     within(gx, rx, tx, f"transposed gather grad_X {op} weighted={weighted}")
 
 
-@pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True)])
+@pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True), (200, False),
+                                    (1 << 23, False)])
 def test_transpose_edges_in_buckets(nx, hub):
     """Inputs of over 2^20 edges group the edges by buckets of columns, then sort each bucket
     by column in LDS (1,024 buckets of 512 columns for 300,000 columns, 4,096 of 2,048 for 5,000,000;
-    `hub` sends 40 % of the edges to one column, so one bucket holds most of them). Same
+    `hub` sends 40 % of the edges to one column, so one bucket holds most of them; 200 columns
+    give 256 buckets of one column; 2^23 columns is the largest the buckets take). Same
     canonical comparison as above, sum and mean, and the gradient w.r.t. X through the
     library's own transposition against the oracle."""
     n, R, F = 1_300_000, 200_000, 4
