@@ -96,18 +96,47 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
     }
 }
 
-// arg[s, f] = min row i of segment s with src[i, f] == out[s, f]
+// arg[s, f] = min row i of segment s with src[i, f] == out[s, f]. The ids of all passes
+// load first, then every pass's row and output vector, then the compares (one memory
+// latency per step, not per pass).
 template <int V>
-__global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *src, const int64_t *idx,
-                                                              const float *out, int64_t n, int64_t S,
+__global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__restrict__ src,
+                                                              const int64_t *__restrict__ idx,
+                                                              const float *__restrict__ out, int64_t n, int64_t S,
                                                               int64_t F, unsigned long long *arg) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
+    int64_t seg[kPasses];
+#pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
-        if (i >= n) break;
-        const int64_t s = idx[i];
-        if ((uint64_t)s >= (uint64_t)S) continue;
+        seg[q] = i < n ? idx[i] : -1;
+    }
+    if (nvec <= m.tpr) {  // one vector per thread and row
+        float x[kPasses][V], o[kPasses][V];
+        bool ok[kPasses];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            ok[q] = m.row(q) < n && (uint64_t)seg[q] < (uint64_t)S && m.j0 < nvec;
+            if (ok[q]) {
+                load_vec<V>(src + m.row(q) * F + (int64_t)m.j0 * V, x[q]);
+                load_vec<V>(out + seg[q] * F + (int64_t)m.j0 * V, o[q]);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if (!ok[q]) continue;
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                if (x[q][k] == o[q][k])
+                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+        }
+        return;
+    }
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t i = m.row(q);
+        const int64_t s = seg[q];
+        if (i >= n || (uint64_t)s >= (uint64_t)S) continue;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V], o[V];
             load_vec<V>(src + i * F + (int64_t)j * V, x);
@@ -119,17 +148,64 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *src, 
     }
 }
 
-// grad_src[i, f] = grad_out[s, f] where i is the recipient of (s, f), else 0
+// grad_src[i, f] = grad_out[s, f] where i is the recipient of (s, f), else 0; ids first,
+// then every pass's gradient and recipient vectors, then the stores
 template <int V>
-__global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *gout, const int64_t *idx,
-                                                                const unsigned long long *arg, int64_t n,
-                                                                int64_t S, int64_t F, float *gsrc) {
+__global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__restrict__ gout,
+                                                                const int64_t *__restrict__ idx,
+                                                                const unsigned long long *__restrict__ arg,
+                                                                int64_t n, int64_t S, int64_t F,
+                                                                float *__restrict__ gsrc) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
+    int64_t seg[kPasses];
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t i = m.row(q);
+        seg[q] = i < n ? idx[i] : -1;
+    }
+    if (nvec <= m.tpr) {
+        float x[kPasses][V];
+        unsigned long long w[kPasses][V];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const bool ok = (uint64_t)seg[q] < (uint64_t)S && m.j0 < nvec;
+            if (ok) {
+                load_vec<V>(gout + seg[q] * F + (int64_t)m.j0 * V, x[q]);
+                const unsigned long long *a = arg + seg[q] * F + (int64_t)m.j0 * V;
+                if constexpr (V >= 2) {  // 16-byte loads: V * 8 bytes at a multiple of V * 8
+#pragma unroll
+                    for (int k = 0; k < V; k += 2) {
+                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
+                        w[q][k] = t.x;
+                        w[q][k + 1] = t.y;
+                    }
+                } else {
+                    w[q][0] = a[0];
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    x[q][k] = 0.0f;
+                    w[q][k] = ~0ull;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t i = m.row(q);
+            if (i >= n || m.j0 >= nvec) continue;
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                if (w[q][k] != (unsigned long long)i) x[q][k] = 0.0f;
+            store_vec<V>(gsrc + i * F + (int64_t)m.j0 * V, x[q]);
+        }
+        return;
+    }
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
         if (i >= n) break;
-        const int64_t s = idx[i];
+        const int64_t s = seg[q];
         const bool ok = (uint64_t)s < (uint64_t)S;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V];
