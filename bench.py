@@ -259,6 +259,14 @@ def suite(reps: int):
     b = n4 * 20 + n4 * 512 + R4 * 512
     ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_x=False), b)
     emit("c4_spmm backward grad_weight", ms, b, cold)
+    # max: recipients (one gathered X row per edge + out), then grad_X (the recipients' grad_out
+    # rows, one atomic add each) and grad_w (one gathered X row per edge, masked): bytes of the
+    # three passes' streams, atomics not counted
+    out4 = geot.gather_scatter(X, col, w, row, R4, "max")
+    b = 3 * (n4 * 20 + n4 * 512 + R4 * 512)
+    ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "max", out=out4), b)
+    emit("c4_spmm backward max (grad_X and grad_weight)", ms, b, cold)
+    del out4
     # a static graph keeps its column-sorted edge list: the gradient w.r.t. X is then one gather
     ms, _ = timed(lambda: geot.transpose_edges(col, w, row, R4, R4, "sum"), 1 << 40)
     emit("c4_spmm transpose_edges (once per static graph)", ms, n4 * 40, False)

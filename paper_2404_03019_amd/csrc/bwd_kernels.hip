@@ -223,56 +223,91 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
     }
 }
 
-// fused form, max: arg[r, f] = min edge e of row r whose rounded product equals out[r, f]
+// fused form, max: arg[r, f] = min edge e of row r whose rounded product equals out[r, f].
+// Ids of all passes first, then every pass's X and output vectors, then the compares.
 template <int V>
-__global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *X, int64_t nx, const int64_t *col,
-                                                             const float *w, const int64_t *row,
-                                                             const float *out, int64_t n, int64_t R,
+__global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__restrict__ X, int64_t nx,
+                                                             const int64_t *__restrict__ col,
+                                                             const float *__restrict__ w,
+                                                             const int64_t *__restrict__ row,
+                                                             const float *__restrict__ out, int64_t n, int64_t R,
                                                              int64_t F, unsigned long long *arg) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
+    int64_t rr[kPasses], cc[kPasses];
+    float wt[kPasses];
+#pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = m.row(q);
-        if (e >= n) break;
-        const int64_t r = row[e];
-        const int64_t c = col[e];
-        if ((uint64_t)r >= (uint64_t)R || (uint64_t)c >= (uint64_t)nx) continue;
-        const float wt = w ? w[e] : 1.0f;
+        rr[q] = e < n ? row[e] : -1;
+        cc[q] = e < n ? col[e] : -1;
+        wt[q] = e < n && w ? w[e] : 1.0f;
+    }
+    if (nvec <= m.tpr) {
+        float x[kPasses][V], o[kPasses][V];
+        bool ok[kPasses];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx && m.j0 < nvec;
+            if (ok[q]) {
+                load_vec<V>(X + cc[q] * F + (int64_t)m.j0 * V, x[q]);
+                load_vec<V>(out + rr[q] * F + (int64_t)m.j0 * V, o[q]);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if (!ok[q]) continue;
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                const float t = w ? wt[q] * x[q][k] : x[q][k];  // the forward's term: one rounded product
+                if (t == o[q][k]) atomicMin(arg + rr[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+            }
+        }
+        return;
+    }
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t e = m.row(q);
+        const int64_t r = rr[q], c = cc[q];
+        if (e >= n || (uint64_t)r >= (uint64_t)R || (uint64_t)c >= (uint64_t)nx) continue;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V], o[V];
             load_vec<V>(X + c * F + (int64_t)j * V, x);
             load_vec<V>(out + r * F + (int64_t)j * V, o);
 #pragma unroll
             for (int k = 0; k < V; ++k) {
-                const float t = w ? wt * x[k] : x[k];  // the forward's term: one rounded product
+                const float t = w ? wt[q] * x[k] : x[k];
                 if (t == o[k]) atomicMin(arg + r * F + (int64_t)j * V + k, (unsigned long long)e);
             }
         }
     }
 }
 
-// fused form, w.r.t. X: grad_X[col[e]] += coef(e) * grad_out[row[e]] (atomic adds)
-template <int V, int OP>
-__global__ __launch_bounds__(256) void gs_bwd_x_kernel(const int64_t *col, int64_t nx, const float *w,
-                                                       const int64_t *row, const int64_t *off,
-                                                       const unsigned long long *arg, const float *gout,
-                                                       int64_t n, int64_t R, int64_t F, float *gX) {
+// fused form, max, w.r.t. X: one thread per V-vector of a row r of the recipients; for each
+// (r, f) with a recipient edge e, grad_X[col[e], f] += coef(e) * grad_out[r, f]. Walks the
+// R * F recipients once (arg and grad_out stream) instead of every edge's row of them.
+template <int V>
+__global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long long *__restrict__ arg,
+                                                           const int64_t *__restrict__ col, int64_t nx,
+                                                           const float *__restrict__ w,
+                                                           const float *__restrict__ gout, int64_t n,
+                                                           int64_t R, int64_t F, float *gX) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     for (int q = 0; q < kPasses; ++q) {
-        const int64_t e = m.row(q);
-        if (e >= n) break;
-        const int64_t r = row[e];
-        const int64_t c = col[e];
-        if ((uint64_t)r >= (uint64_t)R || (uint64_t)c >= (uint64_t)nx) continue;
-        float coef = w ? w[e] : 1.0f;
-        if (OP == GEOT_BWD_MEAN) coef = coef / (float)(off[r + 1] - off[r]);
+        const int64_t r = m.row(q);
+        if (r >= R) break;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float g[V];
+            unsigned long long a[V];
             load_vec<V>(gout + r * F + (int64_t)j * V, g);
 #pragma unroll
+            for (int k = 0; k < V; ++k) a[k] = arg[r * F + (int64_t)j * V + k];
+#pragma unroll
             for (int k = 0; k < V; ++k) {
-                if (OP == GEOT_BWD_MAX && arg[r * F + (int64_t)j * V + k] != (unsigned long long)e) continue;
+                if (a[k] >= (unsigned long long)n) continue;  // no recipient (empty row)
+                const int64_t c = col[a[k]];
+                if ((uint64_t)c >= (uint64_t)nx) continue;
+                const float coef = w ? w[a[k]] : 1.0f;
                 unsafeAtomicAdd(gX + c * F + (int64_t)j * V + k, coef * g[k]);
             }
         }
@@ -318,17 +353,31 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
                 for (int k = 0; k < V; ++k) g[q][k] = x[q][k] = 0.0f;
             }
         }
+        if constexpr (OP == GEOT_BWD_MAX) {
+            // max: the recipients load with the operand rows (16-byte pairs where V >= 2), and
+            // the other edges' products are masked out
+#pragma unroll
+            for (int q = 0; q < kPasses; ++q) {
+                if (!(ok[q] && m.j0 < nvec)) continue;
+                const unsigned long long *a = arg + rr[q] * F + (int64_t)m.j0 * V;
+                const unsigned long long e = (unsigned long long)m.row(q);
+                if constexpr (V >= 2) {
+#pragma unroll
+                    for (int k = 0; k < V; k += 2) {
+                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
+                        if (t.x != e) g[q][k] = 0.0f;
+                        if (t.y != e) g[q][k + 1] = 0.0f;
+                    }
+                } else {
+                    if (a[0] != e) g[q][0] = 0.0f;
+                }
+            }
+        }
 #pragma unroll
         for (int q = 0; q < kPasses; ++q) {
             acc[q] = 0.0f;
-            const int64_t e = m.row(q);
 #pragma unroll
-            for (int k = 0; k < V; ++k) {
-                if (OP == GEOT_BWD_MAX && ok[q] && m.j0 < nvec &&
-                    arg[rr[q] * F + (int64_t)m.j0 * V + k] != (unsigned long long)e)
-                    continue;
-                acc[q] += g[q][k] * x[q][k];
-            }
+            for (int k = 0; k < V; ++k) acc[q] += g[q][k] * x[q][k];
         }
     } else {
 #pragma unroll
@@ -865,18 +914,14 @@ hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const f
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (gX) {
+    if (gX) {  // max only (sum and mean gather over the transposed list)
+        if (op != GEOT_BWD_MAX) return hipErrorInvalidValue;
         e = launch_fill(gX, nx, F, F, 0.0f, st);
         if (e != hipSuccess) return e;
-        if (op == GEOT_BWD_SUM)
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_x_kernel<VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st,
-                                            col, nx, w, row, off, arg, gout, n, R, F, gX));
-        else if (op == GEOT_BWD_MEAN)
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_x_kernel<VV, GEOT_BWD_MEAN>), dim3(g), dim3(256), 0,
-                                            st, col, nx, w, row, off, arg, gout, n, R, F, gX));
-        else
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_x_kernel<VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st,
-                                            col, nx, w, row, off, arg, gout, n, R, F, gX));
+        const int64_t gr = grid_rows(R, (int)(F / V));
+        if (gr > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_x_max_kernel<VV>), dim3((unsigned)gr), dim3(256), 0, st, arg, col,
+                                        nx, w, gout, n, R, F, gX));
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -167,8 +167,9 @@ hipError_t launch_seg_bwd_max(const float *gout, const int64_t *idx, const float
                               int64_t n, int64_t S, int64_t F, int V, unsigned long long *arg, float *gsrc,
                               hipStream_t st);
 
-// fused form: grad_X (zero-filled here, then atomic adds) and/or grad_w; off = row starts
-// (mean), arg [R x F] scratch (max).
+// fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
+// sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);
+// off = row starts (mean), arg [R x F] scratch (max).
 hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const float *w, const int64_t *row,
                          const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
                          int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw,
