@@ -35,6 +35,7 @@ SEG_CASES = [
     (3, 25000, 700, 32, "uniform", "int", 0.2),
     (4, 8000, 400, 33, "one_heavy", "normal", 0.1),
     (5, 6000, 300, 256, "zipf", "normal", 0.0),
+    (6, 7000, 400, 6, "zipf", "int", 0.1),          # 2-wide vectors; integer values tie often
 ]
 
 
@@ -63,6 +64,7 @@ GS_CASES = [
     (13, 10000, 500, 700, 64, "uniform", "normal", False),
     (14, 8000, 300, 3000, 128, "one_heavy", "normal", True),
     (15, 5000, 400, 400, 17, "poisson", "int", True),
+    (16, 6000, 500, 600, 6, "zipf", "int", True),        # 2-wide vectors, ties
 ]
 
 
