@@ -322,7 +322,6 @@ template <int V, int OP>
 __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__ X, int64_t nx,
                                                        const int64_t *__restrict__ col,
                                                        const int64_t *__restrict__ row,
-                                                       const int64_t *__restrict__ off,
                                                        const unsigned long long *__restrict__ arg,
                                                        const float *__restrict__ gout, int64_t n, int64_t R,
                                                        int64_t F, float *__restrict__ gw) {
@@ -928,10 +927,10 @@ hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const f
     if (gw) {
         if (op == GEOT_BWD_SUM || op == GEOT_BWD_MEAN)
             GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st,
-                                            X, nx, col, row, off, arg, gout, n, R, F, gw));
+                                            X, nx, col, row, arg, gout, n, R, F, gw));
         else
             GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st,
-                                            X, nx, col, row, off, arg, gout, n, R, F, gw));
+                                            X, nx, col, row, arg, gout, n, R, F, gw));
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (op == GEOT_BWD_MEAN) {
