@@ -244,6 +244,25 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
         wt[q] = e < n && w ? w[e] : 1.0f;
     }
     if (nvec <= m.tpr) {
+        // The block's edges are the consecutive slots q * rows + rsub. For each (row, column) the
+        // block's lowest matching slot is found with LDS atomics (the slot where the row starts in
+        // the block keys the table); only that slot stores. A row that lies wholly in this block
+        // stores its recipient plainly; a row that continues into the previous or next block takes
+        // the lowest edge over the blocks with a global atomicMin. With sorted rows this equals the
+        // plain rule (the lowest attaining edge); the global atomics are about one per row end.
+        __shared__ unsigned s_min[kPasses * 256 * V];   // slots * columns <= kPasses * 256 * V
+        __shared__ int64_t s_row[kPasses * 256];
+        const int slots = kPasses * m.rows, ncol = nvec * V;
+        const int64_t e0 = (int64_t)blockIdx.x * slots;   // edge of slot 0
+        for (int t = threadIdx.x; t < slots * ncol; t += 256) s_min[t] = 0xffffffffu;
+        if (m.j0 == 0) {
+#pragma unroll
+            for (int q = 0; q < kPasses; ++q)   // slots past the last edge sort after every row
+                s_row[q * m.rows + m.rsub] = m.row(q) < n ? rr[q] : INT64_MAX;
+        }
+        const bool has_prev = e0 > 0, has_next = e0 + slots < n;
+        const int64_t prev_row = has_prev ? row[e0 - 1] : 0;
+        const int64_t next_row = has_next ? row[e0 + slots] : 0;
         float x[kPasses][V], o[kPasses][V];
         bool ok[kPasses];
 #pragma unroll
@@ -254,13 +273,43 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
                 load_vec<V>(out + rr[q] * F + (int64_t)m.j0 * V, o[q]);
             }
         }
+        __syncthreads();
+        unsigned hit[kPasses];   // bit k: column j0 * V + k of this pass's edge attains the maximum
+        int rs[kPasses];         // slot where this pass's row starts in the block
 #pragma unroll
         for (int q = 0; q < kPasses; ++q) {
+            hit[q] = 0;
+            rs[q] = 0;
             if (!ok[q]) continue;
+            const int slot = q * m.rows + m.rsub;
+            int lo = 0, hi = slot;   // lowest slot holding this row (s_row[slot] is it)
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s_row[mid] < rr[q]) lo = mid + 1;
+                else hi = mid;
+            }
+            rs[q] = lo;
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 const float t = w ? wt[q] * x[q][k] : x[q][k];  // the forward's term: one rounded product
-                if (t == o[q][k]) atomicMin(arg + rr[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+                if (t == o[q][k]) {
+                    hit[q] |= 1u << k;
+                    atomicMin(&s_min[lo * ncol + m.j0 * V + k], (unsigned)slot);
+                }
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if (!hit[q]) continue;
+            const int slot = q * m.rows + m.rsub;
+            const bool shared_row = (has_prev && prev_row == rr[q]) || (has_next && next_row == rr[q]);
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                if (!(hit[q] >> k & 1u) || s_min[rs[q] * ncol + m.j0 * V + k] != (unsigned)slot) continue;
+                unsigned long long *a = arg + rr[q] * F + (int64_t)m.j0 * V + k;
+                if (shared_row) atomicMin(a, (unsigned long long)m.row(q));
+                else *a = (unsigned long long)m.row(q);
             }
         }
         return;
