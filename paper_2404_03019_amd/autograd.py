@@ -3,9 +3,9 @@
 The functions here are torch.autograd.Function wrappers: their forward calls
 geot_segment_reduce / geot_gather_scatter and their backward calls
 geot_segment_reduce_backward / geot_gather_scatter_backward. The only torch
-arithmetic is in the layer's dense transform (a plain matrix product) and
-bias, as in the GNN layers of the paper's end-to-end setting (Section V-F:
-message and aggregation fused into one operator, update by a dense layer).
+arithmetic is in the layer's dense transform (a matrix product) and bias, as
+in the GNN layers of the paper's end-to-end setting (Section V-F: message and
+aggregation fused into one operator, update by a dense layer).
 """
 from __future__ import annotations
 
@@ -115,6 +115,43 @@ def gather_scatter(x, col, weight, row, num_rows, reduce="sum", graph=None):
     return GatherScatter.apply(x, col, weight, row, num_rows, reduce, graph)
 
 
+class RowsLinear(torch.autograd.Function):
+    """y = x W^T for x with very many rows (one per graph node).
+
+    The weight gradient gy^T x reduces over all the rows into a small
+    (out x in) result. As one product it runs on only as many output tiles as
+    that result has (MI355X, 2,449,029 x 128 rows: 3.7 ms); as a batched
+    product over 4,096-row chunks, summed, it spreads over the chunks (0.8 ms).
+    fp32 only; other types take the one product."""
+
+    CHUNK = 4096
+
+    @staticmethod
+    def forward(ctx, x, weight):
+        ctx.save_for_backward(x, weight)
+        return torch.nn.functional.linear(x, weight)
+
+    @staticmethod
+    def backward(ctx, gy):
+        x, weight = ctx.saved_tensors
+        gy = gy.contiguous()
+        gx = gy @ weight if ctx.needs_input_grad[0] else None
+        gw = None
+        if ctx.needs_input_grad[1]:
+            c = RowsLinear.CHUNK
+            n, nb = x.shape[0], x.shape[0] // RowsLinear.CHUNK
+            if x.dtype != torch.float32 or nb < 2:
+                gw = gy.t() @ x
+            else:
+                x = x.contiguous()
+                a = gy[:nb * c].view(nb, c, gy.shape[1]).transpose(1, 2)
+                b = x[:nb * c].view(nb, c, x.shape[1])
+                gw = torch.bmm(a, b).sum(0)
+                if nb * c < n:
+                    gw = gw + gy[nb * c:].t() @ x[nb * c:]
+        return gx, gw
+
+
 class GraphConv(torch.nn.Module):
     """h' = aggregate_{e: row[e] = v} w_e * (h W)[col[e]] + b, with the aggregation fused.
 
@@ -135,6 +172,6 @@ class GraphConv(torch.nn.Module):
         if isinstance(col, Graph):
             graph = col
             col, row, num_nodes, weight = graph.col, graph.row, graph.num_nodes, graph.weight
-        z = self.lin(h)
+        z = RowsLinear.apply(h, self.lin.weight)
         out = gather_scatter(z, col, weight, row, num_nodes, self.reduce, graph)
         return out + self.bias if self.bias is not None else out
