@@ -238,8 +238,9 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
  * library counting-sorts the edges by column into a temporary transposed list
  * (one 16-byte record per edge, 20 bytes when num_x_rows >= 2^31, and 12
  * bytes per X row, from its stream-ordered pool; from 2^20 to 2^32 - 1 edges
- * with num_x_rows <= 2^23 the edges are first grouped by buckets of columns,
- * which takes another 16 bytes per edge) and runs the forward gather kernel
+ * with 129 to 2^23 X rows the edges are first grouped by buckets of columns,
+ * which takes another 16 bytes per edge and 12 bytes per bucket and 32,768
+ * edges) and runs the forward gather kernel
  * over it, so every row of grad_X is written without float atomics; for max
  * only the recipients' terms are added, atomically.
  *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
@@ -279,10 +280,10 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
  * atomic cursor); any order is a valid input to the gather. op must be sum or
  * mean (the max gradient depends on the forward result). Edges whose column is
  * out of range are left out, and the tail of the outputs is then unspecified.
- * Temporary memory: 16 bytes per edge (when num_x_rows < 2^31; 32 from 2^20 to
- * 2^32 - 1 edges with num_x_rows <= 2^23, where the edges are grouped by
- * buckets of columns first) and 12 per X row (and 8 per row for mean), from the
- * library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
+ * Temporary memory: 16 bytes per edge (when num_x_rows < 2^31; 32, plus 12
+ * bytes per bucket and 32,768 edges, from 2^20 to 2^32 - 1 edges with 129 to
+ * 2^23 X rows, where the edges are grouped by buckets of columns first) and 12
+ * per X row (and 8 per row for mean), from the library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
  * sizes, num_rows >= 2^31, another op, or outputs that overlap the inputs or
  * each other.                                                               */
 geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,
