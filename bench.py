@@ -226,7 +226,17 @@ def suite(reps: int):
         b = n3 * 8 + n3 * 128 + S3 * 128 + (n3 * 128 + S3 * 128 if op == "max" else 0)
         ms, cold = timed(lambda: geot.segment_reduce_backward(g3, idx, op, src, out, grad_src=gsrc), b)
         emit(f"c3_powerlaw_graph backward {op}", ms, b, cold)
-    del src, idx, g3, gsrc, c3
+    del gsrc
+    # the gradients with bf16 storage and int32 ids: grad_src written as bf16
+    src16, idx32 = src.to(torch.bfloat16), idx.to(torch.int32)
+    gsrc16 = torch.empty_like(src16)
+    for op in ("sum", "mean", "max"):
+        out = geot.segment_reduce(src16, idx32, S3, op)
+        b = n3 * 4 + n3 * 64 + S3 * 128 + (n3 * 64 + S3 * 128 if op == "max" else 0)
+        ms, cold = timed(lambda: geot.segment_reduce_backward(g3, idx32, op, src16, out, grad_src=gsrc16), b)
+        emit(f"c3_powerlaw_graph backward {op} bf16 int32", ms, b, cold)
+    del src16, idx32, gsrc16
+    del src, idx, g3, c3
     torch.cuda.empty_cache()
     c4 = make_config("c4_spmm")
     R4 = c4["num_segments"]

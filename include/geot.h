@@ -233,6 +233,20 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
                                            const float *src, const float *out, float *grad_src,
                                            void *stream);
 
+/* geot_segment_reduce_backward for the storage types of geot_segment_reduce_typed
+ * (Section VI: training; bf16 / fp16 storage is not in the paper): src (read for
+ * max only) and grad_src are of src_type, sorted_index of index_type; grad_out
+ * and out stay fp32. Every gradient value is formed in fp32 as above and stored
+ * rounded to nearest even in src_type, so a 16-bit gradient equals the fp32
+ * gradient of the widened src rounded once (sum and max exactly so; mean within
+ * the fp32 reciprocal's error before that rounding). The fp32 / int64 call is
+ * geot_segment_reduce_backward. Returns GEOT_ERROR_INVALID_VALUE for an
+ * unknown src_type or index_type, besides the checks above.               */
+geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const void *sorted_index,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                                 int64_t F, geot_op_t op, const void *src, geot_dtype_t src_type,
+                                                 const float *out, void *grad_src, void *stream);
+
 /* Gradients of geot_gather_scatter w.r.t. X and the edge weights. The caller
  * keeps only the row-sorted edge list: for the X gradient of sum and mean the
  * library counting-sorts the edges by column into a temporary transposed list

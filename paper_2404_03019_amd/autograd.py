@@ -21,6 +21,7 @@ class SegmentReduce(torch.autograd.Function):
     def forward(ctx, src, index, num_segments: int, reduce: str = "sum"):
         out = geot.segment_reduce(src.contiguous(), index, num_segments, reduce)
         ctx.reduce = reduce
+        ctx.src_dtype = src.dtype
         if reduce == "max":
             ctx.save_for_backward(index, src, out)
         else:
@@ -34,11 +35,10 @@ class SegmentReduce(torch.autograd.Function):
         else:
             (index,) = ctx.saved_tensors
             src = out = None
-        # the gradient kernels take fp32 data and int64 ids; a 16-bit src gets its
-        # gradient cast back by autograd
-        index = index.long()
-        src = src.float() if src is not None else None
-        g = geot.segment_reduce_backward(grad_out.contiguous(), index, ctx.reduce, src, out)
+        # the gradient is written in src's storage type, with src's ids (int64 or int32)
+        g = geot.segment_reduce_backward(grad_out.contiguous(), index, ctx.reduce,
+                                         src.contiguous() if src is not None else None, out,
+                                         dtype=ctx.src_dtype)
         return g, None, None, None
 
 

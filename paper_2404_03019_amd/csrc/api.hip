@@ -669,13 +669,17 @@ geot_status_t geot_gather_scatter(const float *X, int64_t num_x_rows, const int6
                                     out, stream, nullptr);
 }
 
-geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
-                                           int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
-                                           const float *src, const float *out, float *grad_src,
-                                           void *stream) {
+geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const void *sorted_index,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                                 int64_t F, geot_op_t op, const void *src, geot_dtype_t src_type,
+                                                 const float *out, void *grad_src, void *stream) {
     t_detail.clear();
     if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
+    if (src_type != GEOT_DTYPE_F32 && src_type != GEOT_DTYPE_BF16 && src_type != GEOT_DTYPE_F16)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown storage type %d", (int)src_type);
+    if (index_type != GEOT_INDEX_I64 && index_type != GEOT_INDEX_I32)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown index type %d", (int)index_type);
     if (nnz < 0 || num_segments < 0 || F < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
     if (nnz == 0 || F == 0) return GEOT_SUCCESS;
     if (num_segments == 0) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments is 0 but nnz > 0");
@@ -685,27 +689,35 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
         return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
     if (!grad_out || !sorted_index || !grad_src) return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
     if (op == GEOT_OP_MAX && (!src || !out)) return fail(GEOT_ERROR_INVALID_VALUE, "max needs src and out");
-    const size_t gb = (size_t)(nnz * F) * 4;
+    const size_t es = src_type == GEOT_DTYPE_F32 ? 4 : 2, is = index_type == GEOT_INDEX_I32 ? 4 : 8;
+    const size_t gb = (size_t)(nnz * F) * es;
     if (overlaps(grad_src, gb, grad_out, (size_t)(num_segments * F) * 4) ||
-        overlaps(grad_src, gb, sorted_index, (size_t)nnz * 8) || overlaps(grad_src, gb, src, gb) ||
+        overlaps(grad_src, gb, sorted_index, (size_t)nnz * is) ||
+        overlaps(grad_src, gb, src, op == GEOT_OP_MAX ? gb : 0) ||
         overlaps(grad_src, gb, out, op == GEOT_OP_MAX ? (size_t)(num_segments * F) * 4 : 0))
         return fail(GEOT_ERROR_INVALID_VALUE, "grad_src overlaps an input");
+    // widest vector that F and every pointer allow (fp32 operands: 16-byte loads of 4; 16-bit
+    // storage also 8 elements, loaded and stored as 16 bytes)
     const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)grad_src |
                            (op == GEOT_OP_MAX ? ((uintptr_t)src | (uintptr_t)out) : 0);
-    const int V = (F % 4 == 0 && (ptrs & 15) == 0) ? 4 : ((F % 2 == 0 && (ptrs & 7) == 0) ? 2 : 1);
+    int V = 1;
+    if (es == 2 && F % 8 == 0 && (ptrs & 15) == 0) V = 8;
+    else if (F % 4 == 0 && (ptrs & 15) == 0) V = 4;
+    else if (F % 2 == 0 && (ptrs & 7) == 0) V = 2;
+    const int elem = (int)src_type, idx32 = index_type == GEOT_INDEX_I32 ? 1 : 0;
     hipStream_t st = (hipStream_t)stream;
     void *scratch = nullptr;
     StreamCtx *ctx = nullptr;
     if (op == GEOT_OP_MAX) {
         geot_status_t s = stream_scratch((size_t)(num_segments * F) * 8, st, &scratch, nullptr, &ctx);
         if (s != GEOT_SUCCESS) return s;
-        GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, src, out, nnz, num_segments, F, V,
+        GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, nnz, num_segments, F, V, elem,
                                     (unsigned long long *)scratch, grad_src, st),
                  "launch max backward kernels");
         return GEOT_SUCCESS;
     }
     if (op == GEOT_OP_SUM) {
-        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, nullptr, nnz, num_segments, F, V, false,
+        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, nullptr, nnz, num_segments, F, V, elem, false,
                                       grad_src, st),
                  "launch backward kernel");
         return GEOT_SUCCESS;
@@ -715,13 +727,26 @@ geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t 
     if (s != GEOT_SUCCESS) return s;
     int64_t *off = (int64_t *)scratch;
     return poison(ctx, [&]() -> geot_status_t {
-        GEOT_HIP(launch_offsets(sorted_index, nnz, num_segments, off, gaps, st), "launch offsets kernel");
+        if (idx32)
+            GEOT_HIP(launch_offsets_i32(static_cast<const int32_t *>(sorted_index), nnz, num_segments, off, gaps, st),
+                     "launch offsets kernel");
+        else
+            GEOT_HIP(launch_offsets(static_cast<const int64_t *>(sorted_index), nnz, num_segments, off, gaps, st),
+                     "launch offsets kernel");
         GEOT_HIP(launch_gap_fill_i64(off, num_segments + 1, gaps, st), "launch gap fill kernel");
-        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, off, nnz, num_segments, F, V, true,
+        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, off, nnz, num_segments, F, V, elem, true,
                                       grad_src, st),
                  "launch backward kernel");
         return GEOT_SUCCESS;
     }());
+}
+
+geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
+                                           int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
+                                           const float *src, const float *out, float *grad_src,
+                                           void *stream) {
+    return geot_segment_reduce_backward_typed(grad_out, sorted_index, GEOT_INDEX_I64, nnz, num_segments, F, op,
+                                              src, GEOT_DTYPE_F32, out, grad_src, stream);
 }
 
 geot_status_t geot_segment_reduce_typed(const void *src, geot_dtype_t src_type, const void *sorted_index,

@@ -20,7 +20,8 @@ __global__ __launch_bounds__(256) void fill_kernel(float *out, int64_t rows, int
 // segment in (idx[i-1], idx[i]] (so empty segments get the next start), and
 // the last row also writes (idx[n-1], S] = n. Runs longer than kGapRun go to
 // the gap list instead (value = the row they start at).
-__global__ __launch_bounds__(256) void offsets_kernel(const int64_t *idx, int64_t n, int64_t S,
+template <typename I>
+__global__ __launch_bounds__(256) void offsets_kernel(const I *idx, int64_t n, int64_t S,
                                                       int64_t *off, GapList gaps) {
     auto put = [&](int64_t lo, int64_t hi, int64_t row) {  // off[lo, hi) = row
         lo = max(lo, (int64_t)0);
@@ -30,8 +31,8 @@ __global__ __launch_bounds__(256) void offsets_kernel(const int64_t *idx, int64_
     };
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t s = idx[i];
-        const int64_t sp = i > 0 ? idx[i - 1] : -1;
+        const int64_t s = (int64_t)idx[i];
+        const int64_t sp = i > 0 ? (int64_t)idx[i - 1] : -1;
         if (s != sp) put(sp + 1, s + 1, i);
         if (i == n - 1) put(s + 1, S + 1, n);
     }
@@ -135,7 +136,15 @@ hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float va
 hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
                           hipStream_t stream) {
     if (n <= 0) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(offsets_kernel, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(offsets_kernel<int64_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
+                       idx, n, S, off, gaps);
+    return hipGetLastError();
+}
+
+hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
+                              hipStream_t stream) {
+    if (n <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(offsets_kernel<int32_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
                        idx, n, S, off, gaps);
     return hipGetLastError();
 }

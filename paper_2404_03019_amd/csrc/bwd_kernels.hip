@@ -14,6 +14,7 @@
 // members with 64-bit atomicMin (order-independent, so deterministic), the
 // next pass writes the gradients.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -44,20 +45,70 @@ __device__ __forceinline__ RowMap row_map(int nvec) {
     return m;
 }
 
-// grad_src[i] = grad_out[idx[i]] (times 1 / len for mean). The ids of all the
-// block's passes load first, so their latency overlaps; then the rows.
-template <int V, bool MEAN>
+// V fp32 gradient values (8 as two 16-byte loads)
+template <int V>
+__device__ __forceinline__ void load_f32(const float *p, float *x) {
+    if constexpr (V == 8) {
+        load_vec<4>(p, x);
+        load_vec<4>(p + 4, x + 4);
+    } else {
+        load_vec<V>(p, x);
+    }
+}
+
+// fp32 -> bf16 bits, rounded to nearest even (a carry into bit 16 from the
+// lower half plus 0x7fff, plus the kept lowest bit for ties); a NaN stays a
+// quiet NaN
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int E>
+__device__ __forceinline__ uint32_t narrow_bits(float f) {
+    if constexpr (E == ELEM_BF16) return bf16_bits(f);
+    else return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);  // round to nearest even
+}
+
+// V fp32 values stored as V elements of storage type E at p (aligned to V elements)
+template <int E, int V>
+__device__ __forceinline__ void store_elems(typename ElemT<E>::T *p, const float *x) {
+    if constexpr (E == ELEM_F32) {
+        store_vec<V>(p, x);
+    } else if constexpr (V == 1) {
+        *reinterpret_cast<uint16_t *>(p) = (uint16_t)narrow_bits<E>(x[0]);
+    } else {
+        uint32_t w[V / 2];
+#pragma unroll
+        for (int k = 0; k < V / 2; ++k) w[k] = narrow_bits<E>(x[2 * k]) | (narrow_bits<E>(x[2 * k + 1]) << 16);
+        if constexpr (V == 8) {
+            u32x4_t t = {w[0], w[1], w[2], w[3]};
+            *reinterpret_cast<u32x4_t *>(p) = t;
+        } else if constexpr (V == 4) {
+            u32x2_t t = {w[0], w[1]};
+            *reinterpret_cast<u32x2_t *>(p) = t;
+        } else {
+            *reinterpret_cast<uint32_t *>(p) = w[0];
+        }
+    }
+}
+
+// grad_src[i] = grad_out[idx[i]] (times 1 / len for mean), stored in the source's type E.
+// The ids of all the block's passes load first, so their latency overlaps; then the rows.
+template <int E, typename I, int V, bool MEAN>
 __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restrict__ gout,
-                                                            const int64_t *__restrict__ idx,
+                                                            const I *__restrict__ idx,
                                                             const int64_t *__restrict__ off, int64_t n,
-                                                            int64_t S, int64_t F, float *__restrict__ gsrc) {
+                                                            int64_t S, int64_t F,
+                                                            typename ElemT<E>::T *__restrict__ gsrc) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     int64_t seg[kPasses];
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
-        seg[q] = i < n ? idx[i] : -1;
+        seg[q] = i < n ? (int64_t)idx[i] : -1;
     }
     // mean: every pass's segment starts load together, branchless (a segment out of range
     // reads segment 0's), before the first gradient row
@@ -81,7 +132,7 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
             for (int j = m.j0; j < nvec; j += m.tpr) {
                 float x[V];
                 if (ok) {
-                    load_vec<V>(gout + s * F + (int64_t)j * V, x);
+                    load_f32<V>(gout + s * F + (int64_t)j * V, x);
                     if (MEAN) {
 #pragma unroll
                         for (int k = 0; k < V; ++k) x[k] = x[k] * inv;
@@ -90,7 +141,7 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
 #pragma unroll
                     for (int k = 0; k < V; ++k) x[k] = 0.0f;
                 }
-                store_vec<V>(gsrc + i * F + (int64_t)j * V, x);
+                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
             }
         }
     }
@@ -99,9 +150,9 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
 // arg[s, f] = min row i of segment s with src[i, f] == out[s, f]. The ids of all passes
 // load first, then every pass's row and output vector, then the compares (one memory
 // latency per step, not per pass).
-template <int V>
-__global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__restrict__ src,
-                                                              const int64_t *__restrict__ idx,
+template <int E, typename I, int V>
+__global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename ElemT<E>::T *__restrict__ src,
+                                                              const I *__restrict__ idx,
                                                               const float *__restrict__ out, int64_t n, int64_t S,
                                                               int64_t F, unsigned long long *arg) {
     const int nvec = (int)(F / V);
@@ -110,7 +161,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__res
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
-        seg[q] = i < n ? idx[i] : -1;
+        seg[q] = i < n ? (int64_t)idx[i] : -1;
     }
     if (nvec <= m.tpr) {  // one vector per thread and row
         float x[kPasses][V], o[kPasses][V];
@@ -119,8 +170,10 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__res
         for (int q = 0; q < kPasses; ++q) {
             ok[q] = m.row(q) < n && (uint64_t)seg[q] < (uint64_t)S && m.j0 < nvec;
             if (ok[q]) {
-                load_vec<V>(src + m.row(q) * F + (int64_t)m.j0 * V, x[q]);
-                load_vec<V>(out + seg[q] * F + (int64_t)m.j0 * V, o[q]);
+                Raw<E, V> r;
+                load_raw<E, V>(src + m.row(q) * F + (int64_t)m.j0 * V, r);
+                widen<E, V>(r, x[q]);
+                load_f32<V>(out + seg[q] * F + (int64_t)m.j0 * V, o[q]);
             }
         }
 #pragma unroll
@@ -139,8 +192,10 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__res
         if (i >= n || (uint64_t)s >= (uint64_t)S) continue;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V], o[V];
-            load_vec<V>(src + i * F + (int64_t)j * V, x);
-            load_vec<V>(out + s * F + (int64_t)j * V, o);
+            Raw<E, V> r;
+            load_raw<E, V>(src + i * F + (int64_t)j * V, r);
+            widen<E, V>(r, x);
+            load_f32<V>(out + s * F + (int64_t)j * V, o);
 #pragma unroll
             for (int k = 0; k < V; ++k)
                 if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (unsigned long long)i);
@@ -150,19 +205,19 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const float *__res
 
 // grad_src[i, f] = grad_out[s, f] where i is the recipient of (s, f), else 0; ids first,
 // then every pass's gradient and recipient vectors, then the stores
-template <int V>
+template <int E, typename I, int V>
 __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__restrict__ gout,
-                                                                const int64_t *__restrict__ idx,
+                                                                const I *__restrict__ idx,
                                                                 const unsigned long long *__restrict__ arg,
                                                                 int64_t n, int64_t S, int64_t F,
-                                                                float *__restrict__ gsrc) {
+                                                                typename ElemT<E>::T *__restrict__ gsrc) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     int64_t seg[kPasses];
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
-        seg[q] = i < n ? idx[i] : -1;
+        seg[q] = i < n ? (int64_t)idx[i] : -1;
     }
     if (nvec <= m.tpr) {
         float x[kPasses][V];
@@ -171,7 +226,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
         for (int q = 0; q < kPasses; ++q) {
             const bool ok = (uint64_t)seg[q] < (uint64_t)S && m.j0 < nvec;
             if (ok) {
-                load_vec<V>(gout + seg[q] * F + (int64_t)m.j0 * V, x[q]);
+                load_f32<V>(gout + seg[q] * F + (int64_t)m.j0 * V, x[q]);
                 const unsigned long long *a = arg + seg[q] * F + (int64_t)m.j0 * V;
                 if constexpr (V >= 2) {  // 16-byte loads: V * 8 bytes at a multiple of V * 8
 #pragma unroll
@@ -198,7 +253,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
 #pragma unroll
             for (int k = 0; k < V; ++k)
                 if (w[q][k] != (unsigned long long)i) x[q][k] = 0.0f;
-            store_vec<V>(gsrc + i * F + (int64_t)m.j0 * V, x[q]);
+            store_elems<E, V>(gsrc + i * F + (int64_t)m.j0 * V, x[q]);
         }
         return;
     }
@@ -210,7 +265,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V];
             if (ok) {
-                load_vec<V>(gout + s * F + (int64_t)j * V, x);
+                load_f32<V>(gout + s * F + (int64_t)j * V, x);
 #pragma unroll
                 for (int k = 0; k < V; ++k)
                     if (arg[s * F + (int64_t)j * V + k] != (unsigned long long)i) x[k] = 0.0f;
@@ -218,7 +273,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
 #pragma unroll
                 for (int k = 0; k < V; ++k) x[k] = 0.0f;
             }
-            store_vec<V>(gsrc + i * F + (int64_t)j * V, x);
+            store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
         }
     }
 }
@@ -912,37 +967,83 @@ hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long 
         else { constexpr int VV = 1; CALL; } \
     } while (0)
 
-hipError_t launch_seg_bwd_bcast(const float *gout, const int64_t *idx, const int64_t *off, int64_t n,
-                                int64_t S, int64_t F, int V, bool mean, float *gsrc, hipStream_t st) {
+namespace {
+
+template <typename T> struct TypeTag { using type = T; };
+
+// f(E, I) with the storage type and id type as compile-time tags
+template <typename Fn>
+hipError_t by_types(int elem, int idx32, Fn &&f) {
+    auto by_idx = [&](auto e) -> hipError_t {
+        return idx32 ? f(e, TypeTag<int32_t>{}) : f(e, TypeTag<int64_t>{});
+    };
+    if (elem == ELEM_BF16) return by_idx(std::integral_constant<int, ELEM_BF16>{});
+    if (elem == ELEM_F16) return by_idx(std::integral_constant<int, ELEM_F16>{});
+    if (elem == ELEM_F32) return by_idx(std::integral_constant<int, ELEM_F32>{});
+    return hipErrorInvalidValue;
+}
+
+// f(V) with the vector width as a compile-time value (8 for 16-bit storage only)
+template <int E, typename Fn>
+hipError_t by_width(int V, Fn &&f) {
+    if (V == 8) {
+        if constexpr (E != ELEM_F32) return f(std::integral_constant<int, 8>{});
+        else return hipErrorInvalidValue;
+    }
+    if (V == 4) return f(std::integral_constant<int, 4>{});
+    if (V == 2) return f(std::integral_constant<int, 2>{});
+    return f(std::integral_constant<int, 1>{});
+}
+
+}  // namespace
+
+hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off, int64_t n,
+                                int64_t S, int64_t F, int V, int elem, bool mean, void *gsrc, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
-    if (mean)
-        GEOT_BY_V(V, hipLaunchKernelGGL((seg_bwd_bcast_kernel<VV, true>), dim3(g), dim3(256), 0, st,
-                                        gout, idx, off, n, S, F, gsrc));
-    else
-        GEOT_BY_V(V, hipLaunchKernelGGL((seg_bwd_bcast_kernel<VV, false>), dim3(g), dim3(256), 0, st,
-                                        gout, idx, off, n, S, F, gsrc));
-    return hipGetLastError();
+    return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
+        constexpr int E = decltype(et)::value;
+        using I = typename decltype(it)::type;
+        using T = typename ElemT<E>::T;
+        return by_width<E>(V, [&](auto vt) -> hipError_t {
+            constexpr int VV = decltype(vt)::value;
+            if (mean)
+                hipLaunchKernelGGL((seg_bwd_bcast_kernel<E, I, VV, true>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), off, n, S, F, static_cast<T *>(gsrc));
+            else
+                hipLaunchKernelGGL((seg_bwd_bcast_kernel<E, I, VV, false>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), off, n, S, F, static_cast<T *>(gsrc));
+            return hipGetLastError();
+        });
+    });
 }
 
-hipError_t launch_seg_bwd_max(const float *gout, const int64_t *idx, const float *src, const float *out,
-                              int64_t n, int64_t S, int64_t F, int V, unsigned long long *arg, float *gsrc,
-                              hipStream_t st) {
+hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
+                              int64_t n, int64_t S, int64_t F, int V, int elem, unsigned long long *arg,
+                              void *gsrc, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     hipError_t e = launch_fill_u64(arg, S * F, ~0ull, st);
     if (e != hipSuccess) return e;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
-    GEOT_BY_V(V, hipLaunchKernelGGL((seg_bwd_max_arg_kernel<VV>), dim3(g), dim3(256), 0, st, src, idx,
-                                    out, n, S, F, arg));
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    GEOT_BY_V(V, hipLaunchKernelGGL((seg_bwd_max_write_kernel<VV>), dim3(g), dim3(256), 0, st, gout,
-                                    idx, arg, n, S, F, gsrc));
-    return hipGetLastError();
+    return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
+        constexpr int E = decltype(et)::value;
+        using I = typename decltype(it)::type;
+        using T = typename ElemT<E>::T;
+        return by_width<E>(V, [&](auto vt) -> hipError_t {
+            constexpr int VV = decltype(vt)::value;
+            hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
+                               static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, arg);
+            hipError_t e2 = hipGetLastError();
+            if (e2 != hipSuccess) return e2;
+            hipLaunchKernelGGL((seg_bwd_max_write_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
+                               static_cast<const I *>(idx), arg, n, S, F, static_cast<T *>(gsrc));
+            return hipGetLastError();
+        });
+    });
 }
 
 hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const float *w, const int64_t *row,

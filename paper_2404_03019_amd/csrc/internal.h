@@ -112,6 +112,9 @@ hipError_t launch_sp(const SpArgs &a, int red, int mode, int V, int NT, int L, h
 // Long runs go to `gaps` (value = the row they start at): run launch_gap_fill_i64 after.
 hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
                           hipStream_t stream);
+// the same over int32 ids
+hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
+                              hipStream_t stream);
 
 // Grid-wide passes over a gap list: out rows [first, end) = 0 in the columns of
 // tile `value` (tiles of `tw` columns), or arr[first, end) = value. Both leave
@@ -158,14 +161,17 @@ hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, 
 // scratch of the bucketed transposition (0: the input takes the direct one)
 size_t transpose_scratch_bytes(int64_t n, int64_t nx);
 
-// grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean)
-hipError_t launch_seg_bwd_bcast(const float *gout, const int64_t *idx, const int64_t *off, int64_t n,
-                                int64_t S, int64_t F, int V, bool mean, float *gsrc, hipStream_t st);
+// grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean), stored in
+// the source's ElemType `elem` (16-bit: rounded to nearest even); idx int32 when idx32. V is 1,
+// 2, 4 or (16-bit) 8.
+hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off, int64_t n,
+                                int64_t S, int64_t F, int V, int elem, bool mean, void *gsrc, hipStream_t st);
 
-// max: arg [S x F] scratch; grad_src gets grad_out at the first attaining row of each (s, f)
-hipError_t launch_seg_bwd_max(const float *gout, const int64_t *idx, const float *src, const float *out,
-                              int64_t n, int64_t S, int64_t F, int V, unsigned long long *arg, float *gsrc,
-                              hipStream_t st);
+// max: arg [S x F] scratch; grad_src gets grad_out at the first attaining row of each (s, f);
+// src and grad_src of ElemType `elem`
+hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
+                              int64_t n, int64_t S, int64_t F, int V, int elem, unsigned long long *arg,
+                              void *gsrc, hipStream_t st);
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);

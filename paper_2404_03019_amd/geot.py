@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.geot_index_stats.argtypes = [p, i64, i64, ctypes.POINTER(IndexStats), p]
     L.geot_check_index.argtypes = [p, i64, i64, p, i64, p]
     L.geot_segment_reduce_backward.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, p, p]
+    L.geot_segment_reduce_backward_typed.argtypes = [p, p, ctypes.c_int, i64, i64, i64, ctypes.c_int, p,
+                                                     ctypes.c_int, p, p, p]
     L.geot_gather_scatter_backward.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, p, p, p]
     L.geot_transpose_edges.argtypes = [p, i64, p, p, i64, i64, ctypes.c_int, p, p, p, p]
     L.geot_last_choice.argtypes = [pc]
@@ -227,25 +229,32 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
 
 def segment_reduce_backward(grad_out: torch.Tensor, index: torch.Tensor, reduce: str = "sum",
                             src: torch.Tensor | None = None, out: torch.Tensor | None = None,
-                            grad_src: torch.Tensor | None = None) -> torch.Tensor:
-    """Gradient of segment_reduce w.r.t. src (geot_segment_reduce_backward)."""
+                            grad_src: torch.Tensor | None = None, dtype: torch.dtype | None = None
+                            ) -> torch.Tensor:
+    """Gradient of segment_reduce w.r.t. src (geot_segment_reduce_backward_typed).
+
+    The gradient has src's storage type: that of `grad_src` when given, else of `src`
+    (max), else `dtype` (default fp32). The index may be int64 or int32."""
     _dev(grad_out, "grad_out", torch.float32, 2)
-    _dev(index, "index", torch.int64, 1)
+    _dev(index, "index", tuple(INDEX_TYPES), 1)
     S, F = grad_out.shape
+    typ = grad_src.dtype if grad_src is not None else (src.dtype if src is not None else (dtype or torch.float32))
+    if typ not in DTYPES:
+        raise TypeError(f"the gradient's type must be one of {tuple(DTYPES)}")
     if reduce == "max":
         if src is None or out is None:
             raise ValueError("max needs src and out")
-        _dev(src, "src", torch.float32, 2)
+        _dev(src, "src", typ, 2)
         _dev(out, "out", torch.float32, 2)
     if grad_src is None:
-        grad_src = torch.empty((index.numel(), F), dtype=torch.float32, device=grad_out.device)
+        grad_src = torch.empty((index.numel(), F), dtype=typ, device=grad_out.device)
     else:
-        _dev(grad_src, "grad_src", torch.float32, 2)
+        _dev(grad_src, "grad_src", typ, 2)
     with _OnDevice(grad_out.device):
-        st = lib().geot_segment_reduce_backward(
-            grad_out.data_ptr(), index.data_ptr(), index.numel(), S, F, OPS[reduce],
-            src.data_ptr() if src is not None else None, out.data_ptr() if out is not None else None,
-            grad_src.data_ptr(), _stream(grad_out.device))
+        st = lib().geot_segment_reduce_backward_typed(
+            grad_out.data_ptr(), index.data_ptr(), INDEX_TYPES[index.dtype], index.numel(), S, F, OPS[reduce],
+            src.data_ptr() if src is not None else None, DTYPES[typ],
+            out.data_ptr() if out is not None else None, grad_src.data_ptr(), _stream(grad_out.device))
     _raise(st)
     return grad_src
 

@@ -191,3 +191,65 @@ def test_c4_spmm_bf16_i32_sampled():
         z = np.zeros(b - a, dtype=np.int64)
         ref, terms = oracle_gather(wide, col[a:b], w[a:b], z, 1, "sum")
         compare(got[r:r + 1], ref, "sum", terms, f"c4 bf16 row {r} (len {b - a})")
+
+
+BWD_CASES = [
+    # seed, nnz, S, F, dist, values, empty_frac
+    (41, 20000, 900, 32, "zipf", "normal", 0.1),      # 8-wide 16-bit vectors
+    (42, 15000, 700, 3, "lognormal", "normal", 0.05),  # 1-wide
+    (43, 12000, 500, 12, "uniform", "int", 0.2),       # 4-wide; integer values tie under max
+    (44, 8000, 300, 6, "one_heavy", "int", 0.1),       # 2-wide
+]
+HALF_ULP = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 2.0 ** -23}
+# one rounding in the subnormal range is absolute: half the spacing 2^-24 of binary16's
+# subnormals (bf16 shares fp32's exponent range, so its subnormals are far below these values)
+HALF_SUBNORMAL = {"bf16": 0.0, "f16": 2.0 ** -25, "f32": 0.0}
+
+
+@pytest.mark.parametrize("dt,it", [("bf16", "i64"), ("bf16", "i32"), ("f16", "i32"), ("f16", "i64"),
+                                   ("f32", "i32")])
+@pytest.mark.parametrize("case", BWD_CASES, ids=lambda c: f"seed{c[0]}_F{c[3]}")
+def test_segment_backward_typed(dt, it, case):
+    """The gradient is stored in src's type: for sum and max it is the oracle's gradient on
+    the widened src rounded once to that type (bit-exact, torch rounds to nearest even as
+    the library does); for mean it is within one rounding of the type (plus the fp32
+    reciprocal's error) of the exact quotient."""
+    seed, nnz, S, F, dist, values, ef = case
+    p = random_problem(seed, nnz, S, F, dist, values, ef)
+    t, wide = stored(p["src"], dt)
+    s, i = t.to(DEV), ids(p["index"], it)
+    g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
+    gd = torch.from_numpy(g).to(DEV)
+    for op in OPS:
+        say(f"typed segment backward {dt}/{it} seed={seed} F={F} {op}")
+        out = geot.segment_reduce(s, i, S, op)
+        got = geot.segment_reduce_backward(gd, i, op, s if op == "max" else None,
+                                           out if op == "max" else None, dtype=DT[dt])
+        assert got.dtype == DT[dt] and got.shape == (nnz, F)
+        ref = oracle.segment_reduce_backward(g, p["index"], op, wide, out.cpu().numpy())
+        if op in ("sum", "max"):
+            assert torch.equal(got.cpu(), torch.from_numpy(np.ascontiguousarray(ref)).to(DT[dt])), \
+                f"{dt}/{it} seed={seed} {op}"
+        else:
+            err = np.abs(got.cpu().float().numpy().astype(np.float64) - ref.astype(np.float64))
+            lim = (HALF_ULP[dt] + 1e-6) * np.abs(ref.astype(np.float64)) + HALF_SUBNORMAL[dt] + 1e-30
+            assert np.all(err <= lim), f"{dt}/{it} seed={seed} mean: worst {float(np.max(err - lim))}"
+
+
+def test_segment_backward_typed_through_autograd():
+    """A bf16 src with int32 ids: autograd's gradient is bf16 and equals the fp32 gradient of
+    the widened src rounded once."""
+    p = random_problem(45, 30000, 1200, 16, "zipf", "normal", 0.1)
+    t, wide = stored(p["src"], "bf16")
+    from paper_2404_03019_amd.autograd import segment_reduce as ag_segment_reduce
+    for op in OPS:
+        x = t.to(DEV).requires_grad_(True)
+        out = ag_segment_reduce(x, ids(p["index"], "i32"), 1200, op)
+        g = torch.randn(out.shape, device=DEV, generator=torch.Generator(device=DEV).manual_seed(7))
+        out.backward(g)
+        assert x.grad.dtype == torch.bfloat16
+        xf = torch.from_numpy(wide).to(DEV).requires_grad_(True)
+        outf = ag_segment_reduce(xf, ids(p["index"], "i64"), 1200, op)
+        outf.backward(g)
+        # both paths form the same fp32 values (mean: the same products); bf16 rounds them once
+        assert torch.equal(x.grad, xf.grad.to(torch.bfloat16)), op
