@@ -258,8 +258,16 @@ def suite(reps: int):
         geot.segment_reduce(msg, row, R4, "sum")
     ms_u, _ = timed(unfused, b)
     emit("c4_spmm sum unfused (torch gather + segment_reduce)", ms_u, b, False)
-    del X16, col32, row32
     g4 = torch.randn(R4, 128, device=dev)
+    # the gradients with X stored as bf16 and int32 ids (fp32 gradients): the grad_X bytes
+    # count 12 bytes of metadata per edge, grad_w the gathered X row at 2 bytes an element
+    b = n4 * 12 + n4 * 512 + R4 * 512
+    ms, cold = timed(lambda: geot.gather_scatter_backward(X16, col32, w, row32, g4, "sum", need_weight=False), b)
+    emit("c4_spmm backward grad_X bf16 int32", ms, b, cold)
+    b = n4 * 12 + n4 * 256 + R4 * 512
+    ms, cold = timed(lambda: geot.gather_scatter_backward(X16, col32, w, row32, g4, "sum", need_x=False), b)
+    emit("c4_spmm backward grad_weight bf16 int32", ms, b, cold)
+    del X16, col32, row32
     # grad_X: edge metadata + one gathered grad_out row per edge + grad_X written
     b = n4 * 20 + n4 * 512 + R4 * 512
     ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_weight=False), b)

@@ -279,6 +279,21 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
                                            const float *grad_out, const float *out, float *grad_X,
                                            float *grad_weight, void *stream);
 
+/* geot_gather_scatter_backward for the storage and id types of
+ * geot_gather_scatter_typed (Section VI: training; bf16 / fp16 storage is not in
+ * the paper): X (read for grad_weight and for max) of x_type, col and
+ * sorted_row of index_type; weight, grad_out, out, grad_X and grad_weight stay
+ * fp32. X is widened exactly and every gradient is formed in fp32 as above, so
+ * the results equal the fp32 call's on the widened X (to the same bound; max
+ * routes to the same recipients). The fp32 / int64 call is
+ * geot_gather_scatter_backward. Returns GEOT_ERROR_INVALID_VALUE for an unknown
+ * x_type or index_type, besides the checks above.                          */
+geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
+                                                 const void *col, const float *weight, const void *sorted_row,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                                 geot_op_t op, const float *grad_out, const float *out, float *grad_X,
+                                                 float *grad_weight, void *stream);
+
 /* The edge list sorted by source column instead of destination row: the
  * transposed problem whose fused gather gives the X gradient of sum and mean
  * (Section VI: training), kept by callers whose graph does not change between

@@ -64,7 +64,9 @@ class Graph:
         hit = self._transposed.get(reduce)
         if hit is None or hit[0] != version:
             w = self.weight.detach() if self.weight is not None else None
-            hit = (version, geot.transpose_edges(self.col, w, self.row, self.num_src, self.num_nodes, reduce))
+            # the transposition takes int64 ids: int32 ones are widened here, once per graph
+            hit = (version, geot.transpose_edges(self.col.long(), w, self.row.long(), self.num_src, self.num_nodes,
+                                                 reduce))
             self._transposed[reduce] = hit
         return hit[1]
 
@@ -91,8 +93,7 @@ class GatherScatter(torch.autograd.Function):
         weight = weight if ctx.has_weight else None
         need_x = ctx.needs_input_grad[0]
         need_w = ctx.has_weight and ctx.needs_input_grad[2]
-        x, col, row = x.float(), col.long(), row.long()  # the gradient kernels take fp32 and int64
-        grad_out = grad_out.contiguous()
+        grad_out = grad_out.contiguous()   # x keeps its storage type and the ids theirs
         gx = None
         if need_x and ctx.graph is not None and ctx.reduce in ("sum", "mean"):
             sorted_col, row_t, coef = ctx.graph.transposed(ctx.reduce)
@@ -101,7 +102,10 @@ class GatherScatter(torch.autograd.Function):
         gx2, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out, ctx.reduce,
                                                out if ctx.reduce == "max" else None,
                                                need_x=need_x, need_weight=need_w)
-        return (gx if gx is not None else gx2), None, gw, None, None, None, None
+        gx = gx if gx is not None else gx2
+        if gx is not None and gx.dtype != x.dtype:   # fp32 gradient of a 16-bit x: rounded once
+            gx = gx.to(x.dtype)
+        return gx, None, gw, None, None, None, None
 
 
 def segment_reduce(src, index, num_segments, reduce="sum"):

@@ -770,14 +770,20 @@ geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int6
     return reduce(p, (hipStream_t)stream, choice);
 }
 
-geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,
-                                           const float *weight, const int64_t *sorted_row, int64_t nnz,
-                                           int64_t num_rows, int64_t F, geot_op_t op,
-                                           const float *grad_out, const float *out, float *grad_X,
-                                           float *grad_weight, void *stream) {
+geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
+                                                 const void *col, const float *weight, const void *sorted_row,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                                 geot_op_t op, const float *grad_out, const float *out, float *grad_X,
+                                                 float *grad_weight, void *stream) {
     t_detail.clear();
     if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
+    if (x_type != GEOT_DTYPE_F32 && x_type != GEOT_DTYPE_BF16 && x_type != GEOT_DTYPE_F16)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown storage type %d", (int)x_type);
+    if (index_type != GEOT_INDEX_I64 && index_type != GEOT_INDEX_I32)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown index type %d", (int)index_type);
+    const int elem = (int)x_type, idx32 = index_type == GEOT_INDEX_I32 ? 1 : 0;
+    const size_t es = x_type == GEOT_DTYPE_F32 ? 4 : 2, is = idx32 ? 4 : 8;
     if (nnz < 0 || num_rows < 0 || F < 0 || num_x_rows < 0)
         return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
     if (grad_weight && !weight) return fail(GEOT_ERROR_INVALID_VALUE, "grad_weight needs weight");
@@ -796,18 +802,25 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     if ((grad_weight || op == GEOT_OP_MAX) && !X) return fail(GEOT_ERROR_INVALID_VALUE, "X is NULL");
     if (op == GEOT_OP_MAX && !out) return fail(GEOT_ERROR_INVALID_VALUE, "max needs out");
     const size_t xb = (size_t)(num_x_rows * F) * 4;
-    if (grad_X && (overlaps(grad_X, xb, X, xb) || overlaps(grad_X, xb, grad_out, (size_t)(num_rows * F) * 4) ||
-                   overlaps(grad_X, xb, col, (size_t)nnz * 8) || overlaps(grad_X, xb, sorted_row, (size_t)nnz * 8) ||
+    if (grad_X && (overlaps(grad_X, xb, X, X ? (size_t)(num_x_rows * F) * es : 0) ||
+                   overlaps(grad_X, xb, grad_out, (size_t)(num_rows * F) * 4) ||
+                   overlaps(grad_X, xb, col, (size_t)nnz * is) || overlaps(grad_X, xb, sorted_row, (size_t)nnz * is) ||
                    overlaps(grad_X, xb, weight, weight ? (size_t)nnz * 4 : 0) ||
                    overlaps(grad_X, xb, grad_weight, grad_weight ? (size_t)nnz * 4 : 0)))
         return fail(GEOT_ERROR_INVALID_VALUE, "grad_X overlaps another array");
     if (grad_weight && (overlaps(grad_weight, (size_t)nnz * 4, weight, (size_t)nnz * 4) ||
-                        overlaps(grad_weight, (size_t)nnz * 4, col, (size_t)nnz * 8) ||
-                        overlaps(grad_weight, (size_t)nnz * 4, sorted_row, (size_t)nnz * 8)))
+                        overlaps(grad_weight, (size_t)nnz * 4, col, (size_t)nnz * is) ||
+                        overlaps(grad_weight, (size_t)nnz * 4, sorted_row, (size_t)nnz * is) ||
+                        overlaps(grad_weight, (size_t)nnz * 4, X, X ? (size_t)(num_x_rows * F) * es : 0)))
         return fail(GEOT_ERROR_INVALID_VALUE, "grad_weight overlaps an input");
     if (!grad_X && !grad_weight) return GEOT_SUCCESS;
+    // widest vector that F and every pointer allow (fp32 operands: 16-byte loads of 4; 16-bit X
+    // also 8 elements, loaded as 16 bytes)
     const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)X | (uintptr_t)grad_X | (uintptr_t)out;
-    const int V = (F % 4 == 0 && (ptrs & 15) == 0) ? 4 : ((F % 2 == 0 && (ptrs & 7) == 0) ? 2 : 1);
+    int V = 1;
+    if (es == 2 && F % 8 == 0 && (ptrs & 15) == 0) V = 8;
+    else if (F % 4 == 0 && (ptrs & 15) == 0) V = 4;
+    else if (F % 2 == 0 && (ptrs & 7) == 0) V = 2;
     // temporaries from the stream-ordered pool (the forward call below uses the per-stream buffer):
     // row starts (mean), max recipients (max), the transposed edge list (grad_X for sum and mean)
     const bool mean = op == GEOT_OP_MEAN, mx = op == GEOT_OP_MAX;
@@ -843,7 +856,12 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
         s = stream_scratch(0, st, &unused, &gaps, &ctx);
         if (s != GEOT_SUCCESS) return s;
         s = poison(ctx, [&]() -> geot_status_t {
-            GEOT_HIP(launch_offsets(sorted_row, nnz, num_rows, roff, gaps, st), "launch offsets kernel");
+            if (idx32)
+                GEOT_HIP(launch_offsets_i32(static_cast<const int32_t *>(sorted_row), nnz, num_rows, roff, gaps, st),
+                         "launch offsets kernel");
+            else
+                GEOT_HIP(launch_offsets(static_cast<const int64_t *>(sorted_row), nnz, num_rows, roff, gaps, st),
+                         "launch offsets kernel");
             GEOT_HIP(launch_gap_fill_i64(roff, num_rows + 1, gaps, st), "launch gap fill kernel");
             return GEOT_SUCCESS;
         }());
@@ -851,8 +869,8 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     }
     const int bop = op == GEOT_OP_SUM ? GEOT_BWD_SUM : (mean ? GEOT_BWD_MEAN : GEOT_BWD_MAX);
     // weights (and, for max, X through atomic adds of the recipients only)
-    GEOT_HIP(launch_gs_bwd(X, num_x_rows, col, weight, sorted_row, roff, out, grad_out, nnz, num_rows, F,
-                           V, bop, arg, mx ? grad_X : nullptr, grad_weight, st),
+    GEOT_HIP(launch_gs_bwd(X, elem, num_x_rows, col, idx32, weight, sorted_row, roff, out, grad_out, nnz, num_rows,
+                           F, V, bop, arg, mx ? grad_X : nullptr, grad_weight, st),
              "launch fused backward kernels");
     if (transpose) {
         // grad_X = gather_scatter of grad_out over the edges sorted by col (sum of coef * grad_out rows)
@@ -860,7 +878,7 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
         int64_t *row_t = packed ? nullptr : (int64_t *)(base + o_row);
         float *w_t = packed ? nullptr : (float *)(base + o_w);
         int32_t *rec = packed ? (int32_t *)(base + o_rec) : nullptr;
-        GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
+        GEOT_HIP(launch_transpose(col, nx, sorted_row, idx32, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                                   (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, rec,
                                   bucket_b ? base + o_bucket : nullptr, st),
                  "launch transpose kernels");
@@ -888,6 +906,15 @@ geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, c
     void *p_free = sg.p;
     sg.p = nullptr;
     return scratch_free(p_free, st);
+}
+
+geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,
+                                           const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                           int64_t num_rows, int64_t F, geot_op_t op,
+                                           const float *grad_out, const float *out, float *grad_X,
+                                           float *grad_weight, void *stream) {
+    return geot_gather_scatter_backward_typed(X, GEOT_DTYPE_F32, num_x_rows, col, weight, sorted_row, GEOT_INDEX_I64,
+                                              nnz, num_rows, F, op, grad_out, out, grad_X, grad_weight, stream);
 }
 
 geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,
@@ -949,7 +976,7 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
         }());
         if (s != GEOT_SUCCESS) return s;
     }
-    GEOT_HIP(launch_transpose(col, nx, sorted_row, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
+    GEOT_HIP(launch_transpose(col, nx, sorted_row, 0, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                               (int64_t *)(base + o_off), (int64_t *)(base + o_sums), sorted_col_out, row_out,
                               coef_out, rec, bucket_b ? base + o_bucket : nullptr, st),
              "launch transpose kernels");

@@ -280,11 +280,11 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
 
 // fused form, max: arg[r, f] = min edge e of row r whose rounded product equals out[r, f].
 // Ids of all passes first, then every pass's X and output vectors, then the compares.
-template <int V>
-__global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__restrict__ X, int64_t nx,
-                                                             const int64_t *__restrict__ col,
+template <int E, typename I, int V>
+__global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
+                                                             const I *__restrict__ col,
                                                              const float *__restrict__ w,
-                                                             const int64_t *__restrict__ row,
+                                                             const I *__restrict__ row,
                                                              const float *__restrict__ out, int64_t n, int64_t R,
                                                              int64_t F, unsigned long long *arg) {
     const int nvec = (int)(F / V);
@@ -294,8 +294,8 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = m.row(q);
-        rr[q] = e < n ? row[e] : -1;
-        cc[q] = e < n ? col[e] : -1;
+        rr[q] = e < n ? (int64_t)row[e] : -1;
+        cc[q] = e < n ? (int64_t)col[e] : -1;
         wt[q] = e < n && w ? w[e] : 1.0f;
     }
     if (nvec <= m.tpr) {
@@ -316,16 +316,18 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
                 s_row[q * m.rows + m.rsub] = m.row(q) < n ? rr[q] : INT64_MAX;
         }
         const bool has_prev = e0 > 0, has_next = e0 + slots < n;
-        const int64_t prev_row = has_prev ? row[e0 - 1] : 0;
-        const int64_t next_row = has_next ? row[e0 + slots] : 0;
+        const int64_t prev_row = has_prev ? (int64_t)row[e0 - 1] : 0;
+        const int64_t next_row = has_next ? (int64_t)row[e0 + slots] : 0;
         float x[kPasses][V], o[kPasses][V];
         bool ok[kPasses];
 #pragma unroll
         for (int q = 0; q < kPasses; ++q) {
             ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx && m.j0 < nvec;
             if (ok[q]) {
-                load_vec<V>(X + cc[q] * F + (int64_t)m.j0 * V, x[q]);
-                load_vec<V>(out + rr[q] * F + (int64_t)m.j0 * V, o[q]);
+                Raw<E, V> rx;
+                load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx);
+                widen<E, V>(rx, x[q]);
+                load_f32<V>(out + rr[q] * F + (int64_t)m.j0 * V, o[q]);
             }
         }
         __syncthreads();
@@ -375,8 +377,10 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
         if (e >= n || (uint64_t)r >= (uint64_t)R || (uint64_t)c >= (uint64_t)nx) continue;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V], o[V];
-            load_vec<V>(X + c * F + (int64_t)j * V, x);
-            load_vec<V>(out + r * F + (int64_t)j * V, o);
+            Raw<E, V> rx;
+            load_raw<E, V>(X + c * F + (int64_t)j * V, rx);
+            widen<E, V>(rx, x);
+            load_f32<V>(out + r * F + (int64_t)j * V, o);
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 const float t = w ? wt[q] * x[k] : x[k];
@@ -389,9 +393,9 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const float *__rest
 // fused form, max, w.r.t. X: one thread per V-vector of a row r of the recipients; for each
 // (r, f) with a recipient edge e, grad_X[col[e], f] += coef(e) * grad_out[r, f]. Walks the
 // R * F recipients once (arg and grad_out stream) instead of every edge's row of them.
-template <int V>
+template <typename I, int V>
 __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long long *__restrict__ arg,
-                                                           const int64_t *__restrict__ col, int64_t nx,
+                                                           const I *__restrict__ col, int64_t nx,
                                                            const float *__restrict__ w,
                                                            const float *__restrict__ gout, int64_t n,
                                                            int64_t R, int64_t F, float *gX) {
@@ -403,13 +407,13 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long l
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float g[V];
             unsigned long long a[V];
-            load_vec<V>(gout + r * F + (int64_t)j * V, g);
+            load_f32<V>(gout + r * F + (int64_t)j * V, g);
 #pragma unroll
             for (int k = 0; k < V; ++k) a[k] = arg[r * F + (int64_t)j * V + k];
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 if (a[k] >= (unsigned long long)n) continue;  // no recipient (empty row)
-                const int64_t c = col[a[k]];
+                const int64_t c = (int64_t)col[a[k]];
                 if ((uint64_t)c >= (uint64_t)nx) continue;
                 const float coef = w ? w[a[k]] : 1.0f;
                 unsafeAtomicAdd(gX + c * F + (int64_t)j * V + k, coef * g[k]);
@@ -422,10 +426,10 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long l
 // mean divides afterwards, in scale_by_count_kernel). Every thread runs all passes (the group
 // reduction is uniform); the edges' ids load first, then both operand rows of every pass, then
 // the products.
-template <int V, int OP>
-__global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__ X, int64_t nx,
-                                                       const int64_t *__restrict__ col,
-                                                       const int64_t *__restrict__ row,
+template <int E, typename I, int V, int OP>
+__global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
+                                                       const I *__restrict__ col,
+                                                       const I *__restrict__ row,
                                                        const unsigned long long *__restrict__ arg,
                                                        const float *__restrict__ gout, int64_t n, int64_t R,
                                                        int64_t F, float *__restrict__ gw) {
@@ -436,8 +440,8 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = m.row(q);
-        rr[q] = e < n ? row[e] : -1;
-        cc[q] = e < n ? col[e] : -1;
+        rr[q] = e < n ? (int64_t)row[e] : -1;
+        cc[q] = e < n ? (int64_t)col[e] : -1;
     }
 #pragma unroll
     for (int q = 0; q < kPasses; ++q)
@@ -449,8 +453,10 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
 #pragma unroll
         for (int q = 0; q < kPasses; ++q) {
             if (ok[q] && m.j0 < nvec) {
-                load_vec<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
-                load_vec<V>(X + cc[q] * F + (int64_t)m.j0 * V, x[q]);
+                load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
+                Raw<E, V> rx;
+                load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx);
+                widen<E, V>(rx, x[q]);
             } else {
 #pragma unroll
                 for (int k = 0; k < V; ++k) g[q][k] = x[q][k] = 0.0f;
@@ -490,8 +496,10 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
             const int64_t e = m.row(q);
             for (int j = m.j0; j < nvec; j += m.tpr) {
                 float g[V], x[V];
-                load_vec<V>(gout + rr[q] * F + (int64_t)j * V, g);
-                load_vec<V>(X + cc[q] * F + (int64_t)j * V, x);
+                load_f32<V>(gout + rr[q] * F + (int64_t)j * V, g);
+                Raw<E, V> rx;
+                load_raw<E, V>(X + cc[q] * F + (int64_t)j * V, rx);
+                widen<E, V>(rx, x);
 #pragma unroll
                 for (int k = 0; k < V; ++k) {
                     if (OP == GEOT_BWD_MAX && arg[rr[q] * F + (int64_t)j * V + k] != (unsigned long long)e) continue;
@@ -515,13 +523,14 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const float *__restrict__
 // kernel the row starts either waited after the reduction (one more memory latency per
 // block) or held registers through it (5 waves per SIMD instead of 7); both cost C4 1.5 ms,
 // this pass about 0.2. Rows of all passes load first, then their starts and the values.
-__global__ __launch_bounds__(256) void scale_by_count_kernel(float *__restrict__ gw, const int64_t *__restrict__ row,
+template <typename I>
+__global__ __launch_bounds__(256) void scale_by_count_kernel(float *__restrict__ gw, const I *__restrict__ row,
                                                              const int64_t *__restrict__ off, int64_t n, int64_t R) {
     int64_t r[kPasses];
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
-        r[q] = e < n ? row[e] : -1;
+        r[q] = e < n ? (int64_t)row[e] : -1;
     }
     float v[kPasses], c[kPasses];
 #pragma unroll
@@ -541,12 +550,13 @@ __global__ __launch_bounds__(256) void scale_by_count_kernel(float *__restrict__
 
 // ---- counting sort of the edges by source row (the transposed problem) ----
 // both edge passes: block b takes edges [b, b + 1) * 256 * kPasses, one pass of 256 at a time
-__global__ __launch_bounds__(256) void hist_kernel(const int64_t *col, int64_t n, int64_t nx,
+template <typename I>
+__global__ __launch_bounds__(256) void hist_kernel(const I *col, int64_t n, int64_t nx,
                                                    unsigned *counts) {
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
         if (e >= n) break;
-        const int64_t c = col[e];
+        const int64_t c = (int64_t)col[e];
         if ((uint64_t)c < (uint64_t)nx) atomicAdd(counts + c, 1u);
     }
 }
@@ -617,18 +627,18 @@ __global__ __launch_bounds__(256) void scan_add_kernel(int64_t *off, int64_t n, 
 // transposed problem's segment id (col), gather row (row) and coefficient,
 // as three arrays or as one 16-byte record (one store per edge: the slots are
 // random, and every store touches its own cache line)
-template <bool PACKED>
-__global__ __launch_bounds__(256) void place_kernel(const int64_t *col, int64_t nx, const int64_t *row,
+template <bool PACKED, typename I>
+__global__ __launch_bounds__(256) void place_kernel(const I *col, int64_t nx, const I *row,
                                                     const float *w, const int64_t *roff, int64_t nrows, int mean,
                                                     int64_t n, const int64_t *off, unsigned *cursor,
                                                     int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec) {
     for (int q = 0; q < kPasses; ++q) {
         const int64_t e = ((int64_t)blockIdx.x * kPasses + q) * 256 + threadIdx.x;
         if (e >= n) break;
-        const int64_t c = col[e];
+        const int64_t c = (int64_t)col[e];
         if ((uint64_t)c >= (uint64_t)nx) continue;
         const int64_t pos = off[c] + (int64_t)atomicSub(cursor + c, 1u) - 1;
-        const int64_t r = row[e];
+        const int64_t r = (int64_t)row[e];
         float coef = w ? w[e] : 1.0f;
         if (mean && (uint64_t)r < (uint64_t)nrows) coef = coef / (float)(roff[r + 1] - roff[r]);
         if constexpr (PACKED) {
@@ -655,7 +665,8 @@ constexpr int kBucketCols = 2048;  // columns per bucket sorted in LDS
 constexpr int64_t kBucketMinEdges = 1 << 20;  // below this the direct transposition is as fast
 
 // counts of the block's edges per bucket, bucket-major: bcnt[b * nblk + block]
-__global__ __launch_bounds__(256) void bucket_count_kernel(const int64_t *col, int64_t n, int64_t nx, int shift,
+template <typename I>
+__global__ __launch_bounds__(256) void bucket_count_kernel(const I *col, int64_t n, int64_t nx, int shift,
                                                            int nbuckets, int64_t nblk, unsigned *bcnt) {
     __shared__ unsigned h[kMaxBuckets];
     for (int b = threadIdx.x; b < nbuckets; b += 256) h[b] = 0;
@@ -664,7 +675,7 @@ __global__ __launch_bounds__(256) void bucket_count_kernel(const int64_t *col, i
     for (int k = 0; k < kBucketChunk / 256; ++k) {
         const int64_t e = e0 + (int64_t)k * 256 + threadIdx.x;
         if (e >= n) break;
-        const int64_t c = col[e];
+        const int64_t c = (int64_t)col[e];
         if ((uint64_t)c < (uint64_t)nx) atomicAdd(&h[(int)(c >> shift)], 1u);
     }
     __syncthreads();
@@ -679,7 +690,8 @@ __global__ void scan_total_kernel(const int64_t *off, const unsigned *cnt, int64
 // the block's edges as 16-byte records {col, row, coefficient, 0} into bucket order; the
 // cursors hold absolute record positions (n < 2^32 on this path). Each thread loads kU
 // edges before it places them.
-__global__ __launch_bounds__(256) void bucket_scatter_kernel(const int64_t *col, int64_t nx, const int64_t *row,
+template <typename I>
+__global__ __launch_bounds__(256) void bucket_scatter_kernel(const I *col, int64_t nx, const I *row,
                                                              const float *w, const int64_t *roff, int64_t nrows,
                                                              int mean, int64_t n, int shift, int nbuckets, int64_t nblk,
                                                              const int64_t *boff, int32_t *tmp) {
@@ -696,8 +708,8 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const int64_t *col,
         for (int u = 0; u < kU; ++u) {
             const int64_t e = b0 + u * 256 + threadIdx.x;
             const bool in = e < e1;
-            c[u] = in ? col[e] : -1;
-            r[u] = in ? row[e] : 0;
+            c[u] = in ? (int64_t)col[e] : -1;
+            r[u] = in ? (int64_t)row[e] : 0;
             wt[u] = in && w ? w[e] : 1.0f;
         }
 #pragma unroll
@@ -883,7 +895,8 @@ size_t transpose_scratch_bytes(int64_t n, int64_t nx) {
 
 namespace {
 
-hipError_t launch_transpose_bucketed(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
+template <typename I>
+hipError_t launch_transpose_bucketed(const I *col, int64_t nx, const I *row, const float *w,
                                      const int64_t *roff, int64_t nrows, bool mean, int64_t n, int64_t *key_t, int64_t *row_t,
                                      float *w_t, int32_t *rec, char *scratch, hipStream_t st) {
     int shift, nb;
@@ -896,13 +909,14 @@ hipError_t launch_transpose_bucketed(const int64_t *col, int64_t nx, const int64
     int64_t *total = (int64_t *)((char *)bsums + a256((size_t)((len + kScanTile - 1) / kScanTile + 1) * 8));
     int32_t *tmp = (int32_t *)((char *)total + a256(64));
     if (nblk > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(bucket_count_kernel, dim3((unsigned)nblk), dim3(256), 0, st, col, n, nx, shift, nb, nblk, bcnt);
+    hipLaunchKernelGGL(bucket_count_kernel<I>, dim3((unsigned)nblk), dim3(256), 0, st, col, n, nx, shift, nb, nblk,
+                       bcnt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = scan_counts(bcnt, len, boff, bsums, 0, st)) != hipSuccess) return e;
     hipLaunchKernelGGL(scan_total_kernel, dim3(1), dim3(64), 0, st, boff, bcnt, len, total);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bucket_scatter_kernel, dim3((unsigned)nblk), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+    hipLaunchKernelGGL(bucket_scatter_kernel<I>, dim3((unsigned)nblk), dim3(256), 0, st, col, nx, row, w, roff, nrows,
                        mean ? 1 : 0, n, shift, nb, nblk, boff, tmp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (rec)
@@ -914,13 +928,11 @@ hipError_t launch_transpose_bucketed(const int64_t *col, int64_t nx, const int64
     return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
-                            const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
-                            int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                            char *bucket_scratch, hipStream_t st) {
-    if (n <= 0 || nx <= 0) return hipSuccess;
+template <typename I>
+hipError_t launch_transpose_t(const I *col, int64_t nx, const I *row, const float *w,
+                              const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
+                              int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
+                              char *bucket_scratch, hipStream_t st) {
     if (bucket_scratch && transpose_scratch_bytes(n, nx) > 0)
         return launch_transpose_bucketed(col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec, bucket_scratch,
                                          st);
@@ -929,18 +941,32 @@ hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, 
     const int64_t geb = (n + 256 * kPasses - 1) / (256 * kPasses);
     if (geb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned ge = (unsigned)geb;
-    hipLaunchKernelGGL(hist_kernel, dim3(ge), dim3(256), 0, st, col, n, nx, counts);
+    hipLaunchKernelGGL(hist_kernel<I>, dim3(ge), dim3(256), 0, st, col, n, nx, counts);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = scan_counts(counts, nx, off, sums, n, st)) != hipSuccess) return e;
     if (rec)
-        hipLaunchKernelGGL(place_kernel<true>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+        hipLaunchKernelGGL((place_kernel<true, I>), dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
                            mean ? 1 : 0, n,
                            off, counts, key_t, row_t, w_t, rec);
     else
-        hipLaunchKernelGGL(place_kernel<false>, dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
+        hipLaunchKernelGGL((place_kernel<false, I>), dim3(ge), dim3(256), 0, st, col, nx, row, w, roff, nrows,
                            mean ? 1 : 0,
                            n, off, counts, key_t, row_t, w_t, rec);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int idx32, const float *w,
+                            const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
+                            int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
+                            char *bucket_scratch, hipStream_t st) {
+    if (n <= 0 || nx <= 0) return hipSuccess;
+    if (idx32)
+        return launch_transpose_t(static_cast<const int32_t *>(col), nx, static_cast<const int32_t *>(row), w, roff,
+                                  nrows, mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
+    return launch_transpose_t(static_cast<const int64_t *>(col), nx, static_cast<const int64_t *>(row), w, roff, nrows,
+                              mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
 }
 
 hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t *row_t, float *w_t,
@@ -960,12 +986,6 @@ hipError_t launch_fill_u64(unsigned long long *p, int64_t n, unsigned long long 
     return hipGetLastError();
 }
 
-#define GEOT_BY_V(V, CALL)                   \
-    do {                                     \
-        if ((V) == 4) { constexpr int VV = 4; CALL; } \
-        else if ((V) == 2) { constexpr int VV = 2; CALL; } \
-        else { constexpr int VV = 1; CALL; } \
-    } while (0)
 
 namespace {
 
@@ -1046,52 +1066,58 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
     });
 }
 
-hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const float *w, const int64_t *row,
-                         const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw,
-                         hipStream_t st) {
+hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
+                         const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
+                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
-    hipError_t e;
-    if (op == GEOT_BWD_MAX) {
-        e = launch_fill_u64(arg, R * F, ~0ull, st);
-        if (e != hipSuccess) return e;
-        GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_max_arg_kernel<VV>), dim3(g), dim3(256), 0, st, X, nx,
-                                        col, w, row, out, n, R, F, arg));
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (gX) {  // max only (sum and mean gather over the transposed list)
-        if (op != GEOT_BWD_MAX) return hipErrorInvalidValue;
-        e = launch_fill(gX, nx, F, F, 0.0f, st);
-        if (e != hipSuccess) return e;
-        const int64_t gr = grid_rows(R, (int)(F / V));
-        if (gr > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-        GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_x_max_kernel<VV>), dim3((unsigned)gr), dim3(256), 0, st, arg, col,
-                                        nx, w, gout, n, R, F, gX));
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    if (gw) {
-        if (op == GEOT_BWD_SUM || op == GEOT_BWD_MEAN)
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st,
-                                            X, nx, col, row, arg, gout, n, R, F, gw));
-        else
-            GEOT_BY_V(V, hipLaunchKernelGGL((gs_bwd_w_kernel<VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st,
-                                            X, nx, col, row, arg, gout, n, R, F, gw));
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        if (op == GEOT_BWD_MEAN) {
-            const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
-            if (sb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-            hipLaunchKernelGGL(scale_by_count_kernel, dim3((unsigned)sb), dim3(256), 0, st, gw, row, off, n, R);
-            e = hipGetLastError();
-            if (e != hipSuccess) return e;
-        }
-    }
-    return hipSuccess;
+    return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
+        constexpr int E = decltype(et)::value;
+        using I = typename decltype(it)::type;
+        using T = typename ElemT<E>::T;
+        const T *Xt = static_cast<const T *>(X);
+        const I *ct = static_cast<const I *>(col), *rt = static_cast<const I *>(row);
+        return by_width<E>(V, [&](auto vt) -> hipError_t {
+            constexpr int VV = decltype(vt)::value;
+            hipError_t e;
+            if (op == GEOT_BWD_MAX) {
+                e = launch_fill_u64(arg, R * F, ~0ull, st);
+                if (e != hipSuccess) return e;
+                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, Xt, nx, ct, w, rt,
+                                   out, n, R, F, arg);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
+            if (gX) {  // max only (sum and mean gather over the transposed list)
+                if (op != GEOT_BWD_MAX) return hipErrorInvalidValue;
+                e = launch_fill(gX, nx, F, F, 0.0f, st);
+                if (e != hipSuccess) return e;
+                const int64_t gr = grid_rows(R, (int)(F / VV));
+                if (gr > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                hipLaunchKernelGGL((gs_bwd_x_max_kernel<I, VV>), dim3((unsigned)gr), dim3(256), 0, st, arg, ct, nx,
+                                   w, gout, n, R, F, gX);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
+            if (gw) {
+                if (op == GEOT_BWD_MAX)
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st, Xt, nx,
+                                       ct, rt, arg, gout, n, R, F, gw);
+                else
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st, Xt, nx,
+                                       ct, rt, arg, gout, n, R, F, gw);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+                if (op == GEOT_BWD_MEAN) {
+                    const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
+                    if (sb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                    hipLaunchKernelGGL(scale_by_count_kernel<I>, dim3((unsigned)sb), dim3(256), 0, st, gw, rt, off,
+                                       n, R);
+                    if ((e = hipGetLastError()) != hipSuccess) return e;
+                }
+            }
+            return hipSuccess;
+        });
+    });
 }
 
 }  // namespace geot

@@ -154,7 +154,8 @@ hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t 
 // bucket_scratch (transpose_scratch_bytes(n, nx) bytes, or nullptr) lets large inputs group the
 // edges by buckets of columns and sort each bucket in LDS (no global atomic per edge); counts,
 // off and sums are then unused.
-hipError_t launch_transpose(const int64_t *col, int64_t nx, const int64_t *row, const float *w,
+// col and row are int32 when idx32, else int64.
+hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int idx32, const float *w,
                             const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                             int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
                             char *bucket_scratch, hipStream_t st);
@@ -175,10 +176,10 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);
-// off = row starts (mean), arg [R x F] scratch (max).
-hipError_t launch_gs_bwd(const float *X, int64_t nx, const int64_t *col, const float *w, const int64_t *row,
-                         const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw,
-                         hipStream_t st);
+// off = row starts (mean), arg [R x F] scratch (max). X of ElemType elem, col and row int32
+// when idx32.
+hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
+                         const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
+                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw, hipStream_t st);
 
 }  // namespace geot

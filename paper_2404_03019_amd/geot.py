@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
     L.geot_segment_reduce_backward_typed.argtypes = [p, p, ctypes.c_int, i64, i64, i64, ctypes.c_int, p,
                                                      ctypes.c_int, p, p, p]
     L.geot_gather_scatter_backward.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, p, p, p]
+    L.geot_gather_scatter_backward_typed.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64, i64,
+                                                     ctypes.c_int, p, p, p, p, p]
     L.geot_transpose_edges.argtypes = [p, i64, p, p, i64, i64, ctypes.c_int, p, p, p, p]
     L.geot_last_choice.argtypes = [pc]
     L.geot_release_scratch.argtypes = []
@@ -263,10 +265,13 @@ def gather_scatter_backward(x: torch.Tensor, col: torch.Tensor, weight: torch.Te
                             row: torch.Tensor, grad_out: torch.Tensor, reduce: str = "sum",
                             out: torch.Tensor | None = None, need_x: bool = True,
                             need_weight: bool = True):
-    """(grad_x or None, grad_weight or None) of gather_scatter (geot_gather_scatter_backward)."""
-    _dev(x, "x", torch.float32, 2)
-    _dev(col, "col", torch.int64, 1)
-    _dev(row, "row", torch.int64, 1)
+    """(grad_x or None, grad_weight or None) of gather_scatter (geot_gather_scatter_backward_typed).
+
+    x may be fp32, bf16 or fp16 and col / row int64 or int32 (the same type); grad_x and
+    grad_weight are fp32."""
+    _dev(x, "x", tuple(DTYPES), 2)
+    _dev(col, "col", tuple(INDEX_TYPES), 1)
+    _dev(row, "row", (col.dtype,), 1)
     _dev(grad_out, "grad_out", torch.float32, 2)
     if weight is not None:
         _dev(weight, "weight", torch.float32, 1)
@@ -275,12 +280,13 @@ def gather_scatter_backward(x: torch.Tensor, col: torch.Tensor, weight: torch.Te
             raise ValueError("max needs out")
         _dev(out, "out", torch.float32, 2)
     R, F = grad_out.shape
-    gx = torch.empty_like(x) if need_x else None
+    gx = torch.empty(x.shape, dtype=torch.float32, device=x.device) if need_x else None
     gw = torch.empty_like(weight) if (need_weight and weight is not None) else None
     with _OnDevice(x.device):
-        st = lib().geot_gather_scatter_backward(
-            x.data_ptr(), x.shape[0], col.data_ptr(), weight.data_ptr() if weight is not None else None,
-            row.data_ptr(), row.numel(), R, F, OPS[reduce], grad_out.data_ptr(),
+        st = lib().geot_gather_scatter_backward_typed(
+            x.data_ptr(), DTYPES[x.dtype], x.shape[0], col.data_ptr(),
+            weight.data_ptr() if weight is not None else None, row.data_ptr(), INDEX_TYPES[col.dtype],
+            row.numel(), R, F, OPS[reduce], grad_out.data_ptr(),
             out.data_ptr() if out is not None else None, gx.data_ptr() if gx is not None else None,
             gw.data_ptr() if gw is not None else None, _stream(x.device))
     _raise(st)

@@ -253,3 +253,67 @@ def test_segment_backward_typed_through_autograd():
         outf.backward(g)
         # both paths form the same fp32 values (mean: the same products); bf16 rounds them once
         assert torch.equal(x.grad, xf.grad.to(torch.bfloat16)), op
+
+
+GS_BWD_CASES = [
+    # seed, nnz, R, n_x, F, dist, values, weighted
+    (51, 20000, 1200, 900, 32, "zipf", "normal", True),     # 8-wide 16-bit vectors
+    (52, 15000, 800, 2000, 3, "lognormal", "normal", True),  # 1-wide
+    (53, 10000, 500, 700, 12, "uniform", "int", False),      # 4-wide; ties under max
+    (54, 8000, 300, 400, 6, "one_heavy", "int", True),       # 2-wide
+]
+
+
+@pytest.mark.parametrize("dt,it", [("bf16", "i32"), ("bf16", "i64"), ("f16", "i32"), ("f32", "i32")])
+@pytest.mark.parametrize("case", GS_BWD_CASES, ids=lambda c: f"seed{c[0]}_F{c[4]}")
+def test_gather_backward_typed(dt, it, case):
+    """16-bit X and int32 ids: the gradients (fp32) equal the oracle's on the widened X within
+    the fp32 bound, max routing to the same recipients."""
+    seed, nnz, R, nx, F, dist, values, weighted = case
+    q = random_gather_problem(seed, nnz, R, nx, F, dist, values, weighted, 0.05)
+    t, wide = stored(q["X"], dt)
+    X = t.to(DEV)
+    col, row = ids(q["col"], it), ids(q["index"], it)
+    w = torch.from_numpy(q["weight"]).to(DEV) if q["weight"] is not None else None
+    g = np.random.default_rng(seed).standard_normal((R, F)).astype(np.float32)
+    for op in OPS:
+        say(f"typed gather backward {dt}/{it} seed={seed} F={F} {op}")
+        out = geot.gather_scatter(X, col, w, row, R, op)
+        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, out)
+        assert gx.dtype == torch.float32
+        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy())
+        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy(),
+                                                absolute=True)
+        for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
+            if got is None:
+                assert not weighted and what == "grad_w"
+                continue
+            err = np.abs(got.cpu().numpy().astype(np.float64) - ref.astype(np.float64))
+            assert np.all(err <= 1e-5 * terms + 1e-6), f"{what} {dt}/{it} seed={seed} {op}"
+
+
+@pytest.mark.parametrize("op", OPS)
+def test_gather_autograd_bf16_int32(op):
+    """The differentiable fused form over bf16 x and int32 ids, with a Graph (its int32 ids
+    widened for the transposition) and without: x.grad keeps bf16 and equals, within one
+    bf16 rounding, the gradient of the same expression on the widened x with int64 ids;
+    the weight gradient meets the fp32 bound."""
+    from paper_2404_03019_amd.autograd import Graph, gather_scatter
+    q = random_gather_problem(56, 30000, 2000, 1500, 16, "zipf", "normal", True, 0.02)
+    x16, wide = stored(q["X"], "bf16")
+    t = torch.from_numpy(np.random.default_rng(57).standard_normal((2000, 16)).astype(np.float32)).to(DEV)
+    grads = {}
+    for name, xin, it in (("bf16", x16.to(DEV), "i32"), ("f32", torch.from_numpy(wide).to(DEV), "i64")):
+        for use_graph in (False, True):
+            x = xin.clone().requires_grad_(True)
+            w = torch.from_numpy(q["weight"]).to(DEV).requires_grad_(True)
+            col, row = ids(q["col"], it), ids(q["index"], it)
+            graph = Graph(col, row, 2000, w, num_src=1500) if use_graph else None
+            (gather_scatter(x, col, w, row, 2000, op, graph) * t).sum().backward()
+            assert x.grad.dtype == xin.dtype
+            grads[name, use_graph] = (x.grad.float(), w.grad)
+    for use_graph in (False, True):
+        xb, wb = grads["bf16", use_graph]
+        xf, wf = grads["f32", use_graph]
+        assert torch.allclose(xb, xf.to(torch.bfloat16).float(), rtol=2 ** -7, atol=1e-5), (op, use_graph)
+        assert torch.allclose(wb, wf, rtol=1e-4, atol=1e-5), (op, use_graph)
