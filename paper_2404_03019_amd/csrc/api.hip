@@ -452,6 +452,9 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // blocks that write the gap list, as a pass of their own or riding on the final partial level
 constexpr int kFoldedGapBlocks = 1024;
+// segment sum and max gradients from this many bytes of grad_src take the offsets pass first
+// (below, the kernels read the ids, which saves two launches)
+constexpr size_t kBcastOffsetsMinBytes = (size_t)64 << 20;
 
 geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
                             char *base, const std::vector<size_t> &off_v,
@@ -708,35 +711,54 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
     hipStream_t st = (hipStream_t)stream;
     void *scratch = nullptr;
     StreamCtx *ctx = nullptr;
-    if (op == GEOT_OP_MAX) {
-        geot_status_t s = stream_scratch((size_t)(num_segments * F) * 8, st, &scratch, nullptr, &ctx);
-        if (s != GEOT_SUCCESS) return s;
-        GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, nnz, num_segments, F, V, elem,
-                                    (unsigned long long *)scratch, grad_src, st),
-                 "launch max backward kernels");
-        return GEOT_SUCCESS;
-    }
-    if (op == GEOT_OP_SUM) {
-        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, nullptr, nnz, num_segments, F, V, elem, false,
-                                      grad_src, st),
-                 "launch backward kernel");
-        return GEOT_SUCCESS;
-    }
+    const bool mean = op == GEOT_OP_MEAN, mx = op == GEOT_OP_MAX;
+    // From kBcastOffsetsMinBytes (and always for mean, which needs the lengths) an offsets pass
+    // reads the ids once and keeps each block's first and last ids; the kernels that write
+    // grad_src then take every row's segment from the offsets, so that their only HBM stream is
+    // their stores. Below, the ids are read where they are needed (two launches fewer).
+    const bool from_off = mean || gb >= kBcastOffsetsMinBytes;
+    const size_t o_arg = 0, arg_b = mx ? align256((size_t)(num_segments * F) * 8) : 0;
+    const size_t o_off = o_arg + arg_b, o_first = o_off + (from_off ? align256((size_t)(num_segments + 1) * 8) : 0);
+    const int64_t blocks = seg_bwd_blocks(nnz, F, V);
     GapList gaps;
-    geot_status_t s = stream_scratch((size_t)(num_segments + 1) * 8, st, &scratch, &gaps, &ctx);
-    if (s != GEOT_SUCCESS) return s;
-    int64_t *off = (int64_t *)scratch;
+    if (mx || from_off) {
+        geot_status_t s = stream_scratch(o_first + (from_off ? (size_t)blocks * 16 : 0), st, &scratch,
+                                         from_off ? &gaps : nullptr, &ctx);
+        if (s != GEOT_SUCCESS) return s;
+    }
+    unsigned long long *arg = mx ? (unsigned long long *)scratch : nullptr;
+    int64_t *off = from_off ? (int64_t *)((char *)scratch + o_off) : nullptr;
+    int64_t *first = from_off ? (int64_t *)((char *)scratch + o_first) : nullptr;
+    if (!from_off) {
+        if (mx)
+            GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, nullptr, nullptr, nnz, num_segments,
+                                        F, V, elem, arg, grad_src, st),
+                     "launch max backward kernels");
+        else
+            GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, nullptr, nullptr, nnz, num_segments, F, V,
+                                          elem, false, grad_src, st),
+                     "launch backward kernel");
+        return GEOT_SUCCESS;
+    }
+    const int shift = seg_bwd_rows_log2(F, V);
     return poison(ctx, [&]() -> geot_status_t {
         if (idx32)
-            GEOT_HIP(launch_offsets_i32(static_cast<const int32_t *>(sorted_index), nnz, num_segments, off, gaps, st),
+            GEOT_HIP(launch_offsets_i32(static_cast<const int32_t *>(sorted_index), nnz, num_segments, off, gaps, st,
+                                        first, shift),
                      "launch offsets kernel");
         else
-            GEOT_HIP(launch_offsets(static_cast<const int64_t *>(sorted_index), nnz, num_segments, off, gaps, st),
+            GEOT_HIP(launch_offsets(static_cast<const int64_t *>(sorted_index), nnz, num_segments, off, gaps, st,
+                                    first, shift),
                      "launch offsets kernel");
         GEOT_HIP(launch_gap_fill_i64(off, num_segments + 1, gaps, st), "launch gap fill kernel");
-        GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, off, nnz, num_segments, F, V, elem, true,
-                                      grad_src, st),
-                 "launch backward kernel");
+        if (mx)
+            GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, off, first, nnz, num_segments, F, V,
+                                        elem, arg, grad_src, st),
+                     "launch max backward kernels");
+        else
+            GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, off, first, nnz, num_segments, F, V, elem,
+                                          mean, grad_src, st),
+                     "launch backward kernel");
         return GEOT_SUCCESS;
     }());
 }

@@ -19,10 +19,13 @@ __global__ __launch_bounds__(256) void fill_kernel(float *out, int64_t rows, int
 // off[s] = first row i with idx[i] >= s. Row i writes the starts of every
 // segment in (idx[i-1], idx[i]] (so empty segments get the next start), and
 // the last row also writes (idx[n-1], S] = n. Runs longer than kGapRun go to
-// the gap list instead (value = the row they start at).
+// the gap list instead (value = the row they start at). With `first`, the
+// ids of the first and the last row of every block of 2^shift rows go to
+// first[2b] and first[2b + 1] (the segments a block of the gradient kernels
+// starts and ends in).
 template <typename I>
 __global__ __launch_bounds__(256) void offsets_kernel(const I *idx, int64_t n, int64_t S,
-                                                      int64_t *off, GapList gaps) {
+                                                      int64_t *off, GapList gaps, int64_t *first, int shift) {
     auto put = [&](int64_t lo, int64_t hi, int64_t row) {  // off[lo, hi) = row
         lo = max(lo, (int64_t)0);
         hi = min(hi, S + 1);
@@ -35,6 +38,11 @@ __global__ __launch_bounds__(256) void offsets_kernel(const I *idx, int64_t n, i
         const int64_t sp = i > 0 ? (int64_t)idx[i - 1] : -1;
         if (s != sp) put(sp + 1, s + 1, i);
         if (i == n - 1) put(s + 1, S + 1, n);
+        if (first) {   // ids of the first and the last row of each block of 2^shift rows
+            const int64_t mask = ((int64_t)1 << shift) - 1;
+            if ((i & mask) == 0) first[2 * (i >> shift)] = s;
+            if ((i & mask) == mask || i == n - 1) first[2 * (i >> shift) + 1] = s;
+        }
     }
 }
 
@@ -134,18 +142,18 @@ hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float va
 }
 
 hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
-                          hipStream_t stream) {
-    if (n <= 0) return hipErrorInvalidValue;
+                          hipStream_t stream, int64_t *first, int shift) {
+    if (n <= 0 || shift < 0 || shift > 40) return hipErrorInvalidValue;
     hipLaunchKernelGGL(offsets_kernel<int64_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
-                       idx, n, S, off, gaps);
+                       idx, n, S, off, gaps, first, shift);
     return hipGetLastError();
 }
 
 hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
-                              hipStream_t stream) {
-    if (n <= 0) return hipErrorInvalidValue;
+                              hipStream_t stream, int64_t *first, int shift) {
+    if (n <= 0 || shift < 0 || shift > 40) return hipErrorInvalidValue;
     hipLaunchKernelGGL(offsets_kernel<int32_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
-                       idx, n, S, off, gaps);
+                       idx, n, S, off, gaps, first, shift);
     return hipGetLastError();
 }
 

@@ -121,6 +121,34 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
             o1[q] = off[s + 1];
         }
     }
+    if (nvec <= m.tpr) {
+        // one vector per thread and row: every pass's gradient row loads before the first store
+        // (one memory latency per block instead of one per pass)
+        if (m.j0 >= nvec) return;
+        float x[kPasses][V];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const bool ok = m.row(q) < n && (uint64_t)seg[q] < (uint64_t)S;
+            if (ok) {
+                load_f32<V>(gout + seg[q] * F + (int64_t)m.j0 * V, x[q]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) x[q][k] = 0.0f;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t i = m.row(q);
+            if (i >= n) break;
+            if (MEAN && (uint64_t)seg[q] < (uint64_t)S) {
+                const float inv = 1.0f / (float)(o1[q] - o0[q]);
+#pragma unroll
+                for (int k = 0; k < V; ++k) x[q][k] = x[q][k] * inv;
+            }
+            store_elems<E, V>(gsrc + i * F + (int64_t)m.j0 * V, x[q]);
+        }
+        return;
+    }
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
@@ -143,6 +171,125 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_kernel(const float *__restr
                 }
                 store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
             }
+        }
+    }
+}
+
+// Segments of a thread's rows taken from the offsets instead of the ids. The offsets pass
+// stores the ids of every block's first and last rows (first[2b], first[2b + 1]). A block that
+// lies in one segment needs nothing more; another stages off[first[2b] .. first[2b] + 255] in
+// LDS (s_off, 256 entries) and each row finds its segment there by binary search. A row past
+// the staged starts (a block with more than 255 segment ends) or in a block whose first id is
+// out of range reads its id. seg[q] is the segment of m.row(q) (-1 past the last row); with
+// MEAN, inv[q] is 1 / its length. Returns whether the block lies in one segment (then every
+// seg[q] of a row before n is the same). Holds a barrier where the block spans several segments
+// (a condition uniform over the block).
+template <typename I, bool MEAN>
+__device__ __forceinline__ bool segments_from_offsets(const RowMap &m, const I *__restrict__ idx,
+                                                      const int64_t *__restrict__ off,
+                                                      const int64_t *__restrict__ first, int64_t n, int64_t S,
+                                                      int64_t *s_off, int64_t (&seg)[kPasses],
+                                                      float (&inv)[kPasses]) {
+    constexpr int K = 256;
+    const longlong2 ends = *reinterpret_cast<const longlong2 *>(first + 2 * (int64_t)blockIdx.x);
+    const int64_t seg0 = ends.x;
+    const bool valid = (uint64_t)seg0 < (uint64_t)S;
+    const bool one = valid && ends.y == seg0;
+    if (one) {
+        float in = 1.0f;
+        if (MEAN) in = 1.0f / (float)(off[seg0 + 1] - off[seg0]);
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            seg[q] = m.row(q) < n ? seg0 : -1;
+            inv[q] = in;
+        }
+        return true;
+    }
+    if (valid) {
+        s_off[threadIdx.x] = off[min(seg0 + (int64_t)threadIdx.x, S)];
+        __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t i = m.row(q);
+        seg[q] = -1;
+        inv[q] = 1.0f;
+        if (i >= n) continue;
+        int p = K;   // first staged start above row i
+        if (valid) {
+            int lo = 1, hi = K;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (s_off[mid] > i) hi = mid;
+                else lo = mid + 1;
+            }
+            p = lo;
+        }
+        if (p < K) {
+            seg[q] = seg0 + p - 1;
+            if (MEAN) inv[q] = 1.0f / (float)(s_off[p] - s_off[p - 1]);
+        } else {
+            seg[q] = (int64_t)idx[i];
+            if (MEAN && (uint64_t)seg[q] < (uint64_t)S) inv[q] = 1.0f / (float)(off[seg[q] + 1] - off[seg[q]]);
+        }
+    }
+    return false;
+}
+
+// The broadcast gradient with the segments from the offsets. The offsets and the gradient rows
+// stay in cache, so the kernel's HBM traffic is its stores alone: the ids, 6 % of the bytes at
+// F = 32, read in among the stores, slowed the stream by a third.
+template <int E, typename I, int V, bool MEAN>
+__global__ __launch_bounds__(256) void seg_bwd_bcast_off_kernel(const float *__restrict__ gout,
+                                                                const I *__restrict__ idx,
+                                                                const int64_t *__restrict__ off,
+                                                                const int64_t *__restrict__ first, int64_t n,
+                                                                int64_t S, int64_t F,
+                                                                typename ElemT<E>::T *__restrict__ gsrc) {
+    __shared__ int64_t s_off[256];
+    const int nvec = (int)(F / V);
+    const RowMap m = row_map(nvec);
+    int64_t seg[kPasses];
+    float inv[kPasses];
+    if (segments_from_offsets<I, MEAN>(m, idx, off, first, n, S, s_off, seg, inv)) {
+        // one segment: each vector of its gradient row loads once for all the thread's rows
+        if (m.row(0) >= n) return;   // no row here (seg[0] is -1)
+        for (int j = m.j0; j < nvec; j += m.tpr) {
+            float x[V];
+            load_f32<V>(gout + seg[0] * F + (int64_t)j * V, x);
+            if (MEAN) {
+#pragma unroll
+                for (int k = 0; k < V; ++k) x[k] = x[k] * inv[0];
+            }
+#pragma unroll
+            for (int q = 0; q < kPasses; ++q) {
+                const int64_t i = m.row(q);
+                if (i >= n) break;
+                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
+            }
+        }
+        return;
+    }
+    for (int j = m.j0; j < nvec; j += m.tpr) {
+        float x[kPasses][V];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if ((uint64_t)seg[q] < (uint64_t)S) {
+                load_f32<V>(gout + seg[q] * F + (int64_t)j * V, x[q]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) x[q][k] = 0.0f;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t i = m.row(q);
+            if (i >= n) break;
+            if (MEAN) {
+#pragma unroll
+                for (int k = 0; k < V; ++k) x[q][k] = x[q][k] * inv[q];
+            }
+            store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[q]);
         }
     }
 }
@@ -194,6 +341,73 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename Ele
             float x[V], o[V];
             Raw<E, V> r;
             load_raw<E, V>(src + i * F + (int64_t)j * V, r);
+            widen<E, V>(r, x);
+            load_f32<V>(out + s * F + (int64_t)j * V, o);
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (unsigned long long)i);
+        }
+    }
+}
+
+// The recipients with the segments from the offsets (as the broadcast above). The rows of src
+// load first (non-temporal: each is read once), before the segments are known, so that the
+// stream does not wait for the segment lookup; the outputs they are compared with follow (once
+// per thread where the block lies in one segment).
+template <int E, typename I, int V>
+__global__ __launch_bounds__(256) void seg_bwd_max_arg_off_kernel(const typename ElemT<E>::T *__restrict__ src,
+                                                                  const I *__restrict__ idx,
+                                                                  const int64_t *__restrict__ off,
+                                                                  const int64_t *__restrict__ first,
+                                                                  const float *__restrict__ out, int64_t n,
+                                                                  int64_t S, int64_t F, unsigned long long *arg) {
+    __shared__ int64_t s_off[256];
+    const int nvec = (int)(F / V);
+    const RowMap m = row_map(nvec);
+    int64_t seg[kPasses];
+    float inv[kPasses];
+    if (nvec <= m.tpr) {  // one vector per thread and row
+        const bool lane = m.j0 < nvec;
+        Raw<E, V> r[kPasses];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q)
+            if (lane && m.row(q) < n) load_raw<E, V, true>(src + m.row(q) * F + (int64_t)m.j0 * V, r[q]);
+        const bool one = segments_from_offsets<I, false>(m, idx, off, first, n, S, s_off, seg, inv);
+        if (!lane) return;
+        float o[kPasses][V];
+        if (one) {
+            if (m.row(0) >= n) return;   // no row here (seg[0] is -1)
+            load_f32<V>(out + seg[0] * F + (int64_t)m.j0 * V, o[0]);
+#pragma unroll
+            for (int q = 1; q < kPasses; ++q)
+#pragma unroll
+                for (int k = 0; k < V; ++k) o[q][k] = o[0][k];
+        } else {
+#pragma unroll
+            for (int q = 0; q < kPasses; ++q)
+                if ((uint64_t)seg[q] < (uint64_t)S) load_f32<V>(out + seg[q] * F + (int64_t)m.j0 * V, o[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if ((uint64_t)seg[q] >= (uint64_t)S) continue;   // past the last row, or an id out of range
+            float x[V];
+            widen<E, V>(r[q], x);
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                if (x[k] == o[q][k])
+                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+        }
+        return;
+    }
+    segments_from_offsets<I, false>(m, idx, off, first, n, S, s_off, seg, inv);
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t i = m.row(q);
+        const int64_t s = seg[q];
+        if (i >= n || (uint64_t)s >= (uint64_t)S) continue;
+        for (int j = m.j0; j < nvec; j += m.tpr) {
+            float x[V], o[V];
+            Raw<E, V> r;
+            load_raw<E, V, true>(src + i * F + (int64_t)j * V, r);
             widen<E, V>(r, x);
             load_f32<V>(out + s * F + (int64_t)j * V, o);
 #pragma unroll
@@ -274,6 +488,89 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
                 for (int k = 0; k < V; ++k) x[k] = 0.0f;
             }
             store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
+        }
+    }
+}
+
+// The max gradient's stores with the segments from the offsets (as the broadcast above): the
+// recipients and gradient rows stay in cache, so the stores are the kernel's HBM stream.
+template <int E, typename I, int V>
+__global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float *__restrict__ gout,
+                                                                    const I *__restrict__ idx,
+                                                                    const int64_t *__restrict__ off,
+                                                                    const int64_t *__restrict__ first,
+                                                                    const unsigned long long *__restrict__ arg,
+                                                                    int64_t n, int64_t S, int64_t F,
+                                                                    typename ElemT<E>::T *__restrict__ gsrc) {
+    __shared__ int64_t s_off[256];
+    const int nvec = (int)(F / V);
+    const RowMap m = row_map(nvec);
+    int64_t seg[kPasses];
+    float inv[kPasses];
+    if (segments_from_offsets<I, false>(m, idx, off, first, n, S, s_off, seg, inv)) {
+        // one segment: its gradient and recipient vectors load once for all the thread's rows
+        if (m.row(0) >= n) return;   // no row here (seg[0] is -1)
+        for (int j = m.j0; j < nvec; j += m.tpr) {
+            float x[V];
+            unsigned long long w[V];
+            load_f32<V>(gout + seg[0] * F + (int64_t)j * V, x);
+            const unsigned long long *a = arg + seg[0] * F + (int64_t)j * V;
+            if constexpr (V >= 2) {
+#pragma unroll
+                for (int k = 0; k < V; k += 2) {
+                    const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
+                    w[k] = t.x;
+                    w[k + 1] = t.y;
+                }
+            } else {
+                w[0] = a[0];
+            }
+#pragma unroll
+            for (int q = 0; q < kPasses; ++q) {
+                const int64_t i = m.row(q);
+                if (i >= n) break;
+                float y[V];
+#pragma unroll
+                for (int k = 0; k < V; ++k) y[k] = w[k] == (unsigned long long)i ? x[k] : 0.0f;
+                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, y);
+            }
+        }
+        return;
+    }
+    for (int j = m.j0; j < nvec; j += m.tpr) {
+        float x[kPasses][V];
+        unsigned long long w[kPasses][V];
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            if ((uint64_t)seg[q] < (uint64_t)S) {
+                load_f32<V>(gout + seg[q] * F + (int64_t)j * V, x[q]);
+                const unsigned long long *a = arg + seg[q] * F + (int64_t)j * V;
+                if constexpr (V >= 2) {  // 16-byte loads: V * 8 bytes at a multiple of V * 8
+#pragma unroll
+                    for (int k = 0; k < V; k += 2) {
+                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
+                        w[q][k] = t.x;
+                        w[q][k + 1] = t.y;
+                    }
+                } else {
+                    w[q][0] = a[0];
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    x[q][k] = 0.0f;
+                    w[q][k] = ~0ull;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t i = m.row(q);
+            if (i >= n) break;
+#pragma unroll
+            for (int k = 0; k < V; ++k)
+                if (w[q][k] != (unsigned long long)i) x[q][k] = 0.0f;
+            store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[q]);
         }
     }
 }
@@ -1017,9 +1314,21 @@ hipError_t by_width(int V, Fn &&f) {
 
 }  // namespace
 
-hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off, int64_t n,
-                                int64_t S, int64_t F, int V, int elem, bool mean, void *gsrc, hipStream_t st) {
+int seg_bwd_rows_log2(int64_t F, int V) {
+    const int nvec = (int)(F / V);
+    int t = 1, lt = 0;
+    while (t < nvec && t < 64) t <<= 1, ++lt;
+    return 10 - lt;   // kPasses * 256 / t rows
+}
+
+int64_t seg_bwd_blocks(int64_t n, int64_t F, int V) { return grid_rows(n, (int)(F / V)); }
+
+hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off,
+                                const int64_t *first, int64_t n, int64_t S, int64_t F, int V, int elem, bool mean,
+                                void *gsrc, hipStream_t st) {
+    static_assert(kPasses * 256 == 1 << 10, "seg_bwd_rows_log2 assumes 1024 thread-rows per block");
     if (n <= 0) return hipSuccess;
+    if (first && !off) return hipErrorInvalidValue;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
@@ -1029,7 +1338,13 @@ hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, c
         using T = typename ElemT<E>::T;
         return by_width<E>(V, [&](auto vt) -> hipError_t {
             constexpr int VV = decltype(vt)::value;
-            if (mean)
+            if (first && mean)
+                hipLaunchKernelGGL((seg_bwd_bcast_off_kernel<E, I, VV, true>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), off, first, n, S, F, static_cast<T *>(gsrc));
+            else if (first)
+                hipLaunchKernelGGL((seg_bwd_bcast_off_kernel<E, I, VV, false>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), off, first, n, S, F, static_cast<T *>(gsrc));
+            else if (mean)
                 hipLaunchKernelGGL((seg_bwd_bcast_kernel<E, I, VV, true>), dim3(g), dim3(256), 0, st, gout,
                                    static_cast<const I *>(idx), off, n, S, F, static_cast<T *>(gsrc));
             else
@@ -1041,9 +1356,10 @@ hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, c
 }
 
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
-                              int64_t n, int64_t S, int64_t F, int V, int elem, unsigned long long *arg,
-                              void *gsrc, hipStream_t st) {
+                              const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
+                              int elem, unsigned long long *arg, void *gsrc, hipStream_t st) {
     if (n <= 0) return hipSuccess;
+    if (first && !off) return hipErrorInvalidValue;
     hipError_t e = launch_fill_u64(arg, S * F, ~0ull, st);
     if (e != hipSuccess) return e;
     const int64_t gb = grid_rows(n, (int)(F / V));
@@ -1055,12 +1371,21 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
         using T = typename ElemT<E>::T;
         return by_width<E>(V, [&](auto vt) -> hipError_t {
             constexpr int VV = decltype(vt)::value;
-            hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
-                               static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, arg);
+            if (first)
+                hipLaunchKernelGGL((seg_bwd_max_arg_off_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
+                                   static_cast<const T *>(src), static_cast<const I *>(idx), off, first, out, n, S, F,
+                                   arg);
+            else
+                hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
+                                   static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, arg);
             hipError_t e2 = hipGetLastError();
             if (e2 != hipSuccess) return e2;
-            hipLaunchKernelGGL((seg_bwd_max_write_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
-                               static_cast<const I *>(idx), arg, n, S, F, static_cast<T *>(gsrc));
+            if (first)
+                hipLaunchKernelGGL((seg_bwd_max_write_off_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), off, first, arg, n, S, F, static_cast<T *>(gsrc));
+            else
+                hipLaunchKernelGGL((seg_bwd_max_write_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
+                                   static_cast<const I *>(idx), arg, n, S, F, static_cast<T *>(gsrc));
             return hipGetLastError();
         });
     });

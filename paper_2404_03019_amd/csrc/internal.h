@@ -110,11 +110,13 @@ hipError_t launch_sp(const SpArgs &a, int red, int mode, int V, int NT, int L, h
 
 // off[s] = first row with idx >= s for s in [0, S]; one pass over the index.
 // Long runs go to `gaps` (value = the row they start at): run launch_gap_fill_i64 after.
+// With `first` (optional, 2 * ceil(n / 2^shift) entries): first[2b] and first[2b + 1] = the ids
+// of the first and the last row of block b of 2^shift rows.
 hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
-                          hipStream_t stream);
+                          hipStream_t stream, int64_t *first = nullptr, int shift = 0);
 // the same over int32 ids
 hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
-                              hipStream_t stream);
+                              hipStream_t stream, int64_t *first = nullptr, int shift = 0);
 
 // Grid-wide passes over a gap list: out rows [first, end) = 0 in the columns of
 // tile `value` (tiles of `tw` columns), or arr[first, end) = value. Both leave
@@ -164,15 +166,22 @@ size_t transpose_scratch_bytes(int64_t n, int64_t nx);
 
 // grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean), stored in
 // the source's ElemType `elem` (16-bit: rounded to nearest even); idx int32 when idx32. V is 1,
-// 2, 4 or (16-bit) 8.
-hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off, int64_t n,
-                                int64_t S, int64_t F, int V, int elem, bool mean, void *gsrc, hipStream_t st);
+// 2, 4 or (16-bit) 8. With `first` (the ids of each block's first and last rows, from
+// launch_offsets with shift = seg_bwd_rows_log2(F, V)) and complete offsets, rows take their
+// segments from off and the ids are read only where a block spans more than 255 segment ends.
+hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, const int64_t *off,
+                                const int64_t *first, int64_t n, int64_t S, int64_t F, int V, int elem, bool mean,
+                                void *gsrc, hipStream_t st);
+// log2 of the rows one block of the segment gradient kernels covers, and their block count
+int seg_bwd_rows_log2(int64_t F, int V);
+int64_t seg_bwd_blocks(int64_t n, int64_t F, int V);
 
 // max: arg [S x F] scratch; grad_src gets grad_out at the first attaining row of each (s, f);
-// src and grad_src of ElemType `elem`
+// src and grad_src of ElemType `elem`. off and first (optional) as for launch_seg_bwd_bcast:
+// the stores then take their segments from the offsets.
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
-                              int64_t n, int64_t S, int64_t F, int V, int elem, unsigned long long *arg,
-                              void *gsrc, hipStream_t st);
+                              const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
+                              int elem, unsigned long long *arg, void *gsrc, hipStream_t st);
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);

@@ -36,6 +36,7 @@ SEG_CASES = [
     (4, 8000, 400, 33, "one_heavy", "normal", 0.1),
     (5, 6000, 300, 256, "zipf", "normal", 0.0),
     (6, 7000, 400, 6, "zipf", "int", 0.1),          # 2-wide vectors; integer values tie often
+    (7, 4000, 200, 300, "zipf", "normal", 0.1),     # more vectors than a row's 64 threads
 ]
 
 
@@ -56,6 +57,31 @@ def test_segment_backward_parity(case):
             within(got, ref, terms, f"segment backward mean seed={seed}")
         else:
             assert np.array_equal(got, ref), f"segment backward {op} seed={seed} F={F}"
+
+
+@pytest.mark.parametrize("case", [
+    (8, 600_000, 40_000, 32, "zipf", 0.3),          # 77 MB of grad_src: sum takes the offsets pass too
+    (9, 600_000, 3_000_000, 32, "uniform", 0.9),    # blocks spanning > 255 segment ends, long empty runs
+    (10, 300_000, 20_000, 64, "one_heavy", 0.2),
+    (11, 700_001, 1, 32, "uniform", 0.0),           # one segment: every block lies in it, ragged last block
+], ids=lambda c: f"seed{c[0]}-S{c[2]}")
+def test_segment_backward_from_offsets(case):
+    """Large gradients: each row's segment comes from the offsets (staged per block) rather than
+    the ids; sum and max bit-exact, mean within the bound, against the oracle."""
+    seed, nnz, S, F, dist, ef = case
+    p = random_problem(seed, nnz, S, F, dist, "int", ef)   # integer values: max ties
+    src, idx = p["src"], p["index"]
+    g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
+    for op in ("sum", "mean", "max"):
+        say(f"segment backward from offsets seed={seed} S={S} {op}")
+        out = geot.segment_reduce(up(src), up(idx), S, op) if op == "max" else None
+        got = geot.segment_reduce_backward(up(g), up(idx), op, up(src) if out is not None else None,
+                                           out).cpu().numpy()
+        ref = oracle.segment_reduce_backward(g, idx, op, src, None if out is None else out.cpu().numpy())
+        if op == "mean":
+            within(got, ref, np.abs(ref.astype(np.float64)), f"mean seed={seed}")
+        else:
+            assert np.array_equal(got, ref), f"sum seed={seed}"
 
 
 GS_CASES = [
