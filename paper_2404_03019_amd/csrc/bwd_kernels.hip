@@ -23,19 +23,22 @@ namespace geot {
 namespace {
 
 constexpr int kPasses = 4;  // passes of one block over its rows
+constexpr int kWPasses8 = 2;   // the same for the weight gradient with 8-element vectors
 
 struct RowMap {
-    int tpr;    // threads per row
-    int rsub;   // this thread's row within a pass
-    int j0;     // this thread's first vector
-    int rows;   // rows per pass of one block
+    int tpr;      // threads per row
+    int rsub;     // this thread's row within a pass
+    int j0;       // this thread's first vector
+    int rows;     // rows per pass of one block
+    int passes;   // passes of one block
     __device__ int64_t row(int q) const {  // this thread's row in pass q
-        return ((int64_t)blockIdx.x * kPasses + q) * rows + rsub;
+        return ((int64_t)blockIdx.x * passes + q) * rows + rsub;
     }
 };
 
-__device__ __forceinline__ RowMap row_map(int nvec) {
+__device__ __forceinline__ RowMap row_map(int nvec, int passes = kPasses) {
     RowMap m;
+    m.passes = passes;
     int t = 1;
     while (t < nvec && t < 64) t <<= 1;
     m.tpr = t;
@@ -723,7 +726,7 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long l
 // mean divides afterwards, in scale_by_count_kernel). Every thread runs all passes (the group
 // reduction is uniform); the edges' ids load first, then both operand rows of every pass, then
 // the products.
-template <int E, typename I, int V, int OP>
+template <int E, typename I, int V, int OP, int P>
 __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                        const I *__restrict__ col,
                                                        const I *__restrict__ row,
@@ -731,39 +734,41 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
                                                        const float *__restrict__ gout, int64_t n, int64_t R,
                                                        int64_t F, float *__restrict__ gw) {
     const int nvec = (int)(F / V);
-    const RowMap m = row_map(nvec);
-    int64_t rr[kPasses], cc[kPasses];
-    bool ok[kPasses];
+    const RowMap m = row_map(nvec, P);
+    int64_t rr[P], cc[P];
+    bool ok[P];
 #pragma unroll
-    for (int q = 0; q < kPasses; ++q) {
+    for (int q = 0; q < P; ++q) {
         const int64_t e = m.row(q);
         rr[q] = e < n ? (int64_t)row[e] : -1;
         cc[q] = e < n ? (int64_t)col[e] : -1;
     }
 #pragma unroll
-    for (int q = 0; q < kPasses; ++q)
+    for (int q = 0; q < P; ++q)
         ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx;
     static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
-    float acc[kPasses];
+    float acc[P];
     if (nvec <= m.tpr) {  // one vector per thread and row: all loads of the block's passes in flight together
-        float g[kPasses][V], x[kPasses][V];
+        // X rows stay in their loaded words until the products (16-bit X: half the registers of
+        // widened rows; bf16 / int32 on the SpMM graph held 92 VGPRs, 5 waves per SIMD, widened)
+        float g[P][V];
+        Raw<E, V> rx[P];
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
             if (ok[q] && m.j0 < nvec) {
                 load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
-                Raw<E, V> rx;
-                load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx);
-                widen<E, V>(rx, x[q]);
+                load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx[q]);
             } else {
+                rx[q] = Raw<E, V>{};
 #pragma unroll
-                for (int k = 0; k < V; ++k) g[q][k] = x[q][k] = 0.0f;
+                for (int k = 0; k < V; ++k) g[q][k] = 0.0f;
             }
         }
         if constexpr (OP == GEOT_BWD_MAX) {
             // max: the recipients load with the operand rows (16-byte pairs where V >= 2), and
             // the other edges' products are masked out
 #pragma unroll
-            for (int q = 0; q < kPasses; ++q) {
+            for (int q = 0; q < P; ++q) {
                 if (!(ok[q] && m.j0 < nvec)) continue;
                 const unsigned long long *a = arg + rr[q] * F + (int64_t)m.j0 * V;
                 const unsigned long long e = (unsigned long long)m.row(q);
@@ -780,14 +785,16 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
             }
         }
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
+            float x[V];
+            widen<E, V>(rx[q], x);
             acc[q] = 0.0f;
 #pragma unroll
-            for (int k = 0; k < V; ++k) acc[q] += g[q][k] * x[q][k];
+            for (int k = 0; k < V; ++k) acc[q] += g[q][k] * x[k];
         }
     } else {
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
             acc[q] = 0.0f;
             if (!ok[q]) continue;
             const int64_t e = m.row(q);
@@ -806,7 +813,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
         }
     }
 #pragma unroll
-    for (int q = 0; q < kPasses; ++q) {
+    for (int q = 0; q < P; ++q) {
         float a = acc[q];
         for (int d = m.tpr / 2; d >= 1; d >>= 1) a += __shfl_xor(a, d, 64);
         const int64_t e = m.row(q);
@@ -1138,10 +1145,10 @@ __global__ __launch_bounds__(256) void fill_u64_kernel(unsigned long long *p, in
 }
 
 // blocks of kPasses * (256 / tpr) rows; the callers check the count fits a grid
-int64_t grid_rows(int64_t rows, int nvec) {
+int64_t grid_rows(int64_t rows, int nvec, int passes = kPasses) {
     int t = 1;
     while (t < nvec && t < 64) t <<= 1;
-    const int64_t per_block = (int64_t)kPasses * (256 / t);
+    const int64_t per_block = (int64_t)passes * (256 / t);
     const int64_t b = (rows + per_block - 1) / per_block;
     return b < 1 ? 1 : b;
 }
@@ -1425,12 +1432,17 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (gw) {
+                // 8-element vectors: 2 passes per block (their fp32 operand vectors fill half the
+                // registers that 4 passes' do)
+                constexpr int WP = VV == 8 ? kWPasses8 : kPasses;
+                const int64_t gwb = grid_rows(n, (int)(F / VV), WP);
+                if (gwb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
                 if (op == GEOT_BWD_MAX)
-                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX>), dim3(g), dim3(256), 0, st, Xt, nx,
-                                       ct, rt, arg, gout, n, R, F, gw);
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP>), dim3((unsigned)gwb), dim3(256), 0,
+                                       st, Xt, nx, ct, rt, arg, gout, n, R, F, gw);
                 else
-                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM>), dim3(g), dim3(256), 0, st, Xt, nx,
-                                       ct, rt, arg, gout, n, R, F, gw);
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP>), dim3((unsigned)gwb), dim3(256), 0,
+                                       st, Xt, nx, ct, rt, arg, gout, n, R, F, gw);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
                 if (op == GEOT_BWD_MEAN) {
                     const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
