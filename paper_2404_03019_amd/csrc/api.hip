@@ -717,7 +717,8 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
     // grad_src then take every row's segment from the offsets, so that their only HBM stream is
     // their stores. Below, the ids are read where they are needed (two launches fewer).
     const bool from_off = mean || gb >= kBcastOffsetsMinBytes;
-    const size_t o_arg = 0, arg_b = mx ? align256((size_t)(num_segments * F) * 8) : 0;
+    const size_t o_arg = 0,
+                 arg_b = mx ? align256((size_t)(num_segments * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
     const size_t o_off = o_arg + arg_b, o_first = o_off + (from_off ? align256((size_t)(num_segments + 1) * 8) : 0);
     const int64_t blocks = seg_bwd_blocks(nnz, F, V);
     GapList gaps;
@@ -726,7 +727,7 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
                                          from_off ? &gaps : nullptr, &ctx);
         if (s != GEOT_SUCCESS) return s;
     }
-    unsigned long long *arg = mx ? (unsigned long long *)scratch : nullptr;
+    void *arg = mx ? scratch : nullptr;
     int64_t *off = from_off ? (int64_t *)((char *)scratch + o_off) : nullptr;
     int64_t *first = from_off ? (int64_t *)((char *)scratch + o_first) : nullptr;
     if (!from_off) {

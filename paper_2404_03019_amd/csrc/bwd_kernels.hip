@@ -297,14 +297,44 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_off_kernel(const float *__r
     }
 }
 
+// Recipient vectors: V consecutive entries of a recipient table of 32- or 64-bit row numbers
+// (16-byte loads where V entries fill them; entries at a multiple of V)
+template <typename A, int V>
+__device__ __forceinline__ void load_arg(const A *a, A (&w)[V]) {
+    if constexpr (sizeof(A) == 8 && V >= 2) {
+#pragma unroll
+        for (int k = 0; k < V; k += 2) {
+            const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
+            w[k] = t.x;
+            w[k + 1] = t.y;
+        }
+    } else if constexpr (sizeof(A) == 4 && V >= 4) {
+#pragma unroll
+        for (int k = 0; k < V; k += 4) {
+            const uint4 t = *reinterpret_cast<const uint4 *>(a + k);
+            w[k] = t.x;
+            w[k + 1] = t.y;
+            w[k + 2] = t.z;
+            w[k + 3] = t.w;
+        }
+    } else if constexpr (sizeof(A) == 4 && V == 2) {
+        const uint2 t = *reinterpret_cast<const uint2 *>(a);
+        w[0] = t.x;
+        w[1] = t.y;
+    } else {
+#pragma unroll
+        for (int k = 0; k < V; ++k) w[k] = a[k];
+    }
+}
+
 // arg[s, f] = min row i of segment s with src[i, f] == out[s, f]. The ids of all passes
 // load first, then every pass's row and output vector, then the compares (one memory
 // latency per step, not per pass).
-template <int E, typename I, int V>
+template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename ElemT<E>::T *__restrict__ src,
                                                               const I *__restrict__ idx,
                                                               const float *__restrict__ out, int64_t n, int64_t S,
-                                                              int64_t F, unsigned long long *arg) {
+                                                              int64_t F, A *arg) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     int64_t seg[kPasses];
@@ -332,7 +362,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename Ele
 #pragma unroll
             for (int k = 0; k < V; ++k)
                 if (x[q][k] == o[q][k])
-                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (A)m.row(q));
         }
         return;
     }
@@ -348,7 +378,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename Ele
             load_f32<V>(out + s * F + (int64_t)j * V, o);
 #pragma unroll
             for (int k = 0; k < V; ++k)
-                if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (unsigned long long)i);
+                if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (A)i);
         }
     }
 }
@@ -357,13 +387,13 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_kernel(const typename Ele
 // load first (non-temporal: each is read once), before the segments are known, so that the
 // stream does not wait for the segment lookup; the outputs they are compared with follow (once
 // per thread where the block lies in one segment).
-template <int E, typename I, int V>
+template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void seg_bwd_max_arg_off_kernel(const typename ElemT<E>::T *__restrict__ src,
                                                                   const I *__restrict__ idx,
                                                                   const int64_t *__restrict__ off,
                                                                   const int64_t *__restrict__ first,
                                                                   const float *__restrict__ out, int64_t n,
-                                                                  int64_t S, int64_t F, unsigned long long *arg) {
+                                                                  int64_t S, int64_t F, A *arg) {
     __shared__ int64_t s_off[256];
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
@@ -398,7 +428,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_off_kernel(const typename
 #pragma unroll
             for (int k = 0; k < V; ++k)
                 if (x[k] == o[q][k])
-                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (unsigned long long)m.row(q));
+                    atomicMin(arg + seg[q] * F + (int64_t)m.j0 * V + k, (A)m.row(q));
         }
         return;
     }
@@ -415,17 +445,17 @@ __global__ __launch_bounds__(256) void seg_bwd_max_arg_off_kernel(const typename
             load_f32<V>(out + s * F + (int64_t)j * V, o);
 #pragma unroll
             for (int k = 0; k < V; ++k)
-                if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (unsigned long long)i);
+                if (x[k] == o[k]) atomicMin(arg + s * F + (int64_t)j * V + k, (A)i);
         }
     }
 }
 
 // grad_src[i, f] = grad_out[s, f] where i is the recipient of (s, f), else 0; ids first,
 // then every pass's gradient and recipient vectors, then the stores
-template <int E, typename I, int V>
+template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__restrict__ gout,
                                                                 const I *__restrict__ idx,
-                                                                const unsigned long long *__restrict__ arg,
+                                                                const A *__restrict__ arg,
                                                                 int64_t n, int64_t S, int64_t F,
                                                                 typename ElemT<E>::T *__restrict__ gsrc) {
     const int nvec = (int)(F / V);
@@ -438,28 +468,18 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
     }
     if (nvec <= m.tpr) {
         float x[kPasses][V];
-        unsigned long long w[kPasses][V];
+        A w[kPasses][V];
 #pragma unroll
         for (int q = 0; q < kPasses; ++q) {
             const bool ok = (uint64_t)seg[q] < (uint64_t)S && m.j0 < nvec;
             if (ok) {
                 load_f32<V>(gout + seg[q] * F + (int64_t)m.j0 * V, x[q]);
-                const unsigned long long *a = arg + seg[q] * F + (int64_t)m.j0 * V;
-                if constexpr (V >= 2) {  // 16-byte loads: V * 8 bytes at a multiple of V * 8
-#pragma unroll
-                    for (int k = 0; k < V; k += 2) {
-                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
-                        w[q][k] = t.x;
-                        w[q][k + 1] = t.y;
-                    }
-                } else {
-                    w[q][0] = a[0];
-                }
+                load_arg<A, V>(arg + seg[q] * F + (int64_t)m.j0 * V, w[q]);
             } else {
 #pragma unroll
                 for (int k = 0; k < V; ++k) {
                     x[q][k] = 0.0f;
-                    w[q][k] = ~0ull;
+                    w[q][k] = (A)~(A)0;
                 }
             }
         }
@@ -469,7 +489,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
             if (i >= n || m.j0 >= nvec) continue;
 #pragma unroll
             for (int k = 0; k < V; ++k)
-                if (w[q][k] != (unsigned long long)i) x[q][k] = 0.0f;
+                if (w[q][k] != (A)i) x[q][k] = 0.0f;
             store_elems<E, V>(gsrc + i * F + (int64_t)m.j0 * V, x[q]);
         }
         return;
@@ -485,7 +505,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
                 load_f32<V>(gout + s * F + (int64_t)j * V, x);
 #pragma unroll
                 for (int k = 0; k < V; ++k)
-                    if (arg[s * F + (int64_t)j * V + k] != (unsigned long long)i) x[k] = 0.0f;
+                    if (arg[s * F + (int64_t)j * V + k] != (A)i) x[k] = 0.0f;
             } else {
 #pragma unroll
                 for (int k = 0; k < V; ++k) x[k] = 0.0f;
@@ -497,12 +517,12 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
 
 // The max gradient's stores with the segments from the offsets (as the broadcast above): the
 // recipients and gradient rows stay in cache, so the stores are the kernel's HBM stream.
-template <int E, typename I, int V>
+template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float *__restrict__ gout,
                                                                     const I *__restrict__ idx,
                                                                     const int64_t *__restrict__ off,
                                                                     const int64_t *__restrict__ first,
-                                                                    const unsigned long long *__restrict__ arg,
+                                                                    const A *__restrict__ arg,
                                                                     int64_t n, int64_t S, int64_t F,
                                                                     typename ElemT<E>::T *__restrict__ gsrc) {
     __shared__ int64_t s_off[256];
@@ -515,65 +535,52 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float 
         if (m.row(0) >= n) return;   // no row here (seg[0] is -1)
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float x[V];
-            unsigned long long w[V];
+            A w[V];
             load_f32<V>(gout + seg[0] * F + (int64_t)j * V, x);
-            const unsigned long long *a = arg + seg[0] * F + (int64_t)j * V;
-            if constexpr (V >= 2) {
-#pragma unroll
-                for (int k = 0; k < V; k += 2) {
-                    const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
-                    w[k] = t.x;
-                    w[k + 1] = t.y;
-                }
-            } else {
-                w[0] = a[0];
-            }
+            load_arg<A, V>(arg + seg[0] * F + (int64_t)j * V, w);
 #pragma unroll
             for (int q = 0; q < kPasses; ++q) {
                 const int64_t i = m.row(q);
                 if (i >= n) break;
                 float y[V];
 #pragma unroll
-                for (int k = 0; k < V; ++k) y[k] = w[k] == (unsigned long long)i ? x[k] : 0.0f;
+                for (int k = 0; k < V; ++k) y[k] = w[k] == (A)i ? x[k] : 0.0f;
                 store_elems<E, V>(gsrc + i * F + (int64_t)j * V, y);
             }
         }
         return;
     }
+    // several segments: two passes' vectors in flight at a time (all four held the 16-bit kernel
+    // at 108 VGPRs, 4 waves per SIMD, for the single-segment path as well)
+    constexpr int QB = 2;
     for (int j = m.j0; j < nvec; j += m.tpr) {
-        float x[kPasses][V];
-        unsigned long long w[kPasses][V];
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
-            if ((uint64_t)seg[q] < (uint64_t)S) {
-                load_f32<V>(gout + seg[q] * F + (int64_t)j * V, x[q]);
-                const unsigned long long *a = arg + seg[q] * F + (int64_t)j * V;
-                if constexpr (V >= 2) {  // 16-byte loads: V * 8 bytes at a multiple of V * 8
+        for (int q0 = 0; q0 < kPasses; q0 += QB) {
+            float x[QB][V];
+            A w[QB][V];
 #pragma unroll
-                    for (int k = 0; k < V; k += 2) {
-                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
-                        w[q][k] = t.x;
-                        w[q][k + 1] = t.y;
-                    }
+            for (int u = 0; u < QB; ++u) {
+                const int q = q0 + u;
+                if ((uint64_t)seg[q] < (uint64_t)S) {
+                    load_f32<V>(gout + seg[q] * F + (int64_t)j * V, x[u]);
+                    load_arg<A, V>(arg + seg[q] * F + (int64_t)j * V, w[u]);
                 } else {
-                    w[q][0] = a[0];
-                }
-            } else {
 #pragma unroll
-                for (int k = 0; k < V; ++k) {
-                    x[q][k] = 0.0f;
-                    w[q][k] = ~0ull;
+                    for (int k = 0; k < V; ++k) {
+                        x[u][k] = 0.0f;
+                        w[u][k] = (A)~(A)0;
+                    }
                 }
             }
-        }
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
-            const int64_t i = m.row(q);
-            if (i >= n) break;
+            for (int u = 0; u < QB; ++u) {
+                const int64_t i = m.row(q0 + u);
+                if (i >= n) break;
 #pragma unroll
-            for (int k = 0; k < V; ++k)
-                if (w[q][k] != (unsigned long long)i) x[q][k] = 0.0f;
-            store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[q]);
+                for (int k = 0; k < V; ++k)
+                    if (w[u][k] != (A)i) x[u][k] = 0.0f;
+                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[u]);
+            }
         }
     }
 }
@@ -1362,40 +1369,50 @@ hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, c
     });
 }
 
+bool seg_bwd_arg32(int64_t n) { return n < (int64_t)0xffffffffLL; }
+
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
                               const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
-                              int elem, unsigned long long *arg, void *gsrc, hipStream_t st) {
+                              int elem, void *arg, void *gsrc, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     if (first && !off) return hipErrorInvalidValue;
-    hipError_t e = launch_fill_u64(arg, S * F, ~0ull, st);
+    const bool a32 = seg_bwd_arg32(n);
+    // all ones ("no recipient") in either width: S * F entries, rounded up to 8 bytes (the
+    // table's allocation is a multiple of 256 bytes)
+    hipError_t e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (S * F + 1) / 2 : S * F, ~0ull, st);
     if (e != hipSuccess) return e;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
-    return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
-        constexpr int E = decltype(et)::value;
-        using I = typename decltype(it)::type;
-        using T = typename ElemT<E>::T;
-        return by_width<E>(V, [&](auto vt) -> hipError_t {
-            constexpr int VV = decltype(vt)::value;
-            if (first)
-                hipLaunchKernelGGL((seg_bwd_max_arg_off_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
-                                   static_cast<const T *>(src), static_cast<const I *>(idx), off, first, out, n, S, F,
-                                   arg);
-            else
-                hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st,
-                                   static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, arg);
-            hipError_t e2 = hipGetLastError();
-            if (e2 != hipSuccess) return e2;
-            if (first)
-                hipLaunchKernelGGL((seg_bwd_max_write_off_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
-                                   static_cast<const I *>(idx), off, first, arg, n, S, F, static_cast<T *>(gsrc));
-            else
-                hipLaunchKernelGGL((seg_bwd_max_write_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, gout,
-                                   static_cast<const I *>(idx), arg, n, S, F, static_cast<T *>(gsrc));
-            return hipGetLastError();
+    auto run = [&](auto at) -> hipError_t {
+        using A = typename decltype(at)::type;
+        A *ap = static_cast<A *>(arg);
+        return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
+            constexpr int E = decltype(et)::value;
+            using I = typename decltype(it)::type;
+            using T = typename ElemT<E>::T;
+            return by_width<E>(V, [&](auto vt) -> hipError_t {
+                constexpr int VV = decltype(vt)::value;
+                if (first)
+                    hipLaunchKernelGGL((seg_bwd_max_arg_off_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
+                                       static_cast<const T *>(src), static_cast<const I *>(idx), off, first, out, n, S,
+                                       F, ap);
+                else
+                    hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
+                                       static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, ap);
+                hipError_t e2 = hipGetLastError();
+                if (e2 != hipSuccess) return e2;
+                if (first)
+                    hipLaunchKernelGGL((seg_bwd_max_write_off_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st, gout,
+                                       static_cast<const I *>(idx), off, first, ap, n, S, F, static_cast<T *>(gsrc));
+                else
+                    hipLaunchKernelGGL((seg_bwd_max_write_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st, gout,
+                                       static_cast<const I *>(idx), ap, n, S, F, static_cast<T *>(gsrc));
+                return hipGetLastError();
+            });
         });
-    });
+    };
+    return a32 ? run(TypeTag<unsigned>{}) : run(TypeTag<unsigned long long>{});
 }
 
 hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,

@@ -176,12 +176,14 @@ hipError_t launch_seg_bwd_bcast(const float *gout, const void *idx, int idx32, c
 int seg_bwd_rows_log2(int64_t F, int V);
 int64_t seg_bwd_blocks(int64_t n, int64_t F, int V);
 
-// max: arg [S x F] scratch; grad_src gets grad_out at the first attaining row of each (s, f);
-// src and grad_src of ElemType `elem`. off and first (optional) as for launch_seg_bwd_bcast:
-// the stores then take their segments from the offsets.
+// max: arg [S x F] scratch of row numbers, 32-bit where seg_bwd_arg32(n), else 64-bit (a
+// multiple of 8 bytes); grad_src gets grad_out at the first attaining row of each (s, f); src
+// and grad_src of ElemType `elem`. off and first (optional) as for launch_seg_bwd_bcast: the
+// stores then take their segments from the offsets.
+bool seg_bwd_arg32(int64_t n);
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
                               const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
-                              int elem, unsigned long long *arg, void *gsrc, hipStream_t st);
+                              int elem, void *arg, void *gsrc, hipStream_t st);
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);
