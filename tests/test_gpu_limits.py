@@ -62,6 +62,25 @@ def test_more_than_2_31_rows():
             ref = oracle.segment_reduce(rows, z, 1, "mean")
             compare(outs["mean"][s:s + 1], ref, "mean", oracle.abs_term_sum(rows, z, 1, "mean"),
                     f"limits mean segment {s}")
+        # the gradients over the same rows: segments from the offsets pass, 64-bit block and row
+        # arithmetic, and (max) a 32-bit recipient table holding row numbers above 2^31
+        g = torch.from_numpy(np.random.default_rng(12).standard_normal((S, F)).astype(np.float32)).to(DEV)
+        gh = g.cpu().numpy()
+        for op in ("sum", "mean", "max"):
+            out = torch.from_numpy(outs[op]).to(DEV) if op == "max" else None
+            gs = geot.segment_reduce_backward(g, ix, op, src if op == "max" else None, out)
+            say(f"limits: 2^31+ rows, gradient {op} ({itype})")
+            for s in sample(L, 12, 13):
+                a, b = int(starts[s]), int(starts[s + 1])
+                rows = src[a:b].cpu().numpy()
+                z = np.zeros(b - a, dtype=np.int64)
+                got = gs[a:b].cpu().numpy()
+                ref = oracle.segment_reduce_backward(gh[s:s + 1], z, op, rows, outs[op][s:s + 1])
+                if op == "mean":
+                    compare(got, ref, "mean", np.abs(ref.astype(np.float64)), f"limits gradient mean {s}")
+                else:
+                    assert np.array_equal(got, ref), (itype, op, s)
+            del gs
         del ix
     # per-feature conservation over every row (fp64 totals of exact integers)
     tot = torch.sum(src, dim=0, dtype=torch.float64).cpu().numpy()
