@@ -852,7 +852,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     size_t at = 0;
     auto take = [&](size_t b) { const size_t o = at; at = align256(at + b); return o; };
     const size_t o_roff = mean ? take((size_t)(num_rows + 1) * 8) : 0;
-    const size_t o_arg = mx ? take((size_t)(num_rows * F) * 8) : 0;
+    const size_t o_arg = mx ? take((size_t)(num_rows * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
     const int64_t nx = num_x_rows;
     const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
     const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
@@ -872,7 +872,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     if (s != GEOT_SUCCESS) return s;
     char *base = (char *)sg.p;
     int64_t *roff = mean ? (int64_t *)(base + o_roff) : nullptr;
-    unsigned long long *arg = mx ? (unsigned long long *)(base + o_arg) : nullptr;
+    void *arg = mx ? (void *)(base + o_arg) : nullptr;
     if (mean) {
         void *unused = nullptr;
         GapList gaps;

@@ -587,13 +587,13 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float 
 
 // fused form, max: arg[r, f] = min edge e of row r whose rounded product equals out[r, f].
 // Ids of all passes first, then every pass's X and output vectors, then the compares.
-template <int E, typename I, int V>
+template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                              const I *__restrict__ col,
                                                              const float *__restrict__ w,
                                                              const I *__restrict__ row,
                                                              const float *__restrict__ out, int64_t n, int64_t R,
-                                                             int64_t F, unsigned long long *arg) {
+                                                             int64_t F, A *arg) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     int64_t rr[kPasses], cc[kPasses];
@@ -671,9 +671,9 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 if (!(hit[q] >> k & 1u) || s_min[rs[q] * ncol + m.j0 * V + k] != (unsigned)slot) continue;
-                unsigned long long *a = arg + rr[q] * F + (int64_t)m.j0 * V + k;
-                if (shared_row) atomicMin(a, (unsigned long long)m.row(q));
-                else *a = (unsigned long long)m.row(q);
+                A *a = arg + rr[q] * F + (int64_t)m.j0 * V + k;
+                if (shared_row) atomicMin(a, (A)m.row(q));
+                else *a = (A)m.row(q);
             }
         }
         return;
@@ -691,7 +691,7 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 const float t = w ? wt[q] * x[k] : x[k];
-                if (t == o[k]) atomicMin(arg + r * F + (int64_t)j * V + k, (unsigned long long)e);
+                if (t == o[k]) atomicMin(arg + r * F + (int64_t)j * V + k, (A)e);
             }
         }
     }
@@ -700,8 +700,8 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
 // fused form, max, w.r.t. X: one thread per V-vector of a row r of the recipients; for each
 // (r, f) with a recipient edge e, grad_X[col[e], f] += coef(e) * grad_out[r, f]. Walks the
 // R * F recipients once (arg and grad_out stream) instead of every edge's row of them.
-template <typename I, int V>
-__global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long long *__restrict__ arg,
+template <typename I, int V, typename A>
+__global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__ arg,
                                                            const I *__restrict__ col, int64_t nx,
                                                            const float *__restrict__ w,
                                                            const float *__restrict__ gout, int64_t n,
@@ -713,13 +713,12 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long l
         if (r >= R) break;
         for (int j = m.j0; j < nvec; j += m.tpr) {
             float g[V];
-            unsigned long long a[V];
+            A a[V];
             load_f32<V>(gout + r * F + (int64_t)j * V, g);
-#pragma unroll
-            for (int k = 0; k < V; ++k) a[k] = arg[r * F + (int64_t)j * V + k];
+            load_arg<A, V>(arg + r * F + (int64_t)j * V, a);
 #pragma unroll
             for (int k = 0; k < V; ++k) {
-                if (a[k] >= (unsigned long long)n) continue;  // no recipient (empty row)
+                if ((uint64_t)a[k] >= (uint64_t)n) continue;  // no recipient (empty row)
                 const int64_t c = (int64_t)col[a[k]];
                 if ((uint64_t)c >= (uint64_t)nx) continue;
                 const float coef = w ? w[a[k]] : 1.0f;
@@ -733,11 +732,11 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const unsigned long l
 // mean divides afterwards, in scale_by_count_kernel). Every thread runs all passes (the group
 // reduction is uniform); the edges' ids load first, then both operand rows of every pass, then
 // the products.
-template <int E, typename I, int V, int OP, int P>
+template <int E, typename I, int V, int OP, int P, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                        const I *__restrict__ col,
                                                        const I *__restrict__ row,
-                                                       const unsigned long long *__restrict__ arg,
+                                                       const A *__restrict__ arg,
                                                        const float *__restrict__ gout, int64_t n, int64_t R,
                                                        int64_t F, float *__restrict__ gw) {
     const int nvec = (int)(F / V);
@@ -777,18 +776,12 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
 #pragma unroll
             for (int q = 0; q < P; ++q) {
                 if (!(ok[q] && m.j0 < nvec)) continue;
-                const unsigned long long *a = arg + rr[q] * F + (int64_t)m.j0 * V;
-                const unsigned long long e = (unsigned long long)m.row(q);
-                if constexpr (V >= 2) {
+                A a[V];
+                load_arg<A, V>(arg + rr[q] * F + (int64_t)m.j0 * V, a);
+                const A e = (A)m.row(q);
 #pragma unroll
-                    for (int k = 0; k < V; k += 2) {
-                        const ulonglong2 t = *reinterpret_cast<const ulonglong2 *>(a + k);
-                        if (t.x != e) g[q][k] = 0.0f;
-                        if (t.y != e) g[q][k + 1] = 0.0f;
-                    }
-                } else {
-                    if (a[0] != e) g[q][0] = 0.0f;
-                }
+                for (int k = 0; k < V; ++k)
+                    if (a[k] != e) g[q][k] = 0.0f;
             }
         }
 #pragma unroll
@@ -813,7 +806,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
                 widen<E, V>(rx, x);
 #pragma unroll
                 for (int k = 0; k < V; ++k) {
-                    if (OP == GEOT_BWD_MAX && arg[rr[q] * F + (int64_t)j * V + k] != (unsigned long long)e) continue;
+                    if (OP == GEOT_BWD_MAX && arg[rr[q] * F + (int64_t)j * V + k] != (A)e) continue;
                     acc[q] += g[k] * x[k];
                 }
             }
@@ -1417,11 +1410,17 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
 
 hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
                          const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw, hipStream_t st) {
+                         int64_t F, int V, int op, void *arg, float *gX, float *gw, hipStream_t st) {
     if (n <= 0) return hipSuccess;
+    if (op == GEOT_BWD_MAX && !arg) return hipErrorInvalidValue;
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
+    // recipients as 32-bit edge numbers below 2^32 - 1 edges, else 64-bit
+    const bool a32 = seg_bwd_arg32(n);
+    auto run = [&](auto at) -> hipError_t {
+    using A = typename decltype(at)::type;
+    A *ap = static_cast<A *>(arg);
     return by_types(elem, idx32, [&](auto et, auto it) -> hipError_t {
         constexpr int E = decltype(et)::value;
         using I = typename decltype(it)::type;
@@ -1432,10 +1431,10 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
             constexpr int VV = decltype(vt)::value;
             hipError_t e;
             if (op == GEOT_BWD_MAX) {
-                e = launch_fill_u64(arg, R * F, ~0ull, st);
+                e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (R * F + 1) / 2 : R * F, ~0ull, st);
                 if (e != hipSuccess) return e;
-                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV>), dim3(g), dim3(256), 0, st, Xt, nx, ct, w, rt,
-                                   out, n, R, F, arg);
+                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st, Xt, nx, ct, w, rt,
+                                   out, n, R, F, ap);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (gX) {  // max only (sum and mean gather over the transposed list)
@@ -1444,7 +1443,7 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 if (e != hipSuccess) return e;
                 const int64_t gr = grid_rows(R, (int)(F / VV));
                 if (gr > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-                hipLaunchKernelGGL((gs_bwd_x_max_kernel<I, VV>), dim3((unsigned)gr), dim3(256), 0, st, arg, ct, nx,
+                hipLaunchKernelGGL((gs_bwd_x_max_kernel<I, VV, A>), dim3((unsigned)gr), dim3(256), 0, st, ap, ct, nx,
                                    w, gout, n, R, F, gX);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
@@ -1455,11 +1454,11 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 const int64_t gwb = grid_rows(n, (int)(F / VV), WP);
                 if (gwb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
                 if (op == GEOT_BWD_MAX)
-                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP>), dim3((unsigned)gwb), dim3(256), 0,
-                                       st, Xt, nx, ct, rt, arg, gout, n, R, F, gw);
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
+                                       st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
                 else
-                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP>), dim3((unsigned)gwb), dim3(256), 0,
-                                       st, Xt, nx, ct, rt, arg, gout, n, R, F, gw);
+                    hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
+                                       st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
                 if (op == GEOT_BWD_MEAN) {
                     const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
@@ -1472,6 +1471,9 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
             return hipSuccess;
         });
     });
+    };
+    // sum and mean read no recipients: their kernels take the 32-bit instance
+    return a32 || op != GEOT_BWD_MAX ? run(TypeTag<unsigned>{}) : run(TypeTag<unsigned long long>{});
 }
 
 }  // namespace geot

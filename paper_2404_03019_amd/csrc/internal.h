@@ -187,10 +187,11 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);
-// off = row starts (mean), arg [R x F] scratch (max). X of ElemType elem, col and row int32
+// off = row starts (mean), arg [R x F] scratch of edge numbers for max (32-bit where
+// seg_bwd_arg32(n), else 64-bit; a multiple of 8 bytes). X of ElemType elem, col and row int32
 // when idx32.
 hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
                          const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, unsigned long long *arg, float *gX, float *gw, hipStream_t st);
+                         int64_t F, int V, int op, void *arg, float *gX, float *gw, hipStream_t st);
 
 }  // namespace geot
