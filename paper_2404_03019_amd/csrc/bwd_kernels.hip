@@ -24,6 +24,7 @@ namespace {
 
 constexpr int kPasses = 4;  // passes of one block over its rows
 constexpr int kWPasses8 = 2;   // the same for the weight gradient with 8-element vectors
+constexpr int kArgPasses = 2;  // the same for the fused max recipients
 
 struct RowMap {
     int tpr;      // threads per row
@@ -587,7 +588,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float 
 
 // fused form, max: arg[r, f] = min edge e of row r whose rounded product equals out[r, f].
 // Ids of all passes first, then every pass's X and output vectors, then the compares.
-template <int E, typename I, int V, typename A>
+template <int E, typename I, int V, typename A, int P>
 __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                              const I *__restrict__ col,
                                                              const float *__restrict__ w,
@@ -595,11 +596,11 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
                                                              const float *__restrict__ out, int64_t n, int64_t R,
                                                              int64_t F, A *arg) {
     const int nvec = (int)(F / V);
-    const RowMap m = row_map(nvec);
-    int64_t rr[kPasses], cc[kPasses];
-    float wt[kPasses];
+    const RowMap m = row_map(nvec, P);
+    int64_t rr[P], cc[P];
+    float wt[P];
 #pragma unroll
-    for (int q = 0; q < kPasses; ++q) {
+    for (int q = 0; q < P; ++q) {
         const int64_t e = m.row(q);
         rr[q] = e < n ? (int64_t)row[e] : -1;
         cc[q] = e < n ? (int64_t)col[e] : -1;
@@ -612,23 +613,23 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
         // stores its recipient plainly; a row that continues into the previous or next block takes
         // the lowest edge over the blocks with a global atomicMin. With sorted rows this equals the
         // plain rule (the lowest attaining edge); the global atomics are about one per row end.
-        __shared__ unsigned s_min[kPasses * 256 * V];   // slots * columns <= kPasses * 256 * V
-        __shared__ int64_t s_row[kPasses * 256];
-        const int slots = kPasses * m.rows, ncol = nvec * V;
+        __shared__ unsigned s_min[P * 256 * V];   // slots * columns <= P * 256 * V
+        __shared__ int64_t s_row[P * 256];
+        const int slots = P * m.rows, ncol = nvec * V;
         const int64_t e0 = (int64_t)blockIdx.x * slots;   // edge of slot 0
         for (int t = threadIdx.x; t < slots * ncol; t += 256) s_min[t] = 0xffffffffu;
         if (m.j0 == 0) {
 #pragma unroll
-            for (int q = 0; q < kPasses; ++q)   // slots past the last edge sort after every row
+            for (int q = 0; q < P; ++q)   // slots past the last edge sort after every row
                 s_row[q * m.rows + m.rsub] = m.row(q) < n ? rr[q] : INT64_MAX;
         }
         const bool has_prev = e0 > 0, has_next = e0 + slots < n;
         const int64_t prev_row = has_prev ? (int64_t)row[e0 - 1] : 0;
         const int64_t next_row = has_next ? (int64_t)row[e0 + slots] : 0;
-        float x[kPasses][V], o[kPasses][V];
-        bool ok[kPasses];
+        float x[P][V], o[P][V];
+        bool ok[P];
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
             ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx && m.j0 < nvec;
             if (ok[q]) {
                 Raw<E, V> rx;
@@ -638,10 +639,10 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
             }
         }
         __syncthreads();
-        unsigned hit[kPasses];   // bit k: column j0 * V + k of this pass's edge attains the maximum
-        int rs[kPasses];         // slot where this pass's row starts in the block
+        unsigned hit[P];   // bit k: column j0 * V + k of this pass's edge attains the maximum
+        int rs[P];         // slot where this pass's row starts in the block
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
             hit[q] = 0;
             rs[q] = 0;
             if (!ok[q]) continue;
@@ -664,7 +665,7 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
         }
         __syncthreads();
 #pragma unroll
-        for (int q = 0; q < kPasses; ++q) {
+        for (int q = 0; q < P; ++q) {
             if (!hit[q]) continue;
             const int slot = q * m.rows + m.rsub;
             const bool shared_row = (has_prev && prev_row == rr[q]) || (has_next && next_row == rr[q]);
@@ -678,7 +679,7 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_kernel(const typename Elem
         }
         return;
     }
-    for (int q = 0; q < kPasses; ++q) {
+    for (int q = 0; q < P; ++q) {
         const int64_t e = m.row(q);
         const int64_t r = rr[q], c = cc[q];
         if (e >= n || (uint64_t)r >= (uint64_t)R || (uint64_t)c >= (uint64_t)nx) continue;
@@ -1433,8 +1434,10 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
             if (op == GEOT_BWD_MAX) {
                 e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (R * F + 1) / 2 : R * F, ~0ull, st);
                 if (e != hipSuccess) return e;
-                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st, Xt, nx, ct, w, rt,
-                                   out, n, R, F, ap);
+                const int64_t gab = grid_rows(n, (int)(F / VV), kArgPasses);
+                if (gab > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV, A, kArgPasses>), dim3((unsigned)gab), dim3(256), 0, st,
+                                   Xt, nx, ct, w, rt, out, n, R, F, ap);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (gX) {  // max only (sum and mean gather over the transposed list)
