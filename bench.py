@@ -335,6 +335,32 @@ def suite(reps: int):
     print(json.dumps({"suite": "graphconv 2-layer training step, Graph with a kept transposed list",
                       "ms": round(ms_c, 3), "torch_index_add_ms": round(ms_t, 3),
                       "speedup_vs_torch": round(ms_t / ms_c, 2)}), flush=True)
+    del layers
+    # two GIN layers (learned eps) on the same graph without weights, with a kept transposed list
+    gin = torch.nn.ModuleList([ga.GINConv(128, 128, train_eps=True), ga.GINConv(128, 64, train_eps=True)]).to(dev)
+    graph_u = ga.Graph(col, row, R4)
+
+    def step_gin():
+        gin.zero_grad(set_to_none=True)
+        h = torch.relu(gin[0](X, graph_u))
+        loss = ((gin[1](h, graph_u) - target) ** 2).mean()
+        loss.backward()
+
+    def gin_torch(layer, z):
+        u = (1.0 + layer.eps) * z + torch.zeros_like(z).index_add_(0, row, z[col])
+        return layer.lin2(torch.relu(layer.lin1(u)))
+
+    def step_gin_torch():
+        gin.zero_grad(set_to_none=True)
+        h = torch.relu(gin_torch(gin[0], X))
+        loss = ((gin_torch(gin[1], h) - target) ** 2).mean()
+        loss.backward()
+
+    ms_gi, _ = timed(step_gin, 1 << 40)
+    ms_gt, _ = timed(step_gin_torch, 1 << 40)
+    print(json.dumps({"suite": "gin 2-layer training step (SpMM graph without weights, 128-128-64, kept list)",
+                      "ms": round(ms_gi, 3), "torch_index_add_ms": round(ms_gt, 3),
+                      "speedup_vs_torch": round(ms_gt / ms_gi, 2)}), flush=True)
     host_probe()
 
 

@@ -179,3 +179,39 @@ class GraphConv(torch.nn.Module):
         z = RowsLinear.apply(h, self.lin.weight)
         out = gather_scatter(z, col, weight, row, num_nodes, self.reduce, graph)
         return out + self.bias if self.bias is not None else out
+
+
+class GINConv(torch.nn.Module):
+    """h' = MLP((1 + eps) * h + sum_{e: row[e] = v} h[col[e]]): a graph isomorphism network layer
+    whose neighbour sum is one fused gather (no edge weights, no message tensor).
+
+    The edge list is sorted by row (the destination) and sources and destinations are the same
+    nodes. The MLP is Linear-ReLU-Linear with the node-count products of RowsLinear; eps is a
+    learned scalar when train_eps, else a fixed one."""
+
+    def __init__(self, in_features: int, out_features: int, hidden: int | None = None, eps: float = 0.0,
+                 train_eps: bool = False):
+        super().__init__()
+        hidden = hidden or out_features
+        self.lin1 = torch.nn.Linear(in_features, hidden)
+        self.lin2 = torch.nn.Linear(hidden, out_features)
+        e = torch.tensor([float(eps)])
+        if train_eps:
+            self.eps = torch.nn.Parameter(e)
+        else:
+            self.register_buffer("eps", e)
+
+    def forward(self, h, col, row=None, num_nodes: int | None = None):
+        """forward(h, graph) with a Graph (its weights are not used), or forward(h, col, row, num_nodes)."""
+        graph = None
+        if isinstance(col, Graph):
+            graph = col
+            col, row, num_nodes = graph.col, graph.row, graph.num_nodes
+            if graph.weight is not None:   # the transposed list would carry the weights
+                graph = None
+        if h.shape[0] != num_nodes:
+            raise ValueError("a GIN layer needs one feature row per node (sources = destinations)")
+        agg = gather_scatter(h, col, None, row, num_nodes, "sum", graph)
+        z = (1.0 + self.eps) * h + agg
+        z = torch.relu(RowsLinear.apply(z, self.lin1.weight) + self.lin1.bias)
+        return RowsLinear.apply(z, self.lin2.weight) + self.lin2.bias

@@ -78,3 +78,44 @@ def test_graph_cache_follows_weight_updates():
     w.mul_(2.0)
     b = g.transposed("sum")[2]
     assert torch.equal(torch.sort(b).values, torch.sort(2.0 * a).values)
+
+
+@pytest.mark.parametrize("cached", [False, True])
+def test_gin_training_step(cached):
+    """Two GIN layers (learned eps) on an unweighted graph: loss and every parameter gradient
+    against the same model with torch index_add in fp64 on the CPU."""
+    n, F, H, C = 2500, 16, 24, 4
+    q = random_gather_problem(321, 30000, n, n, F, "zipf", "normal", False, 0.05)
+    row, col, X = q["index"], q["col"], q["X"]
+    y = np.random.default_rng(322).integers(0, C, n)
+    torch.manual_seed(323)
+    m = torch.nn.ModuleList([ga.GINConv(F, H, eps=0.1, train_eps=True), ga.GINConv(H, C, train_eps=True)])
+    ref = [ga.GINConv(F, H, eps=0.1, train_eps=True), ga.GINConv(H, C, train_eps=True)]
+    for a, b in zip(m, ref):
+        b.load_state_dict(a.state_dict())
+    m = m.to(DEV)
+    ref = [r.double() for r in ref]
+    rt, ct = torch.from_numpy(row).to(DEV), torch.from_numpy(col).to(DEV)
+    xt = torch.from_numpy(X).to(DEV)
+    if cached:
+        g = ga.Graph(ct, rt, n)
+        logits = m[1](torch.relu(m[0](xt, g)), g)
+    else:
+        logits = m[1](torch.relu(m[0](xt, ct, rt, n)), ct, rt, n)
+    loss = torch.nn.functional.cross_entropy(logits, torch.from_numpy(y).to(DEV))
+    loss.backward()
+
+    def layer(r, z):
+        agg = torch.zeros(n, z.shape[1], dtype=torch.float64).index_add(0, torch.from_numpy(row),
+                                                                        z[torch.from_numpy(col)])
+        u = (1.0 + r.eps) * z + agg
+        return r.lin2(torch.relu(r.lin1(u)))
+
+    lr = layer(ref[1], torch.relu(layer(ref[0], torch.from_numpy(X).double())))
+    loss_r = torch.nn.functional.cross_entropy(lr, torch.from_numpy(y))
+    loss_r.backward()
+    assert abs(loss.item() - loss_r.item()) <= 1e-4 * max(1.0, abs(loss_r.item()))
+    for a, b in zip(m, ref):
+        for (name, pa), pb in zip(a.named_parameters(), b.parameters()):
+            ga_, gb_ = pa.grad.double().cpu(), pb.grad
+            assert torch.allclose(ga_, gb_, rtol=2e-3, atol=2e-5), (name, cached, (ga_ - gb_).abs().max())
