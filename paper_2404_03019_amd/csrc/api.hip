@@ -919,8 +919,11 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
         if (tp.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
         // The transposed list gathers the destination rows, which repeat as often as the rows'
         // edge counts and stay in cache: no column tiles in sequence (on the SpMM graph, 3.41 ms
-        // over the kept list without them, 3.55 ms with two).
+        // over the kept list without them, 3.55 ms with two), and longer row runs per group
+        // (there, one 128-column tile: 64 rows 3.16 ms, 128 rows 3.05-3.12, 256 rows 3.01, 512
+        // rows 3.00, 1,024 rows 3.06).
         untile(&c);
+        if (nnz >= ((int64_t)1 << 20) && c.family == GEOT_FAMILY_EP && c.rows != 0 && c.rows < 256) c.rows = 256;
         Resolved r;
         s = resolve(tp, c, &r, true);
         if (s != GEOT_SUCCESS) return s;
