@@ -1,6 +1,6 @@
 """GPU parity at the size limits: more than 2^31 rows (64-bit row and chunk
 arithmetic, 64-bit counts in the partial levels), one segment of more than
-2^31 rows, and a fused call over more than 2^31 edges.
+2^31 rows, and a fused call over more than 2^31 edges (forward and gradients).
 
 Inputs are built on the GPU with torch's seeded generator (ternary values, so
 every partial sum below 2^24 is exact in fp32); the oracle runs on the rows of
@@ -120,6 +120,32 @@ def test_fused_more_than_2_31_edges():
         for op in ("sum", "max"):
             ref = oracle.gather_scatter(Xh, c, None, z, 1, op)
             assert np.array_equal(got[op][r:r + 1], ref), (op, r)
+    # The gradients of the sum over the same edges (unit weights): grad_X through the bucketed
+    # transposition of more than 2^31 records, grad_w over more than 2^31 edges. grad_out is
+    # ternary, so every partial sum is an integer below 2^24 and exact in any order.
+    g = ternary(R, F, 14)
+    w = torch.ones(BIG, device=DEV)
+    gx, gw = geot.gather_scatter_backward(X, col, w, row, g, "sum")
+    say("limits: 2^31+ edges, gradients")
+    gh = g.cpu().numpy()
+    # grad_X depends on the edges only through the multiplicity of each (row, column) pair: the
+    # oracle takes the distinct pairs as edges weighted by their multiplicity
+    mult = torch.zeros(R * nx, dtype=torch.int64, device=DEV)
+    step = 1 << 28
+    for a in range(0, BIG, step):
+        mult += torch.bincount(row[a:a + step] * nx + col[a:a + step], minlength=R * nx)
+    mult = mult.cpu().numpy()
+    pairs = np.nonzero(mult)[0]                       # row-major: sorted by row
+    assert int(mult.sum()) == BIG and int(mult.max()) < (1 << 24)
+    rx, _ = oracle.gather_scatter_backward(Xh, pairs % nx, mult[pairs].astype(np.float32), pairs // nx, gh, "sum")
+    assert np.array_equal(gx.cpu().numpy(), rx.astype(np.float32)), "grad_X over 2^31+ edges"
+    # grad_w on sampled edges (the first, the last, and random ones; sorted, so rows stay sorted)
+    rng = np.random.default_rng(15)
+    es = np.unique(np.concatenate([[0, BIG - 1], rng.integers(0, BIG, 20000)]))
+    et = torch.from_numpy(es).to(DEV)
+    _, rw = oracle.gather_scatter_backward(Xh, col[et].cpu().numpy(), np.ones(es.size, dtype=np.float32),
+                                           row[et].cpu().numpy(), gh, "sum")
+    assert np.array_equal(gw[et].cpu().numpy(), rw.astype(np.float32)), "grad_w over 2^31+ edges"
 
 
 def test_most_segments():
