@@ -318,3 +318,45 @@ def test_gather_autograd_bf16_int32(op):
         xf, wf = grads["f32", use_graph]
         assert torch.allclose(xb, xf.to(torch.bfloat16).float(), rtol=2 ** -7, atol=1e-5), (op, use_graph)
         assert torch.allclose(wb, wf, rtol=1e-4, atol=1e-5), (op, use_graph)
+
+
+def test_typed_backward_misaligned_and_empty():
+    """Gradients over a bf16 X (and src) view that starts 2 bytes into its buffer, so only
+    2-byte loads are allowed, F = 16; and empty edge lists with int32 ids."""
+    q = random_gather_problem(58, 9000, 600, 700, 16, "zipf", "int", True, 0.05)
+    t, wide = stored(q["X"], "bf16")
+    buf = torch.empty(t.numel() + 1, dtype=torch.bfloat16, device=DEV)
+    X = buf[1:].view(t.shape)
+    X.copy_(t.to(DEV))
+    assert X.data_ptr() % 4 == 2
+    col, row = ids(q["col"], "i32"), ids(q["index"], "i32")
+    w = torch.from_numpy(q["weight"]).to(DEV)
+    g = np.random.default_rng(59).standard_normal((600, 16)).astype(np.float32)
+    for op in OPS:
+        say(f"misaligned bf16 gather backward {op}")
+        out = geot.gather_scatter(X, col, w, row, 600, op)
+        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, out)
+        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy())
+        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy(),
+                                                absolute=True)
+        for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
+            err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+            assert np.all(err <= 1e-5 * terms + 1e-6), f"misaligned {what} {op}"
+    p = random_problem(60, 7000, 400, 16, "zipf", "int", 0.1)
+    ts, sw = stored(p["src"], "bf16")
+    sb = torch.empty(ts.numel() + 1, dtype=torch.bfloat16, device=DEV)
+    src = sb[1:].view(ts.shape)
+    src.copy_(ts.to(DEV))
+    i32 = ids(p["index"], "i32")
+    gs = np.random.default_rng(61).standard_normal((400, 16)).astype(np.float32)
+    out = geot.segment_reduce(src, i32, 400, "max")
+    got = geot.segment_reduce_backward(torch.from_numpy(gs).to(DEV), i32, "max", src, out)
+    ref = oracle.segment_reduce_backward(gs, p["index"], "max", sw, out.cpu().numpy())
+    assert torch.equal(got.cpu(), torch.from_numpy(ref).to(torch.bfloat16)), "misaligned bf16 segment max"
+    # no edges: grad_X is zero, grad_w empty; no rows: grad_src empty
+    e32 = torch.empty(0, dtype=torch.int32, device=DEV)
+    gx, gw = geot.gather_scatter_backward(X, e32, torch.empty(0, device=DEV), e32,
+                                          torch.from_numpy(g).to(DEV), "sum")
+    assert gx.shape == (700, 16) and torch.count_nonzero(gx).item() == 0 and gw.numel() == 0
+    e = geot.segment_reduce_backward(torch.from_numpy(gs).to(DEV), e32, "mean", dtype=torch.bfloat16)
+    assert e.shape == (0, 16) and e.dtype == torch.bfloat16
