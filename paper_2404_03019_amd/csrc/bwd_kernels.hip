@@ -730,9 +730,12 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__
 }
 
 // fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
-// mean divides afterwards, in scale_by_count_kernel). Every thread runs all passes (the group
-// reduction is uniform); the edges' ids load first, then both operand rows of every pass, then
-// the products.
+// mean divides afterwards, in scale_by_count_kernel). A row group takes P consecutive edges
+// (rows are sorted, so they mostly share their grad_out row); every thread runs all of them (the
+// group reduction is uniform). The edges' ids load first, then every edge's X row and, once per
+// run of edges with the same row, the grad_out row (and for max its recipients), then the
+// products. Loading grad_out for every edge cost the SpMM graph 0.9 of 6.6 ms: the rows come
+// from cache, but about 25 times each.
 template <int E, typename I, int V, int OP, int P, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                        const I *__restrict__ col,
@@ -742,11 +745,12 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
                                                        int64_t F, float *__restrict__ gw) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec, P);
+    const int64_t e0 = ((int64_t)blockIdx.x * m.rows + m.rsub) * P;   // this group's first edge
     int64_t rr[P], cc[P];
     bool ok[P];
 #pragma unroll
     for (int q = 0; q < P; ++q) {
-        const int64_t e = m.row(q);
+        const int64_t e = e0 + q;
         rr[q] = e < n ? (int64_t)row[e] : -1;
         cc[q] = e < n ? (int64_t)col[e] : -1;
     }
@@ -755,50 +759,61 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
         ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx;
     static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
     float acc[P];
-    if (nvec <= m.tpr) {  // one vector per thread and row: all loads of the block's passes in flight together
+    if (nvec <= m.tpr) {  // one vector per thread and edge: all loads of the group's edges in flight together
         // X rows stay in their loaded words until the products (16-bit X: half the registers of
         // widened rows; bf16 / int32 on the SpMM graph held 92 VGPRs, 5 waves per SIMD, widened)
+        const bool lane = m.j0 < nvec;
+        bool lead[P];   // the first edge of a run with the same (valid) row: loads the row
         float g[P][V];
+        A a[P][V];
         Raw<E, V> rx[P];
 #pragma unroll
         for (int q = 0; q < P; ++q) {
-            if (ok[q] && m.j0 < nvec) {
-                load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
+            lead[q] = !(q > 0 && ok[q - 1] && rr[q] == rr[q - 1]);
+            if (ok[q] && lane) {
                 load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx[q]);
             } else {
                 rx[q] = Raw<E, V>{};
+            }
+            if (ok[q] && lane && lead[q]) {
+                load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
+                if constexpr (OP == GEOT_BWD_MAX) load_arg<A, V>(arg + rr[q] * F + (int64_t)m.j0 * V, a[q]);
+            } else {
 #pragma unroll
-                for (int k = 0; k < V; ++k) g[q][k] = 0.0f;
+                for (int k = 0; k < V; ++k) {
+                    g[q][k] = 0.0f;
+                    a[q][k] = (A)~(A)0;
+                }
             }
         }
-        if constexpr (OP == GEOT_BWD_MAX) {
-            // max: the recipients load with the operand rows (16-byte pairs where V >= 2), and
-            // the other edges' products are masked out
-#pragma unroll
-            for (int q = 0; q < P; ++q) {
-                if (!(ok[q] && m.j0 < nvec)) continue;
-                A a[V];
-                load_arg<A, V>(arg + rr[q] * F + (int64_t)m.j0 * V, a);
-                const A e = (A)m.row(q);
-#pragma unroll
-                for (int k = 0; k < V; ++k)
-                    if (a[k] != e) g[q][k] = 0.0f;
-            }
-        }
+        float cur[V];
+        A ca[V];
 #pragma unroll
         for (int q = 0; q < P; ++q) {
+            if (lead[q]) {
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    cur[k] = g[q][k];
+                    ca[k] = a[q][k];
+                }
+            }
             float x[V];
             widen<E, V>(rx[q], x);
             acc[q] = 0.0f;
+            const A e = (A)(e0 + q);
 #pragma unroll
-            for (int k = 0; k < V; ++k) acc[q] += g[q][k] * x[k];
+            for (int k = 0; k < V; ++k) {
+                // max: the other edges' products are masked out
+                const float gk = OP == GEOT_BWD_MAX && ca[k] != e ? 0.0f : cur[k];
+                acc[q] += gk * x[k];
+            }
         }
     } else {
 #pragma unroll
         for (int q = 0; q < P; ++q) {
             acc[q] = 0.0f;
             if (!ok[q]) continue;
-            const int64_t e = m.row(q);
+            const int64_t e = e0 + q;
             for (int j = m.j0; j < nvec; j += m.tpr) {
                 float g[V], x[V];
                 load_f32<V>(gout + rr[q] * F + (int64_t)j * V, g);
@@ -817,7 +832,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
     for (int q = 0; q < P; ++q) {
         float a = acc[q];
         for (int d = m.tpr / 2; d >= 1; d >>= 1) a += __shfl_xor(a, d, 64);
-        const int64_t e = m.row(q);
+        const int64_t e = e0 + q;
         if (e < n && m.j0 == 0) {
             gw[e] = ok[q] ? a : 0.0f;
         }
