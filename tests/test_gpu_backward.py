@@ -59,21 +59,40 @@ def test_segment_backward_parity(case):
             assert np.array_equal(got, ref), f"segment backward {op} seed={seed} F={F}"
 
 
+def _offsets_case(case):
+    """(src, index, S, F) of a gradient case that takes its segments from the offsets: at least
+    64 MB of grad_src and segments averaging at least a block's rows (128 at F = 32, fp32)."""
+    seed, kind, F = case
+    if kind == "tiny_then_long":
+        # 2,000 segments of 0 or 1 rows first (a block spans several hundred segment ends: its
+        # rows read their ids), then 1,000 segments of about 3,000 rows
+        rng = np.random.default_rng(seed)
+        L = np.concatenate([(rng.random(2000) < 0.2).astype(np.int64), rng.integers(2500, 3500, 1000)])
+        idx = np.repeat(np.arange(L.size), L)
+        src = rng.integers(-3, 4, (idx.size, F)).astype(np.float32)
+        return src, idx, L.size, F
+    nnz, S, dist, ef = {"one_heavy": (6_000_000, 40_000, "one_heavy", 0.3),
+                        "zipf": (4_000_000, 20_000, "zipf", 0.2),
+                        "one_segment": (700_001, 1, "uniform", 0.0)}[kind]
+    p = random_problem(seed, nnz, S, F, dist, "int", ef)   # integer values: max ties
+    return p["src"], p["index"], S, F
+
+
 @pytest.mark.parametrize("case", [
-    (8, 600_000, 40_000, 32, "zipf", 0.3),          # 77 MB of grad_src: sum takes the offsets pass too
-    (9, 600_000, 3_000_000, 32, "uniform", 0.9),    # blocks spanning > 255 segment ends, long empty runs
-    (10, 300_000, 20_000, 64, "one_heavy", 0.2),
-    (11, 700_001, 1, 32, "uniform", 0.0),           # one segment: every block lies in it, ragged last block
-], ids=lambda c: f"seed{c[0]}-S{c[2]}")
+    (8, "one_heavy", 32),        # one segment of most rows, many short and empty ones
+    (9, "tiny_then_long", 32),   # blocks spanning > 255 segment ends
+    (10, "zipf", 64),
+    (11, "one_segment", 32),     # every block lies in it; ragged last block
+], ids=lambda c: f"seed{c[0]}-{c[1]}")
 def test_segment_backward_from_offsets(case):
     """Large gradients: each row's segment comes from the offsets (staged per block) rather than
     the ids; sum and max bit-exact, mean within the bound, against the oracle."""
-    seed, nnz, S, F, dist, ef = case
-    p = random_problem(seed, nnz, S, F, dist, "int", ef)   # integer values: max ties
-    src, idx = p["src"], p["index"]
+    src, idx, S, F = _offsets_case(case)
+    seed = case[0]
+    assert src.nbytes >= (64 << 20) and idx.size >> (7 if F == 32 else 6) >= S
     g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
     for op in ("sum", "mean", "max"):
-        say(f"segment backward from offsets seed={seed} S={S} {op}")
+        say(f"segment backward from offsets seed={seed} {case[1]} {op}")
         out = geot.segment_reduce(up(src), up(idx), S, op) if op == "max" else None
         got = geot.segment_reduce_backward(up(g), up(idx), op, up(src) if out is not None else None,
                                            out).cpu().numpy()
@@ -81,7 +100,7 @@ def test_segment_backward_from_offsets(case):
         if op == "mean":
             within(got, ref, np.abs(ref.astype(np.float64)), f"mean seed={seed}")
         else:
-            assert np.array_equal(got, ref), f"sum seed={seed}"
+            assert np.array_equal(got, ref), f"{op} seed={seed}"
 
 
 GS_CASES = [

@@ -199,7 +199,7 @@ BWD_CASES = [
     (42, 15000, 700, 3, "lognormal", "normal", 0.05),  # 1-wide
     (43, 12000, 500, 12, "uniform", "int", 0.2),       # 4-wide; integer values tie under max
     (44, 8000, 300, 6, "one_heavy", "int", 0.1),       # 2-wide
-    (45, 1_200_000, 50_000, 32, "zipf", "normal", 0.3),  # >= 64 MB of grad_src: sum also from the offsets
+    (45, 4_000_000, 10_000, 32, "zipf", "normal", 0.3),  # >= 64 MB, segments of >= a block's rows: offsets
 ]
 HALF_ULP = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11, "f32": 2.0 ** -23}
 # one rounding in the subnormal range is absolute: half the spacing 2^-24 of binary16's
