@@ -226,8 +226,11 @@ geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int6
  * Sum and max copy values (exact); mean multiplies by the fp32 reciprocal of
  * the count (two roundings, within 1e-5 relative). Deterministic.
  * Same argument checks as geot_segment_reduce; grad_src must not overlap the
- * inputs. Temporary memory: (num_segments + 1) int64 for mean, num_segments *
- * F uint64 for max, from the per-stream buffer.                              */
+ * inputs. Temporary memory, from the per-stream buffer: for max num_segments *
+ * F row numbers (uint32 below 2^32 - 1 rows, else uint64); for mean, and from
+ * 64 MB of grad_src where the segments average at least one block of rows (16
+ * to 1,024 rows by F), (num_segments + 1) int64 segment starts, in the latter
+ * case with 16 bytes per block.                                              */
 geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
                                            int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
                                            const float *src, const float *out, float *grad_src,
@@ -256,7 +259,9 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
  * which takes another 16 bytes per edge and 12 bytes per bucket and 32,768
  * edges) and runs the forward gather kernel
  * over it, so every row of grad_X is written without float atomics; for max
- * only the recipients' terms are added, atomically.
+ * only the recipients' terms are added, atomically, from a temporary table of
+ * num_rows * F recipient edge numbers (4 bytes each below 2^32 - 1 edges, else
+ * 8; the same pool), and mean takes (num_rows + 1) int64 row starts.
  *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
  *   out          [num_rows x F]: the forward result (read for max only)
  *   grad_X       [num_x_rows x F] fp32 or NULL (skipped), overwritten:
