@@ -729,7 +729,7 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
     const int64_t blocks = seg_bwd_blocks(nnz, F, V);
     GapList gaps;
     if (mx || from_off) {
-        geot_status_t s = stream_scratch(o_first + (from_off ? (size_t)blocks * 16 : 0), st, &scratch,
+        geot_status_t s = stream_scratch(o_first + (use_first ? (size_t)blocks * 16 : 0), st, &scratch,
                                          from_off ? &gaps : nullptr, &ctx);
         if (s != GEOT_SUCCESS) return s;
     }
