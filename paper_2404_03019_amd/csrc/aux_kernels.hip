@@ -24,8 +24,65 @@ __global__ __launch_bounds__(256) void fill_kernel(float *out, int64_t rows, int
 // first[2b] and first[2b + 1] (the segments a block of the gradient kernels
 // starts and ends in).
 template <typename I>
+constexpr int kOffsetsRowsPerThread = 64 / (int)sizeof(I);
+
+template <typename I>
 __global__ __launch_bounds__(256) void offsets_kernel(const I *idx, int64_t n, int64_t S,
                                                       int64_t *off, GapList gaps, int64_t *first, int shift) {
+    auto put = [&](int64_t lo, int64_t hi, int64_t row) {  // off[lo, hi) = row
+        lo = max(lo, (int64_t)0);
+        hi = min(hi, S + 1);
+        if (hi - lo > kGapRun && gap_push(gaps, lo, hi, row, 0, 0, 1)) return;
+        for (int64_t t = lo; t < hi; ++t) off[t] = row;
+    };
+    auto row_done = [&](int64_t i, int64_t s, int64_t sp) {
+        if (s != sp) put(sp + 1, s + 1, i);
+        if (i == n - 1) put(s + 1, S + 1, n);
+        if (first) {   // ids of the first and the last row of each block of 2^shift rows
+            const int64_t mask = ((int64_t)1 << shift) - 1;
+            if ((i & mask) == 0) first[2 * (i >> shift)] = s;
+            if ((i & mask) == mask || i == n - 1) first[2 * (i >> shift) + 1] = s;
+        }
+    };
+    // kOffsetsRowsPerThread<I> consecutive ids (64 bytes) per thread in 16-byte loads (idx
+    // 16-byte aligned; the launcher checks); the id before them comes from the next lower lane,
+    // lane 0 loads its own
+    constexpr int kR = kOffsetsRowsPerThread<I>;
+    const int lane = threadIdx.x & 63;
+    for (int64_t b0 = (int64_t)blockIdx.x * (256 * kR); b0 < n; b0 += (int64_t)gridDim.x * (256 * kR)) {
+        const int64_t base = b0 + (int64_t)threadIdx.x * kR;
+        int64_t cur[kR];
+        if (base + kR <= n) {
+#pragma unroll
+            for (int v = 0; v < kR * (int)sizeof(I) / 16; ++v) {
+                if constexpr (sizeof(I) == 8) {
+                    const longlong2 a = *reinterpret_cast<const longlong2 *>(idx + base + 2 * v);
+                    cur[2 * v] = a.x; cur[2 * v + 1] = a.y;
+                } else {
+                    const int4 a = *reinterpret_cast<const int4 *>(idx + base + 4 * v);
+                    cur[4 * v] = a.x; cur[4 * v + 1] = a.y; cur[4 * v + 2] = a.z; cur[4 * v + 3] = a.w;
+                }
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kR; ++k) cur[k] = base + k < n ? (int64_t)idx[base + k] : 0;
+        }
+        int64_t prev = __shfl_up((long long)cur[kR - 1], 1u, 64);
+        if (lane == 0) prev = base > 0 && base - 1 < n ? (int64_t)idx[base - 1] : -1;
+#pragma unroll
+        for (int k = 0; k < kR; ++k) {
+            const int64_t i = base + k;
+            if (i >= n) break;
+            row_done(i, cur[k], k == 0 ? prev : cur[k - 1]);
+        }
+    }
+}
+
+// The same with one id per thread and step, for an index that is not 16-byte aligned.
+template <typename I>
+__global__ __launch_bounds__(256) void offsets_unaligned_kernel(const I *idx, int64_t n, int64_t S,
+                                                                int64_t *off, GapList gaps, int64_t *first,
+                                                                int shift) {
     auto put = [&](int64_t lo, int64_t hi, int64_t row) {  // off[lo, hi) = row
         lo = max(lo, (int64_t)0);
         hi = min(hi, S + 1);
@@ -38,7 +95,7 @@ __global__ __launch_bounds__(256) void offsets_kernel(const I *idx, int64_t n, i
         const int64_t sp = i > 0 ? (int64_t)idx[i - 1] : -1;
         if (s != sp) put(sp + 1, s + 1, i);
         if (i == n - 1) put(s + 1, S + 1, n);
-        if (first) {   // ids of the first and the last row of each block of 2^shift rows
+        if (first) {
             const int64_t mask = ((int64_t)1 << shift) - 1;
             if ((i & mask) == 0) first[2 * (i >> shift)] = s;
             if ((i & mask) == mask || i == n - 1) first[2 * (i >> shift) + 1] = s;
@@ -144,16 +201,26 @@ hipError_t launch_fill(float *out, int64_t rows, int64_t F, int64_t ld, float va
 hipError_t launch_offsets(const int64_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
                           hipStream_t stream, int64_t *first, int shift) {
     if (n <= 0 || shift < 0 || shift > 40) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(offsets_kernel<int64_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
-                       idx, n, S, off, gaps, first, shift);
+    if (((uintptr_t)idx & 15) == 0)
+        hipLaunchKernelGGL(offsets_kernel<int64_t>, dim3(grid_for(n, 256 * kOffsetsRowsPerThread<int64_t>, 1 << 20)),
+                           dim3(256), 0, stream,
+                           idx, n, S, off, gaps, first, shift);
+    else
+        hipLaunchKernelGGL(offsets_unaligned_kernel<int64_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0,
+                           stream, idx, n, S, off, gaps, first, shift);
     return hipGetLastError();
 }
 
 hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t *off, GapList gaps,
                               hipStream_t stream, int64_t *first, int shift) {
     if (n <= 0 || shift < 0 || shift > 40) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(offsets_kernel<int32_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0, stream,
-                       idx, n, S, off, gaps, first, shift);
+    if (((uintptr_t)idx & 15) == 0)
+        hipLaunchKernelGGL(offsets_kernel<int32_t>, dim3(grid_for(n, 256 * kOffsetsRowsPerThread<int32_t>, 1 << 20)),
+                           dim3(256), 0, stream,
+                           idx, n, S, off, gaps, first, shift);
+    else
+        hipLaunchKernelGGL(offsets_unaligned_kernel<int32_t>, dim3(grid_for(n, 256 * 4, 1 << 20)), dim3(256), 0,
+                           stream, idx, n, S, off, gaps, first, shift);
     return hipGetLastError();
 }
 
