@@ -249,3 +249,24 @@ def test_transpose_mean_with_rows_out_of_range(n):
     got = np.lexsort((cf[keep].view(np.uint32), rt[keep], sc[keep]))
     assert np.array_equal(rt[keep][got], row[ok][want]) and np.array_equal(sc[keep][got], col[ok][want])
     assert np.array_equal(cf[keep][got].view(np.uint32), coef[want].view(np.uint32))
+
+
+@pytest.mark.parametrize("itype", [torch.int64, torch.int32])
+def test_offsets_pass_unaligned_index(itype):
+    """An index view one element into its buffer (not 16-byte aligned) takes the per-row offsets
+    pass: mean gradients and the index statistics equal the aligned call's and the oracle's."""
+    p = random_problem(21, 300_000, 9000, 8, "zipf", "normal", 0.2)
+    idx = p["index"]
+    buf = torch.empty(idx.size + 1, dtype=itype, device=DEV)
+    view = buf[1:]
+    view.copy_(torch.from_numpy(idx).to(itype))
+    assert view.data_ptr() % 16 != 0
+    g = np.random.default_rng(22).standard_normal((9000, 8)).astype(np.float32)
+    got = geot.segment_reduce_backward(up(g), view, "mean").cpu().numpy()
+    aligned = geot.segment_reduce_backward(up(g), torch.from_numpy(idx).to(itype).to(DEV), "mean").cpu().numpy()
+    assert np.array_equal(got, aligned)
+    ref = oracle.segment_reduce_backward(g, idx, "mean")
+    within(got, ref, np.abs(ref.astype(np.float64)), "unaligned index mean")
+    if itype == torch.int64:
+        st, ref_st = geot.index_stats(view, 9000), oracle.index_stats(idx, 9000)
+        assert st["max_len"] == ref_st["max_len"] and st["num_empty"] == ref_st["num_empty"]
