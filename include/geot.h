@@ -258,10 +258,13 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
  * with 129 to 2^23 X rows the edges are first grouped by buckets of columns,
  * which takes another 16 bytes per edge and 12 bytes per bucket and 32,768
  * edges) and runs the forward gather kernel
- * over it, so every row of grad_X is written without float atomics; for max
- * only the recipients' terms are added, atomically, from a temporary table of
- * num_rows * F recipient edge numbers (4 bytes each below 2^32 - 1 edges, else
- * 8; the same pool), and mean takes (num_rows + 1) int64 row starts.
+ * over it, so every row of grad_X is written without float atomics. Max
+ * first finds each (row, feature)'s recipient edge into a temporary table of
+ * num_rows * F edge numbers (4 bytes each below 2^32 - 1 edges, else 8; the
+ * same pool); below 2^32 - 1 edges and 2^31 X rows each row of grad_X then
+ * sums the terms of its column's records whose edge is the recipient (the same
+ * transposed list), else the recipients' terms are added atomically. Mean
+ * takes (num_rows + 1) int64 row starts.
  *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
  *   out          [num_rows x F]: the forward result (read for max only)
  *   grad_X       [num_x_rows x F] fp32 or NULL (skipped), overwritten:

@@ -854,7 +854,10 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     // temporaries from the stream-ordered pool (the forward call below uses the per-stream buffer):
     // row starts (mean), max recipients (max), the transposed edge list (grad_X for sum and mean)
     const bool mean = op == GEOT_OP_MEAN, mx = op == GEOT_OP_MAX;
-    const bool transpose = grad_X && !mx;
+    // max: grad_X pulled over the transposed list where its records are packed (X below 2^31
+    // rows) and the recipients 32-bit; otherwise one atomic add per recipient
+    const bool pull = mx && grad_X && num_x_rows <= (int64_t)INT32_MAX && seg_bwd_arg32(nnz);
+    const bool transpose = grad_X && (!mx || pull);
     size_t at = 0;
     auto take = [&](size_t b) { const size_t o = at; at = align256(at + b); return o; };
     const size_t o_roff = mean ? take((size_t)(num_rows + 1) * 8) : 0;
@@ -863,7 +866,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
     const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
     const size_t o_sums = transpose ? take((size_t)((nx + 4095) / 4096 + 1) * 8) : 0;
-    // the transposed list: 16-byte records {col, row, coefficient, 0} with int32 ids, or
+    // the transposed list: 16-byte records {col, row, coefficient, edge} with int32 ids, or
     // (X with 2^31 rows or more) three arrays
     const bool packed = nx <= (int64_t)INT32_MAX;
     const size_t o_rec = transpose && packed ? take((size_t)nnz * 16) : 0;
@@ -898,9 +901,9 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
         if (s != GEOT_SUCCESS) return s;
     }
     const int bop = op == GEOT_OP_SUM ? GEOT_BWD_SUM : (mean ? GEOT_BWD_MEAN : GEOT_BWD_MAX);
-    // weights (and, for max, X through atomic adds of the recipients only)
+    // weights (and, for max where it is not pulled, X through atomic adds of the recipients only)
     GEOT_HIP(launch_gs_bwd(X, elem, num_x_rows, col, idx32, weight, sorted_row, roff, out, grad_out, nnz, num_rows,
-                           F, V, bop, arg, mx ? grad_X : nullptr, grad_weight, st),
+                           F, V, bop, arg, mx && !pull ? grad_X : nullptr, grad_weight, st),
              "launch fused backward kernels");
     if (transpose) {
         // grad_X = gather_scatter of grad_out over the edges sorted by col (sum of coef * grad_out rows)
@@ -912,6 +915,14 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
                                   (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, rec,
                                   bucket_b ? base + o_bucket : nullptr, st),
                  "launch transpose kernels");
+        if (pull) {
+            GEOT_HIP(launch_gs_bwd_x_max_pull(rec, (const int64_t *)(base + o_off), arg, grad_out, nx, num_rows, F, V,
+                                              grad_X, st),
+                     "launch max pull kernel");
+            void *p_pull = sg.p;
+            sg.p = nullptr;
+            return scratch_free(p_pull, st);
+        }
         Problem tp{true, grad_out, num_rows, row_t, w_t, key_t, nnz, nx, F, GEOT_OP_SUM, grad_X};
         if (packed) {
             tp.idx = rec;

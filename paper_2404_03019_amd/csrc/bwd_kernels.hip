@@ -741,6 +741,62 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__
     }
 }
 
+// fused form, max, w.r.t. X, pulled over the transposed list: a row group per X row c walks the
+// records of column c (16-byte records {column, row, coefficient, edge}, sorted by column;
+// column starts in off) and sums coefficient * grad_out[row, f] over the features f whose
+// recipient is that edge. Every row of grad_X is written once: no fill and no float atomics
+// (on the SpMM graph 313 M of them, about 10 ms). Records load kU at a time.
+template <int V>
+__global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *__restrict__ rec,
+                                                                const int64_t *__restrict__ off,
+                                                                const unsigned *__restrict__ arg,
+                                                                const float *__restrict__ gout, int64_t nx, int64_t R,
+                                                                int64_t F, float *__restrict__ gX) {
+    constexpr int kU = 4;
+    const int nvec = (int)(F / V);
+    const RowMap m = row_map(nvec);
+    for (int q = 0; q < kPasses; ++q) {
+        const int64_t c = m.row(q);
+        if (c >= nx) break;
+        const int64_t lo = off[c], hi = off[c + 1];
+        for (int j = m.j0; j < nvec; j += m.tpr) {
+            float acc[V];
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[k] = 0.0f;
+            for (int64_t k0 = lo; k0 < hi; k0 += kU) {
+                int4 t[kU];
+#pragma unroll
+                for (int u = 0; u < kU; ++u)
+                    t[u] = k0 + u < hi ? *reinterpret_cast<const int4 *>(rec + 4 * (k0 + u)) : make_int4(0, -1, 0, 0);
+                float g[kU][V];
+                unsigned a[kU][V];
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const int64_t r = (int64_t)t[u].y;
+                    if ((uint64_t)r < (uint64_t)R) {
+                        load_f32<V>(gout + r * F + (int64_t)j * V, g[u]);
+                        load_arg<unsigned, V>(arg + r * F + (int64_t)j * V, a[u]);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < V; ++k) {
+                            g[u][k] = 0.0f;
+                            a[u][k] = ~0u;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const float coef = __int_as_float(t[u].z);
+#pragma unroll
+                    for (int k = 0; k < V; ++k)
+                        if (a[u][k] == (unsigned)t[u].w) acc[k] += coef * g[u][k];
+                }
+            }
+            store_vec<V>(gX + c * F + (int64_t)j * V, acc);
+        }
+    }
+}
+
 // fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
 // mean divides afterwards, in scale_by_count_kernel). A row group takes P consecutive edges
 // (rows are sorted, so they mostly share their grad_out row); every thread runs all of them (the
@@ -974,7 +1030,7 @@ __global__ __launch_bounds__(256) void place_kernel(const I *col, int64_t nx, co
         float coef = w ? w[e] : 1.0f;
         if (mean && (uint64_t)r < (uint64_t)nrows) coef = coef / (float)(roff[r + 1] - roff[r]);
         if constexpr (PACKED) {
-            *reinterpret_cast<int4 *>(rec + 4 * pos) = make_int4((int)c, (int)r, __float_as_int(coef), 0);
+            *reinterpret_cast<int4 *>(rec + 4 * pos) = make_int4((int)c, (int)r, __float_as_int(coef), (int)(uint32_t)e);
         } else {
             key_t[pos] = c;
             row_t[pos] = r;
@@ -1051,7 +1107,7 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const I *col, int64
             float coef = wt[u];
             if (mean && (uint64_t)r[u] < (uint64_t)nrows) coef = coef / (float)(roff[r[u] + 1] - roff[r[u]]);
             *reinterpret_cast<int4 *>(tmp + 4 * (int64_t)pos) =
-                make_int4((int)c[u], (int)r[u], __float_as_int(coef), 0);
+                make_int4((int)c[u], (int)r[u], __float_as_int(coef), (int)(uint32_t)(b0 + u * 256 + threadIdx.x));
         }
     }
 }
@@ -1063,7 +1119,8 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const I *col, int64
 template <bool PACKED>
 __global__ __launch_bounds__(256) void bucket_sort_kernel(const int32_t *tmp, const int64_t *boff, int64_t nblk,
                                                           const int64_t *total, int shift, int nbuckets,
-                                                          int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec) {
+                                                          int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
+                                                          int64_t nx, int64_t *col_off) {
     constexpr int kU = 8;
     __shared__ unsigned h[kBucketCols];
     __shared__ unsigned s_t[256];
@@ -1124,8 +1181,11 @@ __global__ __launch_bounds__(256) void bucket_sort_kernel(const int32_t *tmp, co
     for (int k = 0; k < kPer; ++k) {
         const int c = threadIdx.x * kPer + k;
         if (c < ncols) h[c] = run;
+        // column starts (for the max gradient's pull over the columns)
+        if (col_off && c < ncols && ((int64_t)b << shift) + c < nx) col_off[((int64_t)b << shift) + c] = lo + run;
         run += v[k];
     }
+    if (col_off && threadIdx.x == 0 && b == nbuckets - 1) col_off[nx] = hi;
     __syncthreads();
     for (int64_t i0 = lo; i0 < hi; i0 += 256 * kU) {
         int4 rv[kU];
@@ -1230,7 +1290,7 @@ namespace {
 template <typename I>
 hipError_t launch_transpose_bucketed(const I *col, int64_t nx, const I *row, const float *w,
                                      const int64_t *roff, int64_t nrows, bool mean, int64_t n, int64_t *key_t, int64_t *row_t,
-                                     float *w_t, int32_t *rec, char *scratch, hipStream_t st) {
+                                     float *w_t, int32_t *rec, char *scratch, int64_t *col_off, hipStream_t st) {
     int shift, nb;
     int64_t nblk;
     const int64_t len = bucket_words(n, nx, &shift, &nb, &nblk);
@@ -1253,10 +1313,10 @@ hipError_t launch_transpose_bucketed(const I *col, int64_t nx, const I *row, con
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (rec)
         hipLaunchKernelGGL(bucket_sort_kernel<true>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
-                           shift, nb, key_t, row_t, w_t, rec);
+                           shift, nb, key_t, row_t, w_t, rec, nx, col_off);
     else
         hipLaunchKernelGGL(bucket_sort_kernel<false>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
-                           shift, nb, key_t, row_t, w_t, rec);
+                           shift, nb, key_t, row_t, w_t, rec, nx, col_off);
     return hipGetLastError();
 }
 
@@ -1267,7 +1327,7 @@ hipError_t launch_transpose_t(const I *col, int64_t nx, const I *row, const floa
                               char *bucket_scratch, hipStream_t st) {
     if (bucket_scratch && transpose_scratch_bytes(n, nx) > 0)
         return launch_transpose_bucketed(col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec, bucket_scratch,
-                                         st);
+                                         off, st);
     hipError_t e = launch_zero_u64((unsigned long long *)counts, (nx + 1) / 2, st);
     if (e != hipSuccess) return e;
     const int64_t geb = (n + 256 * kPasses - 1) / (256 * kPasses);
@@ -1299,6 +1359,25 @@ hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int id
                                   nrows, mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
     return launch_transpose_t(static_cast<const int64_t *>(col), nx, static_cast<const int64_t *>(row), w, roff, nrows,
                               mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
+}
+
+hipError_t launch_gs_bwd_x_max_pull(const int32_t *rec, const int64_t *off, const void *arg, const float *gout,
+                                    int64_t nx, int64_t R, int64_t F, int V, float *gX, hipStream_t st) {
+    if (nx <= 0 || F <= 0) return hipSuccess;
+    if (!(V == 1 || V == 2 || V == 4 || V == 8) || F % V != 0) return hipErrorInvalidValue;
+    const int64_t gb = grid_rows(nx, (int)(F / V));
+    if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    const unsigned g = (unsigned)gb;
+    const unsigned *a = static_cast<const unsigned *>(arg);
+    if (V == 8)
+        hipLaunchKernelGGL(gs_bwd_x_max_pull_kernel<8>, dim3(g), dim3(256), 0, st, rec, off, a, gout, nx, R, F, gX);
+    else if (V == 4)
+        hipLaunchKernelGGL(gs_bwd_x_max_pull_kernel<4>, dim3(g), dim3(256), 0, st, rec, off, a, gout, nx, R, F, gX);
+    else if (V == 2)
+        hipLaunchKernelGGL(gs_bwd_x_max_pull_kernel<2>, dim3(g), dim3(256), 0, st, rec, off, a, gout, nx, R, F, gX);
+    else
+        hipLaunchKernelGGL(gs_bwd_x_max_pull_kernel<1>, dim3(g), dim3(256), 0, st, rec, off, a, gout, nx, R, F, gX);
+    return hipGetLastError();
 }
 
 hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t *row_t, float *w_t,

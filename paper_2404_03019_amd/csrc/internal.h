@@ -152,10 +152,11 @@ hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t 
 // the row's edge count for mean; roff = row starts) of the transposed problem.
 // counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
 // With rec != nullptr (needs nx and the rows < 2^31) each edge is one 16-byte record
-// {int32 key, int32 row, float coefficient, 0} at rec[4 * slot] and key_t, row_t, w_t are unused.
-// bucket_scratch (transpose_scratch_bytes(n, nx) bytes, or nullptr) lets large inputs group the
-// edges by buckets of columns and sort each bucket in LDS (no global atomic per edge); counts,
-// off and sums are then unused.
+// {int32 key, int32 row, float coefficient, uint32 edge number (its low 32 bits)} at
+// rec[4 * slot] and key_t, row_t, w_t are unused. bucket_scratch (transpose_scratch_bytes(n, nx)
+// bytes, or nullptr) lets large inputs group the edges by buckets of columns and sort each bucket
+// in LDS (no global atomic per edge); counts and sums are then unused. Either way off[c] (nx + 1
+// entries) ends as the start of column c's records.
 // col and row are int32 when idx32, else int64.
 hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int idx32, const float *w,
                             const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
@@ -163,6 +164,10 @@ hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int id
                             char *bucket_scratch, hipStream_t st);
 // scratch of the bucketed transposition (0: the input takes the direct one)
 size_t transpose_scratch_bytes(int64_t n, int64_t nx);
+// fused form, max, w.r.t. X from the packed transposed list (rec, column starts off, both from
+// launch_transpose) and the 32-bit recipients arg [R x F]: grad_X written whole, no atomics
+hipError_t launch_gs_bwd_x_max_pull(const int32_t *rec, const int64_t *off, const void *arg, const float *gout,
+                                    int64_t nx, int64_t R, int64_t F, int V, float *gX, hipStream_t st);
 
 // grad_src[i] = grad_out[idx[i]] (divided by the segment length from off when mean), stored in
 // the source's ElemType `elem` (16-bit: rounded to nearest even); idx int32 when idx32. V is 1,

@@ -270,3 +270,20 @@ def test_offsets_pass_unaligned_index(itype):
     if itype == torch.int64:
         st, ref_st = geot.index_stats(view, 9000), oracle.index_stats(idx, 9000)
         assert st["max_len"] == ref_st["max_len"] and st["num_empty"] == ref_st["num_empty"]
+
+
+@pytest.mark.parametrize("weighted", [True, False])
+def test_gather_backward_max_bucketed(weighted):
+    """Max gradient w.r.t. X pulled over a bucketed transposed list (2,000,000 edges): each X
+    row sums its column's records whose edge is the recipient; integer values, so ties are
+    frequent and the lowest-edge rule decides. Both gradients against the oracle's."""
+    q = random_gather_problem(23, 2_000_000, 50_000, 60_000, 8, "zipf", "int", weighted, 0.05)
+    X, col, w, row = q["X"], q["col"], q["weight"], q["index"]
+    g = np.random.default_rng(24).standard_normal((50_000, 8)).astype(np.float32)
+    out = geot.gather_scatter(up(X), up(col), up(w), up(row), 50_000, "max")
+    gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", out)
+    rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out.cpu().numpy())
+    ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out.cpu().numpy(), absolute=True)
+    within(gx.cpu().numpy(), rx, ax, f"bucketed max grad_X weighted={weighted}")
+    if weighted:
+        within(gw.cpu().numpy(), rw, aw, "bucketed max grad_w")
