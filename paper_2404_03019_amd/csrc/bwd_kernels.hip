@@ -741,6 +741,90 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__
     }
 }
 
+// fused form, max: the recipients by runs of consecutive edges. A row group takes kArgRun
+// consecutive edges and walks them in order, keeping in registers, per feature, the first edge
+// whose rounded term equals out; at each change of row it stores that row's recipients: plainly
+// for a row wholly inside the run, with atomicMin for the run's first and last rows, which may
+// continue into the neighbouring runs (the lowest over the runs is then the lowest attaining
+// edge). No LDS table and no barrier: the slot-table kernel above ran 3.9 M blocks of 16 edges
+// on the SpMM graph. For one vector per thread (nvec <= 64); X rows of kArgBatch edges load
+// together.
+constexpr int kArgRun = 32;
+constexpr int kArgBatch = 4;
+template <int E, typename I, int V, typename A>
+__global__ __launch_bounds__(256) void gs_bwd_max_arg_run_kernel(const typename ElemT<E>::T *__restrict__ X,
+                                                                 int64_t nx, const I *__restrict__ col,
+                                                                 const float *__restrict__ w,
+                                                                 const I *__restrict__ row,
+                                                                 const float *__restrict__ out, int64_t n, int64_t R,
+                                                                 int64_t F, A *arg) {
+    const int nvec = (int)(F / V);
+    const RowMap m = row_map(nvec, 1);
+    if (m.j0 >= nvec) return;   // no barrier below
+    const int64_t e0 = ((int64_t)blockIdx.x * m.rows + m.rsub) * kArgRun;
+    if (e0 >= n) return;
+    const int64_t e1 = min(e0 + (int64_t)kArgRun, n);
+    const int64_t row_before = e0 > 0 ? (int64_t)row[e0 - 1] : -1;
+    const int64_t row_after = e1 < n ? (int64_t)row[e1] : -1;
+    const A none = (A)~(A)0;
+    int64_t cur = -1;   // row of the edges walked so far
+    A best[V];
+    float o[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        best[k] = none;
+        o[k] = 0.0f;
+    }
+    auto flush = [&]() {
+        if ((uint64_t)cur >= (uint64_t)R) return;
+        const bool shared = cur == row_before || cur == row_after;
+        A *a = arg + cur * F + (int64_t)m.j0 * V;
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            if (best[k] == none) continue;
+            if (shared) atomicMin(a + k, best[k]);
+            else a[k] = best[k];
+        }
+    };
+    for (int64_t b = e0; b < e1; b += kArgBatch) {
+        int64_t rr[kArgBatch], cc[kArgBatch];
+        float wt[kArgBatch];
+        Raw<E, V> rx[kArgBatch];
+#pragma unroll
+        for (int u = 0; u < kArgBatch; ++u) {
+            const int64_t e = b + u;
+            rr[u] = e < e1 ? (int64_t)row[e] : -1;
+            cc[u] = e < e1 ? (int64_t)col[e] : -1;
+            wt[u] = e < e1 && w ? w[e] : 1.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < kArgBatch; ++u)
+            if ((uint64_t)rr[u] < (uint64_t)R && (uint64_t)cc[u] < (uint64_t)nx)
+                load_raw<E, V>(X + cc[u] * F + (int64_t)m.j0 * V, rx[u]);
+#pragma unroll
+        for (int u = 0; u < kArgBatch; ++u) {
+            const int64_t e = b + u;
+            if (e >= e1) break;
+            if (rr[u] != cur) {   // a new row: store the last one's recipients, load this one's output
+                flush();
+                cur = rr[u];
+#pragma unroll
+                for (int k = 0; k < V; ++k) best[k] = none;
+                if ((uint64_t)cur < (uint64_t)R) load_f32<V>(out + cur * F + (int64_t)m.j0 * V, o);
+            }
+            if ((uint64_t)rr[u] >= (uint64_t)R || (uint64_t)cc[u] >= (uint64_t)nx) continue;
+            float x[V];
+            widen<E, V>(rx[u], x);
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                const float t = w ? wt[u] * x[k] : x[k];  // the forward's term: one rounded product
+                if (t == o[k] && best[k] == none) best[k] = (A)e;
+            }
+        }
+    }
+    flush();
+}
+
 // fused form, max, w.r.t. X, pulled over the transposed list: a row group per X row c walks the
 // records of column c (16-byte records {column, row, coefficient, edge}, sorted by column;
 // column starts in off) and sums coefficient * grad_out[row, f] over the features f whose
@@ -1233,9 +1317,15 @@ __global__ __launch_bounds__(256) void fill_u64_kernel(unsigned long long *p, in
 }
 
 // blocks of kPasses * (256 / tpr) rows; the callers check the count fits a grid
-int64_t grid_rows(int64_t rows, int nvec, int passes = kPasses) {
+// threads per row of the row-parallel kernels (row_map's tpr)
+int row_threads(int nvec) {
     int t = 1;
     while (t < nvec && t < 64) t <<= 1;
+    return t;
+}
+
+int64_t grid_rows(int64_t rows, int nvec, int passes = kPasses) {
+    const int t = row_threads(nvec);
     const int64_t per_block = (int64_t)passes * (256 / t);
     const int64_t b = (rows + per_block - 1) / per_block;
     return b < 1 ? 1 : b;
@@ -1540,10 +1630,18 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
             if (op == GEOT_BWD_MAX) {
                 e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (R * F + 1) / 2 : R * F, ~0ull, st);
                 if (e != hipSuccess) return e;
-                const int64_t gab = grid_rows(n, (int)(F / VV), kArgPasses);
-                if (gab > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-                hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV, A, kArgPasses>), dim3((unsigned)gab), dim3(256), 0, st,
-                                   Xt, nx, ct, w, rt, out, n, R, F, ap);
+                if (F / VV <= 64) {   // one vector per thread: runs of consecutive edges
+                    const int64_t groups = 256 / (int64_t)row_threads((int)(F / VV));
+                    const int64_t gab = (n + groups * kArgRun - 1) / (groups * kArgRun);
+                    if (gab > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                    hipLaunchKernelGGL((gs_bwd_max_arg_run_kernel<E, I, VV, A>), dim3((unsigned)gab), dim3(256), 0, st,
+                                       Xt, nx, ct, w, rt, out, n, R, F, ap);
+                } else {
+                    const int64_t gab = grid_rows(n, (int)(F / VV), kArgPasses);
+                    if (gab > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                    hipLaunchKernelGGL((gs_bwd_max_arg_kernel<E, I, VV, A, kArgPasses>), dim3((unsigned)gab), dim3(256),
+                                       0, st, Xt, nx, ct, w, rt, out, n, R, F, ap);
+                }
                 if ((e = hipGetLastError()) != hipSuccess) return e;
             }
             if (gX) {  // max only (sum and mean gather over the transposed list)
