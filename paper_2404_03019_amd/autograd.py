@@ -193,8 +193,9 @@ class GINConv(torch.nn.Module):
     whose neighbour sum is one fused gather (no edge weights, no message tensor).
 
     The edge list is sorted by row (the destination) and sources and destinations are the same
-    nodes. The MLP is Linear-ReLU-Linear with the node-count products of RowsLinear; eps is a
-    learned scalar when train_eps, else a fixed one."""
+    nodes. The MLP is Linear-ReLU-Linear with the node-count products of RowsLinear; where its
+    first layer narrows the features it runs before the sum (the same map, since it is linear and
+    the sum unweighted). eps is a learned scalar when train_eps, else a fixed one."""
 
     def __init__(self, in_features: int, out_features: int, hidden: int | None = None, eps: float = 0.0,
                  train_eps: bool = False):
@@ -218,7 +219,13 @@ class GINConv(torch.nn.Module):
                 graph = None
         if h.shape[0] != num_nodes:
             raise ValueError("a GIN layer needs one feature row per node (sources = destinations)")
-        agg = gather_scatter(h, col, None, row, num_nodes, "sum", graph)
-        z = (1.0 + self.eps) * h + agg
-        z = torch.relu(RowsLinear.apply(z, self.lin1.weight) + self.lin1.bias)
+        if self.lin1.out_features < self.lin1.in_features:
+            # the first linear map commutes with the (unweighted) neighbour sum: applied first, the
+            # gather and its gradient move hidden columns instead of input ones
+            h = RowsLinear.apply(h, self.lin1.weight)
+            z = (1.0 + self.eps) * h + gather_scatter(h, col, None, row, num_nodes, "sum", graph) + self.lin1.bias
+        else:
+            z = (1.0 + self.eps) * h + gather_scatter(h, col, None, row, num_nodes, "sum", graph)
+            z = RowsLinear.apply(z, self.lin1.weight) + self.lin1.bias
+        z = torch.relu(z)
         return RowsLinear.apply(z, self.lin2.weight) + self.lin2.bias
