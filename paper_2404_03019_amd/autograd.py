@@ -164,7 +164,8 @@ class RowsLinear(torch.autograd.Function):
 
 
 class GraphConv(torch.nn.Module):
-    """h' = aggregate_{e: row[e] = v} w_e * (h W)[col[e]] + b, with the aggregation fused.
+    """h' = aggregate_{e: row[e] = v} w_e * (h W)[col[e]] + b, with the aggregation fused (for sum
+    and mean, which are linear, the aggregation runs first where W widens the features).
 
     With w_e = 1 / sqrt(deg(row[e]) * deg(col[e])) and self-loops in the edge
     list this is a GCN layer; with reduce="mean" and no weights a GraphSAGE-style
@@ -183,8 +184,11 @@ class GraphConv(torch.nn.Module):
         if isinstance(col, Graph):
             graph = col
             col, row, num_nodes, weight = graph.col, graph.row, graph.num_nodes, graph.weight
-        z = RowsLinear.apply(h, self.lin.weight)
-        out = gather_scatter(z, col, weight, row, num_nodes, self.reduce, graph)
+        if self.reduce != "max" and self.lin.out_features > self.lin.in_features:
+            # sum and mean are linear: aggregating before a widening transform moves the narrower rows
+            out = RowsLinear.apply(gather_scatter(h, col, weight, row, num_nodes, self.reduce, graph), self.lin.weight)
+        else:
+            out = gather_scatter(RowsLinear.apply(h, self.lin.weight), col, weight, row, num_nodes, self.reduce, graph)
         return out + self.bias if self.bias is not None else out
 
 
