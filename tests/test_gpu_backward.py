@@ -110,6 +110,7 @@ GS_CASES = [
     (14, 8000, 300, 3000, 128, "one_heavy", "normal", True),
     (15, 5000, 400, 400, 17, "poisson", "int", True),
     (16, 6000, 500, 600, 6, "zipf", "int", True),        # 2-wide vectors, ties
+    (17, 3000, 200, 400, 300, "zipf", "int", True),      # 75 vectors a row: more than a row's 64 threads
 ]
 
 
