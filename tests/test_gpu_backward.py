@@ -73,7 +73,8 @@ def _offsets_case(case):
         return src, idx, L.size, F
     nnz, S, dist, ef = {"one_heavy": (6_000_000, 40_000, "one_heavy", 0.3),
                         "zipf": (4_000_000, 20_000, "zipf", 0.2),
-                        "one_segment": (700_001, 1, "uniform", 0.0)}[kind]
+                        "one_segment": (700_001, 1, "uniform", 0.0),
+                        "wide": (300_000, 1000, "zipf", 0.1)}[kind]
     p = random_problem(seed, nnz, S, F, dist, "int", ef)   # integer values: max ties
     return p["src"], p["index"], S, F
 
@@ -83,13 +84,14 @@ def _offsets_case(case):
     (9, "tiny_then_long", 32),   # blocks spanning > 255 segment ends
     (10, "zipf", 64),
     (11, "one_segment", 32),     # every block lies in it; ragged last block
+    (12, "wide", 300),           # 75 vectors a row: more than a row's 64 threads, 16 rows a block
 ], ids=lambda c: f"seed{c[0]}-{c[1]}")
 def test_segment_backward_from_offsets(case):
     """Large gradients: each row's segment comes from the offsets (staged per block) rather than
     the ids; sum and max bit-exact, mean within the bound, against the oracle."""
     src, idx, S, F = _offsets_case(case)
     seed = case[0]
-    assert src.nbytes >= (64 << 20) and idx.size >> (7 if F == 32 else 6) >= S
+    assert src.nbytes >= (64 << 20) and idx.size >> {32: 7, 64: 6, 300: 4}[F] >= S
     g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
     for op in ("sum", "mean", "max"):
         say(f"segment backward from offsets seed={seed} {case[1]} {op}")
