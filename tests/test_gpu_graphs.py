@@ -87,3 +87,58 @@ def test_gather_scatter_replays():
         say(f"graph replay {k} gather_scatter max")
         ref, terms = oracle_gather(x, c, ww, r, R, "max")
         compare(out.cpu().numpy(), ref, "max", terms, f"gather replay {k}")
+
+
+@pytest.mark.parametrize("op", ["sum", "mean", "max"])
+@pytest.mark.parametrize("shape", [(3000, 200_000, 8), (600_000, 2000, 32)], ids=["ids", "offsets"])
+def test_segment_backward_replays(op, shape):
+    """The segment gradient captured once: with the ids read directly (few rows, long runs of
+    empty segments through the gap list), and from 64 MB through the offsets pass and each
+    block's first and last ids; max also through its recipient table."""
+    import oracle
+    n, S, F = shape
+    rng = np.random.default_rng(72)
+    src = torch.empty((n, F), device=DEV)
+    idx = torch.empty(n, dtype=torch.int64, device=DEV)
+    g = torch.empty((S, F), device=DEV)
+    out = torch.empty((S, F), device=DEV)
+    gs = torch.empty((n, F), device=DEV)
+
+    def refill():
+        i = np.sort(rng.integers(0, S, n)).astype(np.int64)
+        v = rng.integers(-3, 4, (n, F)).astype(np.float32)   # integer values: max ties
+        gg = rng.standard_normal((S, F)).astype(np.float32)
+        idx.copy_(torch.from_numpy(i))
+        src.copy_(torch.from_numpy(v))
+        g.copy_(torch.from_numpy(gg))
+        if op == "max":
+            geot.segment_reduce(src, idx, S, "max", out=out)
+        torch.cuda.synchronize()
+        return i, v, gg
+
+    def call():
+        geot.segment_reduce_backward(g, idx, op, src if op == "max" else None, out if op == "max" else None,
+                                     grad_src=gs)
+
+    st = torch.cuda.Stream()
+    refill()
+    with torch.cuda.stream(st):
+        call()
+    st.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=st):
+        call()
+    for k in range(3):
+        i, v, gg = refill()
+        gs.fill_(5.0)   # eager work between replays; the replay overwrites every row
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        say(f"graph replay {k} segment backward {op} n={n}")
+        ref = oracle.segment_reduce_backward(gg, i, op, v, out.cpu().numpy() if op == "max" else None)
+        got = gs.cpu().numpy()
+        if op == "mean":
+            err = np.abs(got.astype(np.float64) - ref)
+            assert np.all(err <= 1e-5 * np.abs(ref) + 1e-6), f"replay {k} mean"
+        else:
+            assert np.array_equal(got, ref), f"replay {k} {op}"
