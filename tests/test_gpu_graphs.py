@@ -142,3 +142,55 @@ def test_segment_backward_replays(op, shape):
             assert np.all(err <= 1e-5 * np.abs(ref) + 1e-6), f"replay {k} mean"
         else:
             assert np.array_equal(got, ref), f"replay {k} {op}"
+
+
+@pytest.mark.parametrize("op", ["sum", "mean", "max"])
+def test_gather_backward_replays(op):
+    """Both gradients of the fused form captured once (temporaries from the stream-ordered
+    pool, the transposition, the recipients for max) and replayed with new inputs: every
+    replay within the fp32 bound of the oracle."""
+    import oracle
+    R, nx, F, n = 3000, 2000, 8, 40000
+    rng = np.random.default_rng(73)
+    X = torch.empty((nx, F), device=DEV)
+    col = torch.empty(n, dtype=torch.int64, device=DEV)
+    row = torch.empty(n, dtype=torch.int64, device=DEV)
+    w = torch.empty(n, device=DEV)
+    g = torch.empty((R, F), device=DEV)
+    out = torch.empty((R, F), device=DEV)
+
+    def refill():
+        r = np.sort(rng.integers(0, R, n)).astype(np.int64)
+        c = rng.integers(0, nx, n).astype(np.int64)
+        x = rng.integers(-3, 4, (nx, F)).astype(np.float32)   # integer values: max ties
+        ww = rng.integers(1, 4, n).astype(np.float32)
+        gg = rng.standard_normal((R, F)).astype(np.float32)
+        for t, a in ((row, r), (col, c), (X, x), (w, ww), (g, gg)):
+            t.copy_(torch.from_numpy(a))
+        if op == "max":
+            geot.gather_scatter(X, col, w, row, R, "max", out=out)
+        torch.cuda.synchronize()
+        return x, c, ww, r, gg
+
+    def call():
+        return geot.gather_scatter_backward(X, col, w, row, g, op, out if op == "max" else None)
+
+    st = torch.cuda.Stream()
+    refill()
+    with torch.cuda.stream(st):
+        call()
+    st.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=st):
+        gx, gw = call()
+    for k in range(3):
+        x, c, ww, r, gg = refill()
+        graph.replay()
+        torch.cuda.synchronize()
+        say(f"graph replay {k} gather backward {op}")
+        o = out.cpu().numpy() if op == "max" else None
+        rx, rw = oracle.gather_scatter_backward(x, c, ww, r, gg, op, o)
+        ax, aw = oracle.gather_scatter_backward(x, c, ww, r, gg, op, o, absolute=True)
+        for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
+            err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
+            assert np.all(err <= 1e-5 * terms + 1e-6), f"replay {k} {op} {what}"
