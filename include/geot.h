@@ -51,6 +51,11 @@
  *    calling thread.
  *  - Accumulation is fp32. Sum and mean differ from an fp64 reference by at
  *    most 1e-5 * sum|terms| + 1e-6 per element; max is exact.
+ *  - Max is the IEEE 754-2019 maximum operation folded over a segment: a NaN
+ *    member makes the result NaN, and +0 ranks above -0 (a segment of -0 and +0
+ *    gives +0). The operation is commutative and associative, so the result
+ *    does not depend on the order in which a kernel combines rows. The paper
+ *    does not define these cases; this is the library's reading.
  */
 #ifndef GEOT_H
 #define GEOT_H
@@ -221,6 +226,8 @@ geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int6
  *   mean: grad_src[i, :] = grad_out[s, :] / (rows of segment s), s = sorted_index[i]
  *   max:  grad_out[s, f] goes to the first row i of segment s (lowest index)
  *         with src[i, f] == out[s, f]; every other element of grad_src is 0.
+ *         The test is ==, so either zero attains a zero maximum, and a NaN
+ *         maximum routes no gradient.
  *         src and out (the forward result) are read for max only (may be NULL
  *         otherwise).
  * Sum and max copy values (exact); mean multiplies by the fp32 reciprocal of

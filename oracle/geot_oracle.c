@@ -20,8 +20,11 @@
  *  - empty segments produce 0.0f for sum, mean and max;
  *  - sum and mean accumulate in fp64 and round once to fp32 at the end;
  *    mean divides the fp64 sum by the row (edge) count in fp64;
- *  - max starts from the first member and keeps a strictly larger value, in
- *    fp32; a max never rounds, so it is exact;
+ *  - max is the IEEE 754-2019 maximum operation folded over the members, in fp32
+ *    (a NaN member makes the result NaN; +0 ranks above -0); a max never rounds,
+ *    so it is exact. The paper does not say what max does with NaN or signed
+ *    zeros; this operation is order-independent, so every reduction order the
+ *    GPU may take has the same answer;
  *  - a weighted term is one fp32 multiply w[e] * x (round to nearest even);
  *    without weights the term is x itself;
  *  - the output is overwritten in full (not accumulated into).
@@ -31,7 +34,8 @@
  *  - segment reduction w.r.t. src: sum copies grad_out[idx[i]] to row i; mean
  *    divides it by the segment length (fp64 division, rounded once); max
  *    routes grad_out[s, f] to the first row of segment s (lowest index) whose
- *    src[i, f] equals out[s, f], every other row gets 0;
+ *    src[i, f] equals out[s, f] (compared with ==, so either zero matches a zero
+ *    maximum and a NaN maximum routes nothing), every other row gets 0;
  *  - fused form w.r.t. X: grad_X[c] = sum over edges e with col[e] == c of
  *    coef(e) * grad_out[row[e]] with coef = w[e] (1 without weights), divided
  *    by the row's edge count for mean; for max only the first edge of each
@@ -86,6 +90,16 @@ static float term(const float *rows, int64_t F, const int64_t *col, const float 
     return t;
 }
 
+/* IEEE 754-2019 maximum(a, b): NaN when either operand is NaN, otherwise the
+ * larger value, with +0 taken as larger than -0. */
+static float maximum(float a, float b)
+{
+    if (isnan(a)) return a;
+    if (isnan(b)) return b;
+    if (a == b) return signbit(a) ? b : a; /* equal: the same value, or zeros of either sign */
+    return a > b ? a : b;
+}
+
 /* Shared body of both operations: for each segment s and feature f reduce the
  * terms of rows start[s]..start[s+1]-1 with op. */
 static void reduce_segments(const float *rows, int64_t F, const int64_t *col, const float *w,
@@ -102,7 +116,7 @@ static void reduce_segments(const float *rows, int64_t F, const int64_t *col, co
                 float m = term(rows, F, col, w, b, f);
                 for (int64_t i = b + 1; i < e; ++i) {
                     float t = term(rows, F, col, w, i, f);
-                    if (t > m) m = t;
+                    m = maximum(m, t);
                 }
                 result = m;
             } else {

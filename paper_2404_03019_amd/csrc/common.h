@@ -16,12 +16,16 @@ __device__ __forceinline__ float red_neutral() {
     return RED == RED_SUM ? 0.0f : -INFINITY;
 }
 
+// Max is the IEEE 754-2019 maximum operation: a NaN operand gives NaN, and +0 ranks
+// above -0. It is commutative and associative, so the result of a segment does not
+// depend on the order in which its rows are combined (v_maximum3_f32 on gfx950, one
+// instruction, where fmaxf drops NaN and leaves the sign of a zero to the order).
 template <int RED>
 __device__ __forceinline__ float red_apply(float a, float b) {
     if constexpr (RED == RED_SUM) {
         return a + b;
     } else {
-        return fmaxf(a, b);
+        return __builtin_elementwise_maximum(a, b);
     }
 }
 

@@ -284,6 +284,35 @@ def pin_errors(impl):
         raise AssertionError("no error for column out of range")
 
 
+def pin_max_nan_and_signed_zeros(impl):
+    """Max is the IEEE 754-2019 maximum folded over a segment (the paper is silent on NaN and
+    on the sign of zero): a NaN member gives NaN wherever it sits, +0 ranks above -0 in either
+    order, a segment of only -0 gives -0, and infinities order as numbers. Hand-listed cases,
+    compared as fp32 bit patterns; the fused form forms its terms first (w = -1 turns +0
+    into -0)."""
+    nan, inf = np.float32(np.nan), np.float32(np.inf)
+    cases = [
+        ([1.0, nan, 5.0], "nan"), ([nan, 1.0], "nan"), ([2.0, 3.0, nan], "nan"),
+        ([-0.0, 0.0], 0.0), ([0.0, -0.0], 0.0), ([-0.0, -0.0], -0.0), ([-0.0], -0.0),
+        ([-1.0, -0.0, -2.0], -0.0), ([-inf, -3.0], -3.0), ([inf, nan], "nan"), ([-5.0, inf, 2.0], inf),
+    ]
+    vals = np.array([v for c, _ in cases for v in c], dtype=np.float32).reshape(-1, 1)
+    idx = np.repeat(np.arange(len(cases)), [len(c) for c, _ in cases]).astype(np.int64)
+    got = impl.segment_reduce(vals, idx, len(cases), "max")[:, 0]
+    for k, (c, want) in enumerate(cases):
+        if want == "nan":
+            assert np.isnan(got[k]), f"max of {c} must be NaN"
+        else:
+            assert got[k].view(np.uint32) == np.float32(want).view(np.uint32), f"max of {c}: {got[k]!r}"
+    X = np.array([[0.0], [3.0], [-0.0]], dtype=np.float32)
+    col = np.array([0, 2, 0, 0], dtype=np.int64)
+    w = np.array([-1.0, 1.0, 2.0, -1.0], dtype=np.float32)
+    row = np.array([0, 0, 1, 1], dtype=np.int64)
+    got = impl.gather_scatter(X, col, w, row, 2, "max")[:, 0]
+    # row 0: terms -0 and -0 -> -0; row 1: terms +0 and -0 -> +0
+    assert got.view(np.uint32).tolist() == [0x80000000, 0x00000000], f"fused max of zeros: {got!r}"
+
+
 def pin_abs_term_sum(impl):
     p = random_gather_problem(71, 2000, 100, 50, 3, "zipf", "normal", True, 0.1)
     X, col, w, row, R, L = p["X"], p["col"], p["weight"], p["index"], p["num_segments"], p["lengths"]
@@ -294,6 +323,14 @@ def pin_abs_term_sum(impl):
     assert np.allclose(got, want, rtol=1e-12, atol=0), "abs term sum"
     got_mean = impl.abs_term_sum(X, row, R, "mean", col, w)
     assert np.allclose(got_mean, want / np.maximum(L, 1)[:, None], rtol=1e-12, atol=0), "abs mean"
+    # the segment form: the terms are the rows themselves
+    q = random_problem(72, 3000, 120, 4, "lognormal", "normal", 0.1)
+    src, idx, S, Lq = q["src"], q["index"], q["num_segments"], q["lengths"]
+    want = np.zeros((S, 4))
+    np.add.at(want, idx, np.abs(src.astype(np.float64)))
+    assert np.allclose(impl.abs_term_sum(src, idx, S, "sum"), want, rtol=1e-12, atol=0), "abs segment sum"
+    assert np.allclose(impl.abs_term_sum(src, idx, S, "mean"), want / np.maximum(Lq, 1)[:, None],
+                       rtol=1e-12, atol=0), "abs segment mean"
 
 
 def pin_index_stats(impl):
@@ -414,6 +451,51 @@ def pin_backward_max_ties(impl):
     assert abs(gX.sum() - want_total) <= 1e-9 * max(1.0, abs(want_total)), "fused max recipients"
 
 
+def pin_backward_absolute_terms(impl):
+    """The fused gradients' sums of |terms| (what the gradient tolerance is made of), against
+    numpy's unbuffered add.at of the absolute per-edge terms: |coef(e) * grad_out[row[e], f]|
+    into grad_X[col[e], f] and |grad_out[row[e], f] * X[col[e], f]| into grad_w[e], divided by
+    the row's edge count for mean; for max only the lowest edge of each (row, feature) whose
+    rounded product equals the maximum (found here with numpy's maximum.at) contributes."""
+    rng = np.random.default_rng(98)
+    for weighted in (True, False):
+        q = random_gather_problem(99, 2500, 160, 70, 3, "zipf", "int", weighted, 0.1)
+        X, col, w, row, R, L = q["X"], q["col"], q["weight"], q["index"], q["num_segments"], q["lengths"]
+        n, F = row.size, 3
+        g = rng.standard_normal((R, F)).astype(np.float32)
+        coef = (w if weighted else np.ones(n, dtype=np.float32)).astype(np.float64)
+        msgs = (w[:, None] * X[col]).astype(np.float32) if weighted else X[col]
+        mx = np.full((R, F), -np.inf, dtype=np.float32)
+        np.maximum.at(mx, row, msgs)
+        mx[L == 0] = 0.0
+        starts = np.concatenate([[0], np.cumsum(L)])
+        for op in OPS:
+            use = np.ones((n, F), dtype=bool)
+            if op == "max":
+                use[:] = False
+                for r in np.flatnonzero(L > 0):
+                    for f in range(F):
+                        e = starts[r] + np.flatnonzero(msgs[starts[r]:starts[r + 1], f] == mx[r, f])[0]
+                        use[e, f] = True
+            div = np.maximum(L, 1)[row].astype(np.float64)[:, None] if op == "mean" else 1.0
+            gr = g[row].astype(np.float64)
+            tx = np.where(use, np.abs(coef[:, None] * gr) / div, 0.0)
+            tw = np.where(use, np.abs(gr * X[col].astype(np.float64)) / div, 0.0)
+            want_x = np.zeros((X.shape[0], F))
+            np.add.at(want_x, col, tx)
+            want_w = tw.sum(axis=1)
+            out = impl.gather_scatter(X, col, w, row, R, op) if op == "max" else None
+            ax, aw = impl.gather_scatter_backward(X, col, w, row, g, op, out, absolute=True)
+            assert np.allclose(ax, want_x, rtol=1e-12, atol=0), f"|terms| of grad_X {op} weighted={weighted}"
+            if weighted:
+                assert np.allclose(aw, want_w, rtol=1e-12, atol=0), f"|terms| of grad_w {op}"
+            # and they bound the signed gradients
+            sx, sw = impl.gather_scatter_backward(X, col, w, row, g, op, out)
+            assert np.all(np.abs(sx) <= ax * (1 + 1e-12)), f"|grad_X| <= sum |terms| {op}"
+            if weighted:
+                assert np.all(np.abs(sw) <= aw * (1 + 1e-12)), f"|grad_w| <= sum |terms| {op}"
+
+
 def pin_backward_torch_autograd(impl):
     """torch's autograd of scatter_reduce / index_select on the CPU (tie-free data)."""
     import torch
@@ -456,9 +538,11 @@ ALL_PINS = (
     pin_dense_matmul,
     pin_fusion_equivalence,
     pin_errors,
+    pin_max_nan_and_signed_zeros,
     pin_abs_term_sum,
     pin_index_stats,
     pin_backward_finite_differences,
     pin_backward_max_ties,
+    pin_backward_absolute_terms,
     pin_backward_torch_autograd,
 )

@@ -138,6 +138,47 @@ def test_gather_parity_all_choices(case):
             compare(got, ref, op, terms, f"gather seed={seed} F={F} op={op} choice={ch}")
 
 
+def _special_values(rng, shape, nan_frac):
+    """Values from {+0, -0, +-1, +-2, +-inf} with a fraction of NaNs: ties, zeros of both
+    signs and infinities are frequent, so the max's NaN and signed-zero rules decide."""
+    pool = np.array([0.0, -0.0, 1.0, -1.0, 2.0, -2.0, np.inf, -np.inf, -0.0, 0.0], dtype=np.float32)
+    v = pool[rng.integers(0, pool.size, shape)]
+    v[rng.random(shape) < nan_frac] = np.nan
+    return v
+
+
+@pytest.mark.parametrize("F", [1, 3, 16, 33])
+def test_max_nan_and_signed_zeros_bitwise(F):
+    """Max is IEEE 754-2019 maximum on both sides (NaN propagates, +0 above -0): the GPU
+    result has the oracle's bit pattern (or NaN where the oracle's is NaN) for every kernel
+    choice, in the segment and the fused form, with fp32 and bf16 storage; the max gradient
+    (recipient: the first member == the maximum) matches the oracle exactly."""
+    rng = np.random.default_rng(500 + F)
+    p = random_problem(501 + F, 6000, 700, F, "zipf", "normal", 0.1)
+    idx, S = p["index"], 700
+    for nan_frac in (0.0, 0.002):
+        src = _special_values(rng, (idx.size, F), nan_frac)
+        ref = oracle.segment_reduce(src, idx, S, "max")
+        for ch in RANDOM_CHOICES:
+            say(f"max specials F={F} nan={nan_frac} choice={ch}")
+            compare(run_sr(src, idx, S, "max", ch), ref, "max", None, f"specials F={F} choice={ch}")
+        t16 = torch.from_numpy(src).to(torch.bfloat16)   # +-0, +-inf, NaN and small integers are exact
+        got = geot.segment_reduce(t16.to(DEV), up(idx).to(torch.int32), S, "max").cpu().numpy()
+        compare(got, ref, "max", None, f"specials bf16 F={F}")
+        q = random_gather_problem(502 + F, 5000, 400, 300, F, "lognormal", "normal", True, 0.1)
+        X = _special_values(rng, (300, F), nan_frac)
+        w = np.where(rng.random(q["col"].size) < 0.5, -1.0, 2.0).astype(np.float32)
+        gref = oracle.gather_scatter(X, q["col"], w, q["index"], 400, "max")
+        for ch in RANDOM_CHOICES:
+            compare(run_gs(X, q["col"], w, q["index"], 400, "max", ch), gref, "max", None,
+                    f"fused specials F={F} choice={ch}")
+    src = _special_values(rng, (idx.size, F), 0.0)
+    out = oracle.segment_reduce(src, idx, S, "max")
+    g = rng.standard_normal((S, F)).astype(np.float32)
+    got = geot.segment_reduce_backward(up(g), up(idx), "max", up(src), up(out)).cpu().numpy()
+    assert np.array_equal(got, oracle.segment_reduce_backward(g, idx, "max", src, out)), f"max gradient F={F}"
+
+
 def test_fusion_identity_on_gpu():
     """gather_scatter(X, col, w, row) equals segment_reduce(w * X[col], row) (Section IV):
     bit-exact for max, within the bound for sum and mean."""

@@ -34,7 +34,9 @@ MUTANTS = {
                           "result = -1.0f; /* empty segment */"),
     "columns_reversed": ("out[s * F + f] = result;",
                          "out[s * F + (F - 1 - f)] = result;"),
-    "max_keeps_first": ("if (t > m) m = t;", "if (t > m && i == b) m = t;"),
+    "max_keeps_first": ("m = maximum(m, t);", "if (i < b) m = maximum(m, t);"),
+    "max_drops_nan": ("    if (isnan(a)) return a;\n", ""),
+    "max_zero_sign_by_order": ("if (a == b) return signbit(a) ? b : a;", "if (a == b) return a;"),
     "stats_var_unsquared": ("v += d * d;", "v += d;"),
     "bwd_mean_no_divide": ("r = (float)(g / (double)(e - b));", "r = (float)g;"),
     "bwd_max_last_member": ("} else if (!found && src[i * F + f] == out[s * F + f]) {",
@@ -42,6 +44,8 @@ MUTANTS = {
     "bwd_grad_w_wrong_factor": ("double tx = coef * g, tw = g * x;", "double tx = coef * g, tw = coef * x;"),
     "bwd_grad_x_by_row": ("if (grad_X) grad_X[col[e] * F + f] += tx;",
                           "if (grad_X) grad_X[(r % n_x) * F + f] += tx;"),
+    "bwd_abs_x_signed": ("tx = fabs(tx);", "tx = +tx;"),
+    "bwd_abs_w_signed": ("tw = fabs(tw);", "tw = +tw;"),
 }
 
 RUNNER = r"""
