@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import paper_2404_03019_amd as geot
-from gpu_util import say
+from gpu_util import forward_for_gradient, say
 from workloads import random_gather_problem, random_problem
 
 pytestmark = pytest.mark.gpu
@@ -48,9 +48,11 @@ def test_segment_backward_parity(case):
     g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
     for op in ("sum", "mean", "max"):
         say(f"segment backward seed={seed} F={F} {op}")
-        out_gpu = geot.segment_reduce(up(src), up(idx), S, op)
-        out_np = out_gpu.cpu().numpy()
-        got = geot.segment_reduce_backward(up(g), up(idx), op, up(src), out_gpu).cpu().numpy()
+        out_np = None
+        if op == "max":
+            out_np = forward_for_gradient(oracle.segment_reduce(src, idx, S, op),
+                                          geot.segment_reduce(up(src), up(idx), S, op), f"seed={seed}")
+        got = geot.segment_reduce_backward(up(g), up(idx), op, up(src), up(out_np)).cpu().numpy()
         ref = oracle.segment_reduce_backward(g, idx, op, src, out_np)
         if op == "mean":
             terms = np.abs(ref.astype(np.float64))
@@ -95,10 +97,13 @@ def test_segment_backward_from_offsets(case):
     g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
     for op in ("sum", "mean", "max"):
         say(f"segment backward from offsets seed={seed} {case[1]} {op}")
-        out = geot.segment_reduce(up(src), up(idx), S, op) if op == "max" else None
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.segment_reduce(src, idx, S, op),
+                                       geot.segment_reduce(up(src), up(idx), S, op), f"seed={seed}")
         got = geot.segment_reduce_backward(up(g), up(idx), op, up(src) if out is not None else None,
-                                           out).cpu().numpy()
-        ref = oracle.segment_reduce_backward(g, idx, op, src, None if out is None else out.cpu().numpy())
+                                           up(out)).cpu().numpy()
+        ref = oracle.segment_reduce_backward(g, idx, op, src, out)
         if op == "mean":
             within(got, ref, np.abs(ref.astype(np.float64)), f"mean seed={seed}")
         else:
@@ -124,9 +129,12 @@ def test_gather_backward_parity(case):
     g = np.random.default_rng(seed).standard_normal((R, F)).astype(np.float32)
     for op in ("sum", "mean", "max"):
         say(f"gather backward seed={seed} F={F} {op}")
-        out_gpu = geot.gather_scatter(up(X), up(col), up(w), up(row), R, op)
-        out_np = out_gpu.cpu().numpy()
-        gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op, out_gpu)
+        out_np = None
+        if op == "max":
+            out_np = forward_for_gradient(oracle.gather_scatter(X, col, w, row, R, op),
+                                          geot.gather_scatter(up(X), up(col), up(w), up(row), R, op),
+                                          f"seed={seed}")
+        gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op, up(out_np))
         rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, op, out_np)
         ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, op, out_np, absolute=True)
         within(gx.cpu().numpy(), rx, ax, f"grad_X {op} seed={seed}")
@@ -283,10 +291,11 @@ def test_gather_backward_max_bucketed(weighted):
     q = random_gather_problem(23, 2_000_000, 50_000, 60_000, 8, "zipf", "int", weighted, 0.05)
     X, col, w, row = q["X"], q["col"], q["weight"], q["index"]
     g = np.random.default_rng(24).standard_normal((50_000, 8)).astype(np.float32)
-    out = geot.gather_scatter(up(X), up(col), up(w), up(row), 50_000, "max")
-    gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", out)
-    rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out.cpu().numpy())
-    ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out.cpu().numpy(), absolute=True)
+    out = forward_for_gradient(oracle.gather_scatter(X, col, w, row, 50_000, "max"),
+                               geot.gather_scatter(up(X), up(col), up(w), up(row), 50_000, "max"), "bucketed")
+    gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", up(out))
+    rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out)
+    ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out, absolute=True)
     within(gx.cpu().numpy(), rx, ax, f"bucketed max grad_X weighted={weighted}")
     if weighted:
         within(gw.cpu().numpy(), rw, aw, "bucketed max grad_w")

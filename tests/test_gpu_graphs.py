@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import paper_2404_03019_amd as geot
-from gpu_util import compare, oracle_gather, oracle_segment, say
+from gpu_util import compare, forward_for_gradient, oracle_gather, oracle_segment, say
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -112,7 +112,10 @@ def test_segment_backward_replays(op, shape):
         src.copy_(torch.from_numpy(v))
         g.copy_(torch.from_numpy(gg))
         if op == "max":
-            geot.segment_reduce(src, idx, S, "max", out=out)
+            # the gradient is taken at the oracle's forward result, which the GPU forward must equal
+            o = forward_for_gradient(oracle.segment_reduce(v, i, S, "max"),
+                                     geot.segment_reduce(src, idx, S, "max"), "segment replay")
+            out.copy_(torch.from_numpy(o))
         torch.cuda.synchronize()
         return i, v, gg
 
@@ -168,7 +171,9 @@ def test_gather_backward_replays(op):
         for t, a in ((row, r), (col, c), (X, x), (w, ww), (g, gg)):
             t.copy_(torch.from_numpy(a))
         if op == "max":
-            geot.gather_scatter(X, col, w, row, R, "max", out=out)
+            o = forward_for_gradient(oracle.gather_scatter(x, c, ww, r, R, "max"),
+                                     geot.gather_scatter(X, col, w, row, R, "max"), "gather replay")
+            out.copy_(torch.from_numpy(o))
         torch.cuda.synchronize()
         return x, c, ww, r, gg
 

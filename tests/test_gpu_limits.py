@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_2404_03019_amd as geot
-from gpu_util import compare, say
+from gpu_util import compare, forward_for_gradient, say
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -66,16 +66,26 @@ def test_more_than_2_31_rows():
         # arithmetic, and (max) a 32-bit recipient table holding row numbers above 2^31
         g = torch.from_numpy(np.random.default_rng(12).standard_normal((S, F)).astype(np.float32)).to(DEV)
         gh = g.cpu().numpy()
+        # max: the gradient is taken at a forward result whose sampled rows are the oracle's (each
+        # equal bit for bit to the GPU forward's), so the compared gradients depend on no GPU output
+        gsamp = sample(L, 12, 13)
+        out_max = outs["max"].copy()
+        for s in gsamp:
+            a, b = int(starts[s]), int(starts[s + 1])
+            rows = src[a:b].cpu().numpy()
+            out_max[s:s + 1] = forward_for_gradient(
+                oracle.segment_reduce(rows, np.zeros(b - a, dtype=np.int64), 1, "max"), outs["max"][s:s + 1],
+                f"limits max segment {s}")
         for op in ("sum", "mean", "max"):
-            out = torch.from_numpy(outs[op]).to(DEV) if op == "max" else None
+            out = torch.from_numpy(out_max).to(DEV) if op == "max" else None
             gs = geot.segment_reduce_backward(g, ix, op, src if op == "max" else None, out)
             say(f"limits: 2^31+ rows, gradient {op} ({itype})")
-            for s in sample(L, 12, 13):
+            for s in gsamp:
                 a, b = int(starts[s]), int(starts[s + 1])
                 rows = src[a:b].cpu().numpy()
                 z = np.zeros(b - a, dtype=np.int64)
                 got = gs[a:b].cpu().numpy()
-                ref = oracle.segment_reduce_backward(gh[s:s + 1], z, op, rows, outs[op][s:s + 1])
+                ref = oracle.segment_reduce_backward(gh[s:s + 1], z, op, rows, out_max[s:s + 1])
                 if op == "mean":
                     compare(got, ref, "mean", np.abs(ref.astype(np.float64)), f"limits gradient mean {s}")
                 else:

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_2404_03019_amd as geot
-from gpu_util import compare, oracle_gather, oracle_segment, say
+from gpu_util import compare, forward_for_gradient, oracle_gather, oracle_segment, say
 from workloads import make_config, random_gather_problem, random_problem
 
 pytestmark = pytest.mark.gpu
@@ -30,6 +30,10 @@ def stored(a, dt):
 
 def ids(a, it):
     return torch.from_numpy(np.ascontiguousarray(a)).to(IT[it]).to(DEV)
+
+
+def up(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
 
 
 CHOICES = [
@@ -148,49 +152,36 @@ def test_typed_selector_never_runs_segment_parallel():
     compare(got, ref, "mean", terms, "typed mean, fp32 shape")
 
 
-def _sample_segments(lengths, k, seed):
-    rng = np.random.default_rng(seed)
-    S = lengths.size
-    picks = {0, S - 1, int(np.argmax(lengths)), int(np.argmin(lengths))}
-    picks.update(int(x) for x in np.argsort(lengths)[-8:])
-    picks.update(int(x) for x in rng.choice(S, size=k, replace=False))
-    return np.array(sorted(picks), dtype=np.int64)
-
-
-def test_c3_powerlaw_graph_bf16_i32_sampled():
-    """The power-law workload (114,615,892 x 32) stored as bf16 with int32 ids."""
+def test_c3_powerlaw_graph_bf16_i32_full():
+    """The power-law workload (114,615,892 x 32) stored as bf16 with int32 ids: every output
+    element against the (multi-threaded) oracle run on the stored rows widened to fp32."""
     c = make_config("c3_powerlaw_graph")
-    src, idx, S, L = c["src"], c["index"], c["num_segments"], c["lengths"]
+    src, idx, S = c["src"], c["index"], c["num_segments"]
     s = torch.from_numpy(src).to(DEV).to(torch.bfloat16)
     say("c3 bf16 uploaded")
     got = geot.segment_reduce(s, ids(idx, "i32"), S, "sum").cpu().numpy()
     # the fp32 leaf for this shape, loaded 8 wide: half the lanes, twice the rows
     fp, lc = geot.select(idx.size, S, 32, "sum"), geot.last_choice()
     assert (lc["vec"], lc["lanes"], lc["rows"]) == (8, fp["lanes"] // 2, 2 * fp["rows"]), (lc, fp)
-    starts = np.concatenate([[0], np.cumsum(L)])
-    for seg in _sample_segments(L, 200, 4):
-        a, b = starts[seg], starts[seg + 1]
-        sub = s[a:b].cpu().float().numpy()   # the stored rows, widened on the host
-        z = np.zeros(b - a, dtype=np.int64)
-        ref = oracle.segment_reduce(sub, z, 1, "sum")
-        compare(got[seg:seg + 1], ref, "sum", oracle.abs_term_sum(sub, z, 1, "sum"),
-                f"c3 bf16 segment {seg} (len {b - a})")
+    wide = s.float().cpu().numpy()   # the stored rows, widened exactly
+    del s
+    torch.cuda.empty_cache()
+    m = oracle.mt()
+    compare(got, m.segment_reduce(wide, idx, S, "sum"), "sum", m.abs_term_sum(wide, idx, S, "sum"),
+            "c3 bf16 (every element)")
 
 
-def test_c4_spmm_bf16_i32_sampled():
-    """The SpMM workload with X stored as bf16 and int32 col / row."""
+def test_c4_spmm_bf16_i32_full():
+    """The SpMM workload with X stored as bf16 and int32 col / row: every output element."""
     c = make_config("c4_spmm")
-    X, col, w, row, R, L = c["X"], c["col"], c["weight"], c["index"], c["num_segments"], c["lengths"]
+    X, col, w, row, R = c["X"], c["col"], c["weight"], c["index"], c["num_segments"]
     t, wide = stored(X, "bf16")
     say("c4 bf16 uploaded")
     got = geot.gather_scatter(t.to(DEV), ids(col, "i32"), torch.from_numpy(w).to(DEV), ids(row, "i32"),
                               R, "sum").cpu().numpy()
-    starts = np.concatenate([[0], np.cumsum(L)])
-    for r in _sample_segments(L, 200, 5):
-        a, b = starts[r], starts[r + 1]
-        z = np.zeros(b - a, dtype=np.int64)
-        ref, terms = oracle_gather(wide, col[a:b], w[a:b], z, 1, "sum")
-        compare(got[r:r + 1], ref, "sum", terms, f"c4 bf16 row {r} (len {b - a})")
+    m = oracle.mt()
+    compare(got, m.gather_scatter(wide, col, w, row, R, "sum"), "sum", m.abs_term_sum(wide, row, R, "sum", col, w),
+            "c4 bf16 (every element)")
 
 
 BWD_CASES = [
@@ -223,11 +214,14 @@ def test_segment_backward_typed(dt, it, case):
     gd = torch.from_numpy(g).to(DEV)
     for op in OPS:
         say(f"typed segment backward {dt}/{it} seed={seed} F={F} {op}")
-        out = geot.segment_reduce(s, i, S, op)
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.segment_reduce(wide, p["index"], S, op),
+                                       geot.segment_reduce(s, i, S, op), f"{dt}/{it} seed={seed}")
         got = geot.segment_reduce_backward(gd, i, op, s if op == "max" else None,
-                                           out if op == "max" else None, dtype=DT[dt])
+                                           up(out), dtype=DT[dt])
         assert got.dtype == DT[dt] and got.shape == (nnz, F)
-        ref = oracle.segment_reduce_backward(g, p["index"], op, wide, out.cpu().numpy())
+        ref = oracle.segment_reduce_backward(g, p["index"], op, wide, out)
         if op in ("sum", "max"):
             assert torch.equal(got.cpu(), torch.from_numpy(np.ascontiguousarray(ref)).to(DT[dt])), \
                 f"{dt}/{it} seed={seed} {op}"
@@ -279,11 +273,14 @@ def test_gather_backward_typed(dt, it, case):
     g = np.random.default_rng(seed).standard_normal((R, F)).astype(np.float32)
     for op in OPS:
         say(f"typed gather backward {dt}/{it} seed={seed} F={F} {op}")
-        out = geot.gather_scatter(X, col, w, row, R, op)
-        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, out)
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.gather_scatter(wide, q["col"], q["weight"], q["index"], R, op),
+                                       geot.gather_scatter(X, col, w, row, R, op), f"{dt}/{it} seed={seed}")
+        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, up(out))
         assert gx.dtype == torch.float32
-        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy())
-        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy(),
+        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out)
+        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out,
                                                 absolute=True)
         for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
             if got is None:
@@ -334,10 +331,13 @@ def test_typed_backward_misaligned_and_empty():
     g = np.random.default_rng(59).standard_normal((600, 16)).astype(np.float32)
     for op in OPS:
         say(f"misaligned bf16 gather backward {op}")
-        out = geot.gather_scatter(X, col, w, row, 600, op)
-        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, out)
-        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy())
-        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out.cpu().numpy(),
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.gather_scatter(wide, q["col"], q["weight"], q["index"], 600, op),
+                                       geot.gather_scatter(X, col, w, row, 600, op), "misaligned bf16")
+        gx, gw = geot.gather_scatter_backward(X, col, w, row, torch.from_numpy(g).to(DEV), op, up(out))
+        rx, rw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out)
+        ax, aw = oracle.gather_scatter_backward(wide, q["col"], q["weight"], q["index"], g, op, out,
                                                 absolute=True)
         for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
             err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
@@ -349,9 +349,10 @@ def test_typed_backward_misaligned_and_empty():
     src.copy_(ts.to(DEV))
     i32 = ids(p["index"], "i32")
     gs = np.random.default_rng(61).standard_normal((400, 16)).astype(np.float32)
-    out = geot.segment_reduce(src, i32, 400, "max")
-    got = geot.segment_reduce_backward(torch.from_numpy(gs).to(DEV), i32, "max", src, out)
-    ref = oracle.segment_reduce_backward(gs, p["index"], "max", sw, out.cpu().numpy())
+    out = forward_for_gradient(oracle.segment_reduce(sw, p["index"], 400, "max"),
+                               geot.segment_reduce(src, i32, 400, "max"), "misaligned bf16 segment")
+    got = geot.segment_reduce_backward(torch.from_numpy(gs).to(DEV), i32, "max", src, up(out))
+    ref = oracle.segment_reduce_backward(gs, p["index"], "max", sw, out)
     assert torch.equal(got.cpu(), torch.from_numpy(ref).to(torch.bfloat16)), "misaligned bf16 segment max"
     # no edges: grad_X is zero, grad_w empty; no rows: grad_src empty
     e32 = torch.empty(0, dtype=torch.int32, device=DEV)
