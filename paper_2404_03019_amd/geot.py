@@ -115,10 +115,10 @@ def _choice(choice) -> KernelChoice | None:
 
 
 def _dev(t: torch.Tensor, name: str, dtype, ndim):
+    """Type, rank and layout of one tensor argument (its device is checked by _on_gpu, after
+    the shapes, so that every size mismatch is reported before anything else)."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch tensor")
-    if t.device.type != "cuda":
-        raise ValueError(f"{name} must be on the GPU")
     if t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
         raise TypeError(f"{name} must be {dtype}")
     if t.dim() != ndim:
@@ -126,6 +126,25 @@ def _dev(t: torch.Tensor, name: str, dtype, ndim):
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
+
+
+def _shape(t: torch.Tensor | None, name: str, shape: tuple):
+    if t is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _on_gpu(**tensors):
+    """Every given tensor is on the same GPU (the library reads them through raw pointers)."""
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.device.type != "cuda":
+            raise ValueError(f"{name} must be on the GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, the other arguments on {dev}")
 
 
 def _stream(device) -> int:
@@ -167,15 +186,13 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
     _dev(index, "index", tuple(INDEX_TYPES), 1)
     if index.numel() != src.shape[0]:
         raise ValueError("index must have one entry per row of src")
-    if index.device != src.device:
-        raise ValueError("src and index must be on the same device")
     S, F = int(num_segments), src.shape[1]
+    if out is not None:
+        _dev(out, "out", torch.float32, 2)
+        _shape(out, "out", (S, F))
+    _on_gpu(src=src, index=index, out=out)
     if out is None:
         out = torch.empty((S, F), dtype=torch.float32, device=src.device)
-    else:
-        _dev(out, "out", torch.float32, 2)
-        if tuple(out.shape) != (S, F):
-            raise ValueError("out must be [num_segments, F]")
     c = _choice(choice)
     cp = ctypes.byref(c) if c is not None else None
     with _OnDevice(src.device):
@@ -207,12 +224,12 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
     if col.numel() != row.numel():
         raise ValueError("col and row must have one entry per edge")
     R, F = int(num_rows), x.shape[1]
+    if out is not None:
+        _dev(out, "out", torch.float32, 2)
+        _shape(out, "out", (R, F))
+    _on_gpu(x=x, col=col, weight=weight, row=row, out=out)
     if out is None:
         out = torch.empty((R, F), dtype=torch.float32, device=x.device)
-    else:
-        _dev(out, "out", torch.float32, 2)
-        if tuple(out.shape) != (R, F):
-            raise ValueError("out must be [num_rows, F]")
     c = _choice(choice)
     wp = weight.data_ptr() if weight is not None else None
     cp = ctypes.byref(c) if c is not None else None
@@ -243,15 +260,23 @@ def segment_reduce_backward(grad_out: torch.Tensor, index: torch.Tensor, reduce:
     typ = grad_src.dtype if grad_src is not None else (src.dtype if src is not None else (dtype or torch.float32))
     if typ not in DTYPES:
         raise TypeError(f"the gradient's type must be one of {tuple(DTYPES)}")
+    if reduce not in OPS:
+        raise ValueError(f"unknown reduce {reduce!r}")
     if reduce == "max":
         if src is None or out is None:
             raise ValueError("max needs src and out")
         _dev(src, "src", typ, 2)
         _dev(out, "out", torch.float32, 2)
+        _shape(src, "src", (index.numel(), F))
+        _shape(out, "out", (S, F))
+    else:   # read for max only
+        src = out = None
+    if grad_src is not None:
+        _dev(grad_src, "grad_src", typ, 2)
+        _shape(grad_src, "grad_src", (index.numel(), F))
+    _on_gpu(grad_out=grad_out, index=index, src=src, out=out, grad_src=grad_src)
     if grad_src is None:
         grad_src = torch.empty((index.numel(), F), dtype=typ, device=grad_out.device)
-    else:
-        _dev(grad_src, "grad_src", typ, 2)
     with _OnDevice(grad_out.device):
         st = lib().geot_segment_reduce_backward_typed(
             grad_out.data_ptr(), index.data_ptr(), INDEX_TYPES[index.dtype], index.numel(), S, F, OPS[reduce],
@@ -273,13 +298,25 @@ def gather_scatter_backward(x: torch.Tensor, col: torch.Tensor, weight: torch.Te
     _dev(col, "col", tuple(INDEX_TYPES), 1)
     _dev(row, "row", (col.dtype,), 1)
     _dev(grad_out, "grad_out", torch.float32, 2)
+    if reduce not in OPS:
+        raise ValueError(f"unknown reduce {reduce!r}")
+    R, F = grad_out.shape
+    n = row.numel()
+    if col.numel() != n:
+        raise ValueError("col and row must have one entry per edge")
+    if x.shape[1] != F:
+        raise ValueError(f"x has {x.shape[1]} columns, grad_out {F}")
     if weight is not None:
         _dev(weight, "weight", torch.float32, 1)
+        _shape(weight, "weight", (n,))
     if reduce == "max":
         if out is None:
             raise ValueError("max needs out")
         _dev(out, "out", torch.float32, 2)
-    R, F = grad_out.shape
+        _shape(out, "out", (R, F))
+    else:   # read for max only
+        out = None
+    _on_gpu(x=x, col=col, weight=weight, row=row, grad_out=grad_out, out=out)
     gx = torch.empty(x.shape, dtype=torch.float32, device=x.device) if need_x else None
     gw = torch.empty_like(weight) if (need_weight and weight is not None) else None
     with _OnDevice(x.device):
@@ -307,6 +344,7 @@ def transpose_edges(col: torch.Tensor, weight: torch.Tensor | None, row: torch.T
             raise ValueError("weight must have one entry per edge")
     if col.numel() != row.numel():
         raise ValueError("col and row must have one entry per edge")
+    _on_gpu(col=col, weight=weight, row=row)
     n = row.numel()
     sc = torch.empty(n, dtype=torch.int64, device=row.device)
     rt = torch.empty(n, dtype=torch.int64, device=row.device)
@@ -323,6 +361,7 @@ def transpose_edges(col: torch.Tensor, weight: torch.Tensor | None, row: torch.T
 def index_stats(index: torch.Tensor, num_segments: int) -> dict:
     """Segment-length statistics of a sorted index (geot_index_stats; synchronizes)."""
     _dev(index, "index", torch.int64, 1)
+    _on_gpu(index=index)
     o = IndexStats()
     with _OnDevice(index.device):
         st = lib().geot_index_stats(index.data_ptr(), index.numel(), int(num_segments),
@@ -339,6 +378,7 @@ def check_index(index: torch.Tensor, num_segments: int, col: torch.Tensor | None
     if col is not None:
         _dev(col, "col", torch.int64, 1)
         cp = col.data_ptr()
+    _on_gpu(index=index, col=col)
     with _OnDevice(index.device):
         return int(lib().geot_check_index(index.data_ptr(), index.numel(), int(num_segments), cp,
                                           int(num_x_rows), _stream(index.device)))
