@@ -17,7 +17,8 @@ kernel of the call that takes longest), timed per launch with HIP events on
 the stream it runs on; ``traffic`` comes from committed rocprofv3 counter
 readings (profiles/traffic.json) and is null when the kernel source changed
 since. ``cpu_baseline`` times the CPU oracle on a bounded sample of the same
-inputs on the host (one thread).
+inputs on the host (one thread), and the multi-threaded oracle over both whole
+workloads on the host's cores, with the core count and CPU model.
 """
 from __future__ import annotations
 
@@ -104,6 +105,16 @@ def cpu_baseline(c3, c4, target_s: float):
     probe = run(0.01)
     frac = min(1.0, 0.01 * target_s / max(probe["t3"] + probe["t4"], 1e-3))
     r = run(frac) if frac > 0.01 else probe
+    # the same definitions with the output segments split across host threads
+    # (oracle/geot_oracle_mt.c, bit-identical results), over both whole workloads
+    m = oracle.mt()
+    t0 = time.perf_counter()
+    m.segment_reduce(c3["src"], c3["index"], c3["num_segments"], "sum")
+    t1 = time.perf_counter()
+    m.gather_scatter(c4["X"], c4["col"], c4["weight"], c4["index"], c4["num_segments"], "sum")
+    t2 = time.perf_counter()
+    b_all = seg_bytes(c3["index"].size, c3["num_segments"], 32) + \
+        gather_bytes(c4["index"].size, c4["num_segments"], 128)
     return {
         "value": round(r["bytes"] / (r["t3"] + r["t4"]) / 1e9, 3),
         "unit": "GB/s",
@@ -113,7 +124,28 @@ def cpu_baseline(c3, c4, target_s: float):
                    f"{r['t3']:.1f} s) + first {r['s4']} of 2,449,029 rows of the SpMM workload "
                    f"({r['n4']} edges, {r['t4']:.1f} s); serial C oracle on one host thread; "
                    f"same algorithmic-byte formulas as the GPU value"),
+        "all_cores": {
+            "value": round(b_all / (t2 - t0) / 1e9, 3),
+            "unit": "GB/s",
+            "cores": m.threads,
+            "sample": (f"both whole workloads ({t1 - t0:.1f} s + {t2 - t1:.1f} s): the oracle's definitions "
+                       f"with output segments split across {m.threads} POSIX threads"),
+        },
+        "nproc": os.cpu_count(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": cpu_model(),
     }
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def copy_probe(n: int):

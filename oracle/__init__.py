@@ -8,8 +8,14 @@ from .oracle import (  # noqa: F401
     SOURCE,
     OracleError,
     OracleLib,
+    OracleMT,
+    MT_SOURCE,
     build,
+    build_mt,
+    build_all,
     default,
+    mt,
+    host_threads,
     lib_path,
     check_index,
     segment_reduce,

@@ -25,8 +25,21 @@ class OracleError(RuntimeError):
         self.code = code
 
 
+MT_SOURCE = os.path.join(_HERE, "geot_oracle_mt.c")
+_MT_LIB = os.path.join(_HERE, "liboracle_mt.so")
+
+
 def lib_path() -> str:
     return _LIB
+
+
+def host_threads() -> int:
+    """Threads for the multi-threaded oracle: OMP_NUM_THREADS when set (the host share the
+    machine gives this process), else the CPUs this process may run on."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return min(int(env), 256)
+    return max(1, min(len(os.sched_getaffinity(0)), 256))
 
 
 def build(src: str = SOURCE, out: str = _LIB) -> str:
@@ -35,6 +48,19 @@ def build(src: str = SOURCE, out: str = _LIB) -> str:
            "-o", out, src, "-lm"]
     subprocess.run(cmd, check=True)
     return out
+
+
+def build_mt(src: str = MT_SOURCE, out: str = _MT_LIB) -> str:
+    """Compile the multi-threaded oracle (same flags, POSIX threads)."""
+    cmd = ["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-std=c11", "-pthread", "-shared", "-fPIC",
+           "-o", out, src, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def build_all() -> None:
+    build()
+    build_mt()
 
 
 def _ptr(a):
@@ -170,7 +196,70 @@ class OracleLib:
                     num_empty=ne.value, sum_len_sq=sq.value)
 
 
+class OracleMT:
+    """The multi-threaded oracle (geot_oracle_mt.c): the serial oracle's forward
+    definitions with the output segments split across threads; bit-identical results."""
+
+    def __init__(self, path: str, threads: int | None = None):
+        lib = ctypes.CDLL(path)
+        i64, p, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        lib.oracle_mt_segment_reduce.argtypes = [p, p, i64, i64, i64, ci, p, ci]
+        lib.oracle_mt_gather_scatter.argtypes = [p, i64, p, p, p, i64, i64, i64, ci, p, ci]
+        lib.oracle_mt_abs_term_sum.argtypes = [p, i64, p, p, p, i64, i64, i64, ci, p, ci]
+        for name in ("oracle_mt_segment_reduce", "oracle_mt_gather_scatter", "oracle_mt_abs_term_sum"):
+            getattr(lib, name).restype = ctypes.c_int
+        self._lib = lib
+        self.path = path
+        self.threads = int(threads) if threads else host_threads()
+
+    def segment_reduce(self, src, index, num_segments: int, op: str = "sum") -> np.ndarray:
+        src = _f32(src)
+        if src.ndim == 1:
+            src = src.reshape(-1, 1)
+        index = _i64(index)
+        if src.shape[0] != index.size:
+            raise ValueError("src rows must equal index length")
+        out = np.empty((int(num_segments), src.shape[1]), dtype=np.float32)
+        _check(self._lib.oracle_mt_segment_reduce(_ptr(src), _ptr(index), index.size, int(num_segments),
+                                                  src.shape[1], OPS[op], _ptr(out), self.threads))
+        return out
+
+    def gather_scatter(self, X, col, weight, row, num_rows: int, op: str = "sum") -> np.ndarray:
+        X, col, row = _f32(X), _i64(col), _i64(row)
+        w = None if weight is None else _f32(weight)
+        if col.size != row.size or (w is not None and w.size != row.size):
+            raise ValueError("col, weight and row must have one entry per edge")
+        out = np.empty((int(num_rows), X.shape[1]), dtype=np.float32)
+        _check(self._lib.oracle_mt_gather_scatter(_ptr(X), X.shape[0], _ptr(col), _ptr(w), _ptr(row), row.size,
+                                                  int(num_rows), X.shape[1], OPS[op], _ptr(out), self.threads))
+        return out
+
+    def abs_term_sum(self, rows, index, num_segments: int, op: str = "sum", col=None, weight=None) -> np.ndarray:
+        rows = _f32(rows)
+        if rows.ndim == 1:
+            rows = rows.reshape(-1, 1)
+        index = _i64(index)
+        c = None if col is None else _i64(col)
+        w = None if weight is None else _f32(weight)
+        out = np.empty((int(num_segments), rows.shape[1]), dtype=np.float64)
+        _check(self._lib.oracle_mt_abs_term_sum(_ptr(rows), rows.shape[0], _ptr(c), _ptr(w), _ptr(index),
+                                                index.size, int(num_segments), rows.shape[1], OPS[op], _ptr(out),
+                                                self.threads))
+        return out
+
+
 _default = None
+_default_mt = None
+
+
+def mt() -> OracleMT:
+    """The multi-threaded oracle built in this directory (built with gcc on first use)."""
+    global _default_mt
+    if _default_mt is None:
+        if not os.path.exists(_MT_LIB):
+            build_mt()
+        _default_mt = OracleMT(_MT_LIB)
+    return _default_mt
 
 
 def default() -> OracleLib:

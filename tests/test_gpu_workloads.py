@@ -1,10 +1,12 @@
 """GPU parity on the named workloads at their full sizes, with the selector's default
 kernel choice (the launch configuration the bench times).
 
-Small workloads are compared element by element with the oracle; the two
-large power-law workloads are compared on sampled output rows (the longest
-segment always included), with the oracle run on exactly the rows those
-segments reduce, plus per-feature conservation of the total over all rows.
+Every output element of every workload is compared with the oracle. The two large
+power-law workloads use the multi-threaded oracle (the serial oracle's definitions
+with segments split across host threads, pinned to it bit for bit by
+``test_oracle_mt.py``), and on a sample of rows (the longest segments always
+included) the serial oracle is run too and must agree with it bit for bit; the
+power-law graph is also checked for per-feature conservation over all rows.
 """
 import numpy as np
 import pytest
@@ -78,10 +80,20 @@ def _sample_segments(lengths, k, seed):
     return np.array(sorted(picks), dtype=np.int64)
 
 
-def test_c3_powerlaw_graph_sampled():
+def serial_agrees(ref_mt, rows_of, lengths, seed, what):
+    """The serial oracle on sampled output rows equals the multi-threaded oracle's rows."""
+    starts = np.concatenate([[0], np.cumsum(lengths)])
+    for s in _sample_segments(lengths, 24, seed):
+        a, b = int(starts[s]), int(starts[s + 1])
+        one = rows_of(a, b)
+        assert np.array_equal(one.view(np.uint32), ref_mt[s:s + 1].view(np.uint32)), f"{what}: row {s}"
+
+
+def test_c3_powerlaw_graph_full():
+    """All 232,965 x 32 outputs of the power-law graph reduction (114,615,892 rows)."""
     c = make_config("c3_powerlaw_graph")
     src, idx, S, L = c["src"], c["index"], c["num_segments"], c["lengths"]
-    say("c3 uploaded")
+    say("c3 generated")
     s = up(src)
     got = geot.segment_reduce(s, up(idx), S, "sum")
     # per-feature conservation over all 114,615,892 rows (fp64 totals)
@@ -90,23 +102,26 @@ def test_c3_powerlaw_graph_sampled():
     abs_in = s.abs().sum(dim=0, dtype=torch.float64).cpu().numpy()
     assert np.all(np.abs(tot_in - tot_out) <= 1e-5 * abs_in + 1e-6 * S), "c3 conservation"
     got = got.cpu().numpy()
-    starts = np.concatenate([[0], np.cumsum(L)])
-    for seg in _sample_segments(L, 300, 2):
-        a, b = starts[seg], starts[seg + 1]
-        sub = src[a:b]
-        ref = oracle.segment_reduce(sub, np.zeros(b - a, dtype=np.int64), 1, "sum")
-        terms = oracle.abs_term_sum(sub, np.zeros(b - a, dtype=np.int64), 1, "sum")
-        compare(got[seg:seg + 1], ref, "sum", terms, f"c3 segment {seg} (len {b - a})")
+    del s
+    torch.cuda.empty_cache()
+    say("c3 oracle")
+    m = oracle.mt()
+    ref = m.segment_reduce(src, idx, S, "sum")
+    compare(got, ref, "sum", m.abs_term_sum(src, idx, S, "sum"), "c3 sum (every element)")
+    z = lambda a, b: np.zeros(b - a, dtype=np.int64)
+    serial_agrees(ref, lambda a, b: oracle.segment_reduce(src[a:b], z(a, b), 1, "sum"), L, 2, "c3")
 
 
-def test_c4_spmm_sampled():
+def test_c4_spmm_full():
+    """All 2,449,029 x 128 outputs of the SpMM workload (61,859,140 weighted edges)."""
     c = make_config("c4_spmm")
     X, col, w, row, R, L = c["X"], c["col"], c["weight"], c["index"], c["num_segments"], c["lengths"]
-    say("c4 uploaded")
+    say("c4 generated")
     got = geot.gather_scatter(up(X), up(col), up(w), up(row), R, "sum").cpu().numpy()
-    starts = np.concatenate([[0], np.cumsum(L)])
-    for r in _sample_segments(L, 300, 3):
-        a, b = starts[r], starts[r + 1]
-        z = np.zeros(b - a, dtype=np.int64)
-        ref, terms = oracle_gather(X, col[a:b], w[a:b], z, 1, "sum")
-        compare(got[r:r + 1], ref, "sum", terms, f"c4 row {r} (len {b - a})")
+    torch.cuda.empty_cache()
+    say("c4 oracle")
+    m = oracle.mt()
+    ref = m.gather_scatter(X, col, w, row, R, "sum")
+    compare(got, ref, "sum", m.abs_term_sum(X, row, R, "sum", col, w), "c4 sum (every element)")
+    z = lambda a, b: np.zeros(b - a, dtype=np.int64)
+    serial_agrees(ref, lambda a, b: oracle.gather_scatter(X, col[a:b], w[a:b], z(a, b), 1, "sum"), L, 3, "c4")
