@@ -32,13 +32,18 @@
  *    geot_release_scratch). Any thread may call the library, but calls that
  *    share one stream must be issued one after the other: two host threads
  *    enqueuing on the same stream at once would interleave their kernels
- *    over that stream's buffer. Different streams are independent.
+ *    over that stream's buffer. Different streams are independent. The *_ws
+ *    forms take this memory from the caller instead and allocate nothing.
  *  - The reduction calls (forward) can be captured in a HIP graph and replayed:
  *    they keep no per-call host state and issue no memset. Make one call of the
  *    same shapes on the capture stream first, so the stream's buffer exists
- *    before the capture. The gradient calls and geot_transpose_edges take
- *    their temporaries from the pool on every call (stream-ordered
- *    allocations); their capture is not covered by the tests.
+ *    before the capture; a captured call that would need a larger buffer
+ *    returns GEOT_ERROR_INVALID_VALUE instead of allocating. A buffer that a
+ *    graph captured is never freed when a later call outgrows it (it is kept
+ *    for the graph until geot_release_scratch, which invalidates such graphs).
+ *    The gradient calls and geot_transpose_edges take their temporaries from
+ *    the pool on every call (stream-ordered allocations, recorded as graph
+ *    allocations under capture).
  *  - Preconditions: the index is non-decreasing and 0 <= index < num_segments;
  *    for the gather form 0 <= col < num_x_rows. They are not checked by the
  *    reduction calls (geot_check_index checks them). Violations give
@@ -181,6 +186,43 @@ geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const
                                        const float *weight, const int64_t *sorted_row, int64_t nnz,
                                        int64_t num_rows, int64_t F, geot_op_t op, float *out,
                                        void *stream, const geot_kernel_choice_t *choice);
+
+/* geot_segment_reduce and geot_gather_scatter with the temporary memory given by the
+ * caller (Section II-B and Section IV define the operations; this form changes only who
+ * owns the memory), for callers that manage device memory themselves:
+ *   workspace        device memory of at least the bytes that the matching
+ *                    *_workspace_size query returns for the same sizes, op and
+ *                    choice; 256-byte aligned; must not overlap any argument.
+ *                    NULL is allowed with workspace_bytes == 0 (enough for the
+ *                    calls that need none: nnz, num_segments or F zero).
+ *   workspace_bytes  its size; a call that needs more returns
+ *                    GEOT_ERROR_INVALID_VALUE before any device work
+ *   choice           NULL for the selector's choice, else forced (as *_with)
+ * The call allocates nothing and keeps nothing between calls: it clears the
+ * workspace's first 256 bytes (the counters of its list of empty-segment runs)
+ * with a kernel on `stream`, then uses the workspace for the partial results of
+ * segments that cross block boundaries. Calls that run at the same time must not
+ * share a workspace; calls in order on one stream may. Capturable in a HIP graph
+ * (no allocation, no memset).
+ * *_workspace_size writes the bytes needed by a call of these sizes for any
+ * alignment of its arrays (the pointers decide the vector width, which decides the
+ * number of partials); 0 when the call needs no temporary memory. Pure host
+ * functions. Same argument checks as the calls, without the pointers.        */
+geot_status_t geot_segment_reduce_workspace_size(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
+                                                 const geot_kernel_choice_t *choice, size_t *bytes);
+geot_status_t geot_segment_reduce_ws(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                     int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                     void *workspace, size_t workspace_bytes, void *stream,
+                                     const geot_kernel_choice_t *choice);
+/* weighted: nonzero when the call passes edge weights (the selector's trees differ). */
+geot_status_t geot_gather_scatter_workspace_size(int64_t nnz, int64_t num_rows, int64_t F, geot_op_t op,
+                                                 int32_t weighted, const geot_kernel_choice_t *choice,
+                                                 size_t *bytes);
+geot_status_t geot_gather_scatter_ws(const float *X, int64_t num_x_rows, const int64_t *col,
+                                     const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                     int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                     void *workspace, size_t workspace_bytes, void *stream,
+                                     const geot_kernel_choice_t *choice);
 
 /* Storage types of the reduced data, and index types. Not in the paper: a
  * 16-bit storage type halves the bytes of the stream that dominates every
@@ -368,8 +410,9 @@ geot_status_t geot_check_index(const int64_t *sorted_index, int64_t nnz, int64_t
  * in stream order and grown on demand (partials of block-crossing segments:
  * two rows of F floats per block, about 1.5 % of the input for F = 128; or
  * num_segments + 1 segment starts). This frees every such buffer after
- * synchronizing its stream; later calls allocate again. Call it before
- * destroying a stream the library was used on, or to return the memory. */
+ * synchronizing its stream, and the buffers that captured graphs held (those
+ * graphs must not be replayed afterwards); later calls allocate again. Call it
+ * before destroying a stream the library was used on, or to return the memory. */
 geot_status_t geot_release_scratch(void);
 
 /* The kernel choice the calling thread's last successful reduction used. */

@@ -14,6 +14,9 @@ from .geot import (  # noqa: F401
     lib,
     segment_reduce,
     gather_scatter,
+    workspace_size,
+    segment_reduce_ws,
+    gather_scatter_ws,
     segment_reduce_backward,
     gather_scatter_backward,
     index_stats,

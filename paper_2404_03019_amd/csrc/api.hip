@@ -114,10 +114,14 @@ struct StreamKey {
 struct StreamCtx {
     void *p = nullptr;
     size_t bytes = 0;
-    bool dirty = false;  // a launch failed after the gap list was handed out
+    bool dirty = false;     // a launch failed after the gap list was handed out
+    bool captured = false;  // a call on this buffer was captured into a graph, which keeps its address
 };
 std::mutex g_cache_mu;
 std::map<StreamKey, StreamCtx> g_cache;
+// Buffers replaced by a larger one after a graph captured them: a replay of that graph
+// still reads and writes them, so they are freed only by geot_release_scratch.
+std::vector<std::pair<int, void *>> g_retired;
 
 constexpr size_t kGapHeader = 256;
 constexpr size_t kGapArea = kGapHeader + (size_t)kGapCap * 3 * sizeof(int64_t);
@@ -130,16 +134,27 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
     *user = nullptr;
     int dev = 0;
     GEOT_HIP(hipGetDevice(&dev), "hipGetDevice");
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    GEOT_HIP(hipStreamIsCapturing(st, &cap), "hipStreamIsCapturing");
+    const bool capturing = cap != hipStreamCaptureStatusNone;
     std::lock_guard<std::mutex> lk(g_cache_mu);
     StreamCtx &e = g_cache[StreamKey{dev, st}];
     const size_t need = kGapArea + ((bytes + 255) & ~(size_t)255);
     bool fresh = false;
     if (e.bytes < need) {
+        // Growing inside a capture would record the free and the allocation into the graph.
+        if (capturing)
+            return fail(GEOT_ERROR_INVALID_VALUE,
+                        "stream capture: the stream's temporary buffer holds %zu bytes and this call needs %zu; "
+                        "make one call of these shapes on the stream before capturing",
+                        e.bytes, need);
         const size_t grown = std::max(need, e.bytes + e.bytes / 2);  // grow by half at least
         if (e.p) {
-            GEOT_HIP(hipFreeAsync(e.p, st), "hipFreeAsync");
+            if (e.captured) g_retired.emplace_back(dev, e.p);  // a captured graph still uses it
+            else GEOT_HIP(hipFreeAsync(e.p, st), "hipFreeAsync");
             e.p = nullptr;
             e.bytes = 0;
+            e.captured = false;
         }
         void *q = nullptr;
         geot_status_t s = scratch_alloc(&q, grown, st);
@@ -148,6 +163,7 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
         e.bytes = grown;
         fresh = true;
     }
+    if (capturing) e.captured = true;
     if (fresh || e.dirty) {
         GEOT_HIP(launch_zero_u64((unsigned long long *)e.p, kGapHeader / 8, st), "launch zero kernel");
         e.dirty = false;
@@ -160,6 +176,33 @@ geot_status_t stream_scratch(size_t bytes, hipStream_t st, void **user, GapList 
     }
     *user = bytes ? (char *)e.p + kGapArea : nullptr;
     *ctx_out = &e;
+    return GEOT_SUCCESS;
+}
+
+// Device memory of one reduction call given by the caller (the *_ws calls): its first
+// kGapArea bytes hold the gap list, zeroed by the call itself, then the partials.
+struct Workspace {
+    char *p;
+    size_t bytes;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The temporary memory of one call: `bytes` after the gap list, from the caller's workspace
+// when `ws` is given, else from the stream's cached buffer.
+geot_status_t call_scratch(size_t bytes, hipStream_t st, const Workspace *ws, void **user, GapList *g,
+                           StreamCtx **ctx_out) {
+    if (!ws) return stream_scratch(bytes, st, user, g, ctx_out);
+    *ctx_out = nullptr;
+    const size_t need = kGapArea + align256(bytes);
+    if (ws->bytes < need)
+        return fail(GEOT_ERROR_INVALID_VALUE, "workspace of %zu bytes, this call needs %zu", ws->bytes, need);
+    GEOT_HIP(launch_zero_u64((unsigned long long *)ws->p, kGapHeader / 8, st), "launch zero kernel");
+    unsigned *ctrl = (unsigned *)ws->p;
+    g->count = ctrl;
+    g->ticket = ctrl + 1;
+    g->rec = (int64_t *)(ws->p + kGapHeader);
+    *user = bytes ? ws->p + kGapArea : nullptr;
     return GEOT_SUCCESS;
 }
 
@@ -448,8 +491,6 @@ int64_t piece_rows_k(int64_t n, int64_t G) {
     return std::max<int64_t>(1, std::min<int64_t>(8, ceil_div(n, G)));
 }
 
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-
 // blocks that write the gap list, as a pass of their own or riding on the final partial level
 constexpr int kFoldedGapBlocks = 1024;
 // segment sum and max gradients from this many bytes of grad_src take the offsets pass first
@@ -468,13 +509,24 @@ void piece_shape(const Resolved &r, int *V, int *L) {
     *L = r.V == 8 ? 2 * r.L : r.L;
 }
 
-geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
+// The passes of an element-parallel call: level 0 over the input, then levels over the
+// partials of block-crossing segments until one block remains, and where each level's
+// partials live in the temporary memory.
+struct EpPlan {
+    std::vector<Level> lv;
+    std::vector<size_t> off_v, off_s, off_c;  // per level: values, segment ids, counts
+    size_t bytes = 0;
+    int64_t ld_p = 0;
+};
+
+geot_status_t plan_ep(const Problem &p, const Resolved &r, EpPlan *pl) {
     const int64_t G = kBlock / r.L;
     int Vp, Lp;
     piece_shape(r, &Vp, &Lp);
     const int64_t Gp = kBlock / Lp;
-    const int64_t ld_p = ceil_div(p.F, 4) * 4;
-    std::vector<Level> lv;
+    pl->ld_p = ceil_div(p.F, 4) * 4;
+    std::vector<Level> &lv = pl->lv;
+    lv.clear();
     lv.push_back({p.nnz, r.K, ceil_div(p.nnz, G * r.K)});
     while (lv.back().nchunks > 1) {
         const int64_t n = 2 * lv.back().nchunks;
@@ -482,24 +534,32 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st) {
         lv.push_back({n, K, ceil_div(n, Gp * K)});
         if (lv.size() > 64) return fail(GEOT_ERROR_HIP, "internal: level count");
     }
-    // partial buffers of levels 1..: values, segment ids, counts
-    std::vector<size_t> off_v(lv.size(), 0), off_s(lv.size(), 0), off_c(lv.size(), 0);
+    pl->off_v.assign(lv.size(), 0);
+    pl->off_s.assign(lv.size(), 0);
+    pl->off_c.assign(lv.size(), 0);
     size_t bytes = 0;
     for (size_t l = 1; l < lv.size(); ++l) {
-        off_v[l] = bytes;
-        bytes = align256(bytes + (size_t)lv[l].n * (size_t)ld_p * 4);
-        off_s[l] = bytes;
+        pl->off_v[l] = bytes;
+        bytes = align256(bytes + (size_t)lv[l].n * (size_t)pl->ld_p * 4);
+        pl->off_s[l] = bytes;
         bytes = align256(bytes + (size_t)lv[l].n * 8);
-        off_c[l] = bytes;
+        pl->off_c[l] = bytes;
         bytes = align256(bytes + (size_t)lv[l].n * 8);
     }
+    pl->bytes = bytes;
+    return GEOT_SUCCESS;
+}
+
+geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st, const Workspace *ws = nullptr) {
+    EpPlan pl;
+    geot_status_t s = plan_ep(p, r, &pl);
+    if (s != GEOT_SUCCESS) return s;
     void *scratch = nullptr;
     GapList gaps;
     StreamCtx *ctx = nullptr;
-    geot_status_t s = stream_scratch(bytes, st, &scratch, &gaps, &ctx);
+    s = call_scratch(pl.bytes, st, ws, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
-    s = poison(ctx, run_ep_levels(p, r, lv, (char *)scratch, off_v, off_s, off_c, ld_p, gaps, st));
-    return s;
+    return poison(ctx, run_ep_levels(p, r, pl.lv, (char *)scratch, pl.off_v, pl.off_s, pl.off_c, pl.ld_p, gaps, st));
 }
 
 geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
@@ -568,11 +628,11 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
 geot_status_t run_sp_kernels(const Problem &p, const Resolved &r, int64_t *off, GapList gaps,
                              hipStream_t st);
 
-geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st) {
+geot_status_t run_sp(const Problem &p, const Resolved &r, hipStream_t st, const Workspace *ws = nullptr) {
     void *scratch = nullptr;
     GapList gaps;
     StreamCtx *ctx = nullptr;
-    geot_status_t s = stream_scratch((size_t)(p.S + 1) * 8, st, &scratch, &gaps, &ctx);
+    geot_status_t s = call_scratch((size_t)(p.S + 1) * 8, st, ws, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
     return poison(ctx, run_sp_kernels(p, r, (int64_t *)scratch, gaps, st));
 }
@@ -607,7 +667,33 @@ geot_status_t run_sp_kernels(const Problem &p, const Resolved &r, int64_t *off, 
     return GEOT_SUCCESS;
 }
 
-geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_t *forced) {
+// The kernel choice of a call: the forced one, else the selector's for the problem.
+geot_kernel_choice_t choose(const Problem &p, const geot_kernel_choice_t *forced) {
+    if (forced) return *forced;
+    geot_kernel_choice_t c;
+    select_raw(p.nnz, p.S, p.F, p.op, p.gather ? (p.w ? 1 : 2) : 0, nullptr, &c);
+    if (p.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
+    // The leaves are fit on fp32 timings. A 16-bit X is half the bytes, and there the
+    // ids read once per tile cost more than the smaller slab saves (SpMM shape, bf16:
+    // 2.92 ms with two tiles in sequence, 2.83 ms without).
+    if (p.esize() == 2) untile(&c);
+    return c;
+}
+
+// Temporary bytes (gap list included) that a resolved call takes.
+geot_status_t scratch_need(const Problem &p, const Resolved &r, size_t *need) {
+    if (r.family == GEOT_FAMILY_SP) {
+        *need = kGapArea + align256((size_t)(p.S + 1) * 8);
+        return GEOT_SUCCESS;
+    }
+    EpPlan pl;
+    geot_status_t s = plan_ep(p, r, &pl);
+    if (s == GEOT_SUCCESS) *need = kGapArea + align256(pl.bytes);
+    return s;
+}
+
+geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_t *forced,
+                     const Workspace *ws = nullptr) {
     t_detail.clear();
     geot_status_t s = check_args(p);
     if (s != GEOT_SUCCESS) return s;
@@ -617,23 +703,52 @@ geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_
         t_last_choice = geot_kernel_choice_t{0, 0, 0, 0, 0, 0};
         return GEOT_SUCCESS;
     }
-    geot_kernel_choice_t c;
-    if (forced) {
-        c = *forced;
-    } else {
-        select_raw(p.nnz, p.S, p.F, p.op, p.gather ? (p.w ? 1 : 2) : 0, nullptr, &c);
-        if (p.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
-        // The leaves are fit on fp32 timings. A 16-bit X is half the bytes, and there the
-        // ids read once per tile cost more than the smaller slab saves (SpMM shape, bf16:
-        // 2.92 ms with two tiles in sequence, 2.83 ms without).
-        if (p.esize() == 2) untile(&c);
-    }
+    const geot_kernel_choice_t c = choose(p, forced);
     Resolved r;
     s = resolve(p, c, &r, forced == nullptr);
     if (s != GEOT_SUCCESS) return s;
-    s = r.family == GEOT_FAMILY_SP ? run_sp(p, r, st) : run_ep(p, r, st);
+    s = r.family == GEOT_FAMILY_SP ? run_sp(p, r, st, ws) : run_ep(p, r, st, ws);
     if (s == GEOT_SUCCESS) t_last_choice = to_choice(r);
     return s;
+}
+
+// Workspace a call of this shape needs, whatever the alignment of its arrays: the largest
+// need over the vector widths that F and the pointers may allow (the pointers decide the
+// width, and the width the partials' count).
+geot_status_t workspace_size(Problem p, const geot_kernel_choice_t *forced, size_t *bytes) {
+    t_detail.clear();
+    if (!bytes) return fail(GEOT_ERROR_INVALID_VALUE, "bytes is NULL");
+    *bytes = 0;
+    if (p.op != GEOT_OP_SUM && p.op != GEOT_OP_MEAN && p.op != GEOT_OP_MAX)
+        return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)p.op);
+    if (p.nnz < 0 || p.S < 0 || p.F < 0) return fail(GEOT_ERROR_INVALID_VALUE, "negative size");
+    if (p.S > (int64_t)INT32_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "num_segments must be < 2^31");
+    const int64_t kMax = (int64_t)1 << 62;
+    if (p.F > ((int64_t)1 << 31) || (p.F > 0 && (p.S > kMax / p.F || p.nnz > kMax / p.F)))
+        return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
+    if (p.nnz == 0 || p.S == 0 || p.F == 0) return GEOT_SUCCESS;  // no temporary memory
+    size_t most = 0;
+    for (uintptr_t align : {(uintptr_t)256, (uintptr_t)8, (uintptr_t)4}) {
+        p.src = (const void *)align;
+        p.out = (float *)align;
+        Resolved r;
+        geot_status_t s = resolve(p, choose(p, forced), &r, forced == nullptr);
+        if (s != GEOT_SUCCESS) return s;
+        size_t need = 0;
+        s = scratch_need(p, r, &need);
+        if (s != GEOT_SUCCESS) return s;
+        most = std::max(most, need);
+    }
+    *bytes = most;
+    return GEOT_SUCCESS;
+}
+
+// A caller's workspace: NULL only with 0 bytes (enough for calls that need none), else
+// 256-byte aligned (hipMalloc's alignment; the gap list's records are 8-byte words).
+geot_status_t check_workspace(const void *workspace, size_t bytes) {
+    if (!workspace && bytes > 0) return fail(GEOT_ERROR_INVALID_VALUE, "workspace is NULL with %zu bytes", bytes);
+    if (((uintptr_t)workspace & 255) != 0) return fail(GEOT_ERROR_INVALID_VALUE, "workspace must be 256-byte aligned");
+    return GEOT_SUCCESS;
 }
 
 }  // namespace
@@ -654,6 +769,59 @@ geot_status_t geot_segment_reduce(const float *src, const int64_t *sorted_index,
                                   int64_t num_segments, int64_t F, geot_op_t op, float *out,
                                   void *stream) {
     return geot_segment_reduce_with(src, sorted_index, nnz, num_segments, F, op, out, stream, nullptr);
+}
+
+geot_status_t geot_segment_reduce_workspace_size(int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op,
+                                                 const geot_kernel_choice_t *choice, size_t *bytes) {
+    Problem p{false, nullptr, 0, nullptr, nullptr, nullptr, nnz, num_segments, F, op, nullptr};
+    return workspace_size(p, choice, bytes);
+}
+
+geot_status_t geot_segment_reduce_ws(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                     int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                     void *workspace, size_t workspace_bytes, void *stream,
+                                     const geot_kernel_choice_t *choice) {
+    t_detail.clear();
+    geot_status_t s = check_workspace(workspace, workspace_bytes);
+    if (s != GEOT_SUCCESS) return s;
+    Problem p{false, src, 0, nullptr, nullptr, sorted_index, nnz, num_segments, F, op, out};
+    const size_t out_bytes = (size_t)std::max<int64_t>(num_segments, 0) * (size_t)std::max<int64_t>(F, 0) * 4;
+    if (overlaps(workspace, workspace_bytes, out, out_bytes) ||
+        overlaps(workspace, workspace_bytes, src, (size_t)std::max<int64_t>(nnz, 0) * (size_t)std::max<int64_t>(F, 0) * 4) ||
+        overlaps(workspace, workspace_bytes, sorted_index, (size_t)std::max<int64_t>(nnz, 0) * 8))
+        return fail(GEOT_ERROR_INVALID_VALUE, "workspace overlaps an argument");
+    Workspace ws{(char *)workspace, workspace_bytes};
+    return reduce(p, (hipStream_t)stream, choice, &ws);
+}
+
+geot_status_t geot_gather_scatter_workspace_size(int64_t nnz, int64_t num_rows, int64_t F, geot_op_t op,
+                                                 int32_t weighted, const geot_kernel_choice_t *choice,
+                                                 size_t *bytes) {
+    // only the presence of weights matters to the selector: any non-null stand-in
+    Problem p{true, nullptr, 1, nullptr, weighted ? (const float *)(uintptr_t)256 : nullptr, nullptr,
+              nnz, num_rows, F, op, nullptr};
+    return workspace_size(p, choice, bytes);
+}
+
+geot_status_t geot_gather_scatter_ws(const float *X, int64_t num_x_rows, const int64_t *col,
+                                     const float *weight, const int64_t *sorted_row, int64_t nnz,
+                                     int64_t num_rows, int64_t F, geot_op_t op, float *out,
+                                     void *workspace, size_t workspace_bytes, void *stream,
+                                     const geot_kernel_choice_t *choice) {
+    t_detail.clear();
+    geot_status_t s = check_workspace(workspace, workspace_bytes);
+    if (s != GEOT_SUCCESS) return s;
+    Problem p{true, X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, op, out};
+    const size_t n = (size_t)std::max<int64_t>(nnz, 0);
+    const size_t out_bytes = (size_t)std::max<int64_t>(num_rows, 0) * (size_t)std::max<int64_t>(F, 0) * 4;
+    if (overlaps(workspace, workspace_bytes, out, out_bytes) ||
+        overlaps(workspace, workspace_bytes, X,
+                 (size_t)std::max<int64_t>(num_x_rows, 0) * (size_t)std::max<int64_t>(F, 0) * 4) ||
+        overlaps(workspace, workspace_bytes, col, n * 8) || overlaps(workspace, workspace_bytes, sorted_row, n * 8) ||
+        overlaps(workspace, workspace_bytes, weight, weight ? n * 4 : 0))
+        return fail(GEOT_ERROR_INVALID_VALUE, "workspace overlaps an argument");
+    Workspace ws{(char *)workspace, workspace_bytes};
+    return reduce(p, (hipStream_t)stream, choice, &ws);
 }
 
 geot_status_t geot_gather_scatter_with(const float *X, int64_t num_x_rows, const int64_t *col,
@@ -1142,6 +1310,17 @@ geot_status_t geot_release_scratch(void) {
         if (e != hipSuccess && st == GEOT_SUCCESS) st = hip_fail(e, "release scratch");
     }
     g_cache.clear();
+    for (auto &r : g_retired) {  // buffers captured graphs held (the graphs are invalid from here on)
+        int cur = 0;
+        hipError_t e = hipGetDevice(&cur);
+        if (e == hipSuccess) e = hipSetDevice(r.first);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        if (e == hipSuccess) e = hipFreeAsync(r.second, nullptr);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+        (void)hipSetDevice(cur);
+        if (e != hipSuccess && st == GEOT_SUCCESS) st = hip_fail(e, "release retired scratch");
+    }
+    g_retired.clear();
     return st;
 }
 

@@ -77,6 +77,11 @@ def lib() -> ctypes.CDLL:
     L.geot_gather_scatter_backward_typed.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64, i64,
                                                      ctypes.c_int, p, p, p, p, p]
     L.geot_transpose_edges.argtypes = [p, i64, p, p, i64, i64, ctypes.c_int, p, p, p, p]
+    sz = ctypes.c_size_t
+    L.geot_segment_reduce_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, pc, ctypes.POINTER(sz)]
+    L.geot_gather_scatter_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, i32, pc, ctypes.POINTER(sz)]
+    L.geot_segment_reduce_ws.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, sz, p, pc]
+    L.geot_gather_scatter_ws.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, sz, p, pc]
     L.geot_last_choice.argtypes = [pc]
     L.geot_release_scratch.argtypes = []
     L.geot_profile_begin.argtypes = [i32]
@@ -89,7 +94,9 @@ def lib() -> ctypes.CDLL:
     for name in ("geot_segment_reduce", "geot_segment_reduce_with", "geot_gather_scatter",
                  "geot_gather_scatter_with", "geot_select", "geot_index_stats", "geot_check_index",
                  "geot_last_choice", "geot_profile_begin", "geot_profile_end", "geot_release_scratch",
-                 "geot_segment_reduce_backward", "geot_gather_scatter_backward"):
+                 "geot_segment_reduce_backward", "geot_gather_scatter_backward",
+                 "geot_segment_reduce_workspace_size", "geot_gather_scatter_workspace_size",
+                 "geot_segment_reduce_ws", "geot_gather_scatter_ws"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -242,6 +249,88 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
             st = lib().geot_gather_scatter_typed(x.data_ptr(), DTYPES[x.dtype], x.shape[0], col.data_ptr(),
                                                  wp, row.data_ptr(), INDEX_TYPES[col.dtype], row.numel(),
                                                  R, F, OPS[reduce], out.data_ptr(), _stream(x.device), cp)
+    _raise(st)
+    return out
+
+
+def workspace_size(nnz: int, num_segments: int, F: int, reduce: str = "sum", gather: bool = False,
+                   weighted: bool = True, choice=None) -> int:
+    """Bytes of caller workspace that segment_reduce_ws (gather_scatter_ws with `gather`) needs
+    for these sizes, whatever the alignment of the arrays (the *_workspace_size queries; host only)."""
+    c = _choice(choice)
+    cp = ctypes.byref(c) if c is not None else None
+    n = ctypes.c_size_t()
+    if gather:
+        st = lib().geot_gather_scatter_workspace_size(int(nnz), int(num_segments), int(F), OPS[reduce],
+                                                      1 if weighted else 0, cp, ctypes.byref(n))
+    else:
+        st = lib().geot_segment_reduce_workspace_size(int(nnz), int(num_segments), int(F), OPS[reduce], cp,
+                                                      ctypes.byref(n))
+    _raise(st)
+    return int(n.value)
+
+
+def _workspace(ws: torch.Tensor | None):
+    if ws is None:
+        return None, 0
+    if not isinstance(ws, torch.Tensor) or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor")
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def segment_reduce_ws(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str,
+                      workspace: torch.Tensor | None, out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+    """segment_reduce (fp32 src, int64 index) with its temporary memory in `workspace`
+    (geot_segment_reduce_ws): any contiguous device tensor of at least workspace_size(...) bytes."""
+    _dev(src, "src", torch.float32, 2)
+    _dev(index, "index", torch.int64, 1)
+    if index.numel() != src.shape[0]:
+        raise ValueError("index must have one entry per row of src")
+    S, F = int(num_segments), src.shape[1]
+    if out is not None:
+        _dev(out, "out", torch.float32, 2)
+        _shape(out, "out", (S, F))
+    _on_gpu(src=src, index=index, out=out, workspace=workspace)
+    if out is None:
+        out = torch.empty((S, F), dtype=torch.float32, device=src.device)
+    wp, wb = _workspace(workspace)
+    c = _choice(choice)
+    with _OnDevice(src.device):
+        st = lib().geot_segment_reduce_ws(src.data_ptr(), index.data_ptr(), index.numel(), S, F, OPS[reduce],
+                                          out.data_ptr(), wp, wb, _stream(src.device),
+                                          ctypes.byref(c) if c is not None else None)
+    _raise(st)
+    return out
+
+
+def gather_scatter_ws(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None, row: torch.Tensor,
+                      num_rows: int, reduce: str, workspace: torch.Tensor | None,
+                      out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+    """gather_scatter (fp32 x, int64 col / row) with its temporary memory in `workspace`
+    (geot_gather_scatter_ws)."""
+    _dev(x, "x", torch.float32, 2)
+    _dev(col, "col", torch.int64, 1)
+    _dev(row, "row", torch.int64, 1)
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+        if weight.numel() != row.numel():
+            raise ValueError("weight must have one entry per edge")
+    if col.numel() != row.numel():
+        raise ValueError("col and row must have one entry per edge")
+    R, F = int(num_rows), x.shape[1]
+    if out is not None:
+        _dev(out, "out", torch.float32, 2)
+        _shape(out, "out", (R, F))
+    _on_gpu(x=x, col=col, weight=weight, row=row, out=out, workspace=workspace)
+    if out is None:
+        out = torch.empty((R, F), dtype=torch.float32, device=x.device)
+    wp, wb = _workspace(workspace)
+    c = _choice(choice)
+    with _OnDevice(x.device):
+        st = lib().geot_gather_scatter_ws(x.data_ptr(), x.shape[0], col.data_ptr(),
+                                          weight.data_ptr() if weight is not None else None, row.data_ptr(),
+                                          row.numel(), R, F, OPS[reduce], out.data_ptr(), wp, wb,
+                                          _stream(x.device), ctypes.byref(c) if c is not None else None)
     _raise(st)
     return out
 

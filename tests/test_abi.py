@@ -197,3 +197,44 @@ def test_transpose_arguments_are_checked_on_the_host():
     assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 0, col + 8, b, c, None) == INVALID  # overlap
     assert L.geot_transpose_edges(col, 10, w, row, 100, 5, 0, a, a + 64, c, None) == INVALID  # outputs overlap
     assert L.geot_transpose_edges(None, 10, None, None, 0, 5, 0, None, None, None, None) == SUCCESS
+
+
+def test_workspace_size_query_on_the_host():
+    """The *_workspace_size queries are host functions: sizes, errors, and monotone in the
+    input (a larger input never needs less)."""
+    c1 = geot.workspace_size(65_536, 4096, 32)
+    assert c1 >= 1_500_000   # the empty-run list's counters and records, at least
+    assert geot.workspace_size(0, 4096, 32) == 0 and geot.workspace_size(10, 0, 32) == 0
+    assert geot.workspace_size(10, 4, 0) == 0
+    big = geot.workspace_size(114_615_892, 232_965, 32)
+    assert big > c1
+    assert geot.workspace_size(61_859_140, 2_449_029, 128, gather=True) > c1
+    assert geot.workspace_size(61_859_140, 2_449_029, 128, gather=True, weighted=False) > c1
+    # segment-parallel: the segment starts
+    sp = geot.workspace_size(10_000, 5_000, 8, choice=dict(family="sp"))
+    assert sp >= 5_001 * 8
+    for bad in ((-1, 4, 3), (10, -4, 3), (10, 4, -3), (10, 1 << 31, 3)):
+        with pytest.raises(geot.GeotError):
+            geot.workspace_size(*bad)
+    with pytest.raises(geot.GeotError):
+        geot.workspace_size(10, 4, 3, choice=dict(family="ep", lanes=3))
+    n = ctypes.c_size_t()
+    assert lib().geot_segment_reduce_workspace_size(10, 4, 3, 7, None, ctypes.byref(n)) == INVALID
+    assert lib().geot_segment_reduce_workspace_size(10, 4, 3, 0, None, None) == INVALID
+
+
+def test_workspace_calls_check_on_the_host():
+    """A workspace that is missing, misaligned, too small or overlapping an argument is
+    rejected before any device work."""
+    L = lib()
+    need = geot.workspace_size(1000, 10, 4)
+    src, idx, out, ws = FAKE, FAKE + (1 << 24), FAKE + (1 << 26), FAKE + (1 << 28)
+    call = lambda w, b: L.geot_segment_reduce_ws(src, idx, 1000, 10, 4, 0, out, w, b, None, None)
+    assert call(None, need) == INVALID and "NULL" in _detail()
+    assert call(ws + 64, need) == INVALID and "aligned" in _detail()
+    assert call(ws, 1 << 20) == INVALID and "needs" in _detail()   # below the empty-run list alone
+    assert call(out, need) == INVALID and "overlaps" in _detail()
+    assert L.geot_gather_scatter_ws(src, 100, idx, None, idx + 8192, 1000, 10, 4, 0, out, ws, 16, None,
+                                    None) == INVALID and "needs" in _detail()
+    # nothing to do: no workspace needed
+    assert L.geot_segment_reduce_ws(src, idx, 1000, 0, 4, 0, out, None, 0, None, None) == SUCCESS

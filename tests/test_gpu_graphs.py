@@ -199,3 +199,40 @@ def test_gather_backward_replays(op):
         for got, ref, terms, what in ((gx, rx, ax, "grad_X"), (gw, rw, aw, "grad_w")):
             err = np.abs(got.cpu().numpy().astype(np.float64) - ref)
             assert np.all(err <= 1e-5 * terms + 1e-6), f"replay {k} {op} {what}"
+
+
+def test_two_graphs_of_different_sizes_on_one_stream():
+    """A graph captured on a stream keeps the address of the stream's buffer. A later, larger
+    call on that stream grows the buffer: the captured one is kept (not freed), so the first
+    graph still replays correctly after a second, larger graph was captured on the same
+    stream. Both graphs replay alternately with new inputs."""
+    rng = np.random.default_rng(75)
+    st = torch.cuda.Stream()
+    cases = []
+    for n, S, F in ((4000, 150_000, 4), (600_000, 90_000, 32)):   # the second needs a larger buffer
+        src = torch.empty((n, F), device=DEV)
+        idx = torch.empty(n, dtype=torch.int64, device=DEV)
+        out = torch.empty((S, F), device=DEV)
+        idx.copy_(torch.from_numpy(np.sort(rng.integers(0, S, n)).astype(np.int64)))
+        src.copy_(torch.from_numpy(rng.standard_normal((n, F)).astype(np.float32)))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(st):   # the warm-up call sizes the stream's buffer
+            geot.segment_reduce(src, idx, S, "sum", out=out)
+        st.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=st):
+            geot.segment_reduce(src, idx, S, "sum", out=out)
+        cases.append((g, src, idx, out, n, S, F))
+    for k in range(2):
+        for g, src, idx, out, n, S, F in cases:
+            i = np.sort(rng.integers(0, S, n)).astype(np.int64)
+            v = rng.standard_normal((n, F)).astype(np.float32)
+            idx.copy_(torch.from_numpy(i))
+            src.copy_(torch.from_numpy(v))
+            out.fill_(5.0)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            say(f"two graphs: replay {k} of the n={n} graph")
+            ref, terms = oracle_segment(v, i, S, "sum")
+            compare(out.cpu().numpy(), ref, "sum", terms, f"graph n={n} replay {k}")
