@@ -224,6 +224,29 @@ geot_status_t geot_gather_scatter_ws(const float *X, int64_t num_x_rows, const i
                                      void *workspace, size_t workspace_bytes, void *stream,
                                      const geot_kernel_choice_t *choice);
 
+/* geot_segment_reduce for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation. The
+ * result is geot_segment_reduce's (the selector's choice, the same kernels). The
+ * temporary memory is one static device array per GPU of
+ * geot_noalloc_scratch_bytes() = 128 MiB, held from the library's load until
+ * the process ends; the call allocates nothing (no hipMalloc, no pool, no events).
+ *  - A call whose temporary memory would exceed the array returns
+ *    GEOT_ERROR_INVALID_VALUE before any device work. The need is that of
+ *    geot_segment_reduce_workspace_size for the actual pointers: about 1.5 MiB
+ *    plus two rows of F floats per block of rows (the 114,615,892 x 32 power-law
+ *    graph needs about 64 MiB with 16-byte aligned arrays).
+ *  - Every call on one GPU uses that GPU's single array, and the array keeps the
+ *    last call's contents: each call first clears what must start at zero (the
+ *    counters of its list of empty-segment runs) with a kernel on `stream`. Calls
+ *    that overlap in time on one GPU (other streams, other threads) race on the
+ *    array and give wrong results: issue them one after another on one stream,
+ *    or order the streams.
+ * Other checks, errors and semantics as geot_segment_reduce.                   */
+geot_status_t geot_segment_reduce_noalloc(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                          int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                          void *stream);
+size_t geot_noalloc_scratch_bytes(void);
+
 /* Storage types of the reduced data, and index types. Not in the paper: a
  * 16-bit storage type halves the bytes of the stream that dominates every
  * reduction, and int32 ids halve the index stream. */

@@ -17,6 +17,8 @@ from .geot import (  # noqa: F401
     workspace_size,
     segment_reduce_ws,
     gather_scatter_ws,
+    segment_reduce_noalloc,
+    noalloc_scratch_bytes,
     segment_reduce_backward,
     gather_scatter_backward,
     index_stats,

@@ -17,6 +17,13 @@
 #include "internal.h"
 #include "selector_generated.h"
 
+// Temporary memory of geot_segment_reduce_noalloc, for callers that cannot allocate:
+// one array per GPU, held from the library's load until the process ends. In host code
+// `scratch` names a host-side stand-in, not device memory: kernels and copies take the
+// per-device address that hipGetSymbolAddress returns for it (noalloc_scratch below).
+static constexpr size_t kNoAllocBytes = (size_t)128 << 20;
+static __device__ __align__(256) char scratch[kNoAllocBytes];
+
 namespace geot {
 namespace {
 
@@ -224,8 +231,12 @@ struct Profile {
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
 } g_prof;
 
+// Set while geot_segment_reduce_noalloc runs: it records no profiling events (creating
+// them is a runtime allocation).
+thread_local bool t_no_events = false;
+
 bool prof_take(hipEvent_t *a, hipEvent_t *b) {
-    if (!g_prof.armed || (int)g_prof.ev.size() >= g_prof.cap) return false;
+    if (t_no_events || !g_prof.armed || (int)g_prof.ev.size() >= g_prof.cap) return false;
     hipEvent_t e0, e1;
     if (hipEventCreate(&e0) != hipSuccess) return false;
     if (hipEventCreate(&e1) != hipSuccess) {
@@ -751,12 +762,53 @@ geot_status_t check_workspace(const void *workspace, size_t bytes) {
     return GEOT_SUCCESS;
 }
 
+// ---------------------------------------------------------------------------
+// temporary memory for callers that cannot allocate (geot_segment_reduce_noalloc)
+// ---------------------------------------------------------------------------
+std::mutex g_noalloc_mu;
+std::map<int, char *> g_noalloc_ptr;  // device -> address of that device's `scratch`
+
+// The current device's copy of `scratch`, looked up once per device (with it current).
+geot_status_t noalloc_scratch(char **ptr) {
+    int dev = 0;
+    GEOT_HIP(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_noalloc_mu);
+    auto it = g_noalloc_ptr.find(dev);
+    if (it != g_noalloc_ptr.end()) {
+        *ptr = it->second;
+        return GEOT_SUCCESS;
+    }
+    void *q = nullptr;
+    GEOT_HIP(hipGetSymbolAddress(&q, HIP_SYMBOL(::scratch)), "hipGetSymbolAddress(scratch)");
+    if (!q || ((uintptr_t)q & 255) != 0) return fail(GEOT_ERROR_HIP, "scratch array has no aligned device address");
+    g_noalloc_ptr[dev] = (char *)q;
+    *ptr = (char *)q;
+    return GEOT_SUCCESS;
+}
+
 }  // namespace
 }  // namespace geot
 
 using namespace geot;
 
 extern "C" {
+
+geot_status_t geot_segment_reduce_noalloc(const float *src, const int64_t *sorted_index, int64_t nnz,
+                                          int64_t num_segments, int64_t F, geot_op_t op, float *out,
+                                          void *stream) {
+    t_detail.clear();
+    char *ptr = nullptr;
+    geot_status_t s = noalloc_scratch(&ptr);
+    if (s != GEOT_SUCCESS) return s;
+    Problem p{false, src, 0, nullptr, nullptr, sorted_index, nnz, num_segments, F, op, out};
+    Workspace ws{ptr, kNoAllocBytes};
+    t_no_events = true;
+    s = reduce(p, (hipStream_t)stream, nullptr, &ws);
+    t_no_events = false;
+    return s;
+}
+
+size_t geot_noalloc_scratch_bytes(void) { return kNoAllocBytes; }
 
 geot_status_t geot_segment_reduce_with(const float *src, const int64_t *sorted_index, int64_t nnz,
                                        int64_t num_segments, int64_t F, geot_op_t op, float *out,

@@ -82,6 +82,9 @@ def lib() -> ctypes.CDLL:
     L.geot_gather_scatter_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, i32, pc, ctypes.POINTER(sz)]
     L.geot_segment_reduce_ws.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p, sz, p, pc]
     L.geot_gather_scatter_ws.argtypes = [p, i64, p, p, p, i64, i64, i64, ctypes.c_int, p, p, sz, p, pc]
+    L.geot_segment_reduce_noalloc.argtypes = [p, p, i64, i64, i64, ctypes.c_int, p, p]
+    L.geot_noalloc_scratch_bytes.argtypes = []
+    L.geot_noalloc_scratch_bytes.restype = sz
     L.geot_last_choice.argtypes = [pc]
     L.geot_release_scratch.argtypes = []
     L.geot_profile_begin.argtypes = [i32]
@@ -96,7 +99,7 @@ def lib() -> ctypes.CDLL:
                  "geot_last_choice", "geot_profile_begin", "geot_profile_end", "geot_release_scratch",
                  "geot_segment_reduce_backward", "geot_gather_scatter_backward",
                  "geot_segment_reduce_workspace_size", "geot_gather_scatter_workspace_size",
-                 "geot_segment_reduce_ws", "geot_gather_scatter_ws"):
+                 "geot_segment_reduce_ws", "geot_gather_scatter_ws", "geot_segment_reduce_noalloc"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -333,6 +336,30 @@ def gather_scatter_ws(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor |
                                           _stream(x.device), ctypes.byref(c) if c is not None else None)
     _raise(st)
     return out
+
+
+def segment_reduce_noalloc(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str,
+                           out: torch.Tensor) -> torch.Tensor:
+    """segment_reduce (fp32 src, int64 index) into a given `out`, with no allocation anywhere:
+    the library's static per-GPU array holds its temporaries (geot_segment_reduce_noalloc)."""
+    _dev(src, "src", torch.float32, 2)
+    _dev(index, "index", torch.int64, 1)
+    _dev(out, "out", torch.float32, 2)
+    if index.numel() != src.shape[0]:
+        raise ValueError("index must have one entry per row of src")
+    S, F = int(num_segments), src.shape[1]
+    _shape(out, "out", (S, F))
+    _on_gpu(src=src, index=index, out=out)
+    with _OnDevice(src.device):
+        st = lib().geot_segment_reduce_noalloc(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
+                                               OPS[reduce], out.data_ptr(), _stream(src.device))
+    _raise(st)
+    return out
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size of the static per-GPU array of segment_reduce_noalloc."""
+    return int(lib().geot_noalloc_scratch_bytes())
 
 
 def segment_reduce_backward(grad_out: torch.Tensor, index: torch.Tensor, reduce: str = "sum",
