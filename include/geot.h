@@ -110,8 +110,11 @@ typedef enum { GEOT_FAMILY_AUTO = 0, GEOT_FAMILY_EP = 1, GEOT_FAMILY_SP = 2 } ge
  * waves). Zero in any field means "derive it from the shape". */
 typedef struct {
     int32_t family; /* geot_family_t */
-    int32_t vec;    /* elements per lane load: 1, 2, 4, or 8 for 16-bit storage (the typed calls); clamped
-                       down to what F and alignment allow. With vec 8, lanes is at most 32 */
+    int32_t vec;    /* elements per lane load: 1, 2, 4, or 8 for 16-bit storage (the typed calls), or 3 for
+                       fp32 rows of 3 floats; clamped down to what F and alignment allow. With vec 8,
+                       lanes is at most 32. fp32 rows whose width is no multiple of 4 may still take
+                       vec 4: the vector that would cross a row's end reads the row's last 4
+                       floats instead, overlapping its neighbour */
     int32_t lanes;  /* lanes sharing one row: 1, 2, 4, 8, 16, 32 or 64 */
     int32_t rows;   /* EP: consecutive rows per row group (1..4096) */
     int32_t groups; /* SP: row groups of one wave that cooperate on one segment (1..64/lanes) */

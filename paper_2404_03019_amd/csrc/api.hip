@@ -325,6 +325,16 @@ int widest_vec(const Problem &p) {
     return 1;
 }
 
+// fp32 rows whose width is no multiple of 4 still move in 4-float vectors: gfx950 loads
+// and stores them at any 4-byte aligned address, and the vector that would cross a row's
+// end takes the row's last 4 columns (overlapping its neighbour). Rows of 3 floats take
+// one 3-float vector a lane. 0: neither applies.
+int ragged_vec(const Problem &p) {
+    if (p.elem != ELEM_F32 || p.F < 3 || p.F % 4 == 0) return 0;
+    if (((uintptr_t)p.src & 3) != 0 || ((uintptr_t)p.out & 3) != 0) return 0;
+    return p.F == 3 ? 3 : 4;
+}
+
 geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved *r,
                       bool from_selector = false) {
     const int loads = GEOT_FLAG_NT_LOADS | GEOT_FLAG_CACHED_LOADS;
@@ -337,8 +347,12 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     if (r->family == GEOT_FAMILY_SP && p.typed())
         return fail(GEOT_ERROR_UNSUPPORTED, "the segment-parallel family takes fp32 data with int64 ids only");
     const int vmax = widest_vec(p);
-    int V = c.vec == 0 ? vmax : c.vec;
+    // ragged rows: 4-float vectors (3 for F = 3) where the width allows no exact one (3-float
+    // vectors: one lane a row)
+    const int vrag = ragged_vec(p);
+    int V = c.vec == 0 ? (vrag ? vrag : vmax) : c.vec;
     int lanes = c.lanes, rows = c.rows;
+    if (V == 3 && lanes > 1) V = vmax;   // a 3-float vector covers the row alone
     if (from_selector && p.esize() == 2 && vmax == 8) {
         // tree leaves are fit on fp32 shapes, which load 4 floats here (F % 8 == 0): load 8
         // 16-bit elements instead, keeping the columns of one row group and the bytes it
@@ -348,10 +362,15 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
         if (lanes != 0) lanes = std::max(1, lanes * v32 / V);
         if (rows != 0) rows = std::min(4096, rows * V / v32);
     }
-    if (!(V == 1 || V == 2 || V == 4 || V == 8))
+    if (!(V == 1 || V == 2 || V == 3 || V == 4 || V == 8))
         return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2, 4 or (16-bit storage) 8");
     if (V == 8 && p.esize() != 2) return fail(GEOT_ERROR_UNSUPPORTED, "vec 8 needs 16-bit storage");
-    while (V > vmax) V >>= 1;  // clamp to what F and the pointers allow
+    if (V == 3 && c.vec == 3 && vrag != 3)
+        return fail(GEOT_ERROR_UNSUPPORTED, "vec 3 needs fp32 rows of 3 floats");
+    if (V != vrag || V == 0) {
+        if (V == 3) V = vmax;
+        while (V > vmax) V >>= 1;  // clamp to what F and the pointers allow
+    }
     int L, NT;
     auto_lanes(p.F, V, &L, &NT);
     if (lanes != 0) {

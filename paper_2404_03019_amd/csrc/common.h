@@ -29,13 +29,29 @@ __device__ __forceinline__ float red_apply(float a, float b) {
     }
 }
 
+// fp32 vectors of 2, 3 and 4 elements that need only 4-byte alignment. gfx950 loads and
+// stores them with one dwordx2 / x3 / x4 instruction at any 4-byte aligned address, so a
+// row of odd width (rows at F * 4 bytes) still moves in whole vectors: a lane whose
+// vector would cross the end of the row takes the last V columns instead (overlapping
+// its neighbour's, which it computes identically).
+typedef float f32x2_t __attribute__((ext_vector_type(2), aligned(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4), aligned(4)));
+struct f32x3_t {
+    float x, y, z;
+};
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 template <int V>
 __device__ __forceinline__ void load_vec(const float *p, float *x) {
     if constexpr (V == 4) {
-        const float4 t = *reinterpret_cast<const float4 *>(p);
+        const f32x4_t t = *reinterpret_cast<const f32x4_t *>(p);
         x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    } else if constexpr (V == 3) {
+        const f32x3_t t = *reinterpret_cast<const f32x3_t *>(p);
+        x[0] = t.x; x[1] = t.y; x[2] = t.z;
     } else if constexpr (V == 2) {
-        const float2 t = *reinterpret_cast<const float2 *>(p);
+        const f32x2_t t = *reinterpret_cast<const f32x2_t *>(p);
         x[0] = t.x; x[1] = t.y;
     } else {
         x[0] = *p;
@@ -44,10 +60,6 @@ __device__ __forceinline__ void load_vec(const float *p, float *x) {
 
 // Non-temporal loads (the `nt` cache policy): for data read exactly once, such
 // as streamed rows and ids, which then does not displace data that is reused.
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 template <bool NT, typename T>
 __device__ __forceinline__ T ld(const T *p) {
@@ -62,6 +74,10 @@ __device__ __forceinline__ void load_vec_p(const float *p, float *x) {
     } else if constexpr (V == 4) {
         const f32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t *>(p));
         x[0] = t.x; x[1] = t.y; x[2] = t.z; x[3] = t.w;
+    } else if constexpr (V == 3) {
+        x[0] = __builtin_nontemporal_load(p);
+        x[1] = __builtin_nontemporal_load(p + 1);
+        x[2] = __builtin_nontemporal_load(p + 2);
     } else if constexpr (V == 2) {
         const f32x2_t t = __builtin_nontemporal_load(reinterpret_cast<const f32x2_t *>(p));
         x[0] = t.x; x[1] = t.y;
@@ -76,9 +92,11 @@ __device__ __forceinline__ void store_vec(float *p, const float *x) {
         *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
         *reinterpret_cast<float4 *>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
     } else if constexpr (V == 4) {
-        *reinterpret_cast<float4 *>(p) = make_float4(x[0], x[1], x[2], x[3]);
+        *reinterpret_cast<f32x4_t *>(p) = f32x4_t{x[0], x[1], x[2], x[3]};
+    } else if constexpr (V == 3) {
+        *reinterpret_cast<f32x3_t *>(p) = f32x3_t{x[0], x[1], x[2]};
     } else if constexpr (V == 2) {
-        *reinterpret_cast<float2 *>(p) = make_float2(x[0], x[1]);
+        *reinterpret_cast<f32x2_t *>(p) = f32x2_t{x[0], x[1]};
     } else {
         *p = x[0];
     }
@@ -234,8 +252,9 @@ __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_
         const int rows_per_pass = 256 / tpr;
         const int j0 = threadIdx.x % tpr;
         for (int64_t row = lo + threadIdx.x / tpr; row < hi; row += rows_per_pass) {
-            float *o = out + row * ld + c0;
-            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + (int64_t)j * V, z);
+            float *o = out + row * ld;
+            // a vector that would pass the row's end takes its last V columns (all zero)
+            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + min(c0 + (int64_t)j * V, F - V), z);
         }
     }
     gap_done(g, blk, nblk, cnt);

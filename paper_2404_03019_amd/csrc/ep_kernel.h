@@ -45,8 +45,9 @@ constexpr bool nts_eligible() {
     return MODE == SRC_ROWS && (int64_t)L * V * NT * (int64_t)sizeof(typename ElemT<E>::T) >= 128;
 }
 
+// One block's work of an element-parallel pass: block `bid` of `nblk`.
 template <int RED, int MODE, int V, int NT, int L, int E, typename I, bool NTS>
-__global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
+__device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, const int64_t nblk) {
     constexpr int NV = V * NT;        // floats per lane
     constexpr int GW = 64 / L;        // row groups per wave
     constexpr int NW = kBlock / 64;   // waves per block
@@ -79,9 +80,9 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
 
     if constexpr (MODE == SRC_PIECES) {
         // the final level's extra blocks write the runs of empty segments level 0 listed
-        const int64_t main_blocks = (int64_t)gridDim.x - a.gap_blocks;
-        if (a.gap_blocks > 0 && (int64_t)blockIdx.x >= main_blocks) {
-            gap_fill_rows_body<V>(a.out, a.F, a.ld_out, (int64_t)TW, a.S, a.gaps, blockIdx.x - main_blocks,
+        const int64_t main_blocks = nblk - a.gap_blocks;
+        if (a.gap_blocks > 0 && bid >= main_blocks) {
+            gap_fill_rows_body<V>(a.out, a.F, a.ld_out, (int64_t)TW, a.S, a.gaps, bid - main_blocks,
                                   a.gap_blocks);
             return;
         }
@@ -91,12 +92,12 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     int64_t chunk;
     int tile;
     if (a.tile_major) {
-        const int64_t nch = ((int64_t)gridDim.x - (MODE == SRC_PIECES ? (int64_t)a.gap_blocks : 0)) / a.ntiles;
-        tile = (int)(blockIdx.x / nch);
-        chunk = blockIdx.x - (int64_t)tile * nch;
+        const int64_t nch = (nblk - (MODE == SRC_PIECES ? (int64_t)a.gap_blocks : 0)) / a.ntiles;
+        tile = (int)(bid / nch);
+        chunk = bid - (int64_t)tile * nch;
     } else {
-        chunk = blockIdx.x / a.ntiles;
-        tile = (int)(blockIdx.x - chunk * a.ntiles);
+        chunk = bid / a.ntiles;
+        tile = (int)(bid - chunk * a.ntiles);
     }
     const int64_t bsize = (int64_t)G * a.K;
     const int64_t bstart = chunk * bsize;
@@ -105,12 +106,17 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     const int64_t r1 = min(r0 + (int64_t)a.K, bend);
     const bool has_rows = r0 < r1;
 
+    // Columns of this lane's vectors. Where F is not a multiple of V (fp32 only), the vector
+    // that would cross the row's end takes the row's last V columns instead: its loads stay
+    // inside the row, and the columns it shares with the previous vector are reduced in the
+    // same order by both lanes, so both store the same values.
     int64_t cb[NT];
     bool cv[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         cb[j] = (int64_t)tile * TW + (int64_t)(j * L + gl) * V;
         cv[j] = cb[j] < a.F;
+        if (cv[j]) cb[j] = min(cb[j], a.F - V);
     }
     const float neutral = red_neutral<RED>();
 
@@ -173,10 +179,12 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     auto load_term = [&](int64_t r, RV *xr, Cnt &c) {
         const T *p = src + r * a.ld_src;
         if constexpr (MODE == SRC_PIECES) {
+            // the values load beside the count, not after it: an empty partial's row (never
+            // written) is loaded too and made neutral where it is reduced (see `piece`)
             c = (Cnt)a.cnt[r];
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
-                if (cv[j] && c > 0) load_raw<E, V>(p + cb[j], xr[j]);
+                if (cv[j]) load_raw<E, V>(p + cb[j], xr[j]);
                 else for (int k = 0; k < V; ++k) xr[j].v[k] = neutral;  // partials are fp32
             }
         } else {
@@ -191,6 +199,15 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         for (int j = 0; j < NT; ++j) {
             if (cv[j]) widen<E, V>(xr[j], x + j * V);
             else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
+        }
+    };
+    // a partial's terms: neutral when it is empty (count 0)
+    auto piece = [&](float *x, Cnt c) {
+        if constexpr (MODE == SRC_PIECES) {
+            if (c == 0) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) x[k] = neutral;
+            }
         }
     };
 
@@ -230,7 +247,6 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
         cur = first_seg;
         prev = r0 > 0 ? (int32_t)idx[(r0 - 1) * ms] : -1;
         next = r1 < a.n ? (int32_t)idx[r1 * ms] : -1;
-        if (a.fill_gaps) fill_empty((int64_t)prev + 1, (int64_t)first_seg);
 
         if constexpr (MODE == SRC_GATHER) {
             // Edge metadata (segment id, source row, weight) of the next UG edges is
@@ -336,6 +352,7 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 for (int u = 0; u < U; ++u) {
                     float x[NV];
                     widen_term(xr[u], x);
+                    piece(x, c[u]);
                     step(s[u], x, c[u]);
                 }
             }
@@ -346,10 +363,14 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
                 const int32_t s = (int32_t)idx[r];
                 load_term(r, xr, c);
                 widen_term(xr, x);
+                piece(x, c);
                 step(s, x, c);
             }
         }
-        if (a.fill_gaps && r1 == a.n) fill_empty((int64_t)cur + 1, a.S);  // trailing empty segments
+        // empty segments before this run (written after the row loop, so the first loads of
+        // the loop do not wait for the neighbour's id) and, for the last run, after it
+        if (a.fill_gaps) fill_empty((int64_t)prev + 1, (int64_t)first_seg);
+        if (a.fill_gaps && r1 == a.n) fill_empty((int64_t)cur + 1, a.S);
     }
     const bool single_run = !head_done;  // the run holds one segment only: head == tail
     if (single_run) {
@@ -533,6 +554,11 @@ __global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
     }
 }
 
+template <int RED, int MODE, int V, int NT, int L, int E, typename I, bool NTS>
+__global__ __launch_bounds__(kBlock) void ep_kernel(const EpArgs a) {
+    ep_body<RED, MODE, V, NT, L, E, I, NTS>(a, blockIdx.x, gridDim.x);
+}
+
 template <int RED, int MODE, int V, int NT, int L, int E, typename I>
 hipError_t launch_one(const EpArgs &a, int64_t nchunks, hipStream_t stream) {
     const int64_t blocks = nchunks * a.ntiles + (MODE == SRC_PIECES ? (int64_t)a.gap_blocks : 0);
@@ -581,6 +607,12 @@ hipError_t by_shape(const EpArgs &a, int V, int NT, int L, int64_t nchunks, hipS
         }
     }
     if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1, E, I>(a, L, nchunks, st);
+    if constexpr (E == ELEM_F32) {  // three-float rows (F = 3), one lane a row
+        if (V == 3 && NT == 1) {
+            if (L != 1) return hipErrorInvalidValue;
+            return launch_one<RED, MODE, 3, 1, 1, E, I>(a, nchunks, st);
+        }
+    }
     if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1, E, I>(a, L, nchunks, st);
     if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2, E, I>(a, L, nchunks, st);
     if (V == 1 && NT == 1) return by_lanes<RED, MODE, 1, 1, E, I>(a, L, nchunks, st);

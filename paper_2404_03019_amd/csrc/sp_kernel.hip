@@ -44,6 +44,9 @@ __global__ __launch_bounds__(kBlock) void sp_kernel(const SpArgs a) {
     for (int j = 0; j < NT; ++j) {
         cb[j] = (int64_t)tile * TW + (int64_t)(j * L + gl) * V;
         cv[j] = cb[j] < a.F;
+        // F no multiple of V: the vector that would cross the row's end takes the last V
+        // columns (4-byte aligned loads and stores; shared columns reduce identically)
+        if (cv[j]) cb[j] = min(cb[j], a.F - V);
     }
     const float neutral = red_neutral<RED>();
     const bool live = s < a.S;
@@ -168,6 +171,10 @@ hipError_t by_lanes(const SpArgs &a, int L, hipStream_t st) {
 template <int RED, int MODE>
 hipError_t by_shape(const SpArgs &a, int V, int NT, int L, hipStream_t st) {
     if (V == 4 && NT == 1) return by_lanes<RED, MODE, 4, 1>(a, L, st);
+    if (V == 3 && NT == 1) {  // rows of 3 floats, one lane a row
+        if (L != 1) return hipErrorInvalidValue;
+        return launch_one<RED, MODE, 3, 1, 1>(a, st);
+    }
     if (V == 2 && NT == 1) return by_lanes<RED, MODE, 2, 1>(a, L, st);
     if (V == 2 && NT == 2) return by_lanes<RED, MODE, 2, 2>(a, L, st);
     if (V == 1 && NT == 1) return by_lanes<RED, MODE, 1, 1>(a, L, st);

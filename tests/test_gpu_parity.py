@@ -50,7 +50,7 @@ TINY_CHOICES = [
 ]
 
 
-@pytest.mark.parametrize("F", [1, 3, 4, 8])
+@pytest.mark.parametrize("F", [1, 3, 4, 5, 7, 8])
 def test_tiny_exhaustive_bit_exact(F):
     """Every non-decreasing index with nnz <= 5 over S <= 4 segments, integer values:
     every partial sum is exact, so sum and max must be bit-exact for every kernel choice."""
@@ -177,6 +177,106 @@ def test_max_nan_and_signed_zeros_bitwise(F):
     g = rng.standard_normal((S, F)).astype(np.float32)
     got = geot.segment_reduce_backward(up(g), up(idx), "max", up(src), up(out)).cpu().numpy()
     assert np.array_equal(got, oracle.segment_reduce_backward(g, idx, "max", src, out)), f"max gradient F={F}"
+
+
+RAGGED_F = [3, 5, 6, 7, 13, 15, 17, 31, 33, 63, 65, 127, 129, 255, 257, 301, 513]
+RAGGED_CHOICES = [
+    None,                                               # 4-float vectors (3 for F = 3) by default
+    dict(family="ep", vec=4, rows=1),                   # many blocks: partial levels
+    dict(family="ep", vec=4, lanes=2, rows=5),          # several column tiles, the last one ragged
+    dict(family="ep", vec=4, lanes=2, rows=3, flags=4),  # the same tiles one after another
+    dict(family="ep", vec=1, rows=7),                   # exact 1-float vectors, for comparison
+]
+
+
+@pytest.mark.parametrize("F", RAGGED_F)
+def test_ragged_rows_all_choices(F):
+    """Widths that are no multiple of 4: fp32 rows move in 4-float vectors at 4-byte aligned
+    addresses, the vector that would cross a row's end overlapping its neighbour (3-float
+    vectors for F = 3). Segment and fused forms, every op, every choice, against the oracle;
+    and the default choice bit-identical to exact 1-float vectors for max and to the oracle
+    for sum and mean."""
+    p = random_problem(600 + F, 9000, 700, F, "zipf", "normal", 0.1)
+    src, idx = p["src"], p["index"]
+    q = random_gather_problem(601 + F, 7000, 500, 400, F, "lognormal", "normal", True, 0.1)
+    for op in OPS:
+        ref, terms = oracle_segment(src, idx, 700, op)
+        gref, gterms = oracle_gather(q["X"], q["col"], q["weight"], q["index"], 500, op)
+        for ch in RAGGED_CHOICES:
+            say(f"ragged F={F} {op} choice={ch}")
+            compare(run_sr(src, idx, 700, op, ch), ref, op, terms, f"ragged F={F} {op} {ch}")
+            compare(run_gs(q["X"], q["col"], q["weight"], q["index"], 500, op, ch), gref, op, gterms,
+                    f"ragged gather F={F} {op} {ch}")
+    c = geot.select(9000, 700, F, "sum")
+    assert c["vec"] == (3 if F == 3 else 4), c
+    # a view that starts 4 bytes into its buffer: rows stay 4-byte aligned only
+    buf = torch.empty(src.size + 1, dtype=torch.float32, device=DEV)
+    view = buf[1:].view(src.shape)
+    view.copy_(up(src))
+    got = geot.segment_reduce(view, up(idx), 700, "max").cpu().numpy()
+    compare(got, oracle.segment_reduce(src, idx, 700, "max"), "max", None, f"ragged F={F} offset view")
+
+
+SMALL_CALL_CASES = [
+    # seed, nnz, S, F, dist, values, empty_frac: small inputs (one or two partial levels)
+    (41, 65536, 4096, 32, "zipf", "normal", 0.05),
+    (42, 20000, 19000, 4, "uniform", "normal", 0.6),    # long runs of empty segments, few rows
+    (43, 50000, 1500, 300, "zipf", "normal", 0.5),      # two column tiles
+    (44, 3000, 3000, 3, "one_heavy", "normal", 0.3),
+    (45, 200000, 100, 1, "lognormal", "normal", 0.2),
+    (46, 7, 5, 6, "uniform", "normal", 0.0),            # one block
+]
+
+
+def _runs_problem(seed, nnz, S, F, nseg):
+    """nnz rows in `nseg` segments spread over S: runs of about S / nseg empty segments
+    between them (the empty-run list gets records), and leading and trailing runs."""
+    rng = np.random.default_rng(seed)
+    ids = np.sort(rng.choice(np.arange(40, S - 40), size=nseg, replace=False))
+    cuts = np.sort(rng.choice(np.arange(1, nnz), size=nseg - 1, replace=False))
+    lengths = np.diff(np.concatenate([[0], cuts, [nnz]]))
+    index = np.repeat(ids, lengths).astype(np.int64)
+    return dict(src=rng.standard_normal((nnz, F)).astype(np.float32), index=index)
+
+
+@pytest.mark.parametrize("case", SMALL_CALL_CASES + [(47, 20000, 16000, 4, "runs", None, 10),
+                                                     (48, 9000, 1700, 300, "runs", None, 7)],
+                         ids=lambda c: f"seed{c[0]}-F{c[3]}-{c[4]}")
+def test_small_calls_repeat_and_replay(case):
+    """Small inputs: calls repeated on one stream (five times), through a caller workspace
+    and captured in a HIP graph (replayed with new inputs) all match the oracle; the list
+    of empty-segment runs empties itself after every call. The "runs" cases have long runs
+    of empty segments, which go through that list."""
+    seed, nnz, S, F, dist, values, ef = case
+    if dist == "runs":
+        p = _runs_problem(seed, nnz, S, F, ef)
+    else:
+        p = random_problem(seed, nnz, S, F, dist, values, ef)
+    src, idx = up(p["src"]), up(p["index"])
+    for op in OPS:
+        ref, terms = oracle_segment(p["src"], p["index"], S, op)
+        for k in range(5):
+            compare(geot.segment_reduce(src, idx, S, op).cpu().numpy(), ref, op, terms, f"small {op} call {k}")
+        ws = torch.empty(geot.workspace_size(nnz, S, F, op), dtype=torch.uint8, device=DEV)
+        compare(geot.segment_reduce_ws(src, idx, S, op, ws).cpu().numpy(), ref, op, terms, f"small {op} ws")
+    st = torch.cuda.Stream()
+    out = torch.empty((S, F), device=DEV)
+    with torch.cuda.stream(st):
+        geot.segment_reduce(src, idx, S, "sum", out=out)
+    st.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=st):
+        geot.segment_reduce(src, idx, S, "sum", out=out)
+    rng = np.random.default_rng(seed)
+    for k in range(3):
+        v = rng.standard_normal(p["src"].shape).astype(np.float32)
+        src.copy_(torch.from_numpy(v))
+        out.fill_(9.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        ref, terms = oracle_segment(v, p["index"], S, "sum")
+        compare(out.cpu().numpy(), ref, "sum", terms, f"small replay {k}")
 
 
 def test_fusion_identity_on_gpu():
@@ -409,7 +509,9 @@ def test_tile_major_order_matches_adjacent_tiles(F):
             a = geot.gather_scatter(X, col, w, row, R, op, choice=base)
             b = geot.gather_scatter(X, col, w, row, R, op, choice=dict(base, flags=4))
             tiled = geot.last_choice()["flags"] & 4
-            V = min(base.get("vec", 4), 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1))
+            # fp32 rows of 4 floats or more take 4-float vectors whatever F (the last one
+            # overlapping); an explicit vec 2 needs an even F
+            V = 4 if base.get("vec", 4) == 4 and F >= 4 else (2 if F % 2 == 0 else 1)
             assert bool(tiled) == (F > base["lanes"] * V), geot.last_choice()   # reported when tiles > 1
             assert torch.equal(a, b), f"gather F={F} {op} {base}"
             compare(b.cpu().numpy(), gref, op, gterms, f"tile-major gather F={F} {op} {base}")
