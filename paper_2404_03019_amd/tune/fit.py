@@ -162,7 +162,9 @@ NAMED_WEIGHT = 16.0            # the named benchmark workloads count this many t
 
 
 def lanes_for(F: int) -> int:
-    V = 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1)
+    """Lanes of a row group for fp32 rows of F columns: 4-float vectors from F = 4 on (the last
+    one overlapping when 4 does not divide F), one 3-float vector for F = 3, else F floats."""
+    V = 4 if F >= 4 else F
     vecs = -(-F // V)
     L = 1
     while L < vecs and L < 64:
@@ -170,10 +172,15 @@ def lanes_for(F: int) -> int:
     return L
 
 
+INHERIT = (0, 0, 0, 0)  # a leaf of the statistics tree that keeps the O(1) tree's choice
+
+
 def candidate_space(stats: bool, kind: str | None = None):
     """(family, rows, groups, tiles): tiles > 1 runs the element-parallel kernel over that many
-    column tiles in sequence (tile-major blocks; fused form only)."""
-    c = [(1, k, 1, 1) for k in EP_ROWS]
+    column tiles in sequence (tile-major blocks; fused form only). The statistics trees also
+    have INHERIT: the O(1) tree's choice for the same input."""
+    c = [INHERIT] if stats and kind is not None else []
+    c += [(1, k, 1, 1) for k in EP_ROWS]
     if kind != "segment":
         c += [(1, k, 1, t) for t in (2, 4) for k in TILE_ROWS]
     if stats:
@@ -189,13 +196,16 @@ def cand_key(cand, F: int) -> str:
     return f"f2_r0_g{min(g, 64 // lanes_for(F))}"
 
 
-def cost_matrix(data, cands):
+def cost_matrix(data, cands, inherit=None):
     """C[i, j] = w_i * log(time of candidate j / best measured time of input i); the named
-    workloads get weight NAMED_WEIGHT, every other input weight 1."""
+    workloads get weight NAMED_WEIGHT, every other input weight 1. `inherit(e)` gives the
+    candidate an INHERIT leaf stands for on input e."""
     C = np.full((len(data), len(cands)), MISSING_COST)
     for i, e in enumerate(data):
         tb, _ = best_of(e)
         for j, cand in enumerate(cands):
+            if cand == INHERIT:
+                cand = inherit(e)
             t = e["times"].get(cand_key(cand, e["instance"]["F"]))
             if t is not None and t > 0 and tb > 0:
                 C[i, j] = min(MISSING_COST, math.log(t / tb))
@@ -250,14 +260,20 @@ class CostTree:
         return n["leaf"]
 
 
-def emit_cost_tree(tree, names, cands, indent):
+def emit_cost_tree(tree, names, cands, indent, final=True):
+    """if/else of a tree. With final False (a statistics tree), a leaf returns its choice, and
+    an INHERIT leaf falls through to the O(1) tree that follows."""
     lines = []
 
     def rec(n, depth):
         pad = " " * (indent + 4 * depth)
         if "leaf" in n:
+            if cands[n["leaf"]] == INHERIT:
+                lines.append(f"{pad}// the O(1) tree's choice (below)")
+                return
             fam, k, g, t = cands[n["leaf"]]
-            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};" + (f" out[5] = {t};" if t > 1 else ""))
+            lines.append(f"{pad}out[0] = {fam}; out[3] = {k}; out[4] = {g};" + (f" out[5] = {t};" if t > 1 else "") +
+                         ("" if final else " return;"))
             return
         lines.append(f"{pad}if ({names[n['feature']]} <= {n['threshold']:.9g}) {{")
         rec(n["left"], depth + 1)
@@ -270,7 +286,12 @@ def emit_cost_tree(tree, names, cands, indent):
 
 
 class Fitted:
-    """The four trees (kind x stats) fitted on the database, and the single-pair ablation."""
+    """The four trees (kind x stats) fitted on the database, and the single-pair ablation.
+
+    The statistics tree of each operation refines its O(1) tree: it is fitted after it, with
+    one more candidate, INHERIT, whose cost on an input is that of the O(1) tree's choice. A
+    leaf therefore names another kernel only where that is measured better on the inputs that
+    reach it, and the tree as a whole never costs more than the O(1) tree on the database."""
 
     def __init__(self, data):
         self.data = data
@@ -279,14 +300,16 @@ class Fitted:
             for kind in KINDS:
                 sub = [e for e in data if kind_of(e) == kind]
                 X = [feature_row(e, stats, kind) for e in sub]
-                self.trees[(kind, stats)] = CostTree().fit(X, cost_matrix(sub, candidate_space(stats, kind)))
+                C = cost_matrix(sub, candidate_space(stats, kind), inherit=lambda e: self.choose(e, False))
+                self.trees[(kind, stats)] = CostTree().fit(X, C)
             self.single[stats] = CostTree().fit([feature_row(e, stats) for e in data],
                                                 cost_matrix(data, candidate_space(stats)))
 
     def choose(self, e, stats: bool):
         """(family, rows, groups, tiles) the emitted selector gives input e."""
         kind = kind_of(e)
-        return candidate_space(stats, kind)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
+        c = candidate_space(stats, kind)[self.trees[(kind, stats)].predict_one(feature_row(e, stats, kind))]
+        return self.choose(e, False) if c == INHERIT else c
 
     def choose_as_library(self, e, stats: bool):
         """What geot_select returns: the tree's choice, except that the segment-parallel
@@ -319,7 +342,8 @@ def render(fitted: Fitted) -> str:
             "//",
             f"// Training inputs: {n_seg} segment reductions, {n_gat} fused gather forms. One pair of",
             f"// trees per operation, depth <= {MAX_DEPTH}. Each leaf is the candidate with the least",
-            "// total log-slowdown over the inputs reaching it. out[0] family (1 element-parallel,",
+            "// total log-slowdown over the inputs reaching it; the tree with statistics refines the",
+            "// O(1) one (its leaves that keep the O(1) choice fall through to it). out[0] family (1 element-parallel,",
             "// 2 segment-parallel), out[3] rows per row group, out[4] row groups per segment",
             "// (clamped to the wave); out[1] vec, out[2] lanes: 0 = from the shape; out[5] column",
             "// tiles run one after another (1: the columns' own tiling, in adjacent blocks).",
@@ -337,12 +361,12 @@ def render(fitted: Fitted) -> str:
             "    (void)lnnz; (void)lS; (void)F; (void)lmean; (void)opmax; (void)weighted; (void)cv; (void)lmaxrel;",
             "    out[0] = 1; out[1] = 0; out[2] = 0; out[3] = 0; out[4] = 0; out[5] = 1;"]
     for kind, cond, close in (("segment", "    if (gather == 0) {", None), ("gather", "    } else {", "    }")):
-        body += [cond, "        if (!has_stats) {"]
-        body += emit_cost_tree(fitted.trees[(kind, False)], feature_names(False, kind),
-                               candidate_space(False, kind), 12)
-        body += ["        } else {"]
-        body += emit_cost_tree(fitted.trees[(kind, True)], feature_names(True, kind), candidate_space(True, kind), 12)
+        body += [cond, "        if (has_stats) {  // refines the O(1) tree below: a leaf that keeps its choice falls through"]
+        body += emit_cost_tree(fitted.trees[(kind, True)], feature_names(True, kind), candidate_space(True, kind), 12,
+                               final=False)
         body += ["        }"]
+        body += emit_cost_tree(fitted.trees[(kind, False)], feature_names(False, kind),
+                               candidate_space(False, kind), 8)
     body += ["    }", "}", "", "}  // namespace geot", ""]
     return "\n".join(body)
 
@@ -352,8 +376,10 @@ def _time_of(e, cand):
 
 
 def evaluate(fitted: Fitted):
-    """Per input: chosen time / best measured time, for the per-operation trees, the single
-    pair (ablation), the paper's recipe (per operation, ablation) and the hand rule."""
+    """Per input: chosen time / best measured time over every candidate (the segment-parallel
+    ones included), for the per-operation trees, the single pair (ablation), the paper's recipe
+    (per operation, ablation) and the hand rule; `nostats_ep` is the O(1) tree against the best
+    element-parallel candidate, the only family it chooses from."""
     cn, cs = candidate_space(False), candidate_space(True)
     # the paper's recipe: Top-1 labels, multi-output regressor, rounded leaves
     paper = {}
@@ -370,15 +396,16 @@ def evaluate(fitted: Fitted):
             name=e["instance"]["dist"], id=e["instance"]["id"], F=e["instance"]["F"],
             op=e["instance"]["op"], gather=e["instance"]["gather"], weighted=weighted_of(e),
             nnz=e["features"]["nnz"], best=tb,
-            nostats=_time_of(e, fitted.choose(e, False)) / tbe,
+            nostats=_time_of(e, fitted.choose(e, False)) / tb,
+            nostats_ep=_time_of(e, fitted.choose(e, False)) / tbe,
             stats=_time_of(e, fitted.choose_as_library(e, True)) / tb,
-            single_nostats=_time_of(e, fitted.choose_single(e, False)) / tbe,
+            single_nostats=_time_of(e, fitted.choose_single(e, False)) / tb,
             single_stats=_time_of(e, fitted.choose_single(e, True)) / tb,
             paper_nostats=e["times"].get(predict_cand(paper[(kind, False)], feature_row(e, False, kind), False, e),
-                                         math.nan) / tbe,
+                                         math.nan) / tb,
             paper_stats=e["times"].get(predict_cand(paper[(kind, True)], feature_row(e, True, kind), True, e),
                                        math.nan) / tb,
-            hand=e["times"].get("f1_r0_g0", math.nan) / tbe))
+            hand=e["times"].get("f1_r0_g0", math.nan) / tb))
     return rep
 
 
@@ -404,7 +431,8 @@ def main():
         print(f"-- {gname} ({len(sub)} inputs)")
         if not sub:
             continue
-        for k in ("nostats", "stats", "single_nostats", "single_stats", "paper_nostats", "paper_stats", "hand"):
+        for k in ("nostats", "nostats_ep", "stats", "single_nostats", "single_stats", "paper_nostats", "paper_stats",
+                  "hand"):
             v = [r[k] for r in sub]
             w = sum(1 for x in v if x == x and x <= 1.10)
             print(f"   {k:15s} geomean slowdown vs best {gm(v):.3f}  max {np.nanmax(v):.3f}  within 10%: {w}/{len(v)}")

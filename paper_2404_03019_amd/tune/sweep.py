@@ -97,6 +97,28 @@ def gather_instances(n: int, seed: int):
     return out
 
 
+def paired_instances(n: int, seed: int):
+    """Pairs of segment reductions with the same nnz, num_segments, F and op (so the same O(1)
+    features) and opposite length spreads: one with even lengths (fixed or Poisson), one with
+    heavy-tailed ones (Zipf or wide lognormal). Only the length statistics tell the two apart,
+    which is what the tree with statistics is for."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        F = int(FS[rng.integers(len(FS))])
+        op = "max" if rng.random() < 0.3 else "sum"
+        mean = float(2.0 ** rng.uniform(0.5, 8.0))
+        max_nnz = min(1.2e8, 3e9 / (4 * F + 20))
+        nnz = int(min(max_nnz, 10 ** rng.uniform(4.5, 8.0)))
+        S = max(1, int(round(nnz / mean)))
+        even = ("fixed", "poisson")[rng.integers(2)]
+        heavy = ("zipf", "lognormal_wide")[rng.integers(2)]
+        for j, dist in enumerate((even, heavy)):
+            out.append(dict(id=30000 + 2 * i + j, dist=dist, nnz=nnz, S=S, F=F, op=op, gather=0,
+                            seed=seed * 100003 + 2 * i + j))
+    return out
+
+
 def named_instances():
     """The five named workloads (lengths from their recipes), each op they are run with,
     and the SpMM workload without weights and with max."""
@@ -117,7 +139,9 @@ def named_instances():
 
 
 def lanes_for(F: int) -> int:
-    V = 4 if F % 4 == 0 else (2 if F % 2 == 0 else 1)
+    """Lanes of a row group for fp32 rows of F columns: 4-float vectors from F = 4 on (the last
+    one overlapping when 4 does not divide F), one 3-float vector for F = 3, else F floats."""
+    V = 4 if F >= 4 else F
     vecs = -(-F // V)
     L = 1
     while L < vecs and L < 64:
@@ -155,6 +179,8 @@ def main():
     ap.add_argument("--seed", type=int, default=2024)
     ap.add_argument("--gather-n", type=int, default=120)
     ap.add_argument("--gather-seed", type=int, default=4048)
+    ap.add_argument("--paired-n", type=int, default=40)
+    ap.add_argument("--paired-seed", type=int, default=6072)
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--budget-s", type=float, default=900.0, help="stop after this many seconds")
     args = ap.parse_args()
@@ -177,7 +203,7 @@ def main():
     t_start = time.time()
     with open(args.out, "a") as fout:
         for inst in named_instances() + instances(args.n, args.seed) + \
-                gather_instances(args.gather_n, args.gather_seed):
+                gather_instances(args.gather_n, args.gather_seed) + paired_instances(args.paired_n, args.paired_seed):
             if time.time() - t_start > args.budget_s:
                 print("budget reached", flush=True)
                 break

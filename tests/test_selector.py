@@ -92,11 +92,18 @@ def test_selector_beats_the_hand_rule_and_the_paper_recipe(fitted):
         return math.exp(sum(math.log(x) for x in v) / len(v))
 
     assert gm("nostats") < gm("paper_nostats") < gm("hand")
-    assert gm("nostats") <= 1.05
+    assert gm("stats") < gm("paper_stats")
+    # the O(1) tree against the best element-parallel candidate (the family it chooses from)
+    assert gm("nostats_ep") <= 1.05
+    # the tree with statistics refines the O(1) one: never worse on the database, and within 5 %
+    # of the best of every candidate (the segment-parallel family included)
+    assert gm("stats") <= gm("nostats") + 1e-9
+    assert gm("stats") <= 1.05
     fused = lambda r: r["gather"]
     assert gm("nostats", fused) <= gm("single_nostats", fused) + 1e-9
-    assert gm("nostats", fused) <= 1.05
+    assert gm("nostats_ep", fused) <= 1.05
     named = [r for r in rep if 10000 <= r["id"] < 20000]
-    # the large named workloads (above 0.2 ms) are within 10% of the best candidate
+    # the large named workloads (above 0.2 ms) are within 10% of the best candidate, with or
+    # without statistics
     big = [r for r in named if r["best"] >= 0.2]
-    assert big and all(r["nostats"] <= 1.10 for r in big), big
+    assert big and all(r["nostats"] <= 1.10 and r["stats"] <= 1.10 for r in big), big
