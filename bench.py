@@ -165,6 +165,100 @@ def copy_probe(n: int):
                       "GB/s": round(2 * (1 << 31) / dt / 1e9, 1)}), flush=True)
 
 
+def profile_configs(reps: int):
+    """Each named workload's main calls, `reps` times each, for counter and kernel-trace runs
+    (rocprofv3 --pmc FETCH_SIZE, --pmc WRITE_SIZE, --kernel-trace). Before the calls of the
+    k-th entry a marker runs: a segment reduction with no rows over 2048 * (k + 1) segments of
+    one column, i.e. one fill kernel of k + 1 blocks, and after them one of 1,000 blocks, so
+    the dispatches between the two belong to entry k. The entries, in order, are printed as
+    JSON lines."""
+    import numpy as np
+    import torch
+
+    import paper_2404_03019_amd as geot
+    from workloads import make_config
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    geot.lib()
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    e_src = torch.empty((0, 1), device=dev)
+    e_idx = torch.empty(0, dtype=torch.int64, device=dev)
+    entries = []
+
+    def entry(name, nbytes, fn):
+        k = len(entries)
+        torch.cuda.synchronize()
+        geot.segment_reduce(e_src, e_idx, 2048 * (k + 1), "sum")
+        for _ in range(reps):
+            fn()
+        geot.segment_reduce(e_src, e_idx, 2048 * 1000, "sum")   # end marker: 1,000 blocks
+        torch.cuda.synchronize()
+        entries.append(name)
+        print(json.dumps({"entry": k, "name": name, "algorithmic_bytes": nbytes, "calls": reps,
+                          "choice": geot.last_choice()}), flush=True)
+
+    a = torch.ones(1 << 29, device=dev)
+    b = torch.empty_like(a)
+    entry("plain copy of 2 GiB (calibration)", 2 * (1 << 31), lambda: b.copy_(a))
+    del a, b
+    c = make_config("c1_zipf_small")
+    s, i = up(c["src"]), up(c["index"])
+    entry("c1_zipf_small sum", seg_bytes(i.numel(), 4096, 32), lambda: geot.segment_reduce(s, i, 4096, "sum"))
+    c = make_config("c2_poisson_fsweep", F=256)
+    i = up(c["index"])
+    for F in (1, 3, 4, 15, 16, 64, 256):
+        s = up(c["src"][:, :F])
+        entry(f"c2_poisson_fsweep F={F} sum", seg_bytes(i.numel(), 100_000, F),
+              lambda: geot.segment_reduce(s, i, 100_000, "sum"))
+    del c, s, i
+    c = make_config("c5_pointcloud_knn")
+    s, i = up(c["src"]), up(c["index"])
+    for op in ("mean", "max"):
+        entry(f"c5_pointcloud_knn {op}", seg_bytes(i.numel(), 1_048_576, 64),
+              lambda: geot.segment_reduce(s, i, 1_048_576, op))
+    del c, s, i
+    torch.cuda.empty_cache()
+    c3 = make_config("c3_powerlaw_graph")
+    S3 = c3["num_segments"]
+    s, i = up(c3["src"]), up(c3["index"])
+    n3 = i.numel()
+    del c3
+    entry("c3_powerlaw_graph sum", seg_bytes(n3, S3, 32), lambda: geot.segment_reduce(s, i, S3, "sum"))
+    s16, i32 = s.to(torch.bfloat16), i.to(torch.int32)
+    entry("c3_powerlaw_graph sum bf16 int32", seg_bytes(n3, S3, 32, 2, 4),
+          lambda: geot.segment_reduce(s16, i32, S3, "sum"))
+    del s16, i32
+    g3 = torch.randn(S3, 32, device=dev)
+    gs = torch.empty_like(s)
+    for op in ("sum", "mean", "max"):
+        o = geot.segment_reduce(s, i, S3, op)
+        nb = n3 * 8 + n3 * 128 + S3 * 128 + (n3 * 128 + S3 * 128 if op == "max" else 0)
+        entry(f"c3_powerlaw_graph gradient {op}", nb,
+              lambda: geot.segment_reduce_backward(g3, i, op, s, o, grad_src=gs))
+    del s, i, g3, gs, o
+    torch.cuda.empty_cache()
+    c4 = make_config("c4_spmm")
+    R4 = c4["num_segments"]
+    X, col, w, row = up(c4["X"]), up(c4["col"]), up(c4["weight"]), up(c4["index"])
+    n4 = row.numel()
+    del c4
+    entry("c4_spmm sum", gather_bytes(n4, R4, 128), lambda: geot.gather_scatter(X, col, w, row, R4, "sum"))
+    X16, c32, r32 = X.to(torch.bfloat16), col.to(torch.int32), row.to(torch.int32)
+    entry("c4_spmm sum bf16 int32", gather_bytes(n4, R4, 128, 2, 4),
+          lambda: geot.gather_scatter(X16, c32, w, r32, R4, "sum"))
+    del X16, c32, r32
+    g4 = torch.randn(R4, 128, device=dev)
+    entry("c4_spmm gradient grad_X sum", n4 * 20 + n4 * 512 + R4 * 512,
+          lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_weight=False))
+    entry("c4_spmm gradient grad_weight sum", n4 * 20 + n4 * 512 + R4 * 512,
+          lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_x=False))
+    entry("c4_spmm transpose_edges", n4 * 40, lambda: geot.transpose_edges(col, w, row, R4, R4, "sum"))
+    o4 = geot.gather_scatter(X, col, w, row, R4, "max")
+    entry("c4_spmm gradient max", 3 * (n4 * 20 + n4 * 512 + R4 * 512),
+          lambda: geot.gather_scatter_backward(X, col, w, row, g4, "max", out=o4))
+
+
 def suite(reps: int):
     """One JSON line per measurement: every named workload and op, the gradients on the two
     large workloads, and a two-layer graph-convolution training step (library autograd vs the
@@ -420,11 +514,17 @@ def main():
                     help="approximate host seconds of oracle work for cpu_baseline")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="N",
                     help="only run N plain device copies of 2 GiB (calibrates HBM byte counters)")
+    ap.add_argument("--profile-configs", type=int, default=0, metavar="N",
+                    help="only run every named workload's main calls N times each, behind markers, "
+                         "for rocprofv3 counter and kernel-trace runs")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the headline line: one line per workload, op and gradient")
     args = ap.parse_args()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.profile_configs:
+        profile_configs(args.profile_configs)
         return
     if args.suite:
         suite(max(3, args.steps))
