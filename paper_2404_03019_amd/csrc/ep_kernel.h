@@ -133,12 +133,12 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                 float t[V];
 #pragma unroll
                 for (int k = 0; k < V; ++k) t[k] = v[j * V + k] / fn;
-                store_vec<V>(o + cb[j], t);
+                store_vec_nt<V>(o + cb[j], t);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NT; ++j)
-                if (cv[j]) store_vec<V>(o + cb[j], v + j * V);
+                if (cv[j]) store_vec_nt<V>(o + cb[j], v + j * V);
         }
     };
     // Segments [s_lo, s_hi) have no rows. Short runs are written here by the row
@@ -156,7 +156,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
             float *o = a.out + s * a.ld_out;
 #pragma unroll
             for (int j = 0; j < NT; ++j)
-                if (cv[j]) store_vec<V>(o + cb[j], z);
+                if (cv[j]) store_vec_nt<V>(o + cb[j], z);
         }
     };
     auto write_partial = [&](int slot, int32_t seg, const float *v, Cnt n) {

@@ -130,7 +130,7 @@ __global__ __launch_bounds__(kBlock) void sp_kernel(const SpArgs a) {
                 const float x = acc[j * V + k];
                 t[k] = n == 0 ? 0.0f : (a.mean ? x / fn : x);
             }
-            store_vec<V>(o + cb[j], t);
+            store_vec_nt<V>(o + cb[j], t);
         }
     }
 }
