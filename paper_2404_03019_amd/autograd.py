@@ -50,7 +50,13 @@ class Graph:
     The same edges sorted by source (geot_transpose_edges) turn the gradient
     w.r.t. the source features of sum and mean into one forward gather. That
     copy is built on first use and kept while the weights are unchanged (it is
-    rebuilt when an in-place update bumps the weight tensor's version)."""
+    rebuilt when an in-place update bumps the weight tensor's version).
+
+    The destination ids' length statistics (geot_index_stats, one pass over the ids,
+    synchronizing) are taken on the first forward and kept, so the selector of every
+    gather over this graph also sees how evenly the edges spread over the rows
+    (Section III-C: variance as a feature); they are refreshed when the ids are updated
+    in place."""
 
     # kernel choice for the gather over the transposed list from 2^20 edges: one column tile and
     # 256 rows per row group (the library's tree is fit on forward gathers, whose gathered rows
@@ -62,7 +68,15 @@ class Graph:
         self.num_nodes = int(num_nodes)
         self.num_src = int(num_src if num_src is not None else num_nodes)
         self._transposed = {}
+        self._stats = None
         self.gather_choice = self.TRANSPOSED_GATHER if row.numel() >= (1 << 20) else None
+
+    def stats(self):
+        """geot_index_stats of the destination ids (kept until the ids change in place)."""
+        version = self.row._version
+        if self._stats is None or self._stats[0] != version:
+            self._stats = (version, geot.index_stats(self.row.long(), self.num_nodes) if self.row.numel() else None)
+        return self._stats[1]
 
     def transposed(self, reduce: str):
         """(sorted_col, row_t, coef) for `reduce` in sum / mean."""
@@ -85,7 +99,8 @@ class GatherScatter(torch.autograd.Function):
     @staticmethod
     def forward(ctx, x, col, weight, row, num_rows: int, reduce: str = "sum", graph=None):
         x = x.contiguous()
-        out = geot.gather_scatter(x, col, weight, row, num_rows, reduce)
+        out = geot.gather_scatter(x, col, weight, row, num_rows, reduce,
+                                  stats=graph.stats() if graph is not None else None)
         ctx.reduce = reduce
         ctx.graph = graph
         ctx.save_for_backward(x, col, weight if weight is not None else torch.empty(0), row,

@@ -186,12 +186,22 @@ DTYPES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 INDEX_TYPES = {torch.int64: 0, torch.int32: 1}
 
 
+def _stats_choice(choice, stats, nnz, S, F, reduce, gather, weighted, plain):
+    """The selector's choice with the index statistics `stats` (geot_index_stats of the same
+    index, computed once by the caller, e.g. per static graph) when no choice is forced; the
+    segment-parallel family it may pick takes fp32 data with int64 ids only (`plain`)."""
+    if choice is not None or stats is None or not plain:
+        return choice
+    return select(nnz, S, F, reduce, gather=gather, stats=stats, weighted=weighted)
+
+
 def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, reduce: str = "sum",
-                   out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+                   out: torch.Tensor | None = None, choice=None, stats: dict | None = None) -> torch.Tensor:
     """out[s] = reduce over rows i of src with index[i] == s (geot_segment_reduce).
 
     src may be fp32, bf16 or fp16 and index int64 or int32 (geot_segment_reduce_typed);
-    out is fp32 in every case."""
+    out is fp32 in every case. `stats` (index_stats(index, num_segments), kept by the caller)
+    lets the selector use the length spread (geot_select with statistics)."""
     _dev(src, "src", tuple(DTYPES), 2)
     _dev(index, "index", tuple(INDEX_TYPES), 1)
     if index.numel() != src.shape[0]:
@@ -203,10 +213,11 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
     _on_gpu(src=src, index=index, out=out)
     if out is None:
         out = torch.empty((S, F), dtype=torch.float32, device=src.device)
-    c = _choice(choice)
+    plain = src.dtype == torch.float32 and index.dtype == torch.int64
+    c = _choice(_stats_choice(choice, stats, index.numel(), S, F, reduce, False, True, plain))
     cp = ctypes.byref(c) if c is not None else None
     with _OnDevice(src.device):
-        if src.dtype == torch.float32 and index.dtype == torch.int64:
+        if plain:
             st = lib().geot_segment_reduce_with(src.data_ptr(), index.data_ptr(), index.numel(), S, F,
                                                 OPS[reduce], out.data_ptr(), _stream(src.device), cp)
         else:
@@ -219,11 +230,12 @@ def segment_reduce(src: torch.Tensor, index: torch.Tensor, num_segments: int, re
 
 def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
                    row: torch.Tensor, num_rows: int, reduce: str = "sum",
-                   out: torch.Tensor | None = None, choice=None) -> torch.Tensor:
+                   out: torch.Tensor | None = None, choice=None, stats: dict | None = None) -> torch.Tensor:
     """out[r] = reduce over edges e with row[e] == r of weight[e] * x[col[e]] (geot_gather_scatter).
 
     x may be fp32, bf16 or fp16 and col / row int64 or int32 (both the same;
-    geot_gather_scatter_typed); weight and out are fp32."""
+    geot_gather_scatter_typed); weight and out are fp32. `stats`: index_stats(row, num_rows),
+    as for segment_reduce."""
     _dev(x, "x", tuple(DTYPES), 2)
     _dev(col, "col", tuple(INDEX_TYPES), 1)
     _dev(row, "row", (col.dtype,), 1)
@@ -240,11 +252,12 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
     _on_gpu(x=x, col=col, weight=weight, row=row, out=out)
     if out is None:
         out = torch.empty((R, F), dtype=torch.float32, device=x.device)
-    c = _choice(choice)
+    plain = x.dtype == torch.float32 and col.dtype == torch.int64
+    c = _choice(_stats_choice(choice, stats, row.numel(), R, F, reduce, True, weight is not None, plain))
     wp = weight.data_ptr() if weight is not None else None
     cp = ctypes.byref(c) if c is not None else None
     with _OnDevice(x.device):
-        if x.dtype == torch.float32 and col.dtype == torch.int64:
+        if plain:
             st = lib().geot_gather_scatter_with(x.data_ptr(), x.shape[0], col.data_ptr(), wp,
                                                 row.data_ptr(), row.numel(), R, F, OPS[reduce],
                                                 out.data_ptr(), _stream(x.device), cp)

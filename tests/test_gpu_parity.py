@@ -528,3 +528,28 @@ def test_tile_major_order_matches_adjacent_tiles(F):
         b = geot.gather_scatter(Xb, c32, w, r32, R, "sum", choice=dict(base, flags=4))
         assert geot.last_choice()["flags"] & 4
         assert torch.equal(a, b), f"bf16 gather F={F}"
+
+
+def test_selection_with_index_statistics():
+    """With the index's length statistics the selector also sees the spread of the lengths:
+    short, even segments take the segment-parallel family, a heavy tail keeps the element-
+    parallel one; either way every op matches the oracle. A Graph keeps its ids' statistics
+    for its gathers."""
+    even = random_problem(700, 400_000, 20_000, 15, "poisson", "normal", 0.0)
+    heavy = random_problem(701, 400_000, 20_000, 15, "one_heavy", "normal", 0.1)
+    for name, p, fam in (("even", even, 2), ("heavy", heavy, 1)):
+        s, i = up(p["src"]), up(p["index"])
+        st = geot.index_stats(i, 20_000)
+        for op in OPS:
+            say(f"statistics {name} {op}")
+            got = geot.segment_reduce(s, i, 20_000, op, stats=st)
+            assert geot.last_choice()["family"] == fam, (name, geot.last_choice())
+            ref, terms = oracle_segment(p["src"], p["index"], 20_000, op)
+            compare(got.cpu().numpy(), ref, op, terms, f"statistics {name} {op}")
+    from paper_2404_03019_amd.autograd import Graph, gather_scatter
+    q = random_gather_problem(702, 300_000, 15_000, 9_000, 15, "poisson", "normal", True, 0.0)
+    graph = Graph(up(q["col"]), up(q["index"]), 15_000, up(q["weight"]), num_src=9_000)
+    got = gather_scatter(up(q["X"]), graph.col, graph.weight, graph.row, 15_000, "sum", graph)
+    assert graph.stats()["max_len"] == int(q["lengths"].max())
+    ref, terms = oracle_gather(q["X"], q["col"], q["weight"], q["index"], 15_000, "sum")
+    compare(got.detach().cpu().numpy(), ref, "sum", terms, "graph gather with statistics")
