@@ -748,7 +748,8 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__
 // continue into the neighbouring runs (the lowest over the runs is then the lowest attaining
 // edge). No LDS table and no barrier: the slot-table kernel above ran 3.9 M blocks of 16 edges
 // on the SpMM graph. For one vector per thread (nvec <= 64); X rows of kArgBatch edges load
-// together.
+// together. (Loading the next batch's ids beside them held 83 VGPRs instead of 67, 5 waves per
+// SIMD instead of 7, and measured the same on the SpMM graph: 6.65 ms.)
 constexpr int kArgRun = 32;
 constexpr int kArgBatch = 4;
 template <int E, typename I, int V, typename A>
@@ -858,14 +859,24 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
                 for (int u = 0; u < kU; ++u) {
                     const int64_t r = (int64_t)t[u].y;
                     if ((uint64_t)r < (uint64_t)R) {
-                        load_f32<V>(gout + r * F + (int64_t)j * V, g[u]);
                         load_arg<unsigned, V>(arg + r * F + (int64_t)j * V, a[u]);
                     } else {
 #pragma unroll
-                        for (int k = 0; k < V; ++k) {
-                            g[u][k] = 0.0f;
-                            a[u][k] = ~0u;
-                        }
+                        for (int k = 0; k < V; ++k) a[u][k] = ~0u;
+                    }
+                }
+                // grad_out only where the record's edge receives one of this thread's features
+                // (the SpMM graph: 5.34 -> 4.53 ms; most records receive none)
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    bool any = false;
+#pragma unroll
+                    for (int k = 0; k < V; ++k) any |= a[u][k] == (unsigned)t[u].w;
+                    if (any) {
+                        load_f32<V>(gout + (int64_t)t[u].y * F + (int64_t)j * V, g[u]);
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < V; ++k) g[u][k] = 0.0f;
                     }
                 }
 #pragma unroll
@@ -911,13 +922,72 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
         ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)cc[q] < (uint64_t)nx;
     static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
     float acc[P];
-    if (nvec <= m.tpr) {  // one vector per thread and edge: all loads of the group's edges in flight together
+    if (OP == GEOT_BWD_MAX && nvec <= m.tpr) {
+        // max: each (row, feature) has one recipient, so on a power-law graph most edges of a
+        // long row receive none (on the SpMM graph a third of the edges receive any). The
+        // recipients therefore decide which X vectors are read at all: the grad_out row and its
+        // recipients load first (once per run of equal rows), and a thread loads its X vector of
+        // an edge only where that edge receives one of the thread's features. On the SpMM graph
+        // this pass took 7.28 -> 4.94 ms (fp32 X) and 7.20 -> 5.23 ms (bf16 X, int32 ids).
+        const bool lane = m.j0 < nvec;
+        bool lead[P];
+        float g[P][V];
+        A a[P][V];
+        Raw<E, V> rx[P];
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            lead[q] = !(q > 0 && ok[q - 1] && rr[q] == rr[q - 1]);
+            if (ok[q] && lane && lead[q]) {
+                load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
+                load_arg<A, V>(arg + rr[q] * F + (int64_t)m.j0 * V, a[q]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    g[q][k] = 0.0f;
+                    a[q][k] = (A)~(A)0;
+                }
+            }
+        }
+        float cur[V];
+        A ca[V];
+        unsigned mine[P];   // bit k: this edge is feature k's recipient
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            if (lead[q]) {
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    cur[k] = g[q][k];
+                    ca[k] = a[q][k];
+                }
+            }
+            const A e = (A)(e0 + q);
+            mine[q] = 0u;
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                if (ca[k] == e) mine[q] |= 1u << k;
+                g[q][k] = cur[k];   // this edge's grad_out values (its run's lead row)
+            }
+            if (ok[q] && mine[q]) load_raw<E, V>(X + cc[q] * F + (int64_t)m.j0 * V, rx[q]);
+            else rx[q] = Raw<E, V>{};
+        }
+#pragma unroll
+        for (int q = 0; q < P; ++q) {
+            float x[V];
+            widen<E, V>(rx[q], x);
+            acc[q] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < V; ++k) {
+                // a selected product, not a product by 0: the other features' values may be inf or NaN
+                const float t = g[q][k] * x[k];
+                acc[q] += (mine[q] >> k) & 1u ? t : 0.0f;
+            }
+        }
+    } else if (nvec <= m.tpr) {  // sum, one vector per thread and edge: all loads of the group's edges in flight together
         // X rows stay in their loaded words until the products (16-bit X: half the registers of
         // widened rows; bf16 / int32 on the SpMM graph held 92 VGPRs, 5 waves per SIMD, widened)
         const bool lane = m.j0 < nvec;
         bool lead[P];   // the first edge of a run with the same (valid) row: loads the row
         float g[P][V];
-        A a[P][V];
         Raw<E, V> rx[P];
 #pragma unroll
         for (int q = 0; q < P; ++q) {
@@ -929,36 +999,23 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
             }
             if (ok[q] && lane && lead[q]) {
                 load_f32<V>(gout + rr[q] * F + (int64_t)m.j0 * V, g[q]);
-                if constexpr (OP == GEOT_BWD_MAX) load_arg<A, V>(arg + rr[q] * F + (int64_t)m.j0 * V, a[q]);
             } else {
 #pragma unroll
-                for (int k = 0; k < V; ++k) {
-                    g[q][k] = 0.0f;
-                    a[q][k] = (A)~(A)0;
-                }
+                for (int k = 0; k < V; ++k) g[q][k] = 0.0f;
             }
         }
         float cur[V];
-        A ca[V];
 #pragma unroll
         for (int q = 0; q < P; ++q) {
             if (lead[q]) {
 #pragma unroll
-                for (int k = 0; k < V; ++k) {
-                    cur[k] = g[q][k];
-                    ca[k] = a[q][k];
-                }
+                for (int k = 0; k < V; ++k) cur[k] = g[q][k];
             }
             float x[V];
             widen<E, V>(rx[q], x);
             acc[q] = 0.0f;
-            const A e = (A)(e0 + q);
 #pragma unroll
-            for (int k = 0; k < V; ++k) {
-                // max: the other edges' products are masked out
-                const float gk = OP == GEOT_BWD_MAX && ca[k] != e ? 0.0f : cur[k];
-                acc[q] += gk * x[k];
-            }
+            for (int k = 0; k < V; ++k) acc[q] += cur[k] * x[k];
         }
     } else {
 #pragma unroll

@@ -144,6 +144,40 @@ def test_gather_backward_parity(case):
             assert gw is None
 
 
+@pytest.mark.parametrize("F", [3, 8, 64, 300])
+def test_gather_backward_max_nonfinite_values(F):
+    """Max gradients where X holds infinities and NaNs: an edge takes part in a feature's
+    weight-gradient product only where it is that feature's recipient, so an infinity or NaN in
+    another feature of its X row cannot turn its gradient into NaN (0 * inf). Columns repeat
+    inside rows, so +inf maxima tie and the first edge receives. Against the oracle, which
+    sums over the recipient features only: the same non-finite entries, the rest within the
+    bound. Widths with one vector per thread and with more vectors than a row's threads."""
+    rng = np.random.default_rng(90 + F)
+    nx, R = 40, 30
+    X = rng.standard_normal((nx, F)).astype(np.float32)
+    u = rng.random((nx, F))
+    X[u < 0.15] = np.inf
+    X[(u >= 0.15) & (u < 0.2)] = np.nan
+    lengths = rng.integers(0, 9, R)
+    row = np.repeat(np.arange(R), lengths).astype(np.int64)
+    col = rng.integers(0, nx, row.size).astype(np.int64)
+    col[1::3] = col[0::3][:col[1::3].size]   # repeated columns next to each other
+    w = rng.uniform(0.5, 1.5, row.size).astype(np.float32)
+    g = rng.standard_normal((R, F)).astype(np.float32)
+    out_np = forward_for_gradient(oracle.gather_scatter(X, col, w, row, R, "max"),
+                                  geot.gather_scatter(up(X), up(col), up(w), up(row), R, "max"), f"F={F}")
+    gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", up(out_np))
+    rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out_np)
+    ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out_np, absolute=True)
+    within(gx.cpu().numpy(), rx, ax, f"grad_X max, non-finite X, F={F}")
+    got = gw.cpu().numpy().astype(np.float64)
+    fin = np.isfinite(rw)
+    assert np.array_equal(np.isnan(got), np.isnan(rw)), f"grad_w NaN pattern F={F}"
+    assert np.array_equal(got[np.isinf(rw)], rw[np.isinf(rw)]), f"grad_w infinities F={F}"
+    assert (~fin).any() and fin.any()
+    within(got[fin], rw[fin], aw[fin], f"grad_w max, non-finite X, F={F}")
+
+
 def test_backward_edge_cases():
     # no rows: grad_src is empty; fused form with no edges: grad_X is all zeros
     g = up(np.ones((4, 3), dtype=np.float32))

@@ -1,5 +1,13 @@
 """A two-layer graph-convolution training step through the library's autograd wrappers,
-against the same model written with plain torch index_add in fp64 on the CPU."""
+against the same model written with plain torch index_add in fp64 on the CPU.
+
+Bar: the loss within 1e-5 of the fp64 loss (relative, at least 1 in scale), and every
+parameter gradient within 1e-5 * max|fp64 gradient| elementwise: the library's fp32 bound
+(1e-5 relative) taken over the whole tensor. An elementwise relative bound does not apply
+here: a weight gradient sums thousands of products of both signs, so its small entries are
+the result of cancellation and carry the absolute error of the large ones. For scale, the
+same model in fp32 with torch's CPU ops errs by up to 7e-6 of the largest gradient (the GIN
+weights), and the library's fp32 step by about 1e-6."""
 import numpy as np
 import pytest
 import torch
@@ -9,6 +17,13 @@ from workloads import random_gather_problem
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
+
+
+def close(got, ref, what):
+    """|got - ref| <= 1e-5 * max|ref| elementwise (see the module docstring)."""
+    err = (got.double().cpu() - ref).abs().max().item()
+    scale = ref.abs().max().item()
+    assert err <= 1e-5 * scale, (what, err, scale)
 
 
 def gcn_norm(row, col, n):
@@ -59,11 +74,9 @@ def test_two_layer_training_step(reduce, cached):
     lr = agg(ref[1](hr))
     loss_r = torch.nn.functional.cross_entropy(lr, torch.from_numpy(y))
     loss_r.backward()
-    assert abs(loss.item() - loss_r.item()) <= 1e-4 * max(1.0, abs(loss_r.item()))
+    assert abs(loss.item() - loss_r.item()) <= 1e-5 * max(1.0, abs(loss_r.item()))
     for a, b in zip(m, ref):
-        ga_ = a.lin.weight.grad.double().cpu()
-        gb_ = b.weight.grad
-        assert torch.allclose(ga_, gb_, rtol=2e-3, atol=2e-5), (reduce, (ga_ - gb_).abs().max())
+        close(a.lin.weight.grad, b.weight.grad, reduce)
 
 
 def test_graph_cache_follows_weight_updates():
@@ -114,8 +127,7 @@ def test_gin_training_step(cached):
     lr = layer(ref[1], torch.relu(layer(ref[0], torch.from_numpy(X).double())))
     loss_r = torch.nn.functional.cross_entropy(lr, torch.from_numpy(y))
     loss_r.backward()
-    assert abs(loss.item() - loss_r.item()) <= 1e-4 * max(1.0, abs(loss_r.item()))
+    assert abs(loss.item() - loss_r.item()) <= 1e-5 * max(1.0, abs(loss_r.item()))
     for a, b in zip(m, ref):
         for (name, pa), pb in zip(a.named_parameters(), b.parameters()):
-            ga_, gb_ = pa.grad.double().cpu(), pb.grad
-            assert torch.allclose(ga_, gb_, rtol=2e-3, atol=2e-5), (name, cached, (ga_ - gb_).abs().max())
+            close(pa.grad, pb.grad, (name, cached))
