@@ -137,6 +137,64 @@ def cpu_baseline(c3, c4, target_s: float):
     }
 
 
+def cpu_configs():
+    """The oracle on every named workload on the host: one line per workload with the serial
+    oracle's time (one host thread) and the threaded oracle's (one thread per CPU this process
+    may run on), both with the GPU value's algorithmic-byte formulas. The CPU baseline per
+    workload; it loads no GPU code."""
+    import numpy as np
+
+    import oracle
+    from workloads import make_config
+    from workloads.generators import C2_FEATURES
+
+    ser, mt = oracle.default(), oracle.mt()
+    host = {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
+
+    def secs(fn, reps):
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            ts.append(time.perf_counter() - t0)
+        return float(np.median(ts))
+
+    def line(name, nbytes, fn_ser, fn_mt):
+        reps = 1 if nbytes >= 1e9 else 3   # median of 3 below 1 GB
+        ts, tm = secs(fn_ser, reps), secs(fn_mt, reps)
+        rec = {"cpu": name, "algorithmic_bytes": nbytes, "repetitions": reps,
+               "serial_s": round(ts, 5), "serial_GB/s": round(nbytes / ts / 1e9, 3),
+               "threads": mt.threads, "threaded_s": round(tm, 5), "threaded_GB/s": round(nbytes / tm / 1e9, 3)}
+        rec.update(host)
+        print(json.dumps(rec), flush=True)
+
+    def seg(name, src, idx, S, op):
+        F = src.shape[1]
+        line(name, seg_bytes(idx.size, S, F), lambda: ser.segment_reduce(src, idx, S, op),
+             lambda: mt.segment_reduce(src, idx, S, op))
+
+    c = make_config("c1_zipf_small")
+    seg("c1_zipf_small sum", c["src"], c["index"], c["num_segments"], "sum")
+    c = make_config("c2_poisson_fsweep", F=256)
+    for F in C2_FEATURES:
+        src = np.ascontiguousarray(c["src"][:, :F])
+        for op in ("sum", "mean", "max"):
+            seg(f"c2_poisson_fsweep F={F} {op}", src, c["index"], c["num_segments"], op)
+    del c, src
+    c = make_config("c5_pointcloud_knn")
+    for op in ("mean", "max"):
+        seg(f"c5_pointcloud_knn {op}", c["src"], c["index"], c["num_segments"], op)
+    del c
+    c = make_config("c3_powerlaw_graph")
+    seg("c3_powerlaw_graph sum", c["src"], c["index"], c["num_segments"], "sum")
+    del c
+    c = make_config("c4_spmm")
+    R = c["num_segments"]
+    line("c4_spmm sum", gather_bytes(c["index"].size, R, 128),
+         lambda: ser.gather_scatter(c["X"], c["col"], c["weight"], c["index"], R, "sum"),
+         lambda: mt.gather_scatter(c["X"], c["col"], c["weight"], c["index"], R, "sum"))
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -312,20 +370,27 @@ def suite(reps: int):
     emit("c1_zipf_small sum", ms, b, cold)
     c = make_config("c2_poisson_fsweep", F=256)
     idx = up(c["index"])
+    st2 = geot.index_stats(idx, c["num_segments"])
     for F in C2_FEATURES:
         src = up(c["src"][:, :F])
         b = seg_bytes(idx.numel(), c["num_segments"], F)
         for op in ("sum", "mean", "max"):
             ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], op), b)
             emit(f"c2_poisson_fsweep F={F} {op}", ms, b, cold)
+        # with the index's length statistics (kept by the caller): the selector sees the spread
+        ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], "sum", stats=st2), b)
+        emit(f"c2_poisson_fsweep F={F} sum, with index statistics", ms, b, cold)
         del src
     del c
     c = make_config("c5_pointcloud_knn")
     src, idx = up(c["src"]), up(c["index"])
     b = seg_bytes(idx.numel(), c["num_segments"], 64)
+    st5 = geot.index_stats(idx, c["num_segments"])
     for op in ("mean", "max"):
         ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], op), b)
         emit(f"c5_pointcloud_knn {op}", ms, b, cold)
+        ms, cold = timed(lambda: geot.segment_reduce(src, idx, c["num_segments"], op, stats=st5), b)
+        emit(f"c5_pointcloud_knn {op}, with index statistics", ms, b, cold)
     del src, idx, c
     torch.cuda.empty_cache()
     # the two large workloads, forward and gradients
@@ -519,7 +584,12 @@ def main():
                          "for rocprofv3 counter and kernel-trace runs")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the headline line: one line per workload, op and gradient")
+    ap.add_argument("--cpu-configs", action="store_true",
+                    help="only the CPU baseline per named workload: the serial and the threaded oracle")
     args = ap.parse_args()
+    if args.cpu_configs:
+        cpu_configs()
+        return
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
