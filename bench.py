@@ -418,6 +418,17 @@ def suite(reps: int):
         ms, cold = timed(lambda: geot.segment_reduce_backward(g3, idx, op, src, out, grad_src=gsrc), b)
         emit(f"c3_powerlaw_graph backward {op}", ms, b, cold)
     del gsrc
+    # max recording its recipients (the forward writes a uint32 per output element besides
+    # out), then the gradient from them: one pass that writes grad_src (index + grad_src
+    # written + grad_out and the recipients read)
+    b = seg_bytes(n3, S3, 32) + S3 * 128
+    ms, cold = timed(lambda: geot.segment_reduce_max_arg(src, idx, S3), b)
+    emit("c3_powerlaw_graph max with recipients", ms, b, cold)
+    _, arg3 = geot.segment_reduce_max_arg(src, idx, S3)
+    b = n3 * 8 + n3 * 128 + 2 * S3 * 128
+    ms, cold = timed(lambda: geot.segment_reduce_backward_max_arg(g3, idx, arg3), b)
+    emit("c3_powerlaw_graph backward max from recorded recipients", ms, b, cold)
+    del arg3
     # the gradients with bf16 storage and int32 ids: grad_src written as bf16
     src16, idx32 = src.to(torch.bfloat16), idx.to(torch.int32)
     gsrc16 = torch.empty_like(src16)
@@ -476,6 +487,17 @@ def suite(reps: int):
     ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "max", out=out4), b)
     emit("c4_spmm backward max (grad_X and grad_weight)", ms, b, cold)
     del out4
+    # max recording its recipients, then both gradients from them (no recipient pass): bytes of
+    # the forward plus the recipients written; of the gradients, the weight pass's and the
+    # pull's streams as above (two passes)
+    b = gather_bytes(n4, R4, 128) + R4 * 512
+    ms, cold = timed(lambda: geot.gather_scatter_max_arg(X, col, w, row, R4), b)
+    emit("c4_spmm max with recipients", ms, b, cold)
+    _, arg4 = geot.gather_scatter_max_arg(X, col, w, row, R4)
+    b = 2 * (n4 * 20 + n4 * 512 + R4 * 512)
+    ms, cold = timed(lambda: geot.gather_scatter_backward_max_arg(X, col, w, row, g4, arg4), b)
+    emit("c4_spmm backward max from recorded recipients (grad_X and grad_weight)", ms, b, cold)
+    del arg4
     # a static graph keeps its column-sorted edge list: the gradient w.r.t. X is then one gather
     ms, _ = timed(lambda: geot.transpose_edges(col, w, row, R4, R4, "sum"), 1 << 40)
     emit("c4_spmm transpose_edges (once per static graph)", ms, n4 * 40, False)

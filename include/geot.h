@@ -377,6 +377,51 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
                                                  geot_op_t op, const float *grad_out, const float *out, float *grad_X,
                                                  float *grad_weight, void *stream);
 
+/* Max with recorded recipients (Section VI: training; the paper leaves the
+ * backward pass to future work). The forward max of geot_segment_reduce_typed /
+ * geot_gather_scatter_typed that also writes, for every output element, its
+ * recipient: the lowest row (edge) whose term equals the maximum, the same rule
+ * the max gradients above use (== test, so either zero attains a zero maximum).
+ *   arg  [num_segments x F] (rows x F for the fused form) uint32, overwritten:
+ *        a row number of sorted_index (an edge number of the fused form), or
+ *        0xFFFFFFFF where there is none (an empty segment, a NaN maximum).
+ * out is bit-identical to the plain call's. The gradients then take arg instead
+ * of finding the recipients again (geot_*_backward_max_arg below): for the SpMM
+ * workload that pass reads every edge's X row. Requires nnz < 2^32 - 1
+ * (GEOT_ERROR_UNSUPPORTED otherwise); arg must not overlap out or an input; its
+ * alignment counts with out's for the vector width. Always the element-parallel
+ * kernels (a kernel of each form with the recipients carried beside the values
+ * through the run, the block scan and the partial levels); temporary memory as
+ * for the plain call, plus one uint32 per partial element.
+ * Same storage and index types, checks and errors as the typed calls; choice as
+ * there (NULL: the selector's), except that the segment-parallel family is
+ * refused (GEOT_ERROR_UNSUPPORTED) and never selected.                       */
+geot_status_t geot_segment_reduce_max_arg(const void *src, geot_dtype_t src_type, const void *sorted_index,
+                                          geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                          int64_t F, float *out, uint32_t *arg, void *stream,
+                                          const geot_kernel_choice_t *choice);
+geot_status_t geot_gather_scatter_max_arg(const void *X, geot_dtype_t x_type, int64_t num_x_rows, const void *col,
+                                          const float *weight, const void *sorted_row,
+                                          geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                          float *out, uint32_t *arg, void *stream,
+                                          const geot_kernel_choice_t *choice);
+
+/* The max gradients from recorded recipients (arg of the calls above, for the
+ * same inputs): geot_segment_reduce_backward_typed / geot_gather_scatter_backward_typed
+ * with op = GEOT_OP_MAX, where the recipients are read from arg instead of being
+ * found from src (X) and out, which are not needed (X only for grad_weight).
+ * Results are bit-identical to those calls. grad_src is of src_type. Same
+ * checks; GEOT_ERROR_UNSUPPORTED for nnz >= 2^32 - 1.                       */
+geot_status_t geot_segment_reduce_backward_max_arg(const float *grad_out, const void *sorted_index,
+                                                   geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                                   int64_t F, const uint32_t *arg, void *grad_src,
+                                                   geot_dtype_t src_type, void *stream);
+geot_status_t geot_gather_scatter_backward_max_arg(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
+                                                   const void *col, const float *weight, const void *sorted_row,
+                                                   geot_index_type_t index_type, int64_t nnz, int64_t num_rows,
+                                                   int64_t F, const float *grad_out, const uint32_t *arg,
+                                                   float *grad_X, float *grad_weight, void *stream);
+
 /* The edge list sorted by source column instead of destination row: the
  * transposed problem whose fused gather gives the X gradient of sum and mean
  * (Section VI: training), kept by callers whose graph does not change between

@@ -21,6 +21,10 @@ from .geot import (  # noqa: F401
     noalloc_scratch_bytes,
     segment_reduce_backward,
     gather_scatter_backward,
+    segment_reduce_max_arg,
+    gather_scatter_max_arg,
+    segment_reduce_backward_max_arg,
+    gather_scatter_backward_max_arg,
     index_stats,
     transpose_edges,
     check_index,

@@ -14,31 +14,46 @@ import torch
 from . import geot
 
 
+# below this many rows (edges) the max records its recipients in the forward (32-bit numbers)
+_ARG_ROWS = (1 << 32) - 1
+
+
 class SegmentReduce(torch.autograd.Function):
-    """out = segment_reduce(src, index, num_segments, reduce); differentiable in src."""
+    """out = segment_reduce(src, index, num_segments, reduce); differentiable in src.
+
+    Max records each output element's recipient row in the forward (kept instead of src and
+    out), so the backward is one pass that writes the gradient."""
 
     @staticmethod
     def forward(ctx, src, index, num_segments: int, reduce: str = "sum"):
-        out = geot.segment_reduce(src.contiguous(), index, num_segments, reduce)
+        src = src.contiguous()
         ctx.reduce = reduce
         ctx.src_dtype = src.dtype
-        if reduce == "max":
-            ctx.save_for_backward(index, src, out)
+        ctx.recorded = reduce == "max" and index.numel() < _ARG_ROWS
+        if ctx.recorded:
+            out, arg = geot.segment_reduce_max_arg(src, index, num_segments)
+            ctx.save_for_backward(index, arg)
         else:
-            ctx.save_for_backward(index)
+            out = geot.segment_reduce(src, index, num_segments, reduce)
+            if reduce == "max":
+                ctx.save_for_backward(index, src, out)
+            else:
+                ctx.save_for_backward(index)
         return out
 
     @staticmethod
     def backward(ctx, grad_out):
+        grad_out = grad_out.contiguous()
+        if ctx.recorded:
+            index, arg = ctx.saved_tensors
+            return geot.segment_reduce_backward_max_arg(grad_out, index, arg, ctx.src_dtype), None, None, None
         if ctx.reduce == "max":
             index, src, out = ctx.saved_tensors
         else:
             (index,) = ctx.saved_tensors
             src = out = None
         # the gradient is written in src's storage type, with src's ids (int64 or int32)
-        g = geot.segment_reduce_backward(grad_out.contiguous(), index, ctx.reduce,
-                                         src.contiguous() if src is not None else None, out,
-                                         dtype=ctx.src_dtype)
+        g = geot.segment_reduce_backward(grad_out, index, ctx.reduce, src, out, dtype=ctx.src_dtype)
         return g, None, None, None
 
 
@@ -99,12 +114,16 @@ class GatherScatter(torch.autograd.Function):
     @staticmethod
     def forward(ctx, x, col, weight, row, num_rows: int, reduce: str = "sum", graph=None):
         x = x.contiguous()
-        out = geot.gather_scatter(x, col, weight, row, num_rows, reduce,
-                                  stats=graph.stats() if graph is not None else None)
+        ctx.recorded = reduce == "max" and row.numel() < _ARG_ROWS
+        if ctx.recorded:   # max: each element's recipient edge, kept for the backward instead of out
+            out, kept = geot.gather_scatter_max_arg(x, col, weight, row, num_rows)
+        else:
+            out = geot.gather_scatter(x, col, weight, row, num_rows, reduce,
+                                      stats=graph.stats() if graph is not None else None)
+            kept = out if reduce == "max" else torch.empty(0)
         ctx.reduce = reduce
         ctx.graph = graph
-        ctx.save_for_backward(x, col, weight if weight is not None else torch.empty(0), row,
-                              out if reduce == "max" else torch.empty(0))
+        ctx.save_for_backward(x, col, weight if weight is not None else torch.empty(0), row, kept)
         ctx.has_weight = weight is not None
         return out
 
@@ -121,9 +140,13 @@ class GatherScatter(torch.autograd.Function):
             gx = geot.gather_scatter(grad_out, row_t, coef, sorted_col, x.shape[0], "sum",
                                      choice=ctx.graph.gather_choice)
             need_x = False
-        gx2, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out, ctx.reduce,
-                                               out if ctx.reduce == "max" else None,
-                                               need_x=need_x, need_weight=need_w)
+        if ctx.recorded:   # out holds the recipients the forward recorded
+            gx2, gw = geot.gather_scatter_backward_max_arg(x, col, weight, row, grad_out, out,
+                                                           need_x=need_x, need_weight=need_w)
+        else:
+            gx2, gw = geot.gather_scatter_backward(x, col, weight, row, grad_out, ctx.reduce,
+                                                   out if ctx.reduce == "max" else None,
+                                                   need_x=need_x, need_weight=need_w)
         gx = gx if gx is not None else gx2
         if gx is not None and gx.dtype != x.dtype:   # fp32 gradient of a 16-bit x: rounded once
             gx = gx.to(x.dtype)

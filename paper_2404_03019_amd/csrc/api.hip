@@ -265,6 +265,7 @@ struct Problem {
     int elem = ELEM_F32;   // storage type of src / X
     int idx32 = 0;         // idx and col hold int32
     int meta_stride = 1;   // gather: idx, col and w of edge e at [e * meta_stride] (internal records)
+    uint32_t *arg = nullptr;   // max only: each output element's recipient row (edge), [S x F]
     size_t esize() const { return elem == ELEM_F32 ? 4 : 2; }
     size_t isize() const { return idx32 ? 4 : 8; }
     bool typed() const { return elem != ELEM_F32 || idx32 != 0; }
@@ -316,7 +317,7 @@ int widest_vec(const Problem &p) {
     auto aligned = [&](int V) {
         const uintptr_t ms = (uintptr_t)(p.esize() * V - 1), mo = (uintptr_t)(4 * std::min(V, 4) - 1);
         if (p.F % V != 0) return false;
-        if (((uintptr_t)p.src & ms) != 0 || ((uintptr_t)p.out & mo) != 0) return false;
+        if (((uintptr_t)p.src & ms) != 0 || (((uintptr_t)p.out | (uintptr_t)p.arg) & mo) != 0) return false;
         return true;
     };
     if (p.esize() == 2 && aligned(8)) return 8;
@@ -331,7 +332,7 @@ int widest_vec(const Problem &p) {
 // one 3-float vector a lane. 0: neither applies.
 int ragged_vec(const Problem &p) {
     if (p.elem != ELEM_F32 || p.F < 3 || p.F % 4 == 0) return 0;
-    if (((uintptr_t)p.src & 3) != 0 || ((uintptr_t)p.out & 3) != 0) return 0;
+    if (((uintptr_t)p.src & 3) != 0 || (((uintptr_t)p.out | (uintptr_t)p.arg) & 3) != 0) return 0;
     return p.F == 3 ? 3 : 4;
 }
 
@@ -346,6 +347,8 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
         return fail(GEOT_ERROR_UNSUPPORTED, "unknown kernel family %d", c.family);
     if (r->family == GEOT_FAMILY_SP && p.typed())
         return fail(GEOT_ERROR_UNSUPPORTED, "the segment-parallel family takes fp32 data with int64 ids only");
+    if (r->family == GEOT_FAMILY_SP && p.arg)
+        return fail(GEOT_ERROR_UNSUPPORTED, "recipients come from the element-parallel family only");
     const int vmax = widest_vec(p);
     // ragged rows: 4-float vectors (3 for F = 3) where the width allows no exact one (3-float
     // vectors: one lane a row)
@@ -361,6 +364,14 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
         V = 8;
         if (lanes != 0) lanes = std::max(1, lanes * v32 / V);
         if (rows != 0) rows = std::min(4096, rows * V / v32);
+    }
+    if (from_selector && p.arg && rows != 0) {
+        // Carrying the recipients doubles what the block scan moves and holds registers (the
+        // SpMM gather: 94 -> 117 VGPRs, 4 waves per SIMD); longer row runs amortise the scan
+        // over more rows. Four times the tree's run, measured: the power-law graph 3.41 ->
+        // 2.63 ms (plain max 2.36), the SpMM gather 6.60 -> 5.95 ms (plain 5.21), in bf16 /
+        // int32 5.06 -> 4.73 ms.
+        rows = std::min(4096, rows * 4);
     }
     if (!(V == 1 || V == 2 || V == 3 || V == 4 || V == 8))
         return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2, 4 or (16-bit storage) 8");
@@ -505,6 +516,18 @@ geot_status_t check_args(const Problem &p) {
             overlaps(p.out, out_bytes, p.w, p.gather ? (size_t)p.nnz * 4 : 0))
             return fail(GEOT_ERROR_INVALID_VALUE, "out overlaps an input");
     }
+    if (p.arg) {   // the recipients of a max, 32-bit row (edge) numbers beside out
+        if (p.op != GEOT_OP_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "recipients are those of a max");
+        if (p.nnz >= (int64_t)kNoRecipient)
+            return fail(GEOT_ERROR_UNSUPPORTED, "recipients are 32-bit row numbers: fewer than 2^32 - 1 rows");
+        const size_t src_rows = (size_t)(p.gather ? p.num_x_rows : p.nnz);
+        if (overlaps(p.arg, out_bytes, p.out, out_bytes) ||
+            overlaps(p.arg, out_bytes, p.src, p.nnz > 0 ? src_rows * (size_t)p.F * p.esize() : 0) ||
+            overlaps(p.arg, out_bytes, p.idx, (size_t)p.nnz * p.isize()) ||
+            overlaps(p.arg, out_bytes, p.col, p.gather ? (size_t)p.nnz * p.isize() : 0) ||
+            overlaps(p.arg, out_bytes, p.w, p.gather ? (size_t)p.nnz * 4 : 0))
+            return fail(GEOT_ERROR_INVALID_VALUE, "arg overlaps out or an input");
+    }
     return GEOT_SUCCESS;
 }
 
@@ -530,7 +553,7 @@ constexpr size_t kBcastOffsetsMinBytes = (size_t)64 << 20;
 geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
                             char *base, const std::vector<size_t> &off_v,
                             const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
-                            int64_t ld_p, GapList gaps, hipStream_t st);
+                            const std::vector<size_t> &off_x, int64_t ld_p, GapList gaps, hipStream_t st);
 
 // Shape of the passes over fp32 partials: 8-element vectors (16-bit storage)
 // become 4-element vectors over twice the lanes, so the column tiles match.
@@ -544,7 +567,7 @@ void piece_shape(const Resolved &r, int *V, int *L) {
 // partials live in the temporary memory.
 struct EpPlan {
     std::vector<Level> lv;
-    std::vector<size_t> off_v, off_s, off_c;  // per level: values, segment ids, counts
+    std::vector<size_t> off_v, off_s, off_c, off_x;  // per level: values, segment ids, counts, recipients
     size_t bytes = 0;
     int64_t ld_p = 0;
 };
@@ -567,6 +590,7 @@ geot_status_t plan_ep(const Problem &p, const Resolved &r, EpPlan *pl) {
     pl->off_v.assign(lv.size(), 0);
     pl->off_s.assign(lv.size(), 0);
     pl->off_c.assign(lv.size(), 0);
+    pl->off_x.assign(lv.size(), 0);
     size_t bytes = 0;
     for (size_t l = 1; l < lv.size(); ++l) {
         pl->off_v[l] = bytes;
@@ -575,6 +599,10 @@ geot_status_t plan_ep(const Problem &p, const Resolved &r, EpPlan *pl) {
         bytes = align256(bytes + (size_t)lv[l].n * 8);
         pl->off_c[l] = bytes;
         bytes = align256(bytes + (size_t)lv[l].n * 8);
+        if (p.arg) {
+            pl->off_x[l] = bytes;
+            bytes = align256(bytes + (size_t)lv[l].n * (size_t)pl->ld_p * 4);
+        }
     }
     pl->bytes = bytes;
     return GEOT_SUCCESS;
@@ -589,14 +617,15 @@ geot_status_t run_ep(const Problem &p, const Resolved &r, hipStream_t st, const 
     StreamCtx *ctx = nullptr;
     s = call_scratch(pl.bytes, st, ws, &scratch, &gaps, &ctx);
     if (s != GEOT_SUCCESS) return s;
-    return poison(ctx, run_ep_levels(p, r, pl.lv, (char *)scratch, pl.off_v, pl.off_s, pl.off_c, pl.ld_p, gaps, st));
+    return poison(ctx, run_ep_levels(p, r, pl.lv, (char *)scratch, pl.off_v, pl.off_s, pl.off_c, pl.off_x, pl.ld_p,
+                                     gaps, st));
 }
 
 geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vector<Level> &lv,
                             char *base, const std::vector<size_t> &off_v,
                             const std::vector<size_t> &off_s, const std::vector<size_t> &off_c,
-                            int64_t ld_p, GapList gaps, hipStream_t st) {
-    const int red = p.op == GEOT_OP_MAX ? RED_MAX : RED_SUM;
+                            const std::vector<size_t> &off_x, int64_t ld_p, GapList gaps, hipStream_t st) {
+    const int red = p.op == GEOT_OP_MAX ? (p.arg ? RED_MAXARG : RED_MAX) : RED_SUM;
     for (size_t l = 0; l < lv.size(); ++l) {
         EpArgs a;
         memset(&a, 0, sizeof(a));
@@ -619,8 +648,10 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.ld_src = ld_p;
             a.idx = (const int64_t *)(base + off_s[l]);
             a.cnt = (const int64_t *)(base + off_c[l]);
+            if (p.arg) a.six = (const uint32_t *)(base + off_x[l]);
             a.fill_gaps = 0;
         }
+        a.arg_out = p.arg;
         a.n = lv[l].n;
         a.S = p.S;
         a.F = p.F;
@@ -630,6 +661,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
             a.pv = (float *)(base + off_v[l + 1]);
             a.pseg = (int64_t *)(base + off_s[l + 1]);
             a.pcnt = (int64_t *)(base + off_c[l + 1]);
+            if (p.arg) a.pix = (uint32_t *)(base + off_x[l + 1]);
             a.ld_p = ld_p;
         }
         if (l + 1 == lv.size() && l > 0) {  // the final level also fills the gap list of level 0
@@ -649,7 +681,7 @@ geot_status_t run_ep_levels(const Problem &p, const Resolved &r, const std::vect
         if (prof) GEOT_HIP(hipEventRecord(e1, st), "hipEventRecord");
         if (l == 0 && lv.size() == 1)  // one level: a pass of its own (else the final level's extra blocks)
             GEOT_HIP(launch_gap_fill_rows(p.out, p.F, p.F, std::min(r.V, 4), (int64_t)r.L * r.V * r.NT, p.S,
-                                          gaps, st),
+                                          gaps, p.arg, st),
                      "launch gap fill kernel");
     }
     return GEOT_SUCCESS;
@@ -702,7 +734,7 @@ geot_kernel_choice_t choose(const Problem &p, const geot_kernel_choice_t *forced
     if (forced) return *forced;
     geot_kernel_choice_t c;
     select_raw(p.nnz, p.S, p.F, p.op, p.gather ? (p.w ? 1 : 2) : 0, nullptr, &c);
-    if (p.typed() && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
+    if ((p.typed() || p.arg) && c.family == GEOT_FAMILY_SP) c = geot_kernel_choice_t{GEOT_FAMILY_EP, 0, 0, 0, 0, 0};
     // The leaves are fit on fp32 timings. A 16-bit X is half the bytes, and there the
     // ids read once per tile cost more than the smaller slab saves (SpMM shape, bf16:
     // 2.92 ms with two tiles in sequence, 2.83 ms without).
@@ -730,6 +762,12 @@ geot_status_t reduce(const Problem &p, hipStream_t st, const geot_kernel_choice_
     if (p.S == 0 || p.F == 0) return GEOT_SUCCESS;
     if (p.nnz == 0) {
         GEOT_HIP(launch_fill(p.out, p.S, p.F, p.F, GEOT_EMPTY_FILL, st), "launch fill kernel");
+        if (p.arg) {   // no recipients: all ones
+            float none;
+            const uint32_t bits = kNoRecipient;
+            memcpy(&none, &bits, 4);
+            GEOT_HIP(launch_fill(reinterpret_cast<float *>(p.arg), p.S, p.F, p.F, none, st), "launch fill kernel");
+        }
         t_last_choice = geot_kernel_choice_t{0, 0, 0, 0, 0, 0};
         return GEOT_SUCCESS;
     }
@@ -911,10 +949,12 @@ geot_status_t geot_gather_scatter(const float *X, int64_t num_x_rows, const int6
                                     out, stream, nullptr);
 }
 
-geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const void *sorted_index,
-                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
-                                                 int64_t F, geot_op_t op, const void *src, geot_dtype_t src_type,
-                                                 const float *out, void *grad_src, void *stream) {
+// The segment gradient; for max, `given` (may be NULL) holds the recipients a forward
+// geot_segment_reduce_max_arg recorded, and then src and out are not read.
+static geot_status_t seg_backward(const float *grad_out, const void *sorted_index, geot_index_type_t index_type,
+                                  int64_t nnz, int64_t num_segments, int64_t F, geot_op_t op, const void *src,
+                                  geot_dtype_t src_type, const float *out, const uint32_t *given, void *grad_src,
+                                  void *stream) {
     t_detail.clear();
     if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
@@ -930,18 +970,23 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
     if (F > ((int64_t)1 << 31) || num_segments > kMax / F || nnz > kMax / F)
         return fail(GEOT_ERROR_INVALID_VALUE, "size overflow");
     if (!grad_out || !sorted_index || !grad_src) return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
-    if (op == GEOT_OP_MAX && (!src || !out)) return fail(GEOT_ERROR_INVALID_VALUE, "max needs src and out");
+    if (given && op != GEOT_OP_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "recipients are those of a max");
+    if (given && nnz >= (int64_t)kNoRecipient)
+        return fail(GEOT_ERROR_UNSUPPORTED, "recipients are 32-bit row numbers: fewer than 2^32 - 1 rows");
+    if (op == GEOT_OP_MAX && !given && (!src || !out)) return fail(GEOT_ERROR_INVALID_VALUE, "max needs src and out");
     const size_t es = src_type == GEOT_DTYPE_F32 ? 4 : 2, is = index_type == GEOT_INDEX_I32 ? 4 : 8;
     const size_t gb = (size_t)(nnz * F) * es;
+    const bool reads = op == GEOT_OP_MAX && !given;   // src and out
     if (overlaps(grad_src, gb, grad_out, (size_t)(num_segments * F) * 4) ||
         overlaps(grad_src, gb, sorted_index, (size_t)nnz * is) ||
-        overlaps(grad_src, gb, src, op == GEOT_OP_MAX ? gb : 0) ||
-        overlaps(grad_src, gb, out, op == GEOT_OP_MAX ? (size_t)(num_segments * F) * 4 : 0))
+        overlaps(grad_src, gb, src, reads ? gb : 0) ||
+        overlaps(grad_src, gb, out, reads ? (size_t)(num_segments * F) * 4 : 0) ||
+        overlaps(grad_src, gb, given, given ? (size_t)(num_segments * F) * 4 : 0))
         return fail(GEOT_ERROR_INVALID_VALUE, "grad_src overlaps an input");
     // widest vector that F and every pointer allow (fp32 operands: 16-byte loads of 4; 16-bit
     // storage also 8 elements, loaded and stored as 16 bytes)
-    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)grad_src |
-                           (op == GEOT_OP_MAX ? ((uintptr_t)src | (uintptr_t)out) : 0);
+    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)grad_src | (uintptr_t)given |
+                           (reads ? ((uintptr_t)src | (uintptr_t)out) : 0);
     int V = 1;
     if (es == 2 && F % 8 == 0 && (ptrs & 15) == 0) V = 8;
     else if (F % 4 == 0 && (ptrs & 15) == 0) V = 4;
@@ -963,22 +1008,22 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
     const bool use_first = gb >= kBcastOffsetsMinBytes && (nnz >> rows_log2) >= num_segments;
     const bool from_off = mean || use_first;
     const size_t o_arg = 0,
-                 arg_b = mx ? align256((size_t)(num_segments * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
+                 arg_b = mx && !given ? align256((size_t)(num_segments * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
     const size_t o_off = o_arg + arg_b, o_first = o_off + (from_off ? align256((size_t)(num_segments + 1) * 8) : 0);
     const int64_t blocks = seg_bwd_blocks(nnz, F, V);
     GapList gaps;
-    if (mx || from_off) {
+    if ((mx && !given) || from_off) {
         geot_status_t s = stream_scratch(o_first + (use_first ? (size_t)blocks * 16 : 0), st, &scratch,
                                          from_off ? &gaps : nullptr, &ctx);
         if (s != GEOT_SUCCESS) return s;
     }
-    void *arg = mx ? scratch : nullptr;
+    void *arg = mx ? (given ? (void *)given : scratch) : nullptr;
     int64_t *off = from_off ? (int64_t *)((char *)scratch + o_off) : nullptr;
     int64_t *first = use_first ? (int64_t *)((char *)scratch + o_first) : nullptr;
     if (!from_off) {
         if (mx)
             GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, nullptr, nullptr, nnz, num_segments,
-                                        F, V, elem, arg, grad_src, st),
+                                        F, V, elem, arg, given != nullptr, grad_src, st),
                      "launch max backward kernels");
         else
             GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, nullptr, nullptr, nnz, num_segments, F, V,
@@ -999,7 +1044,7 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
         GEOT_HIP(launch_gap_fill_i64(off, num_segments + 1, gaps, st), "launch gap fill kernel");
         if (mx)
             GEOT_HIP(launch_seg_bwd_max(grad_out, sorted_index, idx32, src, out, off, first, nnz, num_segments, F, V,
-                                        elem, arg, grad_src, st),
+                                        elem, arg, given != nullptr, grad_src, st),
                      "launch max backward kernels");
         else
             GEOT_HIP(launch_seg_bwd_bcast(grad_out, sorted_index, idx32, off, first, nnz, num_segments, F, V, elem,
@@ -1007,6 +1052,26 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
                      "launch backward kernel");
         return GEOT_SUCCESS;
     }());
+}
+
+geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const void *sorted_index,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                                 int64_t F, geot_op_t op, const void *src, geot_dtype_t src_type,
+                                                 const float *out, void *grad_src, void *stream) {
+    return seg_backward(grad_out, sorted_index, index_type, nnz, num_segments, F, op, src, src_type, out, nullptr,
+                        grad_src, stream);
+}
+
+geot_status_t geot_segment_reduce_backward_max_arg(const float *grad_out, const void *sorted_index,
+                                                   geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                                   int64_t F, const uint32_t *arg, void *grad_src,
+                                                   geot_dtype_t src_type, void *stream) {
+    if (!arg) {
+        t_detail.clear();
+        return fail(GEOT_ERROR_INVALID_VALUE, "arg is NULL");
+    }
+    return seg_backward(grad_out, sorted_index, index_type, nnz, num_segments, F, GEOT_OP_MAX, nullptr, src_type,
+                        nullptr, arg, grad_src, stream);
 }
 
 geot_status_t geot_segment_reduce_backward(const float *grad_out, const int64_t *sorted_index,
@@ -1038,11 +1103,40 @@ geot_status_t geot_gather_scatter_typed(const void *X, geot_dtype_t x_type, int6
     return reduce(p, (hipStream_t)stream, choice);
 }
 
-geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
-                                                 const void *col, const float *weight, const void *sorted_row,
-                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
-                                                 geot_op_t op, const float *grad_out, const float *out, float *grad_X,
-                                                 float *grad_weight, void *stream) {
+geot_status_t geot_segment_reduce_max_arg(const void *src, geot_dtype_t src_type, const void *sorted_index,
+                                          geot_index_type_t index_type, int64_t nnz, int64_t num_segments,
+                                          int64_t F, float *out, uint32_t *arg, void *stream,
+                                          const geot_kernel_choice_t *choice) {
+    t_detail.clear();
+    if (!arg) return fail(GEOT_ERROR_INVALID_VALUE, "arg is NULL");
+    Problem p{false, src, 0, nullptr, nullptr, sorted_index, nnz, num_segments, F, GEOT_OP_MAX, out};
+    p.elem = (int)src_type;
+    p.idx32 = (int)index_type;
+    p.arg = arg;
+    return reduce(p, (hipStream_t)stream, choice);
+}
+
+geot_status_t geot_gather_scatter_max_arg(const void *X, geot_dtype_t x_type, int64_t num_x_rows, const void *col,
+                                          const float *weight, const void *sorted_row,
+                                          geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                          float *out, uint32_t *arg, void *stream,
+                                          const geot_kernel_choice_t *choice) {
+    t_detail.clear();
+    if (!arg) return fail(GEOT_ERROR_INVALID_VALUE, "arg is NULL");
+    Problem p{true, X, num_x_rows, col, weight, sorted_row, nnz, num_rows, F, GEOT_OP_MAX, out};
+    p.elem = (int)x_type;
+    p.idx32 = (int)index_type;
+    p.arg = arg;
+    return reduce(p, (hipStream_t)stream, choice);
+}
+
+// The fused-form gradients; for max, `given` (may be NULL) holds the recipients a forward
+// geot_gather_scatter_max_arg recorded, and then out is not read and no recipient pass runs.
+static geot_status_t gs_backward(const void *X, geot_dtype_t x_type, int64_t num_x_rows, const void *col,
+                                 const float *weight, const void *sorted_row, geot_index_type_t index_type,
+                                 int64_t nnz, int64_t num_rows, int64_t F, geot_op_t op, const float *grad_out,
+                                 const float *out, const uint32_t *given, float *grad_X, float *grad_weight,
+                                 void *stream) {
     t_detail.clear();
     if (op != GEOT_OP_SUM && op != GEOT_OP_MEAN && op != GEOT_OP_MAX)
         return fail(GEOT_ERROR_INVALID_VALUE, "unknown op %d", (int)op);
@@ -1067,8 +1161,11 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     }
     if (num_rows == 0 || num_x_rows == 0) return fail(GEOT_ERROR_INVALID_VALUE, "empty row or X range with nnz > 0");
     if (!col || !sorted_row || !grad_out) return fail(GEOT_ERROR_INVALID_VALUE, "NULL array");
-    if ((grad_weight || op == GEOT_OP_MAX) && !X) return fail(GEOT_ERROR_INVALID_VALUE, "X is NULL");
-    if (op == GEOT_OP_MAX && !out) return fail(GEOT_ERROR_INVALID_VALUE, "max needs out");
+    if (given && op != GEOT_OP_MAX) return fail(GEOT_ERROR_INVALID_VALUE, "recipients are those of a max");
+    if (given && nnz >= (int64_t)kNoRecipient)
+        return fail(GEOT_ERROR_UNSUPPORTED, "recipients are 32-bit edge numbers: fewer than 2^32 - 1 edges");
+    if ((grad_weight || (op == GEOT_OP_MAX && !given)) && !X) return fail(GEOT_ERROR_INVALID_VALUE, "X is NULL");
+    if (op == GEOT_OP_MAX && !given && !out) return fail(GEOT_ERROR_INVALID_VALUE, "max needs out");
     const size_t xb = (size_t)(num_x_rows * F) * 4;
     if (grad_X && (overlaps(grad_X, xb, X, X ? (size_t)(num_x_rows * F) * es : 0) ||
                    overlaps(grad_X, xb, grad_out, (size_t)(num_rows * F) * 4) ||
@@ -1085,7 +1182,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     // widest vector that F and every pointer allow (fp32 operands: 16-byte loads of 4; 16-bit X
     // also 8 elements, loaded as 16 bytes, except for max: its three passes ran faster with 4 on
     // the SpMM graph, bf16 / int32: 30.7 against 32.8 ms)
-    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)X | (uintptr_t)grad_X | (uintptr_t)out;
+    const uintptr_t ptrs = (uintptr_t)grad_out | (uintptr_t)X | (uintptr_t)grad_X | (uintptr_t)out | (uintptr_t)given;
     int V = 1;
     if (es == 2 && op != GEOT_OP_MAX && F % 8 == 0 && (ptrs & 15) == 0) V = 8;
     else if (F % 4 == 0 && (ptrs & 15) == 0) V = 4;
@@ -1100,7 +1197,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     size_t at = 0;
     auto take = [&](size_t b) { const size_t o = at; at = align256(at + b); return o; };
     const size_t o_roff = mean ? take((size_t)(num_rows + 1) * 8) : 0;
-    const size_t o_arg = mx ? take((size_t)(num_rows * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
+    const size_t o_arg = mx && !given ? take((size_t)(num_rows * F) * (seg_bwd_arg32(nnz) ? 4 : 8)) : 0;
     const int64_t nx = num_x_rows;
     const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
     const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
@@ -1120,7 +1217,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     if (s != GEOT_SUCCESS) return s;
     char *base = (char *)sg.p;
     int64_t *roff = mean ? (int64_t *)(base + o_roff) : nullptr;
-    void *arg = mx ? (void *)(base + o_arg) : nullptr;
+    void *arg = mx ? (given ? (void *)given : (void *)(base + o_arg)) : nullptr;
     if (mean) {
         void *unused = nullptr;
         GapList gaps;
@@ -1142,7 +1239,7 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     const int bop = op == GEOT_OP_SUM ? GEOT_BWD_SUM : (mean ? GEOT_BWD_MEAN : GEOT_BWD_MAX);
     // weights (and, for max where it is not pulled, X through atomic adds of the recipients only)
     GEOT_HIP(launch_gs_bwd(X, elem, num_x_rows, col, idx32, weight, sorted_row, roff, out, grad_out, nnz, num_rows,
-                           F, V, bop, arg, mx && !pull ? grad_X : nullptr, grad_weight, st),
+                           F, V, bop, arg, given != nullptr, mx && !pull ? grad_X : nullptr, grad_weight, st),
              "launch fused backward kernels");
     if (transpose) {
         // grad_X = gather_scatter of grad_out over the edges sorted by col (sum of coef * grad_out rows)
@@ -1189,6 +1286,28 @@ geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_t
     void *p_free = sg.p;
     sg.p = nullptr;
     return scratch_free(p_free, st);
+}
+
+geot_status_t geot_gather_scatter_backward_typed(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
+                                                 const void *col, const float *weight, const void *sorted_row,
+                                                 geot_index_type_t index_type, int64_t nnz, int64_t num_rows, int64_t F,
+                                                 geot_op_t op, const float *grad_out, const float *out, float *grad_X,
+                                                 float *grad_weight, void *stream) {
+    return gs_backward(X, x_type, num_x_rows, col, weight, sorted_row, index_type, nnz, num_rows, F, op, grad_out,
+                       out, nullptr, grad_X, grad_weight, stream);
+}
+
+geot_status_t geot_gather_scatter_backward_max_arg(const void *X, geot_dtype_t x_type, int64_t num_x_rows,
+                                                   const void *col, const float *weight, const void *sorted_row,
+                                                   geot_index_type_t index_type, int64_t nnz, int64_t num_rows,
+                                                   int64_t F, const float *grad_out, const uint32_t *arg,
+                                                   float *grad_X, float *grad_weight, void *stream) {
+    if (!arg) {
+        t_detail.clear();
+        return fail(GEOT_ERROR_INVALID_VALUE, "arg is NULL");
+    }
+    return gs_backward(X, x_type, num_x_rows, col, weight, sorted_row, index_type, nnz, num_rows, F, GEOT_OP_MAX,
+                       grad_out, nullptr, arg, grad_X, grad_weight, stream);
 }
 
 geot_status_t geot_gather_scatter_backward(const float *X, int64_t num_x_rows, const int64_t *col,

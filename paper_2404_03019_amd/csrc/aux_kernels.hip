@@ -106,8 +106,8 @@ __global__ __launch_bounds__(256) void offsets_unaligned_kernel(const I *idx, in
 // One block per record at a time: rows [first, end) of the record's column tile = 0.
 template <int V>
 __global__ __launch_bounds__(256) void gap_fill_rows_kernel(float *out, int64_t F, int64_t ld,
-                                                            int64_t tw, int64_t rows, GapList g) {
-    gap_fill_rows_body<V>(out, F, ld, tw, rows, g, blockIdx.x, gridDim.x);
+                                                            int64_t tw, int64_t rows, GapList g, uint32_t *arg) {
+    gap_fill_rows_body<V>(out, F, ld, tw, rows, g, blockIdx.x, gridDim.x, arg);
 }
 
 __global__ __launch_bounds__(256) void gap_fill_i64_kernel(int64_t *arr, int64_t len, GapList g) {
@@ -227,13 +227,13 @@ hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t 
 // 1024 blocks: a list with many records keeps the chip busy, an empty list
 // costs one counter read per block.
 hipError_t launch_gap_fill_rows(float *out, int64_t F, int64_t ld, int V, int64_t tw, int64_t rows,
-                                GapList gaps, hipStream_t stream) {
+                                GapList gaps, uint32_t *arg, hipStream_t stream) {
     if (V == 4)
-        hipLaunchKernelGGL(gap_fill_rows_kernel<4>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+        hipLaunchKernelGGL(gap_fill_rows_kernel<4>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps, arg);
     else if (V == 2)
-        hipLaunchKernelGGL(gap_fill_rows_kernel<2>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+        hipLaunchKernelGGL(gap_fill_rows_kernel<2>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps, arg);
     else
-        hipLaunchKernelGGL(gap_fill_rows_kernel<1>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps);
+        hipLaunchKernelGGL(gap_fill_rows_kernel<1>, dim3(1024), dim3(256), 0, stream, out, F, ld, tw, rows, gaps, arg);
     return hipGetLastError();
 }
 

@@ -1620,14 +1620,17 @@ bool seg_bwd_arg32(int64_t n) { return n < (int64_t)0xffffffffLL; }
 
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
                               const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
-                              int elem, void *arg, void *gsrc, hipStream_t st) {
+                              int elem, void *arg, bool given, void *gsrc, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     if (first && !off) return hipErrorInvalidValue;
     const bool a32 = seg_bwd_arg32(n);
+    if (given && !a32) return hipErrorInvalidValue;   // recorded recipients are 32-bit
     // all ones ("no recipient") in either width: S * F entries, rounded up to 8 bytes (the
     // table's allocation is a multiple of 256 bytes)
-    hipError_t e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (S * F + 1) / 2 : S * F, ~0ull, st);
-    if (e != hipSuccess) return e;
+    if (!given) {
+        hipError_t e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (S * F + 1) / 2 : S * F, ~0ull, st);
+        if (e != hipSuccess) return e;
+    }
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
@@ -1640,15 +1643,17 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
             using T = typename ElemT<E>::T;
             return by_width<E>(V, [&](auto vt) -> hipError_t {
                 constexpr int VV = decltype(vt)::value;
-                if (first)
-                    hipLaunchKernelGGL((seg_bwd_max_arg_off_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
-                                       static_cast<const T *>(src), static_cast<const I *>(idx), off, first, out, n, S,
-                                       F, ap);
-                else
-                    hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
-                                       static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, ap);
-                hipError_t e2 = hipGetLastError();
-                if (e2 != hipSuccess) return e2;
+                if (!given) {   // the recipients: the lowest attaining row of each (segment, feature)
+                    if (first)
+                        hipLaunchKernelGGL((seg_bwd_max_arg_off_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
+                                           static_cast<const T *>(src), static_cast<const I *>(idx), off, first, out,
+                                           n, S, F, ap);
+                    else
+                        hipLaunchKernelGGL((seg_bwd_max_arg_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st,
+                                           static_cast<const T *>(src), static_cast<const I *>(idx), out, n, S, F, ap);
+                    hipError_t e2 = hipGetLastError();
+                    if (e2 != hipSuccess) return e2;
+                }
                 if (first)
                     hipLaunchKernelGGL((seg_bwd_max_write_off_kernel<E, I, VV, A>), dim3(g), dim3(256), 0, st, gout,
                                        static_cast<const I *>(idx), off, first, ap, n, S, F, static_cast<T *>(gsrc));
@@ -1664,9 +1669,10 @@ hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, con
 
 hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
                          const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, void *arg, float *gX, float *gw, hipStream_t st) {
+                         int64_t F, int V, int op, void *arg, bool given, float *gX, float *gw, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     if (op == GEOT_BWD_MAX && !arg) return hipErrorInvalidValue;
+    if (given && !seg_bwd_arg32(n)) return hipErrorInvalidValue;   // recorded recipients are 32-bit
     const int64_t gb = grid_rows(n, (int)(F / V));
     if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const unsigned g = (unsigned)gb;
@@ -1684,7 +1690,7 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
         return by_width<E>(V, [&](auto vt) -> hipError_t {
             constexpr int VV = decltype(vt)::value;
             hipError_t e;
-            if (op == GEOT_BWD_MAX) {
+            if (op == GEOT_BWD_MAX && !given) {
                 e = launch_fill_u64(static_cast<unsigned long long *>(arg), a32 ? (R * F + 1) / 2 : R * F, ~0ull, st);
                 if (e != hipSuccess) return e;
                 if (F / VV <= 64) {   // one vector per thread: runs of consecutive edges

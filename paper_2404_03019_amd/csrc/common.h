@@ -29,6 +29,17 @@ __device__ __forceinline__ float red_apply(float a, float b) {
     }
 }
 
+// Max with recipients: (v, i) takes in (b, ib), where i and ib are the lowest rows whose terms
+// equal v and b. The maximum's recipient is the lowest row whose term equals it, so equal
+// values (+0 and -0 compare equal) keep the lower row and a larger one brings its own; a NaN
+// maximum has none. Symmetric and associative, like the maximum itself.
+__device__ __forceinline__ void max_arg(float &v, uint32_t &i, float b, uint32_t ib) {
+    const bool nan = v != v || b != b;
+    const uint32_t r = b > v ? ib : (v > b ? i : min(i, ib));
+    v = __builtin_elementwise_maximum(v, b);
+    i = nan ? kNoRecipient : r;
+}
+
 // fp32 vectors of 2, 3 and 4 elements that need only 4-byte alignment. gfx950 loads and
 // stores them with one dwordx2 / x3 / x4 instruction at any 4-byte aligned address, so a
 // row of odd width (rows at F * 4 bytes) still moves in whole vectors: a lane whose
@@ -255,11 +266,15 @@ __device__ __forceinline__ void gap_done(const GapList &g, int64_t blk, int64_t 
 // clamped to `rows`. The pass's last block empties the list.
 template <int V>
 __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_t ld, int64_t tw, int64_t rows,
-                                                   const GapList &g, int64_t blk, int64_t nblk) {
+                                                   const GapList &g, int64_t blk, int64_t nblk,
+                                                   uint32_t *arg = nullptr) {
     const unsigned cnt = gap_count(g);
-    float z[V];
+    float z[V], none[V];   // arg (max with recipients): empty rows have none
 #pragma unroll
-    for (int k = 0; k < V; ++k) z[k] = 0.0f;
+    for (int k = 0; k < V; ++k) {
+        z[k] = 0.0f;
+        none[k] = __uint_as_float(kNoRecipient);
+    }
     for (int64_t q = blk; q < (int64_t)cnt; q += nblk) {
         const int64_t *r = g.rec + 3 * q;
         const int64_t lo = max(r[0], (int64_t)0), hi = min(r[1], rows);
@@ -274,7 +289,11 @@ __device__ __forceinline__ void gap_fill_rows_body(float *out, int64_t F, int64_
         for (int64_t row = lo + threadIdx.x / tpr; row < hi; row += rows_per_pass) {
             float *o = out + row * ld;
             // a vector that would pass the row's end takes its last V columns (all zero)
-            for (int j = j0; j < nvec; j += tpr) store_vec<V>(o + min(c0 + (int64_t)j * V, F - V), z);
+            for (int j = j0; j < nvec; j += tpr) {
+                const int64_t c = min(c0 + (int64_t)j * V, F - V);
+                store_vec<V>(o + c, z);
+                if (arg) store_vec<V>(reinterpret_cast<float *>(arg + row * ld + c), none);
+            }
         }
     }
     gap_done(g, blk, nblk, cnt);

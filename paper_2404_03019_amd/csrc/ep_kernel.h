@@ -61,6 +61,10 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     static_assert(MODE != SRC_PIECES || (E == ELEM_F32 && std::is_same<I, int64_t>::value),
                   "partials are fp32 with int64 segment ids");
     using T = typename ElemT<E>::T;
+    // max with recipients (RED_MAXARG): beside every value, the lowest row (edge; for a
+    // partial, the row it carries) whose term equals it
+    constexpr bool ARG = RED == RED_MAXARG;
+    constexpr int NX = ARG ? NV : 1;   // recipient registers per lane (one unused otherwise)
     const T *src = static_cast<const T *>(a.src);
     const I *idx = static_cast<const I *>(a.idx);
     const I *col = static_cast<const I *>(a.col);
@@ -70,6 +74,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     __shared__ float s_v[NW][TW];
     __shared__ Cnt s_n[NW];
     __shared__ int s_f[NW];
+    __shared__ uint32_t s_x[NW][ARG ? TW : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -83,7 +88,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         const int64_t main_blocks = nblk - a.gap_blocks;
         if (a.gap_blocks > 0 && bid >= main_blocks) {
             gap_fill_rows_body<V>(a.out, a.F, a.ld_out, (int64_t)TW, a.S, a.gaps, bid - main_blocks,
-                                  a.gap_blocks);
+                                  a.gap_blocks, a.arg_out);
             return;
         }
     }
@@ -121,10 +126,21 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     const float neutral = red_neutral<RED>();
 
     // ---- helpers -------------------------------------------------------
-    auto store_seg = [&](int32_t seg, const float *v, Cnt n) {
+    auto store_seg = [&](int32_t seg, const float *v, Cnt n, const uint32_t *vx) {
         if (MODE == SRC_PIECES && n == 0) return;     // only empty partials: stored elsewhere
         if (seg < 0 || (int64_t)seg >= a.S) return;   // out-of-range id: skip the store
         float *o = a.out + (int64_t)seg * a.ld_out;
+        if constexpr (ARG) {
+            float *ao = reinterpret_cast<float *>(a.arg_out + (int64_t)seg * a.ld_out);
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                if (!cv[j]) continue;
+                float t[V];
+#pragma unroll
+                for (int k = 0; k < V; ++k) t[k] = __uint_as_float(vx[j * V + k]);
+                store_vec_nt<V>(ao + cb[j], t);
+            }
+        }
         if (a.mean) {  // uniform across the grid: a scalar branch, no division on the sum path
             const float fn = (float)n;
 #pragma unroll
@@ -149,17 +165,26 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         s_lo = max(s_lo, (int64_t)0);
         s_hi = min(s_hi, a.S);
         if (s_hi - s_lo > kGapRun && gap_push(a.gaps, s_lo, s_hi, tile, gbase_fill, gl, L)) return;
-        float z[V];
+        float z[V], none[V];
 #pragma unroll
-        for (int k = 0; k < V; ++k) z[k] = 0.0f;
+        for (int k = 0; k < V; ++k) {
+            z[k] = 0.0f;
+            none[k] = __uint_as_float(kNoRecipient);
+        }
         for (int64_t s = s_lo; s < s_hi; ++s) {
             float *o = a.out + s * a.ld_out;
 #pragma unroll
             for (int j = 0; j < NT; ++j)
                 if (cv[j]) store_vec_nt<V>(o + cb[j], z);
+            if constexpr (ARG) {
+                float *ao = reinterpret_cast<float *>(a.arg_out + s * a.ld_out);
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    if (cv[j]) store_vec_nt<V>(ao + cb[j], none);
+            }
         }
     };
-    auto write_partial = [&](int slot, int32_t seg, const float *v, Cnt n) {
+    auto write_partial = [&](int slot, int32_t seg, const float *v, Cnt n, const uint32_t *vx) {
         if (a.pv == nullptr) return;
         const int64_t row = 2 * chunk + slot;
         if (n > 0) {
@@ -167,6 +192,17 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
 #pragma unroll
             for (int j = 0; j < NT; ++j)
                 if (cv[j]) store_vec<V>(p + cb[j], v + j * V);
+            if constexpr (ARG) {
+                float *px = reinterpret_cast<float *>(a.pix + row * a.ld_p);
+#pragma unroll
+                for (int j = 0; j < NT; ++j) {
+                    if (!cv[j]) continue;
+                    float t[V];
+#pragma unroll
+                    for (int k = 0; k < V; ++k) t[k] = __uint_as_float(vx[j * V + k]);
+                    store_vec<V>(px + cb[j], t);
+                }
+            }
         }
         if (tile == 0 && gl == 0) {
             a.pseg[row] = (int64_t)seg;
@@ -201,12 +237,27 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
             else for (int k = 0; k < V; ++k) x[j * V + k] = neutral;
         }
     };
-    // a partial's terms: neutral when it is empty (count 0)
-    auto piece = [&](float *x, Cnt c) {
+    // a partial's terms: neutral when it is empty (count 0), with no recipient
+    auto piece = [&](float *x, Cnt c, uint32_t *xi) {
         if constexpr (MODE == SRC_PIECES) {
             if (c == 0) {
 #pragma unroll
                 for (int k = 0; k < NV; ++k) x[k] = neutral;
+#pragma unroll
+                for (int k = 0; k < NX; ++k) xi[k] = kNoRecipient;
+            }
+        }
+    };
+    // the recipients a partial carries (max with recipients, partial levels): beside its values
+    auto load_six = [&](int64_t r, uint32_t *xi) {
+        if constexpr (ARG && MODE == SRC_PIECES) {
+            const float *p = reinterpret_cast<const float *>(a.six + r * a.ld_src);
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                float t[V];
+                if (cv[j]) load_vec<V>(p + cb[j], t);
+#pragma unroll
+                for (int k = 0; k < V; ++k) xi[j * V + k] = cv[j] ? __float_as_uint(t[k]) : kNoRecipient;
             }
         }
     };
@@ -215,30 +266,50 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     int32_t first_seg = -1, cur = -1;
     Cnt accn = 0, headn = 0;
     float acc[NV], head[NV];
+    uint32_t aix[NX], hix[NX];   // their recipients (max with recipients)
     bool head_done = false;
 #pragma unroll
     for (int k = 0; k < NV; ++k) { acc[k] = neutral; head[k] = neutral; }
+#pragma unroll
+    for (int k = 0; k < NX; ++k) { aix[k] = kNoRecipient; hix[k] = kNoRecipient; }
 
-    auto step = [&](int32_t s, const float *x, Cnt c) {
+    // xi: the terms' recipients (the row or edge itself; for a partial, the ones it carries)
+    auto step = [&](int32_t s, const float *x, Cnt c, const uint32_t *xi) {
         if (s != cur) {
             if (!head_done) {
 #pragma unroll
                 for (int k = 0; k < NV; ++k) head[k] = acc[k];
+#pragma unroll
+                for (int k = 0; k < NX; ++k) hix[k] = aix[k];
                 headn = accn;
                 head_done = true;
             } else {
-                store_seg(cur, acc, accn);  // started and ended inside this run
+                store_seg(cur, acc, accn, aix);  // started and ended inside this run
             }
             if (a.fill_gaps) fill_empty((int64_t)cur + 1, (int64_t)s);
             cur = s;
 #pragma unroll
             for (int k = 0; k < NV; ++k) acc[k] = x[k];
+            if constexpr (ARG) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) aix[k] = xi[k];
+            }
             accn = c;
         } else {
+            if constexpr (ARG) {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) acc[k] = red_apply<RED>(acc[k], x[k]);
+                for (int k = 0; k < NV; ++k) max_arg(acc[k], aix[k], x[k], xi[k]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) acc[k] = red_apply<RED>(acc[k], x[k]);
+            }
             accn += c;
         }
+    };
+    // the recipient of a row's (edge's) own terms: the row itself
+    auto self_ix = [&](int64_t r, uint32_t *xi) {
+#pragma unroll
+        for (int k = 0; k < NX; ++k) xi[k] = (uint32_t)r;
     };
 
     int32_t prev = -1, next = -1;
@@ -310,7 +381,9 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                         widen_term(xr[u], x);
 #pragma unroll
                         for (int k = 0; k < NV; ++k) x[k] = okv[u] ? wt[u] * x[k] : neutral;
-                        step(s[u], x, 1);
+                        uint32_t xi[NX];
+                        self_ix(okv[u] ? r + u : (int64_t)kNoRecipient, xi);
+                        step(s[u], x, 1, xi);
                     }
                 }
             }
@@ -334,7 +407,9 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                     if (r + u < r1) {
                         float x[NV];
                         widen_term(xr[u], x);
-                        step(su, x, 1);
+                        uint32_t xi[NX];
+                        self_ix(r + u, xi);
+                        step(su, x, 1, xi);
                     }
                 }
             }
@@ -344,27 +419,35 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                 int32_t s[U];
                 Cnt c[U];
                 RV xr[U][NT];
+                uint32_t xi[U][NX];
 #pragma unroll
                 for (int u = 0; u < U; ++u) s[u] = (int32_t)idx[r + u];
 #pragma unroll
-                for (int u = 0; u < U; ++u) load_term(r + u, xr[u], c[u]);
+                for (int u = 0; u < U; ++u) {
+                    load_term(r + u, xr[u], c[u]);
+                    if constexpr (MODE == SRC_PIECES) load_six(r + u, xi[u]);
+                    else self_ix(r + u, xi[u]);
+                }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     float x[NV];
                     widen_term(xr[u], x);
-                    piece(x, c[u]);
-                    step(s[u], x, c[u]);
+                    piece(x, c[u], xi[u]);
+                    step(s[u], x, c[u], xi[u]);
                 }
             }
             for (; r < r1; ++r) {
                 RV xr[NT];
                 float x[NV];
+                uint32_t xi[NX];
                 Cnt c;
                 const int32_t s = (int32_t)idx[r];
                 load_term(r, xr, c);
+                if constexpr (MODE == SRC_PIECES) load_six(r, xi);
+                else self_ix(r, xi);
                 widen_term(xr, x);
-                piece(x, c);
-                step(s, x, c);
+                piece(x, c, xi);
+                step(s, x, c, xi);
             }
         }
         // empty segments before this run (written after the row loop, so the first loads of
@@ -376,6 +459,8 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     if (single_run) {
 #pragma unroll
         for (int k = 0; k < NV; ++k) head[k] = acc[k];
+#pragma unroll
+        for (int k = 0; k < NX; ++k) hix[k] = aix[k];
         headn = accn;
     }
     const int32_t last_seg = cur;
@@ -387,15 +472,23 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     // (f1, v1, n1) (+) (f2, v2, n2) = (f1 | f2, f2 ? v2 : v1 (+) v2, f2 ? n2 : n1 + n2).
     bool f = has_rows && (starts || !single_run);
     float v[NV];
+    uint32_t vx[NX];   // recipients of v (max with recipients)
     Cnt n = has_rows ? accn : 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) v[k] = acc[k];
+#pragma unroll
+    for (int k = 0; k < NX; ++k) vx[k] = aix[k];
     // (f, v, n) absorbs the element (fo, vo, no) of an earlier group when `take`
-    auto absorb = [&](bool take, int fo, const float *vo, Cnt no) {
+    auto absorb = [&](bool take, int fo, const float *vo, Cnt no, const uint32_t *vxo) {
         if (take) {
             if (!f) {
+                if constexpr (ARG) {
 #pragma unroll
-                for (int k = 0; k < NV; ++k) v[k] = red_apply<RED>(vo[k], v[k]);
+                    for (int k = 0; k < NV; ++k) max_arg(v[k], vx[k], vo[k], vxo[k]);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < NV; ++k) v[k] = red_apply<RED>(vo[k], v[k]);
+                }
                 n += no;
             }
             f = f || (fo != 0);
@@ -405,11 +498,16 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     auto dpp_row_step = [&](auto shift_tag) {
         constexpr int S = decltype(shift_tag)::value;
         float vo[NV];
+        uint32_t vxo[NX];
 #pragma unroll
         for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowShr + S, 0xf>(v[k]);
+        if constexpr (ARG) {
+#pragma unroll
+            for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)dpp_i<kDppRowShr + S, 0xf>((int)vx[k]);
+        }
         const int fo = dpp_i<kDppRowShr + S, 0xf>((int)f);
         const Cnt no = dpp_cnt<kDppRowShr + S, 0xf>(n);
-        absorb((lane & 15) >= S, fo, vo, no);
+        absorb((lane & 15) >= S, fo, vo, no, vxo);
     };
     if constexpr (L < 16) {
         // 1. segmented scan of the groups of each 16-lane row with DPP row shifts
@@ -422,30 +520,45 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         if constexpr (L == 1) {
             {   // lane 15 -> row 1, lane 47 -> row 3
                 float vo[NV];
+                uint32_t vxo[NX];
 #pragma unroll
                 for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowBcast15, 0xa>(v[k]);
+                if constexpr (ARG) {
+#pragma unroll
+                    for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)dpp_i<kDppRowBcast15, 0xa>((int)vx[k]);
+                }
                 const int fo = dpp_i<kDppRowBcast15, 0xa>((int)f);
                 const Cnt no = dpp_cnt<kDppRowBcast15, 0xa>(n);
-                absorb((row & 1) != 0, fo, vo, no);
+                absorb((row & 1) != 0, fo, vo, no, vxo);
             }
             {   // lane 31 -> rows 2 and 3
                 float vo[NV];
+                uint32_t vxo[NX];
 #pragma unroll
                 for (int k = 0; k < NV; ++k) vo[k] = dpp_f<kDppRowBcast31, 0xc>(v[k]);
+                if constexpr (ARG) {
+#pragma unroll
+                    for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)dpp_i<kDppRowBcast31, 0xc>((int)vx[k]);
+                }
                 const int fo = dpp_i<kDppRowBcast31, 0xc>((int)f);
                 const Cnt no = dpp_cnt<kDppRowBcast31, 0xc>(n);
-                absorb(row >= 2, fo, vo, no);
+                absorb(row >= 2, fo, vo, no, vxo);
             }
         } else {
 #pragma unroll
             for (int dr = 1; dr <= 2; dr <<= 1) {   // previous row, then two rows back
                 const int src = max(row - dr, 0) * 16 + 16 - L + gl;
                 float vo[NV];
+                uint32_t vxo[NX];
 #pragma unroll
                 for (int k = 0; k < NV; ++k) vo[k] = shfl_f(v[k], src);
+                if constexpr (ARG) {
+#pragma unroll
+                    for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)shfl_i((int)vx[k], src);
+                }
                 const int fo = shfl_i((int)f, src);
                 const Cnt no = shfl_cnt(n, src);
-                absorb(row >= dr, fo, vo, no);
+                absorb(row >= dr, fo, vo, no, vxo);
             }
         }
     } else {
@@ -455,9 +568,14 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
             const int fo = shfl_up_i((int)f, d * L);
             const Cnt no = shfl_up_cnt(n, d * L);
             float vo[NV];
+            uint32_t vxo[NX];
 #pragma unroll
             for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], d * L);
-            absorb(gw >= d, fo, vo, no);
+            if constexpr (ARG) {
+#pragma unroll
+                for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)shfl_up_i((int)vx[k], d * L);
+            }
+            absorb(gw >= d, fo, vo, no, vxo);
         }
     }
     if (gw == GW - 1) {
@@ -465,6 +583,12 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         for (int j = 0; j < NT; ++j)
 #pragma unroll
             for (int k = 0; k < V; ++k) s_v[wave][(j * L + gl) * V + k] = v[j * V + k];
+        if constexpr (ARG) {
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+#pragma unroll
+                for (int k = 0; k < V; ++k) s_x[wave][(j * L + gl) * V + k] = vx[j * V + k];
+        }
         if (gl == 0) {
             s_n[wave] = n;
             s_f[wave] = (int)f;
@@ -475,9 +599,12 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     // exclusive prefix of this group: waves before this one, then groups before it in the wave
     bool ef = false;
     float ev[NV];
+    uint32_t ex[NX];
     Cnt en = 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) ev[k] = neutral;
+#pragma unroll
+    for (int k = 0; k < NX; ++k) ex[k] = kNoRecipient;
     for (int w2 = 0; w2 < wave; ++w2) {
         const bool f2 = s_f[w2] != 0;
         const Cnt n2 = s_n[w2];
@@ -486,7 +613,17 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
 #pragma unroll
             for (int k = 0; k < V; ++k) {
                 const float x2 = s_v[w2][(j * L + gl) * V + k];
-                ev[j * V + k] = f2 ? x2 : red_apply<RED>(ev[j * V + k], x2);
+                if constexpr (ARG) {
+                    const uint32_t i2 = s_x[w2][(j * L + gl) * V + k];
+                    if (f2) {
+                        ev[j * V + k] = x2;
+                        ex[j * V + k] = i2;
+                    } else {
+                        max_arg(ev[j * V + k], ex[j * V + k], x2, i2);
+                    }
+                } else {
+                    ev[j * V + k] = f2 ? x2 : red_apply<RED>(ev[j * V + k], x2);
+                }
             }
         en = f2 ? n2 : en + n2;
         ef = ef || f2;
@@ -495,11 +632,28 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         const int fo = shfl_up_i((int)f, L);
         const Cnt no = shfl_up_cnt(n, L);
         float vo[NV];
+        uint32_t vxo[NX];
 #pragma unroll
         for (int k = 0; k < NV; ++k) vo[k] = shfl_up_f(v[k], L);
-        if (gw > 0) {
+        if constexpr (ARG) {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) ev[k] = fo ? vo[k] : red_apply<RED>(ev[k], vo[k]);
+            for (int k = 0; k < NX; ++k) vxo[k] = (uint32_t)shfl_up_i((int)vx[k], L);
+        }
+        if (gw > 0) {
+            if constexpr (ARG) {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) {
+                    if (fo) {
+                        ev[k] = vo[k];
+                        ex[k] = vxo[k];
+                    } else {
+                        max_arg(ev[k], ex[k], vo[k], vxo[k]);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) ev[k] = fo ? vo[k] : red_apply<RED>(ev[k], vo[k]);
+            }
             en = fo ? no : en + no;
             ef = ef || (fo != 0);
         }
@@ -511,35 +665,47 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         bool hi_written = false;
         // value of the run's first segment including what precedes it in the block
         float hv[NV];
+        uint32_t hx[NX];
         Cnt hn;
         bool h_in_block;
         if (starts) {
 #pragma unroll
             for (int k = 0; k < NV; ++k) hv[k] = head[k];
+#pragma unroll
+            for (int k = 0; k < NX; ++k) hx[k] = hix[k];
             hn = headn;
             h_in_block = true;
         } else {
+            if constexpr (ARG) {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) hv[k] = red_apply<RED>(ev[k], head[k]);
+                for (int k = 0; k < NV; ++k) {
+                    hv[k] = ev[k];
+                    hx[k] = ex[k];
+                    max_arg(hv[k], hx[k], head[k], hix[k]);
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < NV; ++k) hv[k] = red_apply<RED>(ev[k], head[k]);
+            }
             hn = en + headn;
             h_in_block = ef;
         }
         if (!single_run) {
             // the first segment ends inside the run
-            if (h_in_block) store_seg(first_seg, hv, hn);
-            else write_partial(0, first_seg, hv, hn);
+            if (h_in_block) store_seg(first_seg, hv, hn, hx);
+            else write_partial(0, first_seg, hv, hn, hx);
             // the last segment began inside the run
             if (ends_tail) {
-                store_seg(last_seg, acc, accn);
+                store_seg(last_seg, acc, accn, aix);
             } else if (last_group) {
-                write_partial(1, last_seg, acc, accn);
+                write_partial(1, last_seg, acc, accn, aix);
                 hi_written = true;
             }
         } else if (ends_tail) {
-            if (h_in_block) store_seg(first_seg, hv, hn);
-            else write_partial(0, first_seg, hv, hn);
+            if (h_in_block) store_seg(first_seg, hv, hn, hx);
+            else write_partial(0, first_seg, hv, hn, hx);
         } else if (last_group) {
-            write_partial(h_in_block ? 1 : 0, first_seg, hv, hn);
+            write_partial(h_in_block ? 1 : 0, first_seg, hv, hn, hx);
             hi_written = h_in_block;
         }
         // empty partials keep the list of partials sorted and complete
@@ -636,6 +802,11 @@ hipError_t ep_dispatch(const EpArgs &a, int red, int mode, int V, int NT, int L,
         if (mode == SRC_GATHER) return by_shape<RED_MAX, SRC_GATHER, E, I>(a, V, NT, L, nchunks, st);
         if constexpr (PIECES)
             if (mode == SRC_PIECES) return by_shape<RED_MAX, SRC_PIECES, E, I>(a, V, NT, L, nchunks, st);
+    } else if (red == RED_MAXARG) {
+        if (mode == SRC_ROWS) return by_shape<RED_MAXARG, SRC_ROWS, E, I>(a, V, NT, L, nchunks, st);
+        if (mode == SRC_GATHER) return by_shape<RED_MAXARG, SRC_GATHER, E, I>(a, V, NT, L, nchunks, st);
+        if constexpr (PIECES)
+            if (mode == SRC_PIECES) return by_shape<RED_MAXARG, SRC_PIECES, E, I>(a, V, NT, L, nchunks, st);
     }
     return hipErrorInvalidValue;
 }

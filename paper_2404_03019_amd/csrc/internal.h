@@ -16,7 +16,11 @@ enum SrcMode : int {
     SRC_PIECES = 2,  // term = partial[row, :] carrying a row count (cnt[row] == 0: no term)
 };
 
-enum RedOp : int { RED_SUM = 0, RED_MAX = 1 };  // mean = sum, divided by the count on store
+// mean = sum, divided by the count on store; RED_MAXARG = max that also records, for every
+// output element, its recipient: the lowest row (edge) whose term equals the maximum
+enum RedOp : int { RED_SUM = 0, RED_MAX = 1, RED_MAXARG = 2 };
+// a recorded recipient where there is none (an empty segment, a NaN maximum)
+constexpr uint32_t kNoRecipient = 0xffffffffu;
 
 // Storage type of src / X at level 0 (partials are always fp32 with int64 ids).
 // Elements are widened to fp32 on load, which is exact for all three types.
@@ -74,6 +78,12 @@ struct EpArgs {
                             // (written by level 0, which has finished), in tiles of the level's width
     int32_t tile_major;     // block b takes column tile b / chunks and chunk b % chunks (else the
                             // ntiles tiles of a chunk are adjacent blocks)
+    // RED_MAXARG only: recipients [S x ld_out] written beside out (kNoRecipient where none),
+    // the recipients of this pass's partials [2 * chunks x ld_p], and (SRC_PIECES) those of
+    // the partials it reads [n x ld_src]
+    uint32_t *arg_out;
+    uint32_t *pix;
+    const uint32_t *six;
 };
 
 // Dispatches on (elem, idx32) to the translation unit holding those instantiations.
@@ -123,7 +133,7 @@ hipError_t launch_offsets_i32(const int32_t *idx, int64_t n, int64_t S, int64_t 
 // the list empty.
 // Records are clamped to the `rows` (or `len`) of the current call.
 hipError_t launch_gap_fill_rows(float *out, int64_t F, int64_t ld, int V, int64_t tw, int64_t rows,
-                                GapList gaps, hipStream_t stream);
+                                 GapList gaps, uint32_t *arg, hipStream_t stream);
 hipError_t launch_gap_fill_i64(int64_t *arr, int64_t len, GapList gaps, hipStream_t stream);
 
 // out[0 .. rows*ld) = value for the first F columns of each row.
@@ -186,17 +196,19 @@ int64_t seg_bwd_blocks(int64_t n, int64_t F, int V);
 // and grad_src of ElemType `elem`. off and first (optional) as for launch_seg_bwd_bcast: the
 // stores then take their segments from the offsets.
 bool seg_bwd_arg32(int64_t n);
+// `given`: arg already holds the (32-bit) recipients, recorded by the forward; no recipient pass.
 hipError_t launch_seg_bwd_max(const float *gout, const void *idx, int idx32, const void *src, const float *out,
                               const int64_t *off, const int64_t *first, int64_t n, int64_t S, int64_t F, int V,
-                              int elem, void *arg, void *gsrc, hipStream_t st);
+                              int elem, void *arg, bool given, void *gsrc, hipStream_t st);
 
 // fused form: grad_w, and for max grad_X (zero-filled here, then one atomic add per recipient;
 // sum and mean take grad_X from the transposed gather, and passing grad_X for them is an error);
 // off = row starts (mean), arg [R x F] scratch of edge numbers for max (32-bit where
 // seg_bwd_arg32(n), else 64-bit; a multiple of 8 bytes). X of ElemType elem, col and row int32
 // when idx32.
+// `given`: arg already holds the (32-bit) recipients, recorded by the forward; no recipient pass.
 hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, int idx32, const float *w,
                          const void *row, const int64_t *off, const float *out, const float *gout, int64_t n, int64_t R,
-                         int64_t F, int V, int op, void *arg, float *gX, float *gw, hipStream_t st);
+                         int64_t F, int V, int op, void *arg, bool given, float *gX, float *gw, hipStream_t st);
 
 }  // namespace geot

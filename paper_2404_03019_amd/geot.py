@@ -77,6 +77,13 @@ def lib() -> ctypes.CDLL:
     L.geot_gather_scatter_backward_typed.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64, i64,
                                                      ctypes.c_int, p, p, p, p, p]
     L.geot_transpose_edges.argtypes = [p, i64, p, p, i64, i64, ctypes.c_int, p, p, p, p]
+    L.geot_segment_reduce_max_arg.argtypes = [p, ctypes.c_int, p, ctypes.c_int, i64, i64, i64, p, p, p, pc]
+    L.geot_gather_scatter_max_arg.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64, i64,
+                                              p, p, p, pc]
+    L.geot_segment_reduce_backward_max_arg.argtypes = [p, p, ctypes.c_int, i64, i64, i64, p, p,
+                                                       ctypes.c_int, p]
+    L.geot_gather_scatter_backward_max_arg.argtypes = [p, ctypes.c_int, i64, p, p, p, ctypes.c_int, i64, i64,
+                                                       i64, p, p, p, p, p]
     sz = ctypes.c_size_t
     L.geot_segment_reduce_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, pc, ctypes.POINTER(sz)]
     L.geot_gather_scatter_workspace_size.argtypes = [i64, i64, i64, ctypes.c_int, i32, pc, ctypes.POINTER(sz)]
@@ -267,6 +274,113 @@ def gather_scatter(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | No
                                                  R, F, OPS[reduce], out.data_ptr(), _stream(x.device), cp)
     _raise(st)
     return out
+
+
+def segment_reduce_max_arg(src: torch.Tensor, index: torch.Tensor, num_segments: int, choice=None):
+    """(out, arg): the max of segment_reduce and its recipients (geot_segment_reduce_max_arg).
+
+    arg [num_segments, F] int32 holds the uint32 row numbers the library writes: the lowest
+    row of each segment whose value equals the maximum, -1 (0xFFFFFFFF) where there is none.
+    Requires fewer than 2^32 - 1 rows."""
+    _dev(src, "src", tuple(DTYPES), 2)
+    _dev(index, "index", tuple(INDEX_TYPES), 1)
+    if index.numel() != src.shape[0]:
+        raise ValueError("index must have one entry per row of src")
+    _on_gpu(src=src, index=index)
+    S, F = int(num_segments), src.shape[1]
+    out = torch.empty((S, F), dtype=torch.float32, device=src.device)
+    arg = torch.empty((S, F), dtype=torch.int32, device=src.device)
+    c = _choice(choice)
+    with _OnDevice(src.device):
+        st = lib().geot_segment_reduce_max_arg(src.data_ptr(), DTYPES[src.dtype], index.data_ptr(),
+                                               INDEX_TYPES[index.dtype], index.numel(), S, F, out.data_ptr(),
+                                               arg.data_ptr(), _stream(src.device),
+                                               ctypes.byref(c) if c is not None else None)
+    _raise(st)
+    return out, arg
+
+
+def gather_scatter_max_arg(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
+                           row: torch.Tensor, num_rows: int, choice=None):
+    """(out, arg): the max of gather_scatter and its recipients (geot_gather_scatter_max_arg):
+    arg [num_rows, F] int32 holds the uint32 edge numbers, -1 where there is none."""
+    _dev(x, "x", tuple(DTYPES), 2)
+    _dev(col, "col", tuple(INDEX_TYPES), 1)
+    _dev(row, "row", (col.dtype,), 1)
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+        if weight.numel() != row.numel():
+            raise ValueError("weight must have one entry per edge")
+    if col.numel() != row.numel():
+        raise ValueError("col and row must have one entry per edge")
+    _on_gpu(x=x, col=col, weight=weight, row=row)
+    R, F = int(num_rows), x.shape[1]
+    out = torch.empty((R, F), dtype=torch.float32, device=x.device)
+    arg = torch.empty((R, F), dtype=torch.int32, device=x.device)
+    c = _choice(choice)
+    with _OnDevice(x.device):
+        st = lib().geot_gather_scatter_max_arg(x.data_ptr(), DTYPES[x.dtype], x.shape[0], col.data_ptr(),
+                                               weight.data_ptr() if weight is not None else None, row.data_ptr(),
+                                               INDEX_TYPES[col.dtype], row.numel(), R, F, out.data_ptr(),
+                                               arg.data_ptr(), _stream(x.device),
+                                               ctypes.byref(c) if c is not None else None)
+    _raise(st)
+    return out, arg
+
+
+def segment_reduce_backward_max_arg(grad_out: torch.Tensor, index: torch.Tensor, arg: torch.Tensor,
+                                    dtype: torch.dtype = torch.float32) -> torch.Tensor:
+    """Gradient of the max of segment_reduce w.r.t. src from recorded recipients (arg of
+    segment_reduce_max_arg; geot_segment_reduce_backward_max_arg), in storage type `dtype`."""
+    _dev(grad_out, "grad_out", torch.float32, 2)
+    _dev(index, "index", tuple(INDEX_TYPES), 1)
+    _dev(arg, "arg", torch.int32, 2)
+    if dtype not in DTYPES:
+        raise TypeError(f"the gradient's type must be one of {tuple(DTYPES)}")
+    S, F = grad_out.shape
+    _shape(arg, "arg", (S, F))
+    _on_gpu(grad_out=grad_out, index=index, arg=arg)
+    grad_src = torch.empty((index.numel(), F), dtype=dtype, device=grad_out.device)
+    with _OnDevice(grad_out.device):
+        st = lib().geot_segment_reduce_backward_max_arg(grad_out.data_ptr(), index.data_ptr(),
+                                                        INDEX_TYPES[index.dtype], index.numel(), S, F,
+                                                        arg.data_ptr(), grad_src.data_ptr(), DTYPES[dtype],
+                                                        _stream(grad_out.device))
+    _raise(st)
+    return grad_src
+
+
+def gather_scatter_backward_max_arg(x: torch.Tensor, col: torch.Tensor, weight: torch.Tensor | None,
+                                    row: torch.Tensor, grad_out: torch.Tensor, arg: torch.Tensor,
+                                    need_x: bool = True, need_weight: bool = True):
+    """(grad_x or None, grad_weight or None) of the max of gather_scatter from recorded
+    recipients (arg of gather_scatter_max_arg; geot_gather_scatter_backward_max_arg)."""
+    _dev(x, "x", tuple(DTYPES), 2)
+    _dev(col, "col", tuple(INDEX_TYPES), 1)
+    _dev(row, "row", (col.dtype,), 1)
+    _dev(grad_out, "grad_out", torch.float32, 2)
+    _dev(arg, "arg", torch.int32, 2)
+    R, F = grad_out.shape
+    n = row.numel()
+    if col.numel() != n:
+        raise ValueError("col and row must have one entry per edge")
+    if x.shape[1] != F:
+        raise ValueError(f"x has {x.shape[1]} columns, grad_out {F}")
+    _shape(arg, "arg", (R, F))
+    if weight is not None:
+        _dev(weight, "weight", torch.float32, 1)
+        _shape(weight, "weight", (n,))
+    _on_gpu(x=x, col=col, weight=weight, row=row, grad_out=grad_out, arg=arg)
+    gx = torch.empty(x.shape, dtype=torch.float32, device=x.device) if need_x else None
+    gw = torch.empty_like(weight) if (need_weight and weight is not None) else None
+    with _OnDevice(x.device):
+        st = lib().geot_gather_scatter_backward_max_arg(
+            x.data_ptr(), DTYPES[x.dtype], x.shape[0], col.data_ptr(),
+            weight.data_ptr() if weight is not None else None, row.data_ptr(), INDEX_TYPES[col.dtype], n, R, F,
+            grad_out.data_ptr(), arg.data_ptr(), gx.data_ptr() if gx is not None else None,
+            gw.data_ptr() if gw is not None else None, _stream(x.device))
+    _raise(st)
+    return gx, gw
 
 
 def workspace_size(nnz: int, num_segments: int, F: int, reduce: str = "sum", gather: bool = False,

@@ -241,3 +241,32 @@ def test_workspace_calls_check_on_the_host():
                                     None) == INVALID and "needs" in _detail()
     # nothing to do: no workspace needed
     assert L.geot_segment_reduce_ws(src, idx, 1000, 0, 4, 0, out, None, 0, None, None) == SUCCESS
+
+
+def test_recipient_calls_check_on_the_host():
+    """The max-with-recipients calls: a missing or overlapping arg, 2^32 - 1 rows or more,
+    a segment-parallel choice, and an op other than max for the recorded gradient, all
+    rejected before any device work."""
+    L = lib()
+    src, idx, out, arg = FAKE, FAKE + (1 << 28), FAKE + (1 << 30), FAKE + (1 << 31)
+    F32, I64 = 0, 0
+    fwd = lambda a, n=1000, c=None: L.geot_segment_reduce_max_arg(src, F32, idx, I64, n, 10, 4, out, a, None,
+                                                                  ctypes.byref(c) if c is not None else None)
+    assert fwd(None) == INVALID and "arg" in _detail()
+    assert fwd(out + 16) == INVALID and "overlap" in _detail()
+    assert fwd(src + 64) == INVALID and "overlap" in _detail()
+    far = lambda k: FAKE + (k << 40)   # room for 2^32 rows of every array
+    assert L.geot_segment_reduce_max_arg(far(0), F32, far(1), I64, (1 << 32) - 1, 10, 4, far(2), far(3), None,
+                                         None) == UNSUPPORTED and "2^32" in _detail()
+    assert fwd(arg, c=KernelChoice(2, 0, 0, 0, 0, 0)) == UNSUPPORTED and "element-parallel" in _detail()
+    X, col, row = FAKE, FAKE + (1 << 26), FAKE + (1 << 27)
+    assert L.geot_gather_scatter_max_arg(X, F32, 100, col, None, row, I64, 1000, 10, 4, out, None, None,
+                                         None) == INVALID
+    g, gs = FAKE + (1 << 32), FAKE + (1 << 33)
+    assert L.geot_segment_reduce_backward_max_arg(g, idx, I64, 1000, 10, 4, None, gs, F32, None) == INVALID
+    assert L.geot_segment_reduce_backward_max_arg(g, idx, I64, (1 << 32) - 1, 10, 4, arg, gs, F32,
+                                                  None) == UNSUPPORTED
+    assert L.geot_gather_scatter_backward_max_arg(X, F32, 100, col, None, row, I64, 1000, 10, 4, g, None, gs,
+                                                  None, None) == INVALID
+    # no rows: nothing to do, no device work
+    assert L.geot_segment_reduce_backward_max_arg(g, idx, I64, 0, 10, 4, arg, gs, F32, None) == SUCCESS
