@@ -294,7 +294,12 @@ def profile_configs(reps: int):
         nb = n3 * 8 + n3 * 128 + S3 * 128 + (n3 * 128 + S3 * 128 if op == "max" else 0)
         entry(f"c3_powerlaw_graph gradient {op}", nb,
               lambda: geot.segment_reduce_backward(g3, i, op, s, o, grad_src=gs))
-    del s, i, g3, gs, o
+    entry("c3_powerlaw_graph max with recipients", seg_bytes(n3, S3, 32) + S3 * 128,
+          lambda: geot.segment_reduce_max_arg(s, i, S3))
+    _, a3 = geot.segment_reduce_max_arg(s, i, S3)
+    entry("c3_powerlaw_graph gradient max from recorded recipients", n3 * 8 + n3 * 128 + 2 * S3 * 128,
+          lambda: geot.segment_reduce_backward_max_arg(g3, i, a3))
+    del s, i, g3, gs, o, a3
     torch.cuda.empty_cache()
     c4 = make_config("c4_spmm")
     R4 = c4["num_segments"]
@@ -315,6 +320,11 @@ def profile_configs(reps: int):
     o4 = geot.gather_scatter(X, col, w, row, R4, "max")
     entry("c4_spmm gradient max", 3 * (n4 * 20 + n4 * 512 + R4 * 512),
           lambda: geot.gather_scatter_backward(X, col, w, row, g4, "max", out=o4))
+    entry("c4_spmm max with recipients", gather_bytes(n4, R4, 128) + R4 * 512,
+          lambda: geot.gather_scatter_max_arg(X, col, w, row, R4))
+    _, a4 = geot.gather_scatter_max_arg(X, col, w, row, R4)
+    entry("c4_spmm gradient max from recorded recipients", 2 * (n4 * 20 + n4 * 512 + R4 * 512),
+          lambda: geot.gather_scatter_backward_max_arg(X, col, w, row, g4, a4))
 
 
 def suite(reps: int):
