@@ -29,15 +29,19 @@ __device__ __forceinline__ float red_apply(float a, float b) {
     }
 }
 
-// Max with recipients: (v, i) takes in (b, ib), where i and ib are the lowest rows whose terms
-// equal v and b. The maximum's recipient is the lowest row whose term equals it, so equal
-// values (+0 and -0 compare equal) keep the lower row and a larger one brings its own; a NaN
-// maximum has none. Symmetric and associative, like the maximum itself.
+// Max with recipients: (v, i), the maximum of some terms and the lowest row among them whose
+// term equals it, takes in (b, ib) from LATER rows (every combine does: the walk goes up the
+// rows, the scan and the levels take earlier groups and partials into later ones). The later
+// side's row counts only where its value is larger: equal values (+0 and -0 compare equal)
+// keep the earlier, lower row. A side with no recipient (an empty partial: the neutral value)
+// yields to the other, which is checked only where one can occur (NONE_OK). NaN maxima are
+// not tracked here: NaN propagates in the value, and the store writes no recipient for it.
+// The result is the recipient rule of the max gradients, whatever the schedule.
+template <bool NONE_OK>
 __device__ __forceinline__ void max_arg(float &v, uint32_t &i, float b, uint32_t ib) {
-    const bool nan = v != v || b != b;
-    const uint32_t r = b > v ? ib : (v > b ? i : min(i, ib));
+    const bool later = b > v || (NONE_OK && i == kNoRecipient);
+    i = later ? ib : i;
     v = __builtin_elementwise_maximum(v, b);
-    i = nan ? kNoRecipient : r;
 }
 
 // fp32 vectors of 2, 3 and 4 elements that need only 4-byte alignment. gfx950 loads and

@@ -21,9 +21,11 @@
 //
 // src / X may be stored as fp32, bf16 or fp16 and the index (and col) as int64
 // or int32: the first pass widens on load and reduces in fp32; later passes
-// read the fp32 partials. Each (storage, index) pair is instantiated in a
-// translation unit of its own (ep_<storage>_<index>.hip), which this header
-// is included into.
+// read the fp32 partials. Max may also record, beside every value, its
+// recipient: the lowest row (edge) whose term equals it (RED_MAXARG; pairs
+// combine by max_arg in common.h through the walk, the scan and the levels).
+// Each (storage, index) pair is instantiated in a translation unit of its own
+// (ep_<storage>_<index>.hip), which this header is included into.
 #pragma once
 
 #include <type_traits>
@@ -137,7 +139,10 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                 if (!cv[j]) continue;
                 float t[V];
 #pragma unroll
-                for (int k = 0; k < V; ++k) t[k] = __uint_as_float(vx[j * V + k]);
+                for (int k = 0; k < V; ++k) {   // a NaN maximum has none
+                    const float m = v[j * V + k];
+                    t[k] = __uint_as_float(m != m ? kNoRecipient : vx[j * V + k]);
+                }
                 store_vec_nt<V>(ao + cb[j], t);
             }
         }
@@ -298,7 +303,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
         } else {
             if constexpr (ARG) {
 #pragma unroll
-                for (int k = 0; k < NV; ++k) max_arg(acc[k], aix[k], x[k], xi[k]);
+                for (int k = 0; k < NV; ++k) max_arg<MODE != SRC_ROWS>(acc[k], aix[k], x[k], xi[k]);
             } else {
 #pragma unroll
                 for (int k = 0; k < NV; ++k) acc[k] = red_apply<RED>(acc[k], x[k]);
@@ -484,7 +489,13 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
             if (!f) {
                 if constexpr (ARG) {
 #pragma unroll
-                    for (int k = 0; k < NV; ++k) max_arg(v[k], vx[k], vo[k], vxo[k]);
+                    for (int k = 0; k < NV; ++k) {
+                        float t = vo[k];
+                        uint32_t ti = vxo[k];
+                        max_arg<true>(t, ti, v[k], vx[k]);
+                        v[k] = t;
+                        vx[k] = ti;
+                    }
                 } else {
 #pragma unroll
                     for (int k = 0; k < NV; ++k) v[k] = red_apply<RED>(vo[k], v[k]);
@@ -619,7 +630,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                         ev[j * V + k] = x2;
                         ex[j * V + k] = i2;
                     } else {
-                        max_arg(ev[j * V + k], ex[j * V + k], x2, i2);
+                        max_arg<true>(ev[j * V + k], ex[j * V + k], x2, i2);
                     }
                 } else {
                     ev[j * V + k] = f2 ? x2 : red_apply<RED>(ev[j * V + k], x2);
@@ -647,7 +658,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                         ev[k] = vo[k];
                         ex[k] = vxo[k];
                     } else {
-                        max_arg(ev[k], ex[k], vo[k], vxo[k]);
+                        max_arg<true>(ev[k], ex[k], vo[k], vxo[k]);
                     }
                 }
             } else {
@@ -681,7 +692,7 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
                 for (int k = 0; k < NV; ++k) {
                     hv[k] = ev[k];
                     hx[k] = ex[k];
-                    max_arg(hv[k], hx[k], head[k], hix[k]);
+                    max_arg<true>(hv[k], hx[k], head[k], hix[k]);
                 }
             } else {
 #pragma unroll
