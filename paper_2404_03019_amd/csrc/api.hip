@@ -367,11 +367,12 @@ geot_status_t resolve(const Problem &p, const geot_kernel_choice_t &c, Resolved 
     }
     if (from_selector && p.arg && rows != 0) {
         // Carrying the recipients doubles what the block scan moves and holds registers (the
-        // SpMM gather: 94 -> 117 VGPRs, 4 waves per SIMD); longer row runs amortise the scan
-        // over more rows. Four times the tree's run, measured: the power-law graph 3.41 ->
-        // 2.63 ms (plain max 2.36), the SpMM gather 6.60 -> 5.95 ms (plain 5.21), in bf16 /
-        // int32 5.06 -> 4.73 ms.
-        rows = std::min(4096, rows * 4);
+        // SpMM gather: 94 -> 114 VGPRs, 4 waves per SIMD); longer row runs amortise the scan
+        // over more rows. Twice the tree's run, measured against 1x, 2x, 4x and 8x: the
+        // power-law graph 2.70 -> 2.54 ms (plain max 2.36), the SpMM gather 5.86 -> 5.59 ms
+        // (plain 5.19), in bf16 / int32 4.06 -> 3.91 ms; 4x was within 2 % on the gathers and
+        // 9 % slower on the power-law graph.
+        rows = std::min(4096, rows * 2);
     }
     if (!(V == 1 || V == 2 || V == 3 || V == 4 || V == 8))
         return fail(GEOT_ERROR_UNSUPPORTED, "vec must be 1, 2, 4 or (16-bit storage) 8");
