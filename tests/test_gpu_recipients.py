@@ -184,6 +184,26 @@ def test_recipients_with_16bit_storage_and_int32_ids(gather):
         out, arg = geot.segment_reduce_max_arg(sb.to(DEV), up(p["index"].astype(np.int32)), 2500)
     compare(out.cpu().numpy(), ref, "max", None, "bf16 out")
     check_arg(arg, want, "bf16 / int32")
+    # the gradients from these recipients, in the same storage and id types, equal the
+    # library's own typed max gradients (which find the recipients again)
+    R = out.shape[0]
+    g = torch.from_numpy(np.random.default_rng(33).standard_normal((R, out.shape[1])).astype(np.float32)).to(DEV)
+    if gather:
+        x, c, r, wt = Xb.to(DEV), up(q["col"].astype(np.int32)), up(q["index"].astype(np.int32)), up(q["weight"])
+        gx, gw = geot.gather_scatter_backward_max_arg(x, c, wt, r, g, arg)
+        mx, mw = geot.gather_scatter_backward(x, c, wt, r, g, "max", out)
+        assert torch.equal(gw.view(torch.int32), mw.view(torch.int32)), "bf16 grad_w from recipients"
+        assert torch.allclose(gx, mx, rtol=1e-5, atol=1e-5), "bf16 grad_X from recipients"
+    else:
+        i32 = up(p["index"].astype(np.int32))
+        gs = geot.segment_reduce_backward_max_arg(g, i32, arg, torch.bfloat16)
+        mine = geot.segment_reduce_backward(g, i32, "max", sb.to(DEV), out)
+        assert gs.dtype == torch.bfloat16
+        assert torch.equal(gs.view(torch.int16), mine.view(torch.int16)), "bf16 grad_src from recipients"
+        # and the oracle's gradient on the widened rows, rounded once to bf16
+        ref_g = oracle.segment_reduce_backward(g.cpu().numpy(), p["index"], "max", sw, ref)
+        want_g = torch.from_numpy(ref_g.astype(np.float32)).to(torch.bfloat16)
+        assert torch.equal(gs.cpu().view(torch.int16), want_g.view(torch.int16)), "bf16 grad_src vs oracle"
 
 
 def test_spmm_max_with_recipients_sampled():
