@@ -52,6 +52,16 @@ def test_more_than_2_31_rows():
         ix = idx if itype == torch.int64 else idx.to(torch.int32)
         outs = {op: geot.segment_reduce(src, ix, S, op).cpu().numpy() for op in ("sum", "mean", "max")}
         say(f"limits: 2^31+ rows reduced ({itype})")
+        # the max recording its recipients: row numbers above 2^31 in 32 bits, ternary values so
+        # every maximum ties and the lowest attaining row must win
+        out_r, arg_r = geot.segment_reduce_max_arg(src, ix, S)
+        assert np.array_equal(out_r.cpu().numpy().view(np.uint32), outs["max"].view(np.uint32))
+        argh = arg_r.cpu().numpy().view(np.uint32)
+        for s in sample(L, 12, 9):
+            a, b = int(starts[s]), int(starts[s + 1])
+            rows = src[a:b].cpu().numpy()
+            m = oracle.segment_reduce(rows, np.zeros(b - a, dtype=np.int64), 1, "max")
+            assert argh[s, 0] == a + int(np.flatnonzero(rows[:, 0] == m[0, 0])[0]), (itype, s)
         for s in sample(L, 12, 8):
             a, b = int(starts[s]), int(starts[s + 1])
             rows = src[a:b].cpu().numpy()
@@ -80,6 +90,9 @@ def test_more_than_2_31_rows():
             out = torch.from_numpy(out_max).to(DEV) if op == "max" else None
             gs = geot.segment_reduce_backward(g, ix, op, src if op == "max" else None, out)
             say(f"limits: 2^31+ rows, gradient {op} ({itype})")
+            if op == "max":   # from the recorded recipients: the same gradient
+                assert torch.equal(geot.segment_reduce_backward_max_arg(g, ix, arg_r).view(torch.int32),
+                                   gs.view(torch.int32)), itype
             for s in gsamp:
                 a, b = int(starts[s]), int(starts[s + 1])
                 rows = src[a:b].cpu().numpy()
