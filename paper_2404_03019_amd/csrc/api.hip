@@ -1203,11 +1203,12 @@ static geot_status_t gs_backward(const void *X, geot_dtype_t x_type, int64_t num
     const size_t o_cnt = transpose ? take((size_t)((nx + 1) & ~(int64_t)1) * 4) : 0;
     const size_t o_off = transpose ? take((size_t)(nx + 1) * 8) : 0;
     const size_t o_sums = transpose ? take((size_t)((nx + 4095) / 4096 + 1) * 8) : 0;
-    // the transposed list: 16-byte records {col, row, coefficient, edge} with int32 ids, or
-    // (X with 2^31 rows or more) three arrays
+    // the transposed list: records {col, row, coefficient, edge} with int32 ids (12 bytes, no
+    // edge, from the radix partition where the edge numbers are not needed), or (X with 2^31
+    // rows or more) three arrays
     const bool packed = nx <= (int64_t)INT32_MAX;
-    const size_t o_rec = transpose && packed ? take((size_t)nnz * 16) : 0;
-    const size_t bucket_b = transpose ? transpose_scratch_bytes(nnz, nx) : 0;
+    const size_t bucket_b = transpose ? transpose_scratch_bytes(nnz, nx, pull) : 0;
+    const size_t o_rec = transpose && packed ? take((size_t)nnz * (bucket_b && !pull ? 12 : 16)) : 0;
     const size_t o_bucket = bucket_b ? take(bucket_b) : 0;
     const size_t o_key = transpose && !packed ? take((size_t)nnz * 8) : 0;
     const size_t o_row = transpose && !packed ? take((size_t)nnz * 8) : 0;
@@ -1248,9 +1249,10 @@ static geot_status_t gs_backward(const void *X, geot_dtype_t x_type, int64_t num
         int64_t *row_t = packed ? nullptr : (int64_t *)(base + o_row);
         float *w_t = packed ? nullptr : (float *)(base + o_w);
         int32_t *rec = packed ? (int32_t *)(base + o_rec) : nullptr;
+        int rec_words = 4;
         GEOT_HIP(launch_transpose(col, nx, sorted_row, idx32, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                                   (int64_t *)(base + o_off), (int64_t *)(base + o_sums), key_t, row_t, w_t, rec,
-                                  bucket_b ? base + o_bucket : nullptr, st),
+                                  bucket_b ? base + o_bucket : nullptr, pull, &rec_words, nullptr, st),
                  "launch transpose kernels");
         if (pull) {
             GEOT_HIP(launch_gs_bwd_x_max_pull(rec, (const int64_t *)(base + o_off), arg, grad_out, nx, num_rows, F, V,
@@ -1266,7 +1268,7 @@ static geot_status_t gs_backward(const void *X, geot_dtype_t x_type, int64_t num
             tp.col = rec + 1;
             tp.w = (const float *)(rec + 2);
             tp.idx32 = 1;
-            tp.meta_stride = 4;
+            tp.meta_stride = rec_words;
         }
         geot_kernel_choice_t c;
         select_raw(nnz, nx, F, GEOT_OP_SUM, 1, nullptr, &c);
@@ -1353,12 +1355,14 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
     const size_t o_cnt = take((size_t)((nx + 1) & ~(int64_t)1) * 4);
     const size_t o_off = take((size_t)(nx + 1) * 8);
     const size_t o_sums = take((size_t)((nx + 4095) / 4096 + 1) * 8);
-    // placed as 16-byte records (one store per edge; grouped by buckets of columns first for
-    // large inputs) and split into the outputs by one streaming pass
-    const size_t bucket_b = transpose_scratch_bytes(nnz, nx);
+    // the radix partition (from 2^20 edges where its bins stay small) writes the outputs from
+    // its final pass; otherwise the edges are placed as 16-byte records (one store per edge;
+    // grouped by buckets of columns first for large inputs) and split into the outputs by one
+    // streaming pass
+    const size_t bucket_b = transpose_scratch_bytes(nnz, nx, false);
     const size_t o_bucket = bucket_b ? take(bucket_b) : 0;
     const bool packed = nx <= (int64_t)INT32_MAX;
-    const size_t o_rec = packed ? take((size_t)nnz * 16) : 0;
+    const size_t o_rec = packed ? take((size_t)nnz * (bucket_b ? 12 : 16)) : 0;
     ScratchGuard sg;
     sg.st = st;
     geot_status_t s = scratch_alloc(&sg.p, at, st);
@@ -1379,11 +1383,13 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
         }());
         if (s != GEOT_SUCCESS) return s;
     }
+    bool written = false;
     GEOT_HIP(launch_transpose(col, nx, sorted_row, 0, weight, roff, num_rows, mean, nnz, (unsigned *)(base + o_cnt),
                               (int64_t *)(base + o_off), (int64_t *)(base + o_sums), sorted_col_out, row_out,
-                              coef_out, rec, bucket_b ? base + o_bucket : nullptr, st),
+                              coef_out, rec, bucket_b ? base + o_bucket : nullptr, false, nullptr, &written, st),
              "launch transpose kernels");
-    if (packed) GEOT_HIP(launch_unpack(rec, nnz, sorted_col_out, row_out, coef_out, st), "launch unpack kernel");
+    if (packed && !written)
+        GEOT_HIP(launch_unpack(rec, nnz, sorted_col_out, row_out, coef_out, st), "launch unpack kernel");
     void *p_free = sg.p;
     sg.p = nullptr;
     return scratch_free(p_free, st);

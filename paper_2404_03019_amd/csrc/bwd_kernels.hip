@@ -1180,136 +1180,179 @@ __global__ __launch_bounds__(256) void place_kernel(const I *col, int64_t nx, co
     }
 }
 
-// ---- the transposition in buckets of columns (large inputs) ---------------
-// The edges are first grouped by buckets of at most kBucketCols consecutive
-// columns (block-local counts in LDS, a scan, a scatter with LDS cursors) as
-// 16-byte records; then one block per bucket counts, scans and places the
-// bucket's records by column in LDS. No pass takes a global atomic per edge
-// (on MI355X those run at about 33 G/s, local or not, and bound the direct
-// transposition).
-constexpr int kBucketChunk = 128 * 256;  // edges per block in the bucket passes
-constexpr int64_t kBucketTarget = 1 << 16;  // records per bucket aimed at
-constexpr int kMaxBuckets = 4096;
-constexpr int kBucketCols = 2048;  // columns per bucket sorted in LDS
-constexpr int64_t kBucketMinEdges = 1 << 20;  // below this the direct transposition is as fast
+// ---- the transposition as a radix partition by columns (from 2^20 edges) ----
+// Columns fall into bins of 2^shift consecutive columns, bins into coarse buckets of 2^b2 bins.
+// One pass counts the edges per bin (LDS counts per block, then summed and scanned), a grouping
+// pass moves the edges as records {column, row, coefficient[, edge]} into coarse-bucket order, a
+// splitting pass moves each coarse bucket's records into bin order, and a final pass sorts each
+// bin by column in LDS. The grouping and splitting passes stage a tile of kRxTile records in
+// LDS, ordered by destination, and take one global atomic per (tile, destination) for the run's
+// place, so every record store is part of a run of consecutive addresses. The final pass writes
+// each bin's records in column order from LDS, as whole runs. Nothing here takes a global atomic
+// per edge (on MI355X those run at about 33 G/s, local or not). The order of the edges within a
+// column depends on timing (the runs of different tiles take their places in arrival order).
+// Records are 12 bytes where the edge numbers are not needed, else 16.
+constexpr int64_t kRxMinEdges = 1 << 20;  // below this the direct transposition is as fast
+constexpr int kRxTile = 8192;      // edges per tile of the grouping pass (and chunks of the counting pass)
+// records per tile of the splitting pass: 12-byte records split fastest in tiles of 4,096 (two
+// blocks per CU: 329 against 430 us on the SpMM graph), 16-byte ones in tiles of 8,192 (399
+// against 424 us)
+template <int W> constexpr int kRxSplitTile = W == 3 ? 4096 : 8192;
+constexpr int kRxMaxBins = 32768;  // bins counted in LDS by the counting pass
+constexpr int kRxBinColsLog = 11;  // at most 2^11 columns per bin (the final pass's LDS counts)
+constexpr int kRxAim = 4096;       // records per bin aimed at
+constexpr int kRxPer = 6;          // records per thread of the final pass
+constexpr int kRxStage = 4096;     // records per round of the final pass's LDS staging
+constexpr int kRxCap = 1024 * kRxPer;  // records per bin sorted from registers; larger bins walk twice
+constexpr int kRxSpan = 1024;      // bins one splitting tile counts in LDS
 
-// counts of the block's edges per bucket, bucket-major: bcnt[b * nblk + block]
-template <typename I>
-__global__ __launch_bounds__(256) void bucket_count_kernel(const I *col, int64_t n, int64_t nx, int shift,
-                                                           int nbuckets, int64_t nblk, unsigned *bcnt) {
-    __shared__ unsigned h[kMaxBuckets];
-    for (int b = threadIdx.x; b < nbuckets; b += 256) h[b] = 0;
+// a record of W words: {column, row, coefficient bits} and for W = 4 the edge number
+template <int W> struct RxRec;
+template <> struct RxRec<3> {
+    using T = int3;
+    static __device__ __forceinline__ T make(int c, int r, int coef, int e) { return make_int3(c, r, coef); }
+};
+template <> struct RxRec<4> {
+    using T = int4;
+    static __device__ __forceinline__ T make(int c, int r, int coef, int e) { return make_int4(c, r, coef, e); }
+};
+
+// exclusive scan of one value per thread over a block of 1024 threads; *total gets the sum.
+// Every thread of the block must call it (two barriers).
+__device__ __forceinline__ unsigned block_excl_scan(unsigned v, unsigned *s_wave, unsigned *total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    unsigned x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const unsigned y = (unsigned)__shfl_up((int)x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) s_wave[wave] = x;
     __syncthreads();
-    const int64_t e0 = (int64_t)blockIdx.x * kBucketChunk;
-    for (int k = 0; k < kBucketChunk / 256; ++k) {
-        const int64_t e = e0 + (int64_t)k * 256 + threadIdx.x;
-        if (e >= n) break;
-        const int64_t c = (int64_t)col[e];
-        if ((uint64_t)c < (uint64_t)nx) atomicAdd(&h[(int)(c >> shift)], 1u);
+    unsigned before = 0, all = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const unsigned t = s_wave[k];
+        before += k < wave ? t : 0u;
+        all += t;
     }
     __syncthreads();
-    for (int b = threadIdx.x; b < nbuckets; b += 256) bcnt[(int64_t)b * nblk + blockIdx.x] = h[b];
+    *total = all;
+    return before + x - v;
 }
 
-// total[0] = off[len - 1] + cnt[len - 1]: the records the scatter writes
-__global__ void scan_total_kernel(const int64_t *off, const unsigned *cnt, int64_t len, int64_t *total) {
-    if (threadIdx.x == 0 && blockIdx.x == 0) total[0] = off[len - 1] + (int64_t)cnt[len - 1];
-}
-
-// the block's edges as 16-byte records {col, row, coefficient, 0} into bucket order; the
-// cursors hold absolute record positions (n < 2^32 on this path). Each thread loads kU
-// edges before it places them.
-template <typename I>
-__global__ __launch_bounds__(256) void bucket_scatter_kernel(const I *col, int64_t nx, const I *row,
-                                                             const float *w, const int64_t *roff, int64_t nrows,
-                                                             int mean, int64_t n, int shift, int nbuckets, int64_t nblk,
-                                                             const int64_t *boff, int32_t *tmp) {
-    constexpr int kU = 4;
-    __shared__ unsigned cur[kMaxBuckets];
-    for (int b = threadIdx.x; b < nbuckets; b += 256) cur[b] = (unsigned)boff[(int64_t)b * nblk + blockIdx.x];
-    __syncthreads();
-    const int64_t e0 = (int64_t)blockIdx.x * kBucketChunk;
-    const int64_t e1 = min(e0 + (int64_t)kBucketChunk, n);
-    for (int64_t b0 = e0; b0 < e1; b0 += 256 * kU) {
-        int64_t c[kU], r[kU];
-        float wt[kU];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int64_t e = b0 + u * 256 + threadIdx.x;
-            const bool in = e < e1;
-            c[u] = in ? (int64_t)col[e] : -1;
-            r[u] = in ? (int64_t)row[e] : 0;
-            wt[u] = in && w ? w[e] : 1.0f;
-        }
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            if ((uint64_t)c[u] >= (uint64_t)nx) continue;
-            const unsigned pos = atomicAdd(&cur[(int)(c[u] >> shift)], 1u);
-            float coef = wt[u];
-            if (mean && (uint64_t)r[u] < (uint64_t)nrows) coef = coef / (float)(roff[r[u] + 1] - roff[r[u]]);
-            *reinterpret_cast<int4 *>(tmp + 4 * (int64_t)pos) =
-                make_int4((int)c[u], (int)r[u], __float_as_int(coef), (int)(uint32_t)(b0 + u * 256 + threadIdx.x));
-        }
-    }
-}
-
-// One block per bucket: its records tmp[start, end) (columns b << shift ..) are
-// counted per column, scanned and placed within the bucket's output range, all
-// in LDS. A wave whose lanes share lane 0's column takes their slots with one
-// LDS atomic (so a column holding most of a bucket does not serialise).
-template <bool PACKED>
-__global__ __launch_bounds__(256) void bucket_sort_kernel(const int32_t *tmp, const int64_t *boff, int64_t nblk,
-                                                          const int64_t *total, int shift, int nbuckets,
-                                                          int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                                                          int64_t nx, int64_t *col_off) {
-    constexpr int kU = 8;
-    __shared__ unsigned h[kBucketCols];
-    __shared__ unsigned s_t[256];
-    const int b = blockIdx.x;
-    const int64_t lo = boff[(int64_t)b * nblk];
-    const int64_t hi = b + 1 < nbuckets ? boff[(int64_t)(b + 1) * nblk] : *total;
-    const int ncols = 1 << shift;
-    const unsigned mask = (unsigned)ncols - 1u;
+// slot of this lane's record among its key's in the LDS counters h: a wave whose lanes share
+// lane 0's key takes their slots with one LDS atomic (so one hub column does not serialise)
+__device__ __forceinline__ unsigned lds_claim(unsigned *h, unsigned key, bool valid) {
     const int lane = threadIdx.x & 63;
-    for (int c = threadIdx.x; c < ncols; c += 256) h[c] = 0;
+    const unsigned k0 = (unsigned)__shfl((int)key, 0, 64);
+    const bool same = valid && key == k0;
+    const unsigned long long m = __ballot(same);
+    const int leader = m ? __ffsll((long long)m) - 1 : 0;
+    unsigned base = 0;
+    if (same && lane == leader) base = atomicAdd(&h[k0], (unsigned)__popcll(m));
+    base = (unsigned)__shfl((int)base, leader, 64);
+    unsigned r = 0;
+    if (same) r = base + (unsigned)__popcll(m & ((1ull << lane) - 1ull));
+    else if (valid) r = atomicAdd(&h[key], 1u);
+    return r;
+}
+
+// per block, the edges of its chunk per bin, cnt[block * nbins + bin], and per coarse bucket,
+// cc[block * 256 + k]
+template <typename I>
+__global__ __launch_bounds__(1024) void rx_count_kernel(const I *col, int64_t n, int64_t nx, int shift, int nbins,
+                                                        int b2, int64_t chunk, unsigned *cnt, unsigned *cc) {
+    constexpr int kU = 16;  // loads in flight per thread
+    __shared__ unsigned h[kRxMaxBins];
+    for (int b = threadIdx.x; b < nbins; b += 1024) h[b] = 0;
     __syncthreads();
-    // slot of this lane's record among its column's (claims from h, aggregating lane 0's column)
-    auto claim = [&](unsigned key, bool valid) -> unsigned {
-        const unsigned k0 = (unsigned)__shfl((int)key, 0, 64);
-        const bool same = valid && key == k0;
-        const unsigned long long m = __ballot(same);
-        const int leader = m ? __ffsll((long long)m) - 1 : 0;
-        unsigned base = 0;
-        if (same && lane == leader) base = atomicAdd(&h[k0], (unsigned)__popcll(m));
-        base = (unsigned)__shfl((int)base, leader, 64);
-        unsigned r = 0;
-        if (same) r = base + (unsigned)__popcll(m & ((1ull << lane) - 1ull));
-        else if (valid) r = atomicAdd(&h[key], 1u);
-        return r;
-    };
-    // kU records per thread in flight: a bucket is walked by its one block
-    for (int64_t i0 = lo; i0 < hi; i0 += 256 * kU) {
-        unsigned key[kU];
+    const int64_t e0 = (int64_t)blockIdx.x * chunk;
+    const int64_t e1 = min(e0 + chunk, n);
+    for (int64_t b0 = e0; b0 < e1; b0 += kU * 1024) {
+        int64_t c[kU];
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const int64_t i = i0 + u * 256 + threadIdx.x;
-            key[u] = i < hi ? ((unsigned)tmp[4 * i] & mask) : 0u;
+            const int64_t e = b0 + u * 1024 + threadIdx.x;
+            c[u] = e < e1 ? (int64_t)col[e] : -1;
         }
 #pragma unroll
-        for (int u = 0; u < kU; ++u) (void)claim(key[u], i0 + u * 256 + threadIdx.x < hi);
+        for (int u = 0; u < kU; ++u)
+            if ((uint64_t)c[u] < (uint64_t)nx) atomicAdd(&h[(int)(c[u] >> shift)], 1u);
     }
     __syncthreads();
-    // exclusive scan of h[0, ncols): 8 columns per thread, then across the threads
-    constexpr int kPer = kBucketCols / 256;
-    unsigned v[kPer];
-    unsigned t = 0;
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-        const int c = threadIdx.x * kPer + k;
-        v[k] = c < ncols ? h[c] : 0u;
-        t += v[k];
+    for (int b = threadIdx.x; b < nbins; b += 1024) cnt[(int64_t)blockIdx.x * nbins + b] = h[b];
+    if (threadIdx.x < 256) {
+        const int k = threadIdx.x;
+        unsigned t = 0;
+        for (int b = k << b2; b < min((k + 1) << b2, nbins); ++b) t += h[b];
+        cc[(int64_t)blockIdx.x * 256 + k] = t;
     }
-    s_t[threadIdx.x] = t;
+}
+
+// tot[bin] = the bin's edges over all counting blocks: a block takes 64 bins, 4 threads per bin
+// each sum every 4th block's counts with 16 loads in flight, and the four sums meet in LDS
+__global__ __launch_bounds__(256) void rx_reduce_kernel(const unsigned *cnt, int64_t nblk, int nbins, unsigned *tot) {
+    __shared__ unsigned s_part[4][64];
+    const int j = threadIdx.x & 63, q = threadIdx.x >> 6;
+    const int b = blockIdx.x * 64 + j;
+    unsigned s = 0;
+    if (b < nbins) {
+        for (int64_t k0 = q; k0 < nblk; k0 += 4 * 16) {
+            unsigned v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int64_t k = k0 + 4 * u;
+                v[u] = k < nblk ? cnt[k * nbins + b] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u) s += v[u];
+        }
+    }
+    s_part[q][j] = s;
+    __syncthreads();
+    if (q == 0 && b < nbins) tot[b] = s_part[0][j] + s_part[1][j] + s_part[2][j] + s_part[3][j];
+}
+
+// one block: start[bin] (exclusive scan of tot, start[nbins] = all records) and the cursors of
+// the splitting pass (fcur[bin] = start[bin]). The totals pass through LDS so that the global
+// loads and stores are coalesced while each thread scans a contiguous range.
+__global__ __launch_bounds__(1024) void rx_scan_kernel(const unsigned *tot, int nbins, int64_t *start,
+                                                       unsigned *fcur) {
+    __shared__ unsigned s_v[kRxMaxBins];
+    __shared__ unsigned s_wave[16];
+    for (int i = threadIdx.x; i < nbins; i += 1024) s_v[i] = tot[i];
+    __syncthreads();
+    const int per = (nbins + 1023) / 1024;
+    const int i0 = threadIdx.x * per, i1 = min(i0 + per, nbins);
+    unsigned t = 0;
+    for (int i = i0; i < i1; ++i) t += s_v[i];
+    unsigned all;
+    unsigned run = block_excl_scan(t, s_wave, &all);
+    for (int i = i0; i < i1; ++i) {
+        const unsigned x = s_v[i];
+        s_v[i] = run;
+        run += x;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < nbins; i += 1024) {
+        start[i] = s_v[i];
+        fcur[i] = s_v[i];
+    }
+    if (threadIdx.x == 0) start[nbins] = all;
+}
+
+// the grouping pass's cursors, one per (counting block, coarse bucket): ccur[blk * 256 + k] =
+// the start of bucket k's first bin plus the bucket's edges in the chunks of the blocks before
+// blk. Block k of this kernel scans over the counting blocks (at most 256). The grouping tiles of
+// one chunk then share its cursors: a few dozen atomics per cursor, not one per tile of the input
+// (with shared cursors the grouping pass took 523 against 481 us on the SpMM graph).
+__global__ __launch_bounds__(256) void rx_cursor_kernel(const unsigned *cc, int64_t nblk, const int64_t *start,
+                                                        int b2, unsigned *ccur) {
+    __shared__ unsigned s_t[256];
+    const int k = blockIdx.x;
+    const unsigned v = (int64_t)threadIdx.x < nblk ? cc[(int64_t)threadIdx.x * 256 + k] : 0u;
+    s_t[threadIdx.x] = v;
     __syncthreads();
     for (int d = 1; d < 256; d <<= 1) {
         const unsigned o = threadIdx.x >= (unsigned)d ? s_t[threadIdx.x - d] : 0u;
@@ -1317,38 +1360,247 @@ __global__ __launch_bounds__(256) void bucket_sort_kernel(const int32_t *tmp, co
         s_t[threadIdx.x] += o;
         __syncthreads();
     }
-    unsigned run = s_t[threadIdx.x] - t;
-#pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-        const int c = threadIdx.x * kPer + k;
-        if (c < ncols) h[c] = run;
-        // column starts (for the max gradient's pull over the columns)
-        if (col_off && c < ncols && ((int64_t)b << shift) + c < nx) col_off[((int64_t)b << shift) + c] = lo + run;
-        run += v[k];
-    }
-    if (col_off && threadIdx.x == 0 && b == nbuckets - 1) col_off[nx] = hi;
+    if ((int64_t)threadIdx.x < nblk)
+        ccur[(int64_t)threadIdx.x * 256 + k] = (unsigned)start[(int64_t)k << b2] + s_t[threadIdx.x] - v;
+}
+
+// grouping pass: tile t's edges [t * kRxTile, ..) as W-word records into coarse-bucket order
+// (bucket = (col >> shift) >> b2): counted and ordered in LDS, then written as one run per bucket
+// at a place taken from the cursors of the tile's chunk (tpc tiles per chunk): neighbouring
+// tiles, which run at the same time, write neighbouring runs (blocks of different chunks side
+// by side measured slower: 538 against 481 us). The cursor atomics are issued before the
+// records are staged and waited for after.
+template <typename I, int W>
+__global__ __launch_bounds__(1024) void rx_group_kernel(const I *col, int64_t nx, const I *row, const float *w,
+                                                        const int64_t *roff, int64_t nrows, int mean, int64_t n,
+                                                        int shift, int b2, int64_t tpc, unsigned *ccur,
+                                                        typename RxRec<W>::T *dst) {
+    using R = typename RxRec<W>::T;
+    constexpr int kRxU = kRxTile / 1024;  // edges per thread
+    __shared__ R s_rec[kRxTile];
+    __shared__ unsigned s_cnt[256];
+    __shared__ unsigned s_base[256];
+    __shared__ unsigned s_wave[16];
+    const int64_t chunk = (int64_t)blockIdx.x / tpc;
+    const int64_t t0 = (int64_t)blockIdx.x * kRxTile;
+    if (threadIdx.x < 256) s_cnt[threadIdx.x] = 0;
     __syncthreads();
-    for (int64_t i0 = lo; i0 < hi; i0 += 256 * kU) {
-        int4 rv[kU];
+    int64_t c[kRxU], r[kRxU];
+    float wt[kRxU];
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int64_t i = i0 + u * 256 + threadIdx.x;
-            rv[u] = i < hi ? *reinterpret_cast<const int4 *>(tmp + 4 * i) : make_int4(0, 0, 0, 0);
+    for (int u = 0; u < kRxU; ++u) {
+        const int64_t e = t0 + u * 1024 + threadIdx.x;
+        const bool in = e < n;
+        c[u] = in ? (int64_t)col[e] : -1;
+        r[u] = in ? (int64_t)row[e] : 0;
+        wt[u] = in && w ? w[e] : 1.0f;
+    }
+    unsigned rank[kRxU];
+    int kb[kRxU];
+#pragma unroll
+    for (int u = 0; u < kRxU; ++u) {
+        kb[u] = (uint64_t)c[u] < (uint64_t)nx ? (int)((c[u] >> shift) >> b2) : -1;
+        rank[u] = kb[u] >= 0 ? atomicAdd(&s_cnt[kb[u]], 1u) : 0u;
+        if (mean && kb[u] >= 0 && (uint64_t)r[u] < (uint64_t)nrows) wt[u] = wt[u] / (float)(roff[r[u] + 1] - roff[r[u]]);
+    }
+    __syncthreads();
+    const unsigned v = threadIdx.x < 256 ? s_cnt[threadIdx.x] : 0u;
+    unsigned m;
+    const unsigned ex = block_excl_scan(v, s_wave, &m);
+    if (threadIdx.x < 256) s_cnt[threadIdx.x] = ex;
+    __syncthreads();
+    unsigned gb = 0;
+    if (threadIdx.x < 256 && v) gb = atomicAdd(&ccur[chunk * 256 + threadIdx.x], v);
+#pragma unroll
+    for (int u = 0; u < kRxU; ++u)
+        if (kb[u] >= 0)
+            s_rec[s_cnt[kb[u]] + rank[u]] = RxRec<W>::make((int)c[u], (int)r[u], __float_as_int(wt[u]),
+                                                           (int)(uint32_t)(t0 + u * 1024 + threadIdx.x));
+    if (threadIdx.x < 256) s_base[threadIdx.x] = gb;
+    __syncthreads();
+    for (unsigned i = threadIdx.x; i < m; i += 1024) {
+        const R x = s_rec[i];
+        const int k = (int)(((unsigned)x.x >> shift) >> b2);
+        const int64_t pos = (int64_t)s_base[k] + (int64_t)(i - s_cnt[k]);
+        if (pos < n) dst[pos] = x;
+    }
+}
+
+// splitting pass: tile t's records src[t * kRxSplitTile, ..) (grouped by coarse bucket) into bin
+// order, one run per bin at a place taken from fcur. A tile counts the bins of the coarse buckets
+// it spans in LDS; one that spans more than kRxSpan bins places each record with an atomic.
+template <int W>
+__global__ __launch_bounds__(1024) void rx_split_kernel(const typename RxRec<W>::T *src, const int64_t *start,
+                                                        int nbins, int shift, int b2, unsigned *fcur,
+                                                        typename RxRec<W>::T *dst) {
+    using R = typename RxRec<W>::T;
+    constexpr int kT = kRxSplitTile<W>;
+    constexpr int kRxU = kT / 1024;  // records per thread
+    __shared__ R s_rec[kT];
+    __shared__ unsigned s_cnt[kRxSpan];
+    __shared__ unsigned s_base[kRxSpan];
+    __shared__ unsigned s_wave[16];
+    const int64_t total = start[nbins];
+    const int64_t t0 = (int64_t)blockIdx.x * kT;
+    if (t0 >= total) return;
+    const int64_t t1 = min(t0 + (int64_t)kT, total);
+    const unsigned f0 = (((unsigned)src[t0].x >> shift) >> b2) << b2;
+    const unsigned f1 = ((((unsigned)src[t1 - 1].x >> shift) >> b2) + 1u) << b2;
+    const unsigned span = f1 > f0 ? f1 - f0 : 0u;
+    R x[kRxU];
+#pragma unroll
+    for (int u = 0; u < kRxU; ++u) {
+        const int64_t i = t0 + u * 1024 + threadIdx.x;
+        if (i < t1) x[u] = src[i];
+        else x[u].x = -1;
+    }
+    if (span == 0 || span > (unsigned)kRxSpan) {
+#pragma unroll
+        for (int u = 0; u < kRxU; ++u) {
+            const unsigned f = (unsigned)x[u].x >> shift;
+            if (t0 + u * 1024 + threadIdx.x < t1 && f < (unsigned)nbins) {
+                const int64_t pos = (int64_t)atomicAdd(&fcur[f], 1u);
+                if (pos < total) dst[pos] = x[u];
+            }
+        }
+        return;
+    }
+    for (unsigned b = threadIdx.x; b < span; b += 1024) s_cnt[b] = 0;
+    __syncthreads();
+    unsigned lf[kRxU], rank[kRxU];
+#pragma unroll
+    for (int u = 0; u < kRxU; ++u) {
+        lf[u] = ((unsigned)x[u].x >> shift) - f0;
+        const bool ok = t0 + u * 1024 + threadIdx.x < t1 && lf[u] < span;
+        if (!ok) lf[u] = 0xffffffffu;
+        rank[u] = ok ? atomicAdd(&s_cnt[lf[u]], 1u) : 0u;
+    }
+    __syncthreads();
+    const unsigned v = threadIdx.x < span ? s_cnt[threadIdx.x] : 0u;
+    unsigned m;
+    const unsigned ex = block_excl_scan(v, s_wave, &m);
+    if (threadIdx.x < span) s_cnt[threadIdx.x] = ex;
+    __syncthreads();
+    unsigned gb = 0;
+    if (threadIdx.x < span && v) gb = atomicAdd(&fcur[f0 + threadIdx.x], v);
+#pragma unroll
+    for (int u = 0; u < kRxU; ++u)
+        if (lf[u] != 0xffffffffu) s_rec[s_cnt[lf[u]] + rank[u]] = x[u];
+    if (threadIdx.x < span) s_base[threadIdx.x] = gb;
+    __syncthreads();
+    for (unsigned i = threadIdx.x; i < m; i += 1024) {
+        const R y = s_rec[i];
+        const unsigned l = ((unsigned)y.x >> shift) - f0;
+        const int64_t pos = (int64_t)s_base[l] + (int64_t)(i - s_cnt[l]);
+        if (pos < total) dst[pos] = y;
+    }
+}
+
+// record slot p of the output: one record, or the three arrays
+template <bool ARRAYS, typename R>
+__device__ __forceinline__ void rx_put(int64_t p, R x, R *rec, int64_t *key_t, int64_t *row_t, float *w_t) {
+    if constexpr (ARRAYS) {
+        key_t[p] = (int64_t)x.x;
+        row_t[p] = (int64_t)x.y;
+        w_t[p] = __int_as_float(x.z);
+    } else {
+        rec[p] = x;
+    }
+}
+
+// final pass, one block per bin: the bin's records src[start[b], start[b + 1]) ordered by
+// column and written from LDS as runs, kRxStage records at a time (up to kRxCap records, held in
+// registers); a bin of one column is copied; a larger bin is walked twice and its records
+// placed one by one within the bin's range. Writes the column starts col_off[c] (col_off[nx]
+// by the last bin).
+template <bool ARRAYS, int W>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8))) void rx_final_kernel(
+    const typename RxRec<W>::T *src, const int64_t *start, int nbins, int shift, int64_t nx,
+    typename RxRec<W>::T *rec, int64_t *key_t, int64_t *row_t, float *w_t, int64_t *col_off) {
+    using R = typename RxRec<W>::T;
+    __shared__ R s_rec[kRxStage];
+    __shared__ unsigned h[1 << kRxBinColsLog];
+    __shared__ unsigned s_wave[16];
+    const int b = blockIdx.x;
+    const int64_t lo = start[b], hi = start[b + 1];
+    const int64_t c0 = (int64_t)b << shift;
+    const int ncols = (int)min((int64_t)1 << shift, nx - c0);
+    const unsigned mask = (1u << shift) - 1u;
+    if (b == nbins - 1 && threadIdx.x == 0 && col_off) col_off[nx] = hi;
+    if (hi <= lo || ncols == 1) {
+        if (col_off)
+            for (int c = threadIdx.x; c < ncols; c += 1024) col_off[c0 + c] = lo;
+        for (int64_t i = lo + threadIdx.x; i < hi; i += 1024) rx_put<ARRAYS>(i, src[i], rec, key_t, row_t, w_t);
+        return;
+    }
+    const int64_t m = hi - lo;
+    for (int c = threadIdx.x; c < ncols; c += 1024) h[c] = 0;
+    __syncthreads();
+    // exclusive scan of h[0, ncols) in place (two columns per thread), and the column starts
+    auto scan_cols = [&]() {
+        const int c = 2 * threadIdx.x;
+        const unsigned a = c < ncols ? h[c] : 0u, d = c + 1 < ncols ? h[c + 1] : 0u;
+        unsigned all;
+        const unsigned ex = block_excl_scan(a + d, s_wave, &all);
+        if (c < ncols) h[c] = ex;
+        if (c + 1 < ncols) h[c + 1] = ex + a;
+        if (col_off && c < ncols) col_off[c0 + c] = lo + ex;
+        if (col_off && c + 1 < ncols) col_off[c0 + c + 1] = lo + ex + a;
+        __syncthreads();
+    };
+    if (m <= kRxCap) {
+        R x[kRxPer];
+        unsigned rank[kRxPer];
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) {
+            const int64_t i = lo + u * 1024 + threadIdx.x;
+            if (i < hi) x[u] = src[i];
+            else x[u].x = 0;
         }
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const bool valid = i0 + u * 256 + threadIdx.x < hi;
-            const unsigned r = claim((unsigned)rv[u].x & mask, valid);
-            if (valid) {
-                const int64_t pos = lo + (int64_t)r;
-                if constexpr (PACKED) {
-                    *reinterpret_cast<int4 *>(rec + 4 * pos) = rv[u];
-                } else {
-                    key_t[pos] = (int64_t)rv[u].x;
-                    row_t[pos] = (int64_t)rv[u].y;
-                    w_t[pos] = __int_as_float(rv[u].z);
-                }
+        for (int u = 0; u < kRxPer; ++u) rank[u] = lds_claim(h, (unsigned)x[u].x & mask, u * 1024 + threadIdx.x < m);
+        __syncthreads();
+        scan_cols();
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) rank[u] += h[(unsigned)x[u].x & mask];
+        for (int64_t s0 = 0; s0 < m; s0 += kRxStage) {
+#pragma unroll
+            for (int u = 0; u < kRxPer; ++u) {
+                const int64_t p = (int64_t)rank[u] - s0;
+                if (u * 1024 + threadIdx.x < m && p >= 0 && p < kRxStage) s_rec[p] = x[u];
             }
+            __syncthreads();
+            const int64_t len = min((int64_t)kRxStage, m - s0);
+            for (int i = threadIdx.x; i < len; i += 1024) rx_put<ARRAYS>(lo + s0 + i, s_rec[i], rec, key_t, row_t, w_t);
+            __syncthreads();
+        }
+        return;
+    }
+    for (int64_t i0 = lo; i0 < hi; i0 += 1024 * kRxPer) {
+        unsigned key[kRxPer];
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) {
+            const int64_t i = i0 + u * 1024 + threadIdx.x;
+            key[u] = i < hi ? ((unsigned)src[i].x & mask) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) (void)lds_claim(h, key[u], i0 + u * 1024 + threadIdx.x < hi);
+    }
+    __syncthreads();
+    scan_cols();
+    for (int64_t i0 = lo; i0 < hi; i0 += 1024 * kRxPer) {
+        R x[kRxPer];
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) {
+            const int64_t i = i0 + u * 1024 + threadIdx.x;
+            if (i < hi) x[u] = src[i];
+            else x[u].x = 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kRxPer; ++u) {
+            const bool valid = i0 + u * 1024 + threadIdx.x < hi;
+            const unsigned r = lds_claim(h, (unsigned)x[u].x & mask, valid);
+            if (valid && (int64_t)r < m) rx_put<ARRAYS>(lo + (int64_t)r, x[u], rec, key_t, row_t, w_t);
         }
     }
 }
@@ -1402,68 +1654,112 @@ hipError_t scan_counts(const unsigned *counts, int64_t len, int64_t *off, int64_
     return hipGetLastError();
 }
 
-// bucket layout: 2^bb buckets of 2^shift columns: at most kBucketCols columns (nx <= 2^23),
-// at most about kBucketTarget records (on average) per bucket, and at least 1024 buckets
-// where the columns allow, so the per-bucket sort has blocks for every CU; nblk blocks of
-// kBucketChunk edges in the grouping passes
-int64_t bucket_words(int64_t n, int64_t nx, int *shift, int *nbuckets, int64_t *nblk) {
-    int nb = 1;
-    while (nb < 23 && ((int64_t)1 << nb) < nx) ++nb;     // bits of the largest column
-    int by_rows = 0;
-    while (by_rows < 12 && (kBucketTarget << by_rows) < n) ++by_rows;
-    const int bb = std::min({nb, 12, std::max({nb - 11, by_rows, 10})});
-    *shift = nb - bb;
-    *nbuckets = 1 << bb;
-    *nblk = (n + kBucketChunk - 1) / kBucketChunk;
-    return (int64_t)*nbuckets * *nblk;
+// radix layout: bins of 2^shift columns, coarse buckets of 2^b2 bins (b2 = 0: the grouping pass
+// places bins directly), and the counting pass's blocks of chunk edges
+struct RxPlan {
+    int shift, b2, nbins;
+    int64_t chunk, nblk;
+};
+
+// Whether the radix partition takes (n, nx), and its layout: at most kRxMaxBins bins of at most
+// 2^kRxBinColsLog columns, the widest bins that keep about kRxAim records per bin on average
+// where that many bins allow it (bins of one column take any number; beyond that the final pass
+// walks the larger bins twice), at most 256 coarse buckets, and 256 counting blocks. Record
+// positions and counts are 32-bit (n < 2^32), columns fit the records' 32-bit word.
+bool rx_plan(int64_t n, int64_t nx, RxPlan *p) {
+    if (n < kRxMinEdges || n > (int64_t)UINT32_MAX || nx <= 128 || nx > ((int64_t)1 << 23)) return false;
+    int nb = 0;
+    while (((int64_t)1 << nb) < nx) ++nb;
+    auto bins = [&](int sh) { return ((nx - 1) >> sh) + 1; };
+    int shift = std::max(0, nb - 15);
+    while (shift < kRxBinColsLog && n <= (int64_t)kRxAim * bins(shift + 1)) ++shift;
+    p->shift = shift;
+    p->nbins = (int)bins(shift);
+    int fb = 0;
+    while ((1 << fb) < p->nbins) ++fb;
+    p->b2 = std::max(0, fb - 8);
+    const int64_t per = (n + 255) / 256;
+    p->chunk = (per + kRxTile - 1) / kRxTile * kRxTile;
+    p->nblk = (n + p->chunk - 1) / p->chunk;
+    return true;
+}
+
+// radix scratch: per-block bin counts, per-block coarse-bucket counts, bin totals, bin starts,
+// the splitting and grouping cursors, and a second buffer of n records of `words` words
+// (offsets into one allocation in o[0..6])
+size_t rx_scratch(const RxPlan &p, int64_t n, int words, size_t o[7]) {
+    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    size_t at = 0;
+    const size_t sz[7] = {(size_t)(p.nblk * p.nbins) * 4, (size_t)p.nblk * 256 * 4, (size_t)p.nbins * 4,
+                          (size_t)(p.nbins + 1) * 8, (size_t)p.nbins * 4, (size_t)p.nblk * 256 * 4,
+                          (size_t)n * 4 * words};
+    for (int i = 0; i < 7; ++i) {
+        o[i] = at;
+        at += a256(sz[i]);
+    }
+    return at;
 }
 
 }  // namespace
 
-size_t transpose_scratch_bytes(int64_t n, int64_t nx) {
-    // per-bucket counts are 32-bit: n < 2^32
-    // and at least 256 buckets (nx > 128)
-    if (n < kBucketMinEdges || n > (int64_t)UINT32_MAX || nx > ((int64_t)1 << 23) || nx <= 128) return 0;
-    int shift, nb;
-    int64_t nblk;
-    const int64_t len = bucket_words(n, nx, &shift, &nb, &nblk);
-    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    return a256((size_t)len * 4) + a256((size_t)(len + 1) * 8) + a256((size_t)((len + kScanTile - 1) / kScanTile + 1) * 8) +
-           a256(64) + a256((size_t)n * 16);
+size_t transpose_scratch_bytes(int64_t n, int64_t nx, bool edges) {
+    RxPlan rp;
+    size_t o[7];
+    return rx_plan(n, nx, &rp) ? rx_scratch(rp, n, edges ? 4 : 3, o) : 0;
 }
 
 namespace {
 
-template <typename I>
-hipError_t launch_transpose_bucketed(const I *col, int64_t nx, const I *row, const float *w,
-                                     const int64_t *roff, int64_t nrows, bool mean, int64_t n, int64_t *key_t, int64_t *row_t,
-                                     float *w_t, int32_t *rec, char *scratch, int64_t *col_off, hipStream_t st) {
-    int shift, nb;
-    int64_t nblk;
-    const int64_t len = bucket_words(n, nx, &shift, &nb, &nblk);
-    auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    unsigned *bcnt = (unsigned *)scratch;
-    int64_t *boff = (int64_t *)(scratch + a256((size_t)len * 4));
-    int64_t *bsums = (int64_t *)((char *)boff + a256((size_t)(len + 1) * 8));
-    int64_t *total = (int64_t *)((char *)bsums + a256((size_t)((len + kScanTile - 1) / kScanTile + 1) * 8));
-    int32_t *tmp = (int32_t *)((char *)total + a256(64));
-    if (nblk > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(bucket_count_kernel<I>, dim3((unsigned)nblk), dim3(256), 0, st, col, n, nx, shift, nb, nblk,
-                       bcnt);
+// The radix partition with W-word records: counts, their sum over blocks and scan, the grouping
+// cursors, then the grouping pass (into rec when a splitting pass follows, else into the scratch
+// records), the splitting pass (rec into the scratch records) and the final pass (into rec, or
+// into the three arrays when `arrays`).
+template <typename I, int W>
+hipError_t launch_transpose_radix(const RxPlan &p, const I *col, int64_t nx, const I *row, const float *w,
+                                  const int64_t *roff, int64_t nrows, bool mean, int64_t n, int64_t *key_t,
+                                  int64_t *row_t, float *w_t, int32_t *rec, char *scratch, int64_t *col_off,
+                                  bool arrays, hipStream_t st) {
+    using R = typename RxRec<W>::T;
+    size_t o[7];
+    (void)rx_scratch(p, n, W, o);
+    unsigned *cnt = (unsigned *)(scratch + o[0]);
+    unsigned *cc = (unsigned *)(scratch + o[1]);
+    unsigned *tot = (unsigned *)(scratch + o[2]);
+    int64_t *start = (int64_t *)(scratch + o[3]);
+    unsigned *fcur = (unsigned *)(scratch + o[4]);
+    unsigned *ccur = (unsigned *)(scratch + o[5]);
+    R *tmp = (R *)(scratch + o[6]);
+    R *r4 = (R *)rec;
+    const int64_t tiles = (n + kRxTile - 1) / kRxTile;
+    const int64_t stiles = (n + kRxSplitTile<W> - 1) / kRxSplitTile<W>;
+    const int ncoarse = ((p.nbins - 1) >> p.b2) + 1;
+    if (p.nblk > 256 || p.chunk % kRxTile != 0 || stiles > 0x7fffffffLL || p.nbins > kRxMaxBins || ncoarse > 256)
+        return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(rx_count_kernel<I>, dim3((unsigned)p.nblk), dim3(1024), 0, st, col, n, nx, p.shift, p.nbins,
+                       p.b2, p.chunk, cnt, cc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = scan_counts(bcnt, len, boff, bsums, 0, st)) != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_total_kernel, dim3(1), dim3(64), 0, st, boff, bcnt, len, total);
+    hipLaunchKernelGGL(rx_reduce_kernel, dim3((unsigned)((p.nbins + 63) / 64)), dim3(256), 0, st, cnt, p.nblk,
+                       p.nbins, tot);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(bucket_scatter_kernel<I>, dim3((unsigned)nblk), dim3(256), 0, st, col, nx, row, w, roff, nrows,
-                       mean ? 1 : 0, n, shift, nb, nblk, boff, tmp);
+    hipLaunchKernelGGL(rx_scan_kernel, dim3(1), dim3(1024), 0, st, tot, p.nbins, start, fcur);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (rec)
-        hipLaunchKernelGGL(bucket_sort_kernel<true>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
-                           shift, nb, key_t, row_t, w_t, rec, nx, col_off);
+    hipLaunchKernelGGL(rx_cursor_kernel, dim3((unsigned)ncoarse), dim3(256), 0, st, cc, p.nblk, start, p.b2, ccur);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((rx_group_kernel<I, W>), dim3((unsigned)tiles), dim3(1024), 0, st, col, nx, row, w, roff,
+                       nrows, mean ? 1 : 0, n, p.shift, p.b2, p.chunk / kRxTile, ccur, p.b2 > 0 ? r4 : tmp);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (p.b2 > 0) {
+        hipLaunchKernelGGL(rx_split_kernel<W>, dim3((unsigned)stiles), dim3(1024), 0, st, r4, start, p.nbins,
+                           p.shift, p.b2, fcur, tmp);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (arrays)
+        hipLaunchKernelGGL((rx_final_kernel<true, W>), dim3((unsigned)p.nbins), dim3(1024), 0, st, tmp, start,
+                           p.nbins, p.shift, nx, nullptr, key_t, row_t, w_t, col_off);
     else
-        hipLaunchKernelGGL(bucket_sort_kernel<false>, dim3((unsigned)nb), dim3(256), 0, st, tmp, boff, nblk, total,
-                           shift, nb, key_t, row_t, w_t, rec, nx, col_off);
+        hipLaunchKernelGGL((rx_final_kernel<false, W>), dim3((unsigned)p.nbins), dim3(1024), 0, st, tmp, start,
+                           p.nbins, p.shift, nx, r4, nullptr, nullptr, nullptr, col_off);
     return hipGetLastError();
 }
 
@@ -1471,10 +1767,18 @@ template <typename I>
 hipError_t launch_transpose_t(const I *col, int64_t nx, const I *row, const float *w,
                               const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                               int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                              char *bucket_scratch, hipStream_t st) {
-    if (bucket_scratch && transpose_scratch_bytes(n, nx) > 0)
-        return launch_transpose_bucketed(col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec, bucket_scratch,
-                                         off, st);
+                              char *rx_scratch_p, bool edges, int *rec_words, bool *arrays_written, hipStream_t st) {
+    RxPlan rp;
+    if (rx_scratch_p && rec && rx_plan(n, nx, &rp)) {
+        const bool arrays = key_t && row_t && w_t;
+        if (arrays_written) *arrays_written = arrays;
+        if (rec_words) *rec_words = edges ? 4 : 3;
+        if (edges)
+            return launch_transpose_radix<I, 4>(rp, col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec,
+                                                rx_scratch_p, off, arrays, st);
+        return launch_transpose_radix<I, 3>(rp, col, nx, row, w, roff, nrows, mean, n, key_t, row_t, w_t, rec,
+                                            rx_scratch_p, off, arrays, st);
+    }
     hipError_t e = launch_zero_u64((unsigned long long *)counts, (nx + 1) / 2, st);
     if (e != hipSuccess) return e;
     const int64_t geb = (n + 256 * kPasses - 1) / (256 * kPasses);
@@ -1499,13 +1803,17 @@ hipError_t launch_transpose_t(const I *col, int64_t nx, const I *row, const floa
 hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int idx32, const float *w,
                             const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                             int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                            char *bucket_scratch, hipStream_t st) {
+                            char *rx_scratch_p, bool edges, int *rec_words, bool *arrays_written, hipStream_t st) {
+    if (arrays_written) *arrays_written = false;
+    if (rec_words) *rec_words = 4;
     if (n <= 0 || nx <= 0) return hipSuccess;
     if (idx32)
         return launch_transpose_t(static_cast<const int32_t *>(col), nx, static_cast<const int32_t *>(row), w, roff,
-                                  nrows, mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
+                                  nrows, mean, n, counts, off, sums, key_t, row_t, w_t, rec, rx_scratch_p, edges,
+                                  rec_words, arrays_written, st);
     return launch_transpose_t(static_cast<const int64_t *>(col), nx, static_cast<const int64_t *>(row), w, roff, nrows,
-                              mean, n, counts, off, sums, key_t, row_t, w_t, rec, bucket_scratch, st);
+                              mean, n, counts, off, sums, key_t, row_t, w_t, rec, rx_scratch_p, edges, rec_words,
+                              arrays_written, st);
 }
 
 hipError_t launch_gs_bwd_x_max_pull(const int32_t *rec, const int64_t *off, const void *arg, const float *gout,
@@ -1673,9 +1981,7 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
     if (n <= 0) return hipSuccess;
     if (op == GEOT_BWD_MAX && !arg) return hipErrorInvalidValue;
     if (given && !seg_bwd_arg32(n)) return hipErrorInvalidValue;   // recorded recipients are 32-bit
-    const int64_t gb = grid_rows(n, (int)(F / V));
-    if (gb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    const unsigned g = (unsigned)gb;
+    if (grid_rows(n, (int)(F / V)) > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     // recipients as 32-bit edge numbers below 2^32 - 1 edges, else 64-bit
     const bool a32 = seg_bwd_arg32(n);
     auto run = [&](auto at) -> hipError_t {

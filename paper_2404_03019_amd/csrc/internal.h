@@ -163,17 +163,22 @@ hipError_t launch_unpack(const int32_t *rec, int64_t n, int64_t *key_t, int64_t 
 // counts [nx] (rounded up to even) and off [nx + 1] / sums [ceil(nx / 4096)] are scratch.
 // With rec != nullptr (needs nx and the rows < 2^31) each edge is one 16-byte record
 // {int32 key, int32 row, float coefficient, uint32 edge number (its low 32 bits)} at
-// rec[4 * slot] and key_t, row_t, w_t are unused. bucket_scratch (transpose_scratch_bytes(n, nx)
-// bytes, or nullptr) lets large inputs group the edges by buckets of columns and sort each bucket
-// in LDS (no global atomic per edge); counts and sums are then unused. Either way off[c] (nx + 1
-// entries) ends as the start of column c's records.
+// rec[4 * slot] and key_t, row_t, w_t are unused. rx_scratch (transpose_scratch_bytes(n, nx,
+// edges) bytes, or nullptr) lets inputs from 2^20 edges take a radix partition by bins of
+// columns in LDS-staged runs, with no global atomic per edge; counts and sums are then unused,
+// and its records have 3 words {key, row, coefficient} unless `edges` asks for the edge numbers.
+// *rec_words (nullable) gets the words per record written to rec (3 or 4). Either way off[c]
+// (nx + 1 entries) ends as the start of column c's records. When rec and all three arrays are
+// given and the radix partition runs, it writes the three arrays directly (rec is then scratch)
+// and sets *arrays_written (nullable); otherwise the records are in rec.
 // col and row are int32 when idx32, else int64.
 hipError_t launch_transpose(const void *col, int64_t nx, const void *row, int idx32, const float *w,
                             const int64_t *roff, int64_t nrows, bool mean, int64_t n, unsigned *counts, int64_t *off,
                             int64_t *sums, int64_t *key_t, int64_t *row_t, float *w_t, int32_t *rec,
-                            char *bucket_scratch, hipStream_t st);
-// scratch of the bucketed transposition (0: the input takes the direct one)
-size_t transpose_scratch_bytes(int64_t n, int64_t nx);
+                            char *rx_scratch, bool edges, int *rec_words, bool *arrays_written, hipStream_t st);
+// scratch of the radix transposition (0: the input takes the direct one); `edges`: 16-byte
+// records that keep the edge numbers, else 12-byte ones
+size_t transpose_scratch_bytes(int64_t n, int64_t nx, bool edges);
 // fused form, max, w.r.t. X from the packed transposed list (rec, column starts off, both from
 // launch_transpose) and the 32-bit recipients arg [R x F]: grad_X written whole, no atomics
 hipError_t launch_gs_bwd_x_max_pull(const int32_t *rec, const int64_t *off, const void *arg, const float *gout,

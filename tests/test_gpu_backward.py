@@ -12,7 +12,7 @@ import torch
 import oracle
 import paper_2404_03019_amd as geot
 from gpu_util import forward_for_gradient, say
-from workloads import random_gather_problem, random_problem
+from workloads import make_config, random_gather_problem, random_problem
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -235,15 +235,31 @@ def test_transpose_edges(weighted, op):
     within(gx, rx, tx, f"transposed gather grad_X {op} weighted={weighted}")
 
 
+def same_triples(sc, rt, cf, col, row, coef):
+    """The transposed list holds exactly the (column, row, coefficient) triples of the edges,
+    sorted by column (the order inside a column is free: both sides in a canonical order)."""
+    assert np.all(np.diff(sc) >= 0)
+    want = np.lexsort((coef.view(np.uint32), row, col))
+    got = np.lexsort((cf.view(np.uint32), rt, sc))
+    assert np.array_equal(sc[got], col[want]) and np.array_equal(rt[got], row[want])
+    assert np.array_equal(cf[got].view(np.uint32), coef[want].view(np.uint32))
+
+
+def mean_coef(w, row, R):
+    deg = np.bincount(row, minlength=R).astype(np.float32)
+    return (w / deg[row]).astype(np.float32)   # one fp32 division, as the library
+
+
 @pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True), (200, False),
                                     (1 << 23, False)])
 def test_transpose_edges_in_buckets(nx, hub):
-    """Inputs of over 2^20 edges group the edges by buckets of columns, then sort each bucket
-    by column in LDS (1,024 buckets of 512 columns for 300,000 columns, 4,096 of 2,048 for 5,000,000;
-    `hub` sends 40 % of the edges to one column, so one bucket holds most of them; 200 columns
-    give 256 buckets of one column; 2^23 columns is the largest the buckets take). Same
-    canonical comparison as above, sum and mean, and the gradient w.r.t. X through the
-    library's own transposition against the oracle."""
+    """Inputs of over 2^20 edges take the radix partition: bins of columns (586 bins of 512
+    columns for 300,000 columns; 2,442 of 2,048 for 5,000,000; 4,096 of 2,048 for 2^23, the
+    most columns it takes), grouped by coarse buckets and split into bins in LDS-staged runs,
+    then each bin sorted by column in LDS. `hub` sends 40 % of the edges to one column, so its
+    bin exceeds what the final pass holds in registers and is walked twice; 200 columns give
+    bins of one column, which are copied. Same canonical comparison as above, sum and mean,
+    and the gradient w.r.t. X through the library's own transposition against the oracle."""
     n, R, F = 1_300_000, 200_000, 4
     rng = np.random.default_rng(43)
     row = np.sort(rng.integers(0, R, n)).astype(np.int64)
@@ -254,15 +270,7 @@ def test_transpose_edges_in_buckets(nx, hub):
     for op in ("sum", "mean"):
         say(f"bucketed transpose nx={nx} hub={hub} {op}")
         sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, op))
-        assert np.all(np.diff(sc) >= 0)
-        coef = w.copy()
-        if op == "mean":
-            deg = np.bincount(row, minlength=R).astype(np.float32)
-            coef = (coef / deg[row]).astype(np.float32)
-        want = np.lexsort((coef.view(np.uint32), row, col))
-        got = np.lexsort((cf.view(np.uint32), rt, sc))
-        assert np.array_equal(sc[got], col[want]) and np.array_equal(rt[got], row[want])
-        assert np.array_equal(cf[got].view(np.uint32), coef[want].view(np.uint32))
+        same_triples(sc, rt, cf, col, row, w if op == "sum" else mean_coef(w, row, R))
     X = rng.standard_normal((nx, F)).astype(np.float32)
     g = rng.standard_normal((R, F)).astype(np.float32)
     for op in ("sum", "mean"):
@@ -270,6 +278,68 @@ def test_transpose_edges_in_buckets(nx, hub):
         rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op)
         tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, absolute=True)
         within(gx.cpu().numpy(), rx, tx, f"bucketed grad_X nx={nx} hub={hub} {op}")
+
+
+def test_transpose_edges_sparse_tail():
+    """3,000,000 edges over 2^23 columns, 99.9 % of them in the first 2^20 columns: the tail's
+    coarse buckets hold a few records each, so a splitting tile there spans more bins than its
+    LDS counts take and places each record with an atomic, and most of the tail's bins are
+    empty (their column starts still written). Canonical comparison, sum and mean, and the
+    gradient w.r.t. X of both (max pulled over the column starts) against the oracle."""
+    n, R, nx, F = 3_000_000, 100_000, 1 << 23, 2
+    rng = np.random.default_rng(47)
+    row = np.sort(rng.integers(0, R, n)).astype(np.int64)
+    col = rng.integers(0, 1 << 20, n).astype(np.int64)
+    tail = rng.random(n) < 0.001
+    col[tail] = rng.integers(1 << 20, nx, int(tail.sum()))
+    w = rng.random(n, dtype=np.float32)
+    for op in ("sum", "mean"):
+        say(f"transpose sparse tail {op}")
+        sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, op))
+        same_triples(sc, rt, cf, col, row, w if op == "sum" else mean_coef(w, row, R))
+    X = rng.integers(-3, 4, (nx, F)).astype(np.float32)
+    g = rng.standard_normal((R, F)).astype(np.float32)
+    for op in ("sum", "mean", "max"):
+        say(f"sparse tail grad_X {op}")
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.gather_scatter(X, col, w, row, R, "max"),
+                                       geot.gather_scatter(up(X), up(col), up(w), up(row), R, "max"), "sparse tail")
+        gx, _ = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op,
+                                             None if out is None else up(out), need_weight=False)
+        rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, out)
+        tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, out, absolute=True)
+        within(gx.cpu().numpy(), rx, tx, f"sparse tail grad_X {op}")
+
+
+def _mix64(x):
+    """splitmix64's finaliser on uint64 (wrapping)."""
+    x = (x ^ (x >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+    x = (x ^ (x >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+    return x ^ (x >> np.uint64(31))
+
+
+def test_transpose_edges_spmm_graph_full():
+    """The SpMM graph's 61,859,140 edges over 2,449,029 columns (19,134 bins of 128 columns,
+    128 per coarse bucket): the sorted columns equal the sorted input columns, and per column
+    the wrapping sum of a 64-bit mix of (row, coefficient bits) equals the input's, so every
+    column holds exactly its edges' (row, coefficient) pairs."""
+    c = make_config("c4_spmm")
+    col, w, row, nx, R = c["col"], c["weight"], c["index"], c["X"].shape[0], c["num_segments"]
+    del c
+    say("transpose spmm graph")
+    sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, "sum"))
+    torch.cuda.empty_cache()
+    assert np.array_equal(sc, np.sort(col))
+    with np.errstate(over="ignore"):
+        def h(r, cbits):
+            return _mix64((r.astype(np.uint64) << np.uint64(32)) | cbits.astype(np.uint64))
+        starts = np.searchsorted(sc, np.arange(nx))
+        nonempty = np.diff(np.append(starts, sc.size)) > 0
+        got = np.add.reduceat(h(rt, cf.view(np.uint32)), starts[nonempty])
+        order = np.argsort(col, kind="stable")
+        want = np.add.reduceat(h(row[order], w[order].view(np.uint32)), starts[nonempty])
+    assert np.array_equal(got, want)
 
 
 @pytest.mark.parametrize("n", [30_000, 1_300_000])
