@@ -327,6 +327,12 @@ def profile_configs(reps: int):
           lambda: geot.gather_scatter_backward_max_arg(X, col, w, row, g4, a4))
 
 
+# the per-edge byte count of a gather over the transposed list charges every gathered row; those
+# are the destination rows of a power-law graph, which repeat and mostly hit in cache, so the
+# rate can exceed the HBM peak and is no HBM rate there
+GATHER_REUSE = "gathered rows repeat (cache hits): the per-edge rate exceeds HBM; see compulsory_bytes"
+
+
 def suite(reps: int):
     """One JSON line per measurement: every named workload and op, the gradients on the two
     large workloads, and a two-layer graph-convolution training step (library autograd vs the
@@ -476,15 +482,17 @@ def suite(reps: int):
     # count 12 bytes of metadata per edge, grad_w the gathered X row at 2 bytes an element
     b = n4 * 12 + n4 * 512 + R4 * 512
     ms, cold = timed(lambda: geot.gather_scatter_backward(X16, col32, w, row32, g4, "sum", need_weight=False), b)
-    emit("c4_spmm backward grad_X bf16 int32", ms, b, cold)
+    emit("c4_spmm backward grad_X bf16 int32", ms, b, cold, compulsory_bytes=n4 * 12 + 2 * R4 * 512,
+         note=GATHER_REUSE)
     b = n4 * 12 + n4 * 256 + R4 * 512
     ms, cold = timed(lambda: geot.gather_scatter_backward(X16, col32, w, row32, g4, "sum", need_x=False), b)
     emit("c4_spmm backward grad_weight bf16 int32", ms, b, cold)
     del X16, col32, row32
-    # grad_X: edge metadata + one gathered grad_out row per edge + grad_X written
+    # grad_X: edge metadata + one gathered grad_out row per edge + grad_X written; the
+    # compulsory bytes read the metadata and each grad_out row once and write grad_X
     b = n4 * 20 + n4 * 512 + R4 * 512
     ms, cold = timed(lambda: geot.gather_scatter_backward(X, col, w, row, g4, "sum", need_weight=False), b)
-    emit("c4_spmm backward grad_X", ms, b, cold)
+    emit("c4_spmm backward grad_X", ms, b, cold, compulsory_bytes=n4 * 20 + 2 * R4 * 512, note=GATHER_REUSE)
     # grad_w: col, row (the weight is not read for sum) + one gathered X row per edge + each
     # grad_out row once (edges are sorted by row) + grad_w written; same count as the forward
     b = n4 * 20 + n4 * 512 + R4 * 512
@@ -519,8 +527,7 @@ def suite(reps: int):
     # power-law graph, which repeat and mostly hit in cache, so its rate is no HBM rate. The
     # compulsory bytes read each grad_out row once
     emit("c4_spmm backward grad_X from a kept transposed list", ms, b, False,
-         compulsory_bytes=n4 * 20 + 2 * R4 * 512,
-         note="gathered rows repeat (cache hits): the per-edge rate exceeds HBM; see compulsory_bytes")
+         compulsory_bytes=n4 * 20 + 2 * R4 * 512, note=GATHER_REUSE)
     del g4, sc, rt, cf
     # two-layer graph convolution training step on the SpMM graph (128 -> 128 -> 64)
     torch.manual_seed(0)
