@@ -147,13 +147,17 @@ def test_segment_backward_replays(op, shape):
             assert np.array_equal(got, ref), f"replay {k} {op}"
 
 
+@pytest.mark.parametrize("shape", [(3000, 2000, 8, 40000), (30000, 300_000, 4, 1_200_000)],
+                         ids=["direct", "radix"])
 @pytest.mark.parametrize("op", ["sum", "mean", "max"])
-def test_gather_backward_replays(op):
+def test_gather_backward_replays(op, shape):
     """Both gradients of the fused form captured once (temporaries from the stream-ordered
     pool, the transposition, the recipients for max) and replayed with new inputs: every
-    replay within the fp32 bound of the oracle."""
+    replay within the fp32 bound of the oracle. 40,000 edges take the direct transposition,
+    1,200,000 edges over 300,000 columns the radix partition (its counts, cursors and bin
+    starts are rewritten by its own kernels on every replay)."""
     import oracle
-    R, nx, F, n = 3000, 2000, 8, 40000
+    R, nx, F, n = shape
     rng = np.random.default_rng(73)
     X = torch.empty((nx, F), device=DEV)
     col = torch.empty(n, dtype=torch.int64, device=DEV)
@@ -192,7 +196,7 @@ def test_gather_backward_replays(op):
         x, c, ww, r, gg = refill()
         graph.replay()
         torch.cuda.synchronize()
-        say(f"graph replay {k} gather backward {op}")
+        say(f"graph replay {k} gather backward {op} n={n}")
         o = out.cpu().numpy() if op == "max" else None
         rx, rw = oracle.gather_scatter_backward(x, c, ww, r, gg, op, o)
         ax, aw = oracle.gather_scatter_backward(x, c, ww, r, gg, op, o, absolute=True)
