@@ -62,6 +62,60 @@ CASES = [
 ]
 
 
+ROW64_CASES = [
+    # seed, nnz, S, dist, values, empty_frac
+    (21, 50000, 3000, "zipf", "normal", 0.1),
+    (22, 70001, 7, "one_heavy", "uniform", 0.0),     # odd row count
+    (23, 12345, 20000, "uniform", "negative", 0.6),  # more segments than rows, long empty runs
+]
+ROW64_CHOICES = [
+    None,
+    dict(family="ep", lanes=4, vec=8, rows=1),    # many blocks, several partial levels
+    dict(family="ep", lanes=4, vec=8, rows=3),
+    dict(family="ep", lanes=4, vec=8, rows=33),
+    dict(family="ep", lanes=4, vec=8, rows=8, flags=2),   # cached loads asked for explicitly
+]
+
+
+@pytest.mark.parametrize("dt,it", [("bf16", "i64"), ("bf16", "i32"), ("f16", "i64"), ("f16", "i32")])
+@pytest.mark.parametrize("case", ROW64_CASES, ids=lambda c: f"seed{c[0]}")
+def test_segment_reduce_64_byte_rows(dt, it, case):
+    """16-bit rows of 64 bytes (F = 32: 8-element vectors, 4 lanes a row, half a cache line
+    a row): odd row counts per group, an odd total, several partial levels and long empty
+    runs, with src at the start of its allocation and 64 bytes into it. Every op and the
+    recording max against the oracle: max and the recipients exact, sum / mean within the
+    bound."""
+    seed, nnz, S, dist, values, ef = case
+    F = 32
+    p = random_problem(seed, nnz, S, F, dist, values, ef)
+    t, wide = stored(p["src"], dt)
+    i = ids(p["index"], it)
+    padded = torch.zeros((nnz + 1, F), dtype=DT[dt])
+    padded[1:] = t
+    for name, s in (("aligned", t.to(DEV)), ("offset", padded.to(DEV)[1:])):
+        assert (s.data_ptr() % 128 == 0) == (name == "aligned")
+        for op in OPS:
+            ref, terms = oracle_segment(wide, p["index"], S, op)
+            for ch in ROW64_CHOICES:
+                say(f"64-byte rows {dt}/{it} seed={seed} {name} {op} choice={ch}")
+                got = geot.segment_reduce(s, i, S, op, choice=ch).cpu().numpy()
+                compare(got, ref, op, terms, f"64-byte rows {dt}/{it} seed={seed} {name} {op} {ch}")
+        ref = oracle.segment_reduce(wide, p["index"], S, "max")
+        for ch in ROW64_CHOICES:
+            out, arg = geot.segment_reduce_max_arg(s, i, S, choice=ch)
+            compare(out.cpu().numpy(), ref, "max", None, f"64-byte rows recording {dt}/{it} {name} {ch}")
+            a = arg.cpu().numpy().view(np.uint32).astype(np.int64)
+            idx = p["index"]
+            # the lowest row of each segment whose value equals the maximum (none: 2^32 - 1)
+            want = np.full((S, F), (1 << 32) - 1, dtype=np.int64)
+            hit = wide == ref[idx]
+            rows = np.broadcast_to(np.arange(nnz)[:, None], (nnz, F))
+            seg_f = idx[:, None] * F + np.arange(F)[None, :]
+            flat = want.reshape(-1)
+            np.minimum.at(flat, seg_f[hit], rows[hit])
+            assert np.array_equal(a, want), f"64-byte rows recipients {dt}/{it} seed={seed} {name} {ch}"
+
+
 @pytest.mark.parametrize("dt,it", [("bf16", "i64"), ("bf16", "i32"), ("f16", "i64"), ("f16", "i32"),
                                    ("f32", "i32")])
 @pytest.mark.parametrize("case", CASES, ids=lambda c: f"seed{c[0]}_F{c[3]}")
