@@ -252,7 +252,7 @@ def mean_coef(w, row, R):
 
 @pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True), (200, False),
                                     (1 << 23, False)])
-def test_transpose_edges_in_buckets(nx, hub):
+def test_transpose_edges_radix(nx, hub):
     """Inputs of over 2^20 edges take the radix partition: bins of columns (586 bins of 512
     columns for 300,000 columns; 2,442 of 2,048 for 5,000,000; 4,096 of 2,048 for 2^23, the
     most columns it takes), grouped by coarse buckets and split into bins in LDS-staged runs,
@@ -268,7 +268,7 @@ def test_transpose_edges_in_buckets(nx, hub):
         col[rng.random(n) < 0.4] = 12345
     w = rng.random(n, dtype=np.float32)
     for op in ("sum", "mean"):
-        say(f"bucketed transpose nx={nx} hub={hub} {op}")
+        say(f"radix transpose nx={nx} hub={hub} {op}")
         sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(up(col), up(w), up(row), nx, R, op))
         same_triples(sc, rt, cf, col, row, w if op == "sum" else mean_coef(w, row, R))
     X = rng.standard_normal((nx, F)).astype(np.float32)
@@ -277,7 +277,7 @@ def test_transpose_edges_in_buckets(nx, hub):
         gx, _ = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), op, need_weight=False)
         rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op)
         tx, _ = oracle.gather_scatter_backward(X, col, w, row, g, op, absolute=True)
-        within(gx.cpu().numpy(), rx, tx, f"bucketed grad_X nx={nx} hub={hub} {op}")
+        within(gx.cpu().numpy(), rx, tx, f"radix grad_X nx={nx} hub={hub} {op}")
 
 
 def test_transpose_edges_sparse_tail():
@@ -388,18 +388,19 @@ def test_offsets_pass_unaligned_index(itype):
 
 
 @pytest.mark.parametrize("weighted", [True, False])
-def test_gather_backward_max_bucketed(weighted):
-    """Max gradient w.r.t. X pulled over a bucketed transposed list (2,000,000 edges): each X
-    row sums its column's records whose edge is the recipient; integer values, so ties are
-    frequent and the lowest-edge rule decides. Both gradients against the oracle's."""
+def test_gather_backward_max_radix(weighted):
+    """Max gradient w.r.t. X pulled over a transposed list from the radix partition with edge
+    numbers (16-byte records; 2,000,000 edges): each X row sums its column's records whose
+    edge is the recipient; integer values, so ties are frequent and the lowest-edge rule
+    decides. Both gradients against the oracle's."""
     q = random_gather_problem(23, 2_000_000, 50_000, 60_000, 8, "zipf", "int", weighted, 0.05)
     X, col, w, row = q["X"], q["col"], q["weight"], q["index"]
     g = np.random.default_rng(24).standard_normal((50_000, 8)).astype(np.float32)
     out = forward_for_gradient(oracle.gather_scatter(X, col, w, row, 50_000, "max"),
-                               geot.gather_scatter(up(X), up(col), up(w), up(row), 50_000, "max"), "bucketed")
+                               geot.gather_scatter(up(X), up(col), up(w), up(row), 50_000, "max"), "radix")
     gx, gw = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", up(out))
     rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out)
     ax, aw = oracle.gather_scatter_backward(X, col, w, row, g, "max", out, absolute=True)
-    within(gx.cpu().numpy(), rx, ax, f"bucketed max grad_X weighted={weighted}")
+    within(gx.cpu().numpy(), rx, ax, f"radix max grad_X weighted={weighted}")
     if weighted:
-        within(gw.cpu().numpy(), rw, aw, "bucketed max grad_w")
+        within(gw.cpu().numpy(), rw, aw, "radix max grad_w")

@@ -143,8 +143,8 @@ def test_fused_more_than_2_31_edges():
         for op in ("sum", "max"):
             ref = oracle.gather_scatter(Xh, c, None, z, 1, op)
             assert np.array_equal(got[op][r:r + 1], ref), (op, r)
-    # The gradients of the sum over the same edges (unit weights): grad_X through the bucketed
-    # transposition of more than 2^31 records, grad_w over more than 2^31 edges. grad_out is
+    # The gradients of the sum over the same edges (unit weights): grad_X through the radix
+    # transposition (bins of one column) of more than 2^31 records, grad_w over more than 2^31 edges. grad_out is
     # ternary, so every partial sum is an integer below 2^24 and exact in any order.
     g = ternary(R, F, 14)
     w = torch.ones(BIG, device=DEV)
