@@ -1667,7 +1667,7 @@ struct RxPlan {
 // walks the larger bins twice), at most 256 coarse buckets, and 256 counting blocks. Record
 // positions and counts are 32-bit (n < 2^32), columns fit the records' 32-bit word.
 bool rx_plan(int64_t n, int64_t nx, RxPlan *p) {
-    if (n < kRxMinEdges || n > (int64_t)UINT32_MAX || nx <= 128 || nx > ((int64_t)1 << 23)) return false;
+    if (n < kRxMinEdges || n > (int64_t)UINT32_MAX || nx < 1 || nx > ((int64_t)1 << 23)) return false;
     int nb = 0;
     while (((int64_t)1 << nb) < nx) ++nb;
     auto bins = [&](int sh) { return ((nx - 1) >> sh) + 1; };

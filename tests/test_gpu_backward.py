@@ -251,14 +251,15 @@ def mean_coef(w, row, R):
 
 
 @pytest.mark.parametrize("nx,hub", [(300_000, False), (5_000_000, False), (300_000, True), (200, False),
-                                    (1 << 23, False)])
+                                    (1 << 23, False), (100, False), (1, False)])
 def test_transpose_edges_radix(nx, hub):
     """Inputs of over 2^20 edges take the radix partition: bins of columns (586 bins of 512
     columns for 300,000 columns; 2,442 of 2,048 for 5,000,000; 4,096 of 2,048 for 2^23, the
     most columns it takes), grouped by coarse buckets and split into bins in LDS-staged runs,
     then each bin sorted by column in LDS. `hub` sends 40 % of the edges to one column, so its
-    bin exceeds what the final pass holds in registers and is walked twice; 200 columns give
-    bins of one column, which are copied. Same canonical comparison as above, sum and mean,
+    bin exceeds what the final pass holds in registers and is walked twice; 200, 100 and 1
+    columns give bins of one column, which are copied (with at most 256 bins the grouping
+    pass places them directly). Same canonical comparison as above, sum and mean,
     and the gradient w.r.t. X through the library's own transposition against the oracle."""
     n, R, F = 1_300_000, 200_000, 4
     rng = np.random.default_rng(43)
