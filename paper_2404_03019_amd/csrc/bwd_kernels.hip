@@ -845,9 +845,13 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
         if (c >= nx) break;
         const int64_t lo = off[c], hi = off[c + 1];
         for (int j = m.j0; j < nvec; j += m.tpr) {
-            float acc[V];
+            // the column's terms add into `run`, which joins acc every kPullRun records, so a
+            // hub column's long chain rounds like short runs (the fp32 bound holds)
+            constexpr int kPullRun = 256;
+            float acc[V], run[V];
 #pragma unroll
-            for (int k = 0; k < V; ++k) acc[k] = 0.0f;
+            for (int k = 0; k < V; ++k) acc[k] = run[k] = 0.0f;
+            int steps = 0;
             for (int64_t k0 = lo; k0 < hi; k0 += kU) {
                 int4 t[kU];
 #pragma unroll
@@ -884,9 +888,19 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
                     const float coef = __int_as_float(t[u].z);
 #pragma unroll
                     for (int k = 0; k < V; ++k)
-                        if (a[u][k] == (unsigned)t[u].w) acc[k] += coef * g[u][k];
+                        if (a[u][k] == (unsigned)t[u].w) run[k] += coef * g[u][k];
+                }
+                if (++steps == kPullRun / kU) {
+#pragma unroll
+                    for (int k = 0; k < V; ++k) {
+                        acc[k] += run[k];
+                        run[k] = 0.0f;
+                    }
+                    steps = 0;
                 }
             }
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[k] += run[k];
             store_vec<V>(gX + c * F + (int64_t)j * V, acc);
         }
     }

@@ -343,6 +343,31 @@ def test_transpose_edges_spmm_graph_full():
     assert np.array_equal(got, want)
 
 
+def test_gather_backward_max_hub_column_keeps_the_fp32_bound():
+    """Max gradient w.r.t. X when one column receives the maximum of most rows: its row of
+    grad_X sums about 600,000 positive terms over the transposed list. The pull adds them in
+    runs of 256 records, so the fp32 error stays within the bound (one serial chain of that
+    many same-signed terms would not)."""
+    rng = np.random.default_rng(93)
+    R, nx, F, per = 600_000, 5000, 4, 3
+    row = np.repeat(np.arange(R), per).astype(np.int64)
+    n = row.size
+    col = rng.integers(1, nx, n).astype(np.int64)
+    col[::per] = 0                                      # every row has one edge to column 0
+    X = (rng.random((nx, F), dtype=np.float32) + 0.5).astype(np.float32)
+    X[0] = 100.0                                        # ... which attains its maximum
+    w = (rng.random(n, dtype=np.float32) + 0.5).astype(np.float32)
+    w[::per] = 1.0
+    g = (rng.random((R, F), dtype=np.float32) + 0.5).astype(np.float32)
+    say("max gradient, hub column")
+    out = forward_for_gradient(oracle.gather_scatter(X, col, w, row, R, "max"),
+                               geot.gather_scatter(up(X), up(col), up(w), up(row), R, "max"), "hub column")
+    gx, _ = geot.gather_scatter_backward(up(X), up(col), up(w), up(row), up(g), "max", up(out), need_weight=False)
+    rx, _ = oracle.gather_scatter_backward(X, col, w, row, g, "max", out)
+    ax, _ = oracle.gather_scatter_backward(X, col, w, row, g, "max", out, absolute=True)
+    within(gx.cpu().numpy(), rx, ax, "hub column max grad_X")
+
+
 @pytest.mark.parametrize("n", [30_000, 1_300_000])
 def test_transpose_mean_with_rows_out_of_range(n):
     """Row ids outside [0, num_rows) break the precondition: their values are unspecified,

@@ -553,3 +553,32 @@ def test_selection_with_index_statistics():
     assert graph.stats()["max_len"] == int(q["lengths"].max())
     ref, terms = oracle_gather(q["X"], q["col"], q["weight"], q["index"], 15_000, "sum")
     compare(got.detach().cpu().numpy(), ref, "sum", terms, "graph gather with statistics")
+
+
+@pytest.mark.parametrize("choice", [dict(family="sp", groups=1), dict(family="sp", groups=4),
+                                    dict(family="ep", rows=4096)],
+                         ids=["sp-groups1", "sp-groups4", "ep-rows4096"])
+def test_long_segments_of_one_sign_keep_the_fp32_bound(choice):
+    """Segments of 700,000 positive terms: one group's serial fp32 chain over such a segment
+    would be off by about 3e-5 of the absolute sum; the segment-parallel kernel adds its rows
+    in runs of 256 (and the element-parallel one in row runs of at most 4,096 rows), so sum
+    and mean stay within 1e-5 * sum|terms| + 1e-6, rows mode and gather mode."""
+    rng = np.random.default_rng(91)
+    S, F, n = 3, 4, 2_100_000
+    idx = np.repeat(np.arange(S), n // S).astype(np.int64)
+    src = rng.random((n, F), dtype=np.float32) + 0.5
+    s, i = torch.from_numpy(src).to("cuda"), torch.from_numpy(idx).to("cuda")
+    for op in ("sum", "mean"):
+        say(f"long one-signed segments {op} {choice}")
+        ref, terms = oracle_segment(src, idx, S, op)
+        compare(geot.segment_reduce(s, i, S, op, choice=choice).cpu().numpy(), ref, op, terms,
+                f"rows {op} {choice}")
+    nx = 1000
+    col = rng.integers(0, nx, n).astype(np.int64)
+    w = rng.random(n, dtype=np.float32) + 0.5
+    X = rng.random((nx, F), dtype=np.float32) + 0.5
+    c, wt, xg = torch.from_numpy(col).to("cuda"), torch.from_numpy(w).to("cuda"), torch.from_numpy(X).to("cuda")
+    for op in ("sum", "mean"):
+        ref, terms = oracle_gather(X, col, w, idx, S, op)
+        compare(geot.gather_scatter(xg, c, wt, i, S, op, choice=choice).cpu().numpy(), ref, op, terms,
+                f"gather {op} {choice}")
