@@ -321,6 +321,14 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     if (has_rows) {
         first_seg = (int32_t)idx[r0 * ms];
         cur = first_seg;
+        if constexpr (ARG && MODE != SRC_PIECES) {
+            // The run's first segment starts from the neutral value: its recipient starts at the
+            // run's first row, which the walk reduces first, so a first term equal to the
+            // neutral value (-inf) keeps it (the rows walk takes the later side only where it is
+            // strictly larger). Partials carry their own recipients and start from none.
+#pragma unroll
+            for (int k = 0; k < NX; ++k) aix[k] = (uint32_t)r0;
+        }
         prev = r0 > 0 ? (int32_t)idx[(r0 - 1) * ms] : -1;
         next = r1 < a.n ? (int32_t)idx[r1 * ms] : -1;
 

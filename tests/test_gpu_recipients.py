@@ -237,3 +237,34 @@ def test_spmm_max_with_recipients_sampled():
     # grad_X sums each column's recipients' terms in the transposed list's order, which
     # depends on timing: equal up to the rounding of a few terms
     assert torch.allclose(gx, mx, rtol=1e-5, atol=1e-5)
+
+
+@pytest.mark.parametrize("ch", [None, dict(family="ep", rows=1), dict(family="ep", lanes=1, rows=3),
+                                dict(family="ep", vec=1, rows=2)], ids=["default", "rows1", "lanes1", "vec1"])
+def test_recipients_of_minus_infinity(ch):
+    """Terms equal to the neutral value of max (-inf), alone in a segment or first in a row
+    group's run (one-row runs put every row first): the recipient is the lowest such row
+    (edge), not none. Segment and fused forms, against the definition on the oracle's out."""
+    rng = np.random.default_rng(95)
+    S, F, n = 3000, 4, 9000
+    idx = np.sort(rng.integers(0, S, n)).astype(np.int64)
+    src = rng.integers(-3, 4, (n, F)).astype(np.float32)
+    src[rng.random((n, F)) < 0.5] = -np.inf
+    ref = oracle.segment_reduce(src, idx, S, "max")
+    want = expected_recipients(src, idx, S, ref)
+    say(f"recipients of -inf, segment form, choice={ch}")
+    out, arg = geot.segment_reduce_max_arg(up(src), up(idx), S, choice=ch)
+    compare(out.cpu().numpy(), ref, "max", None, f"segment -inf {ch}")
+    check_arg(arg, want, f"segment -inf {ch}")
+    nx = 500
+    col = rng.integers(0, nx, n).astype(np.int64)
+    X = rng.integers(-3, 4, (nx, F)).astype(np.float32)
+    X[rng.random((nx, F)) < 0.5] = -np.inf
+    w = np.ones(n, dtype=np.float32)
+    refg = oracle.gather_scatter(X, col, w, idx, S, "max")
+    terms = X[col] * w[:, None]
+    wantg = expected_recipients(terms, idx, S, refg)
+    say(f"recipients of -inf, fused form, choice={ch}")
+    out, arg = geot.gather_scatter_max_arg(up(X), up(col), up(w), up(idx), S, choice=ch)
+    compare(out.cpu().numpy(), refg, "max", None, f"gather -inf {ch}")
+    check_arg(arg, wantg, f"gather -inf {ch}")
