@@ -330,16 +330,19 @@ geot_status_t geot_segment_reduce_backward_typed(const float *grad_out, const vo
  * library counting-sorts the edges by column into a temporary transposed list
  * (one 16-byte record per edge, 20 bytes when num_x_rows >= 2^31, and 12
  * bytes per X row, from its stream-ordered pool; from 2^20 to 2^32 - 1 edges
- * with 129 to 2^23 X rows the edges are first grouped by buckets of columns,
- * which takes another 16 bytes per edge and 12 bytes per bucket and 32,768
- * edges) and runs the forward gather kernel
+ * with at most 2^23 X rows the edges are radix-partitioned by column instead,
+ * through two buffers of 12-byte records, 16 for max, which keeps the edge
+ * numbers, plus about 1 KiB of counts per bin of up to 2,048 columns, at most
+ * 32,768 bins) and runs the forward gather kernel
  * over it, so every row of grad_X is written without float atomics. Max
  * first finds each (row, feature)'s recipient edge into a temporary table of
  * num_rows * F edge numbers (4 bytes each below 2^32 - 1 edges, else 8; the
  * same pool); below 2^32 - 1 edges and 2^31 X rows each row of grad_X then
  * sums the terms of its column's records whose edge is the recipient (the same
- * transposed list), else the recipients' terms are added atomically. Mean
- * takes (num_rows + 1) int64 row starts.
+ * transposed list), else the recipients' terms are added atomically, in
+ * arrival order, so a column that receives very many terms of one sign may
+ * exceed the fp32 bound given below. Mean takes (num_rows + 1) int64 row
+ * starts.
  *   grad_out     [num_rows x F]: gradient of the loss w.r.t. out
  *   out          [num_rows x F]: the forward result (read for max only)
  *   grad_X       [num_x_rows x F] fp32 or NULL (skipped), overwritten:
@@ -437,10 +440,11 @@ geot_status_t geot_gather_scatter_backward_max_arg(const void *X, geot_dtype_t x
  * atomic cursor); any order is a valid input to the gather. op must be sum or
  * mean (the max gradient depends on the forward result). Edges whose column is
  * out of range are left out, and the tail of the outputs is then unspecified.
- * Temporary memory: 16 bytes per edge (when num_x_rows < 2^31; 32, plus 12
- * bytes per bucket and 32,768 edges, from 2^20 to 2^32 - 1 edges with 129 to
- * 2^23 X rows, where the edges are grouped by buckets of columns first) and 12
- * per X row (and 8 per row for mean), from the library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
+ * Temporary memory: 16 bytes per edge (when num_x_rows < 2^31; 24, plus
+ * about 1 KiB per bin of up to 2,048 columns, from 2^20 to 2^32 - 1 edges
+ * with at most 2^23 X rows, where the edges are radix-partitioned by column
+ * and the last pass writes the outputs) and 12 per X row (and 8 per row for
+ * mean), from the library's pool. Returns GEOT_ERROR_INVALID_VALUE for null arrays, negative
  * sizes, num_rows >= 2^31, another op, or outputs that overlap the inputs or
  * each other.                                                               */
 geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const float *weight,

@@ -1356,9 +1356,8 @@ geot_status_t geot_transpose_edges(const int64_t *col, int64_t num_x_rows, const
     const size_t o_off = take((size_t)(nx + 1) * 8);
     const size_t o_sums = take((size_t)((nx + 4095) / 4096 + 1) * 8);
     // the radix partition (from 2^20 edges where its bins stay small) writes the outputs from
-    // its final pass; otherwise the edges are placed as 16-byte records (one store per edge;
-    // grouped by buckets of columns first for large inputs) and split into the outputs by one
-    // streaming pass
+    // its final pass; otherwise the edges are placed as 16-byte records (one store per edge)
+    // and split into the outputs by one streaming pass
     const size_t bucket_b = transpose_scratch_bytes(nnz, nx, false);
     const size_t o_bucket = bucket_b ? take(bucket_b) : 0;
     const bool packed = nx <= (int64_t)INT32_MAX;
