@@ -60,40 +60,48 @@ __device__ __forceinline__ void load_f32(const float *p, float *x) {
     }
 }
 
-// fp32 -> bf16 bits, rounded to nearest even (a carry into bit 16 from the
-// lower half plus 0x7fff, plus the kept lowest bit for ties); a NaN stays a
-// quiet NaN
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
+// Two fp32 values narrowed to storage type E, rounded to nearest even (a NaN stays a NaN),
+// packed low first. gfx950 converts the pair in one instruction (v_cvt_pk_bf16_f32,
+// v_cvt_pk_f16_f32); a rounding written out in integer operations compiled to a branch per
+// element around its NaN case, and held bf16 gradient stores of the power-law graph at 4.7 TB/s.
 template <int E>
-__device__ __forceinline__ uint32_t narrow_bits(float f) {
-    if constexpr (E == ELEM_BF16) return bf16_bits(f);
-    else return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);  // round to nearest even
+__device__ __forceinline__ uint32_t narrow_pair(float a, float b) {
+    const f32x2_t v = {a, b};
+    if constexpr (E == ELEM_BF16) {
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+    } else {
+        typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2_t));
+    }
 }
 
-// V fp32 values stored as V elements of storage type E at p (aligned to V elements)
-template <int E, int V>
+// one value stored with the non-temporal cache policy (NT) or an ordinary store
+template <bool NT, typename T>
+__device__ __forceinline__ void put(T *p, T v) {
+    if constexpr (NT) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+// V fp32 values stored as V elements of storage type E at p (aligned to V elements), with
+// non-temporal stores when NT
+template <int E, int V, bool NT = false>
 __device__ __forceinline__ void store_elems(typename ElemT<E>::T *p, const float *x) {
     if constexpr (E == ELEM_F32) {
-        store_vec<V>(p, x);
+        if constexpr (NT) store_vec_nt<V>(p, x);
+        else store_vec<V>(p, x);
     } else if constexpr (V == 1) {
-        *reinterpret_cast<uint16_t *>(p) = (uint16_t)narrow_bits<E>(x[0]);
+        put<NT>(reinterpret_cast<uint16_t *>(p), (uint16_t)narrow_pair<E>(x[0], 0.0f));
     } else {
         uint32_t w[V / 2];
 #pragma unroll
-        for (int k = 0; k < V / 2; ++k) w[k] = narrow_bits<E>(x[2 * k]) | (narrow_bits<E>(x[2 * k + 1]) << 16);
+        for (int k = 0; k < V / 2; ++k) w[k] = narrow_pair<E>(x[2 * k], x[2 * k + 1]);
         if constexpr (V == 8) {
-            u32x4_t t = {w[0], w[1], w[2], w[3]};
-            *reinterpret_cast<u32x4_t *>(p) = t;
+            put<NT>(reinterpret_cast<u32x4_t *>(p), u32x4_t{w[0], w[1], w[2], w[3]});
         } else if constexpr (V == 4) {
-            u32x2_t t = {w[0], w[1]};
-            *reinterpret_cast<u32x2_t *>(p) = t;
+            put<NT>(reinterpret_cast<u32x2_t *>(p), u32x2_t{w[0], w[1]});
         } else {
-            *reinterpret_cast<uint32_t *>(p) = w[0];
+            put<NT>(reinterpret_cast<uint32_t *>(p), w[0]);
         }
     }
 }
@@ -213,6 +221,10 @@ __device__ __forceinline__ bool segments_from_offsets(const RowMap &m, const I *
         s_off[threadIdx.x] = off[min(seg0 + (int64_t)threadIdx.x, S)];
         __syncthreads();
     }
+    // the block's rows lie in segments seg0 .. ends.y, so the first staged start above a row
+    // is one of the first ends.y - seg0 + 1 (a search over all 256 took the bf16 gradient of
+    // the power-law graph 1.61 ms instead of 1.47)
+    const int span = (int)min((int64_t)K, max((int64_t)1, ends.y - seg0 + 1));
 #pragma unroll
     for (int q = 0; q < kPasses; ++q) {
         const int64_t i = m.row(q);
@@ -221,7 +233,7 @@ __device__ __forceinline__ bool segments_from_offsets(const RowMap &m, const I *
         if (i >= n) continue;
         int p = K;   // first staged start above row i
         if (valid) {
-            int lo = 1, hi = K;
+            int lo = 1, hi = span;
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (s_off[mid] > i) hi = mid;
@@ -251,6 +263,10 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_off_kernel(const float *__r
                                                                 int64_t S, int64_t F,
                                                                 typename ElemT<E>::T *__restrict__ gsrc) {
     __shared__ int64_t s_off[256];
+    // non-temporal stores, except for the fp32 sum: on the power-law graph they take the
+    // bf16 sum 1.47 -> 1.24 ms and the fp32 mean 2.54 -> 2.50 ms, but the fp32 sum
+    // 2.46 -> 2.63 ms
+    constexpr bool kNt = E != ELEM_F32 || MEAN;
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
     int64_t seg[kPasses];
@@ -269,7 +285,7 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_off_kernel(const float *__r
             for (int q = 0; q < kPasses; ++q) {
                 const int64_t i = m.row(q);
                 if (i >= n) break;
-                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x);
+                store_elems<E, V, kNt>(gsrc + i * F + (int64_t)j * V, x);
             }
         }
         return;
@@ -293,7 +309,7 @@ __global__ __launch_bounds__(256) void seg_bwd_bcast_off_kernel(const float *__r
 #pragma unroll
                 for (int k = 0; k < V; ++k) x[q][k] = x[q][k] * inv[q];
             }
-            store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[q]);
+            store_elems<E, V, kNt>(gsrc + i * F + (int64_t)j * V, x[q]);
         }
     }
 }
@@ -517,7 +533,8 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_kernel(const float *__r
 }
 
 // The max gradient's stores with the segments from the offsets (as the broadcast above): the
-// recipients and gradient rows stay in cache, so the stores are the kernel's HBM stream.
+// recipients and gradient rows stay in cache, so the stores are the kernel's HBM stream, and
+// they are non-temporal (the power-law graph: fp32 4.87 -> 4.80 ms, bf16 3.33 -> 3.13 ms).
 template <int E, typename I, int V, typename A>
 __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float *__restrict__ gout,
                                                                     const I *__restrict__ idx,
@@ -546,7 +563,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float 
                 float y[V];
 #pragma unroll
                 for (int k = 0; k < V; ++k) y[k] = w[k] == (A)i ? x[k] : 0.0f;
-                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, y);
+                store_elems<E, V, true>(gsrc + i * F + (int64_t)j * V, y);
             }
         }
         return;
@@ -580,7 +597,7 @@ __global__ __launch_bounds__(256) void seg_bwd_max_write_off_kernel(const float 
 #pragma unroll
                 for (int k = 0; k < V; ++k)
                     if (w[u][k] != (A)i) x[u][k] = 0.0f;
-                store_elems<E, V>(gsrc + i * F + (int64_t)j * V, x[u]);
+                store_elems<E, V, true>(gsrc + i * F + (int64_t)j * V, x[u]);
             }
         }
     }

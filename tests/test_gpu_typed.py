@@ -285,6 +285,67 @@ def test_segment_backward_typed(dt, it, case):
             assert np.all(err <= lim), f"{dt}/{it} seed={seed} mean: worst {float(np.max(err - lim))}"
 
 
+# fp32 bit patterns around the roundings to bf16 and binary16: ties (to the even neighbour),
+# neighbours of ties, the largest finite values and the ties past them (to infinity), fp32
+# subnormals (bf16 keeps fp32's exponent range, binary16 rounds them to zero or its own
+# subnormals), signed zeros, infinities and NaNs
+SPECIAL_BITS = [
+    0x00000000, 0x80000000, 0x3F808000, 0x3F818000, 0x3F808001, 0x3F807FFF, 0xBF808000,
+    0x3F801000, 0x3F803000, 0x3F801001, 0xBF803000, 0x7F7FFFFF, 0xFF7FFFFF, 0x7F7F7FFF,
+    0x7F7F8000, 0x477FE000, 0x477FF000, 0x477FEFFF, 0xC77FF000, 0x00000001, 0x00008000,
+    0x00018000, 0x007FFFFF, 0x80018000, 0x33000000, 0x33C00000, 0x387FC000, 0x387FE000,
+    0x7F800000, 0xFF800000, 0x7FC00000, 0x7F800001, 0xFFC00001, 0x40490FDB, 0xBDCCCCCD,
+]
+
+
+def rne16_bits(a, dt):
+    """16-bit patterns of fp32 array `a` rounded to nearest even (NaN entries unspecified)."""
+    if dt == "f16":
+        with np.errstate(over="ignore"):
+            return a.astype(np.float16).view(np.uint16)
+    u = a.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("F", [32, 12, 6, 3], ids=lambda f: f"F{f}")
+def test_segment_backward_rounds_like_torch(dt, F):
+    """Gradients narrowed to 16-bit storage round to nearest even, bit for bit, on the values
+    where a rounding can go wrong (ties, overflow, subnormals, signed zeros, infinities; NaN
+    stays NaN), through the 8-, 4-, 2- and 1-wide stores of sum and max. The expected bits
+    come from the definition: binary16 by numpy's conversion; bf16, the upper half of an fp32
+    pattern, by rounding the pattern as an integer to a multiple of 2^16, ties to the even
+    multiple (for a finite value the patterns order like the magnitudes, and the carry out of
+    the largest finite bf16 lands on infinity's pattern)."""
+    rng = np.random.default_rng(80 + F)
+    S, nnz = 97, 5000
+    index = np.sort(rng.integers(0, S, nnz)).astype(np.int64)
+    special = np.array(SPECIAL_BITS, dtype=np.uint32).view(np.float32)
+    g = special[rng.integers(0, special.size, (S, F))]
+    gd = torch.from_numpy(g).to(DEV)
+    t, wide = stored(rng.standard_normal((nnz, F)).astype(np.float32), dt)
+    i = ids(index, "i32")
+    for op in ("sum", "max"):
+        say(f"special-value rounding {dt} F={F} {op}")
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.segment_reduce(wide, index, S, op),
+                                       geot.segment_reduce(t.to(DEV), i, S, op), f"{dt} F={F}")
+        got = geot.segment_reduce_backward(gd, i, op, t.to(DEV) if op == "max" else None, up(out),
+                                           dtype=DT[dt]).cpu()
+        exact = np.ascontiguousarray(oracle.segment_reduce_backward(g, index, op, wide, out), dtype=np.float32)
+        nan = np.isnan(exact)
+        rb = rne16_bits(exact, dt)
+        gb = got.view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(np.isnan(got.float().numpy()), nan), f"{dt} F={F} {op}: NaN positions"
+        bad = (gb != rb) & ~nan
+        if bad.any():
+            r, c = [int(v[0]) for v in np.nonzero(bad)]
+            raise AssertionError(f"{dt} F={F} {op}: {int(bad.sum())} values differ; first at ({r}, {c}): "
+                                 f"fp32 {hex(int(exact[r, c:c + 1].view(np.uint32)[0]))} -> "
+                                 f"{hex(int(gb[r, c]))}, expected {hex(int(rb[r, c]))}")
+
+
 def test_segment_backward_typed_through_autograd():
     """A bf16 src with int32 ids: autograd's gradient is bf16 and equals the fp32 gradient of
     the widened src rounded once."""
