@@ -110,6 +110,41 @@ def test_segment_backward_from_offsets(case):
             assert np.array_equal(got, ref), f"{op} seed={seed}"
 
 
+@pytest.mark.parametrize("dt", [torch.bfloat16, torch.float16], ids=["bf16", "f16"])
+@pytest.mark.parametrize("case", [(9, "tiny_then_long", 32), (12, "wide", 300)],
+                         ids=lambda c: f"seed{c[0]}-{c[1]}")
+def test_segment_backward_from_offsets_16bit(case, dt):
+    """The same from 16-bit storage with int32 ids (8-element vectors and 256 rows a block at
+    F = 32; 4-element vectors and 16 rows at F = 300; the gradient stored non-temporally in
+    src's type): sum and max are the oracle's gradient
+    rounded once to the type (torch rounds to nearest even, as the library does), mean is
+    within half a unit in the last place (plus the fp32 bound) of the exact quotient. The
+    integer source values are exact in both types."""
+    src, idx, S, F = _offsets_case(case)
+    seed = case[0]
+    assert src.size * 2 >= (64 << 20) and idx.size >> {32: 8, 300: 4}[F] >= S
+    s16 = up(src).to(dt)
+    i32 = up(idx).to(torch.int32)
+    g = np.random.default_rng(seed).standard_normal((S, F)).astype(np.float32)
+    half_ulp = 2.0 ** -8 if dt == torch.bfloat16 else 2.0 ** -11
+    for op in ("sum", "mean", "max"):
+        say(f"16-bit segment backward from offsets seed={seed} {case[1]} {dt} {op}")
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.segment_reduce(src, idx, S, op),
+                                       geot.segment_reduce(s16, i32, S, op), f"seed={seed} {dt}")
+        got = geot.segment_reduce_backward(up(g), i32, op, s16 if out is not None else None, up(out),
+                                           dtype=dt).cpu()
+        assert got.dtype == dt
+        ref = oracle.segment_reduce_backward(g, idx, op, src, out)
+        if op == "mean":
+            r = np.abs(ref.astype(np.float64))
+            err = np.abs(got.float().numpy().astype(np.float64) - ref.astype(np.float64))
+            assert np.all(err <= (half_ulp + 1e-6) * r + 2.0 ** -25), f"mean seed={seed} {dt}"
+        else:
+            assert torch.equal(got, torch.from_numpy(np.ascontiguousarray(ref)).to(dt)), f"{op} seed={seed} {dt}"
+
+
 GS_CASES = [
     (11, 20000, 1200, 900, 32, "zipf", "normal", True),
     (12, 15000, 800, 2000, 3, "lognormal", "normal", True),
