@@ -31,16 +31,21 @@ def gcn_norm(row, col, n):
     return (1.0 / np.sqrt(np.maximum(deg[row], 1) * np.maximum(deg[col], 1))).astype(np.float32)
 
 
-@pytest.mark.parametrize("reduce,cached,n,nnz", [("sum", False, 3000, 40000), ("mean", False, 3000, 40000),
-                                                 ("max", False, 3000, 40000), ("sum", True, 3000, 40000),
-                                                 ("mean", True, 3000, 40000), ("sum", False, 200_000, 1_500_000),
-                                                 ("sum", True, 200_000, 1_500_000),
-                                                 ("max", False, 200_000, 1_500_000)])
-def test_two_layer_training_step(reduce, cached, n, nnz):
+@pytest.mark.parametrize("reduce,cached,n,nnz,F", [("sum", False, 3000, 40000, 24), ("mean", False, 3000, 40000, 24),
+                                                   ("max", False, 3000, 40000, 24), ("sum", True, 3000, 40000, 24),
+                                                   ("mean", True, 3000, 40000, 24),
+                                                   ("sum", False, 200_000, 1_500_000, 24),
+                                                   ("sum", True, 200_000, 1_500_000, 24),
+                                                   ("max", False, 200_000, 1_500_000, 24),
+                                                   ("sum", True, 3000, 40000, 32), ("mean", False, 3000, 40000, 32),
+                                                   ("sum", False, 3000, 40000, 60)])
+def test_two_layer_training_step(reduce, cached, n, nnz, F):
     """cached: the layers take a Graph, whose transposed edge list serves the gradient. The
     graphs of 1,500,000 edges take the radix transposition (in the Graph's list and inside
-    the gradient calls) and the recording max's gradients from recipients."""
-    F, H, C = 24, 32, 5
+    the gradient calls) and the recording max's gradients from recipients. The first layer
+    aggregates before its transform (its input needs no gradient) at 24 -> 32 and 32 -> 32,
+    and after it at 60 -> 32."""
+    H, C = 32, 5
     q = random_gather_problem(301, nnz, n, n, F, "zipf", "normal", True, 0.0)
     row, col, X = q["index"], q["col"], q["X"]
     w = gcn_norm(row, col, n) if reduce == "sum" else None
