@@ -1254,6 +1254,61 @@ template <> struct RxRec<4> {
     static __device__ __forceinline__ T make(int c, int r, int coef, int e) { return make_int4(c, r, coef, e); }
 };
 
+// Ids per lane load in the radix passes: a 16-byte load (4 int32 or 2 int64 ids) where the
+// arrays are 16-byte aligned (VEC), else 1. One 4-byte id per lane and load held the int32
+// passes below the int64 ones on the SpMM graph (count 140 against 105 us, grouping 540
+// against 425 us) although they read half the bytes.
+template <typename I, bool VEC>
+constexpr int rx_ids_per_load() {
+    return VEC ? 16 / (int)sizeof(I) : 1;
+}
+
+// VL consecutive ids p[e .. e + VL) widened to int64, -1 at and past `end`
+template <typename I, int VL>
+__device__ __forceinline__ void rx_load_ids(const I *p, int64_t e, int64_t end, int64_t *c) {
+    if constexpr (VL == 4) {
+        if (e + 4 <= end) {
+            const int4 t = *reinterpret_cast<const int4 *>(p + e);
+            c[0] = t.x;
+            c[1] = t.y;
+            c[2] = t.z;
+            c[3] = t.w;
+            return;
+        }
+    } else if constexpr (VL == 2) {
+        if (e + 2 <= end) {
+            const longlong2 t = *reinterpret_cast<const longlong2 *>(p + e);
+            c[0] = t.x;
+            c[1] = t.y;
+            return;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VL; ++k) c[k] = e + k < end ? (int64_t)p[e + k] : -1;
+}
+
+// VL consecutive weights w[e ..] (1 where w is NULL or at and past `end`)
+template <int VL>
+__device__ __forceinline__ void rx_load_w(const float *w, int64_t e, int64_t end, float *x) {
+    if (w && e + VL <= end) {
+        if constexpr (VL == 4) {
+            const float4 t = *reinterpret_cast<const float4 *>(w + e);
+            x[0] = t.x;
+            x[1] = t.y;
+            x[2] = t.z;
+            x[3] = t.w;
+            return;
+        } else if constexpr (VL == 2) {
+            const float2 t = *reinterpret_cast<const float2 *>(w + e);
+            x[0] = t.x;
+            x[1] = t.y;
+            return;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < VL; ++k) x[k] = w && e + k < end ? w[e + k] : 1.0f;
+}
+
 // exclusive scan of one value per thread over a block of 1024 threads; *total gets the sum.
 // Every thread of the block must call it (two barriers).
 __device__ __forceinline__ unsigned block_excl_scan(unsigned v, unsigned *s_wave, unsigned *total) {
@@ -1297,10 +1352,11 @@ __device__ __forceinline__ unsigned lds_claim(unsigned *h, unsigned key, bool va
 
 // per block, the edges of its chunk per bin, cnt[block * nbins + bin], and per coarse bucket,
 // cc[block * 256 + k]
-template <typename I>
+template <typename I, bool VEC>
 __global__ __launch_bounds__(1024) void rx_count_kernel(const I *col, int64_t n, int64_t nx, int shift, int nbins,
                                                         int b2, int64_t chunk, unsigned *cnt, unsigned *cc) {
-    constexpr int kU = 16;  // loads in flight per thread
+    constexpr int kU = 16;  // ids in flight per thread
+    constexpr int VL = rx_ids_per_load<I, VEC>();
     __shared__ unsigned h[kRxMaxBins];
     for (int b = threadIdx.x; b < nbins; b += 1024) h[b] = 0;
     __syncthreads();
@@ -1309,10 +1365,8 @@ __global__ __launch_bounds__(1024) void rx_count_kernel(const I *col, int64_t n,
     for (int64_t b0 = e0; b0 < e1; b0 += kU * 1024) {
         int64_t c[kU];
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int64_t e = b0 + u * 1024 + threadIdx.x;
-            c[u] = e < e1 ? (int64_t)col[e] : -1;
-        }
+        for (int u = 0; u < kU / VL; ++u)
+            rx_load_ids<I, VL>(col, b0 + ((int64_t)u * 1024 + threadIdx.x) * VL, e1, c + u * VL);
 #pragma unroll
         for (int u = 0; u < kU; ++u)
             if ((uint64_t)c[u] < (uint64_t)nx) atomicAdd(&h[(int)(c[u] >> shift)], 1u);
@@ -1407,7 +1461,7 @@ __global__ __launch_bounds__(256) void rx_cursor_kernel(const unsigned *cc, int6
 // tiles, which run at the same time, write neighbouring runs (blocks of different chunks side
 // by side measured slower: 538 against 481 us). The cursor atomics are issued before the
 // records are staged and waited for after.
-template <typename I, int W>
+template <typename I, int W, bool VEC>
 __global__ __launch_bounds__(1024) void rx_group_kernel(const I *col, int64_t nx, const I *row, const float *w,
                                                         const int64_t *roff, int64_t nrows, int mean, int64_t n,
                                                         int shift, int b2, int64_t tpc, unsigned *ccur,
@@ -1422,15 +1476,17 @@ __global__ __launch_bounds__(1024) void rx_group_kernel(const I *col, int64_t nx
     const int64_t t0 = (int64_t)blockIdx.x * kRxTile;
     if (threadIdx.x < 256) s_cnt[threadIdx.x] = 0;
     __syncthreads();
+    constexpr int VL = rx_ids_per_load<I, VEC>();
+    // this thread's edges: VL consecutive ones per load, u-th load at t0 + (u * 1024 + tid) * VL
+    auto edge = [&](int u) { return t0 + ((int64_t)(u / VL) * 1024 + threadIdx.x) * VL + u % VL; };
     int64_t c[kRxU], r[kRxU];
     float wt[kRxU];
 #pragma unroll
-    for (int u = 0; u < kRxU; ++u) {
-        const int64_t e = t0 + u * 1024 + threadIdx.x;
-        const bool in = e < n;
-        c[u] = in ? (int64_t)col[e] : -1;
-        r[u] = in ? (int64_t)row[e] : 0;
-        wt[u] = in && w ? w[e] : 1.0f;
+    for (int u = 0; u < kRxU; u += VL) {
+        const int64_t e = edge(u);
+        rx_load_ids<I, VL>(col, e, n, c + u);
+        rx_load_ids<I, VL>(row, e, n, r + u);
+        rx_load_w<VL>(w, e, n, wt + u);
     }
     unsigned rank[kRxU];
     int kb[kRxU];
@@ -1452,7 +1508,7 @@ __global__ __launch_bounds__(1024) void rx_group_kernel(const I *col, int64_t nx
     for (int u = 0; u < kRxU; ++u)
         if (kb[u] >= 0)
             s_rec[s_cnt[kb[u]] + rank[u]] = RxRec<W>::make((int)c[u], (int)r[u], __float_as_int(wt[u]),
-                                                           (int)(uint32_t)(t0 + u * 1024 + threadIdx.x));
+                                                           (int)(uint32_t)edge(u));
     if (threadIdx.x < 256) s_base[threadIdx.x] = gb;
     __syncthreads();
     for (unsigned i = threadIdx.x; i < m; i += 1024) {
@@ -1772,8 +1828,14 @@ hipError_t launch_transpose_radix(const RxPlan &p, const I *col, int64_t nx, con
     const int ncoarse = ((p.nbins - 1) >> p.b2) + 1;
     if (p.nblk > 256 || p.chunk % kRxTile != 0 || stiles > 0x7fffffffLL || p.nbins > kRxMaxBins || ncoarse > 256)
         return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(rx_count_kernel<I>, dim3((unsigned)p.nblk), dim3(1024), 0, st, col, n, nx, p.shift, p.nbins,
-                       p.b2, p.chunk, cnt, cc);
+    // 16-byte id (and weight) loads where every array is 16-byte aligned
+    const bool vec = (((uintptr_t)col | (uintptr_t)row | (uintptr_t)w) & 15) == 0;
+    if (vec)
+        hipLaunchKernelGGL((rx_count_kernel<I, true>), dim3((unsigned)p.nblk), dim3(1024), 0, st, col, n, nx, p.shift,
+                           p.nbins, p.b2, p.chunk, cnt, cc);
+    else
+        hipLaunchKernelGGL((rx_count_kernel<I, false>), dim3((unsigned)p.nblk), dim3(1024), 0, st, col, n, nx, p.shift,
+                           p.nbins, p.b2, p.chunk, cnt, cc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(rx_reduce_kernel, dim3((unsigned)((p.nbins + 63) / 64)), dim3(256), 0, st, cnt, p.nblk,
@@ -1783,8 +1845,12 @@ hipError_t launch_transpose_radix(const RxPlan &p, const I *col, int64_t nx, con
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(rx_cursor_kernel, dim3((unsigned)ncoarse), dim3(256), 0, st, cc, p.nblk, start, p.b2, ccur);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((rx_group_kernel<I, W>), dim3((unsigned)tiles), dim3(1024), 0, st, col, nx, row, w, roff,
-                       nrows, mean ? 1 : 0, n, p.shift, p.b2, p.chunk / kRxTile, ccur, p.b2 > 0 ? r4 : tmp);
+    if (vec)
+        hipLaunchKernelGGL((rx_group_kernel<I, W, true>), dim3((unsigned)tiles), dim3(1024), 0, st, col, nx, row, w,
+                           roff, nrows, mean ? 1 : 0, n, p.shift, p.b2, p.chunk / kRxTile, ccur, p.b2 > 0 ? r4 : tmp);
+    else
+        hipLaunchKernelGGL((rx_group_kernel<I, W, false>), dim3((unsigned)tiles), dim3(1024), 0, st, col, nx, row, w,
+                           roff, nrows, mean ? 1 : 0, n, p.shift, p.b2, p.chunk / kRxTile, ccur, p.b2 > 0 ? r4 : tmp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (p.b2 > 0) {
         hipLaunchKernelGGL(rx_split_kernel<W>, dim3((unsigned)stiles), dim3(1024), 0, st, r4, start, p.nbins,

@@ -316,6 +316,51 @@ def test_transpose_edges_radix(nx, hub):
         within(gx.cpu().numpy(), rx, tx, f"radix grad_X nx={nx} hub={hub} {op}")
 
 
+@pytest.mark.parametrize("it", ["i64", "i32"])
+@pytest.mark.parametrize("aligned", [True, False], ids=["aligned", "offset"])
+def test_radix_id_loads(it, aligned):
+    """The radix passes load 4 int32 or 2 int64 ids (and weights) per lane where col, row and
+    the weights are 16-byte aligned, else one at a time: a ragged edge count (1,300,003: the
+    last tile and the last counting block end inside a vector), int32 and int64 ids, arrays
+    that start at element 0 of their buffers or one element in. The gradients w.r.t. X of sum
+    and mean, and of max with w.r.t. the weights (the max pull reads the edge numbers the
+    grouping pass records), against the oracle; with int64 ids also geot_transpose_edges."""
+    n, R, nx, F = 1_300_003, 150_000, 400_000, 4
+    rng = np.random.default_rng(53)
+    row = np.sort(rng.integers(0, R, n)).astype(np.int64)
+    col = rng.integers(0, nx, n).astype(np.int64)
+    col[rng.random(n) < 0.05] = 777    # a column of about 65,000 edges
+    w = rng.random(n, dtype=np.float32)
+    dt = {"i64": torch.int64, "i32": torch.int32}[it]
+
+    def dev(a, t):
+        k = 0 if aligned else 1
+        buf = torch.empty(a.size + 1, dtype=t, device=DEV)
+        v = buf[k:k + a.size]
+        v.copy_(torch.from_numpy(a).to(t))
+        assert (v.data_ptr() % 16 == 0) == aligned
+        return v
+
+    cd, rd, wd = dev(col, dt), dev(row, dt), dev(w, torch.float32)
+    X = rng.standard_normal((nx, F)).astype(np.float32)
+    g = rng.standard_normal((R, F)).astype(np.float32)
+    for op in ("sum", "mean", "max"):
+        say(f"radix id loads {it} aligned={aligned} {op}")
+        out = None
+        if op == "max":
+            out = forward_for_gradient(oracle.gather_scatter(X, col, w, row, R, op),
+                                       geot.gather_scatter(up(X), cd, wd, rd, R, op), f"{it} aligned={aligned}")
+        gx, gw = geot.gather_scatter_backward(up(X), cd, wd, rd, up(g), op, up(out), need_weight=op == "max")
+        rx, rw = oracle.gather_scatter_backward(X, col, w, row, g, op, out)
+        tx, tw = oracle.gather_scatter_backward(X, col, w, row, g, op, out, absolute=True)
+        within(gx.cpu().numpy(), rx, tx, f"radix id loads grad_X {it} aligned={aligned} {op}")
+        if op == "max":
+            within(gw.cpu().numpy(), rw, tw, f"radix id loads grad_w {it} aligned={aligned}")
+        if it == "i64" and op != "max":
+            sc, rt, cf = (t.cpu().numpy() for t in geot.transpose_edges(cd, wd, rd, nx, R, op))
+            same_triples(sc, rt, cf, col, row, w if op == "sum" else mean_coef(w, row, R))
+
+
 def test_transpose_edges_sparse_tail():
     """3,000,000 edges over 2^23 columns, 99.9 % of them in the first 2^20 columns: the tail's
     coarse buckets hold a few records each, so a splitting tile there spans more bins than its
