@@ -930,7 +930,9 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
 }
 
 // fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
-// mean divides afterwards, in scale_by_count_kernel). A row group takes P consecutive edges
+// mean divides afterwards, in scale_by_count_kernel). This kernel serves max, and sum and mean
+// where a row takes fewer than 8 threads or more than 64 vectors (gs_bwd_w_run_kernel below
+// takes the others). A row group takes P consecutive edges
 // (rows are sorted, so they mostly share their grad_out row); every thread runs all of them (the
 // group reduction is uniform). The edges' ids load first, then every edge's X row and, once per
 // run of edges with the same row, the grad_out row (and for max its recipients), then the
@@ -1082,6 +1084,90 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
         if (e < n && m.j0 == 0) {
             gw[e] = ok[q] ? a : 0.0f;
         }
+    }
+}
+
+// fused form, sum, w.r.t. the weights, where a row's vectors take 8 to 64 threads (one vector
+// each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
+// load, and each row group (tpr threads) walks tpr of them in batches of kB = 4, loading the
+// grad_out row once per run of edges with the same row. A batch's four dot products are
+// reduced together: across the group's highest lane bit each lane keeps two of the four sums
+// and trades the other two, across the next bit one, and a butterfly over the remaining bits
+// completes it, so that 6 shuffles at tpr = 32 (instead of 4 x 5) leave edge q's sum in the
+// lanes whose two highest group bits read q, one of which stores it.
+template <int E, typename I, int V>
+__global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
+                                                           const I *__restrict__ col, const I *__restrict__ row,
+                                                           const float *__restrict__ gout, int64_t n, int64_t R,
+                                                           int64_t F, float *__restrict__ gw) {
+    constexpr int kB = 4;
+    __shared__ int64_t s_c[256], s_r[256];
+    const int nvec = (int)(F / V);
+    int tpr = 1;
+    while (tpr < nvec && tpr < 64) tpr <<= 1;   // 8 .. 64: the launch checks
+    const int gl = threadIdx.x & (tpr - 1);     // lane within the row group
+    const int base = threadIdx.x - gl;          // the group's first edge within the block
+    const int64_t b0 = (int64_t)blockIdx.x * 256;
+    {
+        const int64_t e = b0 + threadIdx.x;
+        s_c[threadIdx.x] = e < n ? (int64_t)col[e] : -1;
+        s_r[threadIdx.x] = e < n ? (int64_t)row[e] : -1;
+    }
+    __syncthreads();
+    const bool lane = gl < nvec;
+    const int hi = tpr >> 1, q2 = tpr >> 2;     // the two highest lane bits of the group
+    const bool bh = (gl & hi) != 0, bq = (gl & q2) != 0;
+    int64_t prev = -1;                           // the row whose grad_out vector `cur` holds
+    float cur[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) cur[k] = 0.0f;
+    for (int j0 = 0; j0 < tpr; j0 += kB) {
+        int64_t rr[kB];
+        bool ok[kB], lead[kB];
+        Raw<E, V> rx[kB];
+        float g[kB][V];
+#pragma unroll
+        for (int q = 0; q < kB; ++q) {
+            const int64_t c = s_c[base + j0 + q];
+            rr[q] = s_r[base + j0 + q];
+            ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)c < (uint64_t)nx;
+            lead[q] = rr[q] != (q > 0 ? rr[q - 1] : prev);
+            if (ok[q] && lane) load_raw<E, V>(X + c * F + (int64_t)gl * V, rx[q]);
+            else rx[q] = Raw<E, V>{};
+            // a new row loads its grad_out vector whether or not this edge's column is valid,
+            // since the next edges of the run use it
+            if (lead[q] && lane && (uint64_t)rr[q] < (uint64_t)R) {
+                load_f32<V>(gout + rr[q] * F + (int64_t)gl * V, g[q]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < V; ++k) g[q][k] = 0.0f;
+            }
+        }
+        float a[kB];
+#pragma unroll
+        for (int q = 0; q < kB; ++q) {
+            if (lead[q]) {
+#pragma unroll
+                for (int k = 0; k < V; ++k) cur[k] = g[q][k];
+            }
+            float x[V];
+            widen<E, V>(rx[q], x);
+            a[q] = 0.0f;
+#pragma unroll
+            for (int k = 0; k < V; ++k) a[q] += cur[k] * x[k];
+        }
+        prev = rr[kB - 1];
+        // keep sums {0, 1} (highest bit clear) or {2, 3}, trade the others
+        const float s0 = __shfl_xor(bh ? a[0] : a[2], hi, 64);
+        const float s1 = __shfl_xor(bh ? a[1] : a[3], hi, 64);
+        const float k0 = (bh ? a[2] : a[0]) + s0;
+        const float k1 = (bh ? a[3] : a[1]) + s1;
+        // keep one of the two by the next bit
+        float v = (bq ? k1 : k0) + __shfl_xor(bq ? k0 : k1, q2, 64);
+        for (int d = q2 >> 1; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+        const int q = (bh ? 2 : 0) + (bq ? 1 : 0);
+        const int64_t e = b0 + base + j0 + q;
+        if ((gl & (q2 - 1)) == 0 && e < n) gw[e] = ok[q] ? v : 0.0f;
     }
 }
 
@@ -2132,9 +2218,13 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 constexpr int WP = VV == 8 ? kWPasses8 : kPasses;
                 const int64_t gwb = grid_rows(n, (int)(F / VV), WP);
                 if (gwb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+                const int tpr = row_threads((int)(F / VV));
                 if (op == GEOT_BWD_MAX)
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
+                else if (tpr >= 8 && F / VV <= 64)
+                    hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                                       st, Xt, nx, ct, rt, gout, n, R, F, gw);
                 else
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
