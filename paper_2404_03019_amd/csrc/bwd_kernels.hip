@@ -1095,12 +1095,15 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
 // and trades the other two, across the next bit one, and a butterfly over the remaining bits
 // completes it, so that 6 shuffles at tpr = 32 (instead of 4 x 5) leave edge q's sum in the
 // lanes whose two highest group bits read q, one of which stores it.
-template <int E, typename I, int V>
+template <int E, typename I, int V, int OP, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                            const I *__restrict__ col, const I *__restrict__ row,
+                                                           const A *__restrict__ arg,
                                                            const float *__restrict__ gout, int64_t n, int64_t R,
                                                            int64_t F, float *__restrict__ gw) {
     constexpr int kB = 4;
+    constexpr bool MX = OP == GEOT_BWD_MAX;
+    static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
     __shared__ int64_t s_c[256], s_r[256];
     const int nvec = (int)(F / V);
     int tpr = 1;
@@ -1117,44 +1120,91 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
     const bool lane = gl < nvec;
     const int hi = tpr >> 1, q2 = tpr >> 2;     // the two highest lane bits of the group
     const bool bh = (gl & hi) != 0, bq = (gl & q2) != 0;
-    int64_t prev = -1;                           // the row whose grad_out vector `cur` holds
+    int64_t prev = -1;                           // the row whose vectors `cur` (and `ca`) hold
     float cur[V];
+    A ca[V];   // max: the recipient edges of the row's features (none: all ones)
 #pragma unroll
-    for (int k = 0; k < V; ++k) cur[k] = 0.0f;
+    for (int k = 0; k < V; ++k) {
+        cur[k] = 0.0f;
+        ca[k] = (A)~(A)0;
+    }
     for (int j0 = 0; j0 < tpr; j0 += kB) {
-        int64_t rr[kB];
+        int64_t rr[kB], cc[MX ? kB : 1];
         bool ok[kB], lead[kB];
-        Raw<E, V> rx[kB];
         float g[kB][V];
+        A ga[MX ? kB : 1][V];
+        Raw<E, V> rx[kB];
 #pragma unroll
         for (int q = 0; q < kB; ++q) {
             const int64_t c = s_c[base + j0 + q];
             rr[q] = s_r[base + j0 + q];
             ok[q] = (uint64_t)rr[q] < (uint64_t)R && (uint64_t)c < (uint64_t)nx;
             lead[q] = rr[q] != (q > 0 ? rr[q - 1] : prev);
-            if (ok[q] && lane) load_raw<E, V>(X + c * F + (int64_t)gl * V, rx[q]);
-            else rx[q] = Raw<E, V>{};
-            // a new row loads its grad_out vector whether or not this edge's column is valid,
-            // since the next edges of the run use it
+            if constexpr (MX) {
+                cc[q] = c;
+            } else {   // sum: every edge's X vector loads at once
+                if (ok[q] && lane) load_raw<E, V>(X + c * F + (int64_t)gl * V, rx[q]);
+                else rx[q] = Raw<E, V>{};
+            }
+            // a new row loads its vectors whether or not this edge's column is valid, since the
+            // next edges of the run use them
             if (lead[q] && lane && (uint64_t)rr[q] < (uint64_t)R) {
                 load_f32<V>(gout + rr[q] * F + (int64_t)gl * V, g[q]);
+                if constexpr (MX) load_arg<A, V>(arg + rr[q] * F + (int64_t)gl * V, ga[q]);
             } else {
 #pragma unroll
-                for (int k = 0; k < V; ++k) g[q][k] = 0.0f;
+                for (int k = 0; k < V; ++k) {
+                    g[q][k] = 0.0f;
+                    if constexpr (MX) ga[q][k] = (A)~(A)0;
+                }
             }
         }
         float a[kB];
+        if constexpr (!MX) {
+            // sum: the products with each edge's run's row
 #pragma unroll
-        for (int q = 0; q < kB; ++q) {
-            if (lead[q]) {
+            for (int q = 0; q < kB; ++q) {
+                if (lead[q]) {
 #pragma unroll
-                for (int k = 0; k < V; ++k) cur[k] = g[q][k];
+                    for (int k = 0; k < V; ++k) cur[k] = g[q][k];
+                }
+                float x[V];
+                widen<E, V>(rx[q], x);
+                a[q] = 0.0f;
+#pragma unroll
+                for (int k = 0; k < V; ++k) a[q] += cur[k] * x[k];
             }
-            float x[V];
-            widen<E, V>(rx[q], x);
-            a[q] = 0.0f;
+        } else {
+            // max: an edge's X vector loads only where the edge receives one of this thread's
+            // features (bit k of mine), so the recipients come first
+            unsigned mine[kB];
 #pragma unroll
-            for (int k = 0; k < V; ++k) a[q] += cur[k] * x[k];
+            for (int q = 0; q < kB; ++q) {
+                if (lead[q]) {
+#pragma unroll
+                    for (int k = 0; k < V; ++k) {
+                        cur[k] = g[q][k];
+                        ca[k] = ga[q][k];
+                    }
+                }
+                mine[q] = 0u;
+#pragma unroll
+                for (int k = 0; k < V; ++k) {
+                    g[q][k] = cur[k];   // from here on: this edge's grad_out values
+                    mine[q] |= (ca[k] == (A)(b0 + base + j0 + q) ? 1u : 0u) << k;
+                }
+                if (ok[q] && lane && mine[q]) load_raw<E, V>(X + cc[q] * F + (int64_t)gl * V, rx[q]);
+                else rx[q] = Raw<E, V>{};
+            }
+#pragma unroll
+            for (int q = 0; q < kB; ++q) {
+                float x[V];
+                widen<E, V>(rx[q], x);
+                a[q] = 0.0f;
+                // a selected product, not a product by 0 (another feature's value may be inf or NaN)
+#pragma unroll
+                for (int k = 0; k < V; ++k) a[q] += (mine[q] >> k) & 1u ? g[q][k] * x[k] : 0.0f;
+            }
         }
         prev = rr[kB - 1];
         // keep sums {0, 1} (highest bit clear) or {2, 3}, trade the others
@@ -2219,12 +2269,16 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 const int64_t gwb = grid_rows(n, (int)(F / VV), WP);
                 if (gwb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
                 const int tpr = row_threads((int)(F / VV));
-                if (op == GEOT_BWD_MAX)
+                const bool runs = tpr >= 8 && F / VV <= 64;
+                if (op == GEOT_BWD_MAX && runs)
+                    hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_MAX, A>), dim3((unsigned)((n + 255) / 256)),
+                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
+                else if (op == GEOT_BWD_MAX)
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
-                else if (tpr >= 8 && F / VV <= 64)
-                    hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                                       st, Xt, nx, ct, rt, gout, n, R, F, gw);
+                else if (runs)
+                    hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_SUM, A>), dim3((unsigned)((n + 255) / 256)),
+                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
                 else
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
