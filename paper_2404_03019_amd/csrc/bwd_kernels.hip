@@ -861,16 +861,90 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
                                                                 const float *__restrict__ gout, int64_t nx, int64_t R,
                                                                 int64_t F, float *__restrict__ gX) {
     constexpr int kU = 4;
+    // the column's terms add into `run`, which joins acc every kPullRun records, so a hub
+    // column's long chain rounds like short runs (the fp32 bound holds)
+    constexpr int kPullRun = 256;
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec);
+    if (nvec <= m.tpr && m.tpr >= kU) {
+        // One vector per thread: the group loads up to tpr records of its column at once (lane i
+        // the i-th: one coalesced load instead of one broadcast load per record) and hands them
+        // out by lane shuffles, so a batch waits only for its recipients and grad_out rows. The
+        // batches are the same runs of kU records as below, so the sums are the same.
+        const int4 *rec4 = reinterpret_cast<const int4 *>(rec);
+        const int gb = (int)(threadIdx.x & 63) - m.j0;   // the group's first lane in the wave
+        const bool lane = m.j0 < nvec;
+        for (int q = 0; q < kPasses; ++q) {
+            const int64_t c = m.row(q);
+            if (c >= nx) break;   // the same for the whole group
+            const int64_t lo = off[c], hi = off[c + 1];
+            float acc[V], run[V];
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[k] = run[k] = 0.0f;
+            int steps = 0;
+            for (int64_t k0 = lo; k0 < hi; k0 += m.tpr) {
+                const int4 mine = k0 + m.j0 < hi ? rec4[k0 + m.j0] : make_int4(0, -1, 0, 0);
+                const int cnt = (int)min((int64_t)m.tpr, hi - k0);
+                for (int u0 = 0; u0 < cnt; u0 += kU) {
+                    int r[kU];
+                    unsigned ed[kU];
+                    float coef[kU];
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {   // u0 + u < tpr: past the column, the sentinel
+                        const int src = gb + u0 + u;
+                        r[u] = __shfl(mine.y, src, 64);
+                        coef[u] = __int_as_float(__shfl(mine.z, src, 64));
+                        ed[u] = (unsigned)__shfl(mine.w, src, 64);
+                    }
+                    unsigned a[kU][V];
+                    float g[kU][V];
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        if (lane && (uint64_t)(int64_t)r[u] < (uint64_t)R) {
+                            load_arg<unsigned, V>(arg + (int64_t)r[u] * F + (int64_t)m.j0 * V, a[u]);
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < V; ++k) a[u][k] = ~0u;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < kU; ++u) {
+                        bool any = false;
+#pragma unroll
+                        for (int k = 0; k < V; ++k) any |= a[u][k] == ed[u];
+                        if (any) {
+                            load_f32<V>(gout + (int64_t)r[u] * F + (int64_t)m.j0 * V, g[u]);
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < V; ++k) g[u][k] = 0.0f;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < kU; ++u)
+#pragma unroll
+                        for (int k = 0; k < V; ++k)
+                            if (a[u][k] == ed[u]) run[k] += coef[u] * g[u][k];
+                    if (++steps == kPullRun / kU) {
+#pragma unroll
+                        for (int k = 0; k < V; ++k) {
+                            acc[k] += run[k];
+                            run[k] = 0.0f;
+                        }
+                        steps = 0;
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < V; ++k) acc[k] += run[k];
+            if (lane) store_vec<V>(gX + c * F + (int64_t)m.j0 * V, acc);
+        }
+        return;
+    }
     for (int q = 0; q < kPasses; ++q) {
         const int64_t c = m.row(q);
         if (c >= nx) break;
         const int64_t lo = off[c], hi = off[c + 1];
         for (int j = m.j0; j < nvec; j += m.tpr) {
-            // the column's terms add into `run`, which joins acc every kPullRun records, so a
-            // hub column's long chain rounds like short runs (the fp32 bound holds)
-            constexpr int kPullRun = 256;
             float acc[V], run[V];
 #pragma unroll
             for (int k = 0; k < V; ++k) acc[k] = run[k] = 0.0f;
