@@ -772,7 +772,8 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_kernel(const A *__restrict__
 // edge). No LDS table and no barrier: the slot-table kernel above ran 3.9 M blocks of 16 edges
 // on the SpMM graph. For one vector per thread (nvec <= 64); X rows of kArgBatch edges load
 // together. (Loading the next batch's ids beside them held 83 VGPRs instead of 67, 5 waves per
-// SIMD instead of 7, and measured the same on the SpMM graph: 6.65 ms.)
+// SIMD instead of 7, and measured the same on the SpMM graph: 6.65 ms; the run's ids loaded by
+// the group together and handed out by shuffles took the whole max gradient 15.0 -> 14.65 ms.)
 constexpr int kArgRun = 32;
 constexpr int kArgBatch = 4;
 template <int E, typename I, int V, typename A>
@@ -784,9 +785,12 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_run_kernel(const typename 
                                                                  int64_t F, A *arg) {
     const int nvec = (int)(F / V);
     const RowMap m = row_map(nvec, 1);
-    if (m.j0 >= nvec) return;   // no barrier below
+    // a group of at least kArgRun threads loads its run's ids together (below)
+    const bool coop = m.tpr >= kArgRun;
+    if (!coop && m.j0 >= nvec) return;   // no barrier or shuffle below
+    const bool lane = m.j0 < nvec;
     const int64_t e0 = ((int64_t)blockIdx.x * m.rows + m.rsub) * kArgRun;
-    if (e0 >= n) return;
+    if (e0 >= n) return;   // the same for the whole group
     const int64_t e1 = min(e0 + (int64_t)kArgRun, n);
     const int64_t row_before = e0 > 0 ? (int64_t)row[e0 - 1] : -1;
     const int64_t row_after = e1 < n ? (int64_t)row[e1] : -1;
@@ -800,7 +804,7 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_run_kernel(const typename 
         o[k] = 0.0f;
     }
     auto flush = [&]() {
-        if ((uint64_t)cur >= (uint64_t)R) return;
+        if ((uint64_t)cur >= (uint64_t)R || !lane) return;
         const bool shared = cur == row_before || cur == row_after;
         A *a = arg + cur * F + (int64_t)m.j0 * V;
 #pragma unroll
@@ -810,20 +814,45 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_run_kernel(const typename 
             else a[k] = best[k];
         }
     };
+    // coop: lane i of the group loads edge e0 + i's ids (one coalesced load each, instead of a
+    // broadcast load per edge and id), handed out by lane shuffles, so that a batch waits only
+    // for its X rows; row ids fit 31 bits (the host rejects num_rows >= 2^31)
+    int my_r = -1, my_clo = -1, my_chi = -1;
+    float my_w = 1.0f;
+    const int gb = (int)(threadIdx.x & 63) - m.j0;   // the group's first lane in the wave
+    if (coop && m.j0 < kArgRun && e0 + m.j0 < e1) {
+        const int64_t e = e0 + m.j0;
+        const int64_t c = (int64_t)col[e];
+        my_r = (int)row[e];
+        my_clo = (int)(uint32_t)(uint64_t)c;
+        my_chi = (int)(uint32_t)((uint64_t)c >> 32);
+        my_w = w ? w[e] : 1.0f;
+    }
     for (int64_t b = e0; b < e1; b += kArgBatch) {
         int64_t rr[kArgBatch], cc[kArgBatch];
         float wt[kArgBatch];
         Raw<E, V> rx[kArgBatch];
+        if (coop) {
 #pragma unroll
-        for (int u = 0; u < kArgBatch; ++u) {
-            const int64_t e = b + u;
-            rr[u] = e < e1 ? (int64_t)row[e] : -1;
-            cc[u] = e < e1 ? (int64_t)col[e] : -1;
-            wt[u] = e < e1 && w ? w[e] : 1.0f;
+            for (int u = 0; u < kArgBatch; ++u) {   // b - e0 + u < kArgRun: past e1, the sentinels
+                const int src = gb + (int)(b - e0) + u;
+                rr[u] = __shfl(my_r, src, 64);
+                cc[u] = (int64_t)(((uint64_t)(uint32_t)__shfl(my_chi, src, 64) << 32) |
+                                  (uint64_t)(uint32_t)__shfl(my_clo, src, 64));
+                wt[u] = __shfl(my_w, src, 64);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kArgBatch; ++u) {
+                const int64_t e = b + u;
+                rr[u] = e < e1 ? (int64_t)row[e] : -1;
+                cc[u] = e < e1 ? (int64_t)col[e] : -1;
+                wt[u] = e < e1 && w ? w[e] : 1.0f;
+            }
         }
 #pragma unroll
         for (int u = 0; u < kArgBatch; ++u)
-            if ((uint64_t)rr[u] < (uint64_t)R && (uint64_t)cc[u] < (uint64_t)nx)
+            if (lane && (uint64_t)rr[u] < (uint64_t)R && (uint64_t)cc[u] < (uint64_t)nx)
                 load_raw<E, V>(X + cc[u] * F + (int64_t)m.j0 * V, rx[u]);
 #pragma unroll
         for (int u = 0; u < kArgBatch; ++u) {
@@ -834,7 +863,7 @@ __global__ __launch_bounds__(256) void gs_bwd_max_arg_run_kernel(const typename 
                 cur = rr[u];
 #pragma unroll
                 for (int k = 0; k < V; ++k) best[k] = none;
-                if ((uint64_t)cur < (uint64_t)R) load_f32<V>(out + cur * F + (int64_t)m.j0 * V, o);
+                if (lane && (uint64_t)cur < (uint64_t)R) load_f32<V>(out + cur * F + (int64_t)m.j0 * V, o);
             }
             if ((uint64_t)rr[u] >= (uint64_t)R || (uint64_t)cc[u] >= (uint64_t)nx) continue;
             float x[V];
