@@ -153,6 +153,8 @@ GS_CASES = [
     (15, 5000, 400, 400, 17, "poisson", "int", True),
     (16, 6000, 500, 600, 6, "zipf", "int", True),        # 2-wide vectors, ties
     (17, 3000, 200, 400, 300, "zipf", "int", True),      # 75 vectors a row: more than a row's 64 threads
+    (18, 5000, 300, 500, 256, "zipf", "int", True),      # 64 threads a row: whole-wave groups, ties
+    (19, 7000, 400, 600, 100, "one_heavy", "normal", False),   # 25 vectors on 32 threads (7 idle)
 ]
 
 
