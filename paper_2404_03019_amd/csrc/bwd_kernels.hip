@@ -1033,9 +1033,9 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
 }
 
 // fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
-// mean divides afterwards, in scale_by_count_kernel). This kernel serves max, and sum and mean
-// where a row takes fewer than 8 threads or more than 64 vectors (gs_bwd_w_run_kernel below
-// takes the others). A row group takes P consecutive edges
+// mean divides afterwards, in scale_by_count_kernel). This kernel serves the rows that take
+// fewer than 8 threads or more than 64 vectors (gs_bwd_w_run_kernel below takes the others,
+// max included). A row group takes P consecutive edges
 // (rows are sorted, so they mostly share their grad_out row); every thread runs all of them (the
 // group reduction is uniform). The edges' ids load first, then every edge's X row and, once per
 // run of edges with the same row, the grad_out row (and for max its recipients), then the
@@ -1190,14 +1190,16 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
     }
 }
 
-// fused form, sum, w.r.t. the weights, where a row's vectors take 8 to 64 threads (one vector
-// each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
+// fused form, sum and max, w.r.t. the weights, where a row's vectors take 8 to 64 threads (one
+// vector each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
 // load, and each row group (tpr threads) walks tpr of them in batches of kB = 4, loading the
 // grad_out row once per run of edges with the same row. A batch's four dot products are
 // reduced together: across the group's highest lane bit each lane keeps two of the four sums
 // and trades the other two, across the next bit one, and a butterfly over the remaining bits
 // completes it, so that 6 shuffles at tpr = 32 (instead of 4 x 5) leave edge q's sum in the
-// lanes whose two highest group bits read q, one of which stores it.
+// lanes whose two highest group bits read q, one of which stores it. Max loads the recipient
+// vectors with the grad_out rows and an edge's X vector only where the edge receives one of the
+// thread's features.
 template <int E, typename I, int V, int OP, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                            const I *__restrict__ col, const I *__restrict__ row,
