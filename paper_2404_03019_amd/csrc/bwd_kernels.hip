@@ -1190,8 +1190,8 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
     }
 }
 
-// fused form, sum and max, w.r.t. the weights, where a row's vectors take 8 to 64 threads (one
-// vector each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
+// fused form, sum, mean and max, w.r.t. the weights, where a row's vectors take 8 to 64 threads
+// (one vector each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
 // load, and each row group (tpr threads) walks tpr of them in batches of kB = 4, loading the
 // grad_out row once per run of edges with the same row. A batch's four dot products are
 // reduced together: across the group's highest lane bit each lane keeps two of the four sums
@@ -1203,12 +1203,14 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
 template <int E, typename I, int V, int OP, typename A>
 __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<E>::T *__restrict__ X, int64_t nx,
                                                            const I *__restrict__ col, const I *__restrict__ row,
-                                                           const A *__restrict__ arg,
+                                                           const A *__restrict__ arg, const int64_t *__restrict__ off,
                                                            const float *__restrict__ gout, int64_t n, int64_t R,
                                                            int64_t F, float *__restrict__ gw) {
     constexpr int kB = 4;
     constexpr bool MX = OP == GEOT_BWD_MAX;
-    static_assert(OP != GEOT_BWD_MEAN, "mean: the sum kernel, then scale_by_count_kernel");
+    // mean: the row's edge count loads with its grad_out row (once per run) and the dot product
+    // is divided by it before the store, as scale_by_count_kernel divides it (the same rounding)
+    constexpr bool MEAN = OP == GEOT_BWD_MEAN;
     __shared__ int64_t s_c[256], s_r[256];
     const int nvec = (int)(F / V);
     int tpr = 1;
@@ -1226,6 +1228,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
     const int hi = tpr >> 1, q2 = tpr >> 2;     // the two highest lane bits of the group
     const bool bh = (gl & hi) != 0, bq = (gl & q2) != 0;
     int64_t prev = -1;                           // the row whose vectors `cur` (and `ca`) hold
+    float cnt = 1.0f;                            // mean: that row's edge count
     float cur[V];
     A ca[V];   // max: the recipient edges of the row's features (none: all ones)
 #pragma unroll
@@ -1237,6 +1240,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
         int64_t rr[kB], cc[MX ? kB : 1];
         bool ok[kB], lead[kB];
         float g[kB][V];
+        float cn[MEAN ? kB : 1];   // mean: the counts of the rows that start here
         A ga[MX ? kB : 1][V];
         Raw<E, V> rx[kB];
 #pragma unroll
@@ -1253,6 +1257,8 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
             }
             // a new row loads its vectors whether or not this edge's column is valid, since the
             // next edges of the run use them
+            if constexpr (MEAN)
+                cn[q] = lead[q] && (uint64_t)rr[q] < (uint64_t)R ? (float)(off[rr[q] + 1] - off[rr[q]]) : 1.0f;
             if (lead[q] && lane && (uint64_t)rr[q] < (uint64_t)R) {
                 load_f32<V>(gout + rr[q] * F + (int64_t)gl * V, g[q]);
                 if constexpr (MX) load_arg<A, V>(arg + rr[q] * F + (int64_t)gl * V, ga[q]);
@@ -1265,14 +1271,17 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
             }
         }
         float a[kB];
+        float cq[MEAN ? kB : 1];   // mean: each edge's row count
         if constexpr (!MX) {
-            // sum: the products with each edge's run's row
+            // sum and mean: the products with each edge's run's row
 #pragma unroll
             for (int q = 0; q < kB; ++q) {
                 if (lead[q]) {
 #pragma unroll
                     for (int k = 0; k < V; ++k) cur[k] = g[q][k];
+                    if constexpr (MEAN) cnt = cn[q];
                 }
+                if constexpr (MEAN) cq[q] = cnt;
                 float x[V];
                 widen<E, V>(rx[q], x);
                 a[q] = 0.0f;
@@ -1322,11 +1331,16 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
         for (int d = q2 >> 1; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
         const int q = (bh ? 2 : 0) + (bq ? 1 : 0);
         const int64_t e = b0 + base + j0 + q;
+        if constexpr (MEAN) {
+            const float c = q == 0 ? cq[0] : q == 1 ? cq[1] : q == 2 ? cq[2] : cq[3];
+            v = v / c;
+        }
         if ((gl & (q2 - 1)) == 0 && e < n) gw[e] = ok[q] ? v : 0.0f;
     }
 }
 
-// mean: grad_w[e] /= the edge count of row[e]. A pass of its own: inside the dot-product
+// mean, for the rows gs_bwd_w_kernel serves: grad_w[e] /= the edge count of row[e]. A pass of
+// its own: inside that dot-product
 // kernel the row starts either waited after the reduction (one more memory latency per
 // block) or held registers through it (5 waves per SIMD instead of 7); both cost C4 1.5 ms,
 // this pass about 0.2. Rows of all passes load first, then their starts and the values.
@@ -2324,6 +2338,7 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                          int64_t F, int V, int op, void *arg, bool given, float *gX, float *gw, hipStream_t st) {
     if (n <= 0) return hipSuccess;
     if (op == GEOT_BWD_MAX && !arg) return hipErrorInvalidValue;
+    if (op == GEOT_BWD_MEAN && gw && !off) return hipErrorInvalidValue;   // mean divides by the row counts
     if (given && !seg_bwd_arg32(n)) return hipErrorInvalidValue;   // recorded recipients are 32-bit
     if (grid_rows(n, (int)(F / V)) > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     // recipients as 32-bit edge numbers below 2^32 - 1 edges, else 64-bit
@@ -2377,18 +2392,21 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 const bool runs = tpr >= 8 && F / VV <= 64;
                 if (op == GEOT_BWD_MAX && runs)
                     hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_MAX, A>), dim3((unsigned)((n + 255) / 256)),
-                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
+                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, off, gout, n, R, F, gw);
                 else if (op == GEOT_BWD_MAX)
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_MAX, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
+                else if (runs && op == GEOT_BWD_MEAN)
+                    hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_MEAN, A>), dim3((unsigned)((n + 255) / 256)),
+                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, off, gout, n, R, F, gw);
                 else if (runs)
                     hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_SUM, A>), dim3((unsigned)((n + 255) / 256)),
-                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
+                                       dim3(256), 0, st, Xt, nx, ct, rt, ap, off, gout, n, R, F, gw);
                 else
                     hipLaunchKernelGGL((gs_bwd_w_kernel<E, I, VV, GEOT_BWD_SUM, WP, A>), dim3((unsigned)gwb), dim3(256), 0,
                                        st, Xt, nx, ct, rt, ap, gout, n, R, F, gw);
                 if ((e = hipGetLastError()) != hipSuccess) return e;
-                if (op == GEOT_BWD_MEAN) {
+                if (op == GEOT_BWD_MEAN && !runs) {
                     const int64_t sb = (n + 256 * kPasses - 1) / (256 * kPasses);
                     if (sb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
                     hipLaunchKernelGGL(scale_by_count_kernel<I>, dim3((unsigned)sb), dim3(256), 0, st, gw, rt, off,
