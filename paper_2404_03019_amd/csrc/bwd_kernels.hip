@@ -1034,7 +1034,7 @@ __global__ __launch_bounds__(256) void gs_bwd_x_max_pull_kernel(const int32_t *_
 
 // fused form, w.r.t. the weights: grad_w[e] = dot(grad_out[row[e]], X[col[e]]) (restricted for max;
 // mean divides afterwards, in scale_by_count_kernel). This kernel serves the rows that take
-// fewer than 8 threads or more than 64 vectors (gs_bwd_w_run_kernel below takes the others,
+// fewer than 4 threads or more than 64 vectors (gs_bwd_w_run_kernel below takes the others,
 // max included). A row group takes P consecutive edges
 // (rows are sorted, so they mostly share their grad_out row); every thread runs all of them (the
 // group reduction is uniform). The edges' ids load first, then every edge's X row and, once per
@@ -1190,14 +1190,15 @@ __global__ __launch_bounds__(256) void gs_bwd_w_kernel(const typename ElemT<E>::
     }
 }
 
-// fused form, sum, mean and max, w.r.t. the weights, where a row's vectors take 8 to 64 threads
+// fused form, sum, mean and max, w.r.t. the weights, where a row's vectors take 4 to 64 threads
 // (one vector each): a block takes 256 consecutive edges and stages their ids in LDS with one coalesced
 // load, and each row group (tpr threads) walks tpr of them in batches of kB = 4, loading the
 // grad_out row once per run of edges with the same row. A batch's four dot products are
 // reduced together: across the group's highest lane bit each lane keeps two of the four sums
 // and trades the other two, across the next bit one, and a butterfly over the remaining bits
 // completes it, so that 6 shuffles at tpr = 32 (instead of 4 x 5) leave edge q's sum in the
-// lanes whose two highest group bits read q, one of which stores it. Max loads the recipient
+// lanes whose two highest group bits read q, one of which stores it (at tpr = 4 the two
+// exchanges finish it and every lane stores its own edge's). Max loads the recipient
 // vectors with the grad_out rows and an edge's X vector only where the edge receives one of the
 // thread's features.
 template <int E, typename I, int V, int OP, typename A>
@@ -1214,7 +1215,7 @@ __global__ __launch_bounds__(256) void gs_bwd_w_run_kernel(const typename ElemT<
     __shared__ int64_t s_c[256], s_r[256];
     const int nvec = (int)(F / V);
     int tpr = 1;
-    while (tpr < nvec && tpr < 64) tpr <<= 1;   // 8 .. 64: the launch checks
+    while (tpr < nvec && tpr < 64) tpr <<= 1;   // 4 .. 64: the launch checks
     const int gl = threadIdx.x & (tpr - 1);     // lane within the row group
     const int base = threadIdx.x - gl;          // the group's first edge within the block
     const int64_t b0 = (int64_t)blockIdx.x * 256;
@@ -2389,7 +2390,7 @@ hipError_t launch_gs_bwd(const void *X, int elem, int64_t nx, const void *col, i
                 const int64_t gwb = grid_rows(n, (int)(F / VV), WP);
                 if (gwb > 0x7fffffffLL) return hipErrorInvalidConfiguration;
                 const int tpr = row_threads((int)(F / VV));
-                const bool runs = tpr >= 8 && F / VV <= 64;
+                const bool runs = tpr >= 4 && F / VV <= 64;
                 if (op == GEOT_BWD_MAX && runs)
                     hipLaunchKernelGGL((gs_bwd_w_run_kernel<E, I, VV, GEOT_BWD_MAX, A>), dim3((unsigned)((n + 255) / 256)),
                                        dim3(256), 0, st, Xt, nx, ct, rt, ap, off, gout, n, R, F, gw);

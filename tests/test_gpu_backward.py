@@ -155,6 +155,7 @@ GS_CASES = [
     (17, 3000, 200, 400, 300, "zipf", "int", True),      # 75 vectors a row: more than a row's 64 threads
     (18, 5000, 300, 500, 256, "zipf", "int", True),      # 64 threads a row: whole-wave groups, ties
     (19, 7000, 400, 600, 100, "one_heavy", "normal", False),   # 25 vectors on 32 threads (7 idle)
+    (20, 8000, 500, 900, 16, "poisson", "normal", True),    # 4 threads a row: every lane stores an edge
 ]
 
 
