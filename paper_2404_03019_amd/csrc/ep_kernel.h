@@ -56,7 +56,11 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     constexpr int G = kBlock / L;     // row groups per block
     constexpr int TW = NT * L * V;    // columns per tile
     constexpr int U = NV >= 4 ? 4 : 8;   // rows loaded ahead per row group
-    constexpr int UG = NV >= 4 ? 4 : 8;  // edges per batch of the gather pipeline
+    // edges per batch of the gather pipeline: 8 for 4-float lanes whose group shares the
+    // metadata loads (L >= 8) and carries no recipients (the SpMM graph: fp32 sum 5.18 ->
+    // 5.14 ms, its gradient w.r.t. X 4.13 -> 4.06 ms), else 4 (8 for narrower lanes; bf16 lanes
+    // of 8 elements took 2.80 -> 2.92 ms with 8)
+    constexpr int UG = NV == 4 && L >= 8 && RED != RED_MAXARG ? 8 : (NV >= 4 ? 4 : 8);
     // Segment ids fit 32 bits (the host rejects num_segments >= 2^31). Row counts
     // of one block fit 32 bits; partial levels add counts of many blocks: 64 bits.
     using Cnt = typename std::conditional<MODE == SRC_PIECES, int64_t, int32_t>::type;
