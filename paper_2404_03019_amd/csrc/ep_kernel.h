@@ -55,10 +55,11 @@ __device__ __forceinline__ void ep_body(const EpArgs &a, const int64_t bid, cons
     constexpr int NW = kBlock / 64;   // waves per block
     constexpr int G = kBlock / L;     // row groups per block
     constexpr int TW = NT * L * V;    // columns per tile
-    // rows loaded ahead per row group: 8 for 4-float lanes with at least 8 lanes a row and no
-    // recipients (the point cloud's mean 0.807 -> 0.786 ms, the power-law graph's sum 2.368 ->
-    // 2.353 ms; 118 VGPRs and 4 waves per SIMD instead of 92 and 5), else 4 (8 for narrower lanes)
-    constexpr int U = NV == 4 && L >= 8 && RED != RED_MAXARG ? 8 : (NV >= 4 ? 4 : 8);
+    // rows loaded ahead per row group: 8 for 4-float lanes with at least 8 lanes a row and for
+    // 8-element lanes (16-bit storage), without recipients (the point cloud's mean 0.807 ->
+    // 0.786 ms, the power-law graph's sum 2.368 -> 2.353 ms, its bf16 sum 1.42 -> 1.38 ms; 118
+    // VGPRs and 4 waves per SIMD instead of 92 and 5), else 4 (8 for narrower lanes)
+    constexpr int U = (NV == 4 && L >= 8 || NV == 8) && RED != RED_MAXARG ? 8 : (NV >= 4 ? 4 : 8);
     // edges per batch of the gather pipeline: 8 for 4-float lanes whose group shares the
     // metadata loads (L >= 8) and carries no recipients (the SpMM graph: fp32 sum 5.18 ->
     // 5.14 ms, its gradient w.r.t. X 4.13 -> 4.06 ms), else 4 (8 for narrower lanes; bf16 lanes
